@@ -1,0 +1,300 @@
+#!/usr/bin/env python3
+"""Tree-verification step benchmark on one MI355X.
+
+A step is one pass of the whole verification hot path at batch 1:
+  host: pick the tree for this step with the hysteretic ladder (tau_on 0.8,
+        tau_off 0.6) from the previous step's top-1 probability at the
+        deepest accepted node;
+  GPU:  tree attention (tree K/V appended to the cache) -> LM-head logits ->
+        softmax statistics -> greedy acceptance -> KV compaction;
+  host: read (accept length, feature) back -- the step's one sync -- and grow
+        the prefix by accept_len + 1.
+
+Default workload: Vicuna-7B shapes (32 x 128 heads, hidden 4096, vocab
+32000), a 5-tree bank with {1, 8, 26, 64, 128} nodes, prefix 2048 growing
+every step.  Inputs are seeded synthetic tensors staged in HBM before timing
+(a pool of per-step inputs is cycled); two copies of the LM-head weight
+alternate between steps so that the 256 MB last-level cache cannot serve the
+weight stream.
+
+Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: the build targets one GPU.
+"""
+from __future__ import annotations
+
+import argparse
+import ctypes
+import json
+import math
+import os
+import sys
+import time
+
+import numpy as np
+
+HBM_PEAK_GBPS = 8000.0
+METRIC = "tree-verify steps/sec and µs/step at batch 1; achieved HBM GB/s vs peak"
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=1000)
+    ap.add_argument("--warmup", type=int, default=50)
+    ap.add_argument("--workload", default="bank5_L2048_7b",
+                    choices=["bank5_L2048_7b", "tree27_L256_7b"])
+    ap.add_argument("--pool", type=int, default=32, help="distinct per-step input sets")
+    ap.add_argument("--weight-copies", type=int, default=2)
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--fixed-topo", type=int, default=-1,
+                    help="disable the scheduler and use this bank entry every step")
+    return ap.parse_args()
+
+
+def log(*a):
+    print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def main():
+    args = parse()
+    if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
+        print("bench.py runs on one GPU only: the tree-verification path of this build is "
+              "single-GPU (see DESIGN.md for how it would shard)", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    from paper_2606_27550_amd import api, synth
+
+    if not torch.cuda.is_available():
+        sys.exit("bench.py needs a GPU")
+    dev = torch.device("cuda:0")
+    torch.cuda.set_device(dev)
+    lib = api.lib
+
+    wl = synth.WORKLOADS[args.workload]
+    Hq, Hkv, d, hid, V = wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.hidden, wl.vocab
+    trees = synth.workload_trees(wl)
+    bank = api.Bank(trees)
+    n_topo = len(trees)
+    Tmax = max(bank.T)
+    Dmax = max(bank.D)
+    L0 = wl.prefix_len
+    grows = args.workload == "bank5_L2048_7b"
+    total_steps = args.warmup + args.steps
+    cap = L0 + (total_steps * (Dmax + 1) if grows else 0) + Tmax + 64
+    scale = 1.0 / math.sqrt(d)
+    theta = wl.rope_theta
+    log(f"workload {wl.name}: bank T={bank.T} D={bank.D}, L0={L0}, cap={cap}")
+
+    # ---------------------------------------------------------- staging
+    t0 = time.time()
+    bf = torch.bfloat16
+
+    def to_dev(bits):
+        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(bf).to(dev)
+
+    w_host = synth.lm_head_weight(wl.ident, V, hid)
+    W = [to_dev(w_host)]
+    for c in range(1, args.weight_copies):
+        W.append(W[0].clone())
+    base = synth.attn_inputs(wl.ident, 1, Hq, Hkv, d, L0, cap)
+    kc0_host, vc0_host = base.k_cache[:, :L0].copy(), base.v_cache[:, :L0].copy()
+    k_cache = torch.zeros((Hkv, cap, d), dtype=bf, device=dev)
+    v_cache = torch.zeros((Hkv, cap, d), dtype=bf, device=dev)
+    k_cache[:, :L0] = to_dev(kc0_host)
+    v_cache[:, :L0] = to_dev(vc0_host)
+    del base
+
+    P = args.pool
+    deltas, spike_tok = synth.regime_spikes(wl.ident, P, Tmax, V, hid)
+    pool = []
+    for e in range(P):
+        a_in = synth.attn_inputs(wl.ident, Tmax, Hq, Hkv, d, 0, Tmax, step=e + 1)
+        x = synth.hidden_rows(wl.ident, Tmax, hid, step=e + 1)
+        if grows:
+            x = synth.plant_spike(x, w_host, spike_tok[e], float(deltas[e]), wl.w_std)
+        u, r = synth.draft_randoms(wl.ident, Tmax, V, step=e + 1)
+        pool.append({"q": to_dev(a_in.q), "kt": to_dev(a_in.k_tree), "vt": to_dev(a_in.v_tree),
+                     "x": to_dev(x), "u": u, "r": r,
+                     "host": (a_in.q, a_in.k_tree, a_in.v_tree, x)})
+    log(f"staged inputs in {time.time() - t0:.1f}s")
+
+    # buffers
+    logits = torch.empty((Tmax, V), dtype=torch.float32, device=dev)
+    ent = torch.empty(Tmax, dtype=torch.float32, device=dev)
+    top1 = torch.empty(Tmax, dtype=torch.float32, device=dev)
+    amax = torch.empty(Tmax, dtype=torch.int32, device=dev)
+    res = torch.zeros(4 + Dmax + 1, dtype=torch.int32, device=dev)   # a, bonus, s(bits), pad, path
+    res_host = torch.zeros(4, dtype=torch.int32).pin_memory()
+    out = torch.empty((Tmax, Hq, d), dtype=bf, device=dev)
+    ws_bytes = api.tree_attn_workspace(Tmax, Hq, Hkv, d, cap - Tmax)
+    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
+
+    # draft tokens: the target's greedy token at the parent with prob p_acc,
+    # computed with the library itself on each pool entry (input synthesis)
+    for e in pool:
+        lib.entmtp_verify_logits(ctypes.c_void_p(e["x"].data_ptr()), ctypes.c_void_p(W[0].data_ptr()),
+                                 Tmax, hid, V, ctypes.c_void_p(logits.data_ptr()),
+                                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
+        api.logit_stats(logits, 1.0, None, None, amax)
+        am = amax.cpu().numpy()
+        e["tok"] = [synth.draft_tokens(trees[k], am, e["u"], e["r"], wl.p_acc) for k in range(n_topo)]
+        e["tok_dev"] = [torch.from_numpy(t).to(dev) for t in e["tok"]]
+    torch.cuda.synchronize()
+
+    # ---------------------------------------------------------- raw step
+    P_ = ctypes.c_void_p
+    stream = P_(torch.cuda.current_stream().cuda_stream)
+    handle = bank.handle
+    kc_p, vc_p = P_(k_cache.data_ptr()), P_(v_cache.data_ptr())
+    out_p, ws_p = P_(out.data_ptr()), P_(ws.data_ptr())
+    lg_p, ent_p, top_p, am_p = (P_(logits.data_ptr()), P_(ent.data_ptr()), P_(top1.data_ptr()),
+                                P_(amax.data_ptr()))
+    res_p = res.data_ptr()
+    a_p, bonus_p, s_p, path_p = P_(res_p), P_(res_p + 4), P_(res_p + 8), P_(res_p + 16)
+    W_p = [P_(w.data_ptr()) for w in W]
+    pool_p = [{"q": P_(e["q"].data_ptr()), "kt": P_(e["kt"].data_ptr()), "vt": P_(e["vt"].data_ptr()),
+               "x": P_(e["x"].data_ptr()), "tok": [P_(t.data_ptr()) for t in e["tok_dev"]]}
+              for e in pool]
+    Ts = bank.T
+
+    def chk(rc):
+        if rc:
+            raise api.EntmtpError(rc, api.last_error())
+
+    state = {"L": L0, "rung": 0 if args.fixed_topo < 0 else args.fixed_topo, "s": 0.0}
+    ev = None
+
+    def step(t, timed_events=None):
+        L = state["L"] if grows else L0
+        topo = state["rung"]
+        T = Ts[topo]
+        e = pool_p[t % P]
+        chk(lib.entmtp_tree_attn(handle, topo, e["q"], e["kt"], e["vt"], kc_p, vc_p, cap, L, Hq, Hkv,
+                                 d, scale, theta, out_p, ws_p, ws_bytes, stream))
+        if timed_events is not None:
+            timed_events[0].record()
+        chk(lib.entmtp_verify_logits(e["x"], W_p[t % len(W_p)], T, hid, V, lg_p, stream))
+        if timed_events is not None:
+            timed_events[1].record()
+        chk(lib.entmtp_logit_stats(lg_p, T, V, 1.0, ent_p, top_p, am_p, stream))
+        chk(lib.entmtp_accept(handle, topo, e["tok"][topo], am_p, top_p, a_p, path_p, bonus_p, s_p,
+                              stream))
+        chk(lib.entmtp_kv_compact(path_p, Dmax + 1, a_p, L, kc_p, vc_p, 1, Hkv * cap * d, Hkv, cap,
+                                  d, stream))
+        res_host.copy_(res[:4], non_blocking=True)
+        torch.cuda.current_stream().synchronize()
+        a = int(res_host[0])
+        s = float(np.frombuffer(np.int32(res_host[2]).tobytes(), np.float32)[0])
+        if grows:
+            state["L"] = L + a + 1
+        if args.fixed_topo < 0:
+            state["rung"] = lib.entmtp_ladder_next(state["rung"], n_topo, s, 0.8, 0.6)
+        return T, L, a, s, topo
+
+    # ---------------------------------------------------------- warmup
+    for t in range(args.warmup):
+        step(t)
+    torch.cuda.synchronize()
+
+    # ---------------------------------------------------------- timed
+    K = args.steps
+    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+              for _ in range(K)]
+    trace = []
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for t in range(K):
+        trace.append(step(args.warmup + t, events[t]))
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+
+    lm_ms = [a.elapsed_time(b) for a, b in events]
+    # algorithmic bytes (what the method must move; fp32 logits excluded)
+    def step_bytes(T, L, a):
+        w = V * hid * 2
+        kv = 2 * Hkv * L * d * 2
+        tree_in = T * (Hq + 2 * Hkv) * d * 2 + T * hid * 2
+        tree_kv_out = T * 2 * Hkv * d * 2
+        att_out = T * Hq * d * 2
+        compact = 2 * (a + 1) * 2 * Hkv * d * 2
+        stats = T * 12
+        return w + kv + tree_in + tree_kv_out + att_out + compact + stats
+
+    bytes_total = sum(step_bytes(T, L, a) for T, L, a, _, _ in trace)
+    lm_bytes = sum(V * hid * 2 + T * hid * 2 for T, _, _, _, _ in trace)
+    lm_s = sum(lm_ms) / 1e3
+    steps_per_s = K / elapsed
+    us = elapsed / K * 1e6
+    hbm = bytes_total / elapsed / 1e9
+    lm_gbps = lm_bytes / lm_s / 1e9
+    Tcount = {}
+    for T, *_ in trace:
+        Tcount[T] = Tcount.get(T, 0) + 1
+    accept_mean = float(np.mean([a + 1 for _, _, a, _, _ in trace]))
+    switches = sum(1 for i in range(1, len(trace)) if trace[i][4] != trace[i - 1][4])
+    log(f"{K} steps in {elapsed:.3f}s: {us:.1f} us/step, {hbm:.0f} GB/s algorithmic; "
+        f"LM head {np.mean(lm_ms) * 1e3:.1f} us avg, {lm_gbps:.0f} GB/s; T histogram {Tcount}; "
+        f"mean tokens/step {accept_mean:.3f}; switches {switches}; final L {state['L']}")
+
+    # ---------------------------------------------------------- cpu baseline
+    cpu = None
+    if not args.no_cpu_baseline:
+        cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta)
+
+    line = {
+        "metric": METRIC, "value": round(steps_per_s, 2), "unit": "steps/s", "n_gpus": 1,
+        "steps": K, "warmup": args.warmup, "ms_per_step": round(elapsed / K * 1e3, 5),
+        "us_per_step": round(us, 2), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "hbm_GBps_algorithmic": round(hbm, 1), "hbm_frac": round(hbm / HBM_PEAK_GBPS, 4),
+        "config": {"workload": wl.name, "batch": 1, "heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                   "hidden": hid, "vocab": V, "prefix_len_start": L0,
+                   "prefix_len_end": state["L"], "bank_T": bank.T,
+                   "scheduler": "hysteretic ladder on=0.8 off=0.6" if args.fixed_topo < 0
+                   else f"fixed topo {args.fixed_topo}",
+                   "T_histogram": {str(k): v for k, v in sorted(Tcount.items())},
+                   "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
+                   "weight_copies": args.weight_copies, "parallelism": "single GPU"},
+        "roofline": {"kernel": "lm_head_kernel (entmtp_verify_logits)", "bound": "hbm",
+                     "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2)},
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta):
+    """The oracle, as it stands, on a bounded sample of the same workload."""
+    from oracle import entmtp_oracle as orc
+    try:
+        from threadpoolctl import threadpool_info
+        threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
+    except Exception:
+        threads = os.cpu_count() or 1
+    Hkv, d, L0 = wl.n_kv_heads, wl.head_dim, wl.prefix_len
+    # sample: the bank's trees in turn, at the starting prefix, until the budget
+    order = list(range(len(trees)))[::-1]
+    done, t0 = [], time.perf_counter()
+    kc = np.zeros((Hkv, L0 + 256, d), np.uint16)
+    vc = np.zeros_like(kc)
+    kc[:, :L0], vc[:, :L0] = kc0, vc0
+    for i, k in enumerate(order):
+        e = pool[i % len(pool)]
+        q, kt, vt, x = e["host"]
+        T = len(trees[k])
+        orc.verify_step(trees[k], q[:T], kt[:T], vt[:T], kc, vc, L0, x[:T], w_host,
+                        e["tok"][k], scale, theta)
+        done.append(T)
+        if time.perf_counter() - t0 > args.cpu_budget_s:
+            break
+    el = time.perf_counter() - t0
+    return {"value": round(len(done) / el, 4), "unit": "steps/s", "cores": threads,
+            "kind": "oracle",
+            "sample": f"{len(done)} oracle steps of {wl.name} (tree sizes {done}, prefix {L0}), "
+                      f"{el:.1f}s; fp64 numpy/BLAS on host cores"}
+
+
+if __name__ == "__main__":
+    main()

@@ -1,0 +1,262 @@
+/*
+ * entmtp.h -- C ABI of the EntMTP tree-verification hot path on AMD Instinct
+ * MI355X (gfx950).
+ *
+ * One decode step of a multi-token-prediction decoder verifies a draft tree in
+ * a single sparse forward pass (paper §2.3), then keeps the longest accepted
+ * root-to-node path and updates the KV cache (§3.2 loop: proposal -> tree
+ * decoding -> verification -> KV-cache update).  The scheduler of §4 picks the
+ * tree for every step from a precompiled bank, so that switching trees is an
+ * index change with no rebuild (§4 "Cost").  This library implements that
+ * pass:
+ *
+ *   entmtp_bank_build     per-tree buffers (mask, position offsets, gather rows)
+ *   entmtp_tree_attn      tree-masked attention over prefix KV + the tree
+ *   entmtp_verify_logits  LM-head logits of the tree's final hidden states
+ *   entmtp_logit_stats    per-node entropy, top-1 probability and argmax
+ *   entmtp_accept         longest accepted path, bonus token
+ *   entmtp_kv_compact     KV-cache compaction of the accepted path
+ *
+ * Conventions shared by every call:
+ *   - Tensor pointers are DEVICE pointers owned by the caller unless the
+ *     argument is documented as host memory.  bf16 tensors are passed as
+ *     uint16_t bit patterns (entmtp_bf16).  All layouts are dense row-major.
+ *   - `stream` is a hipStream_t (NULL = the default stream).  Calls that
+ *     launch work are asynchronous on `stream` and never synchronise it,
+ *     except entmtp_bank_build (see there).
+ *   - Every argument is validated on the host before anything is launched,
+ *     so a call that returns an error has launched nothing.
+ *   - Return value: ENTMTP_OK (0) or a negative status; the message of the
+ *     last error of the calling thread is returned by entmtp_last_error().
+ *   - Asynchronous device faults surface at a later synchronisation of the
+ *     stream, not as a return code of the call that launched the kernel.
+ */
+#ifndef ENTMTP_H
+#define ENTMTP_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define ENTMTP_OK       0
+#define ENTMTP_EINVAL  (-1)  /* null pointer, bad size, unsupported shape, topo out of range */
+#define ENTMTP_ETREE   (-2)  /* malformed tree: parent[0] != -1 or parent[i] not in [0, i) */
+#define ENTMTP_ERANGE  (-3)  /* T > ENTMTP_T_MAX, depth > ENTMTP_D_MAX, cap < L+T, Hq % Hkv */
+#define ENTMTP_ENOSPC  (-4)  /* arena or workspace smaller than required */
+#define ENTMTP_EHIP    (-5)  /* HIP runtime or launch error (message kept) */
+
+#define ENTMTP_T_MAX      256  /* nodes per tree, root included */
+#define ENTMTP_D_MAX      31   /* deepest node (root = depth 0) */
+#define ENTMTP_MASK_WORDS 8    /* uint32 words per mask row (ENTMTP_T_MAX / 32) */
+#define ENTMTP_HEAD_DIM   128  /* the head dimension the attention kernels are built for */
+
+typedef uint16_t entmtp_bf16;
+typedef struct entmtp_bank entmtp_bank;
+
+/* Message of the calling thread's last error ("" if none).  Never NULL. */
+const char* entmtp_last_error(void);
+
+/* Library version string. */
+const char* entmtp_version(void);
+
+/* ------------------------------------------------------------------------ */
+/* TopologyBank (§2.3: trees ship precomputed attention masks, position       */
+/* offsets and gather indices; §4 "Cost": one buffer set per tree, switching  */
+/* trees is a pointer swap).                                                  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Build the bank of `n_trees` draft trees.
+ *
+ *   parents_host   host int32[sum(sizes)]: the trees' parent arrays back to
+ *                  back.  Node 0 of each tree is its root (parent -1); every
+ *                  other node's parent is an earlier node of the same tree.
+ *   sizes_host     host int32[n_trees]: node count T of each tree (root
+ *                  included), 1 <= T <= ENTMTP_T_MAX.
+ *   arena          device buffer that will hold the bank, or NULL.
+ *   arena_bytes    size of `arena`.
+ *   arena_needed   host out (optional): bytes the arena must have.
+ *   stream         stream of the upload.
+ *   out            host out: the bank handle (owned by the library, free with
+ *                  entmtp_bank_destroy).  May be NULL when arena is NULL (size
+ *                  query only).
+ *
+ * With arena == NULL nothing touches the GPU: the call validates the trees,
+ * reports the size and, when `out` is given, returns a host-only bank that
+ * supports entmtp_bank_info / entmtp_bank_export but not the kernels (they
+ * return ENTMTP_EINVAL for it).  With an arena, the host image is uploaded
+ * with one copy on `stream`, which this call then synchronises (the bank is
+ * built once, off the hot path).  Per tree the arena holds:
+ *   parent int32[T], depth int32[T] (position offset of each node),
+ *   mask uint32[T][ENTMTP_MASK_WORDS] (bit j of row i, word j/32 bit j%32,
+ *   set iff node j is node i or an ancestor of it; bits >= T are zero),
+ *   path int32[T][D+1] (ancestor of node i at depth k, -1 past depth(i)),
+ *   retrieve int32[n_leaves][D+1] (path rows of the leaves, ascending),
+ * where D is the tree's depth.  The bank is immutable after the build; the
+ * caller keeps the arena alive while the bank is used.
+ * Errors: EINVAL (null pointers, n_trees < 1), ETREE, ERANGE, ENOSPC, EHIP.
+ */
+int32_t entmtp_bank_build(const int32_t* parents_host, const int32_t* sizes_host,
+                          int32_t n_trees, void* arena, size_t arena_bytes,
+                          size_t* arena_needed, void* stream, entmtp_bank** out);
+
+/* Free the host handle (not the caller's arena).  NULL is accepted. */
+int32_t entmtp_bank_destroy(entmtp_bank* bank);
+
+/* Number of trees in the bank (or a negative status). */
+int32_t entmtp_bank_size(const entmtp_bank* bank);
+
+/* Host outs (each optional): node count, depth and leaf count of tree `topo`. */
+int32_t entmtp_bank_info(const entmtp_bank* bank, int32_t topo, int32_t* T,
+                         int32_t* D, int32_t* n_leaves);
+
+/* Copy tree `topo`'s buffers to host memory (each pointer optional), with the
+ * shapes documented at entmtp_bank_build: mask [T][ENTMTP_MASK_WORDS], depth
+ * [T], path [T][D+1], retrieve [n_leaves][D+1], parent [T]. */
+int32_t entmtp_bank_export(const entmtp_bank* bank, int32_t topo, uint32_t* mask,
+                           int32_t* depth, int32_t* path, int32_t* retrieve,
+                           int32_t* parent);
+
+/* ------------------------------------------------------------------------ */
+/* Tree-masked attention (§2.3 single sparse verification pass; §3.2: the     */
+/* mask size is part of the per-step verifier cost).                          */
+/* ------------------------------------------------------------------------ */
+
+/* Workspace bytes entmtp_tree_attn needs for these sizes (0 on bad sizes).
+ * Non-decreasing in T and prefix_len, so one query at the largest tree and
+ * the cache capacity covers every later call. */
+size_t entmtp_tree_attn_workspace(int32_t T, int32_t Hq, int32_t Hkv, int32_t d,
+                                  int32_t prefix_len);
+
+/*
+ * One attention layer over the draft tree `topo` of `bank`.
+ *
+ *   q        [T][Hq][d] bf16: queries of the tree nodes.
+ *   k_tree   [T][Hkv][d] bf16, v_tree [T][Hkv][d] bf16: the nodes' keys/values.
+ *   k_cache, v_cache  [Hkv][cap][d] bf16: one layer's cache; slots
+ *            [0, prefix_len) hold the prefix (keys already rotated).
+ *   out      [T][Hq][d] bf16.
+ *   workspace  device scratch of at least entmtp_tree_attn_workspace() bytes.
+ *
+ * The call writes the tree's keys and values into cache slots
+ * [prefix_len, prefix_len + T) and computes, for node i and query head h
+ * (KV head g = h / (Hq / Hkv)), softmax-weighted values over the keys at
+ * slots [0, prefix_len) and prefix_len + j for every node j on i's
+ * root-to-node path, with logits scale * (q . k) and fp32 softmax.  When
+ * rope_theta > 0, q_i and k_i are first rotated to position
+ * prefix_len + depth(i) (pairs (c, c + d/2) turned by the angle
+ * pos * rope_theta^(-2c/d), computed in fp64; the rotated key is rounded to
+ * bf16 once, nearest-even); rope_theta == 0 disables the rotation.
+ * Requirements: d == ENTMTP_HEAD_DIM, Hq % Hkv == 0 (else ERANGE),
+ * cap >= prefix_len + T (else ERANGE), prefix_len >= 0.
+ * Errors: EINVAL, ERANGE, ENOSPC (workspace), EHIP.
+ */
+int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const entmtp_bf16* q,
+                         const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                         entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t cap,
+                         int32_t prefix_len, int32_t Hq, int32_t Hkv, int32_t d,
+                         float scale, float rope_theta, entmtp_bf16* out,
+                         void* workspace, size_t workspace_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* LM-head verification logits (§2.2: next-token distribution softmax(W h);  */
+/* §2.3: one verification pass for all tree nodes).                           */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * logits[i][v] = sum_k hidden[i][k] * w_lm[v][k]   (fp32 accumulation)
+ *
+ *   hidden  [T][hid] bf16: final hidden states of the tree nodes.
+ *   w_lm    [V][hid] bf16: LM-head weight (nn.Linear layout).
+ *   logits  [T][V] fp32.
+ * Requirements: 1 <= T <= 4096, hid % 8 == 0, V >= 1, pointers 16-byte aligned.
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_verify_logits(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                             int32_t T, int32_t hid, int32_t V, float* logits,
+                             void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Per-node softmax statistics (§4: the scheduler reads the top-1            */
+/* probability p0 at the verifier's last position; §3 / App. A: entropy).    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For each row i of logits [T][V] (fp32), with y = inv_temp * z:
+ *   argmax[i]  lowest index attaining max(z)              (int32)
+ *   top1p[i]   exp(max y) / sum_v exp(y_v) = 1 / Z         (fp32)
+ *   entropy[i] -sum_v p_v ln p_v = ln Z - sum (y_v - m) e^(y_v - m) / Z, nats
+ * Each output pointer may be NULL to skip it.  inv_temp must be > 0.
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_logit_stats(const float* logits, int32_t T, int32_t V, float inv_temp,
+                           float* entropy, float* top1p, int32_t* argmax, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Acceptance (§2.1 left-to-right acceptance, greedy case; §5.1 accept       */
+/* length).                                                                   */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Greedy verification of tree `topo`: node i >= 1 is accepted when
+ * draft_tokens[i] == argmax[parent(i)] and its parent is accepted (the root
+ * always is).  best = the deepest accepted node, lowest index among equals.
+ *
+ *   draft_tokens  int32[T] (entry 0, the root's, is ignored)
+ *   argmax        int32[T] target greedy tokens (from entmtp_logit_stats)
+ *   top1p         fp32[T] or NULL
+ *   accept_len    int32 out: depth(best) = accepted draft tokens
+ *   path          int32[D+1] out: root-to-best chain, -1 after accept_len
+ *   bonus         int32 out: argmax[best]
+ *   best_top1p    fp32 out or NULL: top1p[best] (the scheduler's feature)
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draft_tokens,
+                      const int32_t* argmax, const float* top1p, int32_t* accept_len,
+                      int32_t* path, int32_t* bonus, float* best_top1p, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* KV-cache update of the accepted path (§3.2 decode loop).                   */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * For every layer l < n_layers and KV head g < Hkv, and j = 0..a with
+ * a = *accept_len (read on the device):
+ *   cache[l][g][prefix_len + j] <- cache[l][g][prefix_len + path[j]]
+ * for both k_cache and v_cache, all reads before any write (a source slot may
+ * be another row's destination).  Layer l's cache starts layer_stride
+ * elements after layer l-1's; each layer is [Hkv][cap][d].  Slots past
+ * prefix_len + a are left as they were.  path (device int32[path_capacity])
+ * and accept_len come from entmtp_accept on the same stream.  The kernel
+ * clamps a to [0, min(path_capacity, ENTMTP_D_MAX + 1) - 1] and skips (leaves
+ * unchanged) any row whose source or destination slot would fall outside
+ * [0, cap).
+ * Requirements: d % 8 == 0, 8 <= d <= 256, prefix_len >= 0, cap >= 1,
+ * path_capacity >= 1, layer_stride >= Hkv * cap * d when n_layers > 1,
+ * 16-byte aligned caches.
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_kv_compact(const int32_t* path, int32_t path_capacity,
+                          const int32_t* accept_len, int32_t prefix_len,
+                          entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t n_layers,
+                          int64_t layer_stride, int32_t Hkv, int32_t cap, int32_t d,
+                          void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Scheduler policy (§4 "Policy"), host only.                                 */
+/* ------------------------------------------------------------------------ */
+
+/* Hysteretic ladder over a bank sorted by size: climb one rung when
+ * s > tau_on, descend one when s <= tau_off, else stay; clamped to
+ * [0, n_rungs).  Returns the next rung (or a negative status). */
+int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
+                           float tau_off);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* ENTMTP_H */

@@ -1,0 +1,298 @@
+"""ctypes binding of ``libentmtp.so``: argument marshalling only.
+
+Every function here forwards to the C ABI declared in ``include/entmtp.h``
+with the same name (minus the ``entmtp_`` prefix); all computation happens in
+the library's HIP kernels.  Tensors are torch tensors on the GPU (bf16 ones as
+``torch.bfloat16``); the stream defaults to torch's current stream.  Importing
+this module fails if the library has not been built.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Sequence
+
+import numpy as np
+
+_LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libentmtp.so")
+
+OK, EINVAL, ETREE, ERANGE, ENOSPC, EHIP = 0, -1, -2, -3, -4, -5
+T_MAX, D_MAX, MASK_WORDS, HEAD_DIM = 256, 31, 8, 128
+
+_c_i32, _c_i64, _c_f32, _c_sz, _c_p = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
+                                       ctypes.c_size_t, ctypes.c_void_p)
+
+# name -> (restype, argtypes), mirroring include/entmtp.h
+_SIGNATURES = {
+    "entmtp_last_error": (ctypes.c_char_p, []),
+    "entmtp_version": (ctypes.c_char_p, []),
+    "entmtp_bank_build": (_c_i32, [_c_p, _c_p, _c_i32, _c_p, _c_sz, ctypes.POINTER(_c_sz), _c_p,
+                                   ctypes.POINTER(_c_p)]),
+    "entmtp_bank_destroy": (_c_i32, [_c_p]),
+    "entmtp_bank_size": (_c_i32, [_c_p]),
+    "entmtp_bank_info": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p]),
+    "entmtp_bank_export": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_tree_attn_workspace": (_c_sz, [_c_i32, _c_i32, _c_i32, _c_i32, _c_i32]),
+    "entmtp_tree_attn": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32,
+                                  _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p, _c_sz, _c_p]),
+    "entmtp_verify_logits": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p]),
+    "entmtp_logit_stats": (_c_i32, [_c_p, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_accept": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_kv_compact": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64, _c_i32,
+                                   _c_i32, _c_i32, _c_p]),
+    "entmtp_ladder_next": (_c_i32, [_c_i32, _c_i32, _c_f32, _c_f32, _c_f32]),
+}
+
+
+def _hip_runtimes():
+    try:
+        with open("/proc/self/maps") as f:
+            return sorted({l.split()[-1] for l in f if "libamdhip64" in l})
+    except OSError:
+        return []
+
+
+def _load():
+    if not os.path.exists(_LIB_PATH):
+        raise ImportError(f"{_LIB_PATH} is missing: build it with "
+                          "`python -m paper_2606_27550_amd.build`")
+    # torch owns the device memory and streams handed to the library, so the
+    # library must resolve to the HIP runtime torch already loaded (the
+    # dynamic loader reuses it by soname when torch comes first).
+    try:
+        import torch  # noqa: F401
+    except ImportError:
+        pass
+    lib = ctypes.CDLL(_LIB_PATH)
+    rts = _hip_runtimes()
+    if len(rts) > 1:
+        raise ImportError("two HIP runtimes are loaded in this process "
+                          f"({rts}); import torch before anything that loads libamdhip64")
+    for name, (res, args) in _SIGNATURES.items():
+        fn = getattr(lib, name)
+        fn.restype = res
+        fn.argtypes = args
+    return lib
+
+
+lib = _load()
+LIB_PATH = _LIB_PATH
+
+
+class EntmtpError(RuntimeError):
+    def __init__(self, code: int, message: str):
+        super().__init__(f"entmtp status {code}: {message}")
+        self.code = code
+
+
+def _check(rc: int) -> int:
+    if rc < 0:
+        raise EntmtpError(rc, lib.entmtp_last_error().decode())
+    return rc
+
+
+def last_error() -> str:
+    return lib.entmtp_last_error().decode()
+
+
+def _p(t):
+    """Device pointer of a tensor (None -> NULL)."""
+    return None if t is None else ctypes.c_void_p(t.data_ptr())
+
+
+def _np_p(a: np.ndarray):
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _stream(stream):
+    if stream is None:
+        import torch
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream if hasattr(stream, "cuda_stream") else int(stream))
+
+
+# --------------------------------------------------------------------- bank --
+
+class Bank:
+    """TopologyBank: the trees' masks, depths, paths and retrieve rows in one
+    device arena.  ``device=None`` builds a host-only bank (info / export
+    only, no GPU involved)."""
+
+    def __init__(self, trees: Sequence[Sequence[int]], device="cuda", stream=None):
+        self.trees = [list(map(int, t)) for t in trees]
+        parents = np.ascontiguousarray(np.concatenate([np.asarray(t, np.int32) for t in self.trees])
+                                       if self.trees else np.zeros(0, np.int32))
+        sizes = np.ascontiguousarray([len(t) for t in self.trees], dtype=np.int32)
+        need = _c_sz(0)
+        handle = _c_p(None)
+        self._handle = None
+        self.arena = None
+        if device is None:
+            _check(lib.entmtp_bank_build(_np_p(parents), _np_p(sizes), len(self.trees), None, 0,
+                                         ctypes.byref(need), None, ctypes.byref(handle)))
+        else:
+            import torch
+            _check(lib.entmtp_bank_build(_np_p(parents), _np_p(sizes), len(self.trees), None, 0,
+                                         ctypes.byref(need), None, None))
+            self.arena = torch.empty(max(int(need.value), 256), dtype=torch.uint8, device=device)
+            _check(lib.entmtp_bank_build(_np_p(parents), _np_p(sizes), len(self.trees),
+                                         _p(self.arena), self.arena.numel(), ctypes.byref(need),
+                                         _stream(stream), ctypes.byref(handle)))
+        self._handle = handle
+        self.arena_bytes = int(need.value)
+        self.T, self.D, self.n_leaves = [], [], []
+        for k in range(len(self.trees)):
+            T, D, nl = _c_i32(), _c_i32(), _c_i32()
+            _check(lib.entmtp_bank_info(self._handle, k, ctypes.byref(T), ctypes.byref(D),
+                                        ctypes.byref(nl)))
+            self.T.append(T.value)
+            self.D.append(D.value)
+            self.n_leaves.append(nl.value)
+
+    @property
+    def handle(self):
+        return self._handle
+
+    def __len__(self):
+        return len(self.trees)
+
+    def export(self, topo: int) -> dict:
+        T, D, nl = self.T[topo], self.D[topo], self.n_leaves[topo]
+        mask = np.zeros((T, MASK_WORDS), np.uint32)
+        depth = np.zeros(T, np.int32)
+        path = np.zeros((T, D + 1), np.int32)
+        retrieve = np.zeros((nl, D + 1), np.int32)
+        parent = np.zeros(T, np.int32)
+        _check(lib.entmtp_bank_export(self._handle, topo, _np_p(mask), _np_p(depth), _np_p(path),
+                                      _np_p(retrieve), _np_p(parent)))
+        return {"T": T, "D": D, "mask": mask, "depth": depth, "path": path,
+                "retrieve": retrieve, "parent": parent,
+                "leaves": np.array([row[row >= 0][-1] for row in retrieve], np.int32)}
+
+    def close(self):
+        if self._handle is not None and self._handle.value:
+            lib.entmtp_bank_destroy(self._handle)
+        self._handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+# ------------------------------------------------------------------ kernels --
+
+def _need(cond: bool, msg: str) -> None:
+    if not cond:
+        raise ValueError(msg)
+
+
+def _dev(t, name, dtype, shape=None, min_numel=None):
+    """Host-side check that a tensor is what the kernel will assume."""
+    import torch
+    _need(isinstance(t, torch.Tensor), f"{name} must be a torch tensor")
+    _need(t.is_cuda, f"{name} must live on the GPU")
+    _need(t.dtype == dtype, f"{name} must be {dtype}, got {t.dtype}")
+    _need(t.is_contiguous(), f"{name} must be contiguous")
+    if shape is not None:
+        _need(tuple(t.shape) == tuple(shape), f"{name} has shape {tuple(t.shape)}, expected {tuple(shape)}")
+    if min_numel is not None:
+        _need(t.numel() >= min_numel, f"{name} needs at least {min_numel} elements")
+
+
+def tree_attn_workspace(T: int, Hq: int, Hkv: int, d: int, prefix_len: int) -> int:
+    return int(lib.entmtp_tree_attn_workspace(T, Hq, Hkv, d, prefix_len))
+
+
+def tree_attn(bank: Bank, topo: int, q, k_tree, v_tree, k_cache, v_cache, prefix_len: int,
+              scale: float, rope_theta: float, out, workspace, stream=None) -> None:
+    """q [T,Hq,d], k_tree/v_tree [T,Hkv,d], caches [Hkv,cap,d], out [T,Hq,d] (bf16)."""
+    import torch
+    _need(0 <= topo < len(bank), "topo out of range")
+    T = bank.T[topo]
+    _need(q.dim() == 3 and k_cache.dim() == 3, "q and caches are 3-D")
+    _, Hq, d = q.shape
+    Hkv, cap, _ = k_cache.shape
+    bf = torch.bfloat16
+    _dev(q, "q", bf, (T, Hq, d))
+    _dev(k_tree, "k_tree", bf, (T, Hkv, d))
+    _dev(v_tree, "v_tree", bf, (T, Hkv, d))
+    _dev(k_cache, "k_cache", bf, (Hkv, cap, d))
+    _dev(v_cache, "v_cache", bf, (Hkv, cap, d))
+    _dev(out, "out", bf, (T, Hq, d))
+    _need(workspace.is_cuda and workspace.is_contiguous(), "workspace must be a contiguous GPU tensor")
+    _check(lib.entmtp_tree_attn(bank.handle, topo, _p(q), _p(k_tree), _p(v_tree), _p(k_cache),
+                                _p(v_cache), cap, prefix_len, Hq, Hkv, d, scale, rope_theta,
+                                _p(out), _p(workspace), workspace.numel() * workspace.element_size(),
+                                _stream(stream)))
+
+
+def verify_logits(hidden, w_lm, logits, stream=None) -> None:
+    """hidden [T,hid] bf16, w_lm [V,hid] bf16 -> logits [T,V] fp32."""
+    import torch
+    _need(hidden.dim() == 2 and w_lm.dim() == 2, "hidden and w_lm are 2-D")
+    T, hid = hidden.shape
+    V = w_lm.shape[0]
+    _dev(hidden, "hidden", torch.bfloat16, (T, hid))
+    _dev(w_lm, "w_lm", torch.bfloat16, (V, hid))
+    _dev(logits, "logits", torch.float32, (T, V))
+    _check(lib.entmtp_verify_logits(_p(hidden), _p(w_lm), T, hid, V, _p(logits), _stream(stream)))
+
+
+def logit_stats(logits, inv_temp: float, entropy, top1p, argmax, stream=None) -> None:
+    import torch
+    _need(logits.dim() == 2, "logits are 2-D")
+    T, V = logits.shape
+    _dev(logits, "logits", torch.float32, (T, V))
+    for name, t, dt in (("entropy", entropy, torch.float32), ("top1p", top1p, torch.float32),
+                        ("argmax", argmax, torch.int32)):
+        if t is not None:
+            _dev(t, name, dt, min_numel=T)
+    _check(lib.entmtp_logit_stats(_p(logits), T, V, inv_temp, _p(entropy), _p(top1p), _p(argmax),
+                                  _stream(stream)))
+
+
+def accept(bank: Bank, topo: int, draft_tokens, argmax, top1p, accept_len, path, bonus,
+           best_top1p=None, stream=None) -> None:
+    import torch
+    _need(0 <= topo < len(bank), "topo out of range")
+    T, D = bank.T[topo], bank.D[topo]
+    _dev(draft_tokens, "draft_tokens", torch.int32, min_numel=T)
+    _dev(argmax, "argmax", torch.int32, min_numel=T)
+    if top1p is not None:
+        _dev(top1p, "top1p", torch.float32, min_numel=T)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=1)
+    _dev(path, "path", torch.int32, min_numel=D + 1)
+    _dev(bonus, "bonus", torch.int32, min_numel=1)
+    if best_top1p is not None:
+        _dev(best_top1p, "best_top1p", torch.float32, min_numel=1)
+    _check(lib.entmtp_accept(bank.handle, topo, _p(draft_tokens), _p(argmax), _p(top1p),
+                             _p(accept_len), _p(path), _p(bonus), _p(best_top1p),
+                             _stream(stream)))
+
+
+def kv_compact(path, accept_len, prefix_len: int, k_cache, v_cache, stream=None) -> None:
+    """Caches [Hkv,cap,d] (one layer) or [n_layers,Hkv,cap,d] (bf16)."""
+    import torch
+    _need(k_cache.dim() in (3, 4) and v_cache.shape == k_cache.shape, "caches are 3-D or 4-D, equal shapes")
+    _dev(k_cache, "k_cache", torch.bfloat16)
+    _dev(v_cache, "v_cache", torch.bfloat16)
+    _dev(path, "path", torch.int32, min_numel=1)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=1)
+    if k_cache.dim() == 3:
+        n_layers, (Hkv, cap, d) = 1, k_cache.shape
+        stride = Hkv * cap * d
+    else:
+        n_layers, Hkv, cap, d = k_cache.shape
+        stride = Hkv * cap * d
+    _check(lib.entmtp_kv_compact(_p(path), path.numel(), _p(accept_len), prefix_len, _p(k_cache),
+                                 _p(v_cache), n_layers, stride, Hkv, cap, d, _stream(stream)))
+
+
+def ladder_next(rung: int, n_rungs: int, s: float, tau_on: float, tau_off: float) -> int:
+    return _check(lib.entmtp_ladder_next(rung, n_rungs, s, tau_on, tau_off))
+
+
+def version() -> str:
+    return lib.entmtp_version().decode()

@@ -1,0 +1,82 @@
+// Greedy tree acceptance and the longest accepted path.
+//
+// Left-to-right acceptance of §2.1, in its greedy form over a tree: a node is
+// accepted when its draft token equals the target's greedy token at its
+// parent and every ancestor is accepted.  With the tree's ancestor bitmask
+// (the same per-node rows the attention kernel uses) "every ancestor is
+// accepted" becomes a subset test of the node's mask row against the set of
+// locally matching nodes, so all nodes are decided in parallel.  The answer is
+// the deepest accepted node, lowest index among equals; its depth is the
+// accept length (§5.1).  One workgroup handles the whole tree.
+#include "common.hpp"
+
+namespace entmtp {
+namespace {
+
+constexpr int kAcceptThreads = ENTMTP_T_MAX;
+
+__global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
+    const int* __restrict__ parent, const int* __restrict__ depth,
+    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
+    const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
+    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
+    float* __restrict__ best_p) {
+  __shared__ uint32_t matched[ENTMTP_MASK_WORDS];
+  __shared__ int s_key[kAcceptThreads / 64];
+  const int i = threadIdx.x;
+  if (i < ENTMTP_MASK_WORDS) matched[i] = 0u;
+  __syncthreads();
+  if (i < T) {
+    const bool ok = (i == 0) || (tok[i] == amax[parent[i]]);
+    if (ok) atomicOr(&matched[i >> 5], 1u << (i & 31));
+  }
+  __syncthreads();
+  // key orders accepted nodes by depth, then by lower index
+  int key = -1;
+  if (i < T) {
+    bool acc = true;
+#pragma unroll
+    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w)
+      acc = acc && ((mask[i * ENTMTP_MASK_WORDS + w] & ~matched[w]) == 0u);
+    if (acc) key = depth[i] * 1024 + (1023 - i);
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) key = max(key, __shfl_xor(key, off, 64));
+  if ((i & 63) == 0) s_key[i >> 6] = key;
+  __syncthreads();
+  key = s_key[0];
+#pragma unroll
+  for (int w = 1; w < kAcceptThreads / 64; ++w) key = max(key, s_key[w]);
+  const int best = 1023 - (key & 1023);
+  const int a = key >> 10;
+  if (i <= D) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
+  if (i == 0) {
+    *accept_len = a;
+    *bonus = amax[best];
+    if (best_p) *best_p = top1p[best];
+  }
+}
+
+}  // namespace
+}  // namespace entmtp
+
+using namespace entmtp;
+
+extern "C" int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo,
+                                 const int32_t* draft_tokens, const int32_t* argmax,
+                                 const float* top1p, int32_t* accept_len, int32_t* path,
+                                 int32_t* bonus, float* best_top1p, void* stream) {
+  clear_error();
+  if (int32_t rc = check_device_bank(bank, topo)) return rc;
+  ENTMTP_CHECK_ARG(draft_tokens && argmax && accept_len && path && bonus, ENTMTP_EINVAL,
+                   "draft_tokens, argmax, accept_len, path and bonus must be non-NULL");
+  ENTMTP_CHECK_ARG(best_top1p == nullptr || top1p != nullptr, ENTMTP_EINVAL,
+                   "best_top1p needs top1p");
+  const TopoDesc& d = bank->desc[topo];
+  hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(kAcceptThreads), 0,
+                     static_cast<hipStream_t>(stream), bank_ptr<int>(bank, d.off_parent),
+                     bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
+                     bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, argmax, top1p,
+                     accept_len, path, bonus, best_top1p);
+  return launch_status("accept launch");
+}

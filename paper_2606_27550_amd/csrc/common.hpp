@@ -1,0 +1,100 @@
+// Internal definitions shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime.h>
+
+#include <cstdint>
+#include <cstdio>
+#include <string>
+#include <vector>
+
+#include "entmtp.h"
+
+namespace entmtp {
+
+// ---------------------------------------------------------------- errors --
+
+// Records `msg` as the calling thread's last error and returns `code`.
+int32_t fail(int32_t code, const char* fmt, ...);
+void clear_error();
+
+#define ENTMTP_CHECK_ARG(cond, code, ...) \
+  do {                                    \
+    if (!(cond)) return ::entmtp::fail(code, __VA_ARGS__); \
+  } while (0)
+
+// Checks the launch that was just made (or any HIP call's return code).
+int32_t hip_status(hipError_t e, const char* what);
+inline int32_t launch_status(const char* what) { return hip_status(hipGetLastError(), what); }
+
+// ------------------------------------------------------------------ bank --
+
+// Byte offsets of one tree's arrays inside the bank arena.
+struct TopoDesc {
+  int32_t T;         // nodes, root included
+  int32_t D;         // depth of the deepest node
+  int32_t n_leaves;
+  int32_t pad;
+  int64_t off_parent;    // int32[T]
+  int64_t off_depth;     // int32[T]
+  int64_t off_mask;      // uint32[T][ENTMTP_MASK_WORDS]
+  int64_t off_path;      // int32[T][D+1]
+  int64_t off_retrieve;  // int32[n_leaves][D+1]
+};
+
+}  // namespace entmtp
+
+struct entmtp_bank {
+  std::vector<entmtp::TopoDesc> desc;
+  std::vector<uint8_t> image;  // host copy of the arena contents
+  uint8_t* arena = nullptr;    // device arena (nullptr for a host-only bank)
+  int device = -1;
+};
+
+namespace entmtp {
+
+// Validates (bank, topo) for a kernel launch; returns 0 or an error status.
+int32_t check_device_bank(const entmtp_bank* bank, int32_t topo);
+
+template <typename T>
+inline const T* bank_ptr(const entmtp_bank* b, int64_t off) {
+  return reinterpret_cast<const T*>(b->arena + off);
+}
+
+inline bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+// --------------------------------------------------------- device helpers --
+
+typedef __bf16 bf16x8 __attribute__((ext_vector_type(8)));
+typedef float f32x4 __attribute__((ext_vector_type(4)));
+typedef float f32x16 __attribute__((ext_vector_type(16)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+
+// fp32 -> bf16 bits, round to nearest even (finite inputs).
+__device__ __forceinline__ uint32_t f32_to_bf16_rne(float f) {
+  uint32_t u = __float_as_uint(f);
+  u += 0x7FFFu + ((u >> 16) & 1u);
+  return u >> 16;
+}
+
+// fp64 -> bf16 bits with a single rounding (nearest even) straight from the
+// double's mantissa: after rounding the mantissa to 7 bits the value is
+// exactly representable in fp32, whose top half is the bf16 pattern.
+__device__ __forceinline__ uint32_t f64_to_bf16_rne(double x) {
+  uint64_t u = static_cast<uint64_t>(__double_as_longlong(x));
+  const uint64_t lsb = (u >> 45) & 1ull;
+  u += 0x00000FFFFFFFFFFFull + lsb;
+  u &= ~0x00001FFFFFFFFFFFull;
+  float f = static_cast<float>(__longlong_as_double(static_cast<long long>(u)));
+  return __float_as_uint(f) >> 16;
+}
+
+__device__ __forceinline__ float bf16_lo(uint32_t w) { return __uint_as_float(w << 16); }
+__device__ __forceinline__ float bf16_hi(uint32_t w) { return __uint_as_float(w & 0xFFFF0000u); }
+__device__ __forceinline__ double bf16_to_f64(uint16_t b) {
+  return static_cast<double>(__uint_as_float(static_cast<uint32_t>(b) << 16));
+}
+
+__device__ __forceinline__ bf16x8 as_bf16x8(u32x4 v) { return __builtin_bit_cast(bf16x8, v); }
+
+}  // namespace entmtp

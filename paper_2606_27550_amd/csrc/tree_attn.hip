@@ -1,0 +1,496 @@
+// Tree-masked attention of the verification pass.
+//
+// §2.3: the draft tree is verified in a single sparse forward pass of the
+// target model with a precomputed tree attention mask and position offsets;
+// §3.2 names the mask size among the per-step verifier costs.  Node i of the
+// tree attends to the whole prefix and to the nodes on its own root-to-node
+// path; it sits at sequence position prefix_len + depth(i).
+//
+// Three kernels, all on the caller's stream:
+//  1. prep: rotate q and the tree's keys to their positions (fp64 angles,
+//     one bf16 rounding), write the tree's K/V into cache slots
+//     [L, L+T) and the rotated queries into the workspace, grouped per KV
+//     head (GQA: query rows = head-in-group x node).
+//  2. attend: flash-decoding over the cache.  A workgroup owns one
+//     (KV head, 32-query tile, key split); its four waves take interleaved
+//     32-key blocks.  S^T = K Q^T and O^T += V^T P^T run on
+//     v_mfma_f32_32x32x16_bf16: K comes from HBM straight into A-operand
+//     registers, V is transposed through a per-wave LDS tile, P never leaves
+//     registers (the S^T accumulator layout is re-read as the B operand of
+//     the PV product after a fixed key permutation).  Keys at or past the
+//     prefix are masked with a 32-bit window cut from the node's ancestor
+//     bitmask.  Online softmax in fp32, base 2.  The four waves merge in LDS.
+//  3. merge: combines the splits' (max, sum, unnormalised output) partials.
+//     Skipped when a single split covers the keys.
+#include <cfloat>
+
+#include "common.hpp"
+
+namespace entmtp {
+namespace {
+
+constexpr int HD = ENTMTP_HEAD_DIM;  // 128
+constexpr int kAttnThreads = 256;
+constexpr int kAttnWaves = 4;
+constexpr int KB = 32;               // keys per block
+constexpr int kQTile = 32;           // query rows per tile
+constexpr int VT_LD = 36;            // bf16 per V^T row in LDS (32 keys + pad)
+constexpr int kMaxSplits = 32;
+constexpr int kMinBlocksPerSplit = 8;
+
+__host__ __device__ inline int rows_padded(int G, int T) {
+  return (G * T + kQTile - 1) / kQTile * kQTile;
+}
+
+// ------------------------------------------------------------------ prep --
+
+__global__ __launch_bounds__(256) void attn_prep_kernel(
+    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kt,
+    const uint16_t* __restrict__ vt, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
+    uint16_t* __restrict__ qrot, const int* __restrict__ depth, int T, int Hq, int Hkv, int cap,
+    int L, double theta, int rows_pad) {
+  constexpr int HALF = HD / 2;
+  __shared__ double s_cos[HALF], s_sin[HALF];
+  const int i = blockIdx.x;
+  const int G = Hq / Hkv;
+  const bool rope = theta > 0.0;
+  if (rope) {
+    const double pos = static_cast<double>(L) + static_cast<double>(depth[i]);
+    for (int c = threadIdx.x; c < HALF; c += blockDim.x) {
+      const double ang = pos * pow(theta, -2.0 * c / HD);
+      double sn, cs;
+      sincos(ang, &sn, &cs);
+      s_cos[c] = cs;
+      s_sin[c] = sn;
+    }
+  }
+  __syncthreads();
+  // queries -> workspace rows (g, gh * T + i)
+  for (int u = threadIdx.x; u < Hq * HALF; u += blockDim.x) {
+    const int h = u / HALF, c = u % HALF;
+    const uint16_t* src = q + (static_cast<size_t>(i) * Hq + h) * HD;
+    uint16_t* dst = qrot + (static_cast<size_t>(h / G) * rows_pad + (h % G) * T + i) * HD;
+    if (rope) {
+      const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
+      dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * s_cos[c] - hi * s_sin[c]));
+      dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * s_cos[c] + lo * s_sin[c]));
+    } else {
+      dst[c] = src[c];
+      dst[c + HALF] = src[c + HALF];
+    }
+  }
+  // keys -> cache slot L + i
+  for (int u = threadIdx.x; u < Hkv * HALF; u += blockDim.x) {
+    const int g = u / HALF, c = u % HALF;
+    const uint16_t* src = kt + (static_cast<size_t>(i) * Hkv + g) * HD;
+    uint16_t* dst = kc + (static_cast<size_t>(g) * cap + L + i) * HD;
+    if (rope) {
+      const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
+      dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * s_cos[c] - hi * s_sin[c]));
+      dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * s_cos[c] + lo * s_sin[c]));
+    } else {
+      dst[c] = src[c];
+      dst[c + HALF] = src[c + HALF];
+    }
+  }
+  // values -> cache slot L + i
+  for (int u = threadIdx.x; u < Hkv * (HD / 8); u += blockDim.x) {
+    const int g = u / (HD / 8), c8 = u % (HD / 8);
+    *reinterpret_cast<u32x4*>(vc + (static_cast<size_t>(g) * cap + L + i) * HD + 8 * c8) =
+        *reinterpret_cast<const u32x4*>(vt + (static_cast<size_t>(i) * Hkv + g) * HD + 8 * c8);
+  }
+}
+
+// ---------------------------------------------------------------- attend --
+
+struct AttnArgs {
+  const uint16_t* qrot;   // [Hkv][rows_pad][HD]
+  const uint16_t* kc;     // [Hkv][cap][HD]
+  const uint16_t* vc;
+  const uint32_t* mask;   // [T][ENTMTP_MASK_WORDS]
+  float* part_o;          // [nsplit][Hkv][rows_pad][HD]
+  float* part_ml;         // [nsplit][Hkv][rows_pad][2]
+  uint16_t* out;          // [T][Hq][HD]
+  int T, G, Hq, Hkv, cap, L, nkeys, rows_pad, nqt, nsplit, bps;
+  float scale_log2;
+};
+
+__device__ __forceinline__ void wave_lds_sync() {
+  __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+  __builtin_amdgcn_wave_barrier();
+  __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+}
+
+__global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
+  // blockIdx -> (kv head, split) group and query tile; the query tiles of one
+  // group land on the same XCD (dispatch is round-robin over 8 XCDs), so
+  // their K/V reads share that XCD's L2.
+  const int bid = blockIdx.x;
+  const int qt = (bid >> 3) % p.nqt;
+  const int gc = ((bid >> 3) / p.nqt) * 8 + (bid & 7);
+  if (gc >= p.Hkv * p.nsplit) return;
+  const int g = gc / p.nsplit, split = gc % p.nsplit;
+
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 31, lh = lane >> 5;
+  const int GT = p.G * p.T;
+
+  // LDS: per-wave V^T tiles during the loop, reused for the wave merge after it
+  constexpr int kVtBytes = HD * VT_LD * 2;                           // 9216
+  constexpr int OLD = HD + 1;                                         // merge row stride (bank spread)
+  constexpr int kMergeBytes = kAttnWaves * kQTile * OLD * 4;         // 66048
+  constexpr int kLdsBytes = kMergeBytes > kAttnWaves * kVtBytes ? kMergeBytes : kAttnWaves * kVtBytes;
+  __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
+  __shared__ uint32_t s_mask[kQTile][ENTMTP_MASK_WORDS + 1];
+  __shared__ float s_m[kAttnWaves][kQTile], s_l[kAttnWaves][kQTile];
+
+  // ancestor masks of this tile's query rows (padding rows see every key)
+  for (int u = tid; u < kQTile * ENTMTP_MASK_WORDS; u += kAttnThreads) {
+    const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
+    const int qrow = qt * kQTile + r;
+    s_mask[r][w] = qrow < GT ? p.mask[(qrow % p.T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+  }
+
+  // Q^T B-operand fragments: lane (query li, half lh) holds d = 16s + 8lh + e
+  const int qrow = qt * kQTile + li;
+  u32x4 qf[8];
+  {
+    const uint16_t* qp = p.qrot + (static_cast<size_t>(g) * p.rows_pad + qrow) * HD + 8 * lh;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      qf[s] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+  }
+  __syncthreads();
+
+  uint32_t* vt = reinterpret_cast<uint32_t*>(lds + wave * kVtBytes);  // [HD][VT_LD/2] key pairs
+  const size_t head_off = static_cast<size_t>(g) * p.cap * HD;
+  const uint16_t* kbase = p.kc + head_off;
+  const uint16_t* vbase = p.vc + head_off;
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 o[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ct][r] = 0.f;
+
+  const int nblocks = (p.nkeys + KB - 1) / KB;
+  const int blk_lo = split * p.bps;
+  const int blk_hi = min(nblocks, blk_lo + p.bps);
+
+  for (int blk = blk_lo + wave; blk < blk_hi; blk += kAttnWaves) {
+    const int kb = blk * KB;
+    // K: A operand, lane (key li, half lh)
+    u32x4 kf[8];
+    {
+      const int key = kb + li;
+      const uint16_t* kp = kbase + static_cast<size_t>(key) * HD + 8 * lh;
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        kf[s] = key < p.nkeys ? *reinterpret_cast<const u32x4*>(kp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+    }
+    // V: key pairs (2pp, 2pp+1) x 8-dim chunk m, transposed into LDS
+    u32x4 v0[4], v1[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int u = lane + 64 * k;
+      const int pp = u & 15, m = u >> 4;
+      const int key0 = kb + 2 * pp;
+      const uint16_t* vp = vbase + static_cast<size_t>(key0) * HD + 8 * m;
+      v0[k] = key0 < p.nkeys ? *reinterpret_cast<const u32x4*>(vp) : u32x4{0u, 0u, 0u, 0u};
+      v1[k] = key0 + 1 < p.nkeys ? *reinterpret_cast<const u32x4*>(vp + HD) : u32x4{0u, 0u, 0u, 0u};
+    }
+    wave_lds_sync();  // previous block's V^T reads are done
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int u = lane + 64 * k;
+      const int pp = u & 15, m = u >> 4;
+#pragma unroll
+      for (int w = 0; w < 4; ++w) {
+        const uint32_t a = v0[k][w], b = v1[k][w];
+        // dims 8m + 2w (low halves) and 8m + 2w + 1 (high halves)
+        vt[(8 * m + 2 * w) * (VT_LD / 2) + pp] = (a & 0xFFFFu) | (b << 16);
+        vt[(8 * m + 2 * w + 1) * (VT_LD / 2) + pp] = (a >> 16) | (b & 0xFFFF0000u);
+      }
+    }
+
+    // S^T[key][query] = K Q^T
+    f32x16 sacc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[s]), as_bf16x8(qf[s]), sacc, 0, 0, 0);
+
+    // mask: lane holds keys n = 8*(r/4) + 4*lh + r%4 of the block for query li
+    uint32_t win = 0xFFFFFFFFu;
+    const int rel = kb - p.L;
+    if (rel > -KB) {
+      if (rel < 0) {
+        const int npre = -rel;
+        win = (0xFFFFFFFFu >> (32 - npre)) | (s_mask[li][0] << npre);
+      } else {
+        const int wi = rel >> 5, sh = rel & 31;
+        const uint32_t lo = s_mask[li][wi];
+        const uint32_t hi = wi + 1 < ENTMTP_MASK_WORDS ? s_mask[li][wi + 1] : 0u;
+        win = sh ? (lo >> sh) | (hi << (32 - sh)) : lo;
+      }
+    }
+    float sv[16];
+    float bmax = -INFINITY;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int n = 8 * (r >> 2) + 4 * lh + (r & 3);
+      const bool vis = ((win >> n) & 1u) && (kb + n < p.nkeys);
+      sv[r] = vis ? sacc[r] * p.scale_log2 : -INFINITY;
+      bmax = fmaxf(bmax, sv[r]);
+    }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float m_new = fmaxf(m_run, bmax);
+    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
+    float rsum = 0.f;
+    float pr[16];
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      pr[r] = (m_new == -INFINITY) ? 0.f : exp2f(sv[r] - m_new);
+      rsum += pr[r];
+    }
+    rsum += __shfl_xor(rsum, 32, 64);
+    l_run = l_run * alpha + rsum;
+    m_run = m_new;
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
+
+    // P^T as B operand: step t covers keys 16t..16t+15; element e of lane
+    // (query li, half lh) is key 16t + 4lh + e (e < 4) or 16t + 8 + 4lh + e-4
+    // -- exactly accumulator entries 8t .. 8t+7.
+    bf16x8 pf[2];
+#pragma unroll
+    for (int t = 0; t < 2; ++t) {
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = f32_to_bf16_rne(pr[8 * t + 2 * e]) | (f32_to_bf16_rne(pr[8 * t + 2 * e + 1]) << 16);
+      pf[t] = as_bf16x8(w);
+    }
+    wave_lds_sync();  // V^T tile written by every lane
+    // O^T[dim][query] += V^T P^T; A operand lane (dim li of tile ct, half lh)
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const uint32_t* row = vt + (32 * ct + li) * (VT_LD / 2);
+#pragma unroll
+      for (int t = 0; t < 2; ++t) {
+        const uint2 x0 = *reinterpret_cast<const uint2*>(row + 8 * t + 2 * lh);
+        const uint2 x1 = *reinterpret_cast<const uint2*>(row + 8 * t + 4 + 2 * lh);
+        const u32x4 w = {x0.x, x0.y, x1.x, x1.y};
+        o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t], o[ct], 0, 0, 0);
+      }
+    }
+  }
+
+  // ---- merge the four waves (fixed order)
+  __syncthreads();  // every wave is done with its V^T tile
+  if (lh == 0) {
+    s_m[wave][li] = m_run;
+    s_l[wave][li] = l_run;
+  }
+  __syncthreads();
+  float M = -INFINITY;
+#pragma unroll
+  for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][li]);
+  const float myscale = (m_run == -INFINITY) ? 0.f : exp2f(m_run - M);
+  float* ored = reinterpret_cast<float*>(lds);  // [wave][query][HD]
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      const int dim = 32 * ct + 8 * (r >> 2) + 4 * lh + (r & 3);
+      ored[(wave * kQTile + li) * OLD + dim] = o[ct][r] * myscale;
+    }
+  __syncthreads();
+  for (int u = tid; u < kQTile * HD; u += kAttnThreads) {
+    const int q = u / HD, dim = u % HD;
+    const int row = qt * kQTile + q;
+    if (row >= GT) continue;
+    float Mq = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) Mq = fmaxf(Mq, s_m[w][q]);
+    float lsum = 0.f, osum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      const float sc = (s_m[w][q] == -INFINITY) ? 0.f : exp2f(s_m[w][q] - Mq);
+      lsum += s_l[w][q] * sc;
+      osum += ored[(w * kQTile + q) * OLD + dim];
+    }
+    if (p.nsplit == 1) {
+      const int gh = row / p.T, node = row % p.T;
+      const int h = g * p.G + gh;
+      p.out[(static_cast<size_t>(node) * p.Hq + h) * HD + dim] =
+          static_cast<uint16_t>(f32_to_bf16_rne(osum / lsum));
+    } else {
+      const size_t prow = (static_cast<size_t>(split) * p.Hkv + g) * p.rows_pad + row;
+      p.part_o[prow * HD + dim] = osum;
+      if (dim == 0) {
+        p.part_ml[prow * 2 + 0] = Mq;
+        p.part_ml[prow * 2 + 1] = lsum;
+      }
+    }
+  }
+}
+
+// ----------------------------------------------------------------- merge --
+
+__global__ __launch_bounds__(HD) void attn_merge_kernel(const float* __restrict__ part_o,
+                                                        const float* __restrict__ part_ml,
+                                                        uint16_t* __restrict__ out, int T, int G,
+                                                        int Hq, int Hkv, int rows_pad,
+                                                        int nsplit) {
+  const int g = blockIdx.x / (G * T), row = blockIdx.x % (G * T);
+  const int dim = threadIdx.x;
+  float M = -INFINITY;
+  for (int c = 0; c < nsplit; ++c)
+    M = fmaxf(M, part_ml[((static_cast<size_t>(c) * Hkv + g) * rows_pad + row) * 2]);
+  float lsum = 0.f, osum = 0.f;
+  for (int c = 0; c < nsplit; ++c) {
+    const size_t prow = (static_cast<size_t>(c) * Hkv + g) * rows_pad + row;
+    const float mc = part_ml[prow * 2];
+    if (mc == -INFINITY) continue;
+    const float sc = exp2f(mc - M);
+    lsum += part_ml[prow * 2 + 1] * sc;
+    osum += part_o[prow * HD + dim] * sc;
+  }
+  const int gh = row / T, node = row % T;
+  out[(static_cast<size_t>(node) * Hq + g * G + gh) * HD + dim] =
+      static_cast<uint16_t>(f32_to_bf16_rne(osum / lsum));
+}
+
+// ------------------------------------------------------------------ host --
+
+struct Plan {
+  int G, rows_pad, nqt, nblocks, nsplit, bps;
+  size_t q_bytes, po_bytes, pml_bytes;
+};
+
+int split_bound(int nblocks) {
+  int b = nblocks / kMinBlocksPerSplit;
+  b = b < 1 ? 1 : b;
+  return b > kMaxSplits ? kMaxSplits : b;
+}
+
+Plan make_plan(int T, int Hq, int Hkv, int L) {
+  Plan pl{};
+  pl.G = Hq / Hkv;
+  pl.rows_pad = rows_padded(pl.G, T);
+  pl.nqt = pl.rows_pad / kQTile;
+  pl.nblocks = (L + T + KB - 1) / KB;
+  const int bound = split_bound(pl.nblocks);
+  // aim for about two workgroups per CU
+  int want = (512 + Hkv * pl.nqt - 1) / (Hkv * pl.nqt);
+  want = want < 1 ? 1 : want;
+  pl.nsplit = want < bound ? want : bound;
+  pl.bps = (pl.nblocks + pl.nsplit - 1) / pl.nsplit;
+  pl.nsplit = (pl.nblocks + pl.bps - 1) / pl.bps;
+  pl.q_bytes = static_cast<size_t>(Hkv) * pl.rows_pad * HD * 2;
+  return pl;
+}
+
+size_t workspace_bytes(int T, int Hq, int Hkv, int L) {
+  // sized with the largest split count the plan can choose, so the figure
+  // never shrinks when T or L grows
+  const int G = Hq / Hkv;
+  const int rows_pad = rows_padded(G, T);
+  const int nblocks = (L + T + KB - 1) / KB;
+  const size_t bound = split_bound(nblocks);
+  auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
+  return al(static_cast<size_t>(Hkv) * rows_pad * HD * 2) +
+         al(bound * Hkv * rows_pad * HD * 4) + al(bound * Hkv * rows_pad * 2 * 4);
+}
+
+}  // namespace
+}  // namespace entmtp
+
+using namespace entmtp;
+
+extern "C" size_t entmtp_tree_attn_workspace(int32_t T, int32_t Hq, int32_t Hkv, int32_t d,
+                                             int32_t prefix_len) {
+  if (T < 1 || T > ENTMTP_T_MAX || Hq < 1 || Hkv < 1 || Hq % Hkv || d != HD || prefix_len < 0)
+    return 0;
+  return workspace_bytes(T, Hq, Hkv, prefix_len);
+}
+
+extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const entmtp_bf16* q,
+                                    const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                                    entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t cap,
+                                    int32_t prefix_len, int32_t Hq, int32_t Hkv, int32_t d,
+                                    float scale, float rope_theta, entmtp_bf16* out,
+                                    void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  if (int32_t rc = check_device_bank(bank, topo)) return rc;
+  ENTMTP_CHECK_ARG(q && k_tree && v_tree && k_cache && v_cache && out && workspace, ENTMTP_EINVAL,
+                   "tensor and workspace pointers must be non-NULL");
+  ENTMTP_CHECK_ARG(d == HD, ENTMTP_EINVAL, "head dim %d unsupported (built for %d)", d, HD);
+  ENTMTP_CHECK_ARG(Hq >= 1 && Hkv >= 1, ENTMTP_EINVAL, "Hq = %d, Hkv = %d must be >= 1", Hq, Hkv);
+  ENTMTP_CHECK_ARG(Hq % Hkv == 0, ENTMTP_ERANGE, "Hq = %d is not a multiple of Hkv = %d", Hq, Hkv);
+  ENTMTP_CHECK_ARG(Hq / Hkv * ENTMTP_T_MAX <= 32 * ENTMTP_T_MAX, ENTMTP_ERANGE,
+                   "query group %d too large", Hq / Hkv);
+  ENTMTP_CHECK_ARG(prefix_len >= 0, ENTMTP_EINVAL, "prefix_len = %d < 0", prefix_len);
+  ENTMTP_CHECK_ARG(scale > 0.f && scale < INFINITY, ENTMTP_EINVAL, "scale must be positive");
+  ENTMTP_CHECK_ARG(rope_theta >= 0.f && rope_theta < INFINITY, ENTMTP_EINVAL,
+                   "rope_theta must be >= 0");
+  ENTMTP_CHECK_ARG(aligned16(q) && aligned16(k_tree) && aligned16(v_tree) && aligned16(k_cache) &&
+                       aligned16(v_cache) && aligned16(workspace),
+                   ENTMTP_EINVAL, "tensors and workspace must be 16-byte aligned");
+  const TopoDesc& td = bank->desc[topo];
+  const int T = td.T;
+  ENTMTP_CHECK_ARG(static_cast<int64_t>(prefix_len) + T <= cap, ENTMTP_ERANGE,
+                   "cache capacity %d below prefix_len + T = %d", cap, prefix_len + T);
+  const size_t need = workspace_bytes(T, Hq, Hkv, prefix_len);
+  ENTMTP_CHECK_ARG(ws_bytes >= need, ENTMTP_ENOSPC, "workspace has %zu bytes, needs %zu",
+                   ws_bytes, need);
+
+  const Plan pl = make_plan(T, Hq, Hkv, prefix_len);
+  auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  uint16_t* qrot = reinterpret_cast<uint16_t*>(ws);
+  float* part_o = reinterpret_cast<float*>(ws + al(pl.q_bytes));
+  const size_t po = static_cast<size_t>(pl.nsplit) * Hkv * pl.rows_pad * HD * 4;
+  float* part_ml = reinterpret_cast<float*>(ws + al(pl.q_bytes) + al(po));
+  auto s = static_cast<hipStream_t>(stream);
+
+  hipLaunchKernelGGL(attn_prep_kernel, dim3(T), dim3(256), 0, s, q, k_tree, v_tree, k_cache,
+                     v_cache, qrot, bank_ptr<int>(bank, td.off_depth), T, Hq, Hkv, cap,
+                     prefix_len, static_cast<double>(rope_theta), pl.rows_pad);
+  if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
+
+  AttnArgs a;
+  a.qrot = qrot;
+  a.kc = k_cache;
+  a.vc = v_cache;
+  a.mask = bank_ptr<uint32_t>(bank, td.off_mask);
+  a.part_o = part_o;
+  a.part_ml = part_ml;
+  a.out = out;
+  a.T = T;
+  a.G = pl.G;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  a.L = prefix_len;
+  a.nkeys = prefix_len + T;
+  a.rows_pad = pl.rows_pad;
+  a.nqt = pl.nqt;
+  a.nsplit = pl.nsplit;
+  a.bps = pl.bps;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  const int groups = (Hkv * pl.nsplit + 7) / 8 * 8;
+  hipLaunchKernelGGL(tree_attn_kernel, dim3(groups * pl.nqt), dim3(kAttnThreads), 0, s, a);
+  if (int32_t rc = launch_status("tree_attn launch")) return rc;
+  if (pl.nsplit > 1) {
+    hipLaunchKernelGGL(attn_merge_kernel, dim3(Hkv * pl.G * T), dim3(HD), 0, s, part_o, part_ml,
+                       out, T, pl.G, Hq, Hkv, pl.rows_pad, pl.nsplit);
+    if (int32_t rc = launch_status("tree_attn merge launch")) return rc;
+  }
+  return ENTMTP_OK;
+}

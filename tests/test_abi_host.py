@@ -1,0 +1,136 @@
+"""Host-side checks of the C ABI (no GPU): the library loads and exports every
+symbol the header declares, the bank planner's image equals the oracle's
+buffers bit for bit, validation errors come back as the documented status
+codes, and the ladder policy matches the oracle."""
+import ctypes
+import itertools
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import entmtp_oracle as orc
+from paper_2606_27550_amd import api, synth
+from tests.conftest import ROOT, golden
+from tests.test_oracle_bank import all_parent_arrays
+
+
+def declared_symbols():
+    text = open(os.path.join(ROOT, "include", "entmtp.h")).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(entmtp_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_every_declared_symbol_is_exported():
+    syms = declared_symbols()
+    assert len(syms) >= 14
+    lib = ctypes.CDLL(api.LIB_PATH)
+    for s in syms:
+        assert hasattr(lib, s), s
+    assert set(syms) == set(api._SIGNATURES), "binding and header disagree"
+
+
+def check_entry(bank, k, parent):
+    e = bank.export(k)
+    ref = orc.bank_entry(parent)
+    assert e["T"] == ref["T"] and e["D"] == ref["D"]
+    np.testing.assert_array_equal(e["mask"], ref["mask"])
+    np.testing.assert_array_equal(e["depth"], ref["depth"])
+    np.testing.assert_array_equal(e["path"], ref["path"])
+    np.testing.assert_array_equal(e["retrieve"], ref["retrieve"])
+    np.testing.assert_array_equal(e["leaves"], ref["leaves"])
+    np.testing.assert_array_equal(e["parent"], np.asarray(parent))
+
+
+def test_bank_matches_oracle_on_all_small_trees():
+    trees = [p for T in range(1, 7) for p in all_parent_arrays(T)]
+    bank = api.Bank(trees, device=None)
+    assert api.lib.entmtp_bank_size(bank.handle) == len(trees)
+    for k, p in enumerate(trees):
+        check_entry(bank, k, p)
+
+
+def test_bank_matches_oracle_on_workload_trees():
+    trees = []
+    for wl in synth.WORKLOADS.values():
+        trees += synth.workload_trees(wl)
+    trees += [synth.chain_tree(32), synth.star_tree(256), [-1]]
+    rng = np.random.default_rng(5)
+    trees += [[-1] + [int(rng.integers(0, i)) for i in range(1, 200)]]
+    bank = api.Bank(trees, device=None)
+    for k, p in enumerate(trees):
+        check_entry(bank, k, p)
+    assert bank.T[:5] == [27, 1, 8, 26, 64]
+
+
+@pytest.mark.parametrize("parents,code", [
+    ([[-1, 0, 2]], api.ETREE), ([[0, 0]], api.ETREE), ([[-1, -1]], api.ETREE),
+    ([[-1, 0], [-1, 1]], api.ETREE), ([[-1] + [0] * 256], api.ERANGE),
+    ([[-1] + list(range(32))], api.ERANGE), ([[]], api.ERANGE), ([], api.EINVAL)])
+def test_bank_errors(parents, code):
+    with pytest.raises(api.EntmtpError) as ei:
+        api.Bank(parents, device=None)
+    assert ei.value.code == code
+    assert api.last_error()
+
+
+def test_bank_limits_accepted():
+    api.Bank([[-1] + [0] * 255, [-1] + list(range(31))], device=None)
+
+
+def test_kernel_calls_reject_bad_arguments_without_launching():
+    lib = api.lib
+    host_bank = api.Bank([[-1, 0]], device=None)
+    p = ctypes.c_void_p(16)                      # never dereferenced: validation fails first
+    # host-only bank cannot drive kernels
+    rc = lib.entmtp_accept(host_bank.handle, 0, p, p, None, p, p, p, None, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
+    rc = lib.entmtp_tree_attn(host_bank.handle, 0, p, p, p, p, p, 100, 0, 32, 32, 128, 0.1, 0.0,
+                              p, p, 1 << 20, None)
+    assert rc == api.EINVAL
+    # sizes
+    assert lib.entmtp_verify_logits(p, p, 0, 4096, 32000, p, None) == api.EINVAL
+    assert lib.entmtp_verify_logits(p, p, 27, 4100 + 2, 32000, p, None) == api.EINVAL
+    assert lib.entmtp_verify_logits(None, p, 27, 4096, 32000, p, None) == api.EINVAL
+    assert lib.entmtp_logit_stats(p, 27, 32000, 0.0, p, p, p, None) == api.EINVAL
+    assert lib.entmtp_logit_stats(p, 0, 32000, 1.0, p, p, p, None) == api.EINVAL
+    assert lib.entmtp_kv_compact(p, 5, p, 10, p, p, 1, 0, 32, 100, 12, None) == api.EINVAL
+    assert lib.entmtp_kv_compact(p, 0, p, 10, p, p, 1, 0, 32, 100, 128, None) == api.EINVAL
+    assert lib.entmtp_kv_compact(p, 5, p, -1, p, p, 1, 0, 32, 100, 128, None) == api.EINVAL
+    assert lib.entmtp_kv_compact(p, 5, p, 10, p, p, 2, 5, 32, 100, 128, None) == api.EINVAL
+    # workspace query
+    assert api.tree_attn_workspace(27, 32, 32, 64, 256) == 0
+    assert api.tree_attn_workspace(27, 30, 8, 128, 256) == 0
+    assert api.tree_attn_workspace(0, 32, 32, 128, 256) == 0
+
+
+def test_workspace_is_monotone():
+    prev_t = 0
+    for T in (1, 8, 26, 27, 32, 33, 64, 128, 200, 256):
+        prev_l = 0
+        for L in (0, 31, 32, 256, 2048, 4096, 9216, 16384, 100000):
+            w = api.tree_attn_workspace(T, 32, 8, 128, L)
+            assert w >= prev_l
+            prev_l = w
+        assert prev_l >= prev_t
+        prev_t = prev_l
+
+
+def test_ladder_matches_oracle():
+    g = golden("ladder_trace.json")
+    rung = 0
+    for s, want in zip(g["s"], g["rungs"]):
+        rung = api.ladder_next(rung, g["n_rungs"], s, g["tau_on"], g["tau_off"])
+        assert rung == want
+    rng = np.random.default_rng(0)
+    r1 = r2 = 2
+    for s in rng.random(5000):
+        s = float(np.float32(s))
+        r1 = api.ladder_next(r1, 5, s, 0.8, 0.6)
+        r2 = orc.ladder_next(r2, 5, s, float(np.float32(0.8)), float(np.float32(0.6)))
+        assert r1 == r2
+    with pytest.raises(api.EntmtpError):
+        api.ladder_next(5, 5, 0.5, 0.8, 0.6)
+    with pytest.raises(api.EntmtpError):
+        api.ladder_next(0, 5, 0.5, 0.6, 0.8)
