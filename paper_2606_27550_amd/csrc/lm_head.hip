@@ -22,6 +22,9 @@
 //    multiplied, so each wave keeps two chunks of loads in flight.
 //  * Accumulation is fp32; logits are written as fp32 so that the argmax and
 //    the statistics never see a rounded logit.
+#include <algorithm>
+#include <type_traits>
+
 #include "common.hpp"
 
 namespace entmtp {
@@ -171,6 +174,405 @@ __global__ __launch_bounds__(kLmThreads) void lm_head_kernel(
   }
 }
 
+// ---------------------------------------------------------------------------
+// Streaming variant for hid % 128 == 0: W and X reach LDS through direct
+// global->LDS loads (global_load_lds_dwordx4), which keep several K-stages in
+// flight without holding them in VGPRs.  Each of the eight waves owns one
+// 16-row W tile and a private ring of S stages (16 rows x 128 k = 4 KB each);
+// the X stage (16*NT nodes x 128 k) is shared by the workgroup.  A load
+// instruction covers 4 rows x 256 contiguous bytes; lane p of a row fetches
+// chunk p ^ row, so the MFMA-layout reads (16 rows, same chunk) hit 16
+// different bank groups.  One barrier per stage; S-1 stages stay in flight.
+// ---------------------------------------------------------------------------
+constexpr int kL3Waves = 8;
+constexpr int kL3Threads = 64 * kL3Waves;
+constexpr int kL3Bk = 128;                 // k per stage
+constexpr int kL3RowBytes = kL3Bk * 2;     // 256
+constexpr int kL3TileBytes = 16 * kL3RowBytes;
+
+// s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding; expcnt not waited on): this
+// wave's direct-to-LDS loads older than the last N have landed and its own
+// LDS reads are complete.
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt range");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
+}
+
+// One direct global->LDS copy of 16 bytes per lane: lane l's bytes land at
+// lds + 16 * l (lds is wave-uniform).  Kept in a device-only function: in a
+// kernel's (host+device) lambda this gfx950 builtin would keep the compiler
+// from emitting the kernel's host launch stub.
+__device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
+  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
+}
+
+// Workgroup barrier without a memory-model fence.  __syncthreads() would add
+// a release fence, which waits for every outstanding load (the LDS-DMA
+// stages count as LDS writes) and so drains the pipeline; here the waits are
+// explicit (wait_vmcnt) and the empty asm statements only stop the compiler
+// from moving LDS accesses across the barrier.
+__device__ __forceinline__ void stage_barrier() {
+  asm volatile("" ::: "memory");
+  __builtin_amdgcn_s_barrier();
+  asm volatile("" ::: "memory");
+}
+
+template <int NT>
+struct L3Shape {
+  static constexpr int TP = 16 * NT;                      // node rows per pass
+  static constexpr int RPI = 4;                           // X rows per load instruction
+  static constexpr int NXI = TP / RPI;                    // distinct X instructions per stage
+  static constexpr int XI = NXI >= kL3Waves ? NXI / kL3Waves : 1;   // per wave
+  static constexpr int PER_STAGE = 4 + XI;                // loads per wave per stage
+  static constexpr int XOFF = kL3Waves * kL3TileBytes;    // X stage after the eight W tiles
+  static constexpr int SLOT = XOFF + TP * kL3RowBytes;    // bytes per ring slot
+  static_assert(NXI % kL3Waves == 0 || NXI < kL3Waves, "X split");
+};
+
+template <int NT, int S>
+__global__ __launch_bounds__(kL3Threads) void lm_head_lds_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    int T, int hid, int V, int G) {
+  using Sh = L3Shape<NT>;
+  static_assert(S >= 2 && S <= 4, "2 to 4 stages");
+  // ring slot k lives at ring + k * SLOT; every access uses a compile-time
+  // slot offset, so the compiler can tell the slot being read from the slots
+  // that loads in flight write to
+  __shared__ __attribute__((aligned(16))) uint8_t ring[S * Sh::SLOT];
+
+  const int r0 = slice_begin(blockIdx.x, G, V);
+  const int r1 = slice_begin(blockIdx.x + 1, G, V);
+  if (r0 >= r1) return;  // empty slice (tiny V): the whole workgroup leaves
+  const int j0 = blockIdx.y * Sh::TP;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int tile0 = r0 + 16 * wave;
+  const bool live = tile0 < r1;
+
+  // Per-lane source pointers (row, swizzled chunk).  Every wave issues
+  // exactly PER_STAGE loads per stage -- the explicit vmcnt waits count on
+  // it -- so lanes of rows past the slice or past T read an in-bounds row
+  // this wave loads anyway (an L2 hit) instead of being masked off; the
+  // results of those rows and columns are never stored.
+  const uint16_t* wsrc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = 4 * i + (lane >> 4);
+    const int row = tile0 + rr < r1 ? tile0 + rr : (live ? tile0 : r0);
+    wsrc[i] = W + static_cast<size_t>(row) * hid + 8 * ((lane & 15) ^ rr);
+  }
+  // X: instruction n fills rows 4n..4n+3 of the stage.  With fewer distinct
+  // instructions than waves (NT = 1) the extra waves repeat one: identical
+  // bytes to identical addresses, and every wave keeps the same load count.
+  const uint16_t* xsrc[Sh::XI];
+  int xoff[Sh::XI];
+#pragma unroll
+  for (int q = 0; q < Sh::XI; ++q) {
+    const int n = (wave * Sh::XI + q) % Sh::NXI;
+    const int rr = n * Sh::RPI + (lane >> 4);   // X row written by this lane
+    const int node = j0 + rr < T ? j0 + rr : j0;
+    xsrc[q] = X + static_cast<size_t>(node) * hid + 8 * ((lane & 15) ^ (rr & 15));
+    xoff[q] = Sh::XOFF + n * Sh::RPI * kL3RowBytes;
+  }
+
+  // Workgroups walk K in rotated order (start stage differs per workgroup):
+  // otherwise every CU streams the same column band of its rows at the same
+  // time, and accesses 8 KB apart pile onto the same HBM channels.
+  const int nch = hid / kL3Bk;
+  const int rot = static_cast<int>((static_cast<unsigned>(blockIdx.x) * 7u) % static_cast<unsigned>(nch));
+  auto issue = [&](uint8_t* base, int stage) {
+    int ks = stage + rot;
+    ks = ks >= nch ? ks - nch : ks;
+    const int koff = ks * kL3Bk;
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      lds_dma16(wsrc[i] + koff, base + wave * kL3TileBytes + i * 1024);
+#pragma unroll
+    for (int q = 0; q < Sh::XI; ++q)
+      lds_dma16(xsrc[q] + koff, base + xoff[q]);
+  };
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+
+  auto compute = [&](const uint8_t* base) {
+    const uint8_t* wt = base + wave * kL3TileBytes;
+    const uint8_t* xt = base + Sh::XOFF;
+#pragma unroll
+    for (int s = 0; s < kL3Bk / 32; ++s) {
+      const int ch = 4 * s + lg;
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(wt + lr * kL3RowBytes + ((ch ^ lr) << 4)));
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const bf16x8 b = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            xt + (n * 16 + lr) * kL3RowBytes + ((ch ^ lr) << 4)));
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[n], 0, 0, 0);
+      }
+    }
+  };
+
+  // One pipeline step: wait for stage c, barrier, refill the slot freed by
+  // stage c-1 with stage c+S-1, multiply stage c.  Loads are issued
+  // unconditionally (past the last stage the index is clamped and the last
+  // stage is fetched again), so after stage c exactly S-2 stages are always
+  // in flight and the wait is exact; the compiler sees one load count on
+  // every path and adds no drain of its own.
+  auto step = [&](const uint8_t* cur, uint8_t* refill, int c) {
+    wait_vmcnt<(S - 2) * Sh::PER_STAGE>();
+    stage_barrier();
+    issue(refill, c + S - 1 < nch ? c + S - 1 : nch - 1);
+    if (live && c < nch) compute(cur);
+  };
+  constexpr int SL = Sh::SLOT;
+  issue(ring, 0);
+  if constexpr (S > 2) issue(ring + SL, 1 < nch ? 1 : nch - 1);
+  if constexpr (S > 3) issue(ring + 2 * SL, 2 < nch ? 2 : nch - 1);
+  for (int c = 0; c < nch; c += S) {
+    step(ring, ring + ((S - 1) % S) * SL, c);
+    step(ring + SL, ring + (S % S) * SL, c + 1);
+    if constexpr (S > 2) step(ring + 2 * SL, ring + ((S + 1) % S) * SL, c + 2);
+    if constexpr (S > 3) step(ring + 3 * SL, ring + ((S + 2) % S) * SL, c + 3);
+  }
+  wait_vmcnt<0>();   // no load may land in LDS after the workgroup is gone
+
+  if (!live) return;
+  const bool vec_ok = (V & 3) == 0;
+  const int v = tile0 + 4 * lg;
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int node = j0 + n * 16 + lr;
+    if (node >= T) continue;
+    float* dst = logits + static_cast<size_t>(node) * V + v;
+    if (vec_ok && v + 3 < r1) {
+      *reinterpret_cast<f32x4*>(dst) = acc[n];
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (v + r < r1) dst[r] = acc[n][r];
+    }
+  }
+}
+
+// ---------------------------------------------------------------------------
+// Hybrid streaming variant (hid % 128 == 0): W through VGPRs, X through LDS.
+// W is the byte stream: each wave keeps S K-stages of its 16-row tile in
+// flight as plain VGPR loads (4 rows x 256 contiguous bytes per
+// instruction -- the fastest read path measured on MI355X) and transposes
+// each stage to MFMA operand layout through a private 4 KB LDS tile (lane p
+// of row r stores chunk p at slot p ^ r: conflict-free both ways).  X, the
+// same for every wave, arrives by direct global->LDS copies into a ring of S
+// shared stages.  A stage's X copy is issued just before the stage's W loads;
+// loads complete in order, so the wait the compiler places for the W
+// registers also covers the X copy, and one barrier per stage publishes
+// every wave's share.  All loads are issued unconditionally (addresses are
+// clamped) so that every path carries the same load count.
+// ---------------------------------------------------------------------------
+constexpr int kHybWaves = 4;                        // 64 rows per workgroup slice
+constexpr int kHybThreads = 64 * kHybWaves;
+
+// X stage split for the hybrid kernel (four waves share the copies)
+template <int NT>
+struct HybShape {
+  static constexpr int TP = 16 * NT;
+  static constexpr int RPI = 4;
+  static constexpr int NXI = TP / RPI;
+  static constexpr int XI = NXI >= kHybWaves ? NXI / kHybWaves : 1;
+  static_assert(NXI % kHybWaves == 0, "X split");
+};
+
+template <int NT, int S, int NCH>
+__global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    int T, int hid, int V, int G) {
+  using Sh = HybShape<NT>;
+  // precondition (host dispatch): hid is a multiple of S * 128, and equals
+  // NCH * 128 when NCH > 0 (the K loop is then unrolled completely: no
+  // loop-carried stage registers, so the compiler's load bookkeeping stays
+  // exact and it never drains the pipeline)
+  constexpr int XSTAGE = Sh::TP * kL3RowBytes;            // bytes of one X stage
+  static_assert(S >= 2 && S <= 4, "two to four X ring slots");
+  // one LDS object per X ring slot, so that the compiler can tell the slot
+  // being read from the slots the copies in flight write to
+  __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot2[S > 2 ? XSTAGE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot3[S > 3 ? XSTAGE : 16];
+  uint8_t* const xring[4] = {xslot0, xslot1, xslot2, xslot3};
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
+
+  const int r0 = slice_begin(blockIdx.x, G, V);
+  const int r1 = slice_begin(blockIdx.x + 1, G, V);
+  if (r0 >= r1) return;  // empty slice (tiny V): the whole workgroup leaves
+  const int j0 = blockIdx.y * Sh::TP;
+  const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+  const int lr = lane & 15, lg = lane >> 4;
+  const int tile0 = r0 + 16 * wave;
+  const bool live = tile0 < r1;
+  const int nch = NCH > 0 ? NCH : hid / kL3Bk;
+  // workgroups walk K in rotated order so that CUs do not all stream the
+  // same column band at once
+  const int rot = static_cast<int>((static_cast<unsigned>(blockIdx.x) * 7u) % static_cast<unsigned>(nch));
+
+  // W: instruction i, lane l -> row 4i + l/16, chunk l%16 (rows past the
+  // slice read an in-bounds row of this slice; their outputs are not stored)
+  const uint16_t* wsrc[4];
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    const int rr = 4 * i + (lane >> 4);
+    const int row = tile0 + rr < r1 ? tile0 + rr : (live ? tile0 : r0);
+    wsrc[i] = W + static_cast<size_t>(row) * hid + 8 * (lane & 15);
+  }
+  // X: copy instruction n fills stage rows 4n..4n+3, lane p of row r fetching
+  // chunk p ^ r; with fewer distinct instructions than waves (NT = 1) extra
+  // waves repeat one (identical bytes to identical addresses)
+  const uint16_t* xsrc[Sh::XI];
+  int xoff[Sh::XI];
+#pragma unroll
+  for (int q = 0; q < Sh::XI; ++q) {
+    const int n = (wave * Sh::XI + q) % Sh::NXI;
+    const int rr = n * Sh::RPI + (lane >> 4);
+    const int node = j0 + rr < T ? j0 + rr : j0;
+    xsrc[q] = X + static_cast<size_t>(node) * hid + 8 * ((lane & 15) ^ (rr & 15));
+    xoff[q] = n * Sh::RPI * kL3RowBytes;
+  }
+
+  u32x4 wbuf[S][4];
+  // issue stage `stage` (clamped by the caller) into ring slot k
+  auto load = [&](u32x4 (&w)[4], uint8_t* xslot, int stage) {
+    int ks = stage + rot;
+    ks = ks >= nch ? ks - nch : ks;
+    const int koff = ks * kL3Bk;
+#pragma unroll
+    for (int q = 0; q < Sh::XI; ++q) lds_dma16(xsrc[q] + koff, xslot + xoff[q]);
+#pragma unroll
+    for (int i = 0; i < 4; ++i)
+      w[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wsrc[i] + koff));
+  };
+
+  f32x4 acc[NT];
+#pragma unroll
+  for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint8_t* tp = tpose + wave * kL3TileBytes;
+  auto compute = [&](const u32x4 (&w)[4], const uint8_t* xs) {
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int r = 4 * i + lg;
+      *reinterpret_cast<u32x4*>(tp + r * kL3RowBytes + ((lr ^ r) << 4)) = w[i];
+    }
+    asm volatile("" ::: "memory");   // the tile's stores precede its reads
+#pragma unroll
+    for (int s = 0; s < kL3Bk / 32; ++s) {
+      const int ch = 4 * s + lg;
+      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(tp + lr * kL3RowBytes + ((ch ^ lr) << 4)));
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const bf16x8 b = as_bf16x8(*reinterpret_cast<const u32x4*>(
+            xs + (n * 16 + lr) * kL3RowBytes + ((ch ^ lr) << 4)));
+        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[n], 0, 0, 0);
+      }
+    }
+    asm volatile("" ::: "memory");   // and the next stage's stores follow them
+  };
+
+  load(wbuf[0], xring[0], 0);
+  if constexpr (S > 2) load(wbuf[1], xring[1], 1 < nch ? 1 : nch - 1);
+  if constexpr (S > 3) load(wbuf[2], xring[2], 2 < nch ? 2 : nch - 1);
+#pragma unroll
+  for (int c = 0; c < (NCH > 0 ? NCH : nch); c += S) {
+#pragma unroll
+    for (int k = 0; k < S; ++k) {
+      const int cc = c + k;
+      // this wave's loads of stage cc (its X share first, then its W
+      // registers) are done once only the S-2 later stages remain in flight;
+      // its LDS reads of stage cc-1 are done too (lgkmcnt(0))
+      wait_vmcnt<(S - 2) * (Sh::XI + 4)>();
+      stage_barrier();                       // every wave's X share of stage cc has landed
+      const int nx = cc + S - 1 < nch ? cc + S - 1 : nch - 1;
+      load(wbuf[(k + S - 1) % S], xring[(k + S - 1) % S], nx);
+      // unconditional (nch % S == 0, and a wave without rows multiplies
+      // in-bounds data it never stores): one straight-line path per step
+      // keeps the compiler's load bookkeeping exact
+      compute(wbuf[k], xring[k]);
+    }
+  }
+  wait_vmcnt<0>();   // no copy may land in LDS after the workgroup is gone
+
+  if (!live) return;
+  const bool vec_ok = (V & 3) == 0;
+  const int v = tile0 + 4 * lg;
+#pragma unroll
+  for (int n = 0; n < NT; ++n) {
+    const int node = j0 + n * 16 + lr;
+    if (node >= T) continue;
+    float* dst = logits + static_cast<size_t>(node) * V + v;
+    if (vec_ok && v + 3 < r1) {
+      *reinterpret_cast<f32x4*>(dst) = acc[n];
+    } else {
+#pragma unroll
+      for (int r = 0; r < 4; ++r)
+        if (v + r < r1) dst[r] = acc[n][r];
+    }
+  }
+}
+
+// Largest vocabulary slice slice_begin() produces for G workgroups (host copy
+// of the same arithmetic).
+int max_slice(int V, int G) {
+  auto begin = [&](int b) {
+    return b >= G ? V : static_cast<int>((static_cast<long long>(V) * b / G) & ~3ll);
+  };
+  int m = 0;
+  for (int b = 0; b < G; ++b) m = std::max(m, begin(b + 1) - begin(b));
+  return m;
+}
+
+// Compute units of the current device (queried once per device).
+int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
+template <int NT, int S, int NCH>
+int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
+                      hipStream_t s) {
+  // Slices of at most 64 rows, and a grid that is a whole multiple of the CU
+  // count: every CU then streams the same number of bytes (a partial extra
+  // round of workgroups on a few CUs costs ~20% at 7B shapes).
+  constexpr int rows = 16 * kHybWaves;
+  const int cus = device_cus();
+  const int max_g = (V + 3) / 4;
+  int G = cus;
+  while (G < max_g && max_slice(V, G) > rows) G += cus;
+  G = G < max_g ? G : max_g;
+  const int passes = (T + NT * 16 - 1) / (NT * 16);
+  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH>), dim3(G, passes), dim3(kHybThreads), 0, s, X,
+                     W, logits, T, hid, V, G);
+  return launch_status("verify_logits launch");
+}
+
+template <int NT, int S>
+int32_t launch_lm_lds(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
+                      hipStream_t s) {
+  constexpr int rows = 16 * kL3Waves;   // 128 rows per slice at most
+  const int want = (V + rows - 5) / (rows - 4);
+  int G = want > 256 ? want : 256;
+  const int max_g = (V + 3) / 4;
+  G = G < max_g ? G : max_g;
+  const int passes = (T + NT * 16 - 1) / (NT * 16);
+  hipLaunchKernelGGL((lm_head_lds_kernel<NT, S>), dim3(G, passes), dim3(kL3Threads), 0, s, X, W,
+                     logits, T, hid, V, G);
+  return launch_status("verify_logits launch");
+}
+
 template <int NT, int BK>
 int32_t launch_lm(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
                   hipStream_t s) {
@@ -201,6 +603,30 @@ extern "C" int32_t entmtp_verify_logits(const entmtp_bf16* hidden, const entmtp_
   ENTMTP_CHECK_ARG(aligned16(hidden) && aligned16(w_lm) && aligned16(logits), ENTMTP_EINVAL,
                    "hidden, w_lm and logits must be 16-byte aligned");
   auto s = static_cast<hipStream_t>(stream);
+  if (hid % kL3Bk == 0) {
+    if (hid == 4096) {              // the 7B hidden size: K loop fully unrolled
+      if (T <= 16) return launch_lm_hyb<1, 4, 32>(hidden, w_lm, logits, T, hid, V, s);
+      if (T <= 32) return launch_lm_hyb<2, 4, 32>(hidden, w_lm, logits, T, hid, V, s);
+      if (T <= 64) return launch_lm_hyb<4, 4, 32>(hidden, w_lm, logits, T, hid, V, s);
+      return launch_lm_hyb<8, 2, 32>(hidden, w_lm, logits, T, hid, V, s);
+    }
+    if (hid == 5120) {              // the 13B hidden size
+      if (T <= 16) return launch_lm_hyb<1, 4, 40>(hidden, w_lm, logits, T, hid, V, s);
+      if (T <= 32) return launch_lm_hyb<2, 4, 40>(hidden, w_lm, logits, T, hid, V, s);
+      if (T <= 64) return launch_lm_hyb<4, 4, 40>(hidden, w_lm, logits, T, hid, V, s);
+      return launch_lm_hyb<8, 2, 40>(hidden, w_lm, logits, T, hid, V, s);
+    }
+    if (hid % (4 * kL3Bk) == 0) {   // the hybrid kernel needs a whole number of 4-stage rounds
+      if (T <= 16) return launch_lm_hyb<1, 4, 0>(hidden, w_lm, logits, T, hid, V, s);
+      if (T <= 32) return launch_lm_hyb<2, 4, 0>(hidden, w_lm, logits, T, hid, V, s);
+      if (T <= 64) return launch_lm_hyb<4, 4, 0>(hidden, w_lm, logits, T, hid, V, s);
+      return launch_lm_hyb<8, 2, 0>(hidden, w_lm, logits, T, hid, V, s);
+    }
+    if (T <= 16) return launch_lm_lds<1, 4>(hidden, w_lm, logits, T, hid, V, s);
+    if (T <= 32) return launch_lm_lds<2, 4>(hidden, w_lm, logits, T, hid, V, s);
+    if (T <= 64) return launch_lm_lds<4, 3>(hidden, w_lm, logits, T, hid, V, s);
+    return launch_lm_lds<8, 2>(hidden, w_lm, logits, T, hid, V, s);
+  }
   if (T <= 16) return launch_lm<1, 256>(hidden, w_lm, logits, T, hid, V, s);
   if (T <= 32) return launch_lm<2, 256>(hidden, w_lm, logits, T, hid, V, s);
   if (T <= 64) return launch_lm<4, 128>(hidden, w_lm, logits, T, hid, V, s);
