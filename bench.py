@@ -48,7 +48,24 @@ def parse():
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--fixed-topo", type=int, default=-1,
                     help="disable the scheduler and use this bank entry every step")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="only run plain 256 MiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
+
+
+def calibrate_copy():
+    """Plain device-to-device copies of a known size: the reference that scales
+    the FETCH_SIZE / WRITE_SIZE counters to bytes."""
+    import torch
+    n = 256 << 20
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    b = torch.empty_like(a)
+    a.fill_(1)
+    for _ in range(5):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibration": "device copy", "bytes_read_per_copy": n,
+                      "bytes_written_per_copy": n, "copies": 5}))
 
 
 def log(*a):
@@ -67,6 +84,9 @@ def main():
 
     if not torch.cuda.is_available():
         sys.exit("bench.py needs a GPU")
+    if args.calibrate_copy:
+        calibrate_copy()
+        return
     dev = torch.device("cuda:0")
     torch.cuda.set_device(dev)
     lib = api.lib
@@ -242,6 +262,8 @@ def main():
     if not args.no_cpu_baseline:
         cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta)
 
+    traffic = lm_head_traffic([T for T, *_ in trace])
+
     line = {
         "metric": METRIC, "value": round(steps_per_s, 2), "unit": "steps/s", "n_gpus": 1,
         "steps": K, "warmup": args.warmup, "ms_per_step": round(elapsed / K * 1e3, 5),
@@ -258,11 +280,37 @@ def main():
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
         "roofline": {"kernel": "lm_head_kernel (entmtp_verify_logits)", "bound": "hbm",
                      "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": round(lm_bytes / K),
                      "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2)},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
+
+
+def lm_head_traffic(Ts):
+    """Measured HBM bytes per LM-head launch (FETCH_SIZE + WRITE_SIZE, scaled by
+    a device-copy calibration) for this step mix, from the committed counter
+    record -- or None when the kernel source changed since it was taken."""
+    from paper_2606_27550_amd import rocprof_summary
+    path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "lm_head_traffic.json")
+    try:
+        rec = json.load(open(path))
+    except (OSError, ValueError):
+        return None
+    if rec.get("lm_head_source_sha256") != rocprof_summary.lm_head_source_hash():
+        return None
+    per = {}
+    for name, v in rec["per_variant"].items():
+        nt = int(name.split("<")[1].split(",")[0])
+        per[nt] = v["fetch_bytes"] + v["write_bytes"]
+    tot = 0.0
+    for T in Ts:
+        nt = 1 if T <= 16 else 2 if T <= 32 else 4 if T <= 64 else 8
+        if nt not in per:
+            return None
+        tot += per[nt]
+    return round(tot / len(Ts))
 
 
 def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta):

@@ -1,0 +1,97 @@
+"""Summaries of rocprofv3 output for the profiles/ folder.
+
+  python -m paper_2606_27550_amd.rocprof_summary stats <kernel_stats.csv> <out.md> "<command>"
+  python -m paper_2606_27550_amd.rocprof_summary traffic <fetch.csv> <write.csv> \
+      <copy_fetch.csv> <copy_write.csv> <copy_bytes> <out.md> <out.json> "<commands>"
+
+``stats`` turns a --kernel-trace --stats CSV into a markdown table.
+``traffic`` turns FETCH_SIZE / WRITE_SIZE counter collections (KiB per
+dispatch) into HBM bytes per launch, scaled by what the same counters read for
+a plain device copy of known size, and records them together with the hash of
+the LM-head kernel source so that a later change to the kernel invalidates them.
+"""
+from __future__ import annotations
+
+import collections
+import csv
+import hashlib
+import json
+import os
+import sys
+
+PKG = os.path.dirname(os.path.abspath(__file__))
+LM_HEAD_SRC = os.path.join(PKG, "csrc", "lm_head.hip")
+
+
+def lm_head_source_hash() -> str:
+    with open(LM_HEAD_SRC, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest()
+
+
+def short(name: str) -> str:
+    name = name.replace("entmtp::(anonymous namespace)::", "")
+    cut = name.find("(")
+    return name[:cut] if cut > 0 else name
+
+
+def stats(csv_path: str, out_md: str, command: str) -> None:
+    rows = list(csv.DictReader(open(csv_path)))
+    lines = [f"# Kernel time: `{command}`", "",
+             "rocprofv3 --kernel-trace --stats summary (per-dispatch durations).", "",
+             "| kernel | calls | avg us | min us | max us | % of GPU time |",
+             "|---|---:|---:|---:|---:|---:|"]
+    for r in rows:
+        lines.append(f"| `{short(r['Name'])}` | {r['Calls']} | {float(r['AverageNs']) / 1e3:.2f} | "
+                     f"{float(r['MinNs']) / 1e3:.2f} | {float(r['MaxNs']) / 1e3:.2f} | "
+                     f"{float(r['Percentage']):.2f} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
+def _counter(csv_path: str):
+    acc = collections.defaultdict(list)
+    for r in csv.DictReader(open(csv_path)):
+        acc[short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
+
+
+def traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes, out_md, out_json,
+            commands) -> None:
+    fetch, n_fetch = _counter(fetch_csv)
+    write, _ = _counter(write_csv)
+    cf, _ = _counter(copy_fetch_csv)
+    cw, _ = _counter(copy_write_csv)
+    copy_kib = float(copy_bytes) / 1024.0
+    ref_f = cf.get("__amd_rocclr_copyBuffer") or max(cf.values())
+    ref_w = cw.get("__amd_rocclr_copyBuffer") or max(cw.values())
+    f_scale = copy_kib / ref_f
+    w_scale = copy_kib / ref_w
+    lines = [f"# HBM traffic per launch (FETCH_SIZE, WRITE_SIZE)", "",
+             "Commands:", ""] + [f"    {c}" for c in commands.split(";")] + [
+             "", f"Calibration: a {copy_bytes} B device copy reads FETCH_SIZE = {ref_f:.1f} KiB and "
+             f"WRITE_SIZE = {ref_w:.1f} KiB per dispatch, so fetch counts are scaled by "
+             f"{f_scale:.4f} and write counts by {w_scale:.4f}.", "",
+             "| kernel | dispatches | fetch MB | write MB | total MB |", "|---|---:|---:|---:|---:|"]
+    per_kernel = {}
+    for k in sorted(fetch, key=lambda k: -fetch[k]):
+        fb = fetch[k] * f_scale * 1024.0
+        wb = write.get(k, 0.0) * w_scale * 1024.0
+        per_kernel[k] = {"fetch_bytes": fb, "write_bytes": wb}
+        lines.append(f"| `{k}` | {n_fetch[k]} | {fb / 1e6:.2f} | {wb / 1e6:.2f} | {(fb + wb) / 1e6:.2f} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+    lm = {k: v for k, v in per_kernel.items() if "lm_head" in k}
+    rec = {"lm_head_source_sha256": lm_head_source_hash(), "fetch_scale": f_scale,
+           "write_scale": w_scale, "per_variant": lm, "commands": commands}
+    with open(out_json, "w") as f:
+        json.dump(rec, f, indent=1)
+        f.write("\n")
+
+
+if __name__ == "__main__":
+    if sys.argv[1] == "stats":
+        stats(sys.argv[2], sys.argv[3], sys.argv[4])
+    elif sys.argv[1] == "traffic":
+        traffic(*sys.argv[2:10])
+    else:
+        sys.exit(__doc__)
