@@ -5,10 +5,12 @@ A step is one pass of the whole verification hot path at batch 1:
   host: pick the tree for this step with the hysteretic ladder (tau_on 0.8,
         tau_off 0.6) from the previous step's top-1 probability at the
         deepest accepted node;
-  GPU:  tree attention (tree K/V appended to the cache) -> LM-head logits ->
-        softmax statistics -> greedy acceptance -> KV compaction;
-  host: read (accept length, feature) back -- the step's one sync -- and grow
-        the prefix by accept_len + 1.
+  GPU:  tree attention (tree K/V appended to the cache) -> LM-head logits with
+        fused softmax statistics -> greedy acceptance -> KV compaction, all
+        enqueued by one entmtp_step_launch;
+  host: poll the pinned record acceptance publishes (accept length, feature)
+        -- the step's one device-to-host read -- and grow the prefix by
+        accept_len + 1 while the compaction finishes.
 
 Default workload: Vicuna-7B shapes (32 x 128 heads, hidden 4096, vocab
 32000), a 5-tree bank with {1, 8, 26, 64, 128} nodes, prefix 2048 growing
@@ -139,78 +141,52 @@ def main():
                      "host": (a_in.q, a_in.k_tree, a_in.v_tree, x)})
     log(f"staged inputs in {time.time() - t0:.1f}s")
 
-    # buffers
-    logits = torch.empty((Tmax, V), dtype=torch.float32, device=dev)
-    ent = torch.empty(Tmax, dtype=torch.float32, device=dev)
-    top1 = torch.empty(Tmax, dtype=torch.float32, device=dev)
-    amax = torch.empty(Tmax, dtype=torch.int32, device=dev)
-    res = torch.zeros(4 + Dmax + 1, dtype=torch.int32, device=dev)   # a, bonus, s(bits), pad, path
-    res_host = torch.zeros(4, dtype=torch.int32).pin_memory()
+    # one step context per LM-head weight copy; all share the caches
+    st = [api.Step(bank, k_cache, v_cache, w, Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax,
+                   scale=scale, rope_theta=theta) for w in W]
     out = torch.empty((Tmax, Hq, d), dtype=bf, device=dev)
-    ws_bytes = api.tree_attn_workspace(Tmax, Hq, Hkv, d, cap - Tmax)
-    ws = torch.empty(ws_bytes, dtype=torch.uint8, device=dev)
 
     # draft tokens: the target's greedy token at the parent with prob p_acc,
     # computed with the library itself on each pool entry (input synthesis)
+    lws = torch.empty(api.verify_logits_stats_workspace(Tmax, hid, V), dtype=torch.uint8, device=dev)
     for e in pool:
-        lib.entmtp_verify_logits(ctypes.c_void_p(e["x"].data_ptr()), ctypes.c_void_p(W[0].data_ptr()),
-                                 Tmax, hid, V, ctypes.c_void_p(logits.data_ptr()),
-                                 ctypes.c_void_p(torch.cuda.current_stream().cuda_stream))
-        api.logit_stats(logits, 1.0, None, None, amax)
-        am = amax.cpu().numpy()
+        api.verify_logits_stats(e["x"], W[0], st[0].logits, 1.0, None, None, st[0].argmax, lws)
+        am = st[0].argmax.cpu().numpy()
         e["tok"] = [synth.draft_tokens(trees[k], am, e["u"], e["r"], wl.p_acc) for k in range(n_topo)]
         e["tok_dev"] = [torch.from_numpy(t).to(dev) for t in e["tok"]]
+    del lws
     torch.cuda.synchronize()
 
     # ---------------------------------------------------------- raw step
     P_ = ctypes.c_void_p
-    stream = P_(torch.cuda.current_stream().cuda_stream)
-    handle = bank.handle
-    kc_p, vc_p = P_(k_cache.data_ptr()), P_(v_cache.data_ptr())
-    out_p, ws_p = P_(out.data_ptr()), P_(ws.data_ptr())
-    lg_p, ent_p, top_p, am_p = (P_(logits.data_ptr()), P_(ent.data_ptr()), P_(top1.data_ptr()),
-                                P_(amax.data_ptr()))
-    res_p = res.data_ptr()
-    a_p, bonus_p, s_p, path_p = P_(res_p), P_(res_p + 4), P_(res_p + 8), P_(res_p + 16)
-    W_p = [P_(w.data_ptr()) for w in W]
+    handles = [s_.handle for s_ in st]
+    out_p = P_(out.data_ptr())
     pool_p = [{"q": P_(e["q"].data_ptr()), "kt": P_(e["kt"].data_ptr()), "vt": P_(e["vt"].data_ptr()),
                "x": P_(e["x"].data_ptr()), "tok": [P_(t.data_ptr()) for t in e["tok_dev"]]}
               for e in pool]
     Ts = bank.T
+    a_c, b_c, s_c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
+    a_r, b_r, s_r = ctypes.byref(a_c), ctypes.byref(b_c), ctypes.byref(s_c)
 
     def chk(rc):
         if rc:
             raise api.EntmtpError(rc, api.last_error())
 
     state = {"L": L0, "rung": 0 if args.fixed_topo < 0 else args.fixed_topo, "s": 0.0}
-    ev = None
 
-    def step(t, timed_events=None):
+    def step(t, ev=(None, None)):
         L = state["L"] if grows else L0
         topo = state["rung"]
-        T = Ts[topo]
         e = pool_p[t % P]
-        chk(lib.entmtp_tree_attn(handle, topo, e["q"], e["kt"], e["vt"], kc_p, vc_p, cap, L, Hq, Hkv,
-                                 d, scale, theta, out_p, ws_p, ws_bytes, stream))
-        if timed_events is not None:
-            timed_events[0].record()
-        chk(lib.entmtp_verify_logits(e["x"], W_p[t % len(W_p)], T, hid, V, lg_p, stream))
-        if timed_events is not None:
-            timed_events[1].record()
-        chk(lib.entmtp_logit_stats(lg_p, T, V, 1.0, ent_p, top_p, am_p, stream))
-        chk(lib.entmtp_accept(handle, topo, e["tok"][topo], am_p, top_p, a_p, path_p, bonus_p, s_p,
-                              stream))
-        chk(lib.entmtp_kv_compact(path_p, Dmax + 1, a_p, L, kc_p, vc_p, 1, Hkv * cap * d, Hkv, cap,
-                                  d, stream))
-        res_host.copy_(res[:4], non_blocking=True)
-        torch.cuda.current_stream().synchronize()
-        a = int(res_host[0])
-        s = float(np.frombuffer(np.int32(res_host[2]).tobytes(), np.float32)[0])
+        chk(lib.entmtp_step_launch(handles[t % len(handles)], topo, L, e["q"], e["kt"], e["vt"],
+                                   out_p, e["x"], e["tok"][topo], ev[0], ev[1]))
+        chk(lib.entmtp_step_wait(handles[t % len(handles)], a_r, b_r, s_r, 30.0))
+        a, s = a_c.value, s_c.value
         if grows:
             state["L"] = L + a + 1
         if args.fixed_topo < 0:
-            state["rung"] = lib.entmtp_ladder_next(state["rung"], n_topo, s, 0.8, 0.6)
-        return T, L, a, s, topo
+            state["rung"] = lib.entmtp_ladder_next(topo, n_topo, s, 0.8, 0.6)
+        return Ts[topo], L, a, s, topo
 
     # ---------------------------------------------------------- warmup
     for t in range(args.warmup):
@@ -221,15 +197,23 @@ def main():
     K = args.steps
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
               for _ in range(K)]
+    for a_, b_ in events:          # torch creates an event's handle on its first record
+        a_.record()
+        b_.record()
+    ev_p = [(P_(a_.cuda_event), P_(b_.cuda_event)) for a_, b_ in events]
     trace = []
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for t in range(K):
-        trace.append(step(args.warmup + t, events[t]))
+        trace.append(step(args.warmup + t, ev_p[t]))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
 
     lm_ms = [a.elapsed_time(b) for a, b in events]
+    by_T = {}
+    for (T, *_), ms in zip(trace, lm_ms):
+        by_T.setdefault(T, []).append(ms)
+    lm_us_by_T = {str(T): round(float(np.mean(v)) * 1e3, 2) for T, v in sorted(by_T.items())}
     # algorithmic bytes (what the method must move; fp32 logits excluded)
     def step_bytes(T, L, a):
         w = V * hid * 2
@@ -255,7 +239,8 @@ def main():
     switches = sum(1 for i in range(1, len(trace)) if trace[i][4] != trace[i - 1][4])
     log(f"{K} steps in {elapsed:.3f}s: {us:.1f} us/step, {hbm:.0f} GB/s algorithmic; "
         f"LM head {np.mean(lm_ms) * 1e3:.1f} us avg, {lm_gbps:.0f} GB/s; T histogram {Tcount}; "
-        f"mean tokens/step {accept_mean:.3f}; switches {switches}; final L {state['L']}")
+        f"mean tokens/step {accept_mean:.3f}; switches {switches}; final L {state['L']}; "
+        f"LM head us by T {lm_us_by_T}")
 
     # ---------------------------------------------------------- cpu baseline
     cpu = None
@@ -278,11 +263,11 @@ def main():
                    "T_histogram": {str(k): v for k, v in sorted(Tcount.items())},
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
-        "roofline": {"kernel": "lm_head_kernel (entmtp_verify_logits)", "bound": "hbm",
+        "roofline": {"kernel": "lm_head_hyb_kernel (entmtp_verify_logits_partials)", "bound": "hbm",
                      "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": round(lm_bytes / K),
-                     "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2)},
+                     "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)

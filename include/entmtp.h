@@ -47,6 +47,7 @@ extern "C" {
 #define ENTMTP_ERANGE  (-3)  /* T > ENTMTP_T_MAX, depth > ENTMTP_D_MAX, cap < L+T, Hq % Hkv */
 #define ENTMTP_ENOSPC  (-4)  /* arena or workspace smaller than required */
 #define ENTMTP_EHIP    (-5)  /* HIP runtime or launch error (message kept) */
+#define ENTMTP_ETIMEDOUT (-6)  /* entmtp_step_wait: no result within the time limit */
 
 #define ENTMTP_T_MAX      256  /* nodes per tree, root included */
 #define ENTMTP_D_MAX      31   /* deepest node (root = depth 0) */
@@ -179,6 +180,42 @@ int32_t entmtp_verify_logits(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
                              int32_t T, int32_t hid, int32_t V, float* logits,
                              void* stream);
 
+/*
+ * Fused form of entmtp_verify_logits followed by entmtp_logit_stats: the
+ * LM-head kernel also reduces every workgroup's vocabulary slice to per-node
+ * softmax partials (largest raw logit with its lowest index, and the sums
+ * sum e^(y-m), sum (y-m) e^(y-m) for y = inv_temp * z), which a small kernel
+ * then combines per node, so the logits are not read back.  Outputs and their
+ * meaning are those of the two separate calls (logits [T][V] fp32 is still
+ * written; entropy / top1p / argmax may each be NULL).
+ *   workspace   device scratch of at least
+ *               entmtp_verify_logits_stats_workspace(T, hid, V) bytes, 16-byte
+ *               aligned (partials, overwritten by every call).
+ * Errors: EINVAL, ENOSPC (workspace), EHIP.
+ */
+size_t entmtp_verify_logits_stats_workspace(int32_t T, int32_t hid, int32_t V);
+int32_t entmtp_verify_logits_stats(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, int32_t T,
+                                   int32_t hid, int32_t V, float inv_temp, float* logits,
+                                   float* entropy, float* top1p, int32_t* argmax,
+                                   void* workspace, size_t workspace_bytes, void* stream);
+
+/*
+ * The two halves of entmtp_verify_logits_stats, for callers that time or
+ * schedule them separately.  Available when hid is a multiple of 512 (the
+ * streaming LM-head kernel); entmtp_stats_partials_bytes returns 0 otherwise
+ * and entmtp_verify_logits_partials then fails with EINVAL.
+ *   partials   device buffer of entmtp_stats_partials_bytes(T, hid, V) bytes,
+ *              16-byte aligned; written by the first call, read by the second
+ *              (same device, same V).
+ */
+size_t entmtp_stats_partials_bytes(int32_t T, int32_t hid, int32_t V);
+int32_t entmtp_verify_logits_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                      int32_t T, int32_t hid, int32_t V, float inv_temp,
+                                      float* logits, void* partials, size_t partials_bytes,
+                                      void* stream);
+int32_t entmtp_stats_finalize(const void* partials, int32_t T, int32_t V, float inv_temp,
+                              float* entropy, float* top1p, int32_t* argmax, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Per-node softmax statistics (§4: the scheduler reads the top-1            */
 /* probability p0 at the verifier's last position; §3 / App. A: entropy).    */
@@ -254,6 +291,105 @@ int32_t entmtp_kv_compact(const int32_t* path, int32_t path_capacity,
  * [0, n_rungs).  Returns the next rung (or a negative status). */
 int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
                            float tau_off);
+
+/* ------------------------------------------------------------------------ */
+/* One verification step, end to end (§4, the decode loop with the tree      */
+/* scheduler and its "Cost" paragraph: verify the chosen tree, accept, update */
+/* the cache, read one scalar back to pick the next tree).                    */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Fixed part of a decode loop, validated once by entmtp_step_create.  All
+ * pointers are device pointers owned by the caller and must stay valid while
+ * the step object is used.
+ *   n_layers, Hq, Hkv, d, scale, rope_theta   as for entmtp_tree_attn; layer l
+ *              of the cache starts at k_cache + l * cache_layer_stride (same for
+ *              v_cache), each layer [Hkv][cap][d] bf16
+ *   tree_rows  rows reserved per layer for the per-step tree inputs: q of
+ *              layer l starts at q + l * tree_rows * Hq * d, k_tree / v_tree at
+ *              + l * tree_rows * Hkv * d, out at + l * tree_rows * Hq * d;
+ *              at least the largest T in the bank
+ *   w_lm, hid, V, inv_temp   the LM head and the statistics temperature as for
+ *              entmtp_verify_logits_stats (hid a multiple of 512)
+ *   logits [tree_rows][V] fp32; entropy, top1p [tree_rows] fp32;
+ *   argmax [tree_rows] int32   outputs of the LM head and statistics
+ *   accept_len [1], bonus [1] int32, best_top1p [1] fp32, path [path_capacity]
+ *              int32 (path_capacity >= 1 + the largest depth in the bank)
+ *              outputs of acceptance, as for entmtp_accept
+ *   workspace  scratch of entmtp_step_workspace() bytes, 256-byte aligned
+ *   stream     the HIP stream every launch goes to (NULL: the null stream)
+ */
+typedef struct entmtp_step_config {
+  int32_t n_layers, Hq, Hkv, d, cap, tree_rows;
+  float scale, rope_theta;
+  entmtp_bf16* k_cache;
+  entmtp_bf16* v_cache;
+  int64_t cache_layer_stride;
+  const entmtp_bf16* w_lm;
+  int32_t hid, V;
+  float inv_temp;
+  float* logits;
+  float* entropy;
+  float* top1p;
+  int32_t* argmax;
+  int32_t* accept_len;
+  int32_t* bonus;
+  float* best_top1p;
+  int32_t* path;
+  int32_t path_capacity;
+  void* workspace;
+  size_t workspace_bytes;
+  void* stream;
+} entmtp_step_config;
+
+typedef struct entmtp_step entmtp_step;
+
+/* Workspace bytes for entmtp_step_create with this bank and configuration
+ * (attention partials for the largest prefix that fits the cache, plus the
+ * LM-head statistics partials); 0 when the configuration is invalid. */
+size_t entmtp_step_workspace(const entmtp_bank* bank, const entmtp_step_config* cfg);
+
+/* Validates cfg against the (device) bank, copies it, and allocates the small
+ * pinned host record that acceptance publishes its result to.  The library
+ * owns *out; release it with entmtp_step_destroy after the stream is idle.
+ * Errors: EINVAL, ERANGE, ENOSPC, EHIP. */
+int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step_config* cfg,
+                           entmtp_step** out);
+void entmtp_step_destroy(entmtp_step* step);
+
+/*
+ * Enqueues one verification step for tree `topo` at prefix length prefix_len,
+ * asynchronously on the configured stream:
+ *   for each layer  entmtp_tree_attn (writes K/V slots [L, L+T) of the layer)
+ *   the LM head with fused statistics partials, then their merge
+ *   greedy acceptance, which also publishes (accept_len, bonus, best_top1p)
+ *   to host memory
+ *   compaction of the accepted path in every layer
+ * Per-step inputs (device): q, k_tree, v_tree, out laid out with tree_rows
+ * rows per layer; hidden [T][hid] bf16; draft_tokens [T] int32.
+ * ev_lm_begin / ev_lm_end: optional hipEvent_t recorded on the stream right
+ * before and after the LM-head launch (NULL: none).
+ * Requirements: prefix_len >= 0, prefix_len + T <= cap.
+ * Errors: EINVAL, ERANGE, EHIP (a failed launch leaves the step unusable for
+ * entmtp_step_wait until the next successful launch).
+ */
+int32_t entmtp_step_launch(entmtp_step* step, int32_t topo, int32_t prefix_len,
+                           const entmtp_bf16* q, const entmtp_bf16* k_tree,
+                           const entmtp_bf16* v_tree, entmtp_bf16* out,
+                           const entmtp_bf16* hidden, const int32_t* draft_tokens,
+                           void* ev_lm_begin, void* ev_lm_end);
+
+/*
+ * Waits for the acceptance result of the latest entmtp_step_launch by polling
+ * the pinned host record (no stream synchronisation; the compaction may still
+ * be running and later work on the stream stays ordered after it).  Writes
+ * the accepted draft count, the bonus token and the top-1 probability at the
+ * accepted node (the scheduler's s, §4) to the host pointers given (each may
+ * be NULL).  Gives up after timeout_s seconds with ETIMEDOUT, or earlier with
+ * EHIP when the stream reports an error.
+ */
+int32_t entmtp_step_wait(entmtp_step* step, int32_t* accept_len, int32_t* bonus,
+                         float* best_top1p, double timeout_s);
 
 #ifdef __cplusplus
 }

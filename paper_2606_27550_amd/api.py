@@ -16,11 +16,23 @@ import numpy as np
 
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libentmtp.so")
 
-OK, EINVAL, ETREE, ERANGE, ENOSPC, EHIP = 0, -1, -2, -3, -4, -5
+OK, EINVAL, ETREE, ERANGE, ENOSPC, EHIP, ETIMEDOUT = 0, -1, -2, -3, -4, -5, -6
 T_MAX, D_MAX, MASK_WORDS, HEAD_DIM = 256, 31, 8, 128
 
 _c_i32, _c_i64, _c_f32, _c_sz, _c_p = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                        ctypes.c_size_t, ctypes.c_void_p)
+
+class StepConfig(ctypes.Structure):
+    """entmtp_step_config, field for field."""
+    _fields_ = [("n_layers", _c_i32), ("Hq", _c_i32), ("Hkv", _c_i32), ("d", _c_i32),
+                ("cap", _c_i32), ("tree_rows", _c_i32), ("scale", _c_f32), ("rope_theta", _c_f32),
+                ("k_cache", _c_p), ("v_cache", _c_p), ("cache_layer_stride", _c_i64),
+                ("w_lm", _c_p), ("hid", _c_i32), ("V", _c_i32), ("inv_temp", _c_f32),
+                ("logits", _c_p), ("entropy", _c_p), ("top1p", _c_p), ("argmax", _c_p),
+                ("accept_len", _c_p), ("bonus", _c_p), ("best_top1p", _c_p), ("path", _c_p),
+                ("path_capacity", _c_i32), ("workspace", _c_p), ("workspace_bytes", _c_sz),
+                ("stream", _c_p)]
+
 
 # name -> (restype, argtypes), mirroring include/entmtp.h
 _SIGNATURES = {
@@ -37,10 +49,24 @@ _SIGNATURES = {
                                   _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p, _c_sz, _c_p]),
     "entmtp_verify_logits": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p]),
     "entmtp_logit_stats": (_c_i32, [_c_p, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_verify_logits_stats_workspace": (_c_sz, [_c_i32, _c_i32, _c_i32]),
+    "entmtp_stats_partials_bytes": (_c_sz, [_c_i32, _c_i32, _c_i32]),
+    "entmtp_verify_logits_partials": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_f32, _c_p, _c_p,
+                                               _c_sz, _c_p]),
+    "entmtp_stats_finalize": (_c_i32, [_c_p, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_verify_logits_stats": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p,
+                                            _c_p, _c_p, _c_sz, _c_p]),
     "entmtp_accept": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "entmtp_kv_compact": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64, _c_i32,
                                    _c_i32, _c_i32, _c_p]),
     "entmtp_ladder_next": (_c_i32, [_c_i32, _c_i32, _c_f32, _c_f32, _c_f32]),
+    "entmtp_step_workspace": (_c_sz, [_c_p, ctypes.POINTER(StepConfig)]),
+    "entmtp_step_create": (_c_i32, [_c_p, ctypes.POINTER(StepConfig), ctypes.POINTER(_c_p)]),
+    "entmtp_step_destroy": (None, [_c_p]),
+    "entmtp_step_launch": (_c_i32, [_c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                    _c_p]),
+    "entmtp_step_wait": (_c_i32, [_c_p, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
+                                  ctypes.POINTER(_c_f32), ctypes.c_double]),
 }
 
 
@@ -240,6 +266,63 @@ def verify_logits(hidden, w_lm, logits, stream=None) -> None:
     _check(lib.entmtp_verify_logits(_p(hidden), _p(w_lm), T, hid, V, _p(logits), _stream(stream)))
 
 
+def verify_logits_stats_workspace(T: int, hid: int, V: int) -> int:
+    return int(lib.entmtp_verify_logits_stats_workspace(T, hid, V))
+
+
+def verify_logits_stats(hidden, w_lm, logits, inv_temp: float, entropy, top1p, argmax, workspace,
+                        stream=None) -> None:
+    """Fused LM head + statistics; same outputs as verify_logits then logit_stats."""
+    import torch
+    _need(hidden.dim() == 2 and w_lm.dim() == 2, "hidden and w_lm are 2-D")
+    T, hid = hidden.shape
+    V = w_lm.shape[0]
+    _dev(hidden, "hidden", torch.bfloat16, (T, hid))
+    _dev(w_lm, "w_lm", torch.bfloat16, (V, hid))
+    _dev(logits, "logits", torch.float32, (T, V))
+    for name, t, dt in (("entropy", entropy, torch.float32), ("top1p", top1p, torch.float32),
+                        ("argmax", argmax, torch.int32)):
+        if t is not None:
+            _dev(t, name, dt, min_numel=T)
+    _need(workspace.is_cuda and workspace.is_contiguous(), "workspace must be a contiguous GPU tensor")
+    _check(lib.entmtp_verify_logits_stats(_p(hidden), _p(w_lm), T, hid, V, inv_temp, _p(logits),
+                                          _p(entropy), _p(top1p), _p(argmax), _p(workspace),
+                                          workspace.numel() * workspace.element_size(),
+                                          _stream(stream)))
+
+
+def stats_partials_bytes(T: int, hid: int, V: int) -> int:
+    return int(lib.entmtp_stats_partials_bytes(T, hid, V))
+
+
+def verify_logits_partials(hidden, w_lm, logits, inv_temp: float, partials, stream=None) -> None:
+    """First half of verify_logits_stats: logits plus per-slice statistics partials."""
+    import torch
+    _need(hidden.dim() == 2 and w_lm.dim() == 2, "hidden and w_lm are 2-D")
+    T, hid = hidden.shape
+    V = w_lm.shape[0]
+    _dev(hidden, "hidden", torch.bfloat16, (T, hid))
+    _dev(w_lm, "w_lm", torch.bfloat16, (V, hid))
+    _dev(logits, "logits", torch.float32, (T, V))
+    _need(partials.is_cuda and partials.is_contiguous(), "partials must be a contiguous GPU tensor")
+    _check(lib.entmtp_verify_logits_partials(_p(hidden), _p(w_lm), T, hid, V, inv_temp, _p(logits),
+                                             _p(partials), partials.numel() * partials.element_size(),
+                                             _stream(stream)))
+
+
+def stats_finalize(partials, T: int, V: int, inv_temp: float, entropy, top1p, argmax,
+                   stream=None) -> None:
+    """Second half of verify_logits_stats: merges the partials into per-node statistics."""
+    import torch
+    _need(partials.is_cuda and partials.is_contiguous(), "partials must be a contiguous GPU tensor")
+    for name, t, dt in (("entropy", entropy, torch.float32), ("top1p", top1p, torch.float32),
+                        ("argmax", argmax, torch.int32)):
+        if t is not None:
+            _dev(t, name, dt, min_numel=T)
+    _check(lib.entmtp_stats_finalize(_p(partials), T, V, inv_temp, _p(entropy), _p(top1p),
+                                     _p(argmax), _stream(stream)))
+
+
 def logit_stats(logits, inv_temp: float, entropy, top1p, argmax, stream=None) -> None:
     import torch
     _need(logits.dim() == 2, "logits are 2-D")
@@ -296,3 +379,79 @@ def ladder_next(rung: int, n_rungs: int, s: float, tau_on: float, tau_off: float
 
 def version() -> str:
     return lib.entmtp_version().decode()
+
+
+# --------------------------------------------------------------------- step --
+
+class Step:
+    """A verification-step context (entmtp_step_*): the caches, the LM head and
+    the per-step outputs are fixed at construction; ``launch`` enqueues one
+    step and ``wait`` returns (accept_len, bonus, best_top1p) from the host
+    record the acceptance kernel publishes.  Output tensors are allocated here
+    and exposed as attributes (logits, entropy, top1p, argmax, accept_len,
+    bonus, best_top1p, path)."""
+
+    def __init__(self, bank: Bank, k_cache, v_cache, w_lm, *, n_layers=1, Hq, Hkv, d=HEAD_DIM,
+                 cap, tree_rows, scale, rope_theta, inv_temp=1.0, cache_layer_stride=0,
+                 stream=None):
+        import torch
+        dev = k_cache.device
+        V, hid = w_lm.shape
+        D = max(bank.D)
+        self.logits = torch.empty((tree_rows, V), dtype=torch.float32, device=dev)
+        self.entropy = torch.empty(tree_rows, dtype=torch.float32, device=dev)
+        self.top1p = torch.empty(tree_rows, dtype=torch.float32, device=dev)
+        self.argmax = torch.empty(tree_rows, dtype=torch.int32, device=dev)
+        self.accept_len = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.bonus = torch.zeros(1, dtype=torch.int32, device=dev)
+        self.best_top1p = torch.zeros(1, dtype=torch.float32, device=dev)
+        self.path = torch.full((D + 1,), -1, dtype=torch.int32, device=dev)
+        _dev(k_cache, "k_cache", torch.bfloat16)
+        _dev(v_cache, "v_cache", torch.bfloat16)
+        _dev(w_lm, "w_lm", torch.bfloat16, (V, hid))
+        self._keep = (bank, k_cache, v_cache, w_lm)
+        c = StepConfig(n_layers, Hq, Hkv, d, cap, tree_rows, scale, rope_theta,
+                       k_cache.data_ptr(), v_cache.data_ptr(), cache_layer_stride, w_lm.data_ptr(),
+                       hid, V, inv_temp, self.logits.data_ptr(), self.entropy.data_ptr(),
+                       self.top1p.data_ptr(), self.argmax.data_ptr(), self.accept_len.data_ptr(),
+                       self.bonus.data_ptr(), self.best_top1p.data_ptr(), self.path.data_ptr(),
+                       D + 1, None, 0, _stream(stream).value)
+        need = int(lib.entmtp_step_workspace(bank.handle, ctypes.byref(c)))
+        if need == 0:
+            _check(lib.entmtp_step_create(bank.handle, ctypes.byref(c), ctypes.byref(_c_p())))
+            raise EntmtpError(EINVAL, "invalid step configuration")
+        self.workspace = torch.empty(need + 256, dtype=torch.uint8, device=dev)
+        base = self.workspace.data_ptr()
+        c.workspace = (base + 255) // 256 * 256
+        c.workspace_bytes = need
+        self.config = c
+        h = _c_p()
+        _check(lib.entmtp_step_create(bank.handle, ctypes.byref(c), ctypes.byref(h)))
+        self._h = h
+        self._a, self._b, self._s = _c_i32(), _c_i32(), _c_f32()
+
+    @property
+    def handle(self):
+        return self._h
+
+    def launch(self, topo: int, prefix_len: int, q, k_tree, v_tree, out, hidden, draft_tokens,
+               ev_lm_begin=None, ev_lm_end=None) -> None:
+        ev = [None if e is None else _c_p(e.cuda_event) for e in (ev_lm_begin, ev_lm_end)]
+        _check(lib.entmtp_step_launch(self._h, topo, prefix_len, _p(q), _p(k_tree), _p(v_tree),
+                                      _p(out), _p(hidden), _p(draft_tokens), ev[0], ev[1]))
+
+    def wait(self, timeout_s: float = 30.0):
+        _check(lib.entmtp_step_wait(self._h, ctypes.byref(self._a), ctypes.byref(self._b),
+                                    ctypes.byref(self._s), timeout_s))
+        return self._a.value, self._b.value, self._s.value
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib.entmtp_step_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass

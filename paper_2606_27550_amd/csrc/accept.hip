@@ -20,7 +20,7 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
     const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
     const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
     int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
-    float* __restrict__ best_p) {
+    float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
   __shared__ uint32_t matched[ENTMTP_MASK_WORDS];
   __shared__ int s_key[kAcceptThreads / 64];
   const int i = threadIdx.x;
@@ -51,9 +51,18 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
   const int a = key >> 10;
   if (i <= D) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
   if (i == 0) {
+    const int bon = amax[best];
+    const float p1 = top1p ? top1p[best] : 0.f;
     *accept_len = a;
-    *bonus = amax[best];
-    if (best_p) *best_p = top1p[best];
+    *bonus = bon;
+    if (best_p) *best_p = p1;
+    if (mirror) {
+      mirror->accept_len = a;
+      mirror->bonus = bon;
+      mirror->best_top1p = p1;
+      __threadfence_system();
+      __hip_atomic_store(&mirror->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    }
   }
 }
 
@@ -61,6 +70,23 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
 }  // namespace entmtp
 
 using namespace entmtp;
+
+namespace entmtp {
+
+int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draft_tokens,
+                      const int32_t* argmax, const float* top1p, int32_t* accept_len,
+                      int32_t* path, int32_t* bonus, float* best_top1p, StepMirror* mirror,
+                      uint32_t seq, hipStream_t stream) {
+  const TopoDesc& d = bank->desc[topo];
+  hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(kAcceptThreads), 0, stream,
+                     bank_ptr<int>(bank, d.off_parent), bank_ptr<int>(bank, d.off_depth),
+                     bank_ptr<uint32_t>(bank, d.off_mask), bank_ptr<int>(bank, d.off_path), d.T,
+                     d.D, draft_tokens, argmax, top1p, accept_len, path, bonus, best_top1p,
+                     mirror, seq);
+  return launch_status("accept launch");
+}
+
+}  // namespace entmtp
 
 extern "C" int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo,
                                  const int32_t* draft_tokens, const int32_t* argmax,
@@ -72,11 +98,6 @@ extern "C" int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo,
                    "draft_tokens, argmax, accept_len, path and bonus must be non-NULL");
   ENTMTP_CHECK_ARG(best_top1p == nullptr || top1p != nullptr, ENTMTP_EINVAL,
                    "best_top1p needs top1p");
-  const TopoDesc& d = bank->desc[topo];
-  hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(kAcceptThreads), 0,
-                     static_cast<hipStream_t>(stream), bank_ptr<int>(bank, d.off_parent),
-                     bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
-                     bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, argmax, top1p,
-                     accept_len, path, bonus, best_top1p);
-  return launch_status("accept launch");
+  return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,
+                       best_top1p, nullptr, 0u, static_cast<hipStream_t>(stream));
 }

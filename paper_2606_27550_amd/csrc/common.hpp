@@ -56,6 +56,24 @@ namespace entmtp {
 // Validates (bank, topo) for a kernel launch; returns 0 or an error status.
 int32_t check_device_bank(const entmtp_bank* bank, int32_t topo);
 
+// Result of one verification step as the host reads it: written by the accept
+// kernel into coherent pinned host memory, fields first, then `seq` with
+// system-scope release, so a host that sees `seq` also sees the fields.
+struct StepMirror {
+  uint32_t seq;
+  int32_t accept_len;
+  int32_t bonus;
+  float best_top1p;
+};
+
+// Launches the accept kernel (no argument checks beyond the bank's); with a
+// non-NULL `mirror` (device address of host memory) it also publishes the
+// result there under sequence number `seq`.
+int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draft_tokens,
+                      const int32_t* argmax, const float* top1p, int32_t* accept_len,
+                      int32_t* path, int32_t* bonus, float* best_top1p, StepMirror* mirror,
+                      uint32_t seq, hipStream_t stream);
+
 template <typename T>
 inline const T* bank_ptr(const entmtp_bank* b, int64_t off) {
   return reinterpret_cast<const T*>(b->arena + off);

@@ -369,6 +369,53 @@ __global__ __launch_bounds__(kL3Threads) void lm_head_lds_kernel(
 // every wave's share.  All loads are issued unconditionally (addresses are
 // clamped) so that every path carries the same load count.
 // ---------------------------------------------------------------------------
+// ---------------------------------------------------------------------------
+// Softmax-statistics partials fused into the LM-head epilogue.  A partial of
+// a set of vocabulary rows is (zmax, idx, Z, S): the largest raw logit and the
+// lowest index attaining it (the argmax is decided on raw fp32 logits), and,
+// with y = inv_temp * z and m = inv_temp * zmax, Z = sum e^(y - m) and
+// S = sum (y - m) e^(y - m).  Partials merge exactly (up to rounding) after
+// rescaling to the larger maximum, so the per-workgroup partials of every
+// vocabulary slice combine into the row's entropy ln Z - S/Z, top-1
+// probability 1/Z and argmax.
+// ---------------------------------------------------------------------------
+struct StatPart {
+  float zmax, Z, S;
+  int idx;
+};
+
+__device__ __forceinline__ void take_max(float& zm, int& zi, float z2, int i2) {
+  if (z2 > zm || (z2 == zm && i2 < zi)) {
+    zm = z2;
+    zi = i2;
+  }
+}
+
+__device__ __forceinline__ void part_merge(StatPart& a, const StatPart& b, float inv_temp) {
+  float zm = a.zmax;
+  int zi = a.idx;
+  take_max(zm, zi, b.zmax, b.idx);
+  if (zm == -INFINITY) return;   // both empty
+  const float my = zm * inv_temp;
+  float Z = 0.f, S = 0.f;
+  if (a.zmax != -INFINITY) {
+    const float ma = a.zmax * inv_temp, f = expf(ma - my);
+    Z += a.Z * f;
+    S += f * (a.S + (ma - my) * a.Z);
+  }
+  if (b.zmax != -INFINITY) {
+    const float mb = b.zmax * inv_temp, f = expf(mb - my);
+    Z += b.Z * f;
+    S += f * (b.S + (mb - my) * b.Z);
+  }
+  a = StatPart{zm, Z, S, zi};
+}
+
+__device__ __forceinline__ StatPart shfl_part(const StatPart& p, int off) {
+  return StatPart{__shfl_xor(p.zmax, off, 64), __shfl_xor(p.Z, off, 64), __shfl_xor(p.S, off, 64),
+                  __shfl_xor(p.idx, off, 64)};
+}
+
 constexpr int kHybWaves = 4;                        // 64 rows per workgroup slice
 constexpr int kHybThreads = 64 * kHybWaves;
 
@@ -382,10 +429,10 @@ struct HybShape {
   static_assert(NXI % kHybWaves == 0, "X split");
 };
 
-template <int NT, int S, int NCH>
+template <int NT, int S, int NCH, bool STATS>
 __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
-    int T, int hid, int V, int G) {
+    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
   using Sh = HybShape<NT>;
   // precondition (host dispatch): hid is a multiple of S * 128, and equals
   // NCH * 128 when NCH > 0 (the K loop is then unrolled completely: no
@@ -404,8 +451,13 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
 
   const int r0 = slice_begin(blockIdx.x, G, V);
   const int r1 = slice_begin(blockIdx.x + 1, G, V);
-  if (r0 >= r1) return;  // empty slice (tiny V): the whole workgroup leaves
   const int j0 = blockIdx.y * Sh::TP;
+  if (r0 >= r1) {  // empty slice (tiny V): the whole workgroup leaves
+    if constexpr (STATS)
+      if (threadIdx.x < Sh::TP && j0 + threadIdx.x < T)
+        part[static_cast<size_t>(j0 + threadIdx.x) * G + blockIdx.x] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
+    return;
+  }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
   const int tile0 = r0 + 16 * wave;
@@ -479,8 +531,8 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
   load(wbuf[0], xring[0], 0);
   if constexpr (S > 2) load(wbuf[1], xring[1], 1 < nch ? 1 : nch - 1);
   if constexpr (S > 3) load(wbuf[2], xring[2], 2 < nch ? 2 : nch - 1);
-#pragma unroll
-  for (int c = 0; c < (NCH > 0 ? NCH : nch); c += S) {
+  // one round = S pipeline steps; stage c + k is multiplied in step k
+  auto round = [&](int c) {
 #pragma unroll
     for (int k = 0; k < S; ++k) {
       const int cc = c + k;
@@ -496,23 +548,77 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
       // keeps the compiler's load bookkeeping exact
       compute(wbuf[k], xring[k]);
     }
+  };
+  if constexpr (NCH > 0) {
+#pragma unroll
+    for (int c = 0; c < NCH; c += S) round(c);
+  } else {
+    for (int c = 0; c < nch; c += S) round(c);
   }
   wait_vmcnt<0>();   // no copy may land in LDS after the workgroup is gone
 
-  if (!live) return;
   const bool vec_ok = (V & 3) == 0;
   const int v = tile0 + 4 * lg;
+  if (live) {
 #pragma unroll
-  for (int n = 0; n < NT; ++n) {
-    const int node = j0 + n * 16 + lr;
-    if (node >= T) continue;
-    float* dst = logits + static_cast<size_t>(node) * V + v;
-    if (vec_ok && v + 3 < r1) {
-      *reinterpret_cast<f32x4*>(dst) = acc[n];
-    } else {
+    for (int n = 0; n < NT; ++n) {
+      const int node = j0 + n * 16 + lr;
+      if (node >= T) continue;
+      float* dst = logits + static_cast<size_t>(node) * V + v;
+      if (vec_ok && v + 3 < r1) {
+        *reinterpret_cast<f32x4*>(dst) = acc[n];
+      } else {
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (v + r < r1) dst[r] = acc[n][r];
+      }
+    }
+  }
+  if constexpr (STATS) {
+    // per node column: wave partial over the wave's rows, then the four
+    // waves in LDS, then one partial per (node, workgroup).  The wave
+    // partials live in the wave's own transposition tile, which its last
+    // multiply has finished reading (LDS operations of a wave stay in
+    // order), so the epilogue adds no LDS and the occupancy is unchanged.
+    static_assert(Sh::TP * sizeof(StatPart) <= kL3TileBytes, "wave partials fit in a tile");
+    StatPart* const wpart_own = reinterpret_cast<StatPart*>(tp);
+#pragma unroll
+    for (int n = 0; n < NT; ++n) {
+      StatPart p{-INFINITY, 0.f, 0.f, 0x7fffffff};
 #pragma unroll
       for (int r = 0; r < 4; ++r)
-        if (v + r < r1) dst[r] = acc[n][r];
+        if (live && v + r < r1) take_max(p.zmax, p.idx, acc[n][r], v + r);
+#pragma unroll
+      for (int off = 16; off <= 32; off <<= 1)
+        take_max(p.zmax, p.idx, __shfl_xor(p.zmax, off, 64), __shfl_xor(p.idx, off, 64));
+      if (p.zmax != -INFINITY) {
+        const float my = p.zmax * inv_temp;
+#pragma unroll
+        for (int r = 0; r < 4; ++r) {
+          if (live && v + r < r1) {
+            const float t = acc[n][r] * inv_temp - my;
+            const float e = expf(t);
+            p.Z += e;
+            if (e > 0.f) p.S += t * e;
+          }
+        }
+      }
+#pragma unroll
+      for (int off = 16; off <= 32; off <<= 1) {
+        p.Z += __shfl_xor(p.Z, off, 64);
+        p.S += __shfl_xor(p.S, off, 64);
+      }
+      if (lg == 0) wpart_own[n * 16 + lr] = p;
+    }
+    __syncthreads();
+    const int c = threadIdx.x;
+    if (c < Sh::TP && j0 + c < T) {
+      const StatPart* wpart = reinterpret_cast<const StatPart*>(tpose);
+      constexpr int kStride = kL3TileBytes / static_cast<int>(sizeof(StatPart));
+      StatPart acc_p = wpart[c];
+#pragma unroll
+      for (int w = 1; w < kHybWaves; ++w) part_merge(acc_p, wpart[w * kStride + c], inv_temp);
+      part[static_cast<size_t>(j0 + c) * G + blockIdx.x] = acc_p;
     }
   }
 }
@@ -541,22 +647,78 @@ int device_cus() {
   return cus[dev];
 }
 
-template <int NT, int S, int NCH>
-int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
-                      hipStream_t s) {
-  // Slices of at most 64 rows, and a grid that is a whole multiple of the CU
-  // count: every CU then streams the same number of bytes (a partial extra
-  // round of workgroups on a few CUs costs ~20% at 7B shapes).
+// Combines the G partials of node blockIdx.x into its statistics.
+constexpr int kFinThreads = 256;
+__global__ __launch_bounds__(kFinThreads) void stats_finalize_kernel(
+    const StatPart* __restrict__ part, int G, float inv_temp, float* __restrict__ entropy,
+    float* __restrict__ top1p, int* __restrict__ argmax) {
+  __shared__ StatPart wsum[kFinThreads / 64];
+  const StatPart* row = part + static_cast<size_t>(blockIdx.x) * G;
+  StatPart p{-INFINITY, 0.f, 0.f, 0x7fffffff};
+  for (int g = threadIdx.x; g < G; g += kFinThreads) part_merge(p, row[g], inv_temp);
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) part_merge(p, shfl_part(p, off), inv_temp);
+  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = p;
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    StatPart a = wsum[0];
+    for (int w = 1; w < kFinThreads / 64; ++w) part_merge(a, wsum[w], inv_temp);
+    if (entropy) entropy[blockIdx.x] = logf(a.Z) - a.S / a.Z;
+    if (top1p) top1p[blockIdx.x] = 1.f / a.Z;
+    if (argmax) argmax[blockIdx.x] = a.idx;
+  }
+}
+
+// Workgroups of the streaming LM-head grid: slices of at most 64 rows, and a
+// whole multiple of the CU count, so that every CU streams the same number
+// of bytes (a partial extra round of workgroups on a few CUs costs ~20% at
+// 7B shapes).
+int hyb_grid(int V) {
   constexpr int rows = 16 * kHybWaves;
   const int cus = device_cus();
   const int max_g = (V + 3) / 4;
   int G = cus;
   while (G < max_g && max_slice(V, G) > rows) G += cus;
-  G = G < max_g ? G : max_g;
+  return G < max_g ? G : max_g;
+}
+
+template <int NT, int S, int NCH, bool STATS = false>
+int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
+                      hipStream_t s, float inv_temp = 1.f, StatPart* part = nullptr) {
+  const int G = hyb_grid(V);
   const int passes = (T + NT * 16 - 1) / (NT * 16);
-  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH>), dim3(G, passes), dim3(kHybThreads), 0, s, X,
-                     W, logits, T, hid, V, G);
+  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS>), dim3(G, passes), dim3(kHybThreads), 0,
+                     s, X, W, logits, T, hid, V, G, inv_temp, part);
   return launch_status("verify_logits launch");
+}
+
+// Streaming LM head with fused statistics partials, then the per-node
+// finalize; false when the streaming kernel does not apply to hid.
+template <bool STATS>
+bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
+                         hipStream_t s, float inv_temp, StatPart* part, int32_t* rc) {
+  if (hid == 4096) {              // the 7B hidden size: K loop fully unrolled
+    if (T <= 16) *rc = launch_lm_hyb<1, 4, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else if (T <= 32) *rc = launch_lm_hyb<2, 4, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else if (T <= 64) *rc = launch_lm_hyb<4, 4, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else *rc = launch_lm_hyb<8, 2, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    return true;
+  }
+  if (hid == 5120) {              // the 13B hidden size
+    if (T <= 16) *rc = launch_lm_hyb<1, 4, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else if (T <= 32) *rc = launch_lm_hyb<2, 4, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else if (T <= 64) *rc = launch_lm_hyb<4, 4, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else *rc = launch_lm_hyb<8, 2, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    return true;
+  }
+  if (hid % (4 * kL3Bk) == 0) {   // a whole number of 4-stage rounds
+    if (T <= 16) *rc = launch_lm_hyb<1, 4, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else if (T <= 32) *rc = launch_lm_hyb<2, 4, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else if (T <= 64) *rc = launch_lm_hyb<4, 4, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    else *rc = launch_lm_hyb<8, 2, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    return true;
+  }
+  return false;
 }
 
 template <int NT, int S>
@@ -603,25 +765,9 @@ extern "C" int32_t entmtp_verify_logits(const entmtp_bf16* hidden, const entmtp_
   ENTMTP_CHECK_ARG(aligned16(hidden) && aligned16(w_lm) && aligned16(logits), ENTMTP_EINVAL,
                    "hidden, w_lm and logits must be 16-byte aligned");
   auto s = static_cast<hipStream_t>(stream);
+  int32_t rc = ENTMTP_OK;
+  if (launch_hyb_dispatch<false>(hidden, w_lm, logits, T, hid, V, s, 1.f, nullptr, &rc)) return rc;
   if (hid % kL3Bk == 0) {
-    if (hid == 4096) {              // the 7B hidden size: K loop fully unrolled
-      if (T <= 16) return launch_lm_hyb<1, 4, 32>(hidden, w_lm, logits, T, hid, V, s);
-      if (T <= 32) return launch_lm_hyb<2, 4, 32>(hidden, w_lm, logits, T, hid, V, s);
-      if (T <= 64) return launch_lm_hyb<4, 4, 32>(hidden, w_lm, logits, T, hid, V, s);
-      return launch_lm_hyb<8, 2, 32>(hidden, w_lm, logits, T, hid, V, s);
-    }
-    if (hid == 5120) {              // the 13B hidden size
-      if (T <= 16) return launch_lm_hyb<1, 4, 40>(hidden, w_lm, logits, T, hid, V, s);
-      if (T <= 32) return launch_lm_hyb<2, 4, 40>(hidden, w_lm, logits, T, hid, V, s);
-      if (T <= 64) return launch_lm_hyb<4, 4, 40>(hidden, w_lm, logits, T, hid, V, s);
-      return launch_lm_hyb<8, 2, 40>(hidden, w_lm, logits, T, hid, V, s);
-    }
-    if (hid % (4 * kL3Bk) == 0) {   // the hybrid kernel needs a whole number of 4-stage rounds
-      if (T <= 16) return launch_lm_hyb<1, 4, 0>(hidden, w_lm, logits, T, hid, V, s);
-      if (T <= 32) return launch_lm_hyb<2, 4, 0>(hidden, w_lm, logits, T, hid, V, s);
-      if (T <= 64) return launch_lm_hyb<4, 4, 0>(hidden, w_lm, logits, T, hid, V, s);
-      return launch_lm_hyb<8, 2, 0>(hidden, w_lm, logits, T, hid, V, s);
-    }
     if (T <= 16) return launch_lm_lds<1, 4>(hidden, w_lm, logits, T, hid, V, s);
     if (T <= 32) return launch_lm_lds<2, 4>(hidden, w_lm, logits, T, hid, V, s);
     if (T <= 64) return launch_lm_lds<4, 3>(hidden, w_lm, logits, T, hid, V, s);
@@ -631,4 +777,72 @@ extern "C" int32_t entmtp_verify_logits(const entmtp_bf16* hidden, const entmtp_
   if (T <= 32) return launch_lm<2, 256>(hidden, w_lm, logits, T, hid, V, s);
   if (T <= 64) return launch_lm<4, 128>(hidden, w_lm, logits, T, hid, V, s);
   return launch_lm<8, 128>(hidden, w_lm, logits, T, hid, V, s);
+}
+
+extern "C" size_t entmtp_stats_partials_bytes(int32_t T, int32_t hid, int32_t V) {
+  if (T < 1 || T > 4096 || V < 1 || hid < 8 || hid % (4 * kL3Bk)) return 0;
+  return static_cast<size_t>(T) * hyb_grid(V) * sizeof(StatPart);
+}
+
+extern "C" int32_t entmtp_verify_logits_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                                 int32_t T, int32_t hid, int32_t V, float inv_temp,
+                                                 float* logits, void* partials,
+                                                 size_t partials_bytes, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(hidden && w_lm && logits && partials, ENTMTP_EINVAL,
+                   "hidden, w_lm, logits and partials must be non-NULL");
+  ENTMTP_CHECK_ARG(T >= 1 && T <= 4096, ENTMTP_EINVAL, "T = %d outside [1, 4096]", T);
+  ENTMTP_CHECK_ARG(hid >= 4 * kL3Bk && hid % (4 * kL3Bk) == 0, ENTMTP_EINVAL,
+                   "hid = %d: the fused path needs a multiple of %d", hid, 4 * kL3Bk);
+  ENTMTP_CHECK_ARG(V >= 1, ENTMTP_EINVAL, "V = %d < 1", V);
+  ENTMTP_CHECK_ARG(inv_temp > 0.f && inv_temp < INFINITY, ENTMTP_EINVAL,
+                   "inv_temp = %g must be positive and finite", static_cast<double>(inv_temp));
+  ENTMTP_CHECK_ARG(aligned16(hidden) && aligned16(w_lm) && aligned16(logits) && aligned16(partials),
+                   ENTMTP_EINVAL, "hidden, w_lm, logits and partials must be 16-byte aligned");
+  const size_t need = entmtp_stats_partials_bytes(T, hid, V);
+  ENTMTP_CHECK_ARG(partials_bytes >= need, ENTMTP_ENOSPC, "partials buffer has %zu bytes, needs %zu",
+                   partials_bytes, need);
+  int32_t rc = ENTMTP_OK;
+  launch_hyb_dispatch<true>(hidden, w_lm, logits, T, hid, V, static_cast<hipStream_t>(stream),
+                            inv_temp, static_cast<StatPart*>(partials), &rc);
+  return rc;
+}
+
+extern "C" int32_t entmtp_stats_finalize(const void* partials, int32_t T, int32_t V, float inv_temp,
+                                         float* entropy, float* top1p, int32_t* argmax,
+                                         void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(partials != nullptr, ENTMTP_EINVAL, "partials is NULL");
+  ENTMTP_CHECK_ARG(T >= 1 && T <= 4096 && V >= 1, ENTMTP_EINVAL, "T = %d, V = %d out of range", T, V);
+  ENTMTP_CHECK_ARG(inv_temp > 0.f && inv_temp < INFINITY, ENTMTP_EINVAL,
+                   "inv_temp = %g must be positive and finite", static_cast<double>(inv_temp));
+  if (!entropy && !top1p && !argmax) return ENTMTP_OK;
+  hipLaunchKernelGGL(stats_finalize_kernel, dim3(T), dim3(kFinThreads), 0,
+                     static_cast<hipStream_t>(stream), static_cast<const StatPart*>(partials),
+                     hyb_grid(V), inv_temp, entropy, top1p, argmax);
+  return launch_status("stats_finalize launch");
+}
+
+extern "C" size_t entmtp_verify_logits_stats_workspace(int32_t T, int32_t hid, int32_t V) {
+  if (T < 1 || T > 4096 || V < 1 || hid < 8 || hid % 8) return 0;
+  const size_t p = entmtp_stats_partials_bytes(T, hid, V);
+  return p ? p : 256;   // other hidden sizes: separate kernels, no partials
+}
+
+extern "C" int32_t entmtp_verify_logits_stats(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                              int32_t T, int32_t hid, int32_t V, float inv_temp,
+                                              float* logits, float* entropy, float* top1p,
+                                              int32_t* argmax, void* workspace,
+                                              size_t workspace_bytes, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(hid >= 8 && hid % 8 == 0, ENTMTP_EINVAL, "hid = %d must be a positive multiple of 8", hid);
+  if (entmtp_stats_partials_bytes(T, hid, V) > 0) {
+    if (int32_t rc = entmtp_verify_logits_partials(hidden, w_lm, T, hid, V, inv_temp, logits,
+                                                   workspace, workspace_bytes, stream))
+      return rc;
+    return entmtp_stats_finalize(workspace, T, V, inv_temp, entropy, top1p, argmax, stream);
+  }
+  // other hidden sizes: logits first, then the statistics pass over them
+  if (int32_t rc = entmtp_verify_logits(hidden, w_lm, T, hid, V, logits, stream)) return rc;
+  return entmtp_logit_stats(logits, T, V, inv_temp, entropy, top1p, argmax, stream);
 }

@@ -1,0 +1,253 @@
+// One verification step, end to end, behind a small native context.
+//
+// The decode loop of §4 verifies the scheduled tree, accepts the longest
+// matching path, updates the cache, and reads one scalar back to the host to
+// pick the next tree ("Cost": a single device-to-host read per step).  The
+// context below validates the fixed sizes once, then each step is a short
+// burst of launches on one stream; the acceptance kernel publishes its result
+// into coherent pinned host memory, and the host polls that record instead of
+// synchronising the stream, so the cache compaction and the host's choice of
+// the next tree overlap.
+#include <chrono>
+#include <cmath>
+#include <cstring>
+
+#include "common.hpp"
+
+using namespace entmtp;
+
+struct entmtp_step {
+  const entmtp_bank* bank = nullptr;
+  entmtp_step_config cfg{};
+  int32_t T_max = 0;
+  int32_t D_max = 0;
+  size_t attn_bytes = 0;       // attention workspace, at the start of cfg.workspace
+  size_t part_offset = 0;      // LM-head statistics partials follow it
+  size_t part_bytes = 0;
+  StepMirror* host = nullptr;  // pinned, coherent
+  StepMirror* dev = nullptr;   // device address of `host`
+  uint32_t seq = 0;            // sequence number of the latest launch
+  bool pending = false;        // a launched step whose result has not been read
+};
+
+namespace {
+
+size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
+  int32_t t = 0, dd = 0;
+  for (const TopoDesc& d : bank->desc) {
+    t = d.T > t ? d.T : t;
+    dd = d.D > dd ? d.D : dd;
+  }
+  *T_max = t;
+  *D_max = dd;
+}
+
+// Workspace split for a validated configuration.
+void layout(const entmtp_step_config& c, int32_t T_max, size_t* attn, size_t* part_off,
+            size_t* part) {
+  *attn = entmtp_tree_attn_workspace(T_max, c.Hq, c.Hkv, c.d, c.cap);
+  *part_off = round256(*attn);
+  *part = entmtp_stats_partials_bytes(T_max, c.hid, c.V);
+}
+
+bool finite_positive(float x) { return x > 0.f && std::isfinite(x); }
+
+// Validates everything but the workspace pointer (its size is what the
+// workspace query answers).
+int32_t check_config(const entmtp_bank* bank, const entmtp_step_config* c, int32_t* T_max,
+                     int32_t* D_max) {
+  if (int32_t rc = check_device_bank(bank, 0)) return rc;
+  ENTMTP_CHECK_ARG(c != nullptr, ENTMTP_EINVAL, "config is NULL");
+  bank_extent(bank, T_max, D_max);
+  ENTMTP_CHECK_ARG(c->n_layers >= 1, ENTMTP_EINVAL, "n_layers = %d < 1", c->n_layers);
+  ENTMTP_CHECK_ARG(c->d == ENTMTP_HEAD_DIM, ENTMTP_EINVAL, "head dim %d unsupported (built for %d)",
+                   c->d, ENTMTP_HEAD_DIM);
+  ENTMTP_CHECK_ARG(c->Hq >= 1 && c->Hkv >= 1, ENTMTP_EINVAL, "Hq = %d, Hkv = %d must be >= 1",
+                   c->Hq, c->Hkv);
+  ENTMTP_CHECK_ARG(c->Hq % c->Hkv == 0, ENTMTP_ERANGE, "Hq = %d is not a multiple of Hkv = %d",
+                   c->Hq, c->Hkv);
+  ENTMTP_CHECK_ARG(c->tree_rows >= *T_max, ENTMTP_EINVAL,
+                   "tree_rows = %d below the bank's largest tree (%d nodes)", c->tree_rows, *T_max);
+  ENTMTP_CHECK_ARG(c->cap >= *T_max, ENTMTP_ERANGE, "cap = %d below the largest tree (%d nodes)",
+                   c->cap, *T_max);
+  ENTMTP_CHECK_ARG(finite_positive(c->scale), ENTMTP_EINVAL, "scale must be positive and finite");
+  ENTMTP_CHECK_ARG(c->rope_theta >= 0.f && std::isfinite(c->rope_theta), ENTMTP_EINVAL,
+                   "rope_theta must be >= 0 and finite");
+  ENTMTP_CHECK_ARG(c->k_cache && c->v_cache && aligned16(c->k_cache) && aligned16(c->v_cache),
+                   ENTMTP_EINVAL, "caches must be non-NULL and 16-byte aligned");
+  ENTMTP_CHECK_ARG(c->n_layers == 1 ||
+                       (c->cache_layer_stride >= static_cast<int64_t>(c->Hkv) * c->cap * c->d &&
+                        c->cache_layer_stride % 8 == 0),
+                   ENTMTP_EINVAL, "cache_layer_stride %lld must cover one layer and keep alignment",
+                   static_cast<long long>(c->cache_layer_stride));
+  ENTMTP_CHECK_ARG(c->w_lm && aligned16(c->w_lm), ENTMTP_EINVAL, "w_lm must be non-NULL and aligned");
+  ENTMTP_CHECK_ARG(c->V >= 1, ENTMTP_EINVAL, "V = %d < 1", c->V);
+  ENTMTP_CHECK_ARG(entmtp_stats_partials_bytes(*T_max, c->hid, c->V) > 0, ENTMTP_EINVAL,
+                   "hid = %d: the step needs a multiple of 512", c->hid);
+  ENTMTP_CHECK_ARG(finite_positive(c->inv_temp), ENTMTP_EINVAL, "inv_temp must be positive and finite");
+  ENTMTP_CHECK_ARG(c->logits && aligned16(c->logits) && c->entropy && c->top1p && c->argmax,
+                   ENTMTP_EINVAL, "logits (16-byte aligned) and statistics outputs must be non-NULL");
+  ENTMTP_CHECK_ARG(c->accept_len && c->bonus && c->best_top1p && c->path, ENTMTP_EINVAL,
+                   "acceptance outputs must be non-NULL");
+  ENTMTP_CHECK_ARG(c->path_capacity >= *D_max + 1, ENTMTP_EINVAL,
+                   "path_capacity = %d below 1 + the bank's depth %d", c->path_capacity, *D_max);
+  return ENTMTP_OK;
+}
+
+}  // namespace
+
+extern "C" size_t entmtp_step_workspace(const entmtp_bank* bank, const entmtp_step_config* cfg) {
+  int32_t T_max = 0, D_max = 0;
+  if (check_config(bank, cfg, &T_max, &D_max) != ENTMTP_OK) {
+    clear_error();
+    return 0;
+  }
+  size_t attn = 0, off = 0, part = 0;
+  layout(*cfg, T_max, &attn, &off, &part);
+  return attn && part ? off + part : 0;
+}
+
+extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step_config* cfg,
+                                      entmtp_step** out) {
+  clear_error();
+  ENTMTP_CHECK_ARG(out != nullptr, ENTMTP_EINVAL, "out is NULL");
+  *out = nullptr;
+  int32_t T_max = 0, D_max = 0;
+  if (int32_t rc = check_config(bank, cfg, &T_max, &D_max)) return rc;
+  size_t attn = 0, off = 0, part = 0;
+  layout(*cfg, T_max, &attn, &off, &part);
+  ENTMTP_CHECK_ARG(attn > 0 && part > 0, ENTMTP_EINVAL, "unsupported attention or LM-head sizes");
+  ENTMTP_CHECK_ARG(cfg->workspace && (reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) == 0,
+                   ENTMTP_EINVAL, "workspace must be non-NULL and 256-byte aligned");
+  ENTMTP_CHECK_ARG(cfg->workspace_bytes >= off + part, ENTMTP_ENOSPC,
+                   "workspace has %zu bytes, needs %zu", cfg->workspace_bytes, off + part);
+  int dev = -1;
+  if (int32_t rc = hip_status(hipGetDevice(&dev), "hipGetDevice")) return rc;
+  ENTMTP_CHECK_ARG(dev == bank->device, ENTMTP_EINVAL,
+                   "current device %d differs from the bank's device %d", dev, bank->device);
+
+  entmtp_step* st = new entmtp_step;
+  st->bank = bank;
+  st->cfg = *cfg;
+  st->T_max = T_max;
+  st->D_max = D_max;
+  st->attn_bytes = attn;
+  st->part_offset = off;
+  st->part_bytes = part;
+  void* h = nullptr;
+  int32_t rc = hip_status(hipHostMalloc(&h, sizeof(StepMirror), hipHostMallocMapped | hipHostMallocCoherent),
+                          "hipHostMalloc (step result record)");
+  if (rc == ENTMTP_OK) {
+    st->host = static_cast<StepMirror*>(h);
+    std::memset(st->host, 0, sizeof(StepMirror));
+    void* d = nullptr;
+    rc = hip_status(hipHostGetDevicePointer(&d, h, 0), "hipHostGetDevicePointer");
+    st->dev = static_cast<StepMirror*>(d);
+  }
+  if (rc != ENTMTP_OK) {
+    entmtp_step_destroy(st);
+    return rc;
+  }
+  *out = st;
+  return ENTMTP_OK;
+}
+
+extern "C" void entmtp_step_destroy(entmtp_step* st) {
+  if (!st) return;
+  if (st->host) (void)hipHostFree(st->host);
+  delete st;
+}
+
+extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t prefix_len,
+                                      const entmtp_bf16* q, const entmtp_bf16* k_tree,
+                                      const entmtp_bf16* v_tree, entmtp_bf16* out,
+                                      const entmtp_bf16* hidden, const int32_t* draft_tokens,
+                                      void* ev_lm_begin, void* ev_lm_end) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
+  st->pending = false;
+  const entmtp_step_config& c = st->cfg;
+  if (int32_t rc = check_device_bank(st->bank, topo)) return rc;
+  ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && draft_tokens, ENTMTP_EINVAL,
+                   "per-step inputs and outputs must be non-NULL");
+  const int32_t T = st->bank->desc[topo].T;
+  ENTMTP_CHECK_ARG(prefix_len >= 0 && static_cast<int64_t>(prefix_len) + T <= c.cap, ENTMTP_ERANGE,
+                   "prefix_len %d + T %d outside the cache capacity %d", prefix_len, T, c.cap);
+  auto s = static_cast<hipStream_t>(c.stream);
+  uint8_t* ws = static_cast<uint8_t*>(c.workspace);
+  void* part = ws + st->part_offset;
+
+  const size_t q_layer = static_cast<size_t>(c.tree_rows) * c.Hq * c.d;
+  const size_t kv_layer = static_cast<size_t>(c.tree_rows) * c.Hkv * c.d;
+  for (int32_t l = 0; l < c.n_layers; ++l) {
+    const size_t cl = static_cast<size_t>(l) * static_cast<size_t>(c.cache_layer_stride);
+    if (int32_t rc = entmtp_tree_attn(st->bank, topo, q + l * q_layer, k_tree + l * kv_layer,
+                                      v_tree + l * kv_layer, c.k_cache + cl, c.v_cache + cl, c.cap,
+                                      prefix_len, c.Hq, c.Hkv, c.d, c.scale, c.rope_theta,
+                                      out + l * q_layer, ws, st->attn_bytes, c.stream))
+      return rc;
+  }
+  if (ev_lm_begin)
+    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_begin), s),
+                                "hipEventRecord"))
+      return rc;
+  if (int32_t rc = entmtp_verify_logits_partials(hidden, c.w_lm, T, c.hid, c.V, c.inv_temp,
+                                                 c.logits, part, st->part_bytes, c.stream))
+    return rc;
+  if (ev_lm_end)
+    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_end), s),
+                                "hipEventRecord"))
+      return rc;
+  if (int32_t rc = entmtp_stats_finalize(part, T, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax,
+                                         c.stream))
+    return rc;
+  const uint32_t seq = st->seq + 1u;
+  if (int32_t rc = launch_accept(st->bank, topo, draft_tokens, c.argmax, c.top1p, c.accept_len,
+                                 c.path, c.bonus, c.best_top1p, st->dev, seq, s))
+    return rc;
+  st->seq = seq;
+  if (int32_t rc = entmtp_kv_compact(c.path, c.path_capacity, c.accept_len, prefix_len, c.k_cache,
+                                     c.v_cache, c.n_layers, c.cache_layer_stride, c.Hkv, c.cap, c.d,
+                                     c.stream))
+    return rc;
+  st->pending = true;
+  return ENTMTP_OK;
+}
+
+extern "C" int32_t entmtp_step_wait(entmtp_step* st, int32_t* accept_len, int32_t* bonus,
+                                    float* best_top1p, double timeout_s) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
+  ENTMTP_CHECK_ARG(st->pending, ENTMTP_EINVAL, "no launched step is waiting to be read");
+  ENTMTP_CHECK_ARG(timeout_s >= 0.0, ENTMTP_EINVAL, "timeout_s must be >= 0");
+  const uint32_t want = st->seq;
+  const auto t0 = std::chrono::steady_clock::now();
+  auto s = static_cast<hipStream_t>(st->cfg.stream);
+  for (uint32_t spin = 1;; ++spin) {
+    if (__atomic_load_n(&st->host->seq, __ATOMIC_ACQUIRE) == want) break;
+    if ((spin & 255u) == 0u) {
+      // every few hundred polls: a failed stream or an expired limit ends the wait
+      const hipError_t e = hipStreamQuery(s);
+      if (e == hipSuccess) {
+        if (__atomic_load_n(&st->host->seq, __ATOMIC_ACQUIRE) == want) break;
+        st->pending = false;
+        return fail(ENTMTP_EHIP, "stream idle but step %u published no result", want);
+      }
+      if (e != hipErrorNotReady) {
+        st->pending = false;
+        return hip_status(e, "stream error while waiting for the step");
+      }
+      const double el = std::chrono::duration<double>(std::chrono::steady_clock::now() - t0).count();
+      if (el > timeout_s)
+        return fail(ENTMTP_ETIMEDOUT, "no result for step %u after %.3f s", want, el);
+    }
+    __builtin_ia32_pause();
+  }
+  if (accept_len) *accept_len = st->host->accept_len;
+  if (bonus) *bonus = st->host->bonus;
+  if (best_top1p) *best_top1p = st->host->best_top1p;
+  st->pending = false;
+  return ENTMTP_OK;
+}

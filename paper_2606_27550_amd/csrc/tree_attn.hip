@@ -36,7 +36,7 @@ constexpr int KB = 32;               // keys per block
 constexpr int kQTile = 32;           // query rows per tile
 constexpr int VT_LD = 36;            // bf16 per V^T row in LDS (32 keys + pad)
 constexpr int kMaxSplits = 32;
-constexpr int kMinBlocksPerSplit = 8;
+constexpr int kMinBlocksPerSplit = 4;   // one block per wave at least
 
 __host__ __device__ inline int rows_padded(int G, int T) {
   return (G * T + kQTile - 1) / kQTile * kQTile;
@@ -49,55 +49,41 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(
     const uint16_t* __restrict__ vt, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
     uint16_t* __restrict__ qrot, const int* __restrict__ depth, int T, int Hq, int Hkv, int cap,
     int L, double theta, int rows_pad) {
+  // grid (T, chunks): block (i, y) takes items [256 y, 256 y + 256) of node
+  // i's list: Hq*64 query pairs, then Hkv*64 key pairs, then Hkv*16 16-byte
+  // value chunks
   constexpr int HALF = HD / 2;
-  __shared__ double s_cos[HALF], s_sin[HALF];
   const int i = blockIdx.x;
+  const int u = blockIdx.y * blockDim.x + threadIdx.x;
   const int G = Hq / Hkv;
-  const bool rope = theta > 0.0;
-  if (rope) {
-    const double pos = static_cast<double>(L) + static_cast<double>(depth[i]);
-    for (int c = threadIdx.x; c < HALF; c += blockDim.x) {
-      const double ang = pos * pow(theta, -2.0 * c / HD);
-      double sn, cs;
-      sincos(ang, &sn, &cs);
-      s_cos[c] = cs;
-      s_sin[c] = sn;
-    }
-  }
-  __syncthreads();
-  // queries -> workspace rows (g, gh * T + i)
-  for (int u = threadIdx.x; u < Hq * HALF; u += blockDim.x) {
-    const int h = u / HALF, c = u % HALF;
-    const uint16_t* src = q + (static_cast<size_t>(i) * Hq + h) * HD;
-    uint16_t* dst = qrot + (static_cast<size_t>(h / G) * rows_pad + (h % G) * T + i) * HD;
-    if (rope) {
-      const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
-      dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * s_cos[c] - hi * s_sin[c]));
-      dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * s_cos[c] + lo * s_sin[c]));
-    } else {
-      dst[c] = src[c];
-      dst[c + HALF] = src[c + HALF];
-    }
-  }
-  // keys -> cache slot L + i
-  for (int u = threadIdx.x; u < Hkv * HALF; u += blockDim.x) {
-    const int g = u / HALF, c = u % HALF;
-    const uint16_t* src = kt + (static_cast<size_t>(i) * Hkv + g) * HD;
-    uint16_t* dst = kc + (static_cast<size_t>(g) * cap + L + i) * HD;
-    if (rope) {
-      const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
-      dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * s_cos[c] - hi * s_sin[c]));
-      dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * s_cos[c] + lo * s_sin[c]));
-    } else {
-      dst[c] = src[c];
-      dst[c + HALF] = src[c + HALF];
-    }
-  }
-  // values -> cache slot L + i
-  for (int u = threadIdx.x; u < Hkv * (HD / 8); u += blockDim.x) {
-    const int g = u / (HD / 8), c8 = u % (HD / 8);
+  const int nq = Hq * HALF, nk = Hkv * HALF, nv = Hkv * (HD / 8);
+  if (u >= nq + nk + nv) return;
+  if (u >= nq + nk) {  // value copy -> cache slot L + i
+    const int w = u - nq - nk;
+    const int g = w / (HD / 8), c8 = w % (HD / 8);
     *reinterpret_cast<u32x4*>(vc + (static_cast<size_t>(g) * cap + L + i) * HD + 8 * c8) =
         *reinterpret_cast<const u32x4*>(vt + (static_cast<size_t>(i) * Hkv + g) * HD + 8 * c8);
+    return;
+  }
+  const bool is_q = u < nq;
+  const int w = is_q ? u : u - nq;
+  const int head = w / HALF, c = w % HALF;
+  const uint16_t* src = (is_q ? q + (static_cast<size_t>(i) * Hq + head) * HD
+                              : kt + (static_cast<size_t>(i) * Hkv + head) * HD);
+  uint16_t* dst = is_q ? qrot + (static_cast<size_t>(head / G) * rows_pad + (head % G) * T + i) * HD
+                       : kc + (static_cast<size_t>(head) * cap + L + i) * HD;
+  if (theta > 0.0) {
+    // position prefix_len + depth(i), pair (c, c + d/2) turned by pos * theta^(-2c/d)
+    const double pos = static_cast<double>(L) + static_cast<double>(depth[i]);
+    const double ang = pos * pow(theta, -2.0 * c / HD);
+    double sn, cs;
+    sincos(ang, &sn, &cs);
+    const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
+    dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * cs - hi * sn));
+    dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * cs + lo * sn));
+  } else {
+    dst[c] = src[c];
+    dst[c + HALF] = src[c + HALF];
   }
 }
 
@@ -379,6 +365,18 @@ int split_bound(int nblocks) {
   return b > kMaxSplits ? kMaxSplits : b;
 }
 
+int device_cus() {
+  static int cus[64] = {0};
+  int dev = 0;
+  if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return 256;
+  if (cus[dev] == 0) {
+    int n = 0;
+    if (hipDeviceGetAttribute(&n, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess || n <= 0) n = 256;
+    cus[dev] = n;
+  }
+  return cus[dev];
+}
+
 Plan make_plan(int T, int Hq, int Hkv, int L) {
   Plan pl{};
   pl.G = Hq / Hkv;
@@ -386,10 +384,24 @@ Plan make_plan(int T, int Hq, int Hkv, int L) {
   pl.nqt = pl.rows_pad / kQTile;
   pl.nblocks = (L + T + KB - 1) / KB;
   const int bound = split_bound(pl.nblocks);
-  // aim for about two workgroups per CU
-  int want = (512 + Hkv * pl.nqt - 1) / (Hkv * pl.nqt);
-  want = want < 1 ? 1 : want;
-  pl.nsplit = want < bound ? want : bound;
+  // One workgroup fits per CU.  Pick the split count so that the workgroups
+  // fill the CUs in whole rounds: the first count (1..bound) whose last round
+  // is at least 90% full, else the best one seen.
+  const int cus = device_cus();
+  const int base = Hkv * pl.nqt;
+  int best = 1;
+  double best_eff = 0.0;
+  for (int ns = 1; ns <= bound; ++ns) {
+    const int wg = base * ns;
+    const int rounds = (wg + cus - 1) / cus;
+    const double eff = static_cast<double>(wg) / (static_cast<double>(rounds) * cus);
+    if (eff > best_eff + 1e-9) {
+      best_eff = eff;
+      best = ns;
+    }
+    if (eff >= 0.9) break;
+  }
+  pl.nsplit = best;
   pl.bps = (pl.nblocks + pl.nsplit - 1) / pl.nsplit;
   pl.nsplit = (pl.nblocks + pl.bps - 1) / pl.bps;
   pl.q_bytes = static_cast<size_t>(Hkv) * pl.rows_pad * HD * 2;
@@ -459,8 +471,9 @@ extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const
   float* part_ml = reinterpret_cast<float*>(ws + al(pl.q_bytes) + al(po));
   auto s = static_cast<hipStream_t>(stream);
 
-  hipLaunchKernelGGL(attn_prep_kernel, dim3(T), dim3(256), 0, s, q, k_tree, v_tree, k_cache,
-                     v_cache, qrot, bank_ptr<int>(bank, td.off_depth), T, Hq, Hkv, cap,
+  const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
+  hipLaunchKernelGGL(attn_prep_kernel, dim3(T, (prep_items + 255) / 256), dim3(256), 0, s, q, k_tree,
+                     v_tree, k_cache, v_cache, qrot, bank_ptr<int>(bank, td.off_depth), T, Hq, Hkv, cap,
                      prefix_len, static_cast<double>(rope_theta), pl.rows_pad);
   if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
 

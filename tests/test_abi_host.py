@@ -99,6 +99,21 @@ def test_kernel_calls_reject_bad_arguments_without_launching():
     assert lib.entmtp_kv_compact(p, 0, p, 10, p, p, 1, 0, 32, 100, 128, None) == api.EINVAL
     assert lib.entmtp_kv_compact(p, 5, p, -1, p, p, 1, 0, 32, 100, 128, None) == api.EINVAL
     assert lib.entmtp_kv_compact(p, 5, p, 10, p, p, 2, 5, 32, 100, 128, None) == api.EINVAL
+    # fused LM head + statistics and its two halves
+    assert lib.entmtp_verify_logits_stats(p, p, 27, 4100, 32000, 1.0, p, p, p, p, p, 1 << 20,
+                                          None) == api.EINVAL
+    assert lib.entmtp_verify_logits_partials(p, p, 27, 264, 32000, 1.0, p, p, 1 << 20,
+                                             None) == api.EINVAL
+    assert lib.entmtp_verify_logits_partials(p, p, 27, 4096, 32000, 0.0, p, p, 1 << 20,
+                                             None) == api.EINVAL
+    assert lib.entmtp_verify_logits_partials(p, p, 27, 4096, 32000, 1.0, p, p, 16,
+                                             None) == api.ENOSPC
+    assert lib.entmtp_stats_finalize(None, 27, 32000, 1.0, p, p, p, None) == api.EINVAL
+    assert lib.entmtp_stats_finalize(p, 27, 32000, float("inf"), p, p, p, None) == api.EINVAL
+    assert api.stats_partials_bytes(27, 264, 32000) == 0
+    assert api.stats_partials_bytes(27, 4096, 32000) >= 27 * 256 * 16
+    assert api.verify_logits_stats_workspace(27, 264, 32000) > 0
+    assert api.verify_logits_stats_workspace(27, 4096, 32000) == api.stats_partials_bytes(27, 4096, 32000)
     # workspace query
     assert api.tree_attn_workspace(27, 32, 32, 64, 256) == 0
     assert api.tree_attn_workspace(27, 30, 8, 128, 256) == 0

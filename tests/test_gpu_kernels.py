@@ -143,6 +143,74 @@ def test_logit_stats_on_margin_logits(api, w7b):
     check_stats(run_stats(api, z32), orc.logit_stats(z32))
 
 
+def run_fused(api, X, W, inv_temp=1.0):
+    T, hid = X.shape
+    V = W.shape[0]
+    logits = torch.full((T, V), float("nan"), device="cuda")
+    H = torch.empty(T, device="cuda")
+    p1 = torch.empty(T, device="cuda")
+    am = torch.empty(T, dtype=torch.int32, device="cuda")
+    ws = torch.empty(max(16, api.verify_logits_stats_workspace(T, hid, V)), dtype=torch.uint8,
+                     device="cuda")
+    api.verify_logits_stats(dev_bf16(X), dev_bf16(W), logits, inv_temp, H, p1, am, ws)
+    return logits.cpu().numpy(), (H.cpu().numpy(), p1.cpu().numpy(), am.cpu().numpy())
+
+
+@pytest.mark.parametrize("T,hid,V", [(1, 512, 1), (3, 512, 63), (16, 1024, 4097), (27, 4096, 32000),
+                                     (33, 512, 1000), (64, 512, 777), (128, 4096, 32000),
+                                     (129, 512, 260), (7, 264, 301), (300, 2048, 100)])
+def test_verify_logits_stats_fused(api, T, hid, V):
+    say("verify_logits_stats", T, hid, V)
+    X = random_bits((T, hid), 11)
+    W = random_bits((V, hid), 12, 0.05)
+    ref = orc.verify_logits(X, W)
+    for it in (1.0, 1 / 0.7):
+        z, st = run_fused(api, X, W, it)
+        assert np.abs(z - ref).max() <= 1e-4 * max(1.0, np.abs(ref).max())
+        # statistics on the kernel's own fp32 logits must match the oracle's
+        # statistics of its fp32-rounded logits: identical argmax when the
+        # top-2 gap exceeds the fp32 accumulation error, stats within the bar
+        H, p1, am = st
+        rH, rp1, ram = orc.logit_stats(ref.astype(np.float32), it)
+        gap = np.sort(ref, axis=1)
+        safe = (gap[:, -1] - gap[:, -2]) > 1e-4 if V > 1 else np.ones(T, bool)
+        np.testing.assert_array_equal(am[safe], ram[safe])
+        assert np.all(np.abs(H - rH) <= RTOL_STATS * np.abs(rH) + 1e-6), (H, rH)
+        assert np.all(np.abs(p1 - rp1) <= RTOL_STATS * np.abs(rp1) + 1e-6), (p1, rp1)
+
+
+@pytest.mark.parametrize("T,V", [(1, 32000), (27, 32000), (64, 4097), (200, 1000)])
+def test_verify_logits_partials_then_finalize_equals_fused(api, T, V):
+    say("verify_logits_partials + stats_finalize", T, V)
+    hid = 1024
+    X = dev_bf16(random_bits((T, hid), 21))
+    W = dev_bf16(random_bits((V, hid), 22, 0.05))
+    ws = torch.empty(api.stats_partials_bytes(T, hid, V), dtype=torch.uint8, device="cuda")
+    out = []
+    for split in (False, True):
+        z = torch.full((T, V), float("nan"), device="cuda")
+        H, p1 = torch.empty(T, device="cuda"), torch.empty(T, device="cuda")
+        am = torch.empty(T, dtype=torch.int32, device="cuda")
+        if split:
+            api.verify_logits_partials(X, W, z, 1 / 0.7, ws)
+            api.stats_finalize(ws, T, V, 1 / 0.7, H, p1, am)
+        else:
+            api.verify_logits_stats(X, W, z, 1 / 0.7, H, p1, am, ws)
+        out.append([t.cpu().numpy() for t in (z, H, p1, am)])
+    for a, b in zip(*out):
+        np.testing.assert_array_equal(a, b)
+
+
+def test_verify_logits_stats_fused_margin_7b(api, w7b):
+    say("verify_logits_stats 7b margin rows")
+    X = margin_hidden(1, 27, w7b)
+    z, (H, p1, am) = run_fused(api, X, w7b)
+    rH, rp1, ram = orc.logit_stats(orc.verify_logits(X, w7b).astype(np.float32))
+    np.testing.assert_array_equal(am, ram)
+    assert np.all(np.abs(H - rH) <= RTOL_STATS * np.abs(rH) + 1e-6)
+    assert np.all(np.abs(p1 - rp1) <= RTOL_STATS * np.abs(rp1) + 1e-6)
+
+
 # ------------------------------------------------------------------ accept --
 
 def run_accept(api, bank, topo, tok, am, p1=None):

@@ -1,0 +1,200 @@
+"""GPU: the step driver (entmtp_step_*) in a closed decode loop.
+
+The driver chains the kernels that the other GPU tests check one at a time.
+Here a loop runs as a decoder would: the ladder picks each tree from the
+previous step's s, and the prefix grows by the accepted tokens.  Every step is
+replayed from the GPU's state before it, (1) on the oracle (open-loop replay
+of the GPU's tree sequence, so a near-threshold s cannot split the two runs)
+and (2) through the individual entry points, which must agree bit for bit.
+"""
+import math
+
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import entmtp_oracle as orc  # noqa: E402
+from paper_2606_27550_amd import synth  # noqa: E402
+from tests.helpers import dev_bf16, dev_i32, host_bits, margin_hidden  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+WL = 77
+ATOL_BF16 = 2e-2
+RTOL_STATS = 1e-3
+W_STD = 0.05
+
+
+@pytest.fixture(scope="module")
+def api():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_27550_amd import api as _api
+    return _api
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+def bank_trees():
+    return [[-1], synth.uniform_attach_tree(WL, 8, 3), synth.uniform_attach_tree(WL + 1, 26, 4),
+            synth.uniform_attach_tree(WL + 2, 64, 5)]
+
+
+def step_inputs(t, n_layers, Tmax, Hq, Hkv, d, w_bits, w64, delta, spike):
+    layers = [synth.attn_inputs(WL, Tmax, Hq, Hkv, d, 0, Tmax, step=t + 1, layer=l)
+              for l in range(n_layers)]
+    x = margin_hidden(WL, Tmax, w_bits, step=t + 1, w64=w64, spikes=(delta, spike), w_std=W_STD)
+    am = (orc.bf16_to_f64(x) @ w64.T).argmax(axis=1)
+    u, r = synth.draft_randoms(WL, Tmax, w_bits.shape[0], step=t + 1)
+    return layers, x, am, u, r
+
+
+def stack(layers, name):
+    return np.ascontiguousarray(np.stack([getattr(a, name) for a in layers]))
+
+
+def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_rung=0):
+    d, theta = 128, 10000.0
+    scale = 1 / math.sqrt(d)
+    trees = bank_trees()
+    bank = api.Bank(trees)
+    Tmax, Dmax = max(bank.T), max(bank.D)
+    cap = L0 + n_steps * (Dmax + 1) + Tmax + 8
+    w_bits = synth.lm_head_weight(WL, V, hid, std=W_STD)
+    w64 = orc.bf16_to_f64(w_bits)
+    W = dev_bf16(w_bits)
+    base = [synth.attn_inputs(WL, 1, Hq, Hkv, d, L0, cap, layer=l) for l in range(n_layers)]
+    kc = dev_bf16(stack(base, "k_cache"))          # [layers][Hkv][cap][d]
+    vc = dev_bf16(stack(base, "v_cache"))
+    kc2, vc2 = kc.clone(), vc.clone()              # the entry-point replay's own cache
+    stride = Hkv * cap * d
+    st = api.Step(bank, kc, vc, W, n_layers=n_layers, Hq=Hq, Hkv=Hkv, d=d, cap=cap,
+                  tree_rows=Tmax, scale=scale, rope_theta=theta, cache_layer_stride=stride)
+    deltas, spikes = synth.regime_spikes(WL, n_steps, Tmax, V, hid)
+
+    # entry-point replay buffers
+    out2 = torch.empty((n_layers, Tmax, Hq, d), dtype=torch.bfloat16, device="cuda")
+    lg2 = torch.empty((Tmax, V), device="cuda")
+    H2, p12 = torch.empty(Tmax, device="cuda"), torch.empty(Tmax, device="cuda")
+    am2 = torch.empty(Tmax, dtype=torch.int32, device="cuda")
+    a2, b2 = torch.zeros(1, dtype=torch.int32, device="cuda"), torch.zeros(1, dtype=torch.int32, device="cuda")
+    s2 = torch.zeros(1, device="cuda")
+    path2 = torch.full((Dmax + 1,), -1, dtype=torch.int32, device="cuda")
+    aws = torch.empty(api.tree_attn_workspace(Tmax, Hq, Hkv, d, cap), dtype=torch.uint8, device="cuda")
+    lws = torch.empty(api.verify_logits_stats_workspace(Tmax, hid, V), dtype=torch.uint8, device="cuda")
+
+    L, rung, topo_trace, switches = L0, start_rung, [], 0
+    for t in range(n_steps):
+        T, parent = bank.T[rung], trees[rung]
+        layers, x, am, u, r = step_inputs(t, n_layers, Tmax, Hq, Hkv, d, w_bits, w64,
+                                          float(deltas[t]), spikes[t])
+        tok = synth.draft_tokens(parent, am, u, r, 0.7)
+        q, kt, vt = (dev_bf16(stack(layers, n)) for n in ("q", "k_tree", "v_tree"))
+        X, tok_d = dev_bf16(x), dev_i32(tok)
+        out = torch.full((n_layers, Tmax, Hq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
+        kc_before, vc_before = host_bits(kc), host_bits(vc)
+        say(f"step {t}: layers {n_layers} topo {rung} T {T} L {L}")
+
+        st.launch(rung, L, q, kt, vt, out, X, tok_d)
+        a, bonus, s = st.wait(timeout_s=60.0)
+        torch.cuda.synchronize()
+
+        # (2) the same step through the individual entry points, bit for bit
+        for l in range(n_layers):
+            api.tree_attn(bank, rung, q[l, :T], kt[l, :T], vt[l, :T], kc2[l], vc2[l], L, scale,
+                          theta, out2[l, :T], aws)
+        api.verify_logits_stats(X[:T], W, lg2[:T], 1.0, H2[:T], p12[:T], am2[:T], lws)
+        api.accept(bank, rung, tok_d, am2, p12, a2, path2, b2, s2)
+        api.kv_compact(path2, a2, L, kc2, vc2)
+        torch.cuda.synchronize()
+        for mine, theirs in ((out[:, :T], out2[:, :T]), (st.logits[:T], lg2[:T]),
+                             (st.entropy[:T], H2[:T]), (st.top1p[:T], p12[:T]),
+                             (st.argmax[:T], am2[:T]), (st.path, path2), (kc, kc2), (vc, vc2)):
+            assert torch.equal(mine.view(torch.int16) if mine.dtype == torch.bfloat16 else mine,
+                               theirs.view(torch.int16) if theirs.dtype == torch.bfloat16 else theirs)
+        assert (a, bonus) == (int(a2.item()), int(b2.item()))
+        assert np.float32(s) == np.float32(s2.item())
+        assert a == int(st.accept_len.item()) and bonus == int(st.bonus.item())
+
+        # (1) the oracle from the GPU's state before the step
+        ref = orc.verify_step(parent, layers[0].q[:T], layers[0].k_tree[:T], layers[0].v_tree[:T],
+                              kc_before[0], vc_before[0], L, x[:T], w_bits, tok, scale, theta)
+        assert np.abs(out[0, :T].float().cpu().numpy() - ref["out"]).max() <= ATOL_BF16
+        assert np.abs(st.logits[:T].cpu().numpy() - ref["logits"]).max() <= ATOL_BF16
+        np.testing.assert_array_equal(st.argmax[:T].cpu().numpy(), ref["argmax"])
+        np.testing.assert_allclose(st.entropy[:T].cpu().numpy(), ref["entropy"], rtol=RTOL_STATS,
+                                   atol=1e-6)
+        np.testing.assert_allclose(st.top1p[:T].cpu().numpy(), ref["top1p"], rtol=RTOL_STATS,
+                                   atol=1e-6)
+        assert (a, bonus) == (ref["accept_len"], ref["bonus"])
+        assert st.path.cpu().numpy()[: a + 1].tolist() == list(ref["path"])
+        assert abs(s - ref["s"]) <= RTOL_STATS * ref["s"] + 1e-6
+        kc_now, vc_now = host_bits(kc), host_bits(vc)
+        n = L + a + 1
+        for l in range(n_layers):
+            if l == 0:
+                rk, rv = ref["k_cache"], ref["v_cache"]
+            else:   # other layers: their own attention append, then the same path
+                _, rk, rv = orc.tree_attention(layers[l].q[:T], layers[l].k_tree[:T],
+                                               layers[l].v_tree[:T], kc_before[l], vc_before[l], L,
+                                               parent, scale, theta)
+                rk, rv = orc.kv_compact(rk, rv, L, ref["path"])
+            np.testing.assert_array_equal(kc_now[l][:, :n], rk[:, :n])
+            np.testing.assert_array_equal(vc_now[l][:, :n], rv[:, :n])
+
+        topo_trace.append(rung)
+        L += a + 1
+        nxt = api.ladder_next(rung, len(trees), s, 0.8, 0.6)
+        switches += nxt != rung
+        rung = nxt
+    st.close()
+    return topo_trace, switches
+
+
+def test_step_closed_loop_one_layer(api):
+    trace, switches = run_loop(api, n_layers=1, n_steps=14)
+    say("topology trace", trace)
+    assert switches >= 2 and len(set(trace)) >= 3   # the loop really moved along the ladder
+
+
+def test_step_closed_loop_three_layers(api):
+    trace, _ = run_loop(api, n_layers=3, n_steps=4, start_rung=3)   # starts on the largest tree
+    assert trace[0] == 3
+
+
+def test_step_errors(api):
+    bank = api.Bank(bank_trees())
+    Hq, Hkv, d, hid, V, cap = 4, 4, 128, 512, 300, 80
+    kc = torch.zeros((Hkv, cap, d), dtype=torch.bfloat16, device="cuda")
+    vc = torch.zeros_like(kc)
+    W = torch.zeros((V, hid), dtype=torch.bfloat16, device="cuda")
+    with pytest.raises(api.EntmtpError) as e:       # tree_rows below the largest tree
+        api.Step(bank, kc, vc, W, Hq=Hq, Hkv=Hkv, cap=cap, tree_rows=63, scale=0.1, rope_theta=0.0)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.EntmtpError) as e:       # hidden size without the fused path
+        api.Step(bank, kc, vc, torch.zeros((V, 264), dtype=torch.bfloat16, device="cuda"), Hq=Hq,
+                 Hkv=Hkv, cap=cap, tree_rows=64, scale=0.1, rope_theta=0.0)
+    assert e.value.code == api.EINVAL
+    st = api.Step(bank, kc, vc, W, Hq=Hq, Hkv=Hkv, cap=cap, tree_rows=64, scale=0.1, rope_theta=0.0)
+    q = torch.zeros((64, Hq, d), dtype=torch.bfloat16, device="cuda")
+    kv = torch.zeros((64, Hkv, d), dtype=torch.bfloat16, device="cuda")
+    X = torch.zeros((64, hid), dtype=torch.bfloat16, device="cuda")
+    tok = torch.zeros(64, dtype=torch.int32, device="cuda")
+    with pytest.raises(api.EntmtpError) as e:       # prefix + T beyond the cache
+        st.launch(3, cap - 63, q, kv, kv, q.clone(), X, tok)
+    assert e.value.code == api.ERANGE
+    with pytest.raises(api.EntmtpError) as e:       # nothing in flight to wait for
+        st.wait(timeout_s=0.1)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.EntmtpError) as e:
+        st.launch(len(bank), 0, q, kv, kv, q.clone(), X, tok)
+    assert e.value.code == api.EINVAL
+    st.launch(3, cap - 64, q, kv, kv, q.clone(), X, tok)   # the largest valid prefix
+    a, bonus, s = st.wait(timeout_s=60.0)
+    torch.cuda.synchronize()
+    # all-zero logits: uniform distribution, argmax 0; zero drafts match it
+    assert bonus == 0 and abs(s - 1.0 / V) <= 1e-6 and a == bank.D[3]
+    st.close()
