@@ -140,7 +140,9 @@ size_t entmtp_tree_attn_workspace(int32_t T, int32_t Hq, int32_t Hkv, int32_t d,
  *   k_cache, v_cache  [Hkv][cap][d] bf16: one layer's cache; slots
  *            [0, prefix_len) hold the prefix (keys already rotated).
  *   out      [T][Hq][d] bf16.
- *   workspace  device scratch of at least entmtp_tree_attn_workspace() bytes.
+ *   workspace  device scratch of at least entmtp_tree_attn_workspace() bytes;
+ *            it holds the rotated queries and split partials of one call, so
+ *            calls that share a workspace must be ordered, never concurrent.
  *
  * The call writes the tree's keys and values into cache slots
  * [prefix_len, prefix_len + T) and computes, for node i and query head h
@@ -186,8 +188,10 @@ int32_t entmtp_verify_logits(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
  * softmax partials (largest raw logit with its lowest index, and the sums
  * sum e^(y-m), sum (y-m) e^(y-m) for y = inv_temp * z), which a small kernel
  * then combines per node, so the logits are not read back.  Outputs and their
- * meaning are those of the two separate calls (logits [T][V] fp32 is still
- * written; entropy / top1p / argmax may each be NULL).
+ * meaning are those of the two separate calls (entropy / top1p / argmax may
+ * each be NULL; logits [T][V] fp32 is written unless it is NULL, which is
+ * allowed when hid is a multiple of 512 -- the statistics then come from the
+ * accumulators alone and no logits reach memory).
  *   workspace   device scratch of at least
  *               entmtp_verify_logits_stats_workspace(T, hid, V) bytes, 16-byte
  *               aligned (partials, overwritten by every call).
@@ -207,6 +211,7 @@ int32_t entmtp_verify_logits_stats(const entmtp_bf16* hidden, const entmtp_bf16*
  *   partials   device buffer of entmtp_stats_partials_bytes(T, hid, V) bytes,
  *              16-byte aligned; written by the first call, read by the second
  *              (same device, same V).
+ *   logits     may be NULL (statistics only).
  */
 size_t entmtp_stats_partials_bytes(int32_t T, int32_t hid, int32_t V);
 int32_t entmtp_verify_logits_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
@@ -311,12 +316,18 @@ int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
  *              at least the largest T in the bank
  *   w_lm, hid, V, inv_temp   the LM head and the statistics temperature as for
  *              entmtp_verify_logits_stats (hid a multiple of 512)
- *   logits [tree_rows][V] fp32; entropy, top1p [tree_rows] fp32;
- *   argmax [tree_rows] int32   outputs of the LM head and statistics
+ *   logits [tree_rows][V] fp32, or NULL to keep no logits (the statistics
+ *              and acceptance do not need them); entropy, top1p [tree_rows]
+ *              fp32; argmax [tree_rows] int32   outputs of the LM head and
+ *              statistics
  *   accept_len [1], bonus [1] int32, best_top1p [1] fp32, path [path_capacity]
  *              int32 (path_capacity >= 1 + the largest depth in the bank)
  *              outputs of acceptance, as for entmtp_accept
- *   workspace  scratch of entmtp_step_workspace() bytes, 256-byte aligned
+ *   workspace  scratch of entmtp_step_workspace() bytes, 256-byte aligned,
+ *              used by this step object only (it holds attention partials,
+ *              statistics partials and an arrival counter that
+ *              entmtp_step_create clears with an asynchronous memset on the
+ *              stream)
  *   stream     the HIP stream every launch goes to (NULL: the null stream)
  */
 typedef struct entmtp_step_config {
@@ -359,12 +370,18 @@ void entmtp_step_destroy(entmtp_step* step);
 
 /*
  * Enqueues one verification step for tree `topo` at prefix length prefix_len,
- * asynchronously on the configured stream:
- *   for each layer  entmtp_tree_attn (writes K/V slots [L, L+T) of the layer)
- *   the LM head with fused statistics partials, then their merge
- *   greedy acceptance, which also publishes (accept_len, bonus, best_top1p)
- *   to host memory
- *   compaction of the accepted path in every layer
+ * asynchronously:
+ *   for each layer  entmtp_tree_attn (writes K/V slots [L, L+T) of the layer),
+ *                   on a side stream the step object owns, forked from the
+ *                   configured stream
+ *   the LM head with fused statistics partials, on the configured stream,
+ *   concurrently with the attention layers
+ *   the statistics merge and greedy acceptance, in one launch; acceptance
+ *   also publishes (accept_len, bonus, best_top1p) to host memory
+ *   compaction of the accepted path in every layer, after the side stream
+ *   has joined the configured stream
+ * Every output is complete once the configured stream is; work enqueued on
+ * that stream afterwards is ordered after the whole step.
  * Per-step inputs (device): q, k_tree, v_tree, out laid out with tree_rows
  * rows per layer; hidden [T][hid] bf16; draft_tokens [T] int32.
  * ev_lm_begin / ev_lm_end: optional hipEvent_t recorded on the stream right
@@ -381,8 +398,9 @@ int32_t entmtp_step_launch(entmtp_step* step, int32_t topo, int32_t prefix_len,
 
 /*
  * Waits for the acceptance result of the latest entmtp_step_launch by polling
- * the pinned host record (no stream synchronisation; the compaction may still
- * be running and later work on the stream stays ordered after it).  Writes
+ * the pinned host record (no stream synchronisation: attention and compaction
+ * may still be running, and later work on the stream stays ordered after
+ * them).  Writes
  * the accepted draft count, the bonus token and the top-1 probability at the
  * accepted node (the scheduler's s, §4) to the host pointers given (each may
  * be NULL).  Gives up after timeout_s seconds with ETIMEDOUT, or earlier with

@@ -393,12 +393,13 @@ class Step:
 
     def __init__(self, bank: Bank, k_cache, v_cache, w_lm, *, n_layers=1, Hq, Hkv, d=HEAD_DIM,
                  cap, tree_rows, scale, rope_theta, inv_temp=1.0, cache_layer_stride=0,
-                 stream=None):
+                 keep_logits=True, stream=None):
         import torch
         dev = k_cache.device
         V, hid = w_lm.shape
         D = max(bank.D)
-        self.logits = torch.empty((tree_rows, V), dtype=torch.float32, device=dev)
+        self.logits = (torch.empty((tree_rows, V), dtype=torch.float32, device=dev) if keep_logits
+                       else None)
         self.entropy = torch.empty(tree_rows, dtype=torch.float32, device=dev)
         self.top1p = torch.empty(tree_rows, dtype=torch.float32, device=dev)
         self.argmax = torch.empty(tree_rows, dtype=torch.int32, device=dev)
@@ -412,7 +413,8 @@ class Step:
         self._keep = (bank, k_cache, v_cache, w_lm)
         c = StepConfig(n_layers, Hq, Hkv, d, cap, tree_rows, scale, rope_theta,
                        k_cache.data_ptr(), v_cache.data_ptr(), cache_layer_stride, w_lm.data_ptr(),
-                       hid, V, inv_temp, self.logits.data_ptr(), self.entropy.data_ptr(),
+                       hid, V, inv_temp, None if self.logits is None else self.logits.data_ptr(),
+                       self.entropy.data_ptr(),
                        self.top1p.data_ptr(), self.argmax.data_ptr(), self.accept_len.data_ptr(),
                        self.bonus.data_ptr(), self.best_top1p.data_ptr(), self.path.data_ptr(),
                        D + 1, None, 0, _stream(stream).value)

@@ -7,15 +7,20 @@
 // accepted" becomes a subset test of the node's mask row against the set of
 // locally matching nodes, so all nodes are decided in parallel.  The answer is
 // the deepest accepted node, lowest index among equals; its depth is the
-// accept length (§5.1).  One workgroup handles the whole tree.
+// accept length (§5.1).  One workgroup handles the whole tree.  Inside a
+// verification step the acceptance runs fused behind the statistics: the
+// last of the tree's per-node statistics blocks to finish accepts the tree.
 #include "common.hpp"
+#include "stats.hpp"
 
 namespace entmtp {
 namespace {
 
 constexpr int kAcceptThreads = ENTMTP_T_MAX;
+static_assert(kAcceptThreads == kFinThreads, "the fused kernel runs both halves with one block size");
 
-__global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
+// The acceptance of one tree by one workgroup of kAcceptThreads threads.
+__device__ __forceinline__ void accept_core(
     const int* __restrict__ parent, const int* __restrict__ depth,
     const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
     const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
@@ -66,6 +71,44 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
   }
 }
 
+__global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
+    const int* __restrict__ parent, const int* __restrict__ depth,
+    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
+    const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
+    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
+    float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
+  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, bonus,
+              best_p, mirror, seq);
+}
+
+// Statistics of node blockIdx.x from the LM head's partials, then -- in the
+// last block to finish, once every node's statistics are visible -- the
+// acceptance of the tree.  `counter` is 0 on entry and left 0 on exit.
+__global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
+    const StatPart* __restrict__ part, int G, float inv_temp, float* __restrict__ entropy,
+    float* __restrict__ top1p, int* __restrict__ amax, unsigned* __restrict__ counter,
+    const int* __restrict__ parent, const int* __restrict__ depth,
+    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
+    const int* __restrict__ tok, int* __restrict__ accept_len, int* __restrict__ path_out,
+    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
+    uint32_t seq) {
+  finalize_node(part, G, inv_temp, entropy, top1p, amax);
+  if (T > 1) {
+    __shared__ int s_last;
+    __threadfence();   // this node's statistics are visible device-wide ...
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = atomicAdd(counter, 1u) == static_cast<unsigned>(T - 1);
+    __syncthreads();   // ... before its arrival is counted
+    if (!s_last) return;
+    __threadfence();   // the last block sees every node's statistics
+    if (threadIdx.x == 0) *counter = 0u;
+  } else {
+    __syncthreads();   // a single block: its own statistics, via LDS ordering
+  }
+  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, bonus,
+              best_p, mirror, seq);
+}
+
 }  // namespace
 }  // namespace entmtp
 
@@ -84,6 +127,22 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
                      d.D, draft_tokens, argmax, top1p, accept_len, path, bonus, best_top1p,
                      mirror, seq);
   return launch_status("accept launch");
+}
+
+int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,
+                               int32_t V, float inv_temp, float* entropy, float* top1p,
+                               int32_t* argmax, unsigned* counter, const int32_t* draft_tokens,
+                               int32_t* accept_len, int32_t* path, int32_t* bonus,
+                               float* best_top1p, StepMirror* mirror, uint32_t seq,
+                               hipStream_t stream) {
+  const TopoDesc& d = bank->desc[topo];
+  hipLaunchKernelGGL(finalize_accept_kernel, dim3(d.T), dim3(kAcceptThreads), 0, stream,
+                     static_cast<const StatPart*>(partials), stats_slices(V), inv_temp, entropy,
+                     top1p, argmax, counter, bank_ptr<int>(bank, d.off_parent),
+                     bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
+                     bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, accept_len, path,
+                     bonus, best_top1p, mirror, seq);
+  return launch_status("finalize_accept launch");
 }
 
 }  // namespace entmtp

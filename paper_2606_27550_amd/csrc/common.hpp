@@ -74,6 +74,16 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
                       int32_t* path, int32_t* bonus, float* best_top1p, StepMirror* mirror,
                       uint32_t seq, hipStream_t stream);
 
+// Finishes the LM head's statistics partials for every node of tree `topo`
+// and, in the same launch, accepts the tree (as launch_accept).  `counter`
+// is one device word, 0 before the launch and 0 after it.
+int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,
+                               int32_t V, float inv_temp, float* entropy, float* top1p,
+                               int32_t* argmax, unsigned* counter, const int32_t* draft_tokens,
+                               int32_t* accept_len, int32_t* path, int32_t* bonus,
+                               float* best_top1p, StepMirror* mirror, uint32_t seq,
+                               hipStream_t stream);
+
 template <typename T>
 inline const T* bank_ptr(const entmtp_bank* b, int64_t off) {
   return reinterpret_cast<const T*>(b->arena + off);

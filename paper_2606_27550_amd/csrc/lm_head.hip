@@ -26,6 +26,7 @@
 #include <type_traits>
 
 #include "common.hpp"
+#include "stats.hpp"
 
 namespace entmtp {
 namespace {
@@ -379,43 +380,6 @@ __global__ __launch_bounds__(kL3Threads) void lm_head_lds_kernel(
 // vocabulary slice combine into the row's entropy ln Z - S/Z, top-1
 // probability 1/Z and argmax.
 // ---------------------------------------------------------------------------
-struct StatPart {
-  float zmax, Z, S;
-  int idx;
-};
-
-__device__ __forceinline__ void take_max(float& zm, int& zi, float z2, int i2) {
-  if (z2 > zm || (z2 == zm && i2 < zi)) {
-    zm = z2;
-    zi = i2;
-  }
-}
-
-__device__ __forceinline__ void part_merge(StatPart& a, const StatPart& b, float inv_temp) {
-  float zm = a.zmax;
-  int zi = a.idx;
-  take_max(zm, zi, b.zmax, b.idx);
-  if (zm == -INFINITY) return;   // both empty
-  const float my = zm * inv_temp;
-  float Z = 0.f, S = 0.f;
-  if (a.zmax != -INFINITY) {
-    const float ma = a.zmax * inv_temp, f = expf(ma - my);
-    Z += a.Z * f;
-    S += f * (a.S + (ma - my) * a.Z);
-  }
-  if (b.zmax != -INFINITY) {
-    const float mb = b.zmax * inv_temp, f = expf(mb - my);
-    Z += b.Z * f;
-    S += f * (b.S + (mb - my) * b.Z);
-  }
-  a = StatPart{zm, Z, S, zi};
-}
-
-__device__ __forceinline__ StatPart shfl_part(const StatPart& p, int off) {
-  return StatPart{__shfl_xor(p.zmax, off, 64), __shfl_xor(p.Z, off, 64), __shfl_xor(p.S, off, 64),
-                  __shfl_xor(p.idx, off, 64)};
-}
-
 constexpr int kHybWaves = 4;                        // 64 rows per workgroup slice
 constexpr int kHybThreads = 64 * kHybWaves;
 
@@ -559,7 +523,7 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
 
   const bool vec_ok = (V & 3) == 0;
   const int v = tile0 + 4 * lg;
-  if (live) {
+  if (live && logits) {   // the statistics path may run without materialised logits
 #pragma unroll
     for (int n = 0; n < NT; ++n) {
       const int node = j0 + n * 16 + lr;
@@ -648,25 +612,10 @@ int device_cus() {
 }
 
 // Combines the G partials of node blockIdx.x into its statistics.
-constexpr int kFinThreads = 256;
 __global__ __launch_bounds__(kFinThreads) void stats_finalize_kernel(
     const StatPart* __restrict__ part, int G, float inv_temp, float* __restrict__ entropy,
     float* __restrict__ top1p, int* __restrict__ argmax) {
-  __shared__ StatPart wsum[kFinThreads / 64];
-  const StatPart* row = part + static_cast<size_t>(blockIdx.x) * G;
-  StatPart p{-INFINITY, 0.f, 0.f, 0x7fffffff};
-  for (int g = threadIdx.x; g < G; g += kFinThreads) part_merge(p, row[g], inv_temp);
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) part_merge(p, shfl_part(p, off), inv_temp);
-  if ((threadIdx.x & 63) == 0) wsum[threadIdx.x >> 6] = p;
-  __syncthreads();
-  if (threadIdx.x == 0) {
-    StatPart a = wsum[0];
-    for (int w = 1; w < kFinThreads / 64; ++w) part_merge(a, wsum[w], inv_temp);
-    if (entropy) entropy[blockIdx.x] = logf(a.Z) - a.S / a.Z;
-    if (top1p) top1p[blockIdx.x] = 1.f / a.Z;
-    if (argmax) argmax[blockIdx.x] = a.idx;
-  }
+  finalize_node(part, G, inv_temp, entropy, top1p, argmax);
 }
 
 // Workgroups of the streaming LM-head grid: slices of at most 64 rows, and a
@@ -750,6 +699,9 @@ int32_t launch_lm(const uint16_t* X, const uint16_t* W, float* logits, int T, in
 }
 
 }  // namespace
+
+int stats_slices(int V) { return hyb_grid(V); }
+
 }  // namespace entmtp
 
 using namespace entmtp;
@@ -789,8 +741,8 @@ extern "C" int32_t entmtp_verify_logits_partials(const entmtp_bf16* hidden, cons
                                                  float* logits, void* partials,
                                                  size_t partials_bytes, void* stream) {
   clear_error();
-  ENTMTP_CHECK_ARG(hidden && w_lm && logits && partials, ENTMTP_EINVAL,
-                   "hidden, w_lm, logits and partials must be non-NULL");
+  ENTMTP_CHECK_ARG(hidden && w_lm && partials, ENTMTP_EINVAL,
+                   "hidden, w_lm and partials must be non-NULL");
   ENTMTP_CHECK_ARG(T >= 1 && T <= 4096, ENTMTP_EINVAL, "T = %d outside [1, 4096]", T);
   ENTMTP_CHECK_ARG(hid >= 4 * kL3Bk && hid % (4 * kL3Bk) == 0, ENTMTP_EINVAL,
                    "hid = %d: the fused path needs a multiple of %d", hid, 4 * kL3Bk);

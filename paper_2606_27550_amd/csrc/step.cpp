@@ -3,11 +3,14 @@
 // The decode loop of §4 verifies the scheduled tree, accepts the longest
 // matching path, updates the cache, and reads one scalar back to the host to
 // pick the next tree ("Cost": a single device-to-host read per step).  The
-// context below validates the fixed sizes once, then each step is a short
-// burst of launches on one stream; the acceptance kernel publishes its result
-// into coherent pinned host memory, and the host polls that record instead of
-// synchronising the stream, so the cache compaction and the host's choice of
-// the next tree overlap.
+// context below validates the fixed sizes once; each step is then a short
+// burst of launches.  Within a step the attention layers and the LM head are
+// independent (the head reads the tree's final hidden states), and only the
+// compaction needs both, so the attention chain runs on a side stream forked
+// from and joined back into the caller's stream, and the two HBM streams
+// overlap.  The acceptance kernel publishes its result into coherent pinned
+// host memory, and the host polls that record instead of synchronising a
+// stream, so the compaction and the host's choice of the next tree overlap.
 #include <chrono>
 #include <cmath>
 #include <cstring>
@@ -24,8 +27,12 @@ struct entmtp_step {
   size_t attn_bytes = 0;       // attention workspace, at the start of cfg.workspace
   size_t part_offset = 0;      // LM-head statistics partials follow it
   size_t part_bytes = 0;
+  size_t counter_offset = 0;   // then one arrival counter (0 between launches)
   StepMirror* host = nullptr;  // pinned, coherent
   StepMirror* dev = nullptr;   // device address of `host`
+  hipStream_t side = nullptr;  // attention chain (default priority, non-blocking)
+  hipEvent_t fork = nullptr;   // caller's stream -> side stream
+  hipEvent_t join = nullptr;   // side stream -> caller's stream
   uint32_t seq = 0;            // sequence number of the latest launch
   bool pending = false;        // a launched step whose result has not been read
 };
@@ -44,12 +51,14 @@ void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
   *D_max = dd;
 }
 
-// Workspace split for a validated configuration.
-void layout(const entmtp_step_config& c, int32_t T_max, size_t* attn, size_t* part_off,
-            size_t* part) {
+// Workspace split for a validated configuration; returns the total bytes.
+size_t layout(const entmtp_step_config& c, int32_t T_max, size_t* attn, size_t* part_off,
+              size_t* part, size_t* counter_off) {
   *attn = entmtp_tree_attn_workspace(T_max, c.Hq, c.Hkv, c.d, c.cap);
   *part_off = round256(*attn);
   *part = entmtp_stats_partials_bytes(T_max, c.hid, c.V);
+  *counter_off = round256(*part_off + *part);
+  return *counter_off + 256;
 }
 
 bool finite_positive(float x) { return x > 0.f && std::isfinite(x); }
@@ -87,8 +96,8 @@ int32_t check_config(const entmtp_bank* bank, const entmtp_step_config* c, int32
   ENTMTP_CHECK_ARG(entmtp_stats_partials_bytes(*T_max, c->hid, c->V) > 0, ENTMTP_EINVAL,
                    "hid = %d: the step needs a multiple of 512", c->hid);
   ENTMTP_CHECK_ARG(finite_positive(c->inv_temp), ENTMTP_EINVAL, "inv_temp must be positive and finite");
-  ENTMTP_CHECK_ARG(c->logits && aligned16(c->logits) && c->entropy && c->top1p && c->argmax,
-                   ENTMTP_EINVAL, "logits (16-byte aligned) and statistics outputs must be non-NULL");
+  ENTMTP_CHECK_ARG(aligned16(c->logits) && c->entropy && c->top1p && c->argmax, ENTMTP_EINVAL,
+                   "statistics outputs must be non-NULL and logits (if any) 16-byte aligned");
   ENTMTP_CHECK_ARG(c->accept_len && c->bonus && c->best_top1p && c->path, ENTMTP_EINVAL,
                    "acceptance outputs must be non-NULL");
   ENTMTP_CHECK_ARG(c->path_capacity >= *D_max + 1, ENTMTP_EINVAL,
@@ -104,9 +113,9 @@ extern "C" size_t entmtp_step_workspace(const entmtp_bank* bank, const entmtp_st
     clear_error();
     return 0;
   }
-  size_t attn = 0, off = 0, part = 0;
-  layout(*cfg, T_max, &attn, &off, &part);
-  return attn && part ? off + part : 0;
+  size_t attn = 0, off = 0, part = 0, coff = 0;
+  const size_t total = layout(*cfg, T_max, &attn, &off, &part, &coff);
+  return attn && part ? total : 0;
 }
 
 extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step_config* cfg,
@@ -116,13 +125,13 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   *out = nullptr;
   int32_t T_max = 0, D_max = 0;
   if (int32_t rc = check_config(bank, cfg, &T_max, &D_max)) return rc;
-  size_t attn = 0, off = 0, part = 0;
-  layout(*cfg, T_max, &attn, &off, &part);
+  size_t attn = 0, off = 0, part = 0, coff = 0;
+  const size_t total = layout(*cfg, T_max, &attn, &off, &part, &coff);
   ENTMTP_CHECK_ARG(attn > 0 && part > 0, ENTMTP_EINVAL, "unsupported attention or LM-head sizes");
   ENTMTP_CHECK_ARG(cfg->workspace && (reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) == 0,
                    ENTMTP_EINVAL, "workspace must be non-NULL and 256-byte aligned");
-  ENTMTP_CHECK_ARG(cfg->workspace_bytes >= off + part, ENTMTP_ENOSPC,
-                   "workspace has %zu bytes, needs %zu", cfg->workspace_bytes, off + part);
+  ENTMTP_CHECK_ARG(cfg->workspace_bytes >= total, ENTMTP_ENOSPC,
+                   "workspace has %zu bytes, needs %zu", cfg->workspace_bytes, total);
   int dev = -1;
   if (int32_t rc = hip_status(hipGetDevice(&dev), "hipGetDevice")) return rc;
   ENTMTP_CHECK_ARG(dev == bank->device, ENTMTP_EINVAL,
@@ -136,6 +145,7 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   st->attn_bytes = attn;
   st->part_offset = off;
   st->part_bytes = part;
+  st->counter_offset = coff;
   void* h = nullptr;
   int32_t rc = hip_status(hipHostMalloc(&h, sizeof(StepMirror), hipHostMallocMapped | hipHostMallocCoherent),
                           "hipHostMalloc (step result record)");
@@ -146,6 +156,16 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
     rc = hip_status(hipHostGetDevicePointer(&d, h, 0), "hipHostGetDevicePointer");
     st->dev = static_cast<StepMirror*>(d);
   }
+  if (rc == ENTMTP_OK)
+    rc = hip_status(hipStreamCreateWithFlags(&st->side, hipStreamNonBlocking), "hipStreamCreate");
+  if (rc == ENTMTP_OK)
+    rc = hip_status(hipEventCreateWithFlags(&st->fork, hipEventDisableTiming), "hipEventCreate");
+  if (rc == ENTMTP_OK)
+    rc = hip_status(hipEventCreateWithFlags(&st->join, hipEventDisableTiming), "hipEventCreate");
+  if (rc == ENTMTP_OK)   // the finalize-accept arrival counter starts at 0 (and stays so between steps)
+    rc = hip_status(hipMemsetAsync(static_cast<uint8_t*>(cfg->workspace) + coff, 0, 256,
+                                   static_cast<hipStream_t>(cfg->stream)),
+                    "hipMemsetAsync (arrival counter)");
   if (rc != ENTMTP_OK) {
     entmtp_step_destroy(st);
     return rc;
@@ -156,6 +176,10 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
 
 extern "C" void entmtp_step_destroy(entmtp_step* st) {
   if (!st) return;
+  if (st->side) (void)hipStreamSynchronize(st->side);
+  if (st->join) (void)hipEventDestroy(st->join);
+  if (st->fork) (void)hipEventDestroy(st->fork);
+  if (st->side) (void)hipStreamDestroy(st->side);
   if (st->host) (void)hipHostFree(st->host);
   delete st;
 }
@@ -179,16 +203,12 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
   uint8_t* ws = static_cast<uint8_t*>(c.workspace);
   void* part = ws + st->part_offset;
 
-  const size_t q_layer = static_cast<size_t>(c.tree_rows) * c.Hq * c.d;
-  const size_t kv_layer = static_cast<size_t>(c.tree_rows) * c.Hkv * c.d;
-  for (int32_t l = 0; l < c.n_layers; ++l) {
-    const size_t cl = static_cast<size_t>(l) * static_cast<size_t>(c.cache_layer_stride);
-    if (int32_t rc = entmtp_tree_attn(st->bank, topo, q + l * q_layer, k_tree + l * kv_layer,
-                                      v_tree + l * kv_layer, c.k_cache + cl, c.v_cache + cl, c.cap,
-                                      prefix_len, c.Hq, c.Hkv, c.d, c.scale, c.rope_theta,
-                                      out + l * q_layer, ws, st->attn_bytes, c.stream))
-      return rc;
-  }
+  // the side stream starts after everything already on the caller's stream
+  // (the previous step's compaction in particular)
+  if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
+
+  // the LM head (the longest kernel) is enqueued first, so that it is running
+  // while the host enqueues the attention chain behind it
   if (ev_lm_begin)
     if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_begin), s),
                                 "hipEventRecord"))
@@ -200,14 +220,31 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
     if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_end), s),
                                 "hipEventRecord"))
       return rc;
-  if (int32_t rc = entmtp_stats_finalize(part, T, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax,
-                                         c.stream))
-    return rc;
   const uint32_t seq = st->seq + 1u;
-  if (int32_t rc = launch_accept(st->bank, topo, draft_tokens, c.argmax, c.top1p, c.accept_len,
-                                 c.path, c.bonus, c.best_top1p, st->dev, seq, s))
+  if (int32_t rc = launch_finalize_accept(
+          st->bank, topo, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax,
+          reinterpret_cast<unsigned*>(ws + st->counter_offset), draft_tokens, c.accept_len, c.path,
+          c.bonus, c.best_top1p, st->dev, seq, s))
     return rc;
   st->seq = seq;
+
+  // attention layers on the side stream, concurrent with the above
+  if (int32_t rc = hip_status(hipStreamWaitEvent(st->side, st->fork, 0), "hipStreamWaitEvent"))
+    return rc;
+  const size_t q_layer = static_cast<size_t>(c.tree_rows) * c.Hq * c.d;
+  const size_t kv_layer = static_cast<size_t>(c.tree_rows) * c.Hkv * c.d;
+  for (int32_t l = 0; l < c.n_layers; ++l) {
+    const size_t cl = static_cast<size_t>(l) * static_cast<size_t>(c.cache_layer_stride);
+    if (int32_t rc = entmtp_tree_attn(st->bank, topo, q + l * q_layer, k_tree + l * kv_layer,
+                                      v_tree + l * kv_layer, c.k_cache + cl, c.v_cache + cl, c.cap,
+                                      prefix_len, c.Hq, c.Hkv, c.d, c.scale, c.rope_theta,
+                                      out + l * q_layer, ws, st->attn_bytes, st->side))
+      return rc;
+  }
+  if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
+
+  // compaction moves rows the attention chain appended
+  if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->join, 0), "hipStreamWaitEvent")) return rc;
   if (int32_t rc = entmtp_kv_compact(c.path, c.path_capacity, c.accept_len, prefix_len, c.k_cache,
                                      c.v_cache, c.n_layers, c.cache_layer_stride, c.Hkv, c.cap, c.d,
                                      c.stream))

@@ -13,7 +13,8 @@
 //     head (GQA: query rows = head-in-group x node).
 //  2. attend: flash-decoding over the cache.  A workgroup owns one
 //     (KV head, 32-query tile, key split); its four waves take interleaved
-//     32-key blocks.  S^T = K Q^T and O^T += V^T P^T run on
+//     32-key blocks, each wave loading its next block while it multiplies the
+//     current one.  S^T = K Q^T and O^T += V^T P^T run on
 //     v_mfma_f32_32x32x16_bf16: K comes from HBM straight into A-operand
 //     registers, V is transposed through a per-wave LDS tile, P never leaves
 //     registers (the S^T accumulator layout is re-read as the B operand of
@@ -164,28 +165,29 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
   const int blk_lo = split * p.bps;
   const int blk_hi = min(nblocks, blk_lo + p.bps);
 
-  for (int blk = blk_lo + wave; blk < blk_hi; blk += kAttnWaves) {
+  // K/V of one block into registers.  Keys past the end are clamped to the
+  // last key (finite data whose probabilities are zero), so every load is
+  // unconditional and the compiler's wait counts stay exact.
+  auto load_kv = [&](int blk, u32x4 (&kf)[8], u32x4 (&va)[4], u32x4 (&vb)[4]) {
     const int kb = blk * KB;
-    // K: A operand, lane (key li, half lh)
-    u32x4 kf[8];
-    {
-      const int key = kb + li;
-      const uint16_t* kp = kbase + static_cast<size_t>(key) * HD + 8 * lh;
+    const int last = p.nkeys - 1;
+    const int key = min(kb + li, last);
+    const uint16_t* kp = kbase + static_cast<size_t>(key) * HD + 8 * lh;
 #pragma unroll
-      for (int s = 0; s < 8; ++s)
-        kf[s] = key < p.nkeys ? *reinterpret_cast<const u32x4*>(kp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
-    }
-    // V: key pairs (2pp, 2pp+1) x 8-dim chunk m, transposed into LDS
-    u32x4 v0[4], v1[4];
+    for (int s = 0; s < 8; ++s) kf[s] = *reinterpret_cast<const u32x4*>(kp + 16 * s);
+    // V: key pairs (2pp, 2pp+1) x 8-dim chunk m
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int u = lane + 64 * k;
       const int pp = u & 15, m = u >> 4;
-      const int key0 = kb + 2 * pp;
-      const uint16_t* vp = vbase + static_cast<size_t>(key0) * HD + 8 * m;
-      v0[k] = key0 < p.nkeys ? *reinterpret_cast<const u32x4*>(vp) : u32x4{0u, 0u, 0u, 0u};
-      v1[k] = key0 + 1 < p.nkeys ? *reinterpret_cast<const u32x4*>(vp + HD) : u32x4{0u, 0u, 0u, 0u};
+      const int k0 = min(kb + 2 * pp, last), k1 = min(kb + 2 * pp + 1, last);
+      va[k] = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k0) * HD + 8 * m);
+      vb[k] = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k1) * HD + 8 * m);
     }
+  };
+
+  auto attend = [&](int blk, const u32x4 (&kf)[8], const u32x4 (&v0)[4], const u32x4 (&v1)[4]) {
+    const int kb = blk * KB;
     wave_lds_sync();  // previous block's V^T reads are done
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -199,7 +201,6 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
         vt[(8 * m + 2 * w + 1) * (VT_LD / 2) + pp] = (a >> 16) | (b & 0xFFFF0000u);
       }
     }
-
     // S^T[key][query] = K Q^T
     f32x16 sacc;
 #pragma unroll
@@ -273,6 +274,25 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
         const u32x4 w = {x0.x, x0.y, x1.x, x1.y};
         o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t], o[ct], 0, 0, 0);
       }
+    }
+  };
+
+  // two-deep pipeline: block b+4 streams in while block b is multiplied (the
+  // load after a wave's last block re-reads that block, an L2 hit)
+  if (blk_lo + wave < blk_hi) {
+    u32x4 kA[8], vA0[4], vA1[4], kB[8], vB0[4], vB1[4];
+    int cur = blk_lo + wave;
+    load_kv(cur, kA, vA0, vA1);
+    while (true) {
+      const int nb = cur + kAttnWaves;
+      load_kv(nb < blk_hi ? nb : cur, kB, vB0, vB1);
+      attend(cur, kA, vA0, vA1);
+      if (nb >= blk_hi) break;
+      const int nb2 = nb + kAttnWaves;
+      load_kv(nb2 < blk_hi ? nb2 : nb, kA, vA0, vA1);
+      attend(nb, kB, vB0, vB1);
+      if (nb2 >= blk_hi) break;
+      cur = nb2;
     }
   }
 
@@ -359,6 +379,8 @@ struct Plan {
   size_t q_bytes, po_bytes, pml_bytes;
 };
 
+size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
 int split_bound(int nblocks) {
   int b = nblocks / kMinBlocksPerSplit;
   b = b < 1 ? 1 : b;
@@ -415,9 +437,8 @@ size_t workspace_bytes(int T, int Hq, int Hkv, int L) {
   const int rows_pad = rows_padded(G, T);
   const int nblocks = (L + T + KB - 1) / KB;
   const size_t bound = split_bound(nblocks);
-  auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
-  return al(static_cast<size_t>(Hkv) * rows_pad * HD * 2) +
-         al(bound * Hkv * rows_pad * HD * 4) + al(bound * Hkv * rows_pad * 2 * 4);
+  return al256(static_cast<size_t>(Hkv) * rows_pad * HD * 2) +
+         al256(bound * Hkv * rows_pad * HD * 4) + al256(bound * Hkv * rows_pad * 2 * 4);
 }
 
 }  // namespace
@@ -463,12 +484,11 @@ extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const
                    ws_bytes, need);
 
   const Plan pl = make_plan(T, Hq, Hkv, prefix_len);
-  auto al = [](size_t x) { return (x + 255) & ~size_t(255); };
   uint8_t* ws = static_cast<uint8_t*>(workspace);
   uint16_t* qrot = reinterpret_cast<uint16_t*>(ws);
-  float* part_o = reinterpret_cast<float*>(ws + al(pl.q_bytes));
   const size_t po = static_cast<size_t>(pl.nsplit) * Hkv * pl.rows_pad * HD * 4;
-  float* part_ml = reinterpret_cast<float*>(ws + al(pl.q_bytes) + al(po));
+  float* part_o = reinterpret_cast<float*>(ws + al256(pl.q_bytes));
+  float* part_ml = reinterpret_cast<float*>(ws + al256(pl.q_bytes) + al256(po));
   auto s = static_cast<hipStream_t>(stream);
 
   const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
