@@ -53,6 +53,7 @@ extern "C" {
 #define ENTMTP_D_MAX      31   /* deepest node (root = depth 0) */
 #define ENTMTP_MASK_WORDS 8    /* uint32 words per mask row (ENTMTP_T_MAX / 32) */
 #define ENTMTP_HEAD_DIM   128  /* the head dimension the attention kernels are built for */
+#define ENTMTP_B_MAX      16   /* sequences per batched call */
 
 typedef uint16_t entmtp_bf16;
 typedef struct entmtp_bank entmtp_bank;
@@ -164,6 +165,33 @@ int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const entmtp_bf1
                          float scale, float rope_theta, entmtp_bf16* out,
                          void* workspace, size_t workspace_bytes, void* stream);
 
+/*
+ * Batched form: B sequences (1 <= B <= ENTMTP_B_MAX), each with its own tree
+ * (topo[b]), prefix length (prefix_len[b]) and cache (k_caches[b],
+ * v_caches[b], each [Hkv][cap][d] bf16) -- the per-sequence tree choice of §4
+ * applied to every sequence of a batch.  topo, prefix_len, k_caches and
+ * v_caches are HOST arrays of B entries (the caches they list are device
+ * buffers); the scheduler runs on the host, so the grid follows the trees.
+ * q, k_tree, v_tree and out hold the sequences' tree rows back to back: the
+ * rows of sequence b start at row_off[b] = T(topo[0]) + ... + T(topo[b-1])
+ * (q / out rows are [Hq][d], k_tree / v_tree rows [Hkv][d]).  Each sequence
+ * is computed exactly as entmtp_tree_attn computes it.
+ *   workspace  device scratch of at least
+ *              entmtp_tree_attn_batched_workspace(B, T_max, Hq, Hkv, d,
+ *              max_prefix_len) bytes, where T_max and max_prefix_len bound
+ *              every sequence's tree size and prefix length.
+ * Errors: EINVAL, ERANGE, ENOSPC, EHIP (the failing sequence is named).
+ */
+size_t entmtp_tree_attn_batched_workspace(int32_t B, int32_t T_max, int32_t Hq, int32_t Hkv,
+                                          int32_t d, int32_t max_prefix_len);
+int32_t entmtp_tree_attn_batched(const entmtp_bank* bank, int32_t B, const int32_t* topo,
+                                 const int32_t* prefix_len, const entmtp_bf16* q,
+                                 const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                                 entmtp_bf16* const* k_caches, entmtp_bf16* const* v_caches,
+                                 int32_t cap, int32_t Hq, int32_t Hkv, int32_t d, float scale,
+                                 float rope_theta, entmtp_bf16* out, void* workspace,
+                                 size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* LM-head verification logits (§2.2: next-token distribution softmax(W h);  */
 /* §2.3: one verification pass for all tree nodes).                           */
@@ -260,6 +288,23 @@ int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
                       const int32_t* argmax, const float* top1p, int32_t* accept_len,
                       int32_t* path, int32_t* bonus, float* best_top1p, void* stream);
 
+/*
+ * Batched form: workgroup b accepts tree topo[b] (HOST array of B entries,
+ * 1 <= B <= ENTMTP_B_MAX) of sequence b.  draft_tokens, argmax and top1p hold
+ * the sequences' rows back to back (rows of sequence b start at
+ * T(topo[0]) + ... + T(topo[b-1]), the layout entmtp_tree_attn_batched uses;
+ * the LM head and statistics run over those rows unchanged).  Outputs, one
+ * per sequence: accept_len[B], bonus[B], best_top1p[B] (may be NULL), and
+ * path [B][path_capacity] (node indices local to the sequence's tree, -1 past
+ * its accept length); path_capacity >= 1 + every tree's depth.
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_accept_batched(const entmtp_bank* bank, int32_t B, const int32_t* topo,
+                              const int32_t* draft_tokens, const int32_t* argmax,
+                              const float* top1p, int32_t* accept_len, int32_t* path,
+                              int32_t path_capacity, int32_t* bonus, float* best_top1p,
+                              void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* KV-cache update of the accepted path (§3.2 decode loop).                   */
 /* ------------------------------------------------------------------------ */
@@ -286,6 +331,20 @@ int32_t entmtp_kv_compact(const int32_t* path, int32_t path_capacity,
                           entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t n_layers,
                           int64_t layer_stride, int32_t Hkv, int32_t cap, int32_t d,
                           void* stream);
+
+/*
+ * Batched form: sequence b (1 <= B <= ENTMTP_B_MAX) keeps the path in row b
+ * of path [B][path_capacity] (device) with accept length accept_len[b]
+ * (device), in its own cache k_caches[b] / v_caches[b] (HOST array of device
+ * pointers) at prefix length prefix_len[b] (HOST array); every sequence is
+ * compacted exactly as entmtp_kv_compact compacts one, in all n_layers
+ * layers.  Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_kv_compact_batched(int32_t B, const int32_t* path, int32_t path_capacity,
+                                  const int32_t* accept_len, const int32_t* prefix_len,
+                                  entmtp_bf16* const* k_caches, entmtp_bf16* const* v_caches,
+                                  int32_t n_layers, int64_t layer_stride, int32_t Hkv,
+                                  int32_t cap, int32_t d, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Scheduler policy (§4 "Policy"), host only.                                 */

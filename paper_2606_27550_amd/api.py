@@ -17,7 +17,7 @@ import numpy as np
 _LIB_PATH = os.path.join(os.path.dirname(os.path.abspath(__file__)), "libentmtp.so")
 
 OK, EINVAL, ETREE, ERANGE, ENOSPC, EHIP, ETIMEDOUT = 0, -1, -2, -3, -4, -5, -6
-T_MAX, D_MAX, MASK_WORDS, HEAD_DIM = 256, 31, 8, 128
+T_MAX, D_MAX, MASK_WORDS, HEAD_DIM, B_MAX = 256, 31, 8, 128, 16
 
 _c_i32, _c_i64, _c_f32, _c_sz, _c_p = (ctypes.c_int32, ctypes.c_int64, ctypes.c_float,
                                        ctypes.c_size_t, ctypes.c_void_p)
@@ -47,6 +47,14 @@ _SIGNATURES = {
     "entmtp_tree_attn_workspace": (_c_sz, [_c_i32, _c_i32, _c_i32, _c_i32, _c_i32]),
     "entmtp_tree_attn": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32,
                                   _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p, _c_sz, _c_p]),
+    "entmtp_tree_attn_batched_workspace": (_c_sz, [_c_i32] * 6),
+    "entmtp_tree_attn_batched": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                          _c_i32, _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p,
+                                          _c_sz, _c_p]),
+    "entmtp_accept_batched": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32,
+                                       _c_p, _c_p, _c_p]),
+    "entmtp_kv_compact_batched": (_c_i32, [_c_i32, _c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_i32,
+                                           _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
     "entmtp_verify_logits": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p]),
     "entmtp_logit_stats": (_c_i32, [_c_p, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p, _c_p]),
     "entmtp_verify_logits_stats_workspace": (_c_sz, [_c_i32, _c_i32, _c_i32]),
@@ -252,6 +260,98 @@ def tree_attn(bank: Bank, topo: int, q, k_tree, v_tree, k_cache, v_cache, prefix
                                 _p(v_cache), cap, prefix_len, Hq, Hkv, d, scale, rope_theta,
                                 _p(out), _p(workspace), workspace.numel() * workspace.element_size(),
                                 _stream(stream)))
+
+
+def _host_i32(values):
+    a = np.ascontiguousarray(np.asarray(values, dtype=np.int32))
+    return a, _np_p(a)
+
+
+def _host_ptrs(tensors):
+    arr = (ctypes.c_void_p * len(tensors))(*[t.data_ptr() for t in tensors])
+    return arr
+
+
+def tree_attn_batched_workspace(B: int, T_max: int, Hq: int, Hkv: int, d: int,
+                                max_prefix_len: int) -> int:
+    return int(lib.entmtp_tree_attn_batched_workspace(B, T_max, Hq, Hkv, d, max_prefix_len))
+
+
+def tree_attn_batched(bank: Bank, topo, prefix_len, q, k_tree, v_tree, k_caches, v_caches,
+                      scale: float, rope_theta: float, out, workspace, stream=None) -> None:
+    """Sequences' tree rows back to back in q [rows,Hq,d], k_tree/v_tree
+    [rows,Hkv,d], out [rows,Hq,d]; one [Hkv,cap,d] cache pair per sequence."""
+    import torch
+    B = len(topo)
+    _need(1 <= B <= B_MAX and len(prefix_len) == B and len(k_caches) == B and len(v_caches) == B,
+          "topo, prefix_len and the cache lists need one entry per sequence")
+    rows = sum(bank.T[t] for t in topo)
+    Hq, d = q.shape[1], q.shape[2]
+    Hkv = k_tree.shape[1]
+    _dev(q, "q", torch.bfloat16, (rows, Hq, d))
+    _dev(k_tree, "k_tree", torch.bfloat16, (rows, Hkv, d))
+    _dev(v_tree, "v_tree", torch.bfloat16, (rows, Hkv, d))
+    _dev(out, "out", torch.bfloat16, (rows, Hq, d))
+    cap = k_caches[0].shape[1]
+    for kc, vc in zip(k_caches, v_caches):
+        _dev(kc, "k_cache", torch.bfloat16, (Hkv, cap, d))
+        _dev(vc, "v_cache", torch.bfloat16, (Hkv, cap, d))
+    _need(workspace.is_cuda and workspace.is_contiguous(), "workspace must be a contiguous GPU tensor")
+    t_arr, t_p = _host_i32(topo)
+    l_arr, l_p = _host_i32(prefix_len)
+    kp, vp = _host_ptrs(k_caches), _host_ptrs(v_caches)
+    _check(lib.entmtp_tree_attn_batched(bank.handle, B, t_p, l_p, _p(q), _p(k_tree), _p(v_tree), kp,
+                                        vp, cap, Hq, Hkv, d, scale, rope_theta, _p(out),
+                                        _p(workspace), workspace.numel() * workspace.element_size(),
+                                        _stream(stream)))
+
+
+def accept_batched(bank: Bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,
+                   best_top1p=None, stream=None) -> None:
+    """Per-node arrays concatenated over sequences; path is [B, path_capacity]."""
+    import torch
+    B = len(topo)
+    rows = sum(bank.T[t] for t in topo)
+    _need(1 <= B <= B_MAX, "1 <= B <= 16")
+    _dev(draft_tokens, "draft_tokens", torch.int32, min_numel=rows)
+    _dev(argmax, "argmax", torch.int32, min_numel=rows)
+    if top1p is not None:
+        _dev(top1p, "top1p", torch.float32, min_numel=rows)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=B)
+    _dev(bonus, "bonus", torch.int32, min_numel=B)
+    if best_top1p is not None:
+        _dev(best_top1p, "best_top1p", torch.float32, min_numel=B)
+    _need(path.dim() == 2 and path.shape[0] == B, "path is [B, path_capacity]")
+    _dev(path, "path", torch.int32)
+    t_arr, t_p = _host_i32(topo)
+    _check(lib.entmtp_accept_batched(bank.handle, B, t_p, _p(draft_tokens), _p(argmax), _p(top1p),
+                                     _p(accept_len), _p(path), path.shape[1], _p(bonus),
+                                     _p(best_top1p), _stream(stream)))
+
+
+def kv_compact_batched(path, accept_len, prefix_len, k_caches, v_caches, stream=None) -> None:
+    """path [B, path_capacity], accept_len [B] on the device; one cache pair per
+    sequence, each [Hkv,cap,d] or [n_layers,Hkv,cap,d]."""
+    import torch
+    B = len(prefix_len)
+    _need(1 <= B <= B_MAX and len(k_caches) == B and len(v_caches) == B,
+          "one prefix length and cache pair per sequence")
+    _need(path.dim() == 2 and path.shape[0] == B, "path is [B, path_capacity]")
+    _dev(path, "path", torch.int32)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=B)
+    shape = k_caches[0].shape
+    for kc, vc in zip(k_caches, v_caches):
+        _need(kc.shape == shape and vc.shape == shape, "caches of equal shapes")
+        _dev(kc, "k_cache", torch.bfloat16)
+        _dev(vc, "v_cache", torch.bfloat16)
+    if len(shape) == 3:
+        n_layers, (Hkv, cap, d) = 1, shape
+    else:
+        n_layers, Hkv, cap, d = shape
+    l_arr, l_p = _host_i32(prefix_len)
+    kp, vp = _host_ptrs(k_caches), _host_ptrs(v_caches)
+    _check(lib.entmtp_kv_compact_batched(B, _p(path), path.shape[1], _p(accept_len), l_p, kp, vp,
+                                         n_layers, Hkv * cap * d, Hkv, cap, d, _stream(stream)))
 
 
 def verify_logits(hidden, w_lm, logits, stream=None) -> None:

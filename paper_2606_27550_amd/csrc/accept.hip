@@ -24,8 +24,9 @@ __device__ __forceinline__ void accept_core(
     const int* __restrict__ parent, const int* __restrict__ depth,
     const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
     const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
-    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
-    float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
+    int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
+    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
+    uint32_t seq) {
   __shared__ uint32_t matched[ENTMTP_MASK_WORDS];
   __shared__ int s_key[kAcceptThreads / 64];
   const int i = threadIdx.x;
@@ -54,7 +55,7 @@ __device__ __forceinline__ void accept_core(
   for (int w = 1; w < kAcceptThreads / 64; ++w) key = max(key, s_key[w]);
   const int best = 1023 - (key & 1023);
   const int a = key >> 10;
-  if (i <= D) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
+  if (i < path_cap) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
   if (i == 0) {
     const int bon = amax[best];
     const float p1 = top1p ? top1p[best] : 0.f;
@@ -77,8 +78,40 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
     const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
     int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
     float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
-  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, bonus,
-              best_p, mirror, seq);
+  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, D + 1,
+              bonus, best_p, mirror, seq);
+}
+
+// One tree of a batch: its bank arrays and its rows in the concatenated
+// per-node arrays.
+struct AcceptSeq {
+  const int* parent;
+  const int* depth;
+  const uint32_t* mask;
+  const int* path_tab;
+  int T, D, row0;
+};
+
+struct AcceptBatch {
+  AcceptSeq s[ENTMTP_B_MAX];
+  const int* tok;
+  const int* amax;
+  const float* top1p;
+  int* accept_len;
+  int* path;
+  int path_cap;
+  int* bonus;
+  float* best;
+};
+
+// Workgroup b accepts tree b.
+__global__ __launch_bounds__(kAcceptThreads) void accept_batched_kernel(AcceptBatch p) {
+  const int b = blockIdx.x;
+  const AcceptSeq& q = p.s[b];
+  accept_core(q.parent, q.depth, q.mask, q.path_tab, q.T, q.D, p.tok + q.row0, p.amax + q.row0,
+              p.top1p ? p.top1p + q.row0 : nullptr, p.accept_len + b,
+              p.path + static_cast<size_t>(b) * p.path_cap, p.path_cap, p.bonus + b,
+              p.best ? p.best + b : nullptr, nullptr, 0u);
 }
 
 // Statistics of node blockIdx.x from the LM head's partials, then -- in the
@@ -105,8 +138,8 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
   } else {
     __syncthreads();   // a single block: its own statistics, via LDS ordering
   }
-  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, bonus,
-              best_p, mirror, seq);
+  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, D + 1,
+              bonus, best_p, mirror, seq);
 }
 
 }  // namespace
@@ -159,4 +192,45 @@ extern "C" int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo,
                    "best_top1p needs top1p");
   return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,
                        best_top1p, nullptr, 0u, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int32_t entmtp_accept_batched(const entmtp_bank* bank, int32_t B, const int32_t* topo,
+                                         const int32_t* draft_tokens, const int32_t* argmax,
+                                         const float* top1p, int32_t* accept_len, int32_t* path,
+                                         int32_t path_capacity, int32_t* bonus,
+                                         float* best_top1p, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(B >= 1 && B <= ENTMTP_B_MAX, ENTMTP_EINVAL, "B = %d outside [1, %d]", B,
+                   ENTMTP_B_MAX);
+  ENTMTP_CHECK_ARG(topo != nullptr, ENTMTP_EINVAL, "topo must be a non-NULL host array");
+  ENTMTP_CHECK_ARG(draft_tokens && argmax && accept_len && path && bonus, ENTMTP_EINVAL,
+                   "draft_tokens, argmax, accept_len, path and bonus must be non-NULL");
+  ENTMTP_CHECK_ARG(best_top1p == nullptr || top1p != nullptr, ENTMTP_EINVAL,
+                   "best_top1p needs top1p");
+  ENTMTP_CHECK_ARG(path_capacity >= 1 && path_capacity <= kAcceptThreads, ENTMTP_EINVAL,
+                   "path_capacity = %d outside [1, %d]", path_capacity, kAcceptThreads);
+  AcceptBatch a;
+  int rows = 0;
+  for (int b = 0; b < B; ++b) {
+    if (int32_t rc = check_device_bank(bank, topo[b])) return rc;
+    const TopoDesc& d = bank->desc[topo[b]];
+    ENTMTP_CHECK_ARG(path_capacity >= d.D + 1, ENTMTP_EINVAL,
+                     "path_capacity = %d below 1 + depth %d of sequence %d's tree", path_capacity,
+                     d.D, b);
+    a.s[b] = AcceptSeq{bank_ptr<int>(bank, d.off_parent), bank_ptr<int>(bank, d.off_depth),
+                       bank_ptr<uint32_t>(bank, d.off_mask), bank_ptr<int>(bank, d.off_path), d.T,
+                       d.D, rows};
+    rows += d.T;
+  }
+  a.tok = draft_tokens;
+  a.amax = argmax;
+  a.top1p = top1p;
+  a.accept_len = accept_len;
+  a.path = path;
+  a.path_cap = path_capacity;
+  a.bonus = bonus;
+  a.best = best_top1p;
+  hipLaunchKernelGGL(accept_batched_kernel, dim3(B), dim3(kAcceptThreads), 0,
+                     static_cast<hipStream_t>(stream), a);
+  return launch_status("accept_batched launch");
 }

@@ -38,45 +38,85 @@ constexpr int kQTile = 32;           // query rows per tile
 constexpr int VT_LD = 36;            // bf16 per V^T row in LDS (32 keys + pad)
 constexpr int kMaxSplits = 32;
 constexpr int kMinBlocksPerSplit = 4;   // one block per wave at least
+constexpr int kMaxSeqs = ENTMTP_B_MAX;
 
 __host__ __device__ inline int rows_padded(int G, int T) {
   return (G * T + kQTile - 1) / kQTile * kQTile;
 }
 
+// ----------------------------------------------------------- descriptors --
+
+// One sequence of a (possibly batched) call, planned on the host.
+struct SeqPlan {
+  uint16_t* kc;            // [Hkv][cap][HD] this sequence's cache
+  uint16_t* vc;
+  const uint32_t* mask;    // [T][ENTMTP_MASK_WORDS] its tree's ancestor bitmask
+  const int* depth;        // [T]
+  int T, L, row0;          // nodes, prefix length, first row in the concatenated q / out
+  int rows_pad, nqt, nsplit, bps;
+  int item0;               // first attend workgroup of the sequence
+  int merge0;              // first merge block of the sequence
+  long long qrot_off;      // element offset of its rotated queries in the workspace
+  long long part_off;      // row offset of its split partials
+};
+
+struct BatchArgs {
+  SeqPlan s[kMaxSeqs];
+  int B, G, Hq, Hkv, cap;
+  float scale_log2;
+  double theta;
+  const uint16_t* q;       // [rows][Hq][HD] (rows = sum of T, sequence after sequence)
+  const uint16_t* kt;      // [rows][Hkv][HD]
+  const uint16_t* vt;
+  uint16_t* qrot;          // workspace
+  float* part_o;           // [part rows][HD]
+  float* part_ml;          // [part rows][2]
+  uint16_t* out;           // [rows][Hq][HD]
+};
+
+// Sequence that owns index `x` of a grid whose per-sequence ranges start at
+// `first(b)` (uniform per workgroup; at most kMaxSeqs steps).
+template <typename F>
+__device__ __forceinline__ int seq_of(const BatchArgs& p, int x, F first) {
+  int b = 0;
+  while (b + 1 < p.B && x >= first(p.s[b + 1])) ++b;
+  return b;
+}
+
 // ------------------------------------------------------------------ prep --
 
-__global__ __launch_bounds__(256) void attn_prep_kernel(
-    const uint16_t* __restrict__ q, const uint16_t* __restrict__ kt,
-    const uint16_t* __restrict__ vt, uint16_t* __restrict__ kc, uint16_t* __restrict__ vc,
-    uint16_t* __restrict__ qrot, const int* __restrict__ depth, int T, int Hq, int Hkv, int cap,
-    int L, double theta, int rows_pad) {
-  // grid (T, chunks): block (i, y) takes items [256 y, 256 y + 256) of node
-  // i's list: Hq*64 query pairs, then Hkv*64 key pairs, then Hkv*16 16-byte
-  // value chunks
+__global__ __launch_bounds__(256) void attn_prep_kernel(BatchArgs p) {
+  // grid (sum of T, chunks): block (row, y) takes items [256 y, 256 y + 256)
+  // of its node's list: Hq*64 query pairs, then Hkv*64 key pairs, then
+  // Hkv*16 16-byte value chunks
   constexpr int HALF = HD / 2;
-  const int i = blockIdx.x;
+  const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.row0; });
+  const SeqPlan& sq = p.s[b];
+  const int row = blockIdx.x;
+  const int i = row - sq.row0;
   const int u = blockIdx.y * blockDim.x + threadIdx.x;
-  const int G = Hq / Hkv;
+  const int Hq = p.Hq, Hkv = p.Hkv, G = p.G, T = sq.T, L = sq.L, cap = p.cap;
   const int nq = Hq * HALF, nk = Hkv * HALF, nv = Hkv * (HD / 8);
   if (u >= nq + nk + nv) return;
   if (u >= nq + nk) {  // value copy -> cache slot L + i
     const int w = u - nq - nk;
     const int g = w / (HD / 8), c8 = w % (HD / 8);
-    *reinterpret_cast<u32x4*>(vc + (static_cast<size_t>(g) * cap + L + i) * HD + 8 * c8) =
-        *reinterpret_cast<const u32x4*>(vt + (static_cast<size_t>(i) * Hkv + g) * HD + 8 * c8);
+    *reinterpret_cast<u32x4*>(sq.vc + (static_cast<size_t>(g) * cap + L + i) * HD + 8 * c8) =
+        *reinterpret_cast<const u32x4*>(p.vt + (static_cast<size_t>(row) * Hkv + g) * HD + 8 * c8);
     return;
   }
   const bool is_q = u < nq;
   const int w = is_q ? u : u - nq;
   const int head = w / HALF, c = w % HALF;
-  const uint16_t* src = (is_q ? q + (static_cast<size_t>(i) * Hq + head) * HD
-                              : kt + (static_cast<size_t>(i) * Hkv + head) * HD);
-  uint16_t* dst = is_q ? qrot + (static_cast<size_t>(head / G) * rows_pad + (head % G) * T + i) * HD
-                       : kc + (static_cast<size_t>(head) * cap + L + i) * HD;
-  if (theta > 0.0) {
+  const uint16_t* src = (is_q ? p.q + (static_cast<size_t>(row) * Hq + head) * HD
+                              : p.kt + (static_cast<size_t>(row) * Hkv + head) * HD);
+  uint16_t* dst = is_q ? p.qrot + sq.qrot_off +
+                             (static_cast<size_t>(head / G) * sq.rows_pad + (head % G) * T + i) * HD
+                       : sq.kc + (static_cast<size_t>(head) * cap + L + i) * HD;
+  if (p.theta > 0.0) {
     // position prefix_len + depth(i), pair (c, c + d/2) turned by pos * theta^(-2c/d)
-    const double pos = static_cast<double>(L) + static_cast<double>(depth[i]);
-    const double ang = pos * pow(theta, -2.0 * c / HD);
+    const double pos = static_cast<double>(L) + static_cast<double>(sq.depth[i]);
+    const double ang = pos * pow(p.theta, -2.0 * c / HD);
     double sn, cs;
     sincos(ang, &sn, &cs);
     const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
@@ -90,37 +130,30 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(
 
 // ---------------------------------------------------------------- attend --
 
-struct AttnArgs {
-  const uint16_t* qrot;   // [Hkv][rows_pad][HD]
-  const uint16_t* kc;     // [Hkv][cap][HD]
-  const uint16_t* vc;
-  const uint32_t* mask;   // [T][ENTMTP_MASK_WORDS]
-  float* part_o;          // [nsplit][Hkv][rows_pad][HD]
-  float* part_ml;         // [nsplit][Hkv][rows_pad][2]
-  uint16_t* out;          // [T][Hq][HD]
-  int T, G, Hq, Hkv, cap, L, nkeys, rows_pad, nqt, nsplit, bps;
-  float scale_log2;
-};
-
 __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
   __builtin_amdgcn_wave_barrier();
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-__global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
-  // blockIdx -> (kv head, split) group and query tile; the query tiles of one
-  // group land on the same XCD (dispatch is round-robin over 8 XCDs), so
+__global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
+  // blockIdx -> sequence, then (kv head, split) group and query tile; the
+  // query tiles of one group land on the same XCD (dispatch is round-robin
+  // over 8 XCDs and every sequence's range starts at a multiple of 8), so
   // their K/V reads share that XCD's L2.
-  const int bid = blockIdx.x;
-  const int qt = (bid >> 3) % p.nqt;
-  const int gc = ((bid >> 3) / p.nqt) * 8 + (bid & 7);
-  if (gc >= p.Hkv * p.nsplit) return;
-  const int g = gc / p.nsplit, split = gc % p.nsplit;
+  const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
+  const SeqPlan& sq = p.s[b];
+  const int bid = blockIdx.x - sq.item0;
+  const int qt = (bid >> 3) % sq.nqt;
+  const int gc = ((bid >> 3) / sq.nqt) * 8 + (bid & 7);
+  if (gc >= p.Hkv * sq.nsplit) return;
+  const int g = gc / sq.nsplit, split = gc % sq.nsplit;
+  const int T = sq.T, L = sq.L, nkeys = sq.L + sq.T, rows_pad = sq.rows_pad;
+  const int nsplit = sq.nsplit;
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 31, lh = lane >> 5;
-  const int GT = p.G * p.T;
+  const int GT = p.G * T;
 
   // LDS: per-wave V^T tiles during the loop, reused for the wave merge after it
   constexpr int kVtBytes = HD * VT_LD * 2;                           // 9216
@@ -135,14 +168,14 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
   for (int u = tid; u < kQTile * ENTMTP_MASK_WORDS; u += kAttnThreads) {
     const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
     const int qrow = qt * kQTile + r;
-    s_mask[r][w] = qrow < GT ? p.mask[(qrow % p.T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+    s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
   }
 
   // Q^T B-operand fragments: lane (query li, half lh) holds d = 16s + 8lh + e
   const int qrow = qt * kQTile + li;
   u32x4 qf[8];
   {
-    const uint16_t* qp = p.qrot + (static_cast<size_t>(g) * p.rows_pad + qrow) * HD + 8 * lh;
+    const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD + 8 * lh;
 #pragma unroll
     for (int s = 0; s < 8; ++s)
       qf[s] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
@@ -151,8 +184,8 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
 
   uint32_t* vt = reinterpret_cast<uint32_t*>(lds + wave * kVtBytes);  // [HD][VT_LD/2] key pairs
   const size_t head_off = static_cast<size_t>(g) * p.cap * HD;
-  const uint16_t* kbase = p.kc + head_off;
-  const uint16_t* vbase = p.vc + head_off;
+  const uint16_t* kbase = sq.kc + head_off;
+  const uint16_t* vbase = sq.vc + head_off;
 
   float m_run = -INFINITY, l_run = 0.f;
   f32x16 o[4];
@@ -161,16 +194,16 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) o[ct][r] = 0.f;
 
-  const int nblocks = (p.nkeys + KB - 1) / KB;
-  const int blk_lo = split * p.bps;
-  const int blk_hi = min(nblocks, blk_lo + p.bps);
+  const int nblocks = (nkeys + KB - 1) / KB;
+  const int blk_lo = split * sq.bps;
+  const int blk_hi = min(nblocks, blk_lo + sq.bps);
 
   // K/V of one block into registers.  Keys past the end are clamped to the
   // last key (finite data whose probabilities are zero), so every load is
   // unconditional and the compiler's wait counts stay exact.
   auto load_kv = [&](int blk, u32x4 (&kf)[8], u32x4 (&va)[4], u32x4 (&vb)[4]) {
     const int kb = blk * KB;
-    const int last = p.nkeys - 1;
+    const int last = nkeys - 1;
     const int key = min(kb + li, last);
     const uint16_t* kp = kbase + static_cast<size_t>(key) * HD + 8 * lh;
 #pragma unroll
@@ -211,7 +244,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
 
     // mask: lane holds keys n = 8*(r/4) + 4*lh + r%4 of the block for query li
     uint32_t win = 0xFFFFFFFFu;
-    const int rel = kb - p.L;
+    const int rel = kb - L;
     if (rel > -KB) {
       if (rel < 0) {
         const int npre = -rel;
@@ -228,7 +261,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
       const int n = 8 * (r >> 2) + 4 * lh + (r & 3);
-      const bool vis = ((win >> n) & 1u) && (kb + n < p.nkeys);
+      const bool vis = ((win >> n) & 1u) && (kb + n < nkeys);
       sv[r] = vis ? sacc[r] * p.scale_log2 : -INFINITY;
       bmax = fmaxf(bmax, sv[r]);
     }
@@ -330,13 +363,13 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
       lsum += s_l[w][q] * sc;
       osum += ored[(w * kQTile + q) * OLD + dim];
     }
-    if (p.nsplit == 1) {
-      const int gh = row / p.T, node = row % p.T;
+    if (nsplit == 1) {
+      const int gh = row / T, node = row % T;
       const int h = g * p.G + gh;
-      p.out[(static_cast<size_t>(node) * p.Hq + h) * HD + dim] =
+      p.out[(static_cast<size_t>(sq.row0 + node) * p.Hq + h) * HD + dim] =
           static_cast<uint16_t>(f32_to_bf16_rne(osum / lsum));
     } else {
-      const size_t prow = (static_cast<size_t>(split) * p.Hkv + g) * p.rows_pad + row;
+      const size_t prow = sq.part_off + (static_cast<size_t>(split) * p.Hkv + g) * rows_pad + row;
       p.part_o[prow * HD + dim] = osum;
       if (dim == 0) {
         p.part_ml[prow * 2 + 0] = Mq;
@@ -348,36 +381,32 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(AttnArgs p) {
 
 // ----------------------------------------------------------------- merge --
 
-__global__ __launch_bounds__(HD) void attn_merge_kernel(const float* __restrict__ part_o,
-                                                        const float* __restrict__ part_ml,
-                                                        uint16_t* __restrict__ out, int T, int G,
-                                                        int Hq, int Hkv, int rows_pad,
-                                                        int nsplit) {
-  const int g = blockIdx.x / (G * T), row = blockIdx.x % (G * T);
+__global__ __launch_bounds__(HD) void attn_merge_kernel(BatchArgs p) {
+  const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.merge0; });
+  const SeqPlan& sq = p.s[b];
+  if (sq.nsplit == 1) return;   // written by the attend kernel
+  const int GT = p.G * sq.T;
+  const int local = blockIdx.x - sq.merge0;
+  const int g = local / GT, row = local % GT;
   const int dim = threadIdx.x;
   float M = -INFINITY;
-  for (int c = 0; c < nsplit; ++c)
-    M = fmaxf(M, part_ml[((static_cast<size_t>(c) * Hkv + g) * rows_pad + row) * 2]);
+  for (int c = 0; c < sq.nsplit; ++c)
+    M = fmaxf(M, p.part_ml[(sq.part_off + (static_cast<size_t>(c) * p.Hkv + g) * sq.rows_pad + row) * 2]);
   float lsum = 0.f, osum = 0.f;
-  for (int c = 0; c < nsplit; ++c) {
-    const size_t prow = (static_cast<size_t>(c) * Hkv + g) * rows_pad + row;
-    const float mc = part_ml[prow * 2];
+  for (int c = 0; c < sq.nsplit; ++c) {
+    const size_t prow = sq.part_off + (static_cast<size_t>(c) * p.Hkv + g) * sq.rows_pad + row;
+    const float mc = p.part_ml[prow * 2];
     if (mc == -INFINITY) continue;
     const float sc = exp2f(mc - M);
-    lsum += part_ml[prow * 2 + 1] * sc;
-    osum += part_o[prow * HD + dim] * sc;
+    lsum += p.part_ml[prow * 2 + 1] * sc;
+    osum += p.part_o[prow * HD + dim] * sc;
   }
-  const int gh = row / T, node = row % T;
-  out[(static_cast<size_t>(node) * Hq + g * G + gh) * HD + dim] =
+  const int gh = row / sq.T, node = row % sq.T;
+  p.out[(static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + gh) * HD + dim] =
       static_cast<uint16_t>(f32_to_bf16_rne(osum / lsum));
 }
 
 // ------------------------------------------------------------------ host --
-
-struct Plan {
-  int G, rows_pad, nqt, nblocks, nsplit, bps;
-  size_t q_bytes, po_bytes, pml_bytes;
-};
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
@@ -399,22 +428,15 @@ int device_cus() {
   return cus[dev];
 }
 
-Plan make_plan(int T, int Hq, int Hkv, int L) {
-  Plan pl{};
-  pl.G = Hq / Hkv;
-  pl.rows_pad = rows_padded(pl.G, T);
-  pl.nqt = pl.rows_pad / kQTile;
-  pl.nblocks = (L + T + KB - 1) / KB;
-  const int bound = split_bound(pl.nblocks);
-  // One workgroup fits per CU.  Pick the split count so that the workgroups
-  // fill the CUs in whole rounds: the first count (1..bound) whose last round
-  // is at least 90% full, else the best one seen.
-  const int cus = device_cus();
-  const int base = Hkv * pl.nqt;
+// Split count of a lone sequence: one workgroup fits per CU, so pick the
+// count that fills the CUs in whole rounds -- the first (1..bound) whose last
+// round is at least 90% full, else the best one seen.
+int split_single(int nblocks, int base_wg, int cus) {
+  const int bound = split_bound(nblocks);
   int best = 1;
   double best_eff = 0.0;
   for (int ns = 1; ns <= bound; ++ns) {
-    const int wg = base * ns;
+    const int wg = base_wg * ns;
     const int rounds = (wg + cus - 1) / cus;
     const double eff = static_cast<double>(wg) / (static_cast<double>(rounds) * cus);
     if (eff > best_eff + 1e-9) {
@@ -423,15 +445,110 @@ Plan make_plan(int T, int Hq, int Hkv, int L) {
     }
     if (eff >= 0.9) break;
   }
-  pl.nsplit = best;
-  pl.bps = (pl.nblocks + pl.nsplit - 1) / pl.nsplit;
-  pl.nsplit = (pl.nblocks + pl.bps - 1) / pl.bps;
-  pl.q_bytes = static_cast<size_t>(Hkv) * pl.rows_pad * HD * 2;
-  return pl;
+  return best;
+}
+
+// Grid sizes of one call.
+struct CallShape {
+  int rows = 0;          // concatenated tree rows (prep grid)
+  int items = 0;         // attend workgroups
+  int merge_blocks = 0;  // merge blocks
+  size_t need = 0;       // workspace bytes
+};
+
+// Plans the sequences of one call: per-sequence split counts (a lone
+// sequence fills the CUs by itself; a batch shares one blocks-per-split
+// target sized to about four workgroups per CU), grid ranges and the packed
+// workspace layout (rotated queries, output partials, (max, sum) partials).
+CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const int32_t* L,
+                    entmtp_bf16* const* kc, entmtp_bf16* const* vc, int cap, int Hq, int Hkv,
+                    BatchArgs& a) {
+  a.B = B;
+  a.G = Hq / Hkv;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  const int cus = device_cus();
+  long long work = 0;
+  for (int b = 0; b < B; ++b) {
+    const int T = bank->desc[topo[b]].T;
+    const int nqt = rows_padded(a.G, T) / kQTile;
+    work += static_cast<long long>(Hkv) * nqt * ((L[b] + T + KB - 1) / KB);
+  }
+  const long long per_wg = (work + 4LL * cus - 1) / (4LL * cus);
+  const int target_bps = static_cast<int>(per_wg > kMinBlocksPerSplit ? per_wg : kMinBlocksPerSplit);
+
+  CallShape sh;
+  long long qrot = 0, part_rows = 0;
+  for (int b = 0; b < B; ++b) {
+    const TopoDesc& td = bank->desc[topo[b]];
+    SeqPlan& q = a.s[b];
+    q.kc = kc[b];
+    q.vc = vc[b];
+    q.mask = bank_ptr<uint32_t>(bank, td.off_mask);
+    q.depth = bank_ptr<int>(bank, td.off_depth);
+    q.T = td.T;
+    q.L = L[b];
+    q.row0 = sh.rows;
+    q.rows_pad = rows_padded(a.G, q.T);
+    q.nqt = q.rows_pad / kQTile;
+    const int nblocks = (q.L + q.T + KB - 1) / KB;
+    int ns;
+    if (B == 1) {
+      ns = split_single(nblocks, Hkv * q.nqt, cus);
+    } else {
+      ns = (nblocks + target_bps - 1) / target_bps;
+      const int bound = split_bound(nblocks);
+      ns = ns < 1 ? 1 : (ns > bound ? bound : ns);
+    }
+    q.bps = (nblocks + ns - 1) / ns;
+    q.nsplit = (nblocks + q.bps - 1) / q.bps;
+    q.item0 = sh.items;
+    q.merge0 = sh.merge_blocks;
+    q.qrot_off = qrot;
+    q.part_off = part_rows;
+    sh.rows += q.T;
+    sh.items += (Hkv * q.nsplit + 7) / 8 * 8 * q.nqt;
+    if (q.nsplit > 1) {
+      sh.merge_blocks += Hkv * a.G * q.T;
+      part_rows += static_cast<long long>(q.nsplit) * Hkv * q.rows_pad;
+    }
+    qrot += static_cast<long long>(Hkv) * q.rows_pad * HD;
+  }
+  const size_t qb = static_cast<size_t>(qrot) * 2;
+  const size_t po = static_cast<size_t>(part_rows) * HD * 4;
+  const size_t pml = static_cast<size_t>(part_rows) * 2 * 4;
+  sh.need = al256(qb) + al256(po) + al256(pml);
+  return sh;
+}
+
+// Points the planned call at its workspace and launches prep, attend and
+// (when some sequence has several splits) merge.
+int32_t launch_call(BatchArgs& a, const CallShape& sh, void* workspace, hipStream_t s) {
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  long long qrot = 0, part_rows = 0;
+  for (int b = 0; b < a.B; ++b) {
+    qrot += static_cast<long long>(a.Hkv) * a.s[b].rows_pad * HD;
+    if (a.s[b].nsplit > 1) part_rows += static_cast<long long>(a.s[b].nsplit) * a.Hkv * a.s[b].rows_pad;
+  }
+  const size_t qb = static_cast<size_t>(qrot) * 2, po = static_cast<size_t>(part_rows) * HD * 4;
+  a.qrot = reinterpret_cast<uint16_t*>(ws);
+  a.part_o = reinterpret_cast<float*>(ws + al256(qb));
+  a.part_ml = reinterpret_cast<float*>(ws + al256(qb) + al256(po));
+  const int prep_items = (a.Hq + a.Hkv) * (HD / 2) + a.Hkv * (HD / 8);
+  hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
+  if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
+  hipLaunchKernelGGL(tree_attn_kernel, dim3(sh.items), dim3(kAttnThreads), 0, s, a);
+  if (int32_t rc = launch_status("tree_attn launch")) return rc;
+  if (sh.merge_blocks > 0) {
+    hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(HD), 0, s, a);
+    if (int32_t rc = launch_status("tree_attn merge launch")) return rc;
+  }
+  return ENTMTP_OK;
 }
 
 size_t workspace_bytes(int T, int Hq, int Hkv, int L) {
-  // sized with the largest split count the plan can choose, so the figure
+  // sized with the largest split count a plan can choose, so the figure
   // never shrinks when T or L grows
   const int G = Hq / Hkv;
   const int rows_pad = rows_padded(G, T);
@@ -439,6 +556,39 @@ size_t workspace_bytes(int T, int Hq, int Hkv, int L) {
   const size_t bound = split_bound(nblocks);
   return al256(static_cast<size_t>(Hkv) * rows_pad * HD * 2) +
          al256(bound * Hkv * rows_pad * HD * 4) + al256(bound * Hkv * rows_pad * 2 * 4);
+}
+
+// Checks shared by the single and batched entry points.
+int32_t check_common(int32_t Hq, int32_t Hkv, int32_t d, float scale, float rope_theta,
+                     const void* q, const void* k_tree, const void* v_tree, const void* out,
+                     const void* workspace) {
+  ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && workspace, ENTMTP_EINVAL,
+                   "tensor and workspace pointers must be non-NULL");
+  ENTMTP_CHECK_ARG(d == HD, ENTMTP_EINVAL, "head dim %d unsupported (built for %d)", d, HD);
+  ENTMTP_CHECK_ARG(Hq >= 1 && Hkv >= 1, ENTMTP_EINVAL, "Hq = %d, Hkv = %d must be >= 1", Hq, Hkv);
+  ENTMTP_CHECK_ARG(Hq % Hkv == 0, ENTMTP_ERANGE, "Hq = %d is not a multiple of Hkv = %d", Hq, Hkv);
+  ENTMTP_CHECK_ARG(Hq / Hkv <= 32, ENTMTP_ERANGE, "query group %d too large", Hq / Hkv);
+  ENTMTP_CHECK_ARG(scale > 0.f && scale < INFINITY, ENTMTP_EINVAL, "scale must be positive");
+  ENTMTP_CHECK_ARG(rope_theta >= 0.f && rope_theta < INFINITY, ENTMTP_EINVAL,
+                   "rope_theta must be >= 0");
+  ENTMTP_CHECK_ARG(aligned16(q) && aligned16(k_tree) && aligned16(v_tree) && aligned16(out) &&
+                       aligned16(workspace),
+                   ENTMTP_EINVAL, "tensors and workspace must be 16-byte aligned");
+  return ENTMTP_OK;
+}
+
+int32_t check_sequence(const entmtp_bank* bank, int32_t topo, int32_t prefix_len,
+                       const void* kc, const void* vc, int32_t cap, int b) {
+  if (int32_t rc = check_device_bank(bank, topo)) return rc;
+  ENTMTP_CHECK_ARG(kc && vc && aligned16(kc) && aligned16(vc), ENTMTP_EINVAL,
+                   "sequence %d: caches must be non-NULL and 16-byte aligned", b);
+  ENTMTP_CHECK_ARG(prefix_len >= 0, ENTMTP_EINVAL, "sequence %d: prefix_len = %d < 0", b,
+                   prefix_len);
+  const int T = bank->desc[topo].T;
+  ENTMTP_CHECK_ARG(static_cast<int64_t>(prefix_len) + T <= cap, ENTMTP_ERANGE,
+                   "sequence %d: cache capacity %d below prefix_len + T = %d", b, cap,
+                   prefix_len + T);
+  return ENTMTP_OK;
 }
 
 }  // namespace
@@ -453,6 +603,13 @@ extern "C" size_t entmtp_tree_attn_workspace(int32_t T, int32_t Hq, int32_t Hkv,
   return workspace_bytes(T, Hq, Hkv, prefix_len);
 }
 
+extern "C" size_t entmtp_tree_attn_batched_workspace(int32_t B, int32_t T_max, int32_t Hq,
+                                                     int32_t Hkv, int32_t d,
+                                                     int32_t max_prefix_len) {
+  if (B < 1 || B > ENTMTP_B_MAX) return 0;
+  return static_cast<size_t>(B) * entmtp_tree_attn_workspace(T_max, Hq, Hkv, d, max_prefix_len);
+}
+
 extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const entmtp_bf16* q,
                                     const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
                                     entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t cap,
@@ -460,70 +617,49 @@ extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const
                                     float scale, float rope_theta, entmtp_bf16* out,
                                     void* workspace, size_t ws_bytes, void* stream) {
   clear_error();
-  if (int32_t rc = check_device_bank(bank, topo)) return rc;
-  ENTMTP_CHECK_ARG(q && k_tree && v_tree && k_cache && v_cache && out && workspace, ENTMTP_EINVAL,
-                   "tensor and workspace pointers must be non-NULL");
-  ENTMTP_CHECK_ARG(d == HD, ENTMTP_EINVAL, "head dim %d unsupported (built for %d)", d, HD);
-  ENTMTP_CHECK_ARG(Hq >= 1 && Hkv >= 1, ENTMTP_EINVAL, "Hq = %d, Hkv = %d must be >= 1", Hq, Hkv);
-  ENTMTP_CHECK_ARG(Hq % Hkv == 0, ENTMTP_ERANGE, "Hq = %d is not a multiple of Hkv = %d", Hq, Hkv);
-  ENTMTP_CHECK_ARG(Hq / Hkv * ENTMTP_T_MAX <= 32 * ENTMTP_T_MAX, ENTMTP_ERANGE,
-                   "query group %d too large", Hq / Hkv);
-  ENTMTP_CHECK_ARG(prefix_len >= 0, ENTMTP_EINVAL, "prefix_len = %d < 0", prefix_len);
-  ENTMTP_CHECK_ARG(scale > 0.f && scale < INFINITY, ENTMTP_EINVAL, "scale must be positive");
-  ENTMTP_CHECK_ARG(rope_theta >= 0.f && rope_theta < INFINITY, ENTMTP_EINVAL,
-                   "rope_theta must be >= 0");
-  ENTMTP_CHECK_ARG(aligned16(q) && aligned16(k_tree) && aligned16(v_tree) && aligned16(k_cache) &&
-                       aligned16(v_cache) && aligned16(workspace),
-                   ENTMTP_EINVAL, "tensors and workspace must be 16-byte aligned");
-  const TopoDesc& td = bank->desc[topo];
-  const int T = td.T;
-  ENTMTP_CHECK_ARG(static_cast<int64_t>(prefix_len) + T <= cap, ENTMTP_ERANGE,
-                   "cache capacity %d below prefix_len + T = %d", cap, prefix_len + T);
-  const size_t need = workspace_bytes(T, Hq, Hkv, prefix_len);
-  ENTMTP_CHECK_ARG(ws_bytes >= need, ENTMTP_ENOSPC, "workspace has %zu bytes, needs %zu",
-                   ws_bytes, need);
-
-  const Plan pl = make_plan(T, Hq, Hkv, prefix_len);
-  uint8_t* ws = static_cast<uint8_t*>(workspace);
-  uint16_t* qrot = reinterpret_cast<uint16_t*>(ws);
-  const size_t po = static_cast<size_t>(pl.nsplit) * Hkv * pl.rows_pad * HD * 4;
-  float* part_o = reinterpret_cast<float*>(ws + al256(pl.q_bytes));
-  float* part_ml = reinterpret_cast<float*>(ws + al256(pl.q_bytes) + al256(po));
-  auto s = static_cast<hipStream_t>(stream);
-
-  const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
-  hipLaunchKernelGGL(attn_prep_kernel, dim3(T, (prep_items + 255) / 256), dim3(256), 0, s, q, k_tree,
-                     v_tree, k_cache, v_cache, qrot, bank_ptr<int>(bank, td.off_depth), T, Hq, Hkv, cap,
-                     prefix_len, static_cast<double>(rope_theta), pl.rows_pad);
-  if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
-
-  AttnArgs a;
-  a.qrot = qrot;
-  a.kc = k_cache;
-  a.vc = v_cache;
-  a.mask = bank_ptr<uint32_t>(bank, td.off_mask);
-  a.part_o = part_o;
-  a.part_ml = part_ml;
-  a.out = out;
-  a.T = T;
-  a.G = pl.G;
-  a.Hq = Hq;
-  a.Hkv = Hkv;
-  a.cap = cap;
-  a.L = prefix_len;
-  a.nkeys = prefix_len + T;
-  a.rows_pad = pl.rows_pad;
-  a.nqt = pl.nqt;
-  a.nsplit = pl.nsplit;
-  a.bps = pl.bps;
+  if (int32_t rc = check_sequence(bank, topo, prefix_len, k_cache, v_cache, cap, 0)) return rc;
+  if (int32_t rc = check_common(Hq, Hkv, d, scale, rope_theta, q, k_tree, v_tree, out, workspace))
+    return rc;
+  const int T = bank->desc[topo].T;
+  ENTMTP_CHECK_ARG(ws_bytes >= workspace_bytes(T, Hq, Hkv, prefix_len), ENTMTP_ENOSPC,
+                   "workspace has %zu bytes, needs %zu", ws_bytes,
+                   workspace_bytes(T, Hq, Hkv, prefix_len));
+  BatchArgs a;
+  const CallShape sh = plan_call(bank, 1, &topo, &prefix_len, &k_cache, &v_cache, cap, Hq, Hkv, a);
   a.scale_log2 = scale * 1.4426950408889634f;
-  const int groups = (Hkv * pl.nsplit + 7) / 8 * 8;
-  hipLaunchKernelGGL(tree_attn_kernel, dim3(groups * pl.nqt), dim3(kAttnThreads), 0, s, a);
-  if (int32_t rc = launch_status("tree_attn launch")) return rc;
-  if (pl.nsplit > 1) {
-    hipLaunchKernelGGL(attn_merge_kernel, dim3(Hkv * pl.G * T), dim3(HD), 0, s, part_o, part_ml,
-                       out, T, pl.G, Hq, Hkv, pl.rows_pad, pl.nsplit);
-    if (int32_t rc = launch_status("tree_attn merge launch")) return rc;
-  }
-  return ENTMTP_OK;
+  a.theta = static_cast<double>(rope_theta);
+  a.q = q;
+  a.kt = k_tree;
+  a.vt = v_tree;
+  a.out = out;
+  return launch_call(a, sh, workspace, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int32_t entmtp_tree_attn_batched(
+    const entmtp_bank* bank, int32_t B, const int32_t* topo, const int32_t* prefix_len,
+    const entmtp_bf16* q, const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+    entmtp_bf16* const* k_caches, entmtp_bf16* const* v_caches, int32_t cap, int32_t Hq,
+    int32_t Hkv, int32_t d, float scale, float rope_theta, entmtp_bf16* out, void* workspace,
+    size_t ws_bytes, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(B >= 1 && B <= ENTMTP_B_MAX, ENTMTP_EINVAL, "B = %d outside [1, %d]", B,
+                   ENTMTP_B_MAX);
+  ENTMTP_CHECK_ARG(topo && prefix_len && k_caches && v_caches, ENTMTP_EINVAL,
+                   "topo, prefix_len, k_caches and v_caches must be non-NULL host arrays");
+  for (int b = 0; b < B; ++b)
+    if (int32_t rc = check_sequence(bank, topo[b], prefix_len[b], k_caches[b], v_caches[b], cap, b))
+      return rc;
+  if (int32_t rc = check_common(Hq, Hkv, d, scale, rope_theta, q, k_tree, v_tree, out, workspace))
+    return rc;
+  BatchArgs a;
+  const CallShape sh = plan_call(bank, B, topo, prefix_len, k_caches, v_caches, cap, Hq, Hkv, a);
+  ENTMTP_CHECK_ARG(ws_bytes >= sh.need, ENTMTP_ENOSPC, "workspace has %zu bytes, needs %zu",
+                   ws_bytes, sh.need);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.theta = static_cast<double>(rope_theta);
+  a.q = q;
+  a.kt = k_tree;
+  a.vt = v_tree;
+  a.out = out;
+  return launch_call(a, sh, workspace, static_cast<hipStream_t>(stream));
 }

@@ -114,6 +114,32 @@ def test_kernel_calls_reject_bad_arguments_without_launching():
     assert api.stats_partials_bytes(27, 4096, 32000) >= 27 * 256 * 16
     assert api.verify_logits_stats_workspace(27, 264, 32000) > 0
     assert api.verify_logits_stats_workspace(27, 4096, 32000) == api.stats_partials_bytes(27, 4096, 32000)
+    # batched calls: sizes and host arrays are checked before the bank
+    two = (ctypes.c_int32 * 2)(0, 0)
+    ptrs = (ctypes.c_void_p * 2)(16, 16)
+    for B in (0, api.B_MAX + 1):
+        assert lib.entmtp_tree_attn_batched(host_bank.handle, B, two, two, p, p, p, ptrs, ptrs, 100,
+                                            32, 8, 128, 0.1, 0.0, p, p, 1 << 20, None) == api.EINVAL
+        assert lib.entmtp_accept_batched(host_bank.handle, B, two, p, p, None, p, p, 4, p, None,
+                                         None) == api.EINVAL
+        assert lib.entmtp_kv_compact_batched(B, p, 4, p, two, ptrs, ptrs, 1, 0, 8, 100, 128,
+                                             None) == api.EINVAL
+    assert lib.entmtp_tree_attn_batched(host_bank.handle, 2, None, two, p, p, p, ptrs, ptrs, 100,
+                                        32, 8, 128, 0.1, 0.0, p, p, 1 << 20, None) == api.EINVAL
+    rc = lib.entmtp_tree_attn_batched(host_bank.handle, 2, two, two, p, p, p, ptrs, ptrs, 100, 32, 8,
+                                      128, 0.1, 0.0, p, p, 1 << 20, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
+    assert lib.entmtp_accept_batched(host_bank.handle, 2, two, p, p, None, p, p, 0, p, None,
+                                     None) == api.EINVAL
+    neg = (ctypes.c_int32 * 2)(0, -1)
+    assert lib.entmtp_kv_compact_batched(2, p, 4, p, neg, ptrs, ptrs, 1, 0, 8, 100, 128,
+                                         None) == api.EINVAL
+    nulls = (ctypes.c_void_p * 2)(16, None)
+    assert lib.entmtp_kv_compact_batched(2, p, 4, p, two, ptrs, nulls, 1, 0, 8, 100, 128,
+                                         None) == api.EINVAL
+    assert api.tree_attn_batched_workspace(8, 128, 32, 8, 128, 16384) == \
+        8 * api.tree_attn_workspace(128, 32, 8, 128, 16384)
+    assert api.tree_attn_batched_workspace(0, 128, 32, 8, 128, 16384) == 0
     # workspace query
     assert api.tree_attn_workspace(27, 32, 32, 64, 256) == 0
     assert api.tree_attn_workspace(27, 30, 8, 128, 256) == 0
