@@ -19,11 +19,34 @@ namespace {
 constexpr int kAcceptThreads = ENTMTP_T_MAX;
 static_assert(kAcceptThreads == kFinThreads, "the fused kernel runs both halves with one block size");
 
+// A thread's node of the tree (thread i holds node i): what the acceptance
+// needs that does not depend on the target's statistics, so a kernel can
+// fetch it before those are ready.
+struct NodeIn {
+  int tok, parent, depth;
+  uint32_t mask[ENTMTP_MASK_WORDS];
+};
+
+__device__ __forceinline__ NodeIn accept_load(const int* __restrict__ parent,
+                                              const int* __restrict__ depth,
+                                              const uint32_t* __restrict__ mask,
+                                              const int* __restrict__ tok, int T) {
+  NodeIn n{};
+  const int i = threadIdx.x;
+  if (i < T) {
+    n.tok = tok[i];
+    n.parent = parent[i];
+    n.depth = depth[i];
+#pragma unroll
+    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w) n.mask[w] = mask[i * ENTMTP_MASK_WORDS + w];
+  }
+  return n;
+}
+
 // The acceptance of one tree by one workgroup of kAcceptThreads threads.
-__device__ __forceinline__ void accept_core(
-    const int* __restrict__ parent, const int* __restrict__ depth,
-    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
-    const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
+__device__ __forceinline__ void accept_finish(
+    const NodeIn& n, const int* __restrict__ path_tab, int T, int D,
+    const int* __restrict__ amax, const float* __restrict__ top1p,
     int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
     int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
     uint32_t seq) {
@@ -33,7 +56,7 @@ __device__ __forceinline__ void accept_core(
   if (i < ENTMTP_MASK_WORDS) matched[i] = 0u;
   __syncthreads();
   if (i < T) {
-    const bool ok = (i == 0) || (tok[i] == amax[parent[i]]);
+    const bool ok = (i == 0) || (n.tok == amax[n.parent]);
     if (ok) atomicOr(&matched[i >> 5], 1u << (i & 31));
   }
   __syncthreads();
@@ -42,9 +65,8 @@ __device__ __forceinline__ void accept_core(
   if (i < T) {
     bool acc = true;
 #pragma unroll
-    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w)
-      acc = acc && ((mask[i * ENTMTP_MASK_WORDS + w] & ~matched[w]) == 0u);
-    if (acc) key = depth[i] * 1024 + (1023 - i);
+    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w) acc = acc && ((n.mask[w] & ~matched[w]) == 0u);
+    if (acc) key = n.depth * 1024 + (1023 - i);
   }
 #pragma unroll
   for (int off = 32; off >= 1; off >>= 1) key = max(key, __shfl_xor(key, off, 64));
@@ -70,6 +92,18 @@ __device__ __forceinline__ void accept_core(
       __hip_atomic_store(&mirror->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
+}
+
+__device__ __forceinline__ void accept_core(
+    const int* __restrict__ parent, const int* __restrict__ depth,
+    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
+    const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
+    int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
+    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
+    uint32_t seq) {
+  const NodeIn n = accept_load(parent, depth, mask, tok, T);
+  accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, path_cap, bonus, best_p,
+                mirror, seq);
 }
 
 __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
@@ -125,6 +159,8 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
     const int* __restrict__ tok, int* __restrict__ accept_len, int* __restrict__ path_out,
     int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
     uint32_t seq) {
+  // the tree's own inputs are fetched while the partials merge
+  const NodeIn n = accept_load(parent, depth, mask, tok, T);
   finalize_node(part, G, inv_temp, entropy, top1p, amax);
   if (T > 1) {
     __shared__ int s_last;
@@ -138,8 +174,8 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
   } else {
     __syncthreads();   // a single block: its own statistics, via LDS ordering
   }
-  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, D + 1,
-              bonus, best_p, mirror, seq);
+  accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, D + 1, bonus, best_p, mirror,
+                seq);
 }
 
 }  // namespace

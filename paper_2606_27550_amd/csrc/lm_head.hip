@@ -622,13 +622,25 @@ __global__ __launch_bounds__(kFinThreads) void stats_finalize_kernel(
 // whole multiple of the CU count, so that every CU streams the same number
 // of bytes (a partial extra round of workgroups on a few CUs costs ~20% at
 // 7B shapes).
-int hyb_grid(int V) {
+int hyb_grid_uncached(int V, int cus) {
   constexpr int rows = 16 * kHybWaves;
-  const int cus = device_cus();
   const int max_g = (V + 3) / 4;
   int G = cus;
   while (G < max_g && max_slice(V, G) > rows) G += cus;
   return G < max_g ? G : max_g;
+}
+
+// (The search above walks every slice; a call in the step's critical path
+// takes the last answer for the same CU count and vocabulary instead.)
+int hyb_grid(int V) {
+  thread_local int last_cus = -1, last_V = -1, last_G = 0;
+  const int cus = device_cus();
+  if (cus != last_cus || V != last_V) {
+    last_G = hyb_grid_uncached(V, cus);
+    last_cus = cus;
+    last_V = V;
+  }
+  return last_G;
 }
 
 template <int NT, int S, int NCH, bool STATS = false>

@@ -97,6 +97,19 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(BatchArgs p) {
   const int u = blockIdx.y * blockDim.x + threadIdx.x;
   const int Hq = p.Hq, Hkv = p.Hkv, G = p.G, T = sq.T, L = sq.L, cap = p.cap;
   const int nq = Hq * HALF, nk = Hkv * HALF, nv = Hkv * (HD / 8);
+  // the block's node sits at one position, so its HALF rotation angles are
+  // shared by every head: computed once per block
+  __shared__ double s_cos[HALF], s_sin[HALF];
+  if (p.theta > 0.0) {
+    if (threadIdx.x < HALF) {
+      // position prefix_len + depth(i), pair (c, c + d/2) turned by pos * theta^(-2c/d)
+      const int c = threadIdx.x;
+      const double pos = static_cast<double>(L) + static_cast<double>(sq.depth[i]);
+      const double ang = pos * pow(p.theta, -2.0 * c / HD);
+      sincos(ang, &s_sin[c], &s_cos[c]);
+    }
+    __syncthreads();
+  }
   if (u >= nq + nk + nv) return;
   if (u >= nq + nk) {  // value copy -> cache slot L + i
     const int w = u - nq - nk;
@@ -114,11 +127,7 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(BatchArgs p) {
                              (static_cast<size_t>(head / G) * sq.rows_pad + (head % G) * T + i) * HD
                        : sq.kc + (static_cast<size_t>(head) * cap + L + i) * HD;
   if (p.theta > 0.0) {
-    // position prefix_len + depth(i), pair (c, c + d/2) turned by pos * theta^(-2c/d)
-    const double pos = static_cast<double>(L) + static_cast<double>(sq.depth[i]);
-    const double ang = pos * pow(p.theta, -2.0 * c / HD);
-    double sn, cs;
-    sincos(ang, &sn, &cs);
+    const double sn = s_sin[c], cs = s_cos[c];
     const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
     dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * cs - hi * sn));
     dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * cs + lo * sn));
