@@ -50,6 +50,9 @@ def parse():
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--fixed-topo", type=int, default=-1,
                     help="disable the scheduler and use this bank entry every step")
+    ap.add_argument("--gpu-scheduler", action="store_true",
+                    help="run the ladder on the GPU (no result read per step) instead of on "
+                         "the host; the same decisions")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 256 MiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
@@ -146,9 +149,16 @@ def main():
     # LM-head weight copy, all sharing the caches; the statistics come from
     # the LM head's accumulators, so no logits are materialised
     run_stream = torch.cuda.Stream()
+    # the ladder runs on the host (one result read per step, as in the paper's
+    # loop) or, with --gpu-scheduler, on the GPU for the growing-prefix
+    # workload (the same decisions); a fixed topology is a ladder that never
+    # moves
+    on_gpu = grows and args.gpu_scheduler
+    tau_on, tau_off = (0.8, 0.6) if args.fixed_topo < 0 else (float("inf"), float("-inf"))
     st = [api.Step(bank, k_cache, v_cache, w, Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax,
-                   scale=scale, rope_theta=theta, keep_logits=False, stream=run_stream)
-          for w in W]
+                   scale=scale, rope_theta=theta, keep_logits=False, tau_on=tau_on,
+                   tau_off=tau_off, stream=run_stream)
+          for w in (W[:1] if on_gpu else W)]
     torch.cuda.synchronize()
     out = torch.empty((Tmax, Hq, d), dtype=bf, device=dev)
 
@@ -163,6 +173,10 @@ def main():
         am = st[0].argmax.cpu().numpy()
         e["tok"] = [synth.draft_tokens(trees[k], am, e["u"], e["r"], wl.p_acc) for k in range(n_topo)]
         e["tok_dev"] = [torch.from_numpy(t).to(dev) for t in e["tok"]]
+        table = np.zeros((n_topo, Tmax), np.int32)
+        for k, t in enumerate(e["tok"]):
+            table[k, : len(t)] = t
+        e["drafts_dev"] = torch.from_numpy(table).to(dev)
     del lg
     torch.cuda.synchronize()
 
@@ -171,8 +185,13 @@ def main():
     handles = [s_.handle for s_ in st]
     out_p = P_(out.data_ptr())
     pool_p = [{"q": P_(e["q"].data_ptr()), "kt": P_(e["kt"].data_ptr()), "vt": P_(e["vt"].data_ptr()),
-               "x": P_(e["x"].data_ptr()), "tok": [P_(t.data_ptr()) for t in e["tok_dev"]]}
+               "x": P_(e["x"].data_ptr()), "tok": [P_(t.data_ptr()) for t in e["tok_dev"]],
+               "drafts": P_(e["drafts_dev"].data_ptr())}
               for e in pool]
+    W_p = [P_(w.data_ptr()) for w in W]
+    total = args.warmup + args.steps
+    steplog = torch.full((total, 4), -1, dtype=torch.int32, device=dev)
+    log_p = [P_(steplog[t].data_ptr()) for t in range(total)]
     Ts = bank.T
     a_c, b_c, s_c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
     a_r, b_r, s_r = ctypes.byref(a_c), ctypes.byref(b_c), ctypes.byref(s_c)
@@ -182,6 +201,12 @@ def main():
             raise api.EntmtpError(rc, api.last_error())
 
     state = {"L": L0, "rung": 0 if args.fixed_topo < 0 else args.fixed_topo, "s": 0.0}
+
+    def step_gpu(t, ev=(None, None)):
+        # nothing is read back: the next step's tree and prefix stay on the GPU
+        e = pool_p[t % P]
+        chk(lib.entmtp_step_launch_device(handles[0], e["q"], e["kt"], e["vt"], out_p, e["x"],
+                                          W_p[t % len(W_p)], e["drafts"], log_p[t], ev[0], ev[1]))
 
     def step(t, ev=(None, None)):
         L = state["L"] if grows else L0
@@ -198,8 +223,11 @@ def main():
         return Ts[topo], L, a, s, topo
 
     # ---------------------------------------------------------- warmup
+    if on_gpu:
+        chk(lib.entmtp_step_device_start(handles[0], state["rung"], L0))
+    run = step_gpu if on_gpu else step
     for t in range(args.warmup):
-        step(t)
+        run(t)
     torch.cuda.synchronize()
 
     # ---------------------------------------------------------- timed
@@ -214,9 +242,14 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for t in range(K):
-        trace.append(step(args.warmup + t, ev_p[t]))
+        trace.append(run(args.warmup + t, ev_p[t]))
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    if on_gpu:   # the steps' (tree, prefix, accept length, s) as the GPU logged them
+        lg = steplog.cpu().numpy()[args.warmup:]
+        trace = [(bank.T[int(r)], int(L), int(a), float(np.int32(sb).view(np.float32)), int(r))
+                 for r, L, a, sb in lg]
+        state["L"] = int(lg[-1, 1] + lg[-1, 2] + 1)
 
     lm_ms = [a.elapsed_time(b) for a, b in events]
     by_T = {}
@@ -267,8 +300,9 @@ def main():
         "config": {"workload": wl.name, "batch": 1, "heads": Hq, "kv_heads": Hkv, "head_dim": d,
                    "hidden": hid, "vocab": V, "prefix_len_start": L0,
                    "prefix_len_end": state["L"], "bank_T": bank.T,
-                   "scheduler": "hysteretic ladder on=0.8 off=0.6" if args.fixed_topo < 0
-                   else f"fixed topo {args.fixed_topo}",
+                   "scheduler": ("hysteretic ladder on=0.8 off=0.6" if args.fixed_topo < 0
+                                 else f"fixed topo {args.fixed_topo}")
+                   + (", on the GPU" if on_gpu else ", on the host"),
                    "T_histogram": {str(k): v for k, v in sorted(Tcount.items())},
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},

@@ -388,6 +388,8 @@ int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
  *              entmtp_step_create clears with an asynchronous memset on the
  *              stream)
  *   stream     the HIP stream every launch goes to (NULL: the null stream)
+ *   tau_on, tau_off   thresholds of the hysteretic ladder (§4 "Policy") for
+ *              device-scheduled steps, tau_off <= tau_on (unused otherwise)
  */
 typedef struct entmtp_step_config {
   int32_t n_layers, Hq, Hkv, d, cap, tree_rows;
@@ -410,6 +412,7 @@ typedef struct entmtp_step_config {
   void* workspace;
   size_t workspace_bytes;
   void* stream;
+  float tau_on, tau_off;
 } entmtp_step_config;
 
 typedef struct entmtp_step entmtp_step;
@@ -467,6 +470,39 @@ int32_t entmtp_step_launch(entmtp_step* step, int32_t topo, int32_t prefix_len,
  */
 int32_t entmtp_step_wait(entmtp_step* step, int32_t* accept_len, int32_t* bonus,
                          float* best_top1p, double timeout_s);
+
+/*
+ * Device-scheduled steps: the tree choice of §4 moved next to the statistics
+ * it reads.  The acceptance kernel of a step also runs the hysteretic ladder
+ * (rung + 1 when s > tau_on, rung - 1 when s <= tau_off, clamped to the bank,
+ * which must be sorted by size) on s = top-1 probability at the accepted node,
+ * and stores the next step's tree and prefix length (L + accept_len + 1) in
+ * device memory, so the host enqueues step after step without reading
+ * anything back.  The decisions are those of entmtp_ladder_next on the same s.
+ *
+ * entmtp_step_device_start: sets the device state to tree `topo` at
+ * prefix_len (asynchronously, on the configured stream).  Requires a bank of
+ * trees of at most 128 nodes.  Errors: EINVAL, ERANGE, EHIP.
+ *
+ * entmtp_step_launch_device: enqueues one step for the tree the device state
+ * holds (the same kernels as entmtp_step_launch, sized for the largest tree).
+ * Inputs as for entmtp_step_launch, except
+ *   w_lm    the LM-head weight for this step ([V][hid] bf16, NULL: the
+ *           configured one)
+ *   drafts  [K][tree_rows] int32 (device): the draft tokens for every bank
+ *           tree (row k for tree k; the step reads the chosen tree's row)
+ *   log     device int32[4] or NULL: receives (tree, prefix length,
+ *           accept_len, s as float bits) of this step
+ * The caller sizes cap for the whole run (prefix growth included); a step
+ * whose prefix length plus tree would exceed cap computes no attention.
+ * Errors: EINVAL (no entmtp_step_device_start yet), EHIP.
+ */
+int32_t entmtp_step_device_start(entmtp_step* step, int32_t topo, int32_t prefix_len);
+int32_t entmtp_step_launch_device(entmtp_step* step, const entmtp_bf16* q,
+                                  const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                                  entmtp_bf16* out, const entmtp_bf16* hidden,
+                                  const entmtp_bf16* w_lm, const int32_t* drafts, int32_t* log,
+                                  void* ev_lm_begin, void* ev_lm_end);
 
 #ifdef __cplusplus
 }

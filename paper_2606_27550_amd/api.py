@@ -31,7 +31,7 @@ class StepConfig(ctypes.Structure):
                 ("logits", _c_p), ("entropy", _c_p), ("top1p", _c_p), ("argmax", _c_p),
                 ("accept_len", _c_p), ("bonus", _c_p), ("best_top1p", _c_p), ("path", _c_p),
                 ("path_capacity", _c_i32), ("workspace", _c_p), ("workspace_bytes", _c_sz),
-                ("stream", _c_p)]
+                ("stream", _c_p), ("tau_on", _c_f32), ("tau_off", _c_f32)]
 
 
 # name -> (restype, argtypes), mirroring include/entmtp.h
@@ -75,6 +75,8 @@ _SIGNATURES = {
                                     _c_p]),
     "entmtp_step_wait": (_c_i32, [_c_p, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
                                   ctypes.POINTER(_c_f32), ctypes.c_double]),
+    "entmtp_step_device_start": (_c_i32, [_c_p, _c_i32, _c_i32]),
+    "entmtp_step_launch_device": (_c_i32, [_c_p] * 11),
 }
 
 
@@ -493,7 +495,7 @@ class Step:
 
     def __init__(self, bank: Bank, k_cache, v_cache, w_lm, *, n_layers=1, Hq, Hkv, d=HEAD_DIM,
                  cap, tree_rows, scale, rope_theta, inv_temp=1.0, cache_layer_stride=0,
-                 keep_logits=True, stream=None):
+                 keep_logits=True, tau_on=0.8, tau_off=0.6, stream=None):
         import torch
         dev = k_cache.device
         V, hid = w_lm.shape
@@ -517,7 +519,7 @@ class Step:
                        self.entropy.data_ptr(),
                        self.top1p.data_ptr(), self.argmax.data_ptr(), self.accept_len.data_ptr(),
                        self.bonus.data_ptr(), self.best_top1p.data_ptr(), self.path.data_ptr(),
-                       D + 1, None, 0, _stream(stream).value)
+                       D + 1, None, 0, _stream(stream).value, tau_on, tau_off)
         need = int(lib.entmtp_step_workspace(bank.handle, ctypes.byref(c)))
         if need == 0:
             _check(lib.entmtp_step_create(bank.handle, ctypes.byref(c), ctypes.byref(_c_p())))
@@ -546,6 +548,17 @@ class Step:
         _check(lib.entmtp_step_wait(self._h, ctypes.byref(self._a), ctypes.byref(self._b),
                                     ctypes.byref(self._s), timeout_s))
         return self._a.value, self._b.value, self._s.value
+
+    def device_start(self, topo: int, prefix_len: int) -> None:
+        _check(lib.entmtp_step_device_start(self._h, topo, prefix_len))
+
+    def launch_device(self, q, k_tree, v_tree, out, hidden, drafts, log=None, w_lm=None,
+                      ev_lm_begin=None, ev_lm_end=None) -> None:
+        """One device-scheduled step; drafts [K, tree_rows] int32, log int32[4] or None."""
+        ev = [None if e is None else _c_p(e.cuda_event) for e in (ev_lm_begin, ev_lm_end)]
+        _check(lib.entmtp_step_launch_device(self._h, _p(q), _p(k_tree), _p(v_tree), _p(out),
+                                             _p(hidden), _p(w_lm), _p(drafts), _p(log), ev[0],
+                                             ev[1]))
 
     def close(self):
         if getattr(self, "_h", None):

@@ -43,8 +43,9 @@ __device__ __forceinline__ NodeIn accept_load(const int* __restrict__ parent,
   return n;
 }
 
-// The acceptance of one tree by one workgroup of kAcceptThreads threads.
-__device__ __forceinline__ void accept_finish(
+// The acceptance of one tree by one workgroup of kAcceptThreads threads;
+// returns (in every thread) depth(best) * 1024 + (1023 - best).
+__device__ __forceinline__ int accept_finish(
     const NodeIn& n, const int* __restrict__ path_tab, int T, int D,
     const int* __restrict__ amax, const float* __restrict__ top1p,
     int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
@@ -92,6 +93,7 @@ __device__ __forceinline__ void accept_finish(
       __hip_atomic_store(&mirror->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
     }
   }
+  return key;
 }
 
 __device__ __forceinline__ void accept_core(
@@ -102,8 +104,8 @@ __device__ __forceinline__ void accept_core(
     int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
     uint32_t seq) {
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
-  accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, path_cap, bonus, best_p,
-                mirror, seq);
+  (void)accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, path_cap, bonus,
+                      best_p, mirror, seq);
 }
 
 __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
@@ -174,8 +176,62 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
   } else {
     __syncthreads();   // a single block: its own statistics, via LDS ordering
   }
-  accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, D + 1, bonus, best_p, mirror,
-                seq);
+  (void)accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, D + 1, bonus, best_p,
+                      mirror, seq);
+}
+
+// The same for a tree the device chose: the tree, its drafts and the prefix
+// length come from *dv.cur; the last block also runs the ladder and writes
+// the next step's state (tree, node count, prefix length).
+__global__ __launch_bounds__(kAcceptThreads) void finalize_accept_device_kernel(
+    FinAccDevice dv, const uint8_t* __restrict__ arena, const StatPart* __restrict__ part, int G,
+    float inv_temp, float* __restrict__ entropy, float* __restrict__ top1p,
+    int* __restrict__ amax, unsigned* __restrict__ counter, int* __restrict__ accept_len,
+    int* __restrict__ path_out, int path_cap, int* __restrict__ bonus, float* __restrict__ best_p,
+    StepMirror* __restrict__ mirror, uint32_t seq) {
+  const DevStep st = *dv.cur;
+  const int T = st.T;
+  if (static_cast<int>(blockIdx.x) >= T) return;   // the grid covers the largest tree
+  const DevTopo* t = dv.topos + st.rung;
+  const int* parent = reinterpret_cast<const int*>(arena + t->off_parent);
+  const int* depth = reinterpret_cast<const int*>(arena + t->off_depth);
+  const uint32_t* mask = reinterpret_cast<const uint32_t*>(arena + t->off_mask);
+  const int* path_tab = reinterpret_cast<const int*>(arena + t->off_path);
+  const int D = t->D;
+  const int* tok = dv.drafts + static_cast<size_t>(st.rung) * dv.tree_rows;
+  const NodeIn n = accept_load(parent, depth, mask, tok, T);
+  finalize_node(part, G, inv_temp, entropy, top1p, amax);
+  if (T > 1) {
+    __shared__ int s_last;
+    __threadfence();
+    __syncthreads();
+    if (threadIdx.x == 0) s_last = atomicAdd(counter, 1u) == static_cast<unsigned>(T - 1);
+    __syncthreads();
+    if (!s_last) return;
+    __threadfence();
+    if (threadIdx.x == 0) *counter = 0u;
+  } else {
+    __syncthreads();
+  }
+  const int key = accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, path_cap,
+                                bonus, best_p, mirror, seq);
+  if (threadIdx.x == 0) {
+    const int a = key >> 10, best = 1023 - (key & 1023);
+    const float s = top1p[best];
+    const int next = ladder_step(st.rung, dv.n_topo, s, dv.tau_on, dv.tau_off);
+    DevStep nx;
+    nx.rung = next;
+    nx.T = dv.topos[next].T;
+    nx.L = st.L + a + 1;
+    nx.pad = 0;
+    *dv.next = nx;
+    if (dv.log) {
+      dv.log[0] = st.rung;
+      dv.log[1] = st.L;
+      dv.log[2] = a;
+      dv.log[3] = __float_as_int(s);
+    }
+  }
 }
 
 }  // namespace
@@ -196,6 +252,19 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
                      d.D, draft_tokens, argmax, top1p, accept_len, path, bonus, best_top1p,
                      mirror, seq);
   return launch_status("accept launch");
+}
+
+int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevice& dv,
+                                      const void* partials, int32_t V, float inv_temp,
+                                      float* entropy, float* top1p, int32_t* argmax,
+                                      unsigned* counter, int32_t* accept_len, int32_t* path,
+                                      int32_t path_capacity, int32_t* bonus, float* best_top1p,
+                                      StepMirror* mirror, uint32_t seq, hipStream_t stream) {
+  hipLaunchKernelGGL(finalize_accept_device_kernel, dim3(dv.t_max), dim3(kAcceptThreads), 0, stream,
+                     dv, bank->arena, static_cast<const StatPart*>(partials), stats_slices(V),
+                     inv_temp, entropy, top1p, argmax, counter, accept_len, path, path_capacity,
+                     bonus, best_top1p, mirror, seq);
+  return launch_status("finalize_accept (device-scheduled) launch");
 }
 
 int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,

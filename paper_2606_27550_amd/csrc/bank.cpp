@@ -219,7 +219,5 @@ extern "C" int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, fl
                    rung, n_rungs);
   ENTMTP_CHECK_ARG(tau_off <= tau_on, ENTMTP_EINVAL, "tau_off %g > tau_on %g",
                    static_cast<double>(tau_off), static_cast<double>(tau_on));
-  if (s > tau_on) return rung + 1 < n_rungs ? rung + 1 : rung;
-  if (s <= tau_off) return rung > 0 ? rung - 1 : 0;
-  return rung;
+  return ladder_step(rung, n_rungs, s, tau_on, tau_off);
 }

@@ -56,6 +56,56 @@ namespace entmtp {
 // Validates (bank, topo) for a kernel launch; returns 0 or an error status.
 int32_t check_device_bank(const entmtp_bank* bank, int32_t topo);
 
+// Device-side state of a decode loop whose tree choice runs on the GPU (§4's
+// policy moved next to the statistics it reads): one slot per step parity,
+// the step with parity p reads slot p and its acceptance writes slot p ^ 1.
+struct DevStep {
+  int rung;   // bank index of the step's tree
+  int T;      // its node count
+  int L;      // prefix length
+  int pad;
+};
+
+// A bank tree as the device-scheduled kernels find it: sizes and byte
+// offsets of its arrays in the bank arena.
+struct DevTopo {
+  int T, D;
+  int off_parent, off_depth, off_mask, off_path;
+  int pad[2];
+  // attention split count for this tree by split bound (index 1..32; the
+  // lone-sequence choice depends on the prefix length only through it)
+  unsigned char splits[36];
+};
+
+// The hysteretic ladder of §4 over a bank sorted by size: climb one rung when
+// s > tau_on, descend one when s <= tau_off, else stay (clamped to the bank).
+__host__ __device__ inline int ladder_step(int rung, int n_rungs, float s, float tau_on,
+                                           float tau_off) {
+  if (s > tau_on) return rung + 1 < n_rungs ? rung + 1 : rung;
+  if (s <= tau_off) return rung > 0 ? rung - 1 : 0;
+  return rung;
+}
+
+// Grids of the attention for a tree chosen on the device: sized for the
+// largest plan any bank tree can need at prefix lengths up to cap - T.
+struct DevAttnShape {
+  int rows = 0, items = 0, merge_blocks = 0, T_max = 0;
+  size_t need = 0;   // workspace bytes
+};
+
+int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, DevAttnShape* out);
+
+// Fills DevTopo::splits of every bank tree for the current device.
+void attn_device_splits(const entmtp_bank* bank, int Hq, int Hkv, DevTopo* topos);
+
+// One attention layer (as entmtp_tree_attn) for the tree and prefix length
+// held in *dev; topos is the bank's device descriptor table.
+int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const DevTopo* topos,
+                           const DevAttnShape& sh, const entmtp_bf16* q, const entmtp_bf16* k_tree,
+                           const entmtp_bf16* v_tree, entmtp_bf16* k_cache, entmtp_bf16* v_cache,
+                           int cap, int Hq, int Hkv, float scale, float rope_theta,
+                           entmtp_bf16* out, void* workspace, hipStream_t stream);
+
 // Result of one verification step as the host reads it: written by the accept
 // kernel into coherent pinned host memory, fields first, then `seq` with
 // system-scope release, so a host that sees `seq` also sees the fields.
@@ -73,6 +123,33 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
                       const int32_t* argmax, const float* top1p, int32_t* accept_len,
                       int32_t* path, int32_t* bonus, float* best_top1p, StepMirror* mirror,
                       uint32_t seq, hipStream_t stream);
+
+// The device-scheduled form: the tree is bank entry cur->rung; the drafts of
+// bank tree k are row k of drafts [n_topo][tree_rows]; after accepting, the
+// ladder picks the next tree from s = top1p[best] and writes *next =
+// {rung', T', L + accept_len + 1}; log (4 ints, may be NULL) receives
+// (rung, L, accept_len, s bits); the grid covers t_max nodes.
+struct FinAccDevice {
+  const DevStep* cur;
+  DevStep* next;
+  const DevTopo* topos;
+  const int32_t* drafts;
+  int32_t tree_rows, n_topo, t_max;
+  float tau_on, tau_off;
+  int32_t* log;
+};
+int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevice& dv,
+                                      const void* partials, int32_t V, float inv_temp,
+                                      float* entropy, float* top1p, int32_t* argmax,
+                                      unsigned* counter, int32_t* accept_len, int32_t* path,
+                                      int32_t path_capacity, int32_t* bonus, float* best_top1p,
+                                      StepMirror* mirror, uint32_t seq, hipStream_t stream);
+
+// Compaction (as entmtp_kv_compact, one sequence) at the prefix length dev->L.
+int32_t launch_compact_device(const DevStep* dev, const int32_t* path, int32_t path_capacity,
+                              const int32_t* accept_len, entmtp_bf16* k_cache,
+                              entmtp_bf16* v_cache, int32_t n_layers, int64_t layer_stride,
+                              int32_t Hkv, int32_t cap, int32_t d, hipStream_t s);
 
 // Finishes the LM head's statistics partials for every node of tree `topo`
 // and, in the same launch, accepts the tree (as launch_accept).  `counter`

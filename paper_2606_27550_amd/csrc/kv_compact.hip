@@ -24,6 +24,7 @@ struct CompactArgs {
   int L[ENTMTP_B_MAX];
   const int* path;       // [B][path_cap]
   const int* accept_len; // [B]
+  const DevStep* dev;    // when set, sequence 0's prefix length is dev->L
   long long layer_stride;
   int path_cap, n_layers, Hkv, cap, d;
 };
@@ -33,7 +34,7 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs
   const int per_seq = p.n_layers * p.Hkv;
   const int b = blockIdx.x / per_seq, rest = blockIdx.x % per_seq;
   const int layer = rest / p.Hkv, g = rest % p.Hkv;
-  const int d = p.d, cap = p.cap, L = p.L[b];
+  const int d = p.d, cap = p.cap, L = p.dev ? p.dev->L : p.L[b];
   const int* path = p.path + static_cast<size_t>(b) * p.path_cap;
   const size_t base = static_cast<size_t>(layer) * p.layer_stride + static_cast<size_t>(g) * cap * d;
   int a = p.accept_len[b];
@@ -86,6 +87,29 @@ int32_t launch_compact(const CompactArgs& a, int B, hipStream_t s) {
   hipLaunchKernelGGL(kv_compact_kernel, dim3(B * a.n_layers * a.Hkv), dim3(kCompactThreads), 0, s, a);
   return launch_status("kv_compact launch");
 }
+
+}  // namespace
+
+int32_t launch_compact_device(const DevStep* dev, const int32_t* path, int32_t path_capacity,
+                              const int32_t* accept_len, entmtp_bf16* k_cache,
+                              entmtp_bf16* v_cache, int32_t n_layers, int64_t layer_stride,
+                              int32_t Hkv, int32_t cap, int32_t d, hipStream_t s) {
+  CompactArgs a{};
+  a.kc[0] = k_cache;
+  a.vc[0] = v_cache;
+  a.path = path;
+  a.accept_len = accept_len;
+  a.dev = dev;
+  a.layer_stride = static_cast<long long>(layer_stride);
+  a.path_cap = path_capacity;
+  a.n_layers = n_layers;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  a.d = d;
+  return launch_compact(a, 1, s);
+}
+
+namespace {
 
 }  // namespace
 }  // namespace entmtp

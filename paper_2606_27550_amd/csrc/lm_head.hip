@@ -393,33 +393,32 @@ struct HybShape {
   static_assert(NXI % kHybWaves == 0, "X split");
 };
 
+// The body of the streaming LM-head kernel for node tile NT (16 * NT nodes per
+// pass, starting at node j0).  The kernels that call it own the LDS: one
+// object per X ring slot, so that the compiler can tell the slot being read
+// from the slots the copies in flight write to (the body is inlined, so the
+// slots stay distinct objects), and the per-wave transposition tiles.
+// Precondition (host dispatch): hid is a multiple of S * 128, and equals
+// NCH * 128 when NCH > 0 (the K loop is then unrolled completely: no
+// loop-carried stage registers, so the compiler's load bookkeeping stays
+// exact and it never drains the pipeline).
 template <int NT, int S, int NCH, bool STATS>
-__global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
-    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
-    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
+__device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8_t* xslot2,
+                                         uint8_t* xslot3, uint8_t* tpose,
+                                         const uint16_t* __restrict__ X,
+                                         const uint16_t* __restrict__ W, float* __restrict__ logits,
+                                         int T, int hid, int V, int G, float inv_temp,
+                                         StatPart* __restrict__ part, int j0, int sl) {
   using Sh = HybShape<NT>;
-  // precondition (host dispatch): hid is a multiple of S * 128, and equals
-  // NCH * 128 when NCH > 0 (the K loop is then unrolled completely: no
-  // loop-carried stage registers, so the compiler's load bookkeeping stays
-  // exact and it never drains the pipeline)
-  constexpr int XSTAGE = Sh::TP * kL3RowBytes;            // bytes of one X stage
   static_assert(S >= 2 && S <= 4, "two to four X ring slots");
-  // one LDS object per X ring slot, so that the compiler can tell the slot
-  // being read from the slots the copies in flight write to
-  __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t xslot2[S > 2 ? XSTAGE : 16];
-  __shared__ __attribute__((aligned(16))) uint8_t xslot3[S > 3 ? XSTAGE : 16];
   uint8_t* const xring[4] = {xslot0, xslot1, xslot2, xslot3};
-  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
 
-  const int r0 = slice_begin(blockIdx.x, G, V);
-  const int r1 = slice_begin(blockIdx.x + 1, G, V);
-  const int j0 = blockIdx.y * Sh::TP;
+  const int r0 = slice_begin(sl, G, V);
+  const int r1 = slice_begin(sl + 1, G, V);
   if (r0 >= r1) {  // empty slice (tiny V): the whole workgroup leaves
     if constexpr (STATS)
       if (threadIdx.x < Sh::TP && j0 + threadIdx.x < T)
-        part[static_cast<size_t>(j0 + threadIdx.x) * G + blockIdx.x] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
+        part[static_cast<size_t>(j0 + threadIdx.x) * G + sl] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
     return;
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -429,7 +428,7 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
   const int nch = NCH > 0 ? NCH : hid / kL3Bk;
   // workgroups walk K in rotated order so that CUs do not all stream the
   // same column band at once
-  const int rot = static_cast<int>((static_cast<unsigned>(blockIdx.x) * 7u) % static_cast<unsigned>(nch));
+  const int rot = static_cast<int>((static_cast<unsigned>(sl) * 7u) % static_cast<unsigned>(nch));
 
   // W: instruction i, lane l -> row 4i + l/16, chunk l%16 (rows past the
   // slice read an in-bounds row of this slice; their outputs are not stored)
@@ -582,9 +581,91 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
       StatPart acc_p = wpart[c];
 #pragma unroll
       for (int w = 1; w < kHybWaves; ++w) part_merge(acc_p, wpart[w * kStride + c], inv_temp);
-      part[static_cast<size_t>(j0 + c) * G + blockIdx.x] = acc_p;
+      part[static_cast<size_t>(j0 + c) * G + sl] = acc_p;
     }
   }
+}
+
+template <int NT, int S, int NCH, bool STATS>
+__global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
+  constexpr int XSTAGE = HybShape<NT>::TP * kL3RowBytes;   // bytes of one X stage
+  __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot2[S > 2 ? XSTAGE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot3[S > 3 ? XSTAGE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
+  hyb_body<NT, S, NCH, STATS>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
+                              inv_temp, part, blockIdx.y * HybShape<NT>::TP, blockIdx.x);
+}
+
+// The same kernel with fewer workgroups than slices: workgroup b takes slices
+// b, b + gridDim.x, ... in turn (one resident workgroup per CU leaves the
+// other half of the CU to concurrent work).
+template <int NT, int S, int NCH, bool STATS>
+__global__ __launch_bounds__(kHybThreads) void lm_head_hyb_loop_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
+  constexpr int XSTAGE = HybShape<NT>::TP * kL3RowBytes;
+  __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot2[S > 2 ? XSTAGE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot3[S > 3 ? XSTAGE : 16];
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
+  for (int sl = blockIdx.x; sl < G; sl += gridDim.x) {
+    if (sl != static_cast<int>(blockIdx.x)) __syncthreads();   // the previous slice is done with the LDS
+    hyb_body<NT, S, NCH, STATS>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
+                                inv_temp, part, blockIdx.y * HybShape<NT>::TP, sl);
+  }
+}
+
+// The same kernel with the node count read from device memory (*T_dev), for
+// steps whose tree is chosen on the GPU.  Two kernels share the range so that
+// each keeps the LDS of its own node tile (and with it room on the CUs for
+// the attention running alongside): the small one takes trees of up to 32
+// nodes (16- or 32-node tile), the large one trees of 33..128 nodes (one
+// 128-node pass); each leaves at once when the tree is not in its range.
+// Statistics partials only.
+template <int NCH>
+__global__ __launch_bounds__(kHybThreads) void lm_head_dyn_small_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    const int* __restrict__ T_dev, int hid, int V, int G, float inv_temp,
+    StatPart* __restrict__ part) {
+  constexpr int XSTAGE = HybShape<2>::TP * kL3RowBytes;
+  __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot2[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot3[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
+  const int T = __builtin_amdgcn_readfirstlane(*T_dev);
+  if (T > 32) return;
+  // slices b, b + gridDim.x, ...: the grid is half the slices, so one
+  // workgroup per CU streams W and the attention overlapping it fits beside
+  for (int sl = blockIdx.x; sl < G; sl += gridDim.x) {
+    if (sl != static_cast<int>(blockIdx.x)) __syncthreads();
+    if (T <= 16)
+      hyb_body<1, 4, NCH, true>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
+                                inv_temp, part, 0, sl);
+    else
+      hyb_body<2, 4, NCH, true>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
+                                inv_temp, part, 0, sl);
+  }
+}
+
+template <int NCH>
+__global__ __launch_bounds__(kHybThreads) void lm_head_dyn_large_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    const int* __restrict__ T_dev, int hid, int V, int G, float inv_temp,
+    StatPart* __restrict__ part) {
+  constexpr int XSTAGE = HybShape<8>::TP * kL3RowBytes;
+  __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
+  const int T = __builtin_amdgcn_readfirstlane(*T_dev);
+  if (T > 32)
+    hyb_body<8, 2, NCH, true>(xslot0, xslot1, xslot0, xslot1, tpose, X, W, logits, T, hid, V, G,
+                              inv_temp, part, 0, blockIdx.x);
 }
 
 // Largest vocabulary slice slice_begin() produces for G workgroups (host copy
@@ -713,6 +794,53 @@ int32_t launch_lm(const uint16_t* X, const uint16_t* W, float* logits, int T, in
 }  // namespace
 
 int stats_slices(int V) { return hyb_grid(V); }
+
+int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, int T, int hid,
+                             int V, float inv_temp, float* logits, void* partials, hipStream_t s) {
+  if (T > 32 || hid % (4 * kL3Bk))
+    return entmtp_verify_logits_partials(hidden, w_lm, T, hid, V, inv_temp, logits, partials,
+                                         static_cast<size_t>(T) * hyb_grid(V) * sizeof(StatPart), s);
+  const int G = hyb_grid(V);
+  const dim3 grid((G + 1) / 2);
+  auto* part = static_cast<StatPart*>(partials);
+  const auto* X = reinterpret_cast<const uint16_t*>(hidden);
+  const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
+  auto go = [&](auto k) {
+    hipLaunchKernelGGL(k, grid, dim3(kHybThreads), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
+  };
+  if (hid == 32 * kL3Bk) {
+    if (T <= 16) go(lm_head_hyb_loop_kernel<1, 4, 32, true>); else go(lm_head_hyb_loop_kernel<2, 4, 32, true>);
+  } else if (hid == 40 * kL3Bk) {
+    if (T <= 16) go(lm_head_hyb_loop_kernel<1, 4, 40, true>); else go(lm_head_hyb_loop_kernel<2, 4, 40, true>);
+  } else {
+    if (T <= 16) go(lm_head_hyb_loop_kernel<1, 4, 0, true>); else go(lm_head_hyb_loop_kernel<2, 4, 0, true>);
+  }
+  return launch_status("verify_logits (step) launch");
+}
+
+int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                 const int* T_dev, int T_max, int hid, int V, float inv_temp,
+                                 void* partials, hipStream_t s) {
+  if (T_max < 1 || T_max > 128 || hid % (4 * kL3Bk))
+    return fail(ENTMTP_EINVAL, "device-sized LM head: T_max %d (at most 128), hid %d (multiple of %d)",
+                T_max, hid, 4 * kL3Bk);
+  const int G = hyb_grid(V);
+  auto* part = static_cast<StatPart*>(partials);
+  const auto* X = reinterpret_cast<const uint16_t*>(hidden);
+  const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
+  auto both = [&](auto small, auto large) -> int32_t {
+    hipLaunchKernelGGL(small, dim3((G + 1) / 2), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev,
+                       hid, V, G, inv_temp, part);
+    if (int32_t rc = launch_status("verify_logits (device-sized, small) launch")) return rc;
+    if (T_max <= 32) return ENTMTP_OK;   // no bank tree needs the large kernel
+    hipLaunchKernelGGL(large, dim3(G), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev, hid, V, G,
+                       inv_temp, part);
+    return launch_status("verify_logits (device-sized, large) launch");
+  };
+  if (hid == 32 * kL3Bk) return both(lm_head_dyn_small_kernel<32>, lm_head_dyn_large_kernel<32>);
+  if (hid == 40 * kL3Bk) return both(lm_head_dyn_small_kernel<40>, lm_head_dyn_large_kernel<40>);
+  return both(lm_head_dyn_small_kernel<0>, lm_head_dyn_large_kernel<0>);
+}
 
 }  // namespace entmtp
 

@@ -82,4 +82,18 @@ __device__ __forceinline__ void finalize_node(const StatPart* __restrict__ part,
 // current device (its grid width).
 int stats_slices(int V);
 
+// The LM head with statistics partials inside a verification step: as
+// entmtp_verify_logits_partials (arguments checked by the step), but for trees
+// of up to 32 nodes with one workgroup per CU looping over two vocabulary
+// slices, which leaves room on every CU for the attention overlapping it.
+int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, int T, int hid,
+                             int V, float inv_temp, float* logits, void* partials, hipStream_t s);
+
+// The LM head with statistics partials (as entmtp_verify_logits_partials,
+// no logits) for a node count the device holds in *T_dev (1 <= T <= T_max
+// <= 128, known only when the kernel runs).
+int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                 const int* T_dev, int T_max, int hid, int V, float inv_temp,
+                                 void* partials, hipStream_t s);
+
 }  // namespace entmtp

@@ -14,8 +14,10 @@
 #include <chrono>
 #include <cmath>
 #include <cstring>
+#include <vector>
 
 #include "common.hpp"
+#include "stats.hpp"
 
 using namespace entmtp;
 
@@ -28,6 +30,10 @@ struct entmtp_step {
   size_t part_offset = 0;      // LM-head statistics partials follow it
   size_t part_bytes = 0;
   size_t counter_offset = 0;   // then one arrival counter (0 between launches)
+  size_t dev_offset = 0;       // then the device-scheduled state: DevStep[2], DevTopo[K]
+  DevAttnShape dshape;         // attention grids for a tree chosen on the device
+  int parity = 0;              // slot of DevStep the next device-scheduled step reads
+  bool dev_started = false;
   StepMirror* host = nullptr;  // pinned, coherent
   StepMirror* dev = nullptr;   // device address of `host`
   hipStream_t side = nullptr;  // attention chain (default priority, non-blocking)
@@ -52,13 +58,14 @@ void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
 }
 
 // Workspace split for a validated configuration; returns the total bytes.
-size_t layout(const entmtp_step_config& c, int32_t T_max, size_t* attn, size_t* part_off,
-              size_t* part, size_t* counter_off) {
+size_t layout(const entmtp_step_config& c, int32_t T_max, int32_t n_topo, size_t* attn,
+              size_t* part_off, size_t* part, size_t* counter_off, size_t* dev_off) {
   *attn = entmtp_tree_attn_workspace(T_max, c.Hq, c.Hkv, c.d, c.cap);
   *part_off = round256(*attn);
   *part = entmtp_stats_partials_bytes(T_max, c.hid, c.V);
   *counter_off = round256(*part_off + *part);
-  return *counter_off + 256;
+  *dev_off = *counter_off + 256;
+  return *dev_off + round256(2 * sizeof(DevStep) + static_cast<size_t>(n_topo) * sizeof(DevTopo));
 }
 
 bool finite_positive(float x) { return x > 0.f && std::isfinite(x); }
@@ -102,6 +109,8 @@ int32_t check_config(const entmtp_bank* bank, const entmtp_step_config* c, int32
                    "acceptance outputs must be non-NULL");
   ENTMTP_CHECK_ARG(c->path_capacity >= *D_max + 1, ENTMTP_EINVAL,
                    "path_capacity = %d below 1 + the bank's depth %d", c->path_capacity, *D_max);
+  ENTMTP_CHECK_ARG(c->tau_off <= c->tau_on, ENTMTP_EINVAL, "tau_off %g > tau_on %g",
+                   static_cast<double>(c->tau_off), static_cast<double>(c->tau_on));
   return ENTMTP_OK;
 }
 
@@ -113,8 +122,9 @@ extern "C" size_t entmtp_step_workspace(const entmtp_bank* bank, const entmtp_st
     clear_error();
     return 0;
   }
-  size_t attn = 0, off = 0, part = 0, coff = 0;
-  const size_t total = layout(*cfg, T_max, &attn, &off, &part, &coff);
+  size_t attn = 0, off = 0, part = 0, coff = 0, doff = 0;
+  const size_t total = layout(*cfg, T_max, static_cast<int32_t>(bank->desc.size()), &attn, &off,
+                              &part, &coff, &doff);
   return attn && part ? total : 0;
 }
 
@@ -125,8 +135,9 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   *out = nullptr;
   int32_t T_max = 0, D_max = 0;
   if (int32_t rc = check_config(bank, cfg, &T_max, &D_max)) return rc;
-  size_t attn = 0, off = 0, part = 0, coff = 0;
-  const size_t total = layout(*cfg, T_max, &attn, &off, &part, &coff);
+  size_t attn = 0, off = 0, part = 0, coff = 0, doff = 0;
+  const size_t total = layout(*cfg, T_max, static_cast<int32_t>(bank->desc.size()), &attn, &off,
+                              &part, &coff, &doff);
   ENTMTP_CHECK_ARG(attn > 0 && part > 0, ENTMTP_EINVAL, "unsupported attention or LM-head sizes");
   ENTMTP_CHECK_ARG(cfg->workspace && (reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) == 0,
                    ENTMTP_EINVAL, "workspace must be non-NULL and 256-byte aligned");
@@ -146,6 +157,7 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   st->part_offset = off;
   st->part_bytes = part;
   st->counter_offset = coff;
+  st->dev_offset = doff;
   void* h = nullptr;
   int32_t rc = hip_status(hipHostMalloc(&h, sizeof(StepMirror), hipHostMallocMapped | hipHostMallocCoherent),
                           "hipHostMalloc (step result record)");
@@ -166,6 +178,28 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
     rc = hip_status(hipMemsetAsync(static_cast<uint8_t*>(cfg->workspace) + coff, 0, 256,
                                    static_cast<hipStream_t>(cfg->stream)),
                     "hipMemsetAsync (arrival counter)");
+  if (rc == ENTMTP_OK) {  // the bank's descriptors for device-scheduled steps
+    std::vector<DevTopo> topos(bank->desc.size());
+    for (size_t k = 0; k < topos.size(); ++k) {
+      const TopoDesc& d = bank->desc[k];
+      topos[k] = DevTopo{};
+      topos[k].T = d.T;
+      topos[k].D = d.D;
+      topos[k].off_parent = static_cast<int>(d.off_parent);
+      topos[k].off_depth = static_cast<int>(d.off_depth);
+      topos[k].off_mask = static_cast<int>(d.off_mask);
+      topos[k].off_path = static_cast<int>(d.off_path);
+    }
+    attn_device_splits(bank, cfg->Hq, cfg->Hkv, topos.data());
+    auto* dst = static_cast<uint8_t*>(cfg->workspace) + doff + 2 * sizeof(DevStep);
+    rc = hip_status(hipMemcpyAsync(dst, topos.data(), topos.size() * sizeof(DevTopo),
+                                   hipMemcpyHostToDevice, static_cast<hipStream_t>(cfg->stream)),
+                    "hipMemcpyAsync (bank descriptors)");
+    if (rc == ENTMTP_OK)
+      rc = hip_status(hipStreamSynchronize(static_cast<hipStream_t>(cfg->stream)),
+                      "hipStreamSynchronize");
+  }
+  if (rc == ENTMTP_OK) rc = attn_device_shape(bank, cfg->Hq, cfg->Hkv, cfg->cap, &st->dshape);
   if (rc != ENTMTP_OK) {
     entmtp_step_destroy(st);
     return rc;
@@ -213,8 +247,7 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
     if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_begin), s),
                                 "hipEventRecord"))
       return rc;
-  if (int32_t rc = entmtp_verify_logits_partials(hidden, c.w_lm, T, c.hid, c.V, c.inv_temp,
-                                                 c.logits, part, st->part_bytes, c.stream))
+  if (int32_t rc = launch_step_partials(hidden, c.w_lm, T, c.hid, c.V, c.inv_temp, c.logits, part, s))
     return rc;
   if (ev_lm_end)
     if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_end), s),
@@ -286,5 +319,103 @@ extern "C" int32_t entmtp_step_wait(entmtp_step* st, int32_t* accept_len, int32_
   if (bonus) *bonus = st->host->bonus;
   if (best_top1p) *best_top1p = st->host->best_top1p;
   st->pending = false;
+  return ENTMTP_OK;
+}
+
+namespace {
+
+__global__ void device_start_kernel(DevStep* state, const DevTopo* topos, int rung, int L) {
+  if (threadIdx.x == 0) state[0] = DevStep{rung, topos[rung].T, L, 0};
+}
+
+}  // namespace
+
+extern "C" int32_t entmtp_step_device_start(entmtp_step* st, int32_t topo, int32_t prefix_len) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
+  if (int32_t rc = check_device_bank(st->bank, topo)) return rc;
+  const entmtp_step_config& c = st->cfg;
+  ENTMTP_CHECK_ARG(prefix_len >= 0 && static_cast<int64_t>(prefix_len) + st->bank->desc[topo].T <= c.cap,
+                   ENTMTP_ERANGE, "prefix_len %d + T %d outside the cache capacity %d", prefix_len,
+                   st->bank->desc[topo].T, c.cap);
+  ENTMTP_CHECK_ARG(st->T_max <= 128, ENTMTP_ERANGE,
+                   "device-scheduled steps support trees of up to 128 nodes (bank has %d)", st->T_max);
+  auto* state = reinterpret_cast<DevStep*>(static_cast<uint8_t*>(c.workspace) + st->dev_offset);
+  hipLaunchKernelGGL(device_start_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(c.stream),
+                     state, reinterpret_cast<const DevTopo*>(state + 2), topo, prefix_len);
+  if (int32_t rc = launch_status("device_start launch")) return rc;
+  st->parity = 0;
+  st->dev_started = true;
+  return ENTMTP_OK;
+}
+
+extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16* q,
+                                             const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                                             entmtp_bf16* out, const entmtp_bf16* hidden,
+                                             const entmtp_bf16* w_lm, const int32_t* drafts,
+                                             int32_t* log, void* ev_lm_begin, void* ev_lm_end) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
+  ENTMTP_CHECK_ARG(st->dev_started, ENTMTP_EINVAL, "entmtp_step_device_start was not called");
+  ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && drafts, ENTMTP_EINVAL,
+                   "per-step inputs and outputs must be non-NULL");
+  const entmtp_step_config& c = st->cfg;
+  auto s = static_cast<hipStream_t>(c.stream);
+  uint8_t* ws = static_cast<uint8_t*>(c.workspace);
+  void* part = ws + st->part_offset;
+  auto* state = reinterpret_cast<DevStep*>(ws + st->dev_offset);
+  const auto* topos = reinterpret_cast<const DevTopo*>(state + 2);
+  DevStep* cur = state + st->parity;
+  DevStep* next = state + (st->parity ^ 1);
+
+  if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
+  if (ev_lm_begin)
+    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_begin), s),
+                                "hipEventRecord"))
+      return rc;
+  ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
+  if (int32_t rc = launch_partials_device_T(hidden, w_lm ? w_lm : c.w_lm, &cur->T, st->T_max, c.hid,
+                                            c.V, c.inv_temp, part, s))
+    return rc;
+  if (ev_lm_end)
+    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_end), s),
+                                "hipEventRecord"))
+      return rc;
+  FinAccDevice dv;
+  dv.cur = cur;
+  dv.next = next;
+  dv.topos = topos;
+  dv.drafts = drafts;
+  dv.tree_rows = c.tree_rows;
+  dv.n_topo = static_cast<int32_t>(st->bank->desc.size());
+  dv.t_max = st->T_max;
+  dv.tau_on = c.tau_on;
+  dv.tau_off = c.tau_off;
+  dv.log = log;
+  if (int32_t rc = launch_finalize_accept_device(
+          st->bank, dv, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax,
+          reinterpret_cast<unsigned*>(ws + st->counter_offset), c.accept_len, c.path,
+          c.path_capacity, c.bonus, c.best_top1p, nullptr, 0u, s))
+    return rc;
+
+  if (int32_t rc = hip_status(hipStreamWaitEvent(st->side, st->fork, 0), "hipStreamWaitEvent"))
+    return rc;
+  const size_t q_layer = static_cast<size_t>(c.tree_rows) * c.Hq * c.d;
+  const size_t kv_layer = static_cast<size_t>(c.tree_rows) * c.Hkv * c.d;
+  for (int32_t l = 0; l < c.n_layers; ++l) {
+    const size_t cl = static_cast<size_t>(l) * static_cast<size_t>(c.cache_layer_stride);
+    if (int32_t rc = launch_attn_device(st->bank, cur, topos, st->dshape, q + l * q_layer,
+                                        k_tree + l * kv_layer, v_tree + l * kv_layer,
+                                        c.k_cache + cl, c.v_cache + cl, c.cap, c.Hq, c.Hkv,
+                                        c.scale, c.rope_theta, out + l * q_layer, ws, st->side))
+      return rc;
+  }
+  if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
+  if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->join, 0), "hipStreamWaitEvent")) return rc;
+  if (int32_t rc = launch_compact_device(cur, c.path, c.path_capacity, c.accept_len, c.k_cache,
+                                         c.v_cache, c.n_layers, c.cache_layer_stride, c.Hkv, c.cap,
+                                         c.d, s))
+    return rc;
+  st->parity ^= 1;
   return ENTMTP_OK;
 }

@@ -44,6 +44,36 @@ __host__ __device__ inline int rows_padded(int G, int T) {
   return (G * T + kQTile - 1) / kQTile * kQTile;
 }
 
+__host__ __device__ inline int split_bound(int nblocks) {
+  int b = nblocks / kMinBlocksPerSplit;
+  b = b < 1 ? 1 : b;
+  return b > kMaxSplits ? kMaxSplits : b;
+}
+
+// Split count of a lone sequence: one workgroup fits per CU, so pick the
+// count that fills the CUs in whole rounds -- the first (1..bound) whose last
+// round is at least 90% full, else the fullest one seen (integer arithmetic,
+// so that the host and the device choose alike).
+__host__ __device__ inline int split_for_bound(int bound, int base_wg, int cus) {
+  int best = 1;
+  long long best_wg = 0, best_rounds = 1;
+  for (int ns = 1; ns <= bound; ++ns) {
+    const long long wg = static_cast<long long>(base_wg) * ns;
+    const long long rounds = (wg + cus - 1) / cus;
+    if (wg * best_rounds > best_wg * rounds) {   // fill wg / (rounds * cus) improves
+      best_wg = wg;
+      best_rounds = rounds;
+      best = ns;
+    }
+    if (10 * wg >= 9 * rounds * cus) break;
+  }
+  return best;
+}
+
+__host__ __device__ inline int split_single(int nblocks, int base_wg, int cus) {
+  return split_for_bound(split_bound(nblocks), base_wg, cus);
+}
+
 // ----------------------------------------------------------- descriptors --
 
 // One sequence of a (possibly batched) call, planned on the host.
@@ -62,6 +92,14 @@ struct SeqPlan {
 
 struct BatchArgs {
   SeqPlan s[kMaxSeqs];
+  // device-planned single sequence (a tree chosen on the GPU): when dev is
+  // set, sequence 0's tree, prefix length and split plan come from *dev, the
+  // bank descriptors and the CU count, and the grids are sized for the
+  // largest plan
+  const DevStep* dev;
+  const DevTopo* topos;
+  const uint8_t* arena;
+  int cus;
   int B, G, Hq, Hkv, cap;
   float scale_log2;
   double theta;
@@ -83,6 +121,39 @@ __device__ __forceinline__ int seq_of(const BatchArgs& p, int x, F first) {
   return b;
 }
 
+// Plan of sequence b: the host's, or -- for a device-planned call -- the
+// plan the host would make for the tree and prefix length the device holds
+// (same arithmetic), with the caches the host passed.
+__device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
+  if (!p.dev) return p.s[b];
+  SeqPlan q = p.s[0];
+  const DevStep st = *p.dev;
+  const DevTopo* t = p.topos + st.rung;   // read in place (no local copy to index)
+  q.T = st.T;
+  q.L = st.L;
+  if (q.L < 0 || q.T < 1 || q.L + q.T > p.cap) {   // outside the cache: no attention at all
+    q.T = 0;
+    q.L = 0;
+    q.nsplit = 1;
+    q.nqt = 0;
+    return q;
+  }
+  q.mask = reinterpret_cast<const uint32_t*>(p.arena + t->off_mask);
+  q.depth = reinterpret_cast<const int*>(p.arena + t->off_depth);
+  q.row0 = 0;
+  q.rows_pad = rows_padded(p.G, q.T);
+  q.nqt = q.rows_pad / kQTile;
+  const int nblocks = (q.L + q.T + KB - 1) / KB;
+  const int ns = t->splits[split_bound(nblocks)];   // = split_single(nblocks, Hkv * nqt, cus)
+  q.bps = (nblocks + ns - 1) / ns;
+  q.nsplit = (nblocks + q.bps - 1) / q.bps;
+  q.item0 = 0;
+  q.merge0 = 0;
+  q.qrot_off = 0;
+  q.part_off = 0;
+  return q;
+}
+
 // ------------------------------------------------------------------ prep --
 
 __global__ __launch_bounds__(256) void attn_prep_kernel(BatchArgs p) {
@@ -91,9 +162,10 @@ __global__ __launch_bounds__(256) void attn_prep_kernel(BatchArgs p) {
   // Hkv*16 16-byte value chunks
   constexpr int HALF = HD / 2;
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.row0; });
-  const SeqPlan& sq = p.s[b];
+  const SeqPlan sq = resolve(p, b);
   const int row = blockIdx.x;
   const int i = row - sq.row0;
+  if (i >= sq.T) return;   // device-planned grids cover the largest tree
   const int u = blockIdx.y * blockDim.x + threadIdx.x;
   const int Hq = p.Hq, Hkv = p.Hkv, G = p.G, T = sq.T, L = sq.L, cap = p.cap;
   const int nq = Hq * HALF, nk = Hkv * HALF, nv = Hkv * (HD / 8);
@@ -151,7 +223,8 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   // over 8 XCDs and every sequence's range starts at a multiple of 8), so
   // their K/V reads share that XCD's L2.
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
-  const SeqPlan& sq = p.s[b];
+  const SeqPlan sq = resolve(p, b);
+  if (sq.T == 0) return;
   const int bid = blockIdx.x - sq.item0;
   const int qt = (bid >> 3) % sq.nqt;
   const int gc = ((bid >> 3) / sq.nqt) * 8 + (bid & 7);
@@ -167,7 +240,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   // LDS: per-wave V^T tiles during the loop, reused for the wave merge after it
   constexpr int kVtBytes = HD * VT_LD * 2;                           // 9216
   constexpr int OLD = HD + 1;                                         // merge row stride (bank spread)
-  constexpr int kMergeBytes = kAttnWaves * kQTile * OLD * 4;         // 66048
+  constexpr int kMergeBytes = 2 * kQTile * OLD * 4;                  // 33024: two wave slots
   constexpr int kLdsBytes = kMergeBytes > kAttnWaves * kVtBytes ? kMergeBytes : kAttnWaves * kVtBytes;
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
   __shared__ uint32_t s_mask[kQTile][ENTMTP_MASK_WORDS + 1];
@@ -338,7 +411,9 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
   }
 
-  // ---- merge the four waves (fixed order)
+  // ---- merge the four waves: waves 2 and 3 into 0 and 1, then 1 into 0,
+  // through two wave-sized LDS slots (so the merge needs no more LDS than the
+  // V^T tiles, and the kernel leaves room on a CU for other work)
   __syncthreads();  // every wave is done with its V^T tile
   if (lh == 0) {
     s_m[wave][li] = m_run;
@@ -349,14 +424,39 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
 #pragma unroll
   for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][li]);
   const float myscale = (m_run == -INFINITY) ? 0.f : exp2f(m_run - M);
-  float* ored = reinterpret_cast<float*>(lds);  // [wave][query][HD]
 #pragma unroll
   for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int dim = 32 * ct + 8 * (r >> 2) + 4 * lh + (r & 3);
-      ored[(wave * kQTile + li) * OLD + dim] = o[ct][r] * myscale;
-    }
+    for (int r = 0; r < 16; ++r) o[ct][r] *= myscale;
+  float* ored = reinterpret_cast<float*>(lds);  // [slot][query][HD]
+  auto put = [&](int slot) {
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int dim = 32 * ct + 8 * (r >> 2) + 4 * lh + (r & 3);
+        ored[(slot * kQTile + li) * OLD + dim] = o[ct][r];
+      }
+  };
+  auto add = [&](int slot) {
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int dim = 32 * ct + 8 * (r >> 2) + 4 * lh + (r & 3);
+        o[ct][r] += ored[(slot * kQTile + li) * OLD + dim];
+      }
+  };
+  if (wave >= 2) put(wave - 2);
+  __syncthreads();
+  if (wave < 2) add(wave);
+  __syncthreads();
+  if (wave == 1) put(0);
+  __syncthreads();
+  if (wave == 0) {
+    add(0);
+    put(0);
+  }
   __syncthreads();
   for (int u = tid; u < kQTile * HD; u += kAttnThreads) {
     const int q = u / HD, dim = u % HD;
@@ -365,13 +465,13 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     float Mq = -INFINITY;
 #pragma unroll
     for (int w = 0; w < kAttnWaves; ++w) Mq = fmaxf(Mq, s_m[w][q]);
-    float lsum = 0.f, osum = 0.f;
+    float lsum = 0.f;
 #pragma unroll
     for (int w = 0; w < kAttnWaves; ++w) {
       const float sc = (s_m[w][q] == -INFINITY) ? 0.f : exp2f(s_m[w][q] - Mq);
       lsum += s_l[w][q] * sc;
-      osum += ored[(w * kQTile + q) * OLD + dim];
     }
+    const float osum = ored[q * OLD + dim];
     if (nsplit == 1) {
       const int gh = row / T, node = row % T;
       const int h = g * p.G + gh;
@@ -392,10 +492,11 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
 
 __global__ __launch_bounds__(HD) void attn_merge_kernel(BatchArgs p) {
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.merge0; });
-  const SeqPlan& sq = p.s[b];
-  if (sq.nsplit == 1) return;   // written by the attend kernel
+  const SeqPlan sq = resolve(p, b);
+  if (sq.nsplit == 1 || sq.T == 0) return;   // written by the attend kernel, or nothing to do
   const int GT = p.G * sq.T;
   const int local = blockIdx.x - sq.merge0;
+  if (local >= p.Hkv * GT) return;   // device-planned grids cover the largest tree
   const int g = local / GT, row = local % GT;
   const int dim = threadIdx.x;
   float M = -INFINITY;
@@ -419,12 +520,6 @@ __global__ __launch_bounds__(HD) void attn_merge_kernel(BatchArgs p) {
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
-int split_bound(int nblocks) {
-  int b = nblocks / kMinBlocksPerSplit;
-  b = b < 1 ? 1 : b;
-  return b > kMaxSplits ? kMaxSplits : b;
-}
-
 int device_cus() {
   static int cus[64] = {0};
   int dev = 0;
@@ -435,26 +530,6 @@ int device_cus() {
     cus[dev] = n;
   }
   return cus[dev];
-}
-
-// Split count of a lone sequence: one workgroup fits per CU, so pick the
-// count that fills the CUs in whole rounds -- the first (1..bound) whose last
-// round is at least 90% full, else the best one seen.
-int split_single(int nblocks, int base_wg, int cus) {
-  const int bound = split_bound(nblocks);
-  int best = 1;
-  double best_eff = 0.0;
-  for (int ns = 1; ns <= bound; ++ns) {
-    const int wg = base_wg * ns;
-    const int rounds = (wg + cus - 1) / cus;
-    const double eff = static_cast<double>(wg) / (static_cast<double>(rounds) * cus);
-    if (eff > best_eff + 1e-9) {
-      best_eff = eff;
-      best = ns;
-    }
-    if (eff >= 0.9) break;
-  }
-  return best;
 }
 
 // Grid sizes of one call.
@@ -472,12 +547,16 @@ struct CallShape {
 CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const int32_t* L,
                     entmtp_bf16* const* kc, entmtp_bf16* const* vc, int cap, int Hq, int Hkv,
                     BatchArgs& a) {
+  a.dev = nullptr;
+  a.topos = nullptr;
+  a.arena = nullptr;
   a.B = B;
   a.G = Hq / Hkv;
   a.Hq = Hq;
   a.Hkv = Hkv;
   a.cap = cap;
   const int cus = device_cus();
+  a.cus = cus;
   long long work = 0;
   for (int b = 0; b < B; ++b) {
     const int T = bank->desc[topo[b]].T;
@@ -601,6 +680,82 @@ int32_t check_sequence(const entmtp_bank* bank, int32_t topo, int32_t prefix_len
 }
 
 }  // namespace
+
+int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, DevAttnShape* out) {
+  const int cus = device_cus();
+  const int G = Hq / Hkv;
+  DevAttnShape sh;
+  for (const TopoDesc& td : bank->desc) {
+    sh.T_max = td.T > sh.T_max ? td.T : sh.T_max;
+    const int nqt = rows_padded(G, td.T) / kQTile;
+    const int max_blocks = (cap + KB - 1) / KB;
+    for (int nblocks = 1; nblocks <= max_blocks; ++nblocks) {
+      const int ns0 = split_single(nblocks, Hkv * nqt, cus);
+      const int bps = (nblocks + ns0 - 1) / ns0;
+      const int ns = (nblocks + bps - 1) / bps;
+      const int items = (Hkv * ns + 7) / 8 * 8 * nqt;
+      sh.items = items > sh.items ? items : sh.items;
+    }
+  }
+  sh.rows = sh.T_max;
+  sh.merge_blocks = Hkv * G * sh.T_max;
+  sh.need = workspace_bytes(sh.T_max, Hq, Hkv, cap);
+  *out = sh;
+  return ENTMTP_OK;
+}
+
+void attn_device_splits(const entmtp_bank* bank, int Hq, int Hkv, DevTopo* topos) {
+  const int cus = device_cus();
+  const int G = Hq / Hkv;
+  for (size_t k = 0; k < bank->desc.size(); ++k) {
+    const int nqt = rows_padded(G, bank->desc[k].T) / kQTile;
+    topos[k].splits[0] = 1;
+    for (int b = 1; b <= kMaxSplits; ++b)
+      topos[k].splits[b] = static_cast<unsigned char>(split_for_bound(b, Hkv * nqt, cus));
+  }
+}
+
+int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const DevTopo* topos,
+                           const DevAttnShape& sh, const entmtp_bf16* q, const entmtp_bf16* k_tree,
+                           const entmtp_bf16* v_tree, entmtp_bf16* k_cache, entmtp_bf16* v_cache,
+                           int cap, int Hq, int Hkv, float scale, float rope_theta,
+                           entmtp_bf16* out, void* workspace, hipStream_t s) {
+  BatchArgs a{};
+  a.dev = dev;
+  a.topos = topos;
+  a.arena = bank->arena;
+  a.cus = device_cus();
+  a.B = 1;
+  a.G = Hq / Hkv;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  a.s[0].kc = k_cache;
+  a.s[0].vc = v_cache;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.theta = static_cast<double>(rope_theta);
+  a.q = q;
+  a.kt = k_tree;
+  a.vt = v_tree;
+  a.out = out;
+  // the workspace regions at the bounds workspace_bytes() sizes them with
+  const int rows_pad = rows_padded(a.G, sh.T_max);
+  const size_t bound = split_bound((cap + sh.T_max + KB - 1) / KB);
+  const size_t qb = static_cast<size_t>(Hkv) * rows_pad * HD * 2;
+  const size_t po = bound * Hkv * rows_pad * HD * 4;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  a.qrot = reinterpret_cast<uint16_t*>(ws);
+  a.part_o = reinterpret_cast<float*>(ws + al256(qb));
+  a.part_ml = reinterpret_cast<float*>(ws + al256(qb) + al256(po));
+  const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
+  hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
+  if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
+  hipLaunchKernelGGL(tree_attn_kernel, dim3(sh.items), dim3(kAttnThreads), 0, s, a);
+  if (int32_t rc = launch_status("tree_attn launch")) return rc;
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(HD), 0, s, a);
+  return launch_status("tree_attn merge launch");
+}
+
 }  // namespace entmtp
 
 using namespace entmtp;

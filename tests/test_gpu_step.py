@@ -204,3 +204,76 @@ def test_step_errors(api):
     # all-zero logits: uniform distribution, argmax 0; zero drafts match it
     assert bonus == 0 and abs(s - 1.0 / V) <= 1e-6 and a == bank.D[3]
     st.close()
+
+
+@pytest.mark.parametrize("n_layers,with128", [(1, False), (2, True)])
+def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
+    """The same closed loop twice: the host reads each step's result and runs
+    the ladder (entmtp_step_launch / _wait / ladder_next), and the GPU does it
+    (entmtp_step_device_start / _launch_device, no host reads until the end).
+    Trees, prefix lengths, accept lengths, s, outputs and caches agree bit for
+    bit."""
+    Hq, Hkv, d, hid, V, L0, n_steps = 8, 2, 128, 512, 1000, 40, 14
+    theta, scale = 10000.0, 1 / math.sqrt(128)
+    trees = bank_trees() + ([synth.uniform_attach_tree(WL + 3, 128, 6)] if with128 else [])
+    bank = api.Bank(trees)
+    K, Tmax, Dmax = len(trees), max(bank.T), max(bank.D)
+    cap = L0 + n_steps * (Dmax + 1) + Tmax + 8
+    rung0 = K - 1 if with128 else 0   # start on the largest tree (two LM-head passes)
+    w_bits = synth.lm_head_weight(WL, V, hid, std=W_STD)
+    w64 = orc.bf16_to_f64(w_bits)
+    W = dev_bf16(w_bits)
+    base = [synth.attn_inputs(WL, 1, Hq, Hkv, d, L0, cap, layer=l) for l in range(n_layers)]
+    kc_h = dev_bf16(stack(base, "k_cache"))
+    vc_h = dev_bf16(stack(base, "v_cache"))
+    kc_d, vc_d = kc_h.clone(), vc_h.clone()
+    stride = Hkv * cap * d
+    kw = dict(n_layers=n_layers, Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax, scale=scale,
+              rope_theta=theta, cache_layer_stride=stride)
+    st_h = api.Step(bank, kc_h, vc_h, W, **kw)
+    st_d = api.Step(bank, kc_d, vc_d, W, keep_logits=False, tau_on=0.8, tau_off=0.6, **kw)
+    deltas, spikes = synth.regime_spikes(WL, n_steps, Tmax, V, hid)
+    steps = []
+    for t in range(n_steps):
+        layers, x, am, u, r = step_inputs(t, n_layers, Tmax, Hq, Hkv, d, w_bits, w64,
+                                          float(deltas[t]), spikes[t])
+        drafts = np.zeros((K, Tmax), np.int32)
+        for k in range(K):
+            drafts[k, : bank.T[k]] = synth.draft_tokens(trees[k], am, u, r, 0.7)
+        steps.append({"q": dev_bf16(stack(layers, "q")), "kt": dev_bf16(stack(layers, "k_tree")),
+                      "vt": dev_bf16(stack(layers, "v_tree")), "x": dev_bf16(x),
+                      "drafts": dev_i32(drafts)})
+    out_h = torch.zeros((n_steps, n_layers, Tmax, Hq, d), dtype=torch.bfloat16, device="cuda")
+    out_d = torch.zeros_like(out_h)
+
+    # host-scheduled
+    L, rung, trace = L0, rung0, []
+    for t, e in enumerate(steps):
+        st_h.launch(rung, L, e["q"], e["kt"], e["vt"], out_h[t], e["x"], e["drafts"][rung])
+        a, bonus, s = st_h.wait(timeout_s=60.0)
+        trace.append((rung, L, a, s))
+        L += a + 1
+        rung = api.ladder_next(rung, K, s, 0.8, 0.6)
+    torch.cuda.synchronize()
+
+    # device-scheduled: every step enqueued without reading anything back
+    log = torch.full((n_steps, 4), -1, dtype=torch.int32, device="cuda")
+    st_d.device_start(rung0, L0)
+    for t, e in enumerate(steps):
+        st_d.launch_device(e["q"], e["kt"], e["vt"], out_d[t], e["x"], e["drafts"], log[t])
+    torch.cuda.synchronize()
+    say("host trace", [(r_, a_) for r_, _, a_, _ in trace])
+    log_h = log.cpu().numpy()
+    for t, (r_, L_, a_, s_) in enumerate(trace):
+        assert tuple(log_h[t, :3]) == (r_, L_, a_), (t, log_h[t], (r_, L_, a_))
+        assert log_h[t, 3:4].view(np.float32)[0] == np.float32(s_)
+    assert len({r_ for r_, *_ in trace}) >= 3
+    if with128:
+        assert trace[0][0] == K - 1
+    for t, (r_, *_rest) in enumerate(trace):
+        T = bank.T[r_]
+        assert torch.equal(out_h[t, :, :T].view(torch.int16), out_d[t, :, :T].view(torch.int16)), t
+    assert torch.equal(kc_h.view(torch.int16), kc_d.view(torch.int16))
+    assert torch.equal(vc_h.view(torch.int16), vc_d.view(torch.int16))
+    st_h.close()
+    st_d.close()
