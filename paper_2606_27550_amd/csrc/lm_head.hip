@@ -1,4 +1,5 @@
-// LM-head verification logits: logits[i][v] = sum_k X[i][k] * W[v][k].
+// LM-head verification logits: logits[i][v] = sum_k X[i][k] * W[v][k], and
+// the per-node softmax statistics taken from the same accumulators.
 //
 // The verification pass of §2.3 scores every draft-tree node with the
 // target's LM head (the next-token distribution softmax(W h) of §2.2).  At
@@ -6,22 +7,31 @@
 // cost is streaming W (V x hid bf16, 262 MB for a 7B vocabulary) once from
 // HBM; the arithmetic intensity is about T flop per byte.
 //
-// Design (gfx950):
-//  * W rows are the MFMA M dimension and tree nodes the N dimension of
-//    v_mfma_f32_16x16x32_bf16.  Each lane loads its A operand straight from
-//    HBM into registers: lane (row r = lane%16, group g = lane/16) reads 16
-//    bytes of row r at k = 32s + 8g for step s, so a wave instruction covers
-//    16 rows x 64 contiguous bytes.  W is never staged in LDS.
-//  * X (the tree's hidden states) is shared by every W row: each workgroup
-//    stages a K-chunk of X in LDS (double buffered, row padding against bank
-//    conflicts) and every wave reads its B operands from there.
-//  * The vocabulary is cut into one contiguous slice per workgroup, sized so
-//    every CU streams the same number of bytes; inside the slice the 16-row
-//    tiles are dealt round-robin to the four waves (at most two each).
-//  * The next K-chunk of W and X is loaded while the current one is
-//    multiplied, so each wave keeps two chunks of loads in flight.
-//  * Accumulation is fp32; logits are written as fp32 so that the argmax and
-//    the statistics never see a rounded logit.
+// The streaming kernel (hyb_body; hid a multiple of 512), on
+// v_mfma_f32_16x16x32_bf16 with W rows as M and tree nodes as N:
+//  * the vocabulary is cut into slices of at most 64 rows, one per workgroup
+//    of four waves, and the grid is a whole multiple of the CU count (a
+//    partial extra round of workgroups costs ~20%);
+//  * each wave streams its own 16-row W tile through VGPRs, 4 rows x 256
+//    contiguous bytes per load instruction, several K-stages deep, and turns
+//    each stage into MFMA operand layout through a private XOR-swizzled LDS
+//    tile;
+//  * X, shared by all waves, arrives by direct global->LDS copies into a ring
+//    of separate LDS objects (one per stage, so the compiler can tell the
+//    slot being read from the slots in flight), one barrier per stage;
+//  * loads are unconditional (clamped rows) and the K loop is unrolled
+//    completely for hid 4096 / 5120, so the explicit wait counts stay exact;
+//  * workgroups walk K in rotated order;
+//  * with statistics, the epilogue reduces each node's accumulators over the
+//    slice to a partial (raw max and its index, sum e^(y-m), sum (y-m)e^(y-m))
+//    through wave shuffles and the wave's own transposition tile, and a small
+//    kernel merges a node's partials (stats.hpp), so logits never need to
+//    reach memory.
+// Node tiles of 16, 32, 64 or 128 nodes select the instantiation; variants
+// loop a workgroup over several slices (one workgroup per CU, leaving room for
+// concurrent attention) or read the node count from device memory (trees
+// chosen on the GPU).  Other hidden sizes use a direct-to-LDS kernel
+// (hid % 128 == 0) or a register-prefetch kernel.
 #include <algorithm>
 #include <type_traits>
 

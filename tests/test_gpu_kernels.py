@@ -211,6 +211,26 @@ def test_verify_logits_stats_fused_margin_7b(api, w7b):
     assert np.all(np.abs(p1 - rp1) <= RTOL_STATS * np.abs(rp1) + 1e-6)
 
 
+def test_verify_logits_13b_hidden_5120(api):
+    """The 13B shape (hidden 5120, fully unrolled 40-stage K loop): logits and
+    fused statistics of a 128-node tree against the oracle."""
+    say("verify_logits 13b shapes")
+    V, hid, T = 32000, 5120, 128
+    w = synth.lm_head_weight(4, V, hid)
+    X = margin_hidden(4, T, w)
+    ref = orc.verify_logits(X, w)
+    z, (H, p1, am) = run_fused(api, X, w)
+    assert np.abs(z - ref).max() <= 1e-4 * max(1.0, np.abs(ref).max())
+    rH, rp1, ram = orc.logit_stats(ref.astype(np.float32))
+    np.testing.assert_array_equal(am, ram)
+    assert np.all(np.abs(H - rH) <= RTOL_STATS * np.abs(rH) + 1e-6)
+    assert np.all(np.abs(p1 - rp1) <= RTOL_STATS * np.abs(rp1) + 1e-6)
+    for T2 in (1, 16, 27, 64):   # the other node tiles at this hidden size
+        z2, st2 = run_fused(api, X[:T2], w)
+        np.testing.assert_array_equal(st2[2], ram[:T2])
+        assert np.abs(z2 - ref[:T2]).max() <= 1e-4 * max(1.0, np.abs(ref).max())
+
+
 # ------------------------------------------------------------------ accept --
 
 def run_accept(api, bank, topo, tok, am, p1=None):

@@ -277,3 +277,62 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
     assert torch.equal(vc_h.view(torch.int16), vc_d.view(torch.int16))
     st_h.close()
     st_d.close()
+
+
+def test_step_32_layer_workload_sampled(api):
+    """The 32-layer workload at its shapes (prefix 4096, 64-node tree of depth
+    5, 32 x 128 heads, hidden 4096, vocab 32000): one step through the step
+    driver; attention checked on the oracle for sampled (layer, KV head)
+    pairs, the LM-head statistics and acceptance exactly, and the compaction
+    of every layer bit for bit against the appended tree rows."""
+    wl = synth.WORKLOADS["tree64_L4096_7b_32layer"]
+    n_layers, H, d, hid, V, L = wl.n_layers, wl.n_heads, wl.head_dim, wl.hidden, wl.vocab, wl.prefix_len
+    trees = synth.workload_trees(wl)
+    bank = api.Bank(trees)
+    T, D = bank.T[0], bank.D[0]
+    cap = L + T + 8
+    scale, theta = 1 / math.sqrt(d), wl.rope_theta
+    say("32-layer step: generating inputs")
+    layers = [synth.attn_inputs(wl.ident, T, H, H, d, L, cap, layer=l) for l in range(n_layers)]
+    kc = dev_bf16(stack(layers, "k_cache"))
+    vc = dev_bf16(stack(layers, "v_cache"))
+    w = synth.lm_head_weight(wl.ident, V, hid)
+    w64 = orc.bf16_to_f64(w)
+    x = margin_hidden(wl.ident, T, w, w64=w64)
+    am = (orc.bf16_to_f64(x) @ w64.T).argmax(axis=1)
+    u, r = synth.draft_randoms(wl.ident, T, V)
+    tok = synth.draft_tokens(trees[0], am, u, r, wl.p_acc)
+    st = api.Step(bank, kc, vc, dev_bf16(w), n_layers=n_layers, Hq=H, Hkv=H, d=d, cap=cap,
+                  tree_rows=T, scale=scale, rope_theta=theta, cache_layer_stride=H * cap * d)
+    out = torch.empty((n_layers, T, H, d), dtype=torch.bfloat16, device="cuda")
+    say("32-layer step: launch")
+    st.launch(0, L, dev_bf16(stack(layers, "q")), dev_bf16(stack(layers, "k_tree")),
+              dev_bf16(stack(layers, "v_tree")), out, dev_bf16(x), dev_i32(tok))
+    a, bonus, s = st.wait(timeout_s=120.0)
+    torch.cuda.synchronize()
+    ra, rpath, rbonus, rbest = orc.accept(trees[0], tok, am)
+    assert (a, bonus) == (ra, rbonus)
+    assert st.path.cpu().numpy()[: a + 1].tolist() == list(rpath)
+    z = orc.verify_logits(x, w).astype(np.float32)
+    rH, rp1, ram = orc.logit_stats(z)
+    np.testing.assert_array_equal(st.argmax.cpu().numpy(), ram)
+    np.testing.assert_allclose(st.top1p.cpu().numpy(), rp1, rtol=RTOL_STATS, atol=1e-6)
+    kc_h, vc_h = host_bits(kc), host_bits(vc)
+    out_h = out.float().cpu().numpy()
+    for l, g in ((0, 0), (13, 7), (31, 31)):
+        x_l = layers[l]
+        ref, rk, rv = orc.tree_attention(x_l.q[:, g:g + 1], x_l.k_tree[:, g:g + 1],
+                                         x_l.v_tree[:, g:g + 1], x_l.k_cache[g:g + 1],
+                                         x_l.v_cache[g:g + 1], L, trees[0], scale, theta)
+        err = np.abs(out_h[l, :, g:g + 1] - ref).max()
+        say(f"  layer {l} head {g}: max abs err {err:.2e}")
+        assert err <= ATOL_BF16
+        rk2, rv2 = orc.kv_compact(rk, rv, L, rpath)
+        np.testing.assert_array_equal(kc_h[l, g:g + 1, : L + a + 1], rk2[:, : L + a + 1])
+        np.testing.assert_array_equal(vc_h[l, g:g + 1, : L + a + 1], rv2[:, : L + a + 1])
+    # every layer: the prefix is untouched and row L + j holds the old tree row path[j]
+    for l in range(n_layers):
+        np.testing.assert_array_equal(vc_h[l, :, :L], layers[l].v_cache[:, :L])
+        for j, node in enumerate(rpath):
+            np.testing.assert_array_equal(vc_h[l, :, L + j], layers[l].v_tree[node])
+    st.close()
