@@ -23,6 +23,8 @@ What the step computes, in the paper's terms:
 * ``accept``: greedy verification -- the longest root-to-node path whose every
   draft token equals the target's argmax at the parent (§2.1, left-to-right
   acceptance, specialised to greedy decoding), and the accept length (§5.1).
+* ``accept_typical``: the same walk under Hydra's typical acceptance
+  condition (posterior threshold and entropy-scaled threshold, §5.1-§5.2).
 * ``kv_compact``: the KV-cache update that keeps the accepted path (§3.2,
   the proposal -> tree decoding -> verification -> KV-cache update loop).
 * ``ladder_next``: the hysteretic threshold policy over a size-sorted bank
@@ -290,6 +292,58 @@ def accept(parent: Sequence[int], draft_tokens: Sequence[int], target_argmax: Se
             best = i
     path = ancestors_or_self(parent, best)
     return depth[best], path, int(target_argmax[best]), best
+
+
+def typical_probs(z_row, inv_temp: float):
+    """Temperature-scaled next-token distribution of one node and its entropy
+    in nats (the quantities the typical acceptance condition compares)."""
+    y = np.asarray(z_row, dtype=np.float64) * float(inv_temp)
+    y = y - y.max()
+    e = np.exp(y)
+    p = e / e.sum()
+    nz = p > 0
+    H = float(-(p[nz] * np.log(p[nz])).sum())
+    return p, H
+
+
+def accept_typical(parent: Sequence[int], draft_tokens: Sequence[int], z, inv_temp: float,
+                   eps: float, alpha: float):
+    """Typical-acceptance tree verification (the verification condition the
+    paper keeps from Hydra, §5.1, with temperature T = 1 / inv_temp, posterior
+    threshold eps and mixing coefficient alpha of §5.2; the rule itself is the
+    published typical acceptance of Medusa/Hydra, not restated in the paper).
+
+    Node i >= 1 is locally acceptable when its draft token's probability under
+    its parent's distribution p = softmax(z[parent] * inv_temp) exceeds
+    min(eps, alpha * exp(-H(p))); it is accepted when its parent is accepted
+    too (the root always is).  The answer is the deepest accepted node (lowest
+    index among equals); the bonus token is the argmax at that node.
+
+    z: the tree's logits [T][V].  Returns (a, path, bonus, best, p_draft,
+    threshold) with p_draft[i] the draft token's probability under node i's
+    parent (0 for the root) and threshold[j] node j's acceptance threshold.
+    """
+    validate_parent(parent)
+    T = len(parent)
+    probs, thr = [], []
+    for j in range(T):
+        p, H = typical_probs(z[j], inv_temp)
+        probs.append(p)
+        thr.append(min(float(eps), float(alpha) * math.exp(-H)))
+    depth = [0] * T
+    ok = [True] + [False] * (T - 1)
+    p_draft = [0.0] * T
+    for i in range(1, T):
+        depth[i] = depth[parent[i]] + 1
+        p_draft[i] = float(probs[parent[i]][int(draft_tokens[i])])
+        ok[i] = ok[parent[i]] and p_draft[i] > thr[parent[i]]
+    best = 0
+    for i in range(T):
+        if ok[i] and depth[i] > depth[best]:
+            best = i
+    path = ancestors_or_self(parent, best)
+    bonus = int(np.argmax(np.asarray(z[best], dtype=np.float64)))
+    return depth[best], path, bonus, best, np.array(p_draft), np.array(thr)
 
 
 # --------------------------------------------------------------------------
