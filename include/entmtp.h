@@ -289,6 +289,37 @@ int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
                       int32_t* path, int32_t* bonus, float* best_top1p, void* stream);
 
 /*
+ * Typical acceptance (the verification condition the paper keeps from Hydra:
+ * temperature, posterior threshold eps, mixing coefficient alpha, §5.1-§5.2;
+ * the rule is the published typical acceptance of Medusa/Hydra).  Node i >= 1
+ * is locally acceptable when its draft token's probability under its parent's
+ * distribution p = softmax(z[parent] * inv_temp) exceeds
+ * min(eps, alpha * exp(-H(p))); the longest accepted path, bonus token and
+ * outputs are then as for entmtp_accept.
+ *
+ * entmtp_draft_logits computes what the test needs beyond the statistics:
+ * z_draft[i] = X[parent(i)] . W[draft_tokens[i]] and z_top[i] = X[parent(i)] .
+ * W[argmax[parent(i)]] (fp32, device [T]; 0 for the root; -inf for a draft
+ * token outside [0, V)).  hidden [T][hid] and w_lm [V][hid] bf16, 16-byte
+ * aligned, hid % 8 == 0.
+ *
+ * entmtp_accept_typical takes those and the statistics entmtp_logit_stats /
+ * entmtp_verify_logits_stats produced with the same inv_temp (entropy in
+ * nats, top1p, argmax): p(draft) = exp((z_draft - z_top) * inv_temp) *
+ * top1p[parent].  eps, alpha >= 0.
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_draft_logits(const entmtp_bank* bank, int32_t topo, const entmtp_bf16* hidden,
+                            const entmtp_bf16* w_lm, int32_t hid, int32_t V,
+                            const int32_t* draft_tokens, const int32_t* argmax, float* z_draft,
+                            float* z_top, void* stream);
+int32_t entmtp_accept_typical(const entmtp_bank* bank, int32_t topo, const int32_t* draft_tokens,
+                              const int32_t* argmax, const float* z_draft, const float* z_top,
+                              const float* entropy, const float* top1p, float inv_temp, float eps,
+                              float alpha, int32_t* accept_len, int32_t* path, int32_t* bonus,
+                              float* best_top1p, void* stream);
+
+/*
  * Batched form: workgroup b accepts tree topo[b] (HOST array of B entries,
  * 1 <= B <= ENTMTP_B_MAX) of sequence b.  draft_tokens, argmax and top1p hold
  * the sequences' rows back to back (rows of sequence b start at

@@ -65,6 +65,10 @@ _SIGNATURES = {
     "entmtp_verify_logits_stats": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p,
                                             _c_p, _c_p, _c_sz, _c_p]),
     "entmtp_accept": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_draft_logits": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p,
+                                     _c_p]),
+    "entmtp_accept_typical": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_f32,
+                                       _c_f32, _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "entmtp_kv_compact": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64, _c_i32,
                                    _c_i32, _c_i32, _c_p]),
     "entmtp_ladder_next": (_c_i32, [_c_i32, _c_i32, _c_f32, _c_f32, _c_f32]),
@@ -455,6 +459,40 @@ def accept(bank: Bank, topo: int, draft_tokens, argmax, top1p, accept_len, path,
     _check(lib.entmtp_accept(bank.handle, topo, _p(draft_tokens), _p(argmax), _p(top1p),
                              _p(accept_len), _p(path), _p(bonus), _p(best_top1p),
                              _stream(stream)))
+
+
+def draft_logits(bank: Bank, topo: int, hidden, w_lm, draft_tokens, argmax, z_draft, z_top,
+                 stream=None) -> None:
+    import torch
+    T = bank.T[topo]
+    V, hid = w_lm.shape
+    _dev(hidden, "hidden", torch.bfloat16, min_numel=T * hid)
+    _need(hidden.shape[-1] == hid, "hidden rows have the LM head's width")
+    _dev(w_lm, "w_lm", torch.bfloat16, (V, hid))
+    _dev(draft_tokens, "draft_tokens", torch.int32, min_numel=T)
+    _dev(argmax, "argmax", torch.int32, min_numel=T)
+    _dev(z_draft, "z_draft", torch.float32, min_numel=T)
+    _dev(z_top, "z_top", torch.float32, min_numel=T)
+    _check(lib.entmtp_draft_logits(bank.handle, topo, _p(hidden), _p(w_lm), hid, V, _p(draft_tokens),
+                                   _p(argmax), _p(z_draft), _p(z_top), _stream(stream)))
+
+
+def accept_typical(bank: Bank, topo: int, draft_tokens, argmax, z_draft, z_top, entropy, top1p,
+                   inv_temp: float, eps: float, alpha: float, accept_len, path, bonus,
+                   best_top1p=None, stream=None) -> None:
+    import torch
+    T, D = bank.T[topo], bank.D[topo]
+    for name, t, dt in (("draft_tokens", draft_tokens, torch.int32), ("argmax", argmax, torch.int32),
+                        ("z_draft", z_draft, torch.float32), ("z_top", z_top, torch.float32),
+                        ("entropy", entropy, torch.float32), ("top1p", top1p, torch.float32)):
+        _dev(t, name, dt, min_numel=T)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=1)
+    _dev(path, "path", torch.int32, min_numel=D + 1)
+    _dev(bonus, "bonus", torch.int32, min_numel=1)
+    _check(lib.entmtp_accept_typical(bank.handle, topo, _p(draft_tokens), _p(argmax), _p(z_draft),
+                                     _p(z_top), _p(entropy), _p(top1p), inv_temp, eps, alpha,
+                                     _p(accept_len), _p(path), _p(bonus), _p(best_top1p),
+                                     _stream(stream)))
 
 
 def kv_compact(path, accept_len, prefix_len: int, k_cache, v_cache, stream=None) -> None:

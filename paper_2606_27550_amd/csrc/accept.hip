@@ -45,8 +45,15 @@ __device__ __forceinline__ NodeIn accept_load(const int* __restrict__ parent,
 
 // The acceptance of one tree by one workgroup of kAcceptThreads threads;
 // returns (in every thread) depth(best) * 1024 + (1023 - best).
+// Greedy local test: node i's draft token is the target's argmax at its parent.
+__device__ __forceinline__ bool greedy_ok(const NodeIn& n, const int* __restrict__ amax, int T) {
+  const int i = threadIdx.x;
+  return i < T && (i == 0 || n.tok == amax[n.parent]);
+}
+
+// `ok`: this thread's node is locally acceptable (the root always is).
 __device__ __forceinline__ int accept_finish(
-    const NodeIn& n, const int* __restrict__ path_tab, int T, int D,
+    const NodeIn& n, bool ok, const int* __restrict__ path_tab, int T, int D,
     const int* __restrict__ amax, const float* __restrict__ top1p,
     int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
     int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
@@ -56,10 +63,7 @@ __device__ __forceinline__ int accept_finish(
   const int i = threadIdx.x;
   if (i < ENTMTP_MASK_WORDS) matched[i] = 0u;
   __syncthreads();
-  if (i < T) {
-    const bool ok = (i == 0) || (n.tok == amax[n.parent]);
-    if (ok) atomicOr(&matched[i >> 5], 1u << (i & 31));
-  }
+  if (i < T && ok) atomicOr(&matched[i >> 5], 1u << (i & 31));
   __syncthreads();
   // key orders accepted nodes by depth, then by lower index
   int key = -1;
@@ -104,8 +108,8 @@ __device__ __forceinline__ void accept_core(
     int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
     uint32_t seq) {
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
-  (void)accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, path_cap, bonus,
-                      best_p, mirror, seq);
+  (void)accept_finish(n, greedy_ok(n, amax, T), path_tab, T, D, amax, top1p, accept_len, path_out,
+                      path_cap, bonus, best_p, mirror, seq);
 }
 
 __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
@@ -176,8 +180,8 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
   } else {
     __syncthreads();   // a single block: its own statistics, via LDS ordering
   }
-  (void)accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, D + 1, bonus, best_p,
-                      mirror, seq);
+  (void)accept_finish(n, greedy_ok(n, amax, T), path_tab, T, D, amax, top1p, accept_len, path_out,
+                      D + 1, bonus, best_p, mirror, seq);
 }
 
 // The same for a tree the device chose: the tree, its drafts and the prefix
@@ -213,8 +217,8 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_device_kernel(
   } else {
     __syncthreads();
   }
-  const int key = accept_finish(n, path_tab, T, D, amax, top1p, accept_len, path_out, path_cap,
-                                bonus, best_p, mirror, seq);
+  const int key = accept_finish(n, greedy_ok(n, amax, T), path_tab, T, D, amax, top1p, accept_len,
+                                path_out, path_cap, bonus, best_p, mirror, seq);
   if (threadIdx.x == 0) {
     const int a = key >> 10, best = 1023 - (key & 1023);
     const float s = top1p[best];
@@ -232,6 +236,79 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_device_kernel(
       dv.log[3] = __float_as_int(s);
     }
   }
+}
+
+// Logits of node i's draft token and of its parent's argmax under the
+// parent's LM-head row: X[parent] . W[tok] and X[parent] . W[argmax[parent]]
+// (fp32), one wave per node.  A draft token outside [0, V) gets -inf.
+__global__ __launch_bounds__(64) void draft_logits_kernel(
+    const int* __restrict__ parent, const uint16_t* __restrict__ X,
+    const uint16_t* __restrict__ W, int hid, int V, const int* __restrict__ tok,
+    const int* __restrict__ amax, float* __restrict__ z_draft, float* __restrict__ z_top) {
+  const int i = blockIdx.x, lane = threadIdx.x;
+  if (i == 0) {
+    if (lane == 0) {
+      z_draft[0] = 0.f;
+      z_top[0] = 0.f;
+    }
+    return;
+  }
+  const int p = parent[i];
+  const int t = tok[i];
+  const bool valid = t >= 0 && t < V;
+  int a = amax[p];
+  a = a < 0 ? 0 : (a >= V ? V - 1 : a);
+  const uint16_t* x = X + static_cast<size_t>(p) * hid;
+  const uint16_t* w1 = W + static_cast<size_t>(valid ? t : 0) * hid;
+  const uint16_t* w2 = W + static_cast<size_t>(a) * hid;
+  float s1 = 0.f, s2 = 0.f;
+  for (int c = lane; c < hid / 8; c += 64) {
+    const u32x4 xv = *reinterpret_cast<const u32x4*>(x + 8 * c);
+    const u32x4 v1 = *reinterpret_cast<const u32x4*>(w1 + 8 * c);
+    const u32x4 v2 = *reinterpret_cast<const u32x4*>(w2 + 8 * c);
+#pragma unroll
+    for (int e = 0; e < 4; ++e) {
+      const float xl = __uint_as_float(xv[e] << 16), xh = __uint_as_float(xv[e] & 0xFFFF0000u);
+      s1 += xl * __uint_as_float(v1[e] << 16) + xh * __uint_as_float(v1[e] & 0xFFFF0000u);
+      s2 += xl * __uint_as_float(v2[e] << 16) + xh * __uint_as_float(v2[e] & 0xFFFF0000u);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    s1 += __shfl_xor(s1, off, 64);
+    s2 += __shfl_xor(s2, off, 64);
+  }
+  if (lane == 0) {
+    z_draft[i] = valid ? s1 : -INFINITY;
+    z_top[i] = s2;
+  }
+}
+
+// Typical acceptance: node i >= 1 is locally acceptable when its draft
+// token's probability under the parent's temperature-scaled distribution,
+// exp((z_draft - z_top) * inv_temp) * top1p[parent], exceeds
+// min(eps, alpha * exp(-entropy[parent])).
+__global__ __launch_bounds__(kAcceptThreads) void accept_typical_kernel(
+    const int* __restrict__ parent, const int* __restrict__ depth,
+    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
+    const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ z_draft,
+    const float* __restrict__ z_top, const float* __restrict__ entropy,
+    const float* __restrict__ top1p, float inv_temp, float eps, float alpha,
+    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
+    float* __restrict__ best_p) {
+  const NodeIn n = accept_load(parent, depth, mask, tok, T);
+  const int i = threadIdx.x;
+  bool ok = false;
+  if (i == 0) {
+    ok = true;
+  } else if (i < T) {
+    const int p = n.parent;
+    const float pd = expf((z_draft[i] - z_top[i]) * inv_temp) * top1p[p];
+    const float thr = fminf(eps, alpha * expf(-entropy[p]));
+    ok = pd > thr;
+  }
+  (void)accept_finish(n, ok, path_tab, T, D, amax, top1p, accept_len, path_out, D + 1, bonus,
+                      best_p, nullptr, 0u);
 }
 
 }  // namespace
@@ -338,4 +415,50 @@ extern "C" int32_t entmtp_accept_batched(const entmtp_bank* bank, int32_t B, con
   hipLaunchKernelGGL(accept_batched_kernel, dim3(B), dim3(kAcceptThreads), 0,
                      static_cast<hipStream_t>(stream), a);
   return launch_status("accept_batched launch");
+}
+
+extern "C" int32_t entmtp_draft_logits(const entmtp_bank* bank, int32_t topo,
+                                       const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                       int32_t hid, int32_t V, const int32_t* draft_tokens,
+                                       const int32_t* argmax, float* z_draft, float* z_top,
+                                       void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(hidden && w_lm && draft_tokens && argmax && z_draft && z_top, ENTMTP_EINVAL,
+                   "pointers must be non-NULL");
+  ENTMTP_CHECK_ARG(hid >= 8 && hid % 8 == 0 && V >= 1, ENTMTP_EINVAL,
+                   "hid = %d (a positive multiple of 8), V = %d", hid, V);
+  ENTMTP_CHECK_ARG(aligned16(hidden) && aligned16(w_lm), ENTMTP_EINVAL,
+                   "hidden and w_lm must be 16-byte aligned");
+  if (int32_t rc = check_device_bank(bank, topo)) return rc;
+  const TopoDesc& d = bank->desc[topo];
+  hipLaunchKernelGGL(draft_logits_kernel, dim3(d.T), dim3(64), 0, static_cast<hipStream_t>(stream),
+                     bank_ptr<int>(bank, d.off_parent), reinterpret_cast<const uint16_t*>(hidden),
+                     reinterpret_cast<const uint16_t*>(w_lm), hid, V, draft_tokens, argmax, z_draft,
+                     z_top);
+  return launch_status("draft_logits launch");
+}
+
+extern "C" int32_t entmtp_accept_typical(const entmtp_bank* bank, int32_t topo,
+                                         const int32_t* draft_tokens, const int32_t* argmax,
+                                         const float* z_draft, const float* z_top,
+                                         const float* entropy, const float* top1p,
+                                         float inv_temp, float eps, float alpha,
+                                         int32_t* accept_len, int32_t* path, int32_t* bonus,
+                                         float* best_top1p, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(draft_tokens && argmax && z_draft && z_top && entropy && top1p && accept_len &&
+                       path && bonus,
+                   ENTMTP_EINVAL, "inputs and outputs (except best_top1p) must be non-NULL");
+  ENTMTP_CHECK_ARG(inv_temp > 0.f && inv_temp < INFINITY, ENTMTP_EINVAL,
+                   "inv_temp must be positive and finite");
+  ENTMTP_CHECK_ARG(eps >= 0.f && alpha >= 0.f && eps < INFINITY && alpha < INFINITY, ENTMTP_EINVAL,
+                   "eps and alpha must be finite and >= 0");
+  if (int32_t rc = check_device_bank(bank, topo)) return rc;
+  const TopoDesc& d = bank->desc[topo];
+  hipLaunchKernelGGL(accept_typical_kernel, dim3(1), dim3(kAcceptThreads), 0,
+                     static_cast<hipStream_t>(stream), bank_ptr<int>(bank, d.off_parent),
+                     bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
+                     bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, argmax, z_draft, z_top,
+                     entropy, top1p, inv_temp, eps, alpha, accept_len, path, bonus, best_top1p);
+  return launch_status("accept_typical launch");
 }

@@ -140,6 +140,23 @@ def test_kernel_calls_reject_bad_arguments_without_launching():
     assert api.tree_attn_batched_workspace(8, 128, 32, 8, 128, 16384) == \
         8 * api.tree_attn_workspace(128, 32, 8, 128, 16384)
     assert api.tree_attn_batched_workspace(0, 128, 32, 8, 128, 16384) == 0
+    # typical acceptance: scalars and pointers before the bank
+    f = ctypes.c_float
+    assert lib.entmtp_draft_logits(host_bank.handle, 0, p, p, 260, 100, p, p, p, p, None) == api.EINVAL
+    assert lib.entmtp_draft_logits(host_bank.handle, 0, p, None, 256, 100, p, p, p, p,
+                                   None) == api.EINVAL
+    assert lib.entmtp_draft_logits(host_bank.handle, 0, p, p, 256, 0, p, p, p, p, None) == api.EINVAL
+    rc = lib.entmtp_draft_logits(host_bank.handle, 0, p, p, 256, 100, p, p, p, p, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
+    for it, eps, alpha in ((0.0, 0.09, 0.3), (float("inf"), 0.09, 0.3), (1.0, -0.1, 0.3),
+                           (1.0, 0.09, float("nan")), (1.0, float("inf"), 0.3)):
+        assert lib.entmtp_accept_typical(host_bank.handle, 0, p, p, p, p, p, p, f(it), f(eps), f(alpha),
+                                         p, p, p, None, None) == api.EINVAL
+    assert lib.entmtp_accept_typical(host_bank.handle, 0, p, p, p, p, None, p, f(1.0), f(0.09),
+                                     f(0.3), p, p, p, None, None) == api.EINVAL
+    rc = lib.entmtp_accept_typical(host_bank.handle, 0, p, p, p, p, p, p, f(1.0), f(0.09), f(0.3),
+                                   p, p, p, None, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
     # workspace query
     assert api.tree_attn_workspace(27, 32, 32, 64, 256) == 0
     assert api.tree_attn_workspace(27, 30, 8, 128, 256) == 0
