@@ -5,12 +5,15 @@ A step is one pass of the whole verification hot path at batch 1:
   host: pick the tree for this step with the hysteretic ladder (tau_on 0.8,
         tau_off 0.6) from the previous step's top-1 probability at the
         deepest accepted node;
-  GPU:  tree attention (tree K/V appended to the cache) -> LM-head logits with
-        fused softmax statistics -> greedy acceptance -> KV compaction, all
-        enqueued by one entmtp_step_launch;
-  host: poll the pinned record acceptance publishes (accept length, feature)
+  GPU:  tree attention (tree K/V appended to the cache), LM-head logits with
+        fused softmax statistics -> greedy acceptance, and KV compaction, all
+        enqueued by one entmtp_step_launch (the compaction of a step goes out
+        with the next step's launch, on the cache stream, beside the next LM
+        head);
+  host: poll the pinned record acceptance publishes (accept length, s, path)
         -- the step's one device-to-host read -- and grow the prefix by
-        accept_len + 1 while the compaction finishes.
+        accept_len + 1.
+The timed region ends with a flush, so it holds exactly K compactions.
 
 Default workload: Vicuna-7B shapes (32 x 128 heads, hidden 4096, vocab
 32000), a 5-tree bank with {1, 8, 26, 64, 128} nodes, prefix 2048 growing
@@ -47,6 +50,9 @@ def parse():
     ap.add_argument("--pool", type=int, default=32, help="distinct per-step input sets")
     ap.add_argument("--weight-copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--event-every", type=int, default=8,
+                    help="time the LM head with HIP events on every n-th timed step (each "
+                         "event pair costs the host a few microseconds)")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--fixed-topo", type=int, default=-1,
                     help="disable the scheduler and use this bank entry every step")
@@ -145,9 +151,9 @@ def main():
     log(f"staged inputs in {time.time() - t0:.1f}s")
 
     # the step loop runs on a stream of its own (non-blocking: launches on the
-    # legacy default stream cost the host more); one step context per
-    # LM-head weight copy, all sharing the caches; the statistics come from
-    # the LM head's accumulators, so no logits are materialised
+    # legacy default stream cost the host more); one step context, the
+    # LM-head weight copy passed per step; the statistics come from the LM
+    # head's accumulators, so no logits are materialised
     run_stream = torch.cuda.Stream()
     # the ladder runs on the host (one result read per step, as in the paper's
     # loop) or, with --gpu-scheduler, on the GPU for the growing-prefix
@@ -155,10 +161,9 @@ def main():
     # moves
     on_gpu = grows and args.gpu_scheduler
     tau_on, tau_off = (0.8, 0.6) if args.fixed_topo < 0 else (float("inf"), float("-inf"))
-    st = [api.Step(bank, k_cache, v_cache, w, Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax,
+    st = [api.Step(bank, k_cache, v_cache, W[0], Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax,
                    scale=scale, rope_theta=theta, keep_logits=False, tau_on=tau_on,
-                   tau_off=tau_off, stream=run_stream)
-          for w in (W[:1] if on_gpu else W)]
+                   tau_off=tau_off, stream=run_stream)]
     torch.cuda.synchronize()
     out = torch.empty((Tmax, Hq, d), dtype=bf, device=dev)
 
@@ -212,9 +217,9 @@ def main():
         L = state["L"] if grows else L0
         topo = state["rung"]
         e = pool_p[t % P]
-        chk(lib.entmtp_step_launch(handles[t % len(handles)], topo, L, e["q"], e["kt"], e["vt"],
-                                   out_p, e["x"], e["tok"][topo], ev[0], ev[1]))
-        chk(lib.entmtp_step_wait(handles[t % len(handles)], a_r, b_r, s_r, 30.0))
+        chk(lib.entmtp_step_launch(handles[0], topo, L, e["q"], e["kt"], e["vt"], out_p, e["x"],
+                                   W_p[t % len(W_p)], e["tok"][topo], ev[0], ev[1]))
+        chk(lib.entmtp_step_wait(handles[0], a_r, b_r, s_r, 30.0))
         a, s = a_c.value, s_c.value
         if grows:
             state["L"] = L + a + 1
@@ -228,12 +233,15 @@ def main():
     run = step_gpu if on_gpu else step
     for t in range(args.warmup):
         run(t)
+    chk(lib.entmtp_step_flush(handles[0]))   # the last warm-up step's compaction
     torch.cuda.synchronize()
 
     # ---------------------------------------------------------- timed
     K = args.steps
+    NE = max(1, args.event_every)
+    sampled = list(range(0, K, NE))      # timed steps whose LM head carries an event pair
     events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in range(K)]
+              for _ in sampled]
     for a_, b_ in events:          # torch creates an event's handle on its first record
         a_.record()
         b_.record()
@@ -242,7 +250,8 @@ def main():
     torch.cuda.synchronize()
     t_start = time.perf_counter()
     for t in range(K):
-        trace.append(run(args.warmup + t, ev_p[t]))
+        trace.append(run(args.warmup + t, ev_p[t // NE] if t % NE == 0 else (None, None)))
+    chk(lib.entmtp_step_flush(handles[0]))   # the last timed step's compaction
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
     if on_gpu:   # the steps' (tree, prefix, accept length, s) as the GPU logged them
@@ -253,7 +262,7 @@ def main():
 
     lm_ms = [a.elapsed_time(b) for a, b in events]
     by_T = {}
-    for (T, *_), ms in zip(trace, lm_ms):
+    for (T, *_), ms in zip([trace[t] for t in sampled], lm_ms):
         by_T.setdefault(T, []).append(ms)
     lm_us_by_T = {str(T): round(float(np.mean(v)) * 1e3, 2) for T, v in sorted(by_T.items())}
     # algorithmic bytes (what the method must move; fp32 logits excluded)
@@ -268,7 +277,7 @@ def main():
         return w + kv + tree_in + tree_kv_out + att_out + compact + stats
 
     bytes_total = sum(step_bytes(T, L, a) for T, L, a, _, _ in trace)
-    lm_bytes = sum(V * hid * 2 + T * hid * 2 for T, _, _, _, _ in trace)
+    lm_bytes = sum(V * hid * 2 + trace[t][0] * hid * 2 for t in sampled)
     lm_s = sum(lm_ms) / 1e3
     steps_per_s = K / elapsed
     us = elapsed / K * 1e6
@@ -287,7 +296,8 @@ def main():
     # ---------------------------------------------------------- cpu baseline
     cpu = None
     if not args.no_cpu_baseline:
-        cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta)
+        cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta,
+                           [topo for *_, topo in trace])
 
     traffic = lm_head_traffic([T for T, *_ in trace])
 
@@ -306,11 +316,13 @@ def main():
                    "T_histogram": {str(k): v for k, v in sorted(Tcount.items())},
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
-        "roofline": {"kernel": "lm_head_hyb_kernel (entmtp_verify_logits_partials)", "bound": "hbm",
+        "roofline": {"kernel": "LM head with statistics partials (lm_head_hyb_loop_kernel up to 32 nodes, lm_head_hyb_kernel above)", "bound": "hbm",
                      "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
                      "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "algorithmic_bytes_per_launch": round(lm_bytes / K),
-                     "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T},
+                     "algorithmic_bytes_per_launch": round(lm_bytes / len(sampled)),
+                     "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T,
+                     "timed_launches": len(sampled),
+                     "timing": f"HIP events around the LM-head launch of every {NE}-th timed step"},
         "cpu_baseline": cpu,
     }
     print(json.dumps(line), flush=True)
@@ -343,8 +355,9 @@ def lm_head_traffic(Ts):
     return round(tot / len(Ts))
 
 
-def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta):
-    """The oracle, as it stands, on a bounded sample of the same workload."""
+def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta, topo_seq):
+    """The oracle, as it stands, on a bounded sample of the same workload: the
+    timed run's own sequence of trees, from its start, until the time budget."""
     from oracle import entmtp_oracle as orc
     try:
         from threadpoolctl import threadpool_info
@@ -352,8 +365,8 @@ def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta):
     except Exception:
         threads = os.cpu_count() or 1
     Hkv, d, L0 = wl.n_kv_heads, wl.head_dim, wl.prefix_len
-    # sample: the bank's trees in turn, at the starting prefix, until the budget
-    order = list(range(len(trees)))[::-1]
+    # sample: the trees the GPU run chose, in order, at the starting prefix
+    order = list(topo_seq) or list(range(len(trees)))
     done, t0 = [], time.perf_counter()
     kc = np.zeros((Hkv, L0 + 256, d), np.uint16)
     vc = np.zeros_like(kc)
@@ -368,9 +381,13 @@ def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta):
         if time.perf_counter() - t0 > args.cpu_budget_s:
             break
     el = time.perf_counter() - t0
+    hist = {}
+    for T in done:
+        hist[T] = hist.get(T, 0) + 1
     return {"value": round(len(done) / el, 4), "unit": "steps/s", "cores": threads,
             "kind": "oracle",
-            "sample": f"{len(done)} oracle steps of {wl.name} (tree sizes {done}, prefix {L0}), "
+            "sample": f"the first {len(done)} steps of the timed run's tree sequence of {wl.name} "
+                      f"(tree-size histogram {dict(sorted(hist.items()))}) at prefix {L0}, "
                       f"{el:.1f}s; fp64 numpy/BLAS on host cores"}
 
 

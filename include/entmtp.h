@@ -415,9 +415,8 @@ int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
  *              outputs of acceptance, as for entmtp_accept
  *   workspace  scratch of entmtp_step_workspace() bytes, 256-byte aligned,
  *              used by this step object only (it holds attention partials,
- *              statistics partials and an arrival counter that
- *              entmtp_step_create clears with an asynchronous memset on the
- *              stream)
+ *              statistics partials and the device-scheduled state, which
+ *              entmtp_step_create initialises on the stream)
  *   stream     the HIP stream every launch goes to (NULL: the null stream)
  *   tau_on, tau_off   thresholds of the hysteretic ladder (§4 "Policy") for
  *              device-scheduled steps, tau_off <= tau_on (unused otherwise)
@@ -463,44 +462,61 @@ void entmtp_step_destroy(entmtp_step* step);
 
 /*
  * Enqueues one verification step for tree `topo` at prefix length prefix_len,
- * asynchronously:
- *   for each layer  entmtp_tree_attn (writes K/V slots [L, L+T) of the layer),
- *                   on a side stream the step object owns, forked from the
- *                   configured stream
- *   the LM head with fused statistics partials, on the configured stream,
- *   concurrently with the attention layers
- *   the statistics merge and greedy acceptance, in one launch; acceptance
- *   also publishes (accept_len, bonus, best_top1p) to host memory
- *   compaction of the accepted path in every layer, after the side stream
- *   has joined the configured stream
- * Every output is complete once the configured stream is; work enqueued on
- * that stream afterwards is ordered after the whole step.
+ * asynchronously, as two chains:
+ *   on the configured stream   the LM head with fused statistics partials,
+ *              then the statistics merge and greedy acceptance (one launch
+ *              for trees of up to 32 nodes, two for larger ones); acceptance
+ *              also publishes its result (accept_len, bonus, best_top1p and
+ *              the accepted path) to pinned host memory
+ *   on a side stream the step object owns, ordered after everything enqueued
+ *   on the configured stream before this call
+ *              the compaction of the previous step (the one whose result
+ *              entmtp_step_wait read last, at that step's prefix length), then
+ *              for each layer entmtp_tree_attn (writes K/V slots [L, L+T))
+ * Nothing on the configured stream waits for the side stream: the LM head of
+ * the next step runs beside this step's compaction and attention.  The
+ * compaction of a step is therefore enqueued by the next launch, or by
+ * entmtp_step_flush, and the cache and `out` are complete on the configured
+ * stream only after entmtp_step_flush.
+ * Every launch must be followed by entmtp_step_wait before the next launch
+ * (the compaction takes the accepted path from the host record).
  * Per-step inputs (device): q, k_tree, v_tree, out laid out with tree_rows
- * rows per layer; hidden [T][hid] bf16; draft_tokens [T] int32.
+ * rows per layer; hidden [T][hid] bf16; draft_tokens [T] int32; w_lm the
+ * LM-head weight for this step ([V][hid] bf16, 16-byte aligned; NULL: the
+ * configured one).
  * ev_lm_begin / ev_lm_end: optional hipEvent_t recorded on the stream right
  * before and after the LM-head launch (NULL: none).
  * Requirements: prefix_len >= 0, prefix_len + T <= cap.
- * Errors: EINVAL, ERANGE, EHIP (a failed launch leaves the step unusable for
- * entmtp_step_wait until the next successful launch).
+ * Errors: EINVAL (also: the previous result was not read), ERANGE, EHIP (a
+ * failed launch leaves the step unusable for entmtp_step_wait until the next
+ * successful launch).
  */
 int32_t entmtp_step_launch(entmtp_step* step, int32_t topo, int32_t prefix_len,
                            const entmtp_bf16* q, const entmtp_bf16* k_tree,
                            const entmtp_bf16* v_tree, entmtp_bf16* out,
-                           const entmtp_bf16* hidden, const int32_t* draft_tokens,
-                           void* ev_lm_begin, void* ev_lm_end);
+                           const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                           const int32_t* draft_tokens, void* ev_lm_begin, void* ev_lm_end);
 
 /*
  * Waits for the acceptance result of the latest entmtp_step_launch by polling
- * the pinned host record (no stream synchronisation: attention and compaction
- * may still be running, and later work on the stream stays ordered after
- * them).  Writes
- * the accepted draft count, the bonus token and the top-1 probability at the
- * accepted node (the scheduler's s, §4) to the host pointers given (each may
- * be NULL).  Gives up after timeout_s seconds with ETIMEDOUT, or earlier with
- * EHIP when the stream reports an error.
+ * the pinned host record (no stream synchronisation: attention may still be
+ * running).  Writes the accepted draft count, the bonus token and the top-1
+ * probability at the accepted node (the scheduler's s, §4) to the host
+ * pointers given (each may be NULL), and keeps the accepted path for the
+ * step's compaction.  Gives up after timeout_s seconds with ETIMEDOUT, or
+ * earlier with EHIP when the stream reports an error.
  */
 int32_t entmtp_step_wait(entmtp_step* step, int32_t* accept_len, int32_t* bonus,
                          float* best_top1p, double timeout_s);
+
+/*
+ * Enqueues the compaction of the last step whose result was read (if not yet
+ * enqueued) and joins the side stream into the configured stream: work
+ * enqueued on the configured stream afterwards sees every step's cache
+ * update and attention output.  Errors: EINVAL (a launched step's result has
+ * not been read), EHIP.
+ */
+int32_t entmtp_step_flush(entmtp_step* step);
 
 /*
  * Device-scheduled steps: the tree choice of §4 moved next to the statistics
@@ -511,12 +527,16 @@ int32_t entmtp_step_wait(entmtp_step* step, int32_t* accept_len, int32_t* bonus,
  * device memory, so the host enqueues step after step without reading
  * anything back.  The decisions are those of entmtp_ladder_next on the same s.
  *
- * entmtp_step_device_start: sets the device state to tree `topo` at
- * prefix_len (asynchronously, on the configured stream).  Requires a bank of
- * trees of at most 128 nodes.  Errors: EINVAL, ERANGE, EHIP.
+ * entmtp_step_device_start: flushes host-scheduled steps (entmtp_step_flush)
+ * and sets the device state to tree `topo` at prefix_len (asynchronously, on
+ * the configured stream).  Requires a bank of trees of at most 128 nodes.
+ * Errors: EINVAL, ERANGE, EHIP.
  *
  * entmtp_step_launch_device: enqueues one step for the tree the device state
- * holds (the same kernels as entmtp_step_launch, sized for the largest tree).
+ * holds (the same kernels as entmtp_step_launch, sized for the largest tree;
+ * the attention runs on the side stream, which the configured stream joins
+ * before the step's compaction, so every output is complete once the
+ * configured stream is).
  * Inputs as for entmtp_step_launch, except
  *   w_lm    the LM-head weight for this step ([V][hid] bf16, NULL: the
  *           configured one)

@@ -76,7 +76,8 @@ _SIGNATURES = {
     "entmtp_step_create": (_c_i32, [_c_p, ctypes.POINTER(StepConfig), ctypes.POINTER(_c_p)]),
     "entmtp_step_destroy": (None, [_c_p]),
     "entmtp_step_launch": (_c_i32, [_c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
-                                    _c_p]),
+                                    _c_p, _c_p]),
+    "entmtp_step_flush": (_c_i32, [_c_p]),
     "entmtp_step_wait": (_c_i32, [_c_p, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
                                   ctypes.POINTER(_c_f32), ctypes.c_double]),
     "entmtp_step_device_start": (_c_i32, [_c_p, _c_i32, _c_i32]),
@@ -577,10 +578,16 @@ class Step:
         return self._h
 
     def launch(self, topo: int, prefix_len: int, q, k_tree, v_tree, out, hidden, draft_tokens,
-               ev_lm_begin=None, ev_lm_end=None) -> None:
+               ev_lm_begin=None, ev_lm_end=None, w_lm=None) -> None:
+        """One host-scheduled step; the previous step's compaction goes with it
+        (``flush`` completes the cache on the configured stream)."""
         ev = [None if e is None else _c_p(e.cuda_event) for e in (ev_lm_begin, ev_lm_end)]
         _check(lib.entmtp_step_launch(self._h, topo, prefix_len, _p(q), _p(k_tree), _p(v_tree),
-                                      _p(out), _p(hidden), _p(draft_tokens), ev[0], ev[1]))
+                                      _p(out), _p(hidden), _p(w_lm), _p(draft_tokens), ev[0],
+                                      ev[1]))
+
+    def flush(self) -> None:
+        _check(lib.entmtp_step_flush(self._h))
 
     def wait(self, timeout_s: float = 30.0):
         _check(lib.entmtp_step_wait(self._h, ctypes.byref(self._a), ctypes.byref(self._b),

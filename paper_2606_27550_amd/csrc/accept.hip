@@ -8,8 +8,13 @@
 // locally matching nodes, so all nodes are decided in parallel.  The answer is
 // the deepest accepted node, lowest index among equals; its depth is the
 // accept length (§5.1).  One workgroup handles the whole tree.  Inside a
-// verification step the acceptance runs fused behind the statistics: the
-// last of the tree's per-node statistics blocks to finish accepts the tree.
+// verification step of a small tree the acceptance runs fused behind the
+// statistics in one workgroup: its wavefronts merge the LM head's partials
+// node by node into LDS, and the same workgroup then accepts the tree from
+// there, so no device-wide fence or arrival counter sits between the two.
+// (The workgroup is one wavefront per SIMD, so it finds room on a CU beside
+// the attention kernel.)  Larger trees merge their statistics in a kernel of
+// their own, one wavefront per node, before the acceptance kernel.
 #include "common.hpp"
 #include "stats.hpp"
 
@@ -17,7 +22,8 @@ namespace entmtp {
 namespace {
 
 constexpr int kAcceptThreads = ENTMTP_T_MAX;
-static_assert(kAcceptThreads == kFinThreads, "the fused kernel runs both halves with one block size");
+constexpr int kFinAccThreads = 256;    // statistics + acceptance of one step, one workgroup
+constexpr int kFusedMaxT = 32;         // larger trees: a separate statistics kernel
 
 // A thread's node of the tree (thread i holds node i): what the acceptance
 // needs that does not depend on the target's statistics, so a kernel can
@@ -46,20 +52,23 @@ __device__ __forceinline__ NodeIn accept_load(const int* __restrict__ parent,
 // The acceptance of one tree by one workgroup of kAcceptThreads threads;
 // returns (in every thread) depth(best) * 1024 + (1023 - best).
 // Greedy local test: node i's draft token is the target's argmax at its parent.
-__device__ __forceinline__ bool greedy_ok(const NodeIn& n, const int* __restrict__ amax, int T) {
+__device__ __forceinline__ bool greedy_ok(const NodeIn& n, const int* amax, int T) {
   const int i = threadIdx.x;
   return i < T && (i == 0 || n.tok == amax[n.parent]);
 }
 
-// `ok`: this thread's node is locally acceptable (the root always is).
+// `ok`: this thread's node is locally acceptable (the root always is).  NTH:
+// the workgroup size (at least ENTMTP_T_MAX).
+template <int NTH = kAcceptThreads>
 __device__ __forceinline__ int accept_finish(
     const NodeIn& n, bool ok, const int* __restrict__ path_tab, int T, int D,
-    const int* __restrict__ amax, const float* __restrict__ top1p,
+    const int* amax, const float* top1p,
     int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
     int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
     uint32_t seq) {
+  static_assert(NTH >= ENTMTP_T_MAX && NTH % 64 == 0, "one thread per possible node");
   __shared__ uint32_t matched[ENTMTP_MASK_WORDS];
-  __shared__ int s_key[kAcceptThreads / 64];
+  __shared__ int s_key[NTH / 64];
   const int i = threadIdx.x;
   if (i < ENTMTP_MASK_WORDS) matched[i] = 0u;
   __syncthreads();
@@ -79,23 +88,35 @@ __device__ __forceinline__ int accept_finish(
   __syncthreads();
   key = s_key[0];
 #pragma unroll
-  for (int w = 1; w < kAcceptThreads / 64; ++w) key = max(key, s_key[w]);
+  for (int w = 1; w < NTH / 64; ++w) key = max(key, s_key[w]);
   const int best = 1023 - (key & 1023);
   const int a = key >> 10;
   if (i < path_cap) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
   if (i == 0) {
-    const int bon = amax[best];
-    const float p1 = top1p ? top1p[best] : 0.f;
     *accept_len = a;
-    *bonus = bon;
-    if (best_p) *best_p = p1;
-    if (mirror) {
-      mirror->accept_len = a;
-      mirror->bonus = bon;
-      mirror->best_top1p = p1;
-      __threadfence_system();
-      __hip_atomic_store(&mirror->seq, seq, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_SYSTEM);
+    *bonus = amax[best];
+    if (best_p) *best_p = top1p ? top1p[best] : 0.f;
+  }
+  if (mirror && i < kMirrorWords) {   // one tagged word per lane
+    uint32_t field;
+    if (i == 0) {
+      field = static_cast<uint32_t>(a);
+    } else if (i == 1) {
+      field = static_cast<uint32_t>(amax[best]);
+    } else if (i == 2) {
+      field = __float_as_uint(top1p ? top1p[best] : 0.f);
+    } else {
+      field = 0u;
+#pragma unroll
+      for (int b = 0; b < 4; ++b) {
+        const int j = (i - 3) * 4 + b;
+        const uint32_t node = j <= a ? static_cast<uint32_t>(path_tab[best * (D + 1) + j]) : 0xffu;
+        field |= (node & 0xffu) << (8 * b);
+      }
     }
+    __hip_atomic_store(reinterpret_cast<uint64_t*>(mirror) + i,
+                       (static_cast<uint64_t>(seq) << 32) | field, __ATOMIC_RELAXED,
+                       __HIP_MEMORY_SCOPE_SYSTEM);
   }
   return key;
 }
@@ -154,48 +175,38 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_batched_kernel(AcceptBa
               p.best ? p.best + b : nullptr, nullptr, 0u);
 }
 
-// Statistics of node blockIdx.x from the LM head's partials, then -- in the
-// last block to finish, once every node's statistics are visible -- the
-// acceptance of the tree.  `counter` is 0 on entry and left 0 on exit.
-__global__ __launch_bounds__(kAcceptThreads) void finalize_accept_kernel(
+// Statistics of every node of the tree from the LM head's partials, then the
+// acceptance of the tree, by one workgroup of kFinAccThreads threads.
+__global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
     const StatPart* __restrict__ part, int G, float inv_temp, float* __restrict__ entropy,
-    float* __restrict__ top1p, int* __restrict__ amax, unsigned* __restrict__ counter,
-    const int* __restrict__ parent, const int* __restrict__ depth,
-    const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
-    const int* __restrict__ tok, int* __restrict__ accept_len, int* __restrict__ path_out,
-    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
-    uint32_t seq) {
+    float* __restrict__ top1p, int* __restrict__ amax, const int* __restrict__ parent,
+    const int* __restrict__ depth, const uint32_t* __restrict__ mask,
+    const int* __restrict__ path_tab, int T, int D, const int* __restrict__ tok,
+    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
+    float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
+  __shared__ float s_p1[ENTMTP_T_MAX];
+  __shared__ int s_am[ENTMTP_T_MAX];
   // the tree's own inputs are fetched while the partials merge
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
-  finalize_node(part, G, inv_temp, entropy, top1p, amax);
-  if (T > 1) {
-    __shared__ int s_last;
-    __threadfence();   // this node's statistics are visible device-wide ...
-    __syncthreads();
-    if (threadIdx.x == 0) s_last = atomicAdd(counter, 1u) == static_cast<unsigned>(T - 1);
-    __syncthreads();   // ... before its arrival is counted
-    if (!s_last) return;
-    __threadfence();   // the last block sees every node's statistics
-    if (threadIdx.x == 0) *counter = 0u;
-  } else {
-    __syncthreads();   // a single block: its own statistics, via LDS ordering
-  }
-  (void)accept_finish(n, greedy_ok(n, amax, T), path_tab, T, D, amax, top1p, accept_len, path_out,
-                      D + 1, bonus, best_p, mirror, seq);
+  finalize_nodes<kFinAccThreads>(part, G, T, inv_temp, entropy, top1p, amax, s_p1, s_am);
+  __syncthreads();
+  (void)accept_finish<kFinAccThreads>(n, greedy_ok(n, s_am, T), path_tab, T, D, s_am, s_p1,
+                                      accept_len, path_out, D + 1, bonus, best_p, mirror, seq);
 }
 
 // The same for a tree the device chose: the tree, its drafts and the prefix
-// length come from *dv.cur; the last block also runs the ladder and writes
-// the next step's state (tree, node count, prefix length).
-__global__ __launch_bounds__(kAcceptThreads) void finalize_accept_device_kernel(
+// length come from *dv.cur; the workgroup also runs the ladder and writes the
+// next step's state (tree, node count, prefix length).
+__global__ __launch_bounds__(kFinAccThreads) void finalize_accept_device_kernel(
     FinAccDevice dv, const uint8_t* __restrict__ arena, const StatPart* __restrict__ part, int G,
     float inv_temp, float* __restrict__ entropy, float* __restrict__ top1p,
-    int* __restrict__ amax, unsigned* __restrict__ counter, int* __restrict__ accept_len,
-    int* __restrict__ path_out, int path_cap, int* __restrict__ bonus, float* __restrict__ best_p,
+    int* __restrict__ amax, int* __restrict__ accept_len, int* __restrict__ path_out,
+    int path_cap, int* __restrict__ bonus, float* __restrict__ best_p,
     StepMirror* __restrict__ mirror, uint32_t seq) {
+  __shared__ float s_p1[ENTMTP_T_MAX];
+  __shared__ int s_am[ENTMTP_T_MAX];
   const DevStep st = *dv.cur;
   const int T = st.T;
-  if (static_cast<int>(blockIdx.x) >= T) return;   // the grid covers the largest tree
   const DevTopo* t = dv.topos + st.rung;
   const int* parent = reinterpret_cast<const int*>(arena + t->off_parent);
   const int* depth = reinterpret_cast<const int*>(arena + t->off_depth);
@@ -204,24 +215,14 @@ __global__ __launch_bounds__(kAcceptThreads) void finalize_accept_device_kernel(
   const int D = t->D;
   const int* tok = dv.drafts + static_cast<size_t>(st.rung) * dv.tree_rows;
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
-  finalize_node(part, G, inv_temp, entropy, top1p, amax);
-  if (T > 1) {
-    __shared__ int s_last;
-    __threadfence();
-    __syncthreads();
-    if (threadIdx.x == 0) s_last = atomicAdd(counter, 1u) == static_cast<unsigned>(T - 1);
-    __syncthreads();
-    if (!s_last) return;
-    __threadfence();
-    if (threadIdx.x == 0) *counter = 0u;
-  } else {
-    __syncthreads();
-  }
-  const int key = accept_finish(n, greedy_ok(n, amax, T), path_tab, T, D, amax, top1p, accept_len,
-                                path_out, path_cap, bonus, best_p, mirror, seq);
+  finalize_nodes<kFinAccThreads>(part, G, T, inv_temp, entropy, top1p, amax, s_p1, s_am);
+  __syncthreads();
+  const int key = accept_finish<kFinAccThreads>(n, greedy_ok(n, s_am, T), path_tab, T, D, s_am,
+                                                s_p1, accept_len, path_out, path_cap, bonus,
+                                                best_p, mirror, seq);
   if (threadIdx.x == 0) {
     const int a = key >> 10, best = 1023 - (key & 1023);
-    const float s = top1p[best];
+    const float s = s_p1[best];
     const int next = ladder_step(st.rung, dv.n_topo, s, dv.tau_on, dv.tau_off);
     DevStep nx;
     nx.rung = next;
@@ -334,26 +335,31 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
 int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevice& dv,
                                       const void* partials, int32_t V, float inv_temp,
                                       float* entropy, float* top1p, int32_t* argmax,
-                                      unsigned* counter, int32_t* accept_len, int32_t* path,
-                                      int32_t path_capacity, int32_t* bonus, float* best_top1p,
-                                      StepMirror* mirror, uint32_t seq, hipStream_t stream) {
-  hipLaunchKernelGGL(finalize_accept_device_kernel, dim3(dv.t_max), dim3(kAcceptThreads), 0, stream,
-                     dv, bank->arena, static_cast<const StatPart*>(partials), stats_slices(V),
-                     inv_temp, entropy, top1p, argmax, counter, accept_len, path, path_capacity,
-                     bonus, best_top1p, mirror, seq);
+                                      int32_t* accept_len, int32_t* path, int32_t path_capacity,
+                                      int32_t* bonus, float* best_top1p, StepMirror* mirror,
+                                      uint32_t seq, hipStream_t stream) {
+  hipLaunchKernelGGL(finalize_accept_device_kernel, dim3(1), dim3(kFinAccThreads), 0, stream, dv,
+                     bank->arena, static_cast<const StatPart*>(partials), stats_slices(V),
+                     inv_temp, entropy, top1p, argmax, accept_len, path, path_capacity, bonus,
+                     best_top1p, mirror, seq);
   return launch_status("finalize_accept (device-scheduled) launch");
 }
 
 int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,
                                int32_t V, float inv_temp, float* entropy, float* top1p,
-                               int32_t* argmax, unsigned* counter, const int32_t* draft_tokens,
-                               int32_t* accept_len, int32_t* path, int32_t* bonus,
-                               float* best_top1p, StepMirror* mirror, uint32_t seq,
-                               hipStream_t stream) {
+                               int32_t* argmax, const int32_t* draft_tokens, int32_t* accept_len,
+                               int32_t* path, int32_t* bonus, float* best_top1p,
+                               StepMirror* mirror, uint32_t seq, hipStream_t stream) {
   const TopoDesc& d = bank->desc[topo];
-  hipLaunchKernelGGL(finalize_accept_kernel, dim3(d.T), dim3(kAcceptThreads), 0, stream,
+  if (d.T > kFusedMaxT) {
+    if (int32_t rc = launch_stats_finalize(partials, d.T, V, inv_temp, entropy, top1p, argmax, stream))
+      return rc;
+    return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,
+                         best_top1p, mirror, seq, stream);
+  }
+  hipLaunchKernelGGL(finalize_accept_kernel, dim3(1), dim3(kFinAccThreads), 0, stream,
                      static_cast<const StatPart*>(partials), stats_slices(V), inv_temp, entropy,
-                     top1p, argmax, counter, bank_ptr<int>(bank, d.off_parent),
+                     top1p, argmax, bank_ptr<int>(bank, d.off_parent),
                      bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
                      bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, accept_len, path,
                      bonus, best_top1p, mirror, seq);

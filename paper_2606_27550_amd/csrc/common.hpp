@@ -106,15 +106,22 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
                            int cap, int Hq, int Hkv, float scale, float rope_theta,
                            entmtp_bf16* out, void* workspace, hipStream_t stream);
 
-// Result of one verification step as the host reads it: written by the accept
-// kernel into coherent pinned host memory, fields first, then `seq` with
-// system-scope release, so a host that sees `seq` also sees the fields.
+// Result of one verification step as the host reads it, written by the accept
+// kernel into coherent pinned host memory.  Every word is 64 bits: the step's
+// sequence number in the upper half and one field in the lower half, stored
+// by one lane as a single system-scope store.  A word is therefore complete
+// or stale, never torn, and the host takes the record once every word it
+// needs carries the sequence number it waits for -- no fence orders the
+// words, so publishing costs the kernel no cache write-back.
+constexpr int kMirrorPathWords = (ENTMTP_D_MAX + 1 + 3) / 4;  // 4 path entries per word
+constexpr int kMirrorWords = 3 + kMirrorPathWords;
 struct StepMirror {
-  uint32_t seq;
-  int32_t accept_len;
-  int32_t bonus;
-  float best_top1p;
+  uint64_t accept_len;
+  uint64_t bonus;
+  uint64_t best_top1p;                  // float bits
+  uint64_t path[kMirrorPathWords];      // node index bytes, entry j in byte j % 4 of word j / 4
 };
+static_assert(sizeof(StepMirror) == kMirrorWords * sizeof(uint64_t), "mirror layout");
 
 // Launches the accept kernel (no argument checks beyond the bank's); with a
 // non-NULL `mirror` (device address of host memory) it also publishes the
@@ -128,22 +135,22 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
 // bank tree k are row k of drafts [n_topo][tree_rows]; after accepting, the
 // ladder picks the next tree from s = top1p[best] and writes *next =
 // {rung', T', L + accept_len + 1}; log (4 ints, may be NULL) receives
-// (rung, L, accept_len, s bits); the grid covers t_max nodes.
+// (rung, L, accept_len, s bits).
 struct FinAccDevice {
   const DevStep* cur;
   DevStep* next;
   const DevTopo* topos;
   const int32_t* drafts;
-  int32_t tree_rows, n_topo, t_max;
+  int32_t tree_rows, n_topo;
   float tau_on, tau_off;
   int32_t* log;
 };
 int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevice& dv,
                                       const void* partials, int32_t V, float inv_temp,
                                       float* entropy, float* top1p, int32_t* argmax,
-                                      unsigned* counter, int32_t* accept_len, int32_t* path,
-                                      int32_t path_capacity, int32_t* bonus, float* best_top1p,
-                                      StepMirror* mirror, uint32_t seq, hipStream_t stream);
+                                      int32_t* accept_len, int32_t* path, int32_t path_capacity,
+                                      int32_t* bonus, float* best_top1p, StepMirror* mirror,
+                                      uint32_t seq, hipStream_t stream);
 
 // Compaction (as entmtp_kv_compact, one sequence) at the prefix length dev->L.
 int32_t launch_compact_device(const DevStep* dev, const int32_t* path, int32_t path_capacity,
@@ -151,15 +158,22 @@ int32_t launch_compact_device(const DevStep* dev, const int32_t* path, int32_t p
                               entmtp_bf16* v_cache, int32_t n_layers, int64_t layer_stride,
                               int32_t Hkv, int32_t cap, int32_t d, hipStream_t s);
 
+// Compaction (as entmtp_kv_compact, one sequence) of a path the host already
+// holds: path_host[0..accept_len] travels in the launch's arguments, so the
+// kernel reads no device result (0 <= accept_len <= ENTMTP_D_MAX).
+int32_t launch_compact_host(const int32_t* path_host, int32_t accept_len, int32_t prefix_len,
+                            entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t n_layers,
+                            int64_t layer_stride, int32_t Hkv, int32_t cap, int32_t d,
+                            hipStream_t s);
+
 // Finishes the LM head's statistics partials for every node of tree `topo`
-// and, in the same launch, accepts the tree (as launch_accept).  `counter`
-// is one device word, 0 before the launch and 0 after it.
+// and accepts the tree (as launch_accept): one launch for trees of up to 32
+// nodes, a statistics launch and an acceptance launch for larger ones.
 int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,
                                int32_t V, float inv_temp, float* entropy, float* top1p,
-                               int32_t* argmax, unsigned* counter, const int32_t* draft_tokens,
-                               int32_t* accept_len, int32_t* path, int32_t* bonus,
-                               float* best_top1p, StepMirror* mirror, uint32_t seq,
-                               hipStream_t stream);
+                               int32_t* argmax, const int32_t* draft_tokens, int32_t* accept_len,
+                               int32_t* path, int32_t* bonus, float* best_top1p,
+                               StepMirror* mirror, uint32_t seq, hipStream_t stream);
 
 template <typename T>
 inline const T* bank_ptr(const entmtp_bank* b, int64_t off) {

@@ -27,6 +27,9 @@ struct CompactArgs {
   const DevStep* dev;    // when set, sequence 0's prefix length is dev->L
   long long layer_stride;
   int path_cap, n_layers, Hkv, cap, d;
+  int by_value;          // 1: one sequence whose path and accept length are below
+  int a_v;
+  int path_v[ENTMTP_D_MAX + 1];
 };
 
 __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs p) {
@@ -37,7 +40,7 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs
   const int d = p.d, cap = p.cap, L = p.dev ? p.dev->L : p.L[b];
   const int* path = p.path + static_cast<size_t>(b) * p.path_cap;
   const size_t base = static_cast<size_t>(layer) * p.layer_stride + static_cast<size_t>(g) * cap * d;
-  int a = p.accept_len[b];
+  int a = p.by_value ? p.a_v : p.accept_len[b];
   const int a_max = (p.path_cap < ENTMTP_D_MAX + 1 ? p.path_cap : ENTMTP_D_MAX + 1) - 1;
   a = a < 0 ? 0 : (a > a_max ? a_max : a);
   const int chunks = d >> 3;  // 16-byte chunks per row
@@ -53,8 +56,9 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs
     if (it < n_items) {
       const int tsel = it / per_tensor, rem = it % per_tensor;
       const int j = rem / chunks, ch = rem % chunks;
-      const int src_row = L + path[j], dst_row = L + j;
-      if (src_row != dst_row && path[j] >= 0 && src_row < cap && dst_row < cap) {
+      const int pj = p.by_value ? p.path_v[j] : path[j];
+      const int src_row = L + pj, dst_row = L + j;
+      if (src_row != dst_row && pj >= 0 && src_row < cap && dst_row < cap) {
         uint16_t* buf = (tsel ? p.vc[b] : p.kc[b]) + base + ch * 8;
         val[q] = *reinterpret_cast<const u32x4*>(buf + static_cast<size_t>(src_row) * d);
         dst[q] = buf + static_cast<size_t>(dst_row) * d;
@@ -109,9 +113,26 @@ int32_t launch_compact_device(const DevStep* dev, const int32_t* path, int32_t p
   return launch_compact(a, 1, s);
 }
 
-namespace {
+int32_t launch_compact_host(const int32_t* path_host, int32_t accept_len, int32_t prefix_len,
+                            entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t n_layers,
+                            int64_t layer_stride, int32_t Hkv, int32_t cap, int32_t d,
+                            hipStream_t s) {
+  CompactArgs a{};
+  a.kc[0] = k_cache;
+  a.vc[0] = v_cache;
+  a.L[0] = prefix_len;
+  a.by_value = 1;
+  a.a_v = accept_len;
+  for (int j = 0; j <= ENTMTP_D_MAX; ++j) a.path_v[j] = j <= accept_len ? path_host[j] : -1;
+  a.layer_stride = static_cast<long long>(layer_stride);
+  a.path_cap = ENTMTP_D_MAX + 1;
+  a.n_layers = n_layers;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  a.d = d;
+  return launch_compact(a, 1, s);
+}
 
-}  // namespace
 }  // namespace entmtp
 
 using namespace entmtp;

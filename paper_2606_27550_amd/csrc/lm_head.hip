@@ -702,11 +702,21 @@ int device_cus() {
   return cus[dev];
 }
 
-// Combines the G partials of node blockIdx.x into its statistics.
-__global__ __launch_bounds__(kFinThreads) void stats_finalize_kernel(
-    const StatPart* __restrict__ part, int G, float inv_temp, float* __restrict__ entropy,
+// Combines the G partials of each node into its statistics: one wavefront
+// per node, kFinNodes nodes per workgroup.
+constexpr int kFinNodes = 4;
+__global__ __launch_bounds__(64 * kFinNodes) void stats_finalize_kernel(
+    const StatPart* __restrict__ part, int G, int T, float inv_temp, float* __restrict__ entropy,
     float* __restrict__ top1p, int* __restrict__ argmax) {
-  finalize_node(part, G, inv_temp, entropy, top1p, argmax);
+  const int node = blockIdx.x * kFinNodes + (threadIdx.x >> 6);
+  if (node >= T) return;   // whole wavefronts
+  StatPart a, b;
+  merge_rows_wave(part + static_cast<size_t>(node) * G, nullptr, G, inv_temp, a, b);
+  if ((threadIdx.x & 63) == 0) {
+    if (entropy) entropy[node] = part_entropy(a);
+    if (top1p) top1p[node] = part_top1p(a);
+    if (argmax) argmax[node] = a.idx;
+  }
 }
 
 // Workgroups of the streaming LM-head grid: slices of at most 64 rows, and a
@@ -734,40 +744,49 @@ int hyb_grid(int V) {
   return last_G;
 }
 
+// ev0 / ev1 (may be NULL) are recorded on the stream right before and after
+// the launch.
 template <int NT, int S, int NCH, bool STATS = false>
 int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
-                      hipStream_t s, float inv_temp = 1.f, StatPart* part = nullptr) {
+                      hipStream_t s, float inv_temp = 1.f, StatPart* part = nullptr,
+                      hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
   const int G = hyb_grid(V);
   const int passes = (T + NT * 16 - 1) / (NT * 16);
-  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS>), dim3(G, passes), dim3(kHybThreads), 0,
-                     s, X, W, logits, T, hid, V, G, inv_temp, part);
-  return launch_status("verify_logits launch");
+  if (ev0)
+    if (int32_t rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord")) return rc;
+  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS>), dim3(G, passes), dim3(kHybThreads),
+                     0, s, X, W, logits, T, hid, V, G, inv_temp, part);
+  if (int32_t rc = launch_status("verify_logits launch")) return rc;
+  return ev1 ? hip_status(hipEventRecord(ev1, s), "hipEventRecord") : ENTMTP_OK;
 }
 
 // Streaming LM head with fused statistics partials, then the per-node
 // finalize; false when the streaming kernel does not apply to hid.
 template <bool STATS>
 bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
-                         hipStream_t s, float inv_temp, StatPart* part, int32_t* rc) {
+                         hipStream_t s, float inv_temp, StatPart* part, int32_t* rc,
+                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
+  auto go = [&](auto nch) {
+    constexpr int NCH = decltype(nch)::value;
+    if (T <= 16)
+      *rc = launch_lm_hyb<1, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+    else if (T <= 32)
+      *rc = launch_lm_hyb<2, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+    else if (T <= 64)
+      *rc = launch_lm_hyb<4, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+    else
+      *rc = launch_lm_hyb<8, 2, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+  };
   if (hid == 4096) {              // the 7B hidden size: K loop fully unrolled
-    if (T <= 16) *rc = launch_lm_hyb<1, 4, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else if (T <= 32) *rc = launch_lm_hyb<2, 4, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else if (T <= 64) *rc = launch_lm_hyb<4, 4, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else *rc = launch_lm_hyb<8, 2, 32, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    go(std::integral_constant<int, 32>{});
     return true;
   }
   if (hid == 5120) {              // the 13B hidden size
-    if (T <= 16) *rc = launch_lm_hyb<1, 4, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else if (T <= 32) *rc = launch_lm_hyb<2, 4, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else if (T <= 64) *rc = launch_lm_hyb<4, 4, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else *rc = launch_lm_hyb<8, 2, 40, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    go(std::integral_constant<int, 40>{});
     return true;
   }
   if (hid % (4 * kL3Bk) == 0) {   // a whole number of 4-stage rounds
-    if (T <= 16) *rc = launch_lm_hyb<1, 4, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else if (T <= 32) *rc = launch_lm_hyb<2, 4, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else if (T <= 64) *rc = launch_lm_hyb<4, 4, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
-    else *rc = launch_lm_hyb<8, 2, 0, STATS>(X, W, logits, T, hid, V, s, inv_temp, part);
+    go(std::integral_constant<int, 0>{});
     return true;
   }
   return false;
@@ -806,15 +825,21 @@ int32_t launch_lm(const uint16_t* X, const uint16_t* W, float* logits, int T, in
 int stats_slices(int V) { return hyb_grid(V); }
 
 int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, int T, int hid,
-                             int V, float inv_temp, float* logits, void* partials, hipStream_t s) {
-  if (T > 32 || hid % (4 * kL3Bk))
-    return entmtp_verify_logits_partials(hidden, w_lm, T, hid, V, inv_temp, logits, partials,
-                                         static_cast<size_t>(T) * hyb_grid(V) * sizeof(StatPart), s);
-  const int G = hyb_grid(V);
-  const dim3 grid((G + 1) / 2);
+                             int V, float inv_temp, float* logits, void* partials, hipStream_t s,
+                             hipEvent_t ev0, hipEvent_t ev1) {
   auto* part = static_cast<StatPart*>(partials);
   const auto* X = reinterpret_cast<const uint16_t*>(hidden);
   const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
+  if (T > 32) {   // the step's configuration was checked: hid is a multiple of 4 rounds
+    int32_t rc = ENTMTP_OK;
+    if (!launch_hyb_dispatch<true>(X, W, logits, T, hid, V, s, inv_temp, part, &rc, ev0, ev1))
+      return fail(ENTMTP_EINVAL, "hid = %d: no streaming LM head", hid);
+    return rc;
+  }
+  const int G = hyb_grid(V);
+  const dim3 grid((G + 1) / 2);
+  if (ev0)
+    if (int32_t rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord")) return rc;
   auto go = [&](auto k) {
     hipLaunchKernelGGL(k, grid, dim3(kHybThreads), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
   };
@@ -825,12 +850,13 @@ int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
   } else {
     if (T <= 16) go(lm_head_hyb_loop_kernel<1, 4, 0, true>); else go(lm_head_hyb_loop_kernel<2, 4, 0, true>);
   }
-  return launch_status("verify_logits (step) launch");
+  if (int32_t rc = launch_status("verify_logits (step) launch")) return rc;
+  return ev1 ? hip_status(hipEventRecord(ev1, s), "hipEventRecord") : ENTMTP_OK;
 }
 
 int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
                                  const int* T_dev, int T_max, int hid, int V, float inv_temp,
-                                 void* partials, hipStream_t s) {
+                                 void* partials, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   if (T_max < 1 || T_max > 128 || hid % (4 * kL3Bk))
     return fail(ENTMTP_EINVAL, "device-sized LM head: T_max %d (at most 128), hid %d (multiple of %d)",
                 T_max, hid, 4 * kL3Bk);
@@ -839,17 +865,29 @@ int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w
   const auto* X = reinterpret_cast<const uint16_t*>(hidden);
   const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
   auto both = [&](auto small, auto large) -> int32_t {
+    if (ev0)
+      if (int32_t rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord")) return rc;
     hipLaunchKernelGGL(small, dim3((G + 1) / 2), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev,
                        hid, V, G, inv_temp, part);
     if (int32_t rc = launch_status("verify_logits (device-sized, small) launch")) return rc;
-    if (T_max <= 32) return ENTMTP_OK;   // no bank tree needs the large kernel
-    hipLaunchKernelGGL(large, dim3(G), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev, hid, V, G,
-                       inv_temp, part);
-    return launch_status("verify_logits (device-sized, large) launch");
+    if (T_max > 32) {   // some bank tree needs the large kernel
+      hipLaunchKernelGGL(large, dim3(G), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev, hid, V, G,
+                         inv_temp, part);
+      if (int32_t rc = launch_status("verify_logits (device-sized, large) launch")) return rc;
+    }
+    return ev1 ? hip_status(hipEventRecord(ev1, s), "hipEventRecord") : ENTMTP_OK;
   };
   if (hid == 32 * kL3Bk) return both(lm_head_dyn_small_kernel<32>, lm_head_dyn_large_kernel<32>);
   if (hid == 40 * kL3Bk) return both(lm_head_dyn_small_kernel<40>, lm_head_dyn_large_kernel<40>);
   return both(lm_head_dyn_small_kernel<0>, lm_head_dyn_large_kernel<0>);
+}
+
+int32_t launch_stats_finalize(const void* partials, int T, int V, float inv_temp, float* entropy,
+                              float* top1p, int* argmax, hipStream_t s) {
+  hipLaunchKernelGGL(stats_finalize_kernel, dim3((T + kFinNodes - 1) / kFinNodes),
+                     dim3(64 * kFinNodes), 0, s, static_cast<const StatPart*>(partials),
+                     hyb_grid(V), T, inv_temp, entropy, top1p, argmax);
+  return launch_status("stats_finalize launch");
 }
 
 }  // namespace entmtp
@@ -919,10 +957,8 @@ extern "C" int32_t entmtp_stats_finalize(const void* partials, int32_t T, int32_
   ENTMTP_CHECK_ARG(inv_temp > 0.f && inv_temp < INFINITY, ENTMTP_EINVAL,
                    "inv_temp = %g must be positive and finite", static_cast<double>(inv_temp));
   if (!entropy && !top1p && !argmax) return ENTMTP_OK;
-  hipLaunchKernelGGL(stats_finalize_kernel, dim3(T), dim3(kFinThreads), 0,
-                     static_cast<hipStream_t>(stream), static_cast<const StatPart*>(partials),
-                     hyb_grid(V), inv_temp, entropy, top1p, argmax);
-  return launch_status("stats_finalize launch");
+  return launch_stats_finalize(partials, T, V, inv_temp, entropy, top1p, argmax,
+                               static_cast<hipStream_t>(stream));
 }
 
 extern "C" size_t entmtp_verify_logits_stats_workspace(int32_t T, int32_t hid, int32_t V) {

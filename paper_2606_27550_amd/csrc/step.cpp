@@ -4,13 +4,21 @@
 // matching path, updates the cache, and reads one scalar back to the host to
 // pick the next tree ("Cost": a single device-to-host read per step).  The
 // context below validates the fixed sizes once; each step is then a short
-// burst of launches.  Within a step the attention layers and the LM head are
-// independent (the head reads the tree's final hidden states), and only the
-// compaction needs both, so the attention chain runs on a side stream forked
-// from and joined back into the caller's stream, and the two HBM streams
-// overlap.  The acceptance kernel publishes its result into coherent pinned
-// host memory, and the host polls that record instead of synchronising a
-// stream, so the compaction and the host's choice of the next tree overlap.
+// burst of launches.
+//
+// Host-scheduled steps run as two chains.  The caller's stream carries what
+// the next tree choice waits for: the LM head and the statistics merge with
+// acceptance, which publishes its result (accept length, bonus token, s and
+// the accepted path) into coherent pinned host memory that the host polls
+// instead of synchronising a stream.  A side stream carries the cache work:
+// the attention layers of the step, preceded by the compaction of the step
+// before it.  The head reads the tree's final hidden states, not the cache,
+// so nothing on the caller's stream waits for the side stream; the only
+// order the cache needs -- step t's compaction before step t+1's attention --
+// is the side stream's own, and the compaction takes the accepted path from
+// the host record in its launch arguments.  So the next LM head starts as
+// soon as the host has chosen the tree, while the previous step's compaction
+// and the next attention run beside it.
 #include <chrono>
 #include <cmath>
 #include <cstring>
@@ -29,7 +37,6 @@ struct entmtp_step {
   size_t attn_bytes = 0;       // attention workspace, at the start of cfg.workspace
   size_t part_offset = 0;      // LM-head statistics partials follow it
   size_t part_bytes = 0;
-  size_t counter_offset = 0;   // then one arrival counter (0 between launches)
   size_t dev_offset = 0;       // then the device-scheduled state: DevStep[2], DevTopo[K]
   DevAttnShape dshape;         // attention grids for a tree chosen on the device
   int parity = 0;              // slot of DevStep the next device-scheduled step reads
@@ -41,6 +48,11 @@ struct entmtp_step {
   hipEvent_t join = nullptr;   // side stream -> caller's stream
   uint32_t seq = 0;            // sequence number of the latest launch
   bool pending = false;        // a launched step whose result has not been read
+  int32_t pending_L = 0;       // its prefix length
+  // the compaction of the latest step whose result was read, not yet enqueued
+  bool compact_due = false;
+  int32_t due_L = 0, due_a = 0;
+  int32_t due_path[ENTMTP_D_MAX + 1] = {};
 };
 
 namespace {
@@ -59,12 +71,11 @@ void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
 
 // Workspace split for a validated configuration; returns the total bytes.
 size_t layout(const entmtp_step_config& c, int32_t T_max, int32_t n_topo, size_t* attn,
-              size_t* part_off, size_t* part, size_t* counter_off, size_t* dev_off) {
+              size_t* part_off, size_t* part, size_t* dev_off) {
   *attn = entmtp_tree_attn_workspace(T_max, c.Hq, c.Hkv, c.d, c.cap);
   *part_off = round256(*attn);
   *part = entmtp_stats_partials_bytes(T_max, c.hid, c.V);
-  *counter_off = round256(*part_off + *part);
-  *dev_off = *counter_off + 256;
+  *dev_off = round256(*part_off + *part);
   return *dev_off + round256(2 * sizeof(DevStep) + static_cast<size_t>(n_topo) * sizeof(DevTopo));
 }
 
@@ -122,9 +133,9 @@ extern "C" size_t entmtp_step_workspace(const entmtp_bank* bank, const entmtp_st
     clear_error();
     return 0;
   }
-  size_t attn = 0, off = 0, part = 0, coff = 0, doff = 0;
+  size_t attn = 0, off = 0, part = 0, doff = 0;
   const size_t total = layout(*cfg, T_max, static_cast<int32_t>(bank->desc.size()), &attn, &off,
-                              &part, &coff, &doff);
+                              &part, &doff);
   return attn && part ? total : 0;
 }
 
@@ -135,9 +146,9 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   *out = nullptr;
   int32_t T_max = 0, D_max = 0;
   if (int32_t rc = check_config(bank, cfg, &T_max, &D_max)) return rc;
-  size_t attn = 0, off = 0, part = 0, coff = 0, doff = 0;
+  size_t attn = 0, off = 0, part = 0, doff = 0;
   const size_t total = layout(*cfg, T_max, static_cast<int32_t>(bank->desc.size()), &attn, &off,
-                              &part, &coff, &doff);
+                              &part, &doff);
   ENTMTP_CHECK_ARG(attn > 0 && part > 0, ENTMTP_EINVAL, "unsupported attention or LM-head sizes");
   ENTMTP_CHECK_ARG(cfg->workspace && (reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) == 0,
                    ENTMTP_EINVAL, "workspace must be non-NULL and 256-byte aligned");
@@ -156,7 +167,6 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   st->attn_bytes = attn;
   st->part_offset = off;
   st->part_bytes = part;
-  st->counter_offset = coff;
   st->dev_offset = doff;
   void* h = nullptr;
   int32_t rc = hip_status(hipHostMalloc(&h, sizeof(StepMirror), hipHostMallocMapped | hipHostMallocCoherent),
@@ -174,10 +184,6 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
     rc = hip_status(hipEventCreateWithFlags(&st->fork, hipEventDisableTiming), "hipEventCreate");
   if (rc == ENTMTP_OK)
     rc = hip_status(hipEventCreateWithFlags(&st->join, hipEventDisableTiming), "hipEventCreate");
-  if (rc == ENTMTP_OK)   // the finalize-accept arrival counter starts at 0 (and stays so between steps)
-    rc = hip_status(hipMemsetAsync(static_cast<uint8_t*>(cfg->workspace) + coff, 0, 256,
-                                   static_cast<hipStream_t>(cfg->stream)),
-                    "hipMemsetAsync (arrival counter)");
   if (rc == ENTMTP_OK) {  // the bank's descriptors for device-scheduled steps
     std::vector<DevTopo> topos(bank->desc.size());
     for (size_t k = 0; k < topos.size(); ++k) {
@@ -218,14 +224,44 @@ extern "C" void entmtp_step_destroy(entmtp_step* st) {
   delete st;
 }
 
+namespace {
+
+// Enqueues the compaction the host holds (if any) on the side stream.
+int32_t enqueue_due_compaction(entmtp_step* st) {
+  if (!st->compact_due) return ENTMTP_OK;
+  const entmtp_step_config& c = st->cfg;
+  st->compact_due = false;
+  return launch_compact_host(st->due_path, st->due_a, st->due_L, c.k_cache, c.v_cache, c.n_layers,
+                             c.cache_layer_stride, c.Hkv, c.cap, c.d, st->side);
+}
+
+int32_t flush_side(entmtp_step* st) {
+  ENTMTP_CHECK_ARG(!st->pending, ENTMTP_EINVAL,
+                   "a launched step's result has not been read (entmtp_step_wait)");
+  if (int32_t rc = enqueue_due_compaction(st)) return rc;
+  if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
+  return hip_status(hipStreamWaitEvent(static_cast<hipStream_t>(st->cfg.stream), st->join, 0),
+                    "hipStreamWaitEvent");
+}
+
+}  // namespace
+
+extern "C" int32_t entmtp_step_flush(entmtp_step* st) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
+  return flush_side(st);
+}
+
 extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t prefix_len,
                                       const entmtp_bf16* q, const entmtp_bf16* k_tree,
                                       const entmtp_bf16* v_tree, entmtp_bf16* out,
-                                      const entmtp_bf16* hidden, const int32_t* draft_tokens,
-                                      void* ev_lm_begin, void* ev_lm_end) {
+                                      const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                                      const int32_t* draft_tokens, void* ev_lm_begin,
+                                      void* ev_lm_end) {
   clear_error();
   ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
-  st->pending = false;
+  ENTMTP_CHECK_ARG(!st->pending, ENTMTP_EINVAL,
+                   "the previous step's result has not been read (entmtp_step_wait)");
   const entmtp_step_config& c = st->cfg;
   if (int32_t rc = check_device_bank(st->bank, topo)) return rc;
   ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && draft_tokens, ENTMTP_EINVAL,
@@ -233,37 +269,33 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
   const int32_t T = st->bank->desc[topo].T;
   ENTMTP_CHECK_ARG(prefix_len >= 0 && static_cast<int64_t>(prefix_len) + T <= c.cap, ENTMTP_ERANGE,
                    "prefix_len %d + T %d outside the cache capacity %d", prefix_len, T, c.cap);
+  ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
   auto s = static_cast<hipStream_t>(c.stream);
   uint8_t* ws = static_cast<uint8_t*>(c.workspace);
   void* part = ws + st->part_offset;
 
-  // the side stream starts after everything already on the caller's stream
-  // (the previous step's compaction in particular)
+  // the side stream's work of this step starts after everything the caller
+  // enqueued before it (the step's inputs)
   if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
 
   // the LM head (the longest kernel) is enqueued first, so that it is running
   // while the host enqueues the attention chain behind it
-  if (ev_lm_begin)
-    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_begin), s),
-                                "hipEventRecord"))
-      return rc;
-  if (int32_t rc = launch_step_partials(hidden, c.w_lm, T, c.hid, c.V, c.inv_temp, c.logits, part, s))
+  if (int32_t rc = launch_step_partials(hidden, w_lm ? w_lm : c.w_lm, T, c.hid, c.V, c.inv_temp,
+                                        c.logits, part, s, static_cast<hipEvent_t>(ev_lm_begin),
+                                        static_cast<hipEvent_t>(ev_lm_end)))
     return rc;
-  if (ev_lm_end)
-    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_end), s),
-                                "hipEventRecord"))
-      return rc;
-  const uint32_t seq = st->seq + 1u;
+  const uint32_t seq = st->seq + 1u == 0u ? 1u : st->seq + 1u;   // 0 is the record's initial tag
   if (int32_t rc = launch_finalize_accept(
-          st->bank, topo, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax,
-          reinterpret_cast<unsigned*>(ws + st->counter_offset), draft_tokens, c.accept_len, c.path,
-          c.bonus, c.best_top1p, st->dev, seq, s))
+          st->bank, topo, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax, draft_tokens,
+          c.accept_len, c.path, c.bonus, c.best_top1p, st->dev, seq, s))
     return rc;
   st->seq = seq;
 
-  // attention layers on the side stream, concurrent with the above
+  // the cache chain on the side stream, concurrent with the above: the
+  // previous step's compaction, then this step's attention layers
   if (int32_t rc = hip_status(hipStreamWaitEvent(st->side, st->fork, 0), "hipStreamWaitEvent"))
     return rc;
+  if (int32_t rc = enqueue_due_compaction(st)) return rc;
   const size_t q_layer = static_cast<size_t>(c.tree_rows) * c.Hq * c.d;
   const size_t kv_layer = static_cast<size_t>(c.tree_rows) * c.Hkv * c.d;
   for (int32_t l = 0; l < c.n_layers; ++l) {
@@ -274,15 +306,8 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
                                       out + l * q_layer, ws, st->attn_bytes, st->side))
       return rc;
   }
-  if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
-
-  // compaction moves rows the attention chain appended
-  if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->join, 0), "hipStreamWaitEvent")) return rc;
-  if (int32_t rc = entmtp_kv_compact(c.path, c.path_capacity, c.accept_len, prefix_len, c.k_cache,
-                                     c.v_cache, c.n_layers, c.cache_layer_stride, c.Hkv, c.cap, c.d,
-                                     c.stream))
-    return rc;
   st->pending = true;
+  st->pending_L = prefix_len;
   return ENTMTP_OK;
 }
 
@@ -295,13 +320,25 @@ extern "C" int32_t entmtp_step_wait(entmtp_step* st, int32_t* accept_len, int32_
   const uint32_t want = st->seq;
   const auto t0 = std::chrono::steady_clock::now();
   auto s = static_cast<hipStream_t>(st->cfg.stream);
+  const uint64_t* words = reinterpret_cast<const uint64_t*>(st->host);
+  // the record is complete once every word it needs carries the sequence number
+  auto complete = [&]() {
+    const uint64_t w0 = __atomic_load_n(&words[0], __ATOMIC_ACQUIRE);
+    if (static_cast<uint32_t>(w0 >> 32) != want) return false;
+    const int a = static_cast<int32_t>(static_cast<uint32_t>(w0));
+    const int n = 3 + (a < 0 || a > ENTMTP_D_MAX ? kMirrorPathWords : a / 4 + 1);
+    for (int k = 1; k < n; ++k)
+      if (static_cast<uint32_t>(__atomic_load_n(&words[k], __ATOMIC_ACQUIRE) >> 32) != want)
+        return false;
+    return true;
+  };
   for (uint32_t spin = 1;; ++spin) {
-    if (__atomic_load_n(&st->host->seq, __ATOMIC_ACQUIRE) == want) break;
+    if (complete()) break;
     if ((spin & 255u) == 0u) {
       // every few hundred polls: a failed stream or an expired limit ends the wait
       const hipError_t e = hipStreamQuery(s);
       if (e == hipSuccess) {
-        if (__atomic_load_n(&st->host->seq, __ATOMIC_ACQUIRE) == want) break;
+        if (complete()) break;
         st->pending = false;
         return fail(ENTMTP_EHIP, "stream idle but step %u published no result", want);
       }
@@ -315,10 +352,23 @@ extern "C" int32_t entmtp_step_wait(entmtp_step* st, int32_t* accept_len, int32_
     }
     __builtin_ia32_pause();
   }
-  if (accept_len) *accept_len = st->host->accept_len;
-  if (bonus) *bonus = st->host->bonus;
-  if (best_top1p) *best_top1p = st->host->best_top1p;
+  const int32_t a = static_cast<int32_t>(static_cast<uint32_t>(words[0]));
   st->pending = false;
+  if (a < 0 || a > st->D_max)
+    return fail(ENTMTP_EHIP, "step %u published accept length %d outside [0, %d]", want, a,
+                st->D_max);
+  if (accept_len) *accept_len = a;
+  if (bonus) *bonus = static_cast<int32_t>(static_cast<uint32_t>(words[1]));
+  if (best_top1p) {
+    const uint32_t bits = static_cast<uint32_t>(words[2]);
+    std::memcpy(best_top1p, &bits, sizeof(float));
+  }
+  // the path for this step's compaction, which the next launch (or a flush) enqueues
+  for (int j = 0; j <= a; ++j)
+    st->due_path[j] = static_cast<int32_t>((words[3 + j / 4] >> (8 * (j % 4))) & 0xffu);
+  st->due_a = a;
+  st->due_L = st->pending_L;
+  st->compact_due = true;
   return ENTMTP_OK;
 }
 
@@ -340,6 +390,8 @@ extern "C" int32_t entmtp_step_device_start(entmtp_step* st, int32_t topo, int32
                    st->bank->desc[topo].T, c.cap);
   ENTMTP_CHECK_ARG(st->T_max <= 128, ENTMTP_ERANGE,
                    "device-scheduled steps support trees of up to 128 nodes (bank has %d)", st->T_max);
+  // host-scheduled steps before this one finish their cache work first
+  if (int32_t rc = flush_side(st)) return rc;
   auto* state = reinterpret_cast<DevStep*>(static_cast<uint8_t*>(c.workspace) + st->dev_offset);
   hipLaunchKernelGGL(device_start_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(c.stream),
                      state, reinterpret_cast<const DevTopo*>(state + 2), topo, prefix_len);
@@ -369,18 +421,12 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   DevStep* next = state + (st->parity ^ 1);
 
   if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
-  if (ev_lm_begin)
-    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_begin), s),
-                                "hipEventRecord"))
-      return rc;
   ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
   if (int32_t rc = launch_partials_device_T(hidden, w_lm ? w_lm : c.w_lm, &cur->T, st->T_max, c.hid,
-                                            c.V, c.inv_temp, part, s))
+                                            c.V, c.inv_temp, part, s,
+                                            static_cast<hipEvent_t>(ev_lm_begin),
+                                            static_cast<hipEvent_t>(ev_lm_end)))
     return rc;
-  if (ev_lm_end)
-    if (int32_t rc = hip_status(hipEventRecord(static_cast<hipEvent_t>(ev_lm_end), s),
-                                "hipEventRecord"))
-      return rc;
   FinAccDevice dv;
   dv.cur = cur;
   dv.next = next;
@@ -388,13 +434,11 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   dv.drafts = drafts;
   dv.tree_rows = c.tree_rows;
   dv.n_topo = static_cast<int32_t>(st->bank->desc.size());
-  dv.t_max = st->T_max;
   dv.tau_on = c.tau_on;
   dv.tau_off = c.tau_off;
   dv.log = log;
   if (int32_t rc = launch_finalize_accept_device(
-          st->bank, dv, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax,
-          reinterpret_cast<unsigned*>(ws + st->counter_offset), c.accept_len, c.path,
+          st->bank, dv, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax, c.accept_len, c.path,
           c.path_capacity, c.bonus, c.best_top1p, nullptr, 0u, s))
     return rc;
 

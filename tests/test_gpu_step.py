@@ -57,7 +57,12 @@ def stack(layers, name):
 
 
 def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_rung=0,
-             keep_logits=True):
+             keep_logits=True, flush_each=True):
+    """Closed loop through the step driver, each step checked (1) on the
+    oracle from the cache state before it and (2) bit for bit against the same
+    step through the individual entry points (whose cache is compacted every
+    step).  flush_each=False leaves every compaction to the next launch and
+    compares the driver's cache once, after the final flush."""
     d, theta = 128, 10000.0
     scale = 1 / math.sqrt(d)
     trees = bank_trees()
@@ -97,11 +102,13 @@ def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_
         q, kt, vt = (dev_bf16(stack(layers, n)) for n in ("q", "k_tree", "v_tree"))
         X, tok_d = dev_bf16(x), dev_i32(tok)
         out = torch.full((n_layers, Tmax, Hq, d), float("nan"), dtype=torch.bfloat16, device="cuda")
-        kc_before, vc_before = host_bits(kc), host_bits(vc)
+        kc_before, vc_before = host_bits(kc2), host_bits(vc2)
         say(f"step {t}: layers {n_layers} topo {rung} T {T} L {L}")
 
         st.launch(rung, L, q, kt, vt, out, X, tok_d)
         a, bonus, s = st.wait(timeout_s=60.0)
+        if flush_each:
+            st.flush()
         torch.cuda.synchronize()
 
         # (2) the same step through the individual entry points, bit for bit
@@ -113,7 +120,9 @@ def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_
         api.kv_compact(path2, a2, L, kc2, vc2)
         torch.cuda.synchronize()
         pairs = [(out[:, :T], out2[:, :T]), (st.entropy[:T], H2[:T]), (st.top1p[:T], p12[:T]),
-                 (st.argmax[:T], am2[:T]), (st.path, path2), (kc, kc2), (vc, vc2)]
+                 (st.argmax[:T], am2[:T]), (st.path, path2)]
+        if flush_each:
+            pairs += [(kc, kc2), (vc, vc2)]
         if keep_logits:
             pairs.append((st.logits[:T], lg2[:T]))
         for mine, theirs in pairs:
@@ -137,7 +146,7 @@ def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_
         assert (a, bonus) == (ref["accept_len"], ref["bonus"])
         assert st.path.cpu().numpy()[: a + 1].tolist() == list(ref["path"])
         assert abs(s - ref["s"]) <= RTOL_STATS * ref["s"] + 1e-6
-        kc_now, vc_now = host_bits(kc), host_bits(vc)
+        kc_now, vc_now = host_bits(kc2), host_bits(vc2)
         n = L + a + 1
         for l in range(n_layers):
             if l == 0:
@@ -155,6 +164,11 @@ def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_
         nxt = api.ladder_next(rung, len(trees), s, 0.8, 0.6)
         switches += nxt != rung
         rung = nxt
+    if not flush_each:
+        st.flush()
+        torch.cuda.synchronize()
+        assert torch.equal(kc.view(torch.int16), kc2.view(torch.int16))
+        assert torch.equal(vc.view(torch.int16), vc2.view(torch.int16))
     st.close()
     return topo_trace, switches
 
@@ -163,6 +177,12 @@ def test_step_closed_loop_one_layer(api):
     trace, switches = run_loop(api, n_layers=1, n_steps=14)
     say("topology trace", trace)
     assert switches >= 2 and len(set(trace)) >= 3   # the loop really moved along the ladder
+
+
+def test_step_closed_loop_compaction_left_to_next_launch(api):
+    # the pipelined form: no flush between steps, one at the end
+    trace, switches = run_loop(api, n_layers=2, n_steps=10, flush_each=False)
+    assert switches >= 1
 
 
 def test_step_closed_loop_three_layers(api):
@@ -199,7 +219,14 @@ def test_step_errors(api):
         st.launch(len(bank), 0, q, kv, kv, q.clone(), X, tok)
     assert e.value.code == api.EINVAL
     st.launch(3, cap - 64, q, kv, kv, q.clone(), X, tok)   # the largest valid prefix
+    with pytest.raises(api.EntmtpError) as e:       # its result not read yet
+        st.launch(3, 0, q, kv, kv, q.clone(), X, tok)
+    assert e.value.code == api.EINVAL
+    with pytest.raises(api.EntmtpError) as e:
+        st.flush()
+    assert e.value.code == api.EINVAL
     a, bonus, s = st.wait(timeout_s=60.0)
+    st.flush()
     torch.cuda.synchronize()
     # all-zero logits: uniform distribution, argmax 0; zero drafts match it
     assert bonus == 0 and abs(s - 1.0 / V) <= 1e-6 and a == bank.D[3]
@@ -254,6 +281,7 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
         trace.append((rung, L, a, s))
         L += a + 1
         rung = api.ladder_next(rung, K, s, 0.8, 0.6)
+    st_h.flush()
     torch.cuda.synchronize()
 
     # device-scheduled: every step enqueued without reading anything back
@@ -309,6 +337,7 @@ def test_step_32_layer_workload_sampled(api):
     st.launch(0, L, dev_bf16(stack(layers, "q")), dev_bf16(stack(layers, "k_tree")),
               dev_bf16(stack(layers, "v_tree")), out, dev_bf16(x), dev_i32(tok))
     a, bonus, s = st.wait(timeout_s=120.0)
+    st.flush()
     torch.cuda.synchronize()
     ra, rpath, rbonus, rbest = orc.accept(trees[0], tok, am)
     assert (a, bonus) == (ra, rbonus)
