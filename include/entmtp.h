@@ -510,11 +510,11 @@ int32_t entmtp_step_wait(entmtp_step* step, int32_t* accept_len, int32_t* bonus,
                          float* best_top1p, double timeout_s);
 
 /*
- * Enqueues the compaction of the last step whose result was read (if not yet
- * enqueued) and joins the side stream into the configured stream: work
- * enqueued on the configured stream afterwards sees every step's cache
- * update and attention output.  Errors: EINVAL (a launched step's result has
- * not been read), EHIP.
+ * Enqueues the compaction of the last step (for host-scheduled steps: the
+ * last one whose result was read) if not yet enqueued, and joins the side
+ * stream into the configured stream: work enqueued on the configured stream
+ * afterwards sees every step's cache update and attention output.  Errors:
+ * EINVAL (a launched host-scheduled step's result has not been read), EHIP.
  */
 int32_t entmtp_step_flush(entmtp_step* step);
 
@@ -533,10 +533,15 @@ int32_t entmtp_step_flush(entmtp_step* step);
  * Errors: EINVAL, ERANGE, EHIP.
  *
  * entmtp_step_launch_device: enqueues one step for the tree the device state
- * holds (the same kernels as entmtp_step_launch, sized for the largest tree;
- * the attention runs on the side stream, which the configured stream joins
- * before the step's compaction, so every output is complete once the
- * configured stream is).
+ * holds (the same kernels as entmtp_step_launch, sized for the largest
+ * tree), in the same two chains: the LM head and acceptance on the
+ * configured stream, and on the side stream (ordered after everything the
+ * caller enqueued before the call) the previous step's compaction and this
+ * step's attention.  Acceptance of step t waits only for the side stream's
+ * work of step t-2, so the host can enqueue steps ahead of the GPU.  As with
+ * entmtp_step_launch, the last step's compaction goes out with
+ * entmtp_step_flush, after which every output is complete on the configured
+ * stream; accept_len and path of the configuration hold the latest step's.
  * Inputs as for entmtp_step_launch, except
  *   w_lm    the LM-head weight for this step ([V][hid] bf16, NULL: the
  *           configured one)

@@ -15,111 +15,17 @@
 // (The workgroup is one wavefront per SIMD, so it finds room on a CU beside
 // the attention kernel.)  Larger trees merge their statistics in a kernel of
 // their own, one wavefront per node, before the acceptance kernel.
+#include "accept.hpp"
 #include "common.hpp"
 #include "stats.hpp"
 
 namespace entmtp {
 namespace {
 
-constexpr int kAcceptThreads = ENTMTP_T_MAX;
 constexpr int kFinAccThreads = 256;    // statistics + acceptance of one step, one workgroup
 constexpr int kFusedMaxT = 32;         // larger trees: a separate statistics kernel
 
-// A thread's node of the tree (thread i holds node i): what the acceptance
-// needs that does not depend on the target's statistics, so a kernel can
-// fetch it before those are ready.
-struct NodeIn {
-  int tok, parent, depth;
-  uint32_t mask[ENTMTP_MASK_WORDS];
-};
 
-__device__ __forceinline__ NodeIn accept_load(const int* __restrict__ parent,
-                                              const int* __restrict__ depth,
-                                              const uint32_t* __restrict__ mask,
-                                              const int* __restrict__ tok, int T) {
-  NodeIn n{};
-  const int i = threadIdx.x;
-  if (i < T) {
-    n.tok = tok[i];
-    n.parent = parent[i];
-    n.depth = depth[i];
-#pragma unroll
-    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w) n.mask[w] = mask[i * ENTMTP_MASK_WORDS + w];
-  }
-  return n;
-}
-
-// The acceptance of one tree by one workgroup of kAcceptThreads threads;
-// returns (in every thread) depth(best) * 1024 + (1023 - best).
-// Greedy local test: node i's draft token is the target's argmax at its parent.
-__device__ __forceinline__ bool greedy_ok(const NodeIn& n, const int* amax, int T) {
-  const int i = threadIdx.x;
-  return i < T && (i == 0 || n.tok == amax[n.parent]);
-}
-
-// `ok`: this thread's node is locally acceptable (the root always is).  NTH:
-// the workgroup size (at least ENTMTP_T_MAX).
-template <int NTH = kAcceptThreads>
-__device__ __forceinline__ int accept_finish(
-    const NodeIn& n, bool ok, const int* __restrict__ path_tab, int T, int D,
-    const int* amax, const float* top1p,
-    int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
-    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
-    uint32_t seq) {
-  static_assert(NTH >= ENTMTP_T_MAX && NTH % 64 == 0, "one thread per possible node");
-  __shared__ uint32_t matched[ENTMTP_MASK_WORDS];
-  __shared__ int s_key[NTH / 64];
-  const int i = threadIdx.x;
-  if (i < ENTMTP_MASK_WORDS) matched[i] = 0u;
-  __syncthreads();
-  if (i < T && ok) atomicOr(&matched[i >> 5], 1u << (i & 31));
-  __syncthreads();
-  // key orders accepted nodes by depth, then by lower index
-  int key = -1;
-  if (i < T) {
-    bool acc = true;
-#pragma unroll
-    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w) acc = acc && ((n.mask[w] & ~matched[w]) == 0u);
-    if (acc) key = n.depth * 1024 + (1023 - i);
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) key = max(key, __shfl_xor(key, off, 64));
-  if ((i & 63) == 0) s_key[i >> 6] = key;
-  __syncthreads();
-  key = s_key[0];
-#pragma unroll
-  for (int w = 1; w < NTH / 64; ++w) key = max(key, s_key[w]);
-  const int best = 1023 - (key & 1023);
-  const int a = key >> 10;
-  if (i < path_cap) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
-  if (i == 0) {
-    *accept_len = a;
-    *bonus = amax[best];
-    if (best_p) *best_p = top1p ? top1p[best] : 0.f;
-  }
-  if (mirror && i < kMirrorWords) {   // one tagged word per lane
-    uint32_t field;
-    if (i == 0) {
-      field = static_cast<uint32_t>(a);
-    } else if (i == 1) {
-      field = static_cast<uint32_t>(amax[best]);
-    } else if (i == 2) {
-      field = __float_as_uint(top1p ? top1p[best] : 0.f);
-    } else {
-      field = 0u;
-#pragma unroll
-      for (int b = 0; b < 4; ++b) {
-        const int j = (i - 3) * 4 + b;
-        const uint32_t node = j <= a ? static_cast<uint32_t>(path_tab[best * (D + 1) + j]) : 0xffu;
-        field |= (node & 0xffu) << (8 * b);
-      }
-    }
-    __hip_atomic_store(reinterpret_cast<uint64_t*>(mirror) + i,
-                       (static_cast<uint64_t>(seq) << 32) | field, __ATOMIC_RELAXED,
-                       __HIP_MEMORY_SCOPE_SYSTEM);
-  }
-  return key;
-}
 
 __device__ __forceinline__ void accept_core(
     const int* __restrict__ parent, const int* __restrict__ depth,
@@ -197,7 +103,8 @@ __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
 // The same for a tree the device chose: the tree, its drafts and the prefix
 // length come from *dv.cur; the workgroup also runs the ladder and writes the
 // next step's state (tree, node count, prefix length).
-__global__ __launch_bounds__(kFinAccThreads) void finalize_accept_device_kernel(
+constexpr int kFinAccDevThreads = 1024;   // any bank tree (up to 128 nodes) in at most 4 passes
+__global__ __launch_bounds__(kFinAccDevThreads) void finalize_accept_device_kernel(
     FinAccDevice dv, const uint8_t* __restrict__ arena, const StatPart* __restrict__ part, int G,
     float inv_temp, float* __restrict__ entropy, float* __restrict__ top1p,
     int* __restrict__ amax, int* __restrict__ accept_len, int* __restrict__ path_out,
@@ -215,11 +122,16 @@ __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_device_kernel(
   const int D = t->D;
   const int* tok = dv.drafts + static_cast<size_t>(st.rung) * dv.tree_rows;
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
-  finalize_nodes<kFinAccThreads>(part, G, T, inv_temp, entropy, top1p, amax, s_p1, s_am);
+  finalize_nodes<kFinAccDevThreads>(part, G, T, inv_temp, entropy, top1p, amax, s_p1, s_am);
   __syncthreads();
-  const int key = accept_finish<kFinAccThreads>(n, greedy_ok(n, s_am, T), path_tab, T, D, s_am,
-                                                s_p1, accept_len, path_out, path_cap, bonus,
-                                                best_p, mirror, seq);
+  const int key = accept_finish<kFinAccDevThreads>(n, greedy_ok(n, s_am, T), path_tab, T, D, s_am,
+                                                   s_p1, accept_len, path_out, path_cap, bonus,
+                                                   best_p, mirror, seq);
+  {
+    const int i = threadIdx.x, a = key >> 10, best = 1023 - (key & 1023);
+    if (dv.user_path && i < path_cap) dv.user_path[i] = i <= a ? path_tab[best * (D + 1) + i] : -1;
+    if (dv.user_accept_len && i == 0) *dv.user_accept_len = a;
+  }
   if (threadIdx.x == 0) {
     const int a = key >> 10, best = 1023 - (key & 1023);
     const float s = s_p1[best];
@@ -338,7 +250,7 @@ int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevic
                                       int32_t* accept_len, int32_t* path, int32_t path_capacity,
                                       int32_t* bonus, float* best_top1p, StepMirror* mirror,
                                       uint32_t seq, hipStream_t stream) {
-  hipLaunchKernelGGL(finalize_accept_device_kernel, dim3(1), dim3(kFinAccThreads), 0, stream, dv,
+  hipLaunchKernelGGL(finalize_accept_device_kernel, dim3(1), dim3(kFinAccDevThreads), 0, stream, dv,
                      bank->arena, static_cast<const StatPart*>(partials), stats_slices(V),
                      inv_temp, entropy, top1p, argmax, accept_len, path, path_capacity, bonus,
                      best_top1p, mirror, seq);

@@ -135,7 +135,8 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
 // bank tree k are row k of drafts [n_topo][tree_rows]; after accepting, the
 // ladder picks the next tree from s = top1p[best] and writes *next =
 // {rung', T', L + accept_len + 1}; log (4 ints, may be NULL) receives
-// (rung, L, accept_len, s bits).
+// (rung, L, accept_len, s bits); user_accept_len / user_path (may be NULL)
+// receive copies of the accept length and path.
 struct FinAccDevice {
   const DevStep* cur;
   DevStep* next;
@@ -144,6 +145,8 @@ struct FinAccDevice {
   int32_t tree_rows, n_topo;
   float tau_on, tau_off;
   int32_t* log;
+  int32_t* user_accept_len;
+  int32_t* user_path;
 };
 int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevice& dv,
                                       const void* partials, int32_t V, float inv_temp,

@@ -19,6 +19,7 @@
 // the host record in its launch arguments.  So the next LM head starts as
 // soon as the host has chosen the tree, while the previous step's compaction
 // and the next attention run beside it.
+#include <algorithm>
 #include <chrono>
 #include <cmath>
 #include <cstring>
@@ -37,10 +38,16 @@ struct entmtp_step {
   size_t attn_bytes = 0;       // attention workspace, at the start of cfg.workspace
   size_t part_offset = 0;      // LM-head statistics partials follow it
   size_t part_bytes = 0;
-  size_t dev_offset = 0;       // then the device-scheduled state: DevStep[2], DevTopo[K]
+  size_t dev_offset = 0;       // then the device-scheduled state: DevStep[kRing], DevTopo[K],
+  size_t ring_offset = 0;      // and the acceptance ring: kRing x (accept_len, path[path_capacity])
   DevAttnShape dshape;         // attention grids for a tree chosen on the device
-  int parity = 0;              // slot of DevStep the next device-scheduled step reads
+  // device-scheduled steps: step t reads state slot t % kRing and writes slot
+  // (t + 1) % kRing; its accept length and path go to ring slot t % kRing
+  static constexpr int kRing = 4;
   bool dev_started = false;
+  uint64_t dev_t = 0;          // steps launched since entmtp_step_device_start
+  uint64_t dev_compact = 0;    // steps whose compaction has been enqueued
+  hipEvent_t ev_side[kRing] = {};   // side-stream work of device-scheduled step t done
   StepMirror* host = nullptr;  // pinned, coherent
   StepMirror* dev = nullptr;   // device address of `host`
   hipStream_t side = nullptr;  // attention chain (default priority, non-blocking)
@@ -71,12 +78,15 @@ void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
 
 // Workspace split for a validated configuration; returns the total bytes.
 size_t layout(const entmtp_step_config& c, int32_t T_max, int32_t n_topo, size_t* attn,
-              size_t* part_off, size_t* part, size_t* dev_off) {
+              size_t* part_off, size_t* part, size_t* dev_off, size_t* ring_off) {
   *attn = entmtp_tree_attn_workspace(T_max, c.Hq, c.Hkv, c.d, c.cap);
   *part_off = round256(*attn);
   *part = entmtp_stats_partials_bytes(T_max, c.hid, c.V);
   *dev_off = round256(*part_off + *part);
-  return *dev_off + round256(2 * sizeof(DevStep) + static_cast<size_t>(n_topo) * sizeof(DevTopo));
+  *ring_off = *dev_off + round256(entmtp_step::kRing * sizeof(DevStep) +
+                                  static_cast<size_t>(n_topo) * sizeof(DevTopo));
+  return *ring_off + round256(static_cast<size_t>(entmtp_step::kRing) *
+                              (1 + std::max(c.path_capacity, 1)) * sizeof(int32_t));
 }
 
 bool finite_positive(float x) { return x > 0.f && std::isfinite(x); }
@@ -133,9 +143,9 @@ extern "C" size_t entmtp_step_workspace(const entmtp_bank* bank, const entmtp_st
     clear_error();
     return 0;
   }
-  size_t attn = 0, off = 0, part = 0, doff = 0;
+  size_t attn = 0, off = 0, part = 0, doff = 0, roff = 0;
   const size_t total = layout(*cfg, T_max, static_cast<int32_t>(bank->desc.size()), &attn, &off,
-                              &part, &doff);
+                              &part, &doff, &roff);
   return attn && part ? total : 0;
 }
 
@@ -146,9 +156,9 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   *out = nullptr;
   int32_t T_max = 0, D_max = 0;
   if (int32_t rc = check_config(bank, cfg, &T_max, &D_max)) return rc;
-  size_t attn = 0, off = 0, part = 0, doff = 0;
+  size_t attn = 0, off = 0, part = 0, doff = 0, roff = 0;
   const size_t total = layout(*cfg, T_max, static_cast<int32_t>(bank->desc.size()), &attn, &off,
-                              &part, &doff);
+                              &part, &doff, &roff);
   ENTMTP_CHECK_ARG(attn > 0 && part > 0, ENTMTP_EINVAL, "unsupported attention or LM-head sizes");
   ENTMTP_CHECK_ARG(cfg->workspace && (reinterpret_cast<uintptr_t>(cfg->workspace) & 255u) == 0,
                    ENTMTP_EINVAL, "workspace must be non-NULL and 256-byte aligned");
@@ -168,6 +178,7 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
   st->part_offset = off;
   st->part_bytes = part;
   st->dev_offset = doff;
+  st->ring_offset = roff;
   void* h = nullptr;
   int32_t rc = hip_status(hipHostMalloc(&h, sizeof(StepMirror), hipHostMallocMapped | hipHostMallocCoherent),
                           "hipHostMalloc (step result record)");
@@ -184,6 +195,9 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
     rc = hip_status(hipEventCreateWithFlags(&st->fork, hipEventDisableTiming), "hipEventCreate");
   if (rc == ENTMTP_OK)
     rc = hip_status(hipEventCreateWithFlags(&st->join, hipEventDisableTiming), "hipEventCreate");
+  for (int k = 0; k < entmtp_step::kRing && rc == ENTMTP_OK; ++k)
+    rc = hip_status(hipEventCreateWithFlags(&st->ev_side[k], hipEventDisableTiming),
+                    "hipEventCreate");
   if (rc == ENTMTP_OK) {  // the bank's descriptors for device-scheduled steps
     std::vector<DevTopo> topos(bank->desc.size());
     for (size_t k = 0; k < topos.size(); ++k) {
@@ -197,7 +211,7 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
       topos[k].off_path = static_cast<int>(d.off_path);
     }
     attn_device_splits(bank, cfg->Hq, cfg->Hkv, topos.data());
-    auto* dst = static_cast<uint8_t*>(cfg->workspace) + doff + 2 * sizeof(DevStep);
+    auto* dst = static_cast<uint8_t*>(cfg->workspace) + doff + entmtp_step::kRing * sizeof(DevStep);
     rc = hip_status(hipMemcpyAsync(dst, topos.data(), topos.size() * sizeof(DevTopo),
                                    hipMemcpyHostToDevice, static_cast<hipStream_t>(cfg->stream)),
                     "hipMemcpyAsync (bank descriptors)");
@@ -217,6 +231,8 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
 extern "C" void entmtp_step_destroy(entmtp_step* st) {
   if (!st) return;
   if (st->side) (void)hipStreamSynchronize(st->side);
+  for (int k = 0; k < entmtp_step::kRing; ++k)
+    if (st->ev_side[k]) (void)hipEventDestroy(st->ev_side[k]);
   if (st->join) (void)hipEventDestroy(st->join);
   if (st->fork) (void)hipEventDestroy(st->fork);
   if (st->side) (void)hipStreamDestroy(st->side);
@@ -235,10 +251,37 @@ int32_t enqueue_due_compaction(entmtp_step* st) {
                              c.cache_layer_stride, c.Hkv, c.cap, c.d, st->side);
 }
 
+DevStep* dev_state(entmtp_step* st) {
+  return reinterpret_cast<DevStep*>(static_cast<uint8_t*>(st->cfg.workspace) + st->dev_offset);
+}
+
+int32_t* dev_ring(entmtp_step* st, uint64_t t) {
+  return reinterpret_cast<int32_t*>(static_cast<uint8_t*>(st->cfg.workspace) + st->ring_offset) +
+         (t % entmtp_step::kRing) * (1 + static_cast<size_t>(st->cfg.path_capacity));
+}
+
+// Device-scheduled step t's compaction, on the side stream (already ordered
+// after its acceptance).
+int32_t enqueue_device_compaction(entmtp_step* st, uint64_t t) {
+  const entmtp_step_config& c = st->cfg;
+  int32_t* ring = dev_ring(st, t);
+  st->dev_compact = t + 1;
+  return launch_compact_device(dev_state(st) + t % entmtp_step::kRing, ring + 1, c.path_capacity,
+                               ring, c.k_cache, c.v_cache, c.n_layers, c.cache_layer_stride, c.Hkv,
+                               c.cap, c.d, st->side);
+}
+
 int32_t flush_side(entmtp_step* st) {
   ENTMTP_CHECK_ARG(!st->pending, ENTMTP_EINVAL,
                    "a launched step's result has not been read (entmtp_step_wait)");
   if (int32_t rc = enqueue_due_compaction(st)) return rc;
+  if (st->dev_started && st->dev_compact < st->dev_t) {   // the last device-scheduled step's
+    auto s = static_cast<hipStream_t>(st->cfg.stream);
+    if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
+    if (int32_t rc = hip_status(hipStreamWaitEvent(st->side, st->fork, 0), "hipStreamWaitEvent"))
+      return rc;
+    if (int32_t rc = enqueue_device_compaction(st, st->dev_t - 1)) return rc;
+  }
   if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
   return hip_status(hipStreamWaitEvent(static_cast<hipStream_t>(st->cfg.stream), st->join, 0),
                     "hipStreamWaitEvent");
@@ -264,6 +307,10 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
                    "the previous step's result has not been read (entmtp_step_wait)");
   const entmtp_step_config& c = st->cfg;
   if (int32_t rc = check_device_bank(st->bank, topo)) return rc;
+  if (st->dev_started) {   // device-scheduled steps before this one finish their cache work
+    if (int32_t rc = flush_side(st)) return rc;
+    st->dev_started = false;
+  }
   ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && draft_tokens, ENTMTP_EINVAL,
                    "per-step inputs and outputs must be non-NULL");
   const int32_t T = st->bank->desc[topo].T;
@@ -390,14 +437,16 @@ extern "C" int32_t entmtp_step_device_start(entmtp_step* st, int32_t topo, int32
                    st->bank->desc[topo].T, c.cap);
   ENTMTP_CHECK_ARG(st->T_max <= 128, ENTMTP_ERANGE,
                    "device-scheduled steps support trees of up to 128 nodes (bank has %d)", st->T_max);
-  // host-scheduled steps before this one finish their cache work first
+  // steps before this one finish their cache work first
   if (int32_t rc = flush_side(st)) return rc;
-  auto* state = reinterpret_cast<DevStep*>(static_cast<uint8_t*>(c.workspace) + st->dev_offset);
+  DevStep* state = dev_state(st);
   hipLaunchKernelGGL(device_start_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(c.stream),
-                     state, reinterpret_cast<const DevTopo*>(state + 2), topo, prefix_len);
+                     state, reinterpret_cast<const DevTopo*>(state + entmtp_step::kRing), topo,
+                     prefix_len);
   if (int32_t rc = launch_status("device_start launch")) return rc;
-  st->parity = 0;
   st->dev_started = true;
+  st->dev_t = 0;
+  st->dev_compact = 0;
   return ENTMTP_OK;
 }
 
@@ -411,22 +460,37 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   ENTMTP_CHECK_ARG(st->dev_started, ENTMTP_EINVAL, "entmtp_step_device_start was not called");
   ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && drafts, ENTMTP_EINVAL,
                    "per-step inputs and outputs must be non-NULL");
+  ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
   const entmtp_step_config& c = st->cfg;
   auto s = static_cast<hipStream_t>(c.stream);
   uint8_t* ws = static_cast<uint8_t*>(c.workspace);
   void* part = ws + st->part_offset;
-  auto* state = reinterpret_cast<DevStep*>(ws + st->dev_offset);
-  const auto* topos = reinterpret_cast<const DevTopo*>(state + 2);
-  DevStep* cur = state + st->parity;
-  DevStep* next = state + (st->parity ^ 1);
+  constexpr int R = entmtp_step::kRing;
+  const uint64_t t = st->dev_t;
+  DevStep* state = dev_state(st);
+  const auto* topos = reinterpret_cast<const DevTopo*>(state + R);
+  DevStep* cur = state + t % R;
+  DevStep* next = state + (t + 1) % R;
+  int32_t* ring = dev_ring(st, t);
 
+  // the cache chain starts after everything the caller enqueued so far: the
+  // previous step's acceptance (this step's tree and prefix length) and this
+  // step's inputs
   if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
-  ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
+
+  // the caller's stream: LM head, then statistics + acceptance + ladder
   if (int32_t rc = launch_partials_device_T(hidden, w_lm ? w_lm : c.w_lm, &cur->T, st->T_max, c.hid,
                                             c.V, c.inv_temp, part, s,
                                             static_cast<hipEvent_t>(ev_lm_begin),
                                             static_cast<hipEvent_t>(ev_lm_end)))
     return rc;
+  // step t writes state slot t+1 and ring slot t: the side stream must be
+  // done with step t-2 (whose compaction read slot t-2 and ring slot t-2, and
+  // whose predecessor's compaction read slot t-3 = t+1 mod R)
+  if (t >= 2)
+    if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->ev_side[(t - 2) % R], 0),
+                                "hipStreamWaitEvent"))
+      return rc;
   FinAccDevice dv;
   dv.cur = cur;
   dv.next = next;
@@ -437,13 +501,19 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   dv.tau_on = c.tau_on;
   dv.tau_off = c.tau_off;
   dv.log = log;
-  if (int32_t rc = launch_finalize_accept_device(
-          st->bank, dv, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax, c.accept_len, c.path,
-          c.path_capacity, c.bonus, c.best_top1p, nullptr, 0u, s))
+  dv.user_accept_len = c.accept_len;
+  dv.user_path = c.path;
+  if (int32_t rc = launch_finalize_accept_device(st->bank, dv, part, c.V, c.inv_temp, c.entropy,
+                                                 c.top1p, c.argmax, ring, ring + 1,
+                                                 c.path_capacity, c.bonus, c.best_top1p, nullptr,
+                                                 0u, s))
     return rc;
 
+  // the side stream: the previous step's compaction, then this step's attention
   if (int32_t rc = hip_status(hipStreamWaitEvent(st->side, st->fork, 0), "hipStreamWaitEvent"))
     return rc;
+  if (t >= 1 && st->dev_compact < t)
+    if (int32_t rc = enqueue_device_compaction(st, t - 1)) return rc;
   const size_t q_layer = static_cast<size_t>(c.tree_rows) * c.Hq * c.d;
   const size_t kv_layer = static_cast<size_t>(c.tree_rows) * c.Hkv * c.d;
   for (int32_t l = 0; l < c.n_layers; ++l) {
@@ -454,12 +524,8 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
                                         c.scale, c.rope_theta, out + l * q_layer, ws, st->side))
       return rc;
   }
-  if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
-  if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->join, 0), "hipStreamWaitEvent")) return rc;
-  if (int32_t rc = launch_compact_device(cur, c.path, c.path_capacity, c.accept_len, c.k_cache,
-                                         c.v_cache, c.n_layers, c.cache_layer_stride, c.Hkv, c.cap,
-                                         c.d, s))
+  if (int32_t rc = hip_status(hipEventRecord(st->ev_side[t % R], st->side), "hipEventRecord"))
     return rc;
-  st->parity ^= 1;
+  st->dev_t = t + 1;
   return ENTMTP_OK;
 }

@@ -181,7 +181,7 @@ def test_step_closed_loop_one_layer(api):
 
 def test_step_closed_loop_compaction_left_to_next_launch(api):
     # the pipelined form: no flush between steps, one at the end
-    trace, switches = run_loop(api, n_layers=2, n_steps=10, flush_each=False)
+    trace, switches = run_loop(api, n_layers=2, n_steps=10, flush_each=False, keep_logits=False)
     assert switches >= 1
 
 
@@ -257,7 +257,7 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
     stride = Hkv * cap * d
     kw = dict(n_layers=n_layers, Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax, scale=scale,
               rope_theta=theta, cache_layer_stride=stride)
-    st_h = api.Step(bank, kc_h, vc_h, W, **kw)
+    st_h = api.Step(bank, kc_h, vc_h, W, keep_logits=False, **kw)
     st_d = api.Step(bank, kc_d, vc_d, W, keep_logits=False, tau_on=0.8, tau_off=0.6, **kw)
     deltas, spikes = synth.regime_spikes(WL, n_steps, Tmax, V, hid)
     steps = []
@@ -289,6 +289,7 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
     st_d.device_start(rung0, L0)
     for t, e in enumerate(steps):
         st_d.launch_device(e["q"], e["kt"], e["vt"], out_d[t], e["x"], e["drafts"], log[t])
+    st_d.flush()
     torch.cuda.synchronize()
     say("host trace", [(r_, a_) for r_, _, a_, _ in trace])
     log_h = log.cpu().numpy()
@@ -303,6 +304,11 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
         assert torch.equal(out_h[t, :, :T].view(torch.int16), out_d[t, :, :T].view(torch.int16)), t
     assert torch.equal(kc_h.view(torch.int16), kc_d.view(torch.int16))
     assert torch.equal(vc_h.view(torch.int16), vc_d.view(torch.int16))
+    # the configuration's outputs hold the last step's result in both modes
+    assert int(st_d.accept_len.item()) == trace[-1][2] == int(st_h.accept_len.item())
+    a_last = trace[-1][2]
+    assert torch.equal(st_d.path[: a_last + 1], st_h.path[: a_last + 1])
+    assert (st_d.path[a_last + 1:] == -1).all()
     st_h.close()
     st_d.close()
 
