@@ -28,6 +28,7 @@ from __future__ import annotations
 
 import argparse
 import ctypes
+import gc
 import json
 import math
 import os
@@ -56,6 +57,8 @@ def parse():
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--fixed-topo", type=int, default=-1,
                     help="disable the scheduler and use this bank entry every step")
+    ap.add_argument("--graph", action="store_true",
+                    help="with --gpu-scheduler: replay segments of steps captured as HIP graphs")
     ap.add_argument("--gpu-scheduler", action="store_true",
                     help="run the ladder on the GPU (no result read per step) instead of on "
                          "the host; the same decisions")
@@ -196,7 +199,7 @@ def main():
     W_p = [P_(w.data_ptr()) for w in W]
     total = args.warmup + args.steps
     steplog = torch.full((total, 4), -1, dtype=torch.int32, device=dev)
-    log_p = [P_(steplog[t].data_ptr()) for t in range(total)]
+    log_base = P_(steplog.data_ptr())
     Ts = bank.T
     a_c, b_c, s_c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
     a_r, b_r, s_r = ctypes.byref(a_c), ctypes.byref(b_c), ctypes.byref(s_c)
@@ -211,7 +214,8 @@ def main():
         # nothing is read back: the next step's tree and prefix stay on the GPU
         e = pool_p[t % P]
         chk(lib.entmtp_step_launch_device(handles[0], e["q"], e["kt"], e["vt"], out_p, e["x"],
-                                          W_p[t % len(W_p)], e["drafts"], log_p[t], ev[0], ev[1]))
+                                          W_p[t % len(W_p)], e["drafts"], log_base, total, ev[0],
+                                          ev[1]))
 
     def step(t, ev=(None, None)):
         L = state["L"] if grows else L0
@@ -247,13 +251,44 @@ def main():
         b_.record()
     ev_p = [(P_(a_.cuda_event), P_(b_.cuda_event)) for a_, b_ in events]
     trace = []
+    graphs, graph_steps = [], 0
+    if on_gpu and args.graph:
+        # segments of SEG steps (a whole number of input-pool and weight-copy
+        # cycles, and of the device state ring), all captured before the timed
+        # region; the steps past the last whole segment run eagerly (and carry
+        # the LM-head events, which graph replays do not)
+        SEG = math.lcm(P, len(W_p), 4)
+        for g0 in range(0, K - K % SEG, SEG):
+            ts = range(args.warmup + g0, args.warmup + g0 + SEG)
+            arr = lambda vals: (ctypes.c_void_p * SEG)(*[v.value for v in vals])   # noqa: E731
+            h = ctypes.c_void_p()
+            chk(lib.entmtp_step_device_graph(
+                handles[0], SEG, arr([pool_p[t % P]["q"] for t in ts]),
+                arr([pool_p[t % P]["kt"] for t in ts]), arr([pool_p[t % P]["vt"] for t in ts]),
+                arr([out_p] * SEG), arr([pool_p[t % P]["x"] for t in ts]),
+                arr([W_p[t % len(W_p)] for t in ts]), arr([pool_p[t % P]["drafts"] for t in ts]),
+                log_base, total, ctypes.byref(h)))
+            graphs.append(h)
+        graph_steps = len(graphs) * SEG
+        sampled = [t for t in sampled if t >= graph_steps]
+        log(f"captured {len(graphs)} graphs of {SEG} steps")
     torch.cuda.synchronize()
+    # no garbage collection inside the timed region: a full collection of the
+    # interpreter's heap stalls the host loop for tens of milliseconds
+    gc.collect()
+    gc.disable()
     t_start = time.perf_counter()
-    for t in range(K):
+    for g in graphs:
+        chk(lib.entmtp_step_graph_launch(handles[0], g))
+    for t in range(graph_steps, K):
         trace.append(run(args.warmup + t, ev_p[t // NE] if t % NE == 0 else (None, None)))
+    events = [events[t // NE] for t in sampled]
     chk(lib.entmtp_step_flush(handles[0]))   # the last timed step's compaction
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
+    gc.enable()
+    for g in graphs:
+        lib.entmtp_step_graph_destroy(g)
     if on_gpu:   # the steps' (tree, prefix, accept length, s) as the GPU logged them
         lg = steplog.cpu().numpy()[args.warmup:]
         trace = [(bank.T[int(r)], int(L), int(a), float(np.int32(sb).view(np.float32)), int(r))

@@ -547,8 +547,9 @@ int32_t entmtp_step_flush(entmtp_step* step);
  *           configured one)
  *   drafts  [K][tree_rows] int32 (device): the draft tokens for every bank
  *           tree (row k for tree k; the step reads the chosen tree's row)
- *   log     device int32[4] or NULL: receives (tree, prefix length,
- *           accept_len, s as float bits) of this step
+ *   log     device int32[log_rows][4] or NULL: row (step index since
+ *           entmtp_step_device_start) % log_rows receives (tree, prefix
+ *           length, accept_len, s as float bits) of the step
  * The caller sizes cap for the whole run (prefix growth included); a step
  * whose prefix length plus tree would exceed cap computes no attention.
  * Errors: EINVAL (no entmtp_step_device_start yet), EHIP.
@@ -558,7 +559,30 @@ int32_t entmtp_step_launch_device(entmtp_step* step, const entmtp_bf16* q,
                                   const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
                                   entmtp_bf16* out, const entmtp_bf16* hidden,
                                   const entmtp_bf16* w_lm, const int32_t* drafts, int32_t* log,
-                                  void* ev_lm_begin, void* ev_lm_end);
+                                  int32_t log_rows, void* ev_lm_begin, void* ev_lm_end);
+
+/*
+ * A segment of device-scheduled steps as one HIP graph: since such steps read
+ * nothing back, n_steps of them (a multiple of 4, the depth of the device
+ * state ring) are captured from the configured stream (which must not be the
+ * null stream) with their per-step inputs -- host arrays of n_steps device
+ * pointers, w_lm may be NULL (the configured weight) -- and a final flush, so
+ * that the segment depends on nothing outside it.  Each
+ * entmtp_step_graph_launch then runs the segment's steps on the configured
+ * stream, continuing from whatever tree and prefix length the device state
+ * holds (the log rows follow the device's step count); replays of one graph
+ * may follow each other and eager steps.  *graph receives an opaque handle;
+ * release it with entmtp_step_graph_destroy.  Requires
+ * entmtp_step_device_start first.  Errors: EINVAL, ERANGE, EHIP.
+ */
+int32_t entmtp_step_device_graph(entmtp_step* step, int32_t n_steps, const entmtp_bf16* const* q,
+                                 const entmtp_bf16* const* k_tree,
+                                 const entmtp_bf16* const* v_tree, entmtp_bf16* const* out,
+                                 const entmtp_bf16* const* hidden, const entmtp_bf16* const* w_lm,
+                                 const int32_t* const* drafts, int32_t* log, int32_t log_rows,
+                                 void** graph);
+int32_t entmtp_step_graph_launch(entmtp_step* step, void* graph);
+void entmtp_step_graph_destroy(void* graph);
 
 #ifdef __cplusplus
 }

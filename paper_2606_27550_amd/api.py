@@ -81,7 +81,10 @@ _SIGNATURES = {
     "entmtp_step_wait": (_c_i32, [_c_p, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
                                   ctypes.POINTER(_c_f32), ctypes.c_double]),
     "entmtp_step_device_start": (_c_i32, [_c_p, _c_i32, _c_i32]),
-    "entmtp_step_launch_device": (_c_i32, [_c_p] * 11),
+    "entmtp_step_launch_device": (_c_i32, [_c_p] * 9 + [_c_i32, _c_p, _c_p]),
+    "entmtp_step_device_graph": (_c_i32, [_c_p, _c_i32] + [_c_p] * 8 + [_c_i32, _c_p]),
+    "entmtp_step_graph_launch": (_c_i32, [_c_p, _c_p]),
+    "entmtp_step_graph_destroy": (None, [_c_p]),
 }
 
 
@@ -599,15 +602,53 @@ class Step:
 
     def launch_device(self, q, k_tree, v_tree, out, hidden, drafts, log=None, w_lm=None,
                       ev_lm_begin=None, ev_lm_end=None) -> None:
-        """One device-scheduled step; drafts [K, tree_rows] int32, log int32[4] or None."""
+        """One device-scheduled step; drafts [K, tree_rows] int32; log int32 [rows, 4]
+        (row = device step count % rows) or None."""
         ev = [None if e is None else _c_p(e.cuda_event) for e in (ev_lm_begin, ev_lm_end)]
+        rows = 0 if log is None else log.numel() // 4
         _check(lib.entmtp_step_launch_device(self._h, _p(q), _p(k_tree), _p(v_tree), _p(out),
-                                             _p(hidden), _p(w_lm), _p(drafts), _p(log), ev[0],
-                                             ev[1]))
+                                             _p(hidden), _p(w_lm), _p(drafts), _p(log), rows,
+                                             ev[0], ev[1]))
+
+    def device_graph(self, steps, log=None):
+        """Capture device-scheduled steps as one replayable graph: ``steps`` is a
+        list (length a multiple of 4) of dicts with q, k_tree, v_tree, out,
+        hidden, drafts and optionally w_lm.  Returns a StepGraph."""
+        n = len(steps)
+        arr = lambda key: _host_ptrs([e.get(key) for e in steps])   # noqa: E731
+        h = _c_p()
+        rows = 0 if log is None else log.numel() // 4
+        w = arr("w_lm") if any(e.get("w_lm") is not None for e in steps) else None
+        _check(lib.entmtp_step_device_graph(self._h, n, arr("q"), arr("k_tree"), arr("v_tree"),
+                                            arr("out"), arr("hidden"), w, arr("drafts"), _p(log),
+                                            rows, ctypes.byref(h)))
+        return StepGraph(self, h, steps, log)
 
     def close(self):
         if getattr(self, "_h", None):
             lib.entmtp_step_destroy(self._h)
+            self._h = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+
+class StepGraph:
+    """A captured segment of device-scheduled steps (entmtp_step_device_graph);
+    keeps the tensors it was captured with alive."""
+
+    def __init__(self, step: Step, handle, keep, log):
+        self._step, self._h, self._keep = step, handle, (keep, log)
+
+    def launch(self) -> None:
+        _check(lib.entmtp_step_graph_launch(self._step.handle, self._h))
+
+    def close(self):
+        if getattr(self, "_h", None):
+            lib.entmtp_step_graph_destroy(self._h)
             self._h = None
 
     def __del__(self):

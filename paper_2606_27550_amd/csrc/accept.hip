@@ -140,13 +140,14 @@ __global__ __launch_bounds__(kFinAccDevThreads) void finalize_accept_device_kern
     nx.rung = next;
     nx.T = dv.topos[next].T;
     nx.L = st.L + a + 1;
-    nx.pad = 0;
+    nx.step = st.step + 1;
     *dv.next = nx;
     if (dv.log) {
-      dv.log[0] = st.rung;
-      dv.log[1] = st.L;
-      dv.log[2] = a;
-      dv.log[3] = __float_as_int(s);
+      int32_t* row = dv.log + 4 * static_cast<size_t>(st.step % dv.log_rows);
+      row[0] = st.rung;
+      row[1] = st.L;
+      row[2] = a;
+      row[3] = __float_as_int(s);
     }
   }
 }

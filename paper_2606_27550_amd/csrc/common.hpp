@@ -63,7 +63,7 @@ struct DevStep {
   int rung;   // bank index of the step's tree
   int T;      // its node count
   int L;      // prefix length
-  int pad;
+  int step;   // steps since the device state was started
 };
 
 // A bank tree as the device-scheduled kernels find it: sizes and byte
@@ -135,8 +135,9 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
 // bank tree k are row k of drafts [n_topo][tree_rows]; after accepting, the
 // ladder picks the next tree from s = top1p[best] and writes *next =
 // {rung', T', L + accept_len + 1}; log (4 ints, may be NULL) receives
-// (rung, L, accept_len, s bits); user_accept_len / user_path (may be NULL)
-// receive copies of the accept length and path.
+// (rung, L, accept_len, s bits) in row cur->step % log_rows of a
+// [log_rows][4] array; user_accept_len / user_path (may be NULL) receive
+// copies of the accept length and path.
 struct FinAccDevice {
   const DevStep* cur;
   DevStep* next;
@@ -145,6 +146,7 @@ struct FinAccDevice {
   int32_t tree_rows, n_topo;
   float tau_on, tau_off;
   int32_t* log;
+  int32_t log_rows;
   int32_t* user_accept_len;
   int32_t* user_path;
 };

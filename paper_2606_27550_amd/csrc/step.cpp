@@ -47,6 +47,7 @@ struct entmtp_step {
   bool dev_started = false;
   uint64_t dev_t = 0;          // steps launched since entmtp_step_device_start
   uint64_t dev_compact = 0;    // steps whose compaction has been enqueued
+  uint64_t dev_sync_t = 0;     // steps whose side-stream work the caller's stream has joined
   hipEvent_t ev_side[kRing] = {};   // side-stream work of device-scheduled step t done
   StepMirror* host = nullptr;  // pinned, coherent
   StepMirror* dev = nullptr;   // device address of `host`
@@ -282,6 +283,7 @@ int32_t flush_side(entmtp_step* st) {
       return rc;
     if (int32_t rc = enqueue_device_compaction(st, st->dev_t - 1)) return rc;
   }
+  st->dev_sync_t = st->dev_t;
   if (int32_t rc = hip_status(hipEventRecord(st->join, st->side), "hipEventRecord (join)")) return rc;
   return hip_status(hipStreamWaitEvent(static_cast<hipStream_t>(st->cfg.stream), st->join, 0),
                     "hipStreamWaitEvent");
@@ -447,6 +449,7 @@ extern "C" int32_t entmtp_step_device_start(entmtp_step* st, int32_t topo, int32
   st->dev_started = true;
   st->dev_t = 0;
   st->dev_compact = 0;
+  st->dev_sync_t = 0;
   return ENTMTP_OK;
 }
 
@@ -454,12 +457,14 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
                                              const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
                                              entmtp_bf16* out, const entmtp_bf16* hidden,
                                              const entmtp_bf16* w_lm, const int32_t* drafts,
-                                             int32_t* log, void* ev_lm_begin, void* ev_lm_end) {
+                                             int32_t* log, int32_t log_rows, void* ev_lm_begin,
+                                             void* ev_lm_end) {
   clear_error();
   ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
   ENTMTP_CHECK_ARG(st->dev_started, ENTMTP_EINVAL, "entmtp_step_device_start was not called");
   ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && drafts, ENTMTP_EINVAL,
                    "per-step inputs and outputs must be non-NULL");
+  ENTMTP_CHECK_ARG(log == nullptr || log_rows >= 1, ENTMTP_EINVAL, "log_rows = %d < 1", log_rows);
   ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
   const entmtp_step_config& c = st->cfg;
   auto s = static_cast<hipStream_t>(c.stream);
@@ -487,7 +492,7 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   // step t writes state slot t+1 and ring slot t: the side stream must be
   // done with step t-2 (whose compaction read slot t-2 and ring slot t-2, and
   // whose predecessor's compaction read slot t-3 = t+1 mod R)
-  if (t >= 2)
+  if (t >= st->dev_sync_t + 2)   // (earlier steps: joined by a flush already)
     if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->ev_side[(t - 2) % R], 0),
                                 "hipStreamWaitEvent"))
       return rc;
@@ -501,6 +506,7 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   dv.tau_on = c.tau_on;
   dv.tau_off = c.tau_off;
   dv.log = log;
+  dv.log_rows = log_rows;
   dv.user_accept_len = c.accept_len;
   dv.user_path = c.path;
   if (int32_t rc = launch_finalize_accept_device(st->bank, dv, part, c.V, c.inv_temp, c.entropy,
@@ -528,4 +534,60 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
     return rc;
   st->dev_t = t + 1;
   return ENTMTP_OK;
+}
+
+extern "C" int32_t entmtp_step_device_graph(entmtp_step* st, int32_t n_steps,
+                                            const entmtp_bf16* const* q,
+                                            const entmtp_bf16* const* k_tree,
+                                            const entmtp_bf16* const* v_tree,
+                                            entmtp_bf16* const* out,
+                                            const entmtp_bf16* const* hidden,
+                                            const entmtp_bf16* const* w_lm,
+                                            const int32_t* const* drafts, int32_t* log,
+                                            int32_t log_rows, void** graph) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr && graph != nullptr, ENTMTP_EINVAL, "step or graph is NULL");
+  *graph = nullptr;
+  ENTMTP_CHECK_ARG(st->dev_started, ENTMTP_EINVAL, "entmtp_step_device_start was not called");
+  ENTMTP_CHECK_ARG(n_steps >= entmtp_step::kRing && n_steps % entmtp_step::kRing == 0,
+                   ENTMTP_EINVAL, "n_steps = %d must be a positive multiple of %d", n_steps,
+                   entmtp_step::kRing);
+  ENTMTP_CHECK_ARG(q && k_tree && v_tree && out && hidden && drafts, ENTMTP_EINVAL,
+                   "per-step pointer arrays must be non-NULL host arrays");
+  ENTMTP_CHECK_ARG(st->cfg.stream != nullptr, ENTMTP_EINVAL,
+                   "capturing needs a created stream (not the null stream)");
+  auto s = static_cast<hipStream_t>(st->cfg.stream);
+  // the segment starts from a joined state, so it depends on nothing outside it
+  if (int32_t rc = flush_side(st)) return rc;
+  if (int32_t rc = hip_status(hipStreamBeginCapture(s, hipStreamCaptureModeRelaxed),
+                              "hipStreamBeginCapture"))
+    return rc;
+  int32_t rc = ENTMTP_OK;
+  for (int32_t i = 0; i < n_steps && rc == ENTMTP_OK; ++i)
+    rc = entmtp_step_launch_device(st, q[i], k_tree[i], v_tree[i], out[i], hidden[i],
+                                   w_lm ? w_lm[i] : nullptr, drafts[i], log, log_rows, nullptr,
+                                   nullptr);
+  if (rc == ENTMTP_OK) rc = flush_side(st);   // ... and ends joined
+  hipGraph_t g = nullptr;
+  const hipError_t e = hipStreamEndCapture(s, &g);
+  if (rc == ENTMTP_OK) rc = hip_status(e, "hipStreamEndCapture");
+  hipGraphExec_t exec = nullptr;
+  if (rc == ENTMTP_OK)
+    rc = hip_status(hipGraphInstantiate(&exec, g, nullptr, nullptr, 0), "hipGraphInstantiate");
+  if (g) (void)hipGraphDestroy(g);
+  if (rc != ENTMTP_OK) return rc;
+  *graph = exec;
+  return ENTMTP_OK;
+}
+
+extern "C" int32_t entmtp_step_graph_launch(entmtp_step* st, void* graph) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr && graph != nullptr, ENTMTP_EINVAL, "step or graph is NULL");
+  return hip_status(hipGraphLaunch(static_cast<hipGraphExec_t>(graph),
+                                   static_cast<hipStream_t>(st->cfg.stream)),
+                    "hipGraphLaunch");
+}
+
+extern "C" void entmtp_step_graph_destroy(void* graph) {
+  if (graph) (void)hipGraphExecDestroy(static_cast<hipGraphExec_t>(graph));
 }

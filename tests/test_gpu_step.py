@@ -288,7 +288,7 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
     log = torch.full((n_steps, 4), -1, dtype=torch.int32, device="cuda")
     st_d.device_start(rung0, L0)
     for t, e in enumerate(steps):
-        st_d.launch_device(e["q"], e["kt"], e["vt"], out_d[t], e["x"], e["drafts"], log[t])
+        st_d.launch_device(e["q"], e["kt"], e["vt"], out_d[t], e["x"], e["drafts"], log)
     st_d.flush()
     torch.cuda.synchronize()
     say("host trace", [(r_, a_) for r_, _, a_, _ in trace])
@@ -371,3 +371,80 @@ def test_step_32_layer_workload_sampled(api):
         for j, node in enumerate(rpath):
             np.testing.assert_array_equal(vc_h[l, :, L + j], layers[l].v_tree[node])
     st.close()
+
+
+def test_device_step_graph_replays_match_eager_steps(api):
+    """A segment of 8 device-scheduled steps captured as one graph and replayed
+    three times -- with unrelated eager work and synchronisations between the
+    replays -- against the same 24 steps launched one by one: per-replay logs,
+    attention outputs, statistics and caches bit for bit."""
+    Hq, Hkv, d, hid, V, L0, n_seg, reps = 8, 2, 128, 512, 1000, 40, 8, 3
+    theta, scale = 10000.0, 1 / math.sqrt(128)
+    trees = bank_trees()
+    bank = api.Bank(trees)
+    K, Tmax, Dmax = len(trees), max(bank.T), max(bank.D)
+    n_steps = n_seg * reps
+    cap = L0 + n_steps * (Dmax + 1) + Tmax + 8
+    w_bits = synth.lm_head_weight(WL, V, hid, std=W_STD)
+    w64 = orc.bf16_to_f64(w_bits)
+    W = dev_bf16(w_bits)
+    W2 = W.clone()                       # a second weight copy, as the benchmark alternates
+    base = synth.attn_inputs(WL, 1, Hq, Hkv, d, L0, cap)
+    kc_e, vc_e = dev_bf16(base.k_cache), dev_bf16(base.v_cache)
+    kc_g, vc_g = kc_e.clone(), vc_e.clone()
+    kw = dict(Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax, scale=scale, rope_theta=theta,
+              keep_logits=False, stream=torch.cuda.Stream())
+    st_e = api.Step(bank, kc_e, vc_e, W, **kw)
+    kw["stream"] = torch.cuda.Stream()
+    st_g = api.Step(bank, kc_g, vc_g, W, **kw)
+    deltas, spikes = synth.regime_spikes(WL, n_seg, Tmax, V, hid)
+    seg = []
+    for i in range(n_seg):
+        layers, x, am, u, r = step_inputs(i, 1, Tmax, Hq, Hkv, d, w_bits, w64, float(deltas[i]),
+                                          spikes[i])
+        drafts = np.zeros((K, Tmax), np.int32)
+        for k in range(K):
+            drafts[k, : bank.T[k]] = synth.draft_tokens(trees[k], am, u, r, 0.7)
+        seg.append({"q": dev_bf16(layers[0].q), "k_tree": dev_bf16(layers[0].k_tree),
+                    "v_tree": dev_bf16(layers[0].v_tree), "hidden": dev_bf16(x),
+                    "drafts": dev_i32(drafts), "w_lm": W if i % 2 == 0 else W2,
+                    "out": torch.zeros((Tmax, Hq, d), dtype=torch.bfloat16, device="cuda")})
+    log_e = torch.full((n_steps, 4), -1, dtype=torch.int32, device="cuda")
+    log_g = torch.full((n_steps, 4), -1, dtype=torch.int32, device="cuda")
+
+    # eager: the 24 steps one by one, snapshotting after each segment
+    snaps = []
+    out_e = [torch.zeros_like(e["out"]) for e in seg]
+    st_e.device_start(0, L0)
+    for rep in range(reps):
+        for i, e in enumerate(seg):
+            st_e.launch_device(e["q"], e["k_tree"], e["v_tree"], out_e[i], e["hidden"], e["drafts"],
+                               log_e, w_lm=e["w_lm"])
+        st_e.flush()
+        torch.cuda.synchronize()
+        snaps.append({"k": kc_e.clone(), "v": vc_e.clone(), "out": [o.clone() for o in out_e],
+                      "top1p": st_e.top1p.clone(), "path": st_e.path.clone()})
+
+    # graph: one capture, three replays
+    st_g.device_start(0, L0)
+    graph = st_g.device_graph(seg, log_g)
+    torch.cuda.synchronize()
+    assert (log_g == -1).all()           # capturing ran nothing
+    for rep in range(reps):
+        graph.launch()
+        torch.cuda.synchronize()
+        junk = torch.randn(1 << 16, device="cuda").sum()   # eager work between replays
+        junk.item()
+        say(f"graph replay {rep}: log rows {log_g[rep * n_seg:(rep + 1) * n_seg, 0].tolist()}")
+        sn = snaps[rep]
+        assert torch.equal(log_g[: (rep + 1) * n_seg], log_e[: (rep + 1) * n_seg]), rep
+        assert (log_g[(rep + 1) * n_seg:] == -1).all()
+        assert torch.equal(kc_g.view(torch.int16), sn["k"].view(torch.int16)), rep
+        assert torch.equal(vc_g.view(torch.int16), sn["v"].view(torch.int16)), rep
+        for i, e in enumerate(seg):
+            assert torch.equal(e["out"].view(torch.int16), sn["out"][i].view(torch.int16)), (rep, i)
+        assert torch.equal(st_g.top1p, sn["top1p"]) and torch.equal(st_g.path, sn["path"])
+    assert len(set(log_e[:, 0].tolist())) >= 2          # the ladder moved inside the segments
+    graph.close()
+    st_e.close()
+    st_g.close()
