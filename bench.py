@@ -379,14 +379,16 @@ def lm_head_traffic(Ts):
     for name, v in rec["per_variant"].items():
         if not name.rstrip(">").endswith("true"):   # the timed kernel is the statistics variant
             continue
+        kernel = name.split("<")[0].split()[-1]
         nt = int(name.split("<")[1].split(",")[0])
-        per[nt] = v["fetch_bytes"] + v["write_bytes"]
+        per[(kernel, nt)] = v["fetch_bytes"] + v["write_bytes"]
     tot = 0.0
-    for T in Ts:
-        nt = 1 if T <= 16 else 2 if T <= 32 else 4 if T <= 64 else 8
-        if nt not in per:
+    for T in Ts:   # the step's launch: the loop kernel up to 32 nodes, the grid kernel above
+        key = (("lm_head_hyb_loop_kernel", 1 if T <= 16 else 2) if T <= 32 else
+               ("lm_head_hyb_kernel", 4 if T <= 64 else 8))
+        if key not in per:
             return None
-        tot += per[nt]
+        tot += per[key]
     return round(tot / len(Ts))
 
 
