@@ -29,6 +29,9 @@ What the step computes, in the paper's terms:
   the proposal -> tree decoding -> verification -> KV-cache update loop).
 * ``ladder_next``: the hysteretic threshold policy over a size-sorted bank
   (§4, "Policy").
+* ``frontier_scores`` / ``frontier_select``: Algorithm 1's inner step -- every
+  one-node augmentation of a tree scored from one rollout of the tree joined
+  with its frontier, and the tie-broken choice of the node to add (§3.1).
 
 Floating point is fp64 throughout.  Tensors that the interface stores as bf16
 are passed in as uint16 bit patterns and widened exactly.
@@ -387,6 +390,104 @@ def binary_next(current_is_big: bool, s: float, tau_on: float, tau_off: float) -
     if s <= tau_off:
         return False
     return current_is_big
+
+
+# --------------------------------------------------------------------------
+# Acceptance frontier: scoring one-node augmentations (§3.1, Algorithm 1)
+# --------------------------------------------------------------------------
+#
+# A node of a draft tree is named, as in Medusa/Hydra tree lists, by its tuple
+# of child ranks along the root-to-node path; with a parent array whose
+# children appear in rank order, a node's rank is the number of earlier
+# siblings.  |nu| is the node's depth and sum(nu) its rank sum, Algorithm 1's
+# tie-break keys.
+
+def child_ranks(parent: Sequence[int]) -> list[int]:
+    """Rank of every node among its parent's children (index order); 0 for
+    the root."""
+    validate_parent(parent)
+    seen: dict[int, int] = {}
+    rank = [0] * len(parent)
+    for i in range(1, len(parent)):
+        rank[i] = seen.get(parent[i], 0)
+        seen[parent[i]] = rank[i] + 1
+    return rank
+
+
+def rank_sums(parent: Sequence[int]) -> list[int]:
+    """sum(nu): the child ranks added up along each node's root-to-node path."""
+    rank = child_ranks(parent)
+    return [sum(rank[j] for j in ancestors_or_self(parent, i)) for i in range(len(parent))]
+
+
+def depths(parent: Sequence[int]) -> list[int]:
+    validate_parent(parent)
+    d = [0] * len(parent)
+    for i in range(1, len(parent)):
+        d[i] = d[parent[i]] + 1
+    return d
+
+
+def next_children(parent: Sequence[int], max_depth: int) -> list[int]:
+    """NextChildren(T, D) (Algorithm 1, not spelled out in the paper): every
+    node of T, the root included, whose depth is below D proposes its
+    next-ranked child.  Returns the candidates' parents, in node order."""
+    d = depths(parent)
+    return [p for p in range(len(parent)) if d[p] < max_depth]
+
+
+def joint_tree(parent: Sequence[int], max_depth: int):
+    """T joined with its frontier F: T's nodes keep their indices and the
+    candidates follow in the order of next_children.  Returns (parent array
+    of T u F, in_tree flags)."""
+    cand = next_children(parent, max_depth)
+    joint = list(parent) + cand
+    return joint, [True] * len(parent) + [False] * len(cand)
+
+
+def _accepted(parent: Sequence[int], ok_row) -> list[bool]:
+    """Accepted nodes of one sample: the node and every ancestor below the
+    root locally acceptable (the root always is)."""
+    acc = [True] * len(parent)
+    for i in range(1, len(parent)):
+        acc[i] = acc[parent[i]] and bool(ok_row[i])
+    return acc
+
+
+def frontier_scores(parent: Sequence[int], in_tree: Sequence[bool], local_ok) -> list[int]:
+    """Algorithm 1's scoring step over one rollout of the joint tree T u F:
+    for each sample (one verification of the joint tree), the accept length
+    of T is the deepest accepted node of T, and that of T u {nu} for a
+    candidate nu is the larger of it and depth(nu) when nu itself is
+    accepted -- a candidate's only ancestors are in T, so its acceptance does
+    not depend on the other candidates.  local_ok[s][i]: node i's draft token
+    passes the local test in sample s (greedy: it equals the target's argmax
+    at the parent).  Returns, per node, the accept length summed over the
+    samples: for candidates that of T u {nu}, for members of T that of T."""
+    d = depths(parent)
+    J = len(parent)
+    sums = [0] * J
+    for row in local_ok:
+        acc = _accepted(parent, row)
+        a_T = max(d[i] for i in range(J) if in_tree[i] and acc[i])
+        for i in range(J):
+            sums[i] += a_T if in_tree[i] else max(a_T, d[i] if acc[i] else 0)
+    return sums
+
+
+def frontier_select(parent: Sequence[int], in_tree: Sequence[bool], sums: Sequence[int]) -> int:
+    """nu* = argmax over the candidates of (mean accept length, -sum(nu),
+    -|nu|) (Algorithm 1); the mean over a common sample count orders as the
+    sum.  Equal keys: the lower node index.  -1 when there is no candidate."""
+    rs, d = rank_sums(parent), depths(parent)
+    best, best_key = -1, None
+    for i in range(len(parent)):
+        if in_tree[i]:
+            continue
+        key = (sums[i], -rs[i], -d[i])
+        if best_key is None or key > best_key:
+            best, best_key = i, key
+    return best
 
 
 # --------------------------------------------------------------------------
