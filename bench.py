@@ -51,6 +51,8 @@ def parse():
     ap.add_argument("--pool", type=int, default=32, help="distinct per-step input sets")
     ap.add_argument("--weight-copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--no-extras", action="store_true",
+                    help="skip the timings of the typical-acceptance and frontier kernels")
     ap.add_argument("--event-every", type=int, default=8,
                     help="time the LM head with HIP events on every n-th timed step (each "
                          "event pair costs the host a few microseconds)")
@@ -335,6 +337,7 @@ def main():
                            [topo for *_, topo in trace])
 
     traffic = lm_head_traffic([T for T, *_ in trace])
+    extras = None if args.no_extras else next_rows(api, synth, W[0], pool, hid, V, dev)
 
     line = {
         "metric": METRIC, "value": round(steps_per_s, 2), "unit": "steps/s", "n_gpus": 1,
@@ -359,8 +362,67 @@ def main():
                      "timed_launches": len(sampled),
                      "timing": f"HIP events around the LM-head launch of every {NE}-th timed step"},
         "cpu_baseline": cpu,
+        "next_rows": extras,
     }
     print(json.dumps(line), flush=True)
+
+
+def next_rows(api, synth, W, pool, hid, V, dev, reps=50):
+    """Timings (HIP events, after the timed region) of the kernels beyond the
+    greedy step: typical acceptance on a 26-node tree at these shapes, and the
+    frontier scoring of the offline search at its rollout size (100 prompts x
+    256 tokens of samples over a 64-node tree and its frontier)."""
+    import torch
+    out = {}
+    # typical acceptance (T 0.7, eps 0.09, alpha 0.3): draft logits + the walk
+    tree = synth.uniform_attach_tree(3, 26, 4)
+    bank = api.Bank([tree])
+    T = len(tree)
+    X = pool[0]["x"][:T]
+    lg = torch.empty((T, V), dtype=torch.float32, device=dev)
+    H, p1 = torch.empty(T, device=dev), torch.empty(T, device=dev)
+    am = torch.empty(T, dtype=torch.int32, device=dev)
+    ws = torch.empty(api.verify_logits_stats_workspace(T, hid, V), dtype=torch.uint8, device=dev)
+    api.verify_logits_stats(X, W, lg, 1 / 0.7, H, p1, am, ws)
+    tok = am[torch.tensor([max(p, 0) for p in tree], device=dev)].contiguous()
+    zd, zt = torch.empty(T, device=dev), torch.empty(T, device=dev)
+    a = torch.zeros(1, dtype=torch.int32, device=dev)
+    path = torch.zeros(32, dtype=torch.int32, device=dev)
+    bonus = torch.zeros(1, dtype=torch.int32, device=dev)
+
+    def timed(fn):
+        fn()
+        torch.cuda.synchronize()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) * 1e3 / reps
+
+    out["typical_draft_logits_us"] = round(timed(
+        lambda: api.draft_logits(bank, 0, X, W, tok, am, zd, zt)), 2)
+    out["typical_accept_us"] = round(timed(
+        lambda: api.accept_typical(bank, 0, tok, am, zd, zt, H, p1, 1 / 0.7, 0.09, 0.3, a, path,
+                                   bonus)), 2)
+    out["typical_tree_nodes"] = T
+    # frontier scoring at rollout size
+    parent = synth.uniform_attach_tree(79, 64, 5)
+    joint, in_tree = api.frontier_tree(parent, 6)
+    fb = api.Bank([joint])
+    J, S = len(joint), 100 * 256
+    g = torch.Generator(device="cpu").manual_seed(7)
+    ok = (torch.rand((S, J), generator=g) < 0.7).to(torch.uint8).to(dev)
+    it = torch.tensor(in_tree, dtype=torch.uint8, device=dev)
+    sums = torch.zeros(J, dtype=torch.int32, device=dev)
+    best = torch.zeros(1, dtype=torch.int32, device=dev)
+    us = timed(lambda: api.frontier_score(fb, 0, it, sums, best, local_ok=ok))
+    out["frontier_score_us"] = round(us, 2)
+    out["frontier_samples"] = S
+    out["frontier_joint_nodes"] = J
+    out["frontier_samples_per_s"] = round(S / (us * 1e-6), 1)
+    return out
 
 
 def lm_head_traffic(Ts):

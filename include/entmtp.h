@@ -388,6 +388,40 @@ int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
                            float tau_off);
 
 /* ------------------------------------------------------------------------ */
+/* Acceptance frontier (§3.1, Algorithm 1: the scoring step of the greedy     */
+/* offline tree search)                                                       */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Scores every one-node augmentation T u {nu} of a draft tree T from one
+ * rollout of the joint tree T u F, and picks the node Algorithm 1 adds.
+ *   bank, topo   the joint tree (a bank tree); nodes are ranked among their
+ *                parent's children in index order, and a node's rank sum is
+ *                the sum of the ranks on its root-to-node path (the Medusa
+ *                tuple of the node, added up)
+ *   in_tree      device uint8[T]: nonzero for the nodes of T (the root counts
+ *                as one whatever its flag), 0 for the candidates
+ *   n_samples    S >= 1 verifications of the joint tree (S x depth < 2^31)
+ *   local_ok     device uint8[S][T] or NULL: nonzero when node i's draft token
+ *                passes the local test in sample s (any acceptance rule); when
+ *                NULL, draft_tokens and argmax (device int32[S][T]) decide it
+ *                greedily: draft_tokens[s][i] == argmax[s][parent(i)]
+ *   sums         device int32[T] out: for a candidate, the accept length of
+ *                T u {nu} summed over the samples -- per sample the larger of
+ *                T's accept length (its deepest accepted node) and depth(nu)
+ *                when nu and its ancestors are accepted; for a node of T,
+ *                T's own accept length summed
+ *   best         device int32[1] out: the candidate with the largest sum, then
+ *                the smaller rank sum, then the smaller depth, then the lower
+ *                index; -1 without candidates
+ * Errors: EINVAL, ERANGE, EHIP.
+ */
+int32_t entmtp_frontier_score(const entmtp_bank* bank, int32_t topo, const uint8_t* in_tree,
+                              int32_t n_samples, const uint8_t* local_ok,
+                              const int32_t* draft_tokens, const int32_t* argmax, int32_t* sums,
+                              int32_t* best, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* One verification step, end to end (§4, the decode loop with the tree      */
 /* scheduler and its "Cost" paragraph: verify the chosen tree, accept, update */
 /* the cache, read one scalar back to pick the next tree).                    */

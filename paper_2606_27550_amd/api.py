@@ -69,6 +69,8 @@ _SIGNATURES = {
                                      _c_p]),
     "entmtp_accept_typical": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_f32,
                                        _c_f32, _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_frontier_score": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p,
+                                       _c_p]),
     "entmtp_kv_compact": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64, _c_i32,
                                    _c_i32, _c_i32, _c_p]),
     "entmtp_ladder_next": (_c_i32, [_c_i32, _c_i32, _c_f32, _c_f32, _c_f32]),
@@ -496,6 +498,46 @@ def accept_typical(bank: Bank, topo: int, draft_tokens, argmax, z_draft, z_top, 
     _check(lib.entmtp_accept_typical(bank.handle, topo, _p(draft_tokens), _p(argmax), _p(z_draft),
                                      _p(z_top), _p(entropy), _p(top1p), inv_temp, eps, alpha,
                                      _p(accept_len), _p(path), _p(bonus), _p(best_top1p),
+                                     _stream(stream)))
+
+
+def frontier_tree(parent, max_depth: int):
+    """The joint tree T u F of the offline search's scoring step (host
+    bookkeeping): every node of T whose depth is below max_depth, the root
+    included, proposes its next-ranked child; the candidates follow T's nodes
+    in node order.  Returns (parent list of T u F, in_tree list of 0/1)."""
+    depth = [0] * len(parent)
+    for i in range(1, len(parent)):
+        _need(0 <= parent[i] < i, "parents precede their children")
+        depth[i] = depth[parent[i]] + 1
+    cands = [p for p, dp in enumerate(depth) if dp < max_depth]
+    return list(parent) + cands, [1] * len(parent) + [0] * len(cands)
+
+
+def frontier_score(bank: Bank, topo: int, in_tree, sums, best, local_ok=None, draft_tokens=None,
+                   argmax=None, stream=None) -> None:
+    """Scores of T's one-node augmentations from samples of the joint tree
+    (bank tree ``topo``): local_ok uint8 [S, T], or draft_tokens and argmax
+    int32 [S, T] for the greedy test."""
+    import torch
+    T = bank.T[topo]
+    _dev(in_tree, "in_tree", torch.uint8, min_numel=T)
+    _dev(sums, "sums", torch.int32, min_numel=T)
+    _dev(best, "best", torch.int32, min_numel=1)
+    if local_ok is not None:
+        _dev(local_ok, "local_ok", torch.uint8)
+        _need(local_ok.dim() == 2 and local_ok.shape[1] == T, "local_ok is [S, T]")
+        S = local_ok.shape[0]
+    else:
+        _need(draft_tokens is not None and argmax is not None,
+              "give local_ok, or draft_tokens and argmax")
+        _dev(draft_tokens, "draft_tokens", torch.int32)
+        _dev(argmax, "argmax", torch.int32)
+        _need(draft_tokens.dim() == 2 and draft_tokens.shape[1] == T and
+              argmax.shape == draft_tokens.shape, "draft_tokens and argmax are [S, T]")
+        S = draft_tokens.shape[0]
+    _check(lib.entmtp_frontier_score(bank.handle, topo, _p(in_tree), S, _p(local_ok),
+                                     _p(draft_tokens), _p(argmax), _p(sums), _p(best),
                                      _stream(stream)))
 
 

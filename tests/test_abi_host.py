@@ -157,6 +157,13 @@ def test_kernel_calls_reject_bad_arguments_without_launching():
     rc = lib.entmtp_accept_typical(host_bank.handle, 0, p, p, p, p, p, p, f(1.0), f(0.09), f(0.3),
                                    p, p, p, None, None)
     assert rc == api.EINVAL and "arena" in api.last_error()
+    # frontier scoring: sizes and inputs before the bank
+    u8 = ctypes.c_void_p(16)
+    assert lib.entmtp_frontier_score(host_bank.handle, 0, u8, 0, u8, None, None, p, p, None) == api.EINVAL
+    assert lib.entmtp_frontier_score(host_bank.handle, 0, u8, 4, None, p, None, p, p, None) == api.EINVAL
+    assert lib.entmtp_frontier_score(host_bank.handle, 0, None, 4, u8, None, None, p, p, None) == api.EINVAL
+    rc = lib.entmtp_frontier_score(host_bank.handle, 0, u8, 4, u8, None, None, p, p, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
     # workspace query
     assert api.tree_attn_workspace(27, 32, 32, 64, 256) == 0
     assert api.tree_attn_workspace(27, 30, 8, 128, 256) == 0
@@ -192,3 +199,16 @@ def test_ladder_matches_oracle():
         api.ladder_next(5, 5, 0.5, 0.8, 0.6)
     with pytest.raises(api.EntmtpError):
         api.ladder_next(0, 5, 0.5, 0.6, 0.8)
+
+
+def test_frontier_tree_matches_oracle():
+    """The binding's host bookkeeping of the joint tree T u F against the
+    oracle's NextChildren."""
+    rng = np.random.default_rng(5)
+    for _ in range(200):
+        n = int(rng.integers(1, 30))
+        parent = [-1] + [int(rng.integers(0, i)) for i in range(1, n)]
+        D = int(rng.integers(0, 8))
+        joint, in_tree = api.frontier_tree(parent, D)
+        ref, ref_in = orc.joint_tree(parent, D)
+        assert joint == ref and in_tree == [int(x) for x in ref_in]
