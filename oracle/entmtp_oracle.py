@@ -25,6 +25,8 @@ What the step computes, in the paper's terms:
   acceptance, specialised to greedy decoding), and the accept length (§5.1).
 * ``accept_typical``: the same walk under Hydra's typical acceptance
   condition (posterior threshold and entropy-scaled threshold, §5.1-§5.2).
+* ``accept_stochastic``: speculative-sampling verification (min(1, p/p_hat)
+  acceptance with residual resampling, §2.1) over the tree's children.
 * ``kv_compact``: the KV-cache update that keeps the accepted path (§3.2,
   the proposal -> tree decoding -> verification -> KV-cache update loop).
 * ``ladder_next``: the hysteretic threshold policy over a size-sorted bank
@@ -347,6 +349,73 @@ def accept_typical(parent: Sequence[int], draft_tokens: Sequence[int], z, inv_te
     path = ancestors_or_self(parent, best)
     bonus = int(np.argmax(np.asarray(z[best], dtype=np.float64)))
     return depth[best], path, bonus, best, np.array(p_draft), np.array(thr)
+
+
+def _inverse_cdf(r: np.ndarray, u: float) -> int:
+    """The smallest index b with r[0] + ... + r[b] > u * sum(r): a draw from
+    the (unnormalised) distribution r with the uniform u."""
+    c = np.cumsum(r)
+    hit = np.nonzero(c > u * c[-1])[0]
+    return int(hit[0]) if len(hit) else int(np.nonzero(r > 0)[0][-1])
+
+
+def accept_stochastic(parent: Sequence[int], draft_tokens: Sequence[int], z, q, inv_temp: float,
+                      u_accept: Sequence[float], u_sample: Sequence[float]):
+    """Speculative-sampling verification of a draft tree (§2.1).
+
+    §2.1 gives the rule for one chain: the draft token t at a position is kept
+    with probability min(1, p(t) / p_hat(t)) -- p the target's distribution,
+    p_hat the draft's -- left to right; at the first rejection the suffix is
+    dropped and a replacement is drawn from norm(max(0, p - p_hat)).  On a
+    tree the walk starts at the root with r = p at that node and tries the
+    node's children in index (rank) order, each drafted from the node's draft
+    distribution q[node]: child c passes when u_accept[c] * q(t_c) < r(t_c)
+    (u < min(1, r / q); with q(t_c) = 0, when r(t_c) > 0).  The first child
+    that passes becomes the current node, with r = p at it; each child that
+    fails replaces r by norm(max(0, r - q[node])) before the next sibling is
+    tried (recursive rejection sampling; for a chain it is exactly the rule
+    above).  When no child passes, or the current node is a leaf, the bonus
+    token is drawn from r with u_sample[node] (inverse CDF over the
+    vocabulary in index order).  Should a residual vanish (r = q exactly in
+    arithmetic), the distribution before that subtraction is kept.
+
+    z [T][V] target logits, p = softmax(z * inv_temp); q [T][V] draft
+    distributions.  Returns (a, path, bonus, best, trace) where trace lists
+    every comparison made, as (child, u * q(t), r(t)), and last the draw,
+    as ('sample', u * sum(r), cumulative sums around the drawn index).
+    """
+    validate_parent(parent)
+    T = len(parent)
+    d = depths(parent)
+    children = [[] for _ in range(T)]
+    for i in range(1, T):
+        children[parent[i]].append(i)
+    trace = []
+    cur = 0
+    while True:
+        y = np.asarray(z[cur], dtype=np.float64) * float(inv_temp)
+        e = np.exp(y - y.max())
+        r = e / e.sum()
+        qn = np.asarray(q[cur], dtype=np.float64)
+        nxt = None
+        for c in children[cur]:
+            t = int(draft_tokens[c])
+            lhs, rhs = float(u_accept[c]) * qn[t], r[t]
+            trace.append((c, lhs, rhs))
+            if (qn[t] > 0 and lhs < rhs) or (qn[t] == 0 and rhs > 0):
+                nxt = c
+                break
+            w = np.maximum(r - qn, 0.0)
+            if w.sum() > 0:
+                r = w / w.sum()
+        if nxt is None:
+            bonus = _inverse_cdf(r, float(u_sample[cur]))
+            c_all = np.cumsum(r)
+            lo = c_all[bonus - 1] if bonus > 0 else 0.0
+            trace.append(("sample", float(u_sample[cur]) * c_all[-1], lo, c_all[bonus]))
+            path = ancestors_or_self(parent, cur)
+            return d[cur], path, bonus, cur, trace
+        cur = nxt
 
 
 # --------------------------------------------------------------------------
