@@ -369,9 +369,10 @@ def main():
 
 def next_rows(api, synth, W, pool, hid, V, dev, reps=50):
     """Timings (HIP events, after the timed region) of the kernels beyond the
-    greedy step: typical acceptance on a 26-node tree at these shapes, and the
-    frontier scoring of the offline search at its rollout size (100 prompts x
-    256 tokens of samples over a 64-node tree and its frontier)."""
+    greedy step: typical and speculative-sampling acceptance on a 26-node tree
+    at these shapes, and the frontier scoring of the offline search at its
+    rollout size (100 prompts x 256 tokens of samples over a 64-node tree and
+    its frontier)."""
     import torch
     out = {}
     # typical acceptance (T 0.7, eps 0.09, alpha 0.3): draft logits + the walk
@@ -407,6 +408,16 @@ def next_rows(api, synth, W, pool, hid, V, dev, reps=50):
         lambda: api.accept_typical(bank, 0, tok, am, zd, zt, H, p1, 1 / 0.7, 0.09, 0.3, a, path,
                                    bonus)), 2)
     out["typical_tree_nodes"] = T
+    # speculative sampling on the same tree: logits, a draft distribution per
+    # node (softmax of perturbed logits) and uniforms
+    gq = torch.Generator(device="cpu").manual_seed(5)
+    qd = torch.softmax(lg + torch.randn(lg.shape, generator=gq).to(dev), dim=1).contiguous()
+    ua = torch.rand(T, generator=gq).to(dev)
+    usd = torch.rand(T, generator=gq).to(dev)
+    wsp = torch.empty(V, dtype=torch.float32, device=dev)
+    out["stochastic_accept_us"] = round(timed(
+        lambda: api.accept_stochastic(bank, 0, tok, lg, qd, 1 / 0.7, am, p1, ua, usd, wsp, a,
+                                      path, bonus)), 2)
     # frontier scoring at rollout size
     parent = synth.uniform_attach_tree(79, 64, 5)
     joint, in_tree = api.frontier_tree(parent, 6)

@@ -387,6 +387,42 @@ int32_t entmtp_kv_compact_batched(int32_t B, const int32_t* path, int32_t path_c
 int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
                            float tau_off);
 
+/*
+ * Speculative-sampling verification (§2.1: keep a draft token t with
+ * probability min(1, p(t) / p_hat(t)), else draw a replacement from
+ * norm(max(0, p - p_hat)) and drop the rest).  On a tree: from the root, with
+ * r = p at the current node, the node's children are tried in index (rank)
+ * order, all drafted from the node's draft distribution q[node]; child c
+ * passes when u_accept[c] * q(t_c) < r(t_c) (with q(t_c) = 0: when
+ * r(t_c) > 0) and becomes the current node (r = p at it); a child that fails
+ * replaces r by norm(max(0, r - q[node])) (kept as is if that has no mass)
+ * before the next sibling.  With no child passing, or at a leaf, the bonus
+ * token is drawn from r with u_sample[node]: the smallest index b whose
+ * cumulative mass (vocabulary in index order) exceeds u_sample * total.  A
+ * chain tree gives exactly the §2.1 rule.  A draft token outside [0, V)
+ * never passes (the residual update follows as for any rejection).
+ *   logits   device fp32 [T][V]: the target's logits per node, p =
+ *            softmax(logits * inv_temp)
+ *   argmax, top1p  device [T]: the statistics of those logits at the same
+ *            inv_temp (entmtp_logit_stats / entmtp_verify_logits_stats), so
+ *            that p(v) = exp((z_v - z_argmax) * inv_temp) * top1p needs no
+ *            pass over the vocabulary
+ *   q        device fp32 [T][V]: the draft distribution node i's children
+ *            were drawn from (rows sum to 1)
+ *   u_accept, u_sample  device fp32 [T]: uniforms in [0, 1) (the method's
+ *            random numbers, supplied by the caller)
+ *   workspace  device fp32 [V] scratch (the residual), used by this call only
+ *   accept_len, path [D+1] (entries past accept_len -1), bonus: as for
+ *            entmtp_accept
+ * Errors: EINVAL, EHIP.
+ */
+int32_t entmtp_accept_stochastic(const entmtp_bank* bank, int32_t topo,
+                                 const int32_t* draft_tokens, const float* logits, const float* q,
+                                 int32_t V, float inv_temp, const int32_t* argmax,
+                                 const float* top1p, const float* u_accept,
+                                 const float* u_sample, float* workspace, int32_t* accept_len,
+                                 int32_t* path, int32_t* bonus, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Acceptance frontier (§3.1, Algorithm 1: the scoring step of the greedy     */
 /* offline tree search)                                                       */

@@ -71,6 +71,8 @@ _SIGNATURES = {
                                        _c_f32, _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "entmtp_frontier_score": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p,
                                        _c_p]),
+    "entmtp_accept_stochastic": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_i32, _c_f32, _c_p,
+                                          _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p]),
     "entmtp_kv_compact": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64, _c_i32,
                                    _c_i32, _c_i32, _c_p]),
     "entmtp_ladder_next": (_c_i32, [_c_i32, _c_i32, _c_f32, _c_f32, _c_f32]),
@@ -539,6 +541,33 @@ def frontier_score(bank: Bank, topo: int, in_tree, sums, best, local_ok=None, dr
     _check(lib.entmtp_frontier_score(bank.handle, topo, _p(in_tree), S, _p(local_ok),
                                      _p(draft_tokens), _p(argmax), _p(sums), _p(best),
                                      _stream(stream)))
+
+
+def accept_stochastic(bank: Bank, topo: int, draft_tokens, logits, q, inv_temp: float, argmax,
+                      top1p, u_accept, u_sample, workspace, accept_len, path, bonus,
+                      stream=None) -> None:
+    """Speculative-sampling tree verification; logits and q fp32 [T, V],
+    argmax / top1p the logits' statistics at inv_temp, uniforms fp32 [T],
+    workspace fp32 [V]."""
+    import torch
+    T, D = bank.T[topo], bank.D[topo]
+    _need(logits.dim() == 2 and logits.shape[0] >= T, "logits is [T, V]")
+    V = logits.shape[1]
+    _dev(logits, "logits", torch.float32)
+    _dev(q, "q", torch.float32, tuple(logits.shape))
+    _dev(draft_tokens, "draft_tokens", torch.int32, min_numel=T)
+    _dev(argmax, "argmax", torch.int32, min_numel=T)
+    _dev(top1p, "top1p", torch.float32, min_numel=T)
+    _dev(u_accept, "u_accept", torch.float32, min_numel=T)
+    _dev(u_sample, "u_sample", torch.float32, min_numel=T)
+    _dev(workspace, "workspace", torch.float32, min_numel=V)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=1)
+    _dev(path, "path", torch.int32, min_numel=D + 1)
+    _dev(bonus, "bonus", torch.int32, min_numel=1)
+    _check(lib.entmtp_accept_stochastic(bank.handle, topo, _p(draft_tokens), _p(logits), _p(q), V,
+                                        inv_temp, _p(argmax), _p(top1p), _p(u_accept),
+                                        _p(u_sample), _p(workspace),
+                                        _p(accept_len), _p(path), _p(bonus), _stream(stream)))
 
 
 def kv_compact(path, accept_len, prefix_len: int, k_cache, v_cache, stream=None) -> None:

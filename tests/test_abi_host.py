@@ -164,6 +164,17 @@ def test_kernel_calls_reject_bad_arguments_without_launching():
     assert lib.entmtp_frontier_score(host_bank.handle, 0, None, 4, u8, None, None, p, p, None) == api.EINVAL
     rc = lib.entmtp_frontier_score(host_bank.handle, 0, u8, 4, u8, None, None, p, p, None)
     assert rc == api.EINVAL and "arena" in api.last_error()
+    # stochastic acceptance
+    fs = ctypes.c_float
+    assert lib.entmtp_accept_stochastic(host_bank.handle, 0, p, p, p, 0, fs(1.0), p, p, p, p, p, p,
+                                        p, p, None) == api.EINVAL
+    assert lib.entmtp_accept_stochastic(host_bank.handle, 0, p, p, p, 100, fs(0.0), p, p, p, p, p,
+                                        p, p, p, None) == api.EINVAL
+    assert lib.entmtp_accept_stochastic(host_bank.handle, 0, p, p, p, 100, fs(1.0), None, p, p, p,
+                                        p, p, p, p, None) == api.EINVAL
+    rc = lib.entmtp_accept_stochastic(host_bank.handle, 0, p, p, p, 100, fs(1.0), p, p, p, p, p, p,
+                                      p, p, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
     # workspace query
     assert api.tree_attn_workspace(27, 32, 32, 64, 256) == 0
     assert api.tree_attn_workspace(27, 30, 8, 128, 256) == 0
