@@ -14,7 +14,9 @@
 //  2. attend: flash-decoding over the cache.  A workgroup owns one
 //     (KV head, 32-query tile, key split); its four waves take interleaved
 //     32-key blocks, each wave loading its next block while it multiplies the
-//     current one.  S^T = K Q^T and O^T += V^T P^T run on
+//     current one (K two blocks deep in registers, V one; the query tile's
+//     fragments live once per workgroup in LDS, which keeps the kernel under
+//     320 registers per lane and lets it share a SIMD with the LM head).  S^T = K Q^T and O^T += V^T P^T run on
 //     v_mfma_f32_32x32x16_bf16: K comes from HBM straight into A-operand
 //     registers, V is transposed through a per-wave LDS tile, P never leaves
 //     registers (the S^T accumulator layout is re-read as the B operand of
@@ -253,14 +255,15 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
   }
 
-  // Q^T B-operand fragments: lane (query li, half lh) holds d = 16s + 8lh + e
-  const int qrow = qt * kQTile + li;
-  u32x4 qf[8];
+  // Q^T B-operand fragments, the same for the four waves (they split keys,
+  // not queries), staged once in LDS: lane (query li, half lh) reads
+  // d = 16s + 8lh + e from slot [s][lane]
+  __shared__ u32x4 s_qf[8][64];
   {
+    const int qrow = qt * kQTile + li;
     const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD + 8 * lh;
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-      qf[s] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+    for (int s = wave; s < 8; s += kAttnWaves)
+      s_qf[s][lane] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
   }
   __syncthreads();
 
@@ -283,13 +286,16 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   // K/V of one block into registers.  Keys past the end are clamped to the
   // last key (finite data whose probabilities are zero), so every load is
   // unconditional and the compiler's wait counts stay exact.
-  auto load_kv = [&](int blk, u32x4 (&kf)[8], u32x4 (&va)[4], u32x4 (&vb)[4]) {
+  auto load_k = [&](int blk, u32x4 (&kf)[8]) {
     const int kb = blk * KB;
-    const int last = nkeys - 1;
-    const int key = min(kb + li, last);
+    const int key = min(kb + li, nkeys - 1);
     const uint16_t* kp = kbase + static_cast<size_t>(key) * HD + 8 * lh;
 #pragma unroll
     for (int s = 0; s < 8; ++s) kf[s] = *reinterpret_cast<const u32x4*>(kp + 16 * s);
+  };
+  auto load_v = [&](int blk, u32x4 (&va)[4], u32x4 (&vb)[4]) {
+    const int kb = blk * KB;
+    const int last = nkeys - 1;
     // V: key pairs (2pp, 2pp+1) x 8-dim chunk m
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -301,8 +307,8 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
   };
 
-  auto attend = [&](int blk, const u32x4 (&kf)[8], const u32x4 (&v0)[4], const u32x4 (&v1)[4]) {
-    const int kb = blk * KB;
+  // a block's V into this wave's V^T tile
+  auto stage_v = [&](const u32x4 (&v0)[4], const u32x4 (&v1)[4]) {
     wave_lds_sync();  // previous block's V^T reads are done
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -316,13 +322,19 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
         vt[(8 * m + 2 * w + 1) * (VT_LD / 2) + pp] = (a >> 16) | (b & 0xFFFF0000u);
       }
     }
+  };
+
+  // the block's scores, online softmax and P V (V from the staged tile)
+  auto attend = [&](int blk, const u32x4 (&kf)[8]) {
+    const int kb = blk * KB;
     // S^T[key][query] = K Q^T
     f32x16 sacc;
 #pragma unroll
     for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
 #pragma unroll
     for (int s = 0; s < 8; ++s)
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[s]), as_bf16x8(qf[s]), sacc, 0, 0, 0);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[s]), as_bf16x8(s_qf[s][lane]), sacc,
+                                                     0, 0, 0);
 
     // mask: lane holds keys n = 8*(r/4) + 4*lh + r%4 of the block for query li
     uint32_t win = 0xFFFFFFFFu;
@@ -392,20 +404,30 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
   };
 
-  // two-deep pipeline: block b+4 streams in while block b is multiplied (the
-  // load after a wave's last block re-reads that block, an L2 hit)
+  // K two deep (block b+4 streams in while block b is multiplied); V one
+  // deep, the next block's loads issued as soon as this block's V is in its
+  // LDS tile.  (The loads after a wave's last block re-read that block, an
+  // L2 hit.)  Keeping V's registers single lets the kernel share a SIMD with
+  // an LM-head wavefront.
   if (blk_lo + wave < blk_hi) {
-    u32x4 kA[8], vA0[4], vA1[4], kB[8], vB0[4], vB1[4];
+    u32x4 kA[8], kB[8], v0[4], v1[4];
     int cur = blk_lo + wave;
-    load_kv(cur, kA, vA0, vA1);
+    load_k(cur, kA);
+    load_v(cur, v0, v1);
     while (true) {
       const int nb = cur + kAttnWaves;
-      load_kv(nb < blk_hi ? nb : cur, kB, vB0, vB1);
-      attend(cur, kA, vA0, vA1);
+      const int nbc = nb < blk_hi ? nb : cur;
+      load_k(nbc, kB);
+      stage_v(v0, v1);
+      load_v(nbc, v0, v1);
+      attend(cur, kA);
       if (nb >= blk_hi) break;
       const int nb2 = nb + kAttnWaves;
-      load_kv(nb2 < blk_hi ? nb2 : nb, kA, vA0, vA1);
-      attend(nb, kB, vB0, vB1);
+      const int nb2c = nb2 < blk_hi ? nb2 : nb;
+      load_k(nb2c, kA);
+      stage_v(v0, v1);
+      load_v(nb2c, v0, v1);
+      attend(nb, kB);
       if (nb2 >= blk_hi) break;
       cur = nb2;
     }
