@@ -47,7 +47,8 @@ def parse():
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="bank5_L2048_7b",
-                    choices=["bank5_L2048_7b", "tree27_L256_7b"])
+                    choices=["bank5_L2048_7b", "tree27_L256_7b", "tree64_L4096_7b_32layer",
+                             "tree128_L8192_13b"])
     ap.add_argument("--pool", type=int, default=32, help="distinct per-step input sets")
     ap.add_argument("--weight-copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -133,15 +134,27 @@ def main():
     W = [to_dev(w_host)]
     for c in range(1, args.weight_copies):
         W.append(W[0].clone())
+    NL = wl.n_layers
     base = synth.attn_inputs(wl.ident, 1, Hq, Hkv, d, L0, cap)
     kc0_host, vc0_host = base.k_cache[:, :L0].copy(), base.v_cache[:, :L0].copy()
-    k_cache = torch.zeros((Hkv, cap, d), dtype=bf, device=dev)
-    v_cache = torch.zeros((Hkv, cap, d), dtype=bf, device=dev)
-    k_cache[:, :L0] = to_dev(kc0_host)
-    v_cache[:, :L0] = to_dev(vc0_host)
+    k_cache = torch.zeros((NL, Hkv, cap, d), dtype=bf, device=dev)   # [layer][head][slot][dim]
+    v_cache = torch.zeros((NL, Hkv, cap, d), dtype=bf, device=dev)
+    k_cache[0, :, :L0] = to_dev(kc0_host)
+    v_cache[0, :, :L0] = to_dev(vc0_host)
     del base
+    # further layers (the 32-layer workload): seeded N(0, 1) drawn on the GPU,
+    # a generator per layer (the oracle baseline covers single-layer work)
+    gen = torch.Generator(device=dev)
 
-    P = args.pool
+    def randn_dev(shape, seed):
+        gen.manual_seed(seed)
+        return torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(bf)
+
+    for l in range(1, NL):
+        k_cache[l, :, :L0] = randn_dev((Hkv, L0, d), 1000 * wl.ident + 2 * l)
+        v_cache[l, :, :L0] = randn_dev((Hkv, L0, d), 1000 * wl.ident + 2 * l + 1)
+
+    P = args.pool if NL == 1 else min(args.pool, 4)
     deltas, spike_tok = synth.regime_spikes(wl.ident, P, Tmax, V, hid)
     pool = []
     for e in range(P):
@@ -150,7 +163,13 @@ def main():
         if grows:
             x = synth.plant_spike(x, w_host, spike_tok[e], float(deltas[e]), wl.w_std)
         u, r = synth.draft_randoms(wl.ident, Tmax, V, step=e + 1)
-        pool.append({"q": to_dev(a_in.q), "kt": to_dev(a_in.k_tree), "vt": to_dev(a_in.v_tree),
+        q_l, kt_l, vt_l = [to_dev(a_in.q)], [to_dev(a_in.k_tree)], [to_dev(a_in.v_tree)]
+        for l in range(1, NL):   # layer-major, as the step reads them
+            sd = 1000 * wl.ident + 100 * (e + 1) + 3 * l
+            q_l.append(randn_dev((Tmax, Hq, d), sd))
+            kt_l.append(randn_dev((Tmax, Hkv, d), sd + 1))
+            vt_l.append(randn_dev((Tmax, Hkv, d), sd + 2))
+        pool.append({"q": torch.stack(q_l), "kt": torch.stack(kt_l), "vt": torch.stack(vt_l),
                      "x": to_dev(x), "u": u, "r": r,
                      "host": (a_in.q, a_in.k_tree, a_in.v_tree, x)})
     log(f"staged inputs in {time.time() - t0:.1f}s")
@@ -166,11 +185,11 @@ def main():
     # moves
     on_gpu = grows and args.gpu_scheduler
     tau_on, tau_off = (0.8, 0.6) if args.fixed_topo < 0 else (float("inf"), float("-inf"))
-    st = [api.Step(bank, k_cache, v_cache, W[0], Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax,
-                   scale=scale, rope_theta=theta, keep_logits=False, tau_on=tau_on,
-                   tau_off=tau_off, stream=run_stream)]
+    st = [api.Step(bank, k_cache, v_cache, W[0], n_layers=NL, Hq=Hq, Hkv=Hkv, d=d, cap=cap,
+                   tree_rows=Tmax, scale=scale, rope_theta=theta, keep_logits=False, tau_on=tau_on,
+                   tau_off=tau_off, cache_layer_stride=Hkv * cap * d, stream=run_stream)]
     torch.cuda.synchronize()
-    out = torch.empty((Tmax, Hq, d), dtype=bf, device=dev)
+    out = torch.empty((NL, Tmax, Hq, d), dtype=bf, device=dev)
 
     # draft tokens: the target's greedy token at the parent with prob p_acc,
     # computed with the library itself on each pool entry (input synthesis)
@@ -305,11 +324,11 @@ def main():
     # algorithmic bytes (what the method must move; fp32 logits excluded)
     def step_bytes(T, L, a):
         w = V * hid * 2
-        kv = 2 * Hkv * L * d * 2
-        tree_in = T * (Hq + 2 * Hkv) * d * 2 + T * hid * 2
-        tree_kv_out = T * 2 * Hkv * d * 2
-        att_out = T * Hq * d * 2
-        compact = 2 * (a + 1) * 2 * Hkv * d * 2
+        kv = NL * 2 * Hkv * L * d * 2
+        tree_in = NL * T * (Hq + 2 * Hkv) * d * 2 + T * hid * 2
+        tree_kv_out = NL * T * 2 * Hkv * d * 2
+        att_out = NL * T * Hq * d * 2
+        compact = NL * 2 * (a + 1) * 2 * Hkv * d * 2
         stats = T * 12
         return w + kv + tree_in + tree_kv_out + att_out + compact + stats
 
@@ -332,7 +351,7 @@ def main():
 
     # ---------------------------------------------------------- cpu baseline
     cpu = None
-    if not args.no_cpu_baseline:
+    if not args.no_cpu_baseline and NL == 1:
         cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta,
                            [topo for *_, topo in trace])
 
@@ -345,7 +364,8 @@ def main():
         "us_per_step": round(us, 2), "higher_is_better": True, "scaling": "weak",
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "hbm_GBps_algorithmic": round(hbm, 1), "hbm_frac": round(hbm / HBM_PEAK_GBPS, 4),
-        "config": {"workload": wl.name, "batch": 1, "heads": Hq, "kv_heads": Hkv, "head_dim": d,
+        "config": {"workload": wl.name, "batch": 1, "layers": NL, "heads": Hq, "kv_heads": Hkv,
+                   "head_dim": d,
                    "hidden": hid, "vocab": V, "prefix_len_start": L0,
                    "prefix_len_end": state["L"], "bank_T": bank.T,
                    "scheduler": ("hysteretic ladder on=0.8 off=0.6" if args.fixed_topo < 0
