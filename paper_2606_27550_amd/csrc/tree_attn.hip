@@ -12,17 +12,20 @@
 //     [L, L+T) and the rotated queries into the workspace, grouped per KV
 //     head (GQA: query rows = head-in-group x node).
 //  2. attend: flash-decoding over the cache.  A workgroup owns one
-//     (KV head, 32-query tile, key split); its four waves take interleaved
-//     32-key blocks, each wave loading its next block while it multiplies the
-//     current one (K two blocks deep in registers, V one; the query tile's
-//     fragments live once per workgroup in LDS, which keeps the kernel under
-//     320 registers per lane and lets it share a SIMD with the LM head).  S^T = K Q^T and O^T += V^T P^T run on
-//     v_mfma_f32_32x32x16_bf16: K comes from HBM straight into A-operand
-//     registers, V is transposed through a per-wave LDS tile, P never leaves
-//     registers (the S^T accumulator layout is re-read as the B operand of
-//     the PV product after a fixed key permutation).  Keys at or past the
-//     prefix are masked with a 32-bit window cut from the node's ancestor
-//     bitmask.  Online softmax in fp32, base 2.  The four waves merge in LDS.
+//     (KV head, group of two 32-query tiles, key split); its four waves take
+//     interleaved 32-key blocks, each wave loading its next block while it
+//     multiplies the current one (K two blocks deep in registers, V one) and
+//     applying every block to both tiles, so a KV block is read once per 64
+//     query rows.  The tiles' fragments live once per workgroup in LDS.
+//     S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16: K comes
+//     from HBM straight into A-operand registers, V is transposed through a
+//     per-wave LDS tile, P never leaves registers (the S^T accumulator layout
+//     is re-read as the B operand of the PV product after a fixed key
+//     permutation).  Blocks wholly inside the prefix skip the mask; the
+//     others take a 32-bit window cut from the node's ancestor bitmask.
+//     Online softmax in fp32, base 2, with a lazily raised running max (the
+//     accumulators are rescaled only when a block's max passes the reference
+//     by more than 2^8).  The four waves merge in LDS.
 //  3. merge: combines the splits' (max, sum, unnormalised output) partials.
 //     Skipped when a single split covers the keys.
 #include <cfloat>
@@ -32,11 +35,15 @@
 namespace entmtp {
 namespace {
 
+typedef __bf16 bf16x2 __attribute__((ext_vector_type(2)));
+typedef float f32x2 __attribute__((ext_vector_type(2)));
+
 constexpr int HD = ENTMTP_HEAD_DIM;  // 128
 constexpr int kAttnThreads = 256;
 constexpr int kAttnWaves = 4;
 constexpr int KB = 32;               // keys per block
 constexpr int kQTile = 32;           // query rows per tile
+constexpr float kLazyLog2 = 8.f;     // the running max is raised only past this many doublings
 constexpr int VT_LD = 36;            // bf16 per V^T row in LDS (32 keys + pad)
 constexpr int kMaxSplits = 32;
 constexpr int kMinBlocksPerSplit = 4;   // one block per wave at least
@@ -45,6 +52,9 @@ constexpr int kMaxSeqs = ENTMTP_B_MAX;
 __host__ __device__ inline int rows_padded(int G, int T) {
   return (G * T + kQTile - 1) / kQTile * kQTile;
 }
+
+// Workgroups along the query rows: groups of nt 32-row tiles.
+__host__ __device__ inline int query_groups(int nqt, int nt) { return (nqt + nt - 1) / nt; }
 
 __host__ __device__ inline int split_bound(int nblocks) {
   int b = nblocks / kMinBlocksPerSplit;
@@ -85,7 +95,7 @@ struct SeqPlan {
   const uint32_t* mask;    // [T][ENTMTP_MASK_WORDS] its tree's ancestor bitmask
   const int* depth;        // [T]
   int T, L, row0;          // nodes, prefix length, first row in the concatenated q / out
-  int rows_pad, nqt, nsplit, bps;
+  int rows_pad, nqt, nqg, nsplit, bps;   // padded rows, query tiles, query groups, splits
   int item0;               // first attend workgroup of the sequence
   int merge0;              // first merge block of the sequence
   long long qrot_off;      // element offset of its rotated queries in the workspace
@@ -102,6 +112,7 @@ struct BatchArgs {
   const DevTopo* topos;
   const uint8_t* arena;
   int cus;
+  int nt;                  // query tiles per workgroup of the launched kernel (1 or 2)
   int B, G, Hq, Hkv, cap;
   float scale_log2;
   double theta;
@@ -138,6 +149,7 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
     q.L = 0;
     q.nsplit = 1;
     q.nqt = 0;
+    q.nqg = 0;
     return q;
   }
   q.mask = reinterpret_cast<const uint32_t*>(p.arena + t->off_mask);
@@ -145,8 +157,9 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
   q.row0 = 0;
   q.rows_pad = rows_padded(p.G, q.T);
   q.nqt = q.rows_pad / kQTile;
+  q.nqg = query_groups(q.nqt, p.nt);
   const int nblocks = (q.L + q.T + KB - 1) / KB;
-  const int ns = t->splits[split_bound(nblocks)];   // = split_single(nblocks, Hkv * nqt, cus)
+  const int ns = t->splits[split_bound(nblocks)];   // = split_single(nblocks, Hkv * nqg, cus)
   q.bps = (nblocks + ns - 1) / ns;
   q.nsplit = (nblocks + q.bps - 1) / q.bps;
   q.item0 = 0;
@@ -219,66 +232,49 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
+// NT = query tiles per workgroup (1 or 2); every wave holds all NT tiles.
+template <int NT>
 __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
-  // blockIdx -> sequence, then (kv head, split) group and query tile; the
-  // query tiles of one group land on the same XCD (dispatch is round-robin
-  // over 8 XCDs and every sequence's range starts at a multiple of 8), so
-  // their K/V reads share that XCD's L2.
+  // blockIdx -> sequence, then (kv head, split) group and query-tile group;
+  // the query groups of one (head, split) land on the same XCD (dispatch is
+  // round-robin over 8 XCDs and every sequence's range starts at a multiple
+  // of 8), so their K/V reads share that XCD's L2.
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
   const SeqPlan sq = resolve(p, b);
   if (sq.T == 0) return;
   const int bid = blockIdx.x - sq.item0;
-  const int qt = (bid >> 3) % sq.nqt;
-  const int gc = ((bid >> 3) / sq.nqt) * 8 + (bid & 7);
+  const int qg = (bid >> 3) % sq.nqg;
+  const int gc = ((bid >> 3) / sq.nqg) * 8 + (bid & 7);
   if (gc >= p.Hkv * sq.nsplit) return;
   const int g = gc / sq.nsplit, split = gc % sq.nsplit;
   const int T = sq.T, L = sq.L, nkeys = sq.L + sq.T, rows_pad = sq.rows_pad;
   const int nsplit = sq.nsplit;
+  const int qt0 = qg * NT;                      // first query tile of the group
+  const bool two = NT == 2 && qt0 + 1 < sq.nqt;   // the group's second tile exists (uniform)
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 31, lh = lane >> 5;
   const int GT = p.G * T;
+  constexpr int QR = NT * kQTile;   // query rows of a group
 
-  // LDS: per-wave V^T tiles during the loop, reused for the wave merge after it
+  // LDS: the tiles' Q fragments and per-wave V^T tiles during the loop, one
+  // region reused for the wave merge after it
+  constexpr int kQfBytes = NT * 8 * 64 * 16;
   constexpr int kVtBytes = HD * VT_LD * 2;                           // 9216
-  constexpr int OLD = HD + 1;                                         // merge row stride (bank spread)
-  constexpr int kMergeBytes = 2 * kQTile * OLD * 4;                  // 33024: two wave slots
-  constexpr int kLdsBytes = kMergeBytes > kAttnWaves * kVtBytes ? kMergeBytes : kAttnWaves * kVtBytes;
+  constexpr int OLD = HD + 4;                                         // merge row stride (floats)
+  constexpr int kMergeBytes = 2 * kQTile * OLD * 4;                  // 33792: two wave slots
+  constexpr int kLoopBytes = kQfBytes + kAttnWaves * kVtBytes;
+  constexpr int kLdsBytes = kMergeBytes > kLoopBytes ? kMergeBytes : kLoopBytes;
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
-  __shared__ uint32_t s_mask[kQTile][ENTMTP_MASK_WORDS + 1];
-  __shared__ float s_m[kAttnWaves][kQTile], s_l[kAttnWaves][kQTile];
+  __shared__ uint32_t s_mask[QR][ENTMTP_MASK_WORDS + 1];
+  __shared__ float s_m[kAttnWaves][QR], s_l[kAttnWaves][QR];
+  u32x4 (*s_qf)[8][64] = reinterpret_cast<u32x4 (*)[8][64]>(lds);   // [NT][s][lane]
+  uint32_t* vt = reinterpret_cast<uint32_t*>(lds + kQfBytes + wave * kVtBytes);  // [HD][VT_LD/2]
 
-  // ancestor masks of this tile's query rows (padding rows see every key)
-  for (int u = tid; u < kQTile * ENTMTP_MASK_WORDS; u += kAttnThreads) {
-    const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
-    const int qrow = qt * kQTile + r;
-    s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
-  }
-
-  // Q^T B-operand fragments, the same for the four waves (they split keys,
-  // not queries), staged once in LDS: lane (query li, half lh) reads
-  // d = 16s + 8lh + e from slot [s][lane]
-  __shared__ u32x4 s_qf[8][64];
-  {
-    const int qrow = qt * kQTile + li;
-    const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD + 8 * lh;
-    for (int s = wave; s < 8; s += kAttnWaves)
-      s_qf[s][lane] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
-  }
-  __syncthreads();
-
-  uint32_t* vt = reinterpret_cast<uint32_t*>(lds + wave * kVtBytes);  // [HD][VT_LD/2] key pairs
   const size_t head_off = static_cast<size_t>(g) * p.cap * HD;
   const uint16_t* kbase = sq.kc + head_off;
   const uint16_t* vbase = sq.vc + head_off;
-
-  float m_run = -INFINITY, l_run = 0.f;
-  f32x16 o[4];
-#pragma unroll
-  for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[ct][r] = 0.f;
-
+  const float c = p.scale_log2;
   const int nblocks = (nkeys + KB - 1) / KB;
   const int blk_lo = split * sq.bps;
   const int blk_hi = min(nblocks, blk_lo + sq.bps);
@@ -307,8 +303,54 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
   };
 
-  // a block's V into this wave's V^T tile
-  auto stage_v = [&](const u32x4 (&v0)[4], const u32x4 (&v1)[4]) {
+  // the wave's first block is requested before the prologue, so its latency
+  // overlaps the staging of the queries
+  const bool active = blk_lo + wave < blk_hi;
+  u32x4 kA[8], kB[8], v0[4], v1[4];
+  int cur = blk_lo + wave;
+  if (active) {
+    load_k(cur, kA);
+    load_v(cur, v0, v1);
+  }
+
+  // ancestor masks of the group's query rows (padding rows see every key)
+  for (int u = tid; u < QR * ENTMTP_MASK_WORDS; u += kAttnThreads) {
+    const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
+    const int qrow = qt0 * kQTile + r;
+    s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+  }
+  // Q^T B-operand fragments, the same for the four waves (they split keys,
+  // not queries), staged once in LDS: lane (query li, half lh) of tile t
+  // reads d = 16s + 8lh + e from slot [t][s][lane]
+  for (int x = tid; x < NT * 8 * 64; x += kAttnThreads) {
+    const int t = x >> 9, s = (x >> 6) & 7, ln = x & 63;
+    const int qrow = (qt0 + t) * kQTile + (ln & 31);
+    const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD +
+                         8 * (ln >> 5) + 16 * s;
+    s_qf[t][s][ln] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp) : u32x4{0u, 0u, 0u, 0u};
+  }
+  __syncthreads();
+
+  // running (max, sum) per query in base-2 scaled units and the output
+  // accumulators, per tile.  The max is raised lazily: the reference m stays
+  // until a block's maximum exceeds it by more than kLazyLog2, so that the
+  // accumulators are rescaled only a few times per row instead of per block
+  // (probabilities relative to m then reach at most 2^kLazyLog2).
+  float m_run[NT], l_run[NT];
+  f32x16 o[NT][4];
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    m_run[t] = -INFINITY;
+    l_run[t] = 0.f;
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int r = 0; r < 16; ++r) o[t][ct][r] = 0.f;
+  }
+
+  // a block's V into this wave's V^T tile: word (dim, key pair) packs the
+  // pair's two bf16 values of that dim
+  auto stage_v = [&](const u32x4 (&va)[4], const u32x4 (&vb)[4]) {
     wave_lds_sync();  // previous block's V^T reads are done
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -316,78 +358,105 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
       const int pp = u & 15, m = u >> 4;
 #pragma unroll
       for (int w = 0; w < 4; ++w) {
-        const uint32_t a = v0[k][w], b = v1[k][w];
+        const uint32_t a = va[k][w], bw = vb[k][w];
         // dims 8m + 2w (low halves) and 8m + 2w + 1 (high halves)
-        vt[(8 * m + 2 * w) * (VT_LD / 2) + pp] = (a & 0xFFFFu) | (b << 16);
-        vt[(8 * m + 2 * w + 1) * (VT_LD / 2) + pp] = (a >> 16) | (b & 0xFFFF0000u);
+        vt[(8 * m + 2 * w) * (VT_LD / 2) + pp] = __builtin_amdgcn_perm(bw, a, 0x05040100u);
+        vt[(8 * m + 2 * w + 1) * (VT_LD / 2) + pp] = __builtin_amdgcn_perm(bw, a, 0x07060302u);
       }
     }
   };
 
-  // the block's scores, online softmax and P V (V from the staged tile)
-  auto attend = [&](int blk, const u32x4 (&kf)[8]) {
-    const int kb = blk * KB;
-    // S^T[key][query] = K Q^T
-    f32x16 sacc;
+  // scores of one tile -> its probabilities as the B operand of the PV
+  // product (bf16), with the lazy rescale of the tile's accumulators.
+  // Lane (query li, half lh) holds keys n = 8*(r/4) + 4*lh + r%4 of the block.
+  auto softmax = [&](int t, f32x16& sacc, int kb, bool plain, bf16x8 (&pf)[2]) {
+    float bmax = -INFINITY;
+    if (plain) {   // the whole block lies in the prefix: every key is visible
 #pragma unroll
-    for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
-#pragma unroll
-    for (int s = 0; s < 8; ++s)
-      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[s]), as_bf16x8(s_qf[s][lane]), sacc,
-                                                     0, 0, 0);
-
-    // mask: lane holds keys n = 8*(r/4) + 4*lh + r%4 of the block for query li
-    uint32_t win = 0xFFFFFFFFu;
-    const int rel = kb - L;
-    if (rel > -KB) {
+      for (int r = 0; r < 16; ++r) bmax = fmaxf(bmax, sacc[r]);
+    } else {
+      // 32-key window of the query's visibility: prefix keys, then the
+      // ancestor bitmask from position L on
+      uint32_t win = 0xFFFFFFFFu;
+      const int rel = kb - L;
+      const uint32_t* mrow = s_mask[t * kQTile + li];
       if (rel < 0) {
         const int npre = -rel;
-        win = (0xFFFFFFFFu >> (32 - npre)) | (s_mask[li][0] << npre);
+        win = (0xFFFFFFFFu >> (32 - npre)) | (mrow[0] << npre);
       } else {
         const int wi = rel >> 5, sh = rel & 31;
-        const uint32_t lo = s_mask[li][wi];
-        const uint32_t hi = wi + 1 < ENTMTP_MASK_WORDS ? s_mask[li][wi + 1] : 0u;
+        const uint32_t lo = mrow[wi];
+        const uint32_t hi = wi + 1 < ENTMTP_MASK_WORDS ? mrow[wi + 1] : 0u;
         win = sh ? (lo >> sh) | (hi << (32 - sh)) : lo;
       }
-    }
-    float sv[16];
-    float bmax = -INFINITY;
 #pragma unroll
-    for (int r = 0; r < 16; ++r) {
-      const int n = 8 * (r >> 2) + 4 * lh + (r & 3);
-      const bool vis = ((win >> n) & 1u) && (kb + n < nkeys);
-      sv[r] = vis ? sacc[r] * p.scale_log2 : -INFINITY;
-      bmax = fmaxf(bmax, sv[r]);
+      for (int r = 0; r < 16; ++r) {
+        const int n = 8 * (r >> 2) + 4 * lh + (r & 3);
+        const bool vis = ((win >> n) & 1u) && (kb + n < nkeys);
+        sacc[r] = vis ? sacc[r] : -INFINITY;
+        bmax = fmaxf(bmax, sacc[r]);
+      }
     }
     bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
-    const float m_new = fmaxf(m_run, bmax);
-    const float alpha = (m_new == -INFINITY) ? 1.f : exp2f(m_run - m_new);
-    float rsum = 0.f;
+    const float mb = bmax * c;   // -inf stays -inf (c > 0)
+    const bool need = mb > m_run[t] + kLazyLog2;
+    if (__any(need)) {   // uniform branch: rare once the row maximum has settled
+      const float mn = need ? mb : m_run[t];
+      const float alpha = !need ? 1.f : (m_run[t] == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run[t] - mn));
+      l_run[t] *= alpha;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[t][ct][r] *= alpha;
+      m_run[t] = mn;
+    }
+    // with m still -inf every key so far is hidden from the query: p = 0
+    const float mneg = m_run[t] == -INFINITY ? 0.f : -m_run[t];
     float pr[16];
+    float rsum = 0.f;
 #pragma unroll
     for (int r = 0; r < 16; ++r) {
-      pr[r] = (m_new == -INFINITY) ? 0.f : exp2f(sv[r] - m_new);
+      pr[r] = __builtin_amdgcn_exp2f(fmaf(sacc[r], c, mneg));
       rsum += pr[r];
     }
     rsum += __shfl_xor(rsum, 32, 64);
-    l_run = l_run * alpha + rsum;
-    m_run = m_new;
+    l_run[t] += rsum;
+    // P^T as B operand: step u covers keys 16u..16u+15; element e of lane
+    // (query li, half lh) is key 16u + 4lh + e (e < 4) or 16u + 8 + 4lh + e-4
+    // -- exactly accumulator entries 8u .. 8u+7.
 #pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
-
-    // P^T as B operand: step t covers keys 16t..16t+15; element e of lane
-    // (query li, half lh) is key 16t + 4lh + e (e < 4) or 16t + 8 + 4lh + e-4
-    // -- exactly accumulator entries 8t .. 8t+7.
-    bf16x8 pf[2];
-#pragma unroll
-    for (int t = 0; t < 2; ++t) {
+    for (int u = 0; u < 2; ++u) {
       u32x4 w;
 #pragma unroll
       for (int e = 0; e < 4; ++e)
-        w[e] = f32_to_bf16_rne(pr[8 * t + 2 * e]) | (f32_to_bf16_rne(pr[8 * t + 2 * e + 1]) << 16);
-      pf[t] = as_bf16x8(w);
+        w[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+                                               (f32x2{pr[8 * u + 2 * e], pr[8 * u + 2 * e + 1]}), bf16x2));
+      pf[u] = as_bf16x8(w);
+    }
+  };
+
+  // the block's scores, softmax and P V for the group's tiles (V from the
+  // staged tile, each V^T fragment read once for all tiles)
+  auto attend = [&](int blk, const u32x4 (&kf)[8]) {
+    const int kb = blk * KB;
+    const bool plain = kb + KB <= L;
+    f32x16 sacc[NT];
+    bf16x8 pf[NT][2];
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      if (t > 0 && !two) break;
+      // S^T[key][query] = K Q^T
+#pragma unroll
+      for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
+#pragma unroll
+      for (int s = 0; s < 8; ++s)
+        sacc[t] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf[s]), as_bf16x8(s_qf[t][s][lane]),
+                                                        sacc[t], 0, 0, 0);
+    }
+#pragma unroll
+    for (int t = 0; t < NT; ++t) {
+      if (t > 0 && !two) break;
+      softmax(t, sacc[t], kb, plain, pf[t]);
     }
     wave_lds_sync();  // V^T tile written by every lane
     // O^T[dim][query] += V^T P^T; A operand lane (dim li of tile ct, half lh)
@@ -395,11 +464,14 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     for (int ct = 0; ct < 4; ++ct) {
       const uint32_t* row = vt + (32 * ct + li) * (VT_LD / 2);
 #pragma unroll
-      for (int t = 0; t < 2; ++t) {
-        const uint2 x0 = *reinterpret_cast<const uint2*>(row + 8 * t + 2 * lh);
-        const uint2 x1 = *reinterpret_cast<const uint2*>(row + 8 * t + 4 + 2 * lh);
+      for (int u = 0; u < 2; ++u) {
+        const uint2 x0 = *reinterpret_cast<const uint2*>(row + 8 * u + 2 * lh);
+        const uint2 x1 = *reinterpret_cast<const uint2*>(row + 8 * u + 4 + 2 * lh);
         const u32x4 w = {x0.x, x0.y, x1.x, x1.y};
-        o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t], o[ct], 0, 0, 0);
+#pragma unroll
+        for (int t = 0; t < NT; ++t)
+          if (t == 0 || two)
+            o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t][u], o[t][ct], 0, 0, 0);
       }
     }
   };
@@ -407,13 +479,8 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   // K two deep (block b+4 streams in while block b is multiplied); V one
   // deep, the next block's loads issued as soon as this block's V is in its
   // LDS tile.  (The loads after a wave's last block re-read that block, an
-  // L2 hit.)  Keeping V's registers single lets the kernel share a SIMD with
-  // an LM-head wavefront.
-  if (blk_lo + wave < blk_hi) {
-    u32x4 kA[8], kB[8], v0[4], v1[4];
-    int cur = blk_lo + wave;
-    load_k(cur, kA);
-    load_v(cur, v0, v1);
+  // L2 hit.)
+  if (active) {
     while (true) {
       const int nb = cur + kAttnWaves;
       const int nbc = nb < blk_hi ? nb : cur;
@@ -433,78 +500,87 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
   }
 
-  // ---- merge the four waves: waves 2 and 3 into 0 and 1, then 1 into 0,
-  // through two wave-sized LDS slots (so the merge needs no more LDS than the
-  // V^T tiles, and the kernel leaves room on a CU for other work)
-  __syncthreads();  // every wave is done with its V^T tile
+  // ---- merge the four waves, tile by tile: each wave rescales to the
+  // common reference max; waves 2 and 3 hand their sums to 0 and 1 through
+  // two LDS slots, 0 and 1 write the pair sums back, and all threads combine
+  // the two slots into the output (float4 rows, no more LDS than the loop's)
+  __syncthreads();  // every wave is done with its Q fragments and V^T tile
   if (lh == 0) {
-    s_m[wave][li] = m_run;
-    s_l[wave][li] = l_run;
-  }
-  __syncthreads();
-  float M = -INFINITY;
 #pragma unroll
-  for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][li]);
-  const float myscale = (m_run == -INFINITY) ? 0.f : exp2f(m_run - M);
-#pragma unroll
-  for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-    for (int r = 0; r < 16; ++r) o[ct][r] *= myscale;
-  float* ored = reinterpret_cast<float*>(lds);  // [slot][query][HD]
-  auto put = [&](int slot) {
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int dim = 32 * ct + 8 * (r >> 2) + 4 * lh + (r & 3);
-        ored[(slot * kQTile + li) * OLD + dim] = o[ct][r];
-      }
-  };
-  auto add = [&](int slot) {
-#pragma unroll
-    for (int ct = 0; ct < 4; ++ct)
-#pragma unroll
-      for (int r = 0; r < 16; ++r) {
-        const int dim = 32 * ct + 8 * (r >> 2) + 4 * lh + (r & 3);
-        o[ct][r] += ored[(slot * kQTile + li) * OLD + dim];
-      }
-  };
-  if (wave >= 2) put(wave - 2);
-  __syncthreads();
-  if (wave < 2) add(wave);
-  __syncthreads();
-  if (wave == 1) put(0);
-  __syncthreads();
-  if (wave == 0) {
-    add(0);
-    put(0);
-  }
-  __syncthreads();
-  for (int u = tid; u < kQTile * HD; u += kAttnThreads) {
-    const int q = u / HD, dim = u % HD;
-    const int row = qt * kQTile + q;
-    if (row >= GT) continue;
-    float Mq = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < kAttnWaves; ++w) Mq = fmaxf(Mq, s_m[w][q]);
-    float lsum = 0.f;
-#pragma unroll
-    for (int w = 0; w < kAttnWaves; ++w) {
-      const float sc = (s_m[w][q] == -INFINITY) ? 0.f : exp2f(s_m[w][q] - Mq);
-      lsum += s_l[w][q] * sc;
+    for (int t = 0; t < NT; ++t) {
+      s_m[wave][t * kQTile + li] = m_run[t];
+      s_l[wave][t * kQTile + li] = l_run[t];
     }
-    const float osum = ored[q * OLD + dim];
-    if (nsplit == 1) {
-      const int gh = row / T, node = row % T;
-      const int h = g * p.G + gh;
-      p.out[(static_cast<size_t>(sq.row0 + node) * p.Hq + h) * HD + dim] =
-          static_cast<uint16_t>(f32_to_bf16_rne(osum / lsum));
-    } else {
-      const size_t prow = sq.part_off + (static_cast<size_t>(split) * p.Hkv + g) * rows_pad + row;
-      p.part_o[prow * HD + dim] = osum;
-      if (dim == 0) {
-        p.part_ml[prow * 2 + 0] = Mq;
-        p.part_ml[prow * 2 + 1] = lsum;
+  }
+  __syncthreads();
+  float* ored = reinterpret_cast<float*>(lds);  // [slot][query][OLD]
+#pragma unroll
+  for (int t = 0; t < NT; ++t) {
+    if (t > 0 && !two) break;
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][t * kQTile + li]);
+    const float myscale = (m_run[t] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run[t] - M);
+    // lane (query li, half lh) holds dims 32ct + 8j + 4lh + i in o[t][ct][4j + i]
+    auto slot_at = [&](int slot, int ct, int j) {
+      return reinterpret_cast<float4*>(ored + (slot * kQTile + li) * OLD + 32 * ct + 8 * j + 4 * lh);
+    };
+    if (t > 0) __syncthreads();   // the previous tile's slots are read out
+    if (wave >= 2) {
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int j = 0; j < 4; ++j)
+          *slot_at(wave - 2, ct, j) = make_float4(o[t][ct][4 * j] * myscale, o[t][ct][4 * j + 1] * myscale,
+                                                  o[t][ct][4 * j + 2] * myscale, o[t][ct][4 * j + 3] * myscale);
+    }
+    __syncthreads();
+    if (wave < 2) {
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int j = 0; j < 4; ++j) {
+          float4* sl = slot_at(wave, ct, j);
+          const float4 x = *sl;
+          *sl = make_float4(x.x + o[t][ct][4 * j] * myscale, x.y + o[t][ct][4 * j + 1] * myscale,
+                            x.z + o[t][ct][4 * j + 2] * myscale, x.w + o[t][ct][4 * j + 3] * myscale);
+        }
+    }
+    __syncthreads();
+    // thread -> (query q, four dims): 32 x 32 float4 items, four per thread
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int x = tid + kAttnThreads * i;
+      const int q = x >> 5, d4 = 4 * (x & 31);
+      const int row = (qt0 + t) * kQTile + q;
+      if (row >= GT) continue;
+      const int sr = t * kQTile + q;
+      float Mq = -INFINITY;
+#pragma unroll
+      for (int w = 0; w < kAttnWaves; ++w) Mq = fmaxf(Mq, s_m[w][sr]);
+      float lsum = 0.f;
+#pragma unroll
+      for (int w = 0; w < kAttnWaves; ++w) {
+        const float sc = (s_m[w][sr] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(s_m[w][sr] - Mq);
+        lsum += s_l[w][sr] * sc;
+      }
+      const float4 s0 = *reinterpret_cast<const float4*>(ored + q * OLD + d4);
+      const float4 s1 = *reinterpret_cast<const float4*>(ored + (kQTile + q) * OLD + d4);
+      const float4 os = make_float4(s0.x + s1.x, s0.y + s1.y, s0.z + s1.z, s0.w + s1.w);
+      if (nsplit == 1) {
+        const int gh = row / T, node = row % T;
+        const int h = g * p.G + gh;
+        uint2 pk;
+        pk.x = f32_to_bf16_rne(os.x / lsum) | (f32_to_bf16_rne(os.y / lsum) << 16);
+        pk.y = f32_to_bf16_rne(os.z / lsum) | (f32_to_bf16_rne(os.w / lsum) << 16);
+        *reinterpret_cast<uint2*>(p.out + (static_cast<size_t>(sq.row0 + node) * p.Hq + h) * HD + d4) = pk;
+      } else {
+        const size_t prow = sq.part_off + (static_cast<size_t>(split) * p.Hkv + g) * rows_pad + row;
+        *reinterpret_cast<float4*>(p.part_o + prow * HD + d4) = os;
+        if (d4 == 0) {
+          p.part_ml[prow * 2 + 0] = Mq;
+          p.part_ml[prow * 2 + 1] = lsum;
+        }
       }
     }
   }
@@ -541,6 +617,21 @@ __global__ __launch_bounds__(HD) void attn_merge_kernel(BatchArgs p) {
 // ------------------------------------------------------------------ host --
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
+
+void launch_attend(const BatchArgs& a, int items, hipStream_t s) {
+  if (a.nt == 2)
+    hipLaunchKernelGGL(tree_attn_kernel<2>, dim3(items), dim3(kAttnThreads), 0, s, a);
+  else
+    hipLaunchKernelGGL(tree_attn_kernel<1>, dim3(items), dim3(kAttnThreads), 0, s, a);
+}
+
+// Query tiles per workgroup of device-planned calls on a bank: two when some
+// topology has more than one tile.
+int device_tiles(const entmtp_bank* bank, int G) {
+  for (const TopoDesc& td : bank->desc)
+    if (rows_padded(G, td.T) > kQTile) return 2;
+  return 1;
+}
 
 int device_cus() {
   static int cus[64] = {0};
@@ -579,12 +670,15 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
   a.cap = cap;
   const int cus = device_cus();
   a.cus = cus;
+  a.nt = 1;   // two tiles per workgroup as soon as some sequence has more than one
   long long work = 0;
   for (int b = 0; b < B; ++b) {
     const int T = bank->desc[topo[b]].T;
     const int nqt = rows_padded(a.G, T) / kQTile;
+    if (nqt > 1) a.nt = 2;
     work += static_cast<long long>(Hkv) * nqt * ((L[b] + T + KB - 1) / KB);
   }
+  work = (work + a.nt - 1) / a.nt;
   const long long per_wg = (work + 4LL * cus - 1) / (4LL * cus);
   const int target_bps = static_cast<int>(per_wg > kMinBlocksPerSplit ? per_wg : kMinBlocksPerSplit);
 
@@ -602,10 +696,11 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     q.row0 = sh.rows;
     q.rows_pad = rows_padded(a.G, q.T);
     q.nqt = q.rows_pad / kQTile;
+    q.nqg = query_groups(q.nqt, a.nt);
     const int nblocks = (q.L + q.T + KB - 1) / KB;
     int ns;
     if (B == 1) {
-      ns = split_single(nblocks, Hkv * q.nqt, cus);
+      ns = split_single(nblocks, Hkv * q.nqg, cus);
     } else {
       ns = (nblocks + target_bps - 1) / target_bps;
       const int bound = split_bound(nblocks);
@@ -618,7 +713,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     q.qrot_off = qrot;
     q.part_off = part_rows;
     sh.rows += q.T;
-    sh.items += (Hkv * q.nsplit + 7) / 8 * 8 * q.nqt;
+    sh.items += (Hkv * q.nsplit + 7) / 8 * 8 * q.nqg;
     if (q.nsplit > 1) {
       sh.merge_blocks += Hkv * a.G * q.T;
       part_rows += static_cast<long long>(q.nsplit) * Hkv * q.rows_pad;
@@ -648,7 +743,7 @@ int32_t launch_call(BatchArgs& a, const CallShape& sh, void* workspace, hipStrea
   const int prep_items = (a.Hq + a.Hkv) * (HD / 2) + a.Hkv * (HD / 8);
   hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
   if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
-  hipLaunchKernelGGL(tree_attn_kernel, dim3(sh.items), dim3(kAttnThreads), 0, s, a);
+  launch_attend(a, sh.items, s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
   if (sh.merge_blocks > 0) {
     hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(HD), 0, s, a);
@@ -709,13 +804,13 @@ int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, Dev
   DevAttnShape sh;
   for (const TopoDesc& td : bank->desc) {
     sh.T_max = td.T > sh.T_max ? td.T : sh.T_max;
-    const int nqt = rows_padded(G, td.T) / kQTile;
+    const int nqg = query_groups(rows_padded(G, td.T) / kQTile, device_tiles(bank, G));
     const int max_blocks = (cap + KB - 1) / KB;
     for (int nblocks = 1; nblocks <= max_blocks; ++nblocks) {
-      const int ns0 = split_single(nblocks, Hkv * nqt, cus);
+      const int ns0 = split_single(nblocks, Hkv * nqg, cus);
       const int bps = (nblocks + ns0 - 1) / ns0;
       const int ns = (nblocks + bps - 1) / bps;
-      const int items = (Hkv * ns + 7) / 8 * 8 * nqt;
+      const int items = (Hkv * ns + 7) / 8 * 8 * nqg;
       sh.items = items > sh.items ? items : sh.items;
     }
   }
@@ -730,10 +825,10 @@ void attn_device_splits(const entmtp_bank* bank, int Hq, int Hkv, DevTopo* topos
   const int cus = device_cus();
   const int G = Hq / Hkv;
   for (size_t k = 0; k < bank->desc.size(); ++k) {
-    const int nqt = rows_padded(G, bank->desc[k].T) / kQTile;
+    const int nqg = query_groups(rows_padded(G, bank->desc[k].T) / kQTile, device_tiles(bank, G));
     topos[k].splits[0] = 1;
     for (int b = 1; b <= kMaxSplits; ++b)
-      topos[k].splits[b] = static_cast<unsigned char>(split_for_bound(b, Hkv * nqt, cus));
+      topos[k].splits[b] = static_cast<unsigned char>(split_for_bound(b, Hkv * nqg, cus));
   }
 }
 
@@ -747,6 +842,7 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   a.topos = topos;
   a.arena = bank->arena;
   a.cus = device_cus();
+  a.nt = device_tiles(bank, Hq / Hkv);
   a.B = 1;
   a.G = Hq / Hkv;
   a.Hq = Hq;
@@ -772,7 +868,7 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
   hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
   if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
-  hipLaunchKernelGGL(tree_attn_kernel, dim3(sh.items), dim3(kAttnThreads), 0, s, a);
+  launch_attend(a, sh.items, s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
   hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(HD), 0, s, a);
   return launch_status("tree_attn merge launch");
