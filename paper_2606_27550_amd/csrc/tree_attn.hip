@@ -588,30 +588,65 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
 
 // ----------------------------------------------------------------- merge --
 
-__global__ __launch_bounds__(HD) void attn_merge_kernel(BatchArgs p) {
+// One half-wavefront per output row (kMergeRows rows per block): lane c <
+// nsplit reads split c's (max, sum), the group reduces them to the common max
+// and the normalised split weights, then each lane combines four dims of
+// every split's partial output (independent float4 loads, unrolled).
+constexpr int kMergeRows = 8;
+constexpr int kMergeThreads = 32 * kMergeRows;
+static_assert(kMaxSplits <= 32, "a half-wavefront holds one lane per split");
+
+__global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) {
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.merge0; });
   const SeqPlan sq = resolve(p, b);
   if (sq.nsplit == 1 || sq.T == 0) return;   // written by the attend kernel, or nothing to do
   const int GT = p.G * sq.T;
-  const int local = blockIdx.x - sq.merge0;
-  if (local >= p.Hkv * GT) return;   // device-planned grids cover the largest tree
+  const int local = (blockIdx.x - sq.merge0) * kMergeRows + (threadIdx.x >> 5);
+  if (local >= p.Hkv * GT) return;   // past the last row (device-planned grids cover the largest tree)
   const int g = local / GT, row = local % GT;
-  const int dim = threadIdx.x;
-  float M = -INFINITY;
-  for (int c = 0; c < sq.nsplit; ++c)
-    M = fmaxf(M, p.part_ml[(sq.part_off + (static_cast<size_t>(c) * p.Hkv + g) * sq.rows_pad + row) * 2]);
-  float lsum = 0.f, osum = 0.f;
-  for (int c = 0; c < sq.nsplit; ++c) {
-    const size_t prow = sq.part_off + (static_cast<size_t>(c) * p.Hkv + g) * sq.rows_pad + row;
-    const float mc = p.part_ml[prow * 2];
-    if (mc == -INFINITY) continue;
-    const float sc = exp2f(mc - M);
-    lsum += p.part_ml[prow * 2 + 1] * sc;
-    osum += p.part_o[prow * HD + dim] * sc;
+  const int lane = threadIdx.x & 31;
+  const int nsplit = sq.nsplit;
+  auto prow_of = [&](int c) {
+    return sq.part_off + (static_cast<size_t>(c) * p.Hkv + g) * sq.rows_pad + row;
+  };
+  float mc = -INFINITY, lc = 0.f;
+  if (lane < nsplit) {
+    const float2 ml = *reinterpret_cast<const float2*>(p.part_ml + prow_of(lane) * 2);
+    mc = ml.x;
+    lc = ml.y;
+  }
+  float M = mc;
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 32));
+  const float w = mc == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(mc - M);
+  float lsum = lc * w;
+#pragma unroll
+  for (int off = 16; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off, 32);
+  const float wn = w / lsum;   // the split's share of the row
+  const int d4 = 4 * lane;
+  float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  for (int c0 = 0; c0 < nsplit; c0 += 4) {   // four splits' loads in flight at a time
+    float4 o[4];
+    float wc[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      const int c = min(c0 + k, nsplit - 1);
+      wc[k] = c0 + k < nsplit ? __shfl(wn, c, 32) : 0.f;
+      o[k] = *reinterpret_cast<const float4*>(p.part_o + prow_of(c) * HD + d4);
+    }
+#pragma unroll
+    for (int k = 0; k < 4; ++k) {
+      acc.x += wc[k] * o[k].x;
+      acc.y += wc[k] * o[k].y;
+      acc.z += wc[k] * o[k].z;
+      acc.w += wc[k] * o[k].w;
+    }
   }
   const int gh = row / sq.T, node = row % sq.T;
-  p.out[(static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + gh) * HD + dim] =
-      static_cast<uint16_t>(f32_to_bf16_rne(osum / lsum));
+  uint2 pk;
+  pk.x = f32_to_bf16_rne(acc.x) | (f32_to_bf16_rne(acc.y) << 16);
+  pk.y = f32_to_bf16_rne(acc.z) | (f32_to_bf16_rne(acc.w) << 16);
+  *reinterpret_cast<uint2*>(p.out + (static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + gh) * HD + d4) = pk;
 }
 
 // ------------------------------------------------------------------ host --
@@ -715,7 +750,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     sh.rows += q.T;
     sh.items += (Hkv * q.nsplit + 7) / 8 * 8 * q.nqg;
     if (q.nsplit > 1) {
-      sh.merge_blocks += Hkv * a.G * q.T;
+      sh.merge_blocks += (Hkv * a.G * q.T + kMergeRows - 1) / kMergeRows;
       part_rows += static_cast<long long>(q.nsplit) * Hkv * q.rows_pad;
     }
     qrot += static_cast<long long>(Hkv) * q.rows_pad * HD;
@@ -746,7 +781,7 @@ int32_t launch_call(BatchArgs& a, const CallShape& sh, void* workspace, hipStrea
   launch_attend(a, sh.items, s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
   if (sh.merge_blocks > 0) {
-    hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(HD), 0, s, a);
+    hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
     if (int32_t rc = launch_status("tree_attn merge launch")) return rc;
   }
   return ENTMTP_OK;
@@ -815,7 +850,7 @@ int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, Dev
     }
   }
   sh.rows = sh.T_max;
-  sh.merge_blocks = Hkv * G * sh.T_max;
+  sh.merge_blocks = (Hkv * G * sh.T_max + kMergeRows - 1) / kMergeRows;
   sh.need = workspace_bytes(sh.T_max, Hq, Hkv, cap);
   *out = sh;
   return ENTMTP_OK;
@@ -870,7 +905,7 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
   launch_attend(a, sh.items, s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
-  hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(HD), 0, s, a);
+  hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
   return launch_status("tree_attn merge launch");
 }
 
