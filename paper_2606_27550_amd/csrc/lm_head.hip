@@ -27,6 +27,11 @@
 //    through wave shuffles and the wave's own transposition tile, and a small
 //    kernel merges a node's partials (stats.hpp), so logits never need to
 //    reach memory.
+//  * each k-step's A and B fragments are read from LDS one step ahead of
+//    their products, so the LDS latency hides behind the MFMAs;
+//  * 64- and 128-node tiles give each wave two 16-row W tiles (a workgroup
+//    takes two consecutive slices), so every X fragment read from LDS feeds
+//    two products.
 // Node tiles of 16, 32, 64 or 128 nodes select the instantiation; variants
 // loop a workgroup over several slices (one workgroup per CU, leaving room for
 // concurrent attention) or read the node count from device memory (trees
@@ -391,6 +396,9 @@ __global__ __launch_bounds__(kL3Threads) void lm_head_lds_kernel(
 // probability 1/Z and argmax.
 // ---------------------------------------------------------------------------
 constexpr int kHybWaves = 4;                        // 64 rows per workgroup slice
+// 64- and 128-node tiles: two W tiles per wave (slices paired per
+// workgroup), X ring depth 4 and 2 (the 128-node X stage is 32 KB)
+constexpr int kHybW4 = 2, kHybS4 = 4, kHybW8 = 2, kHybS8 = 2;
 constexpr int kHybThreads = 64 * kHybWaves;
 
 // X stage split for the hybrid kernel (four waves share the copies)
@@ -412,7 +420,7 @@ struct HybShape {
 // NCH * 128 when NCH > 0 (the K loop is then unrolled completely: no
 // loop-carried stage registers, so the compiler's load bookkeeping stays
 // exact and it never drains the pipeline).
-template <int NT, int S, int NCH, bool STATS>
+template <int NT, int S, int NCH, bool STATS, int WT = 1>
 __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8_t* xslot2,
                                          uint8_t* xslot3, uint8_t* tpose,
                                          const uint16_t* __restrict__ X,
@@ -421,20 +429,31 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
                                          StatPart* __restrict__ part, int j0, int sl) {
   using Sh = HybShape<NT>;
   static_assert(S >= 2 && S <= 4, "two to four X ring slots");
+  static_assert(WT == 1 || WT == 2, "one or two W tiles per wave");
   uint8_t* const xring[4] = {xslot0, xslot1, xslot2, xslot3};
 
-  const int r0 = slice_begin(sl, G, V);
-  const int r1 = slice_begin(sl + 1, G, V);
-  if (r0 >= r1) {  // empty slice (tiny V): the whole workgroup leaves
+  // a workgroup takes WT consecutive slices (sl is the first slice / WT)
+  const int r0 = slice_begin(WT * sl, G, V);
+  const int r1 = slice_begin(WT * sl + WT, G, V);
+  if (r0 >= r1) {  // empty slices (tiny V): the whole workgroup leaves
     if constexpr (STATS)
       if (threadIdx.x < Sh::TP && j0 + threadIdx.x < T)
-        part[static_cast<size_t>(j0 + threadIdx.x) * G + sl] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
+#pragma unroll
+        for (int u = 0; u < WT; ++u)
+          part[static_cast<size_t>(j0 + threadIdx.x) * G + WT * sl + u] =
+              StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
     return;
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
   const int lr = lane & 15, lg = lane >> 4;
-  const int tile0 = r0 + 16 * wave;
-  const bool live = tile0 < r1;
+  // wave w owns the 16-row tiles w, w + 4 (when WT = 2) of the rows [r0, r1)
+  int tile0[WT];
+  bool live[WT];
+#pragma unroll
+  for (int t = 0; t < WT; ++t) {
+    tile0[t] = r0 + 16 * (wave + kHybWaves * t);
+    live[t] = tile0[t] < r1;
+  }
   const int nch = NCH > 0 ? NCH : hid / kL3Bk;
   // workgroups walk K in rotated order so that CUs do not all stream the
   // same column band at once
@@ -442,13 +461,15 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
 
   // W: instruction i, lane l -> row 4i + l/16, chunk l%16 (rows past the
   // slice read an in-bounds row of this slice; their outputs are not stored)
-  const uint16_t* wsrc[4];
+  const uint16_t* wsrc[WT][4];
 #pragma unroll
-  for (int i = 0; i < 4; ++i) {
-    const int rr = 4 * i + (lane >> 4);
-    const int row = tile0 + rr < r1 ? tile0 + rr : (live ? tile0 : r0);
-    wsrc[i] = W + static_cast<size_t>(row) * hid + 8 * (lane & 15);
-  }
+  for (int t = 0; t < WT; ++t)
+#pragma unroll
+    for (int i = 0; i < 4; ++i) {
+      const int rr = 4 * i + (lane >> 4);
+      const int row = tile0[t] + rr < r1 ? tile0[t] + rr : (live[t] ? tile0[t] : r0);
+      wsrc[t][i] = W + static_cast<size_t>(row) * hid + 8 * (lane & 15);
+    }
   // X: copy instruction n fills stage rows 4n..4n+3, lane p of row r fetching
   // chunk p ^ r; with fewer distinct instructions than waves (NT = 1) extra
   // waves repeat one (identical bytes to identical addresses)
@@ -463,40 +484,64 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
     xoff[q] = n * Sh::RPI * kL3RowBytes;
   }
 
-  u32x4 wbuf[S][4];
+  u32x4 wbuf[S][WT][4];
   // issue stage `stage` (clamped by the caller) into ring slot k
-  auto load = [&](u32x4 (&w)[4], uint8_t* xslot, int stage) {
+  auto load = [&](u32x4 (&w)[WT][4], uint8_t* xslot, int stage) {
     int ks = stage + rot;
     ks = ks >= nch ? ks - nch : ks;
     const int koff = ks * kL3Bk;
 #pragma unroll
     for (int q = 0; q < Sh::XI; ++q) lds_dma16(xsrc[q] + koff, xslot + xoff[q]);
 #pragma unroll
-    for (int i = 0; i < 4; ++i)
-      w[i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wsrc[i] + koff));
+    for (int t = 0; t < WT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i)
+        w[t][i] = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(wsrc[t][i] + koff));
   };
 
-  f32x4 acc[NT];
+  f32x4 acc[WT][NT];
 #pragma unroll
-  for (int n = 0; n < NT; ++n) acc[n] = f32x4{0.f, 0.f, 0.f, 0.f};
-  uint8_t* tp = tpose + wave * kL3TileBytes;
-  auto compute = [&](const u32x4 (&w)[4], const uint8_t* xs) {
+  for (int t = 0; t < WT; ++t)
 #pragma unroll
-    for (int i = 0; i < 4; ++i) {
-      const int r = 4 * i + lg;
-      *reinterpret_cast<u32x4*>(tp + r * kL3RowBytes + ((lr ^ r) << 4)) = w[i];
-    }
+    for (int n = 0; n < NT; ++n) acc[t][n] = f32x4{0.f, 0.f, 0.f, 0.f};
+  uint8_t* tp = tpose + wave * WT * kL3TileBytes;
+  // each X fragment read from LDS feeds the WT tiles' products
+  auto compute = [&](const u32x4 (&w)[WT][4], const uint8_t* xs) {
+#pragma unroll
+    for (int t = 0; t < WT; ++t)
+#pragma unroll
+      for (int i = 0; i < 4; ++i) {
+        const int r = 4 * i + lg;
+        *reinterpret_cast<u32x4*>(tp + t * kL3TileBytes + r * kL3RowBytes + ((lr ^ r) << 4)) = w[t][i];
+      }
     asm volatile("" ::: "memory");   // the tile's stores precede its reads
+    // operand fragments of k-step s (32 k): A from the wave's tiles, B from
+    // the X stage; the next step's fragments are read while this step's
+    // products run, so the LDS latency hides behind the MFMAs
+    bf16x8 fa[2][WT], fb[2][NT];
+    auto fetch = [&](int s, int buf) {
+      const int ch = 4 * s + lg;
+#pragma unroll
+      for (int t = 0; t < WT; ++t)
+        fa[buf][t] = as_bf16x8(*reinterpret_cast<const u32x4*>(tp + t * kL3TileBytes + lr * kL3RowBytes +
+                                                              ((ch ^ lr) << 4)));
+#pragma unroll
+      for (int n = 0; n < NT; ++n)
+        fb[buf][n] = as_bf16x8(*reinterpret_cast<const u32x4*>(xs + (n * 16 + lr) * kL3RowBytes +
+                                                              ((ch ^ lr) << 4)));
+    };
+    fetch(0, 0);
 #pragma unroll
     for (int s = 0; s < kL3Bk / 32; ++s) {
-      const int ch = 4 * s + lg;
-      const bf16x8 a = as_bf16x8(*reinterpret_cast<const u32x4*>(tp + lr * kL3RowBytes + ((ch ^ lr) << 4)));
+      if (s + 1 < kL3Bk / 32) fetch(s + 1, (s + 1) & 1);
+      // keep the scheduler from sinking the reads back to their uses
+      __builtin_amdgcn_sched_barrier(0);
 #pragma unroll
-      for (int n = 0; n < NT; ++n) {
-        const bf16x8 b = as_bf16x8(*reinterpret_cast<const u32x4*>(
-            xs + (n * 16 + lr) * kL3RowBytes + ((ch ^ lr) << 4)));
-        acc[n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(a, b, acc[n], 0, 0, 0);
-      }
+      for (int n = 0; n < NT; ++n)
+#pragma unroll
+        for (int t = 0; t < WT; ++t)
+          acc[t][n] = __builtin_amdgcn_mfma_f32_16x16x32_bf16(fa[s & 1][t], fb[s & 1][n], acc[t][n], 0, 0, 0);
+      __builtin_amdgcn_sched_barrier(0);
     }
     asm volatile("" ::: "memory");   // and the next stage's stores follow them
   };
@@ -512,7 +557,7 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
       // this wave's loads of stage cc (its X share first, then its W
       // registers) are done once only the S-2 later stages remain in flight;
       // its LDS reads of stage cc-1 are done too (lgkmcnt(0))
-      wait_vmcnt<(S - 2) * (Sh::XI + 4)>();
+      wait_vmcnt<(S - 2) * (Sh::XI + 4 * WT)>();
       stage_barrier();                       // every wave's X share of stage cc has landed
       const int nx = cc + S - 1 < nch ? cc + S - 1 : nch - 1;
       load(wbuf[(k + S - 1) % S], xring[(k + S - 1) % S], nx);
@@ -531,19 +576,26 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
   wait_vmcnt<0>();   // no copy may land in LDS after the workgroup is gone
 
   const bool vec_ok = (V & 3) == 0;
-  const int v = tile0 + 4 * lg;
-  if (live && logits) {   // the statistics path may run without materialised logits
+  int vt[WT];   // first of the lane's four rows in tile t
 #pragma unroll
-    for (int n = 0; n < NT; ++n) {
-      const int node = j0 + n * 16 + lr;
-      if (node >= T) continue;
-      float* dst = logits + static_cast<size_t>(node) * V + v;
-      if (vec_ok && v + 3 < r1) {
-        *reinterpret_cast<f32x4*>(dst) = acc[n];
-      } else {
+  for (int t = 0; t < WT; ++t) vt[t] = tile0[t] + 4 * lg;
+  if (logits) {   // the statistics path may run without materialised logits
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (v + r < r1) dst[r] = acc[n][r];
+    for (int t = 0; t < WT; ++t) {
+      if (!live[t]) continue;
+      const int v = vt[t];
+#pragma unroll
+      for (int n = 0; n < NT; ++n) {
+        const int node = j0 + n * 16 + lr;
+        if (node >= T) continue;
+        float* dst = logits + static_cast<size_t>(node) * V + v;
+        if (vec_ok && v + 3 < r1) {
+          *reinterpret_cast<f32x4*>(dst) = acc[t][n];
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (v + r < r1) dst[r] = acc[t][n][r];
+        }
       }
     }
   }
@@ -559,22 +611,26 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
     for (int n = 0; n < NT; ++n) {
       StatPart p{-INFINITY, 0.f, 0.f, 0x7fffffff};
 #pragma unroll
-      for (int r = 0; r < 4; ++r)
-        if (live && v + r < r1) take_max(p.zmax, p.idx, acc[n][r], v + r);
+      for (int t = 0; t < WT; ++t)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (live[t] && vt[t] + r < r1) take_max(p.zmax, p.idx, acc[t][n][r], vt[t] + r);
 #pragma unroll
       for (int off = 16; off <= 32; off <<= 1)
         take_max(p.zmax, p.idx, __shfl_xor(p.zmax, off, 64), __shfl_xor(p.idx, off, 64));
       if (p.zmax != -INFINITY) {
         const float my = p.zmax * inv_temp;
 #pragma unroll
-        for (int r = 0; r < 4; ++r) {
-          if (live && v + r < r1) {
-            const float t = acc[n][r] * inv_temp - my;
-            const float e = expf(t);
-            p.Z += e;
-            if (e > 0.f) p.S += t * e;
+        for (int t = 0; t < WT; ++t)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (live[t] && vt[t] + r < r1) {
+              const float y = acc[t][n][r] * inv_temp - my;
+              const float e = expf(y);
+              p.Z += e;
+              if (e > 0.f) p.S += y * e;
+            }
           }
-        }
       }
 #pragma unroll
       for (int off = 16; off <= 32; off <<= 1) {
@@ -587,16 +643,21 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
     const int c = threadIdx.x;
     if (c < Sh::TP && j0 + c < T) {
       const StatPart* wpart = reinterpret_cast<const StatPart*>(tpose);
-      constexpr int kStride = kL3TileBytes / static_cast<int>(sizeof(StatPart));
+      constexpr int kStride = WT * kL3TileBytes / static_cast<int>(sizeof(StatPart));
       StatPart acc_p = wpart[c];
 #pragma unroll
       for (int w = 1; w < kHybWaves; ++w) part_merge(acc_p, wpart[w * kStride + c], inv_temp);
-      part[static_cast<size_t>(j0 + c) * G + sl] = acc_p;
+      // the workgroup's slices: the combined partial in the first, neutral
+      // partials in the others
+      part[static_cast<size_t>(j0 + c) * G + WT * sl] = acc_p;
+#pragma unroll
+      for (int u = 1; u < WT; ++u)
+        part[static_cast<size_t>(j0 + c) * G + WT * sl + u] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
     }
   }
 }
 
-template <int NT, int S, int NCH, bool STATS>
+template <int NT, int S, int NCH, bool STATS, int WT = 1>
 __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
     int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
@@ -605,9 +666,9 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
   __shared__ __attribute__((aligned(16))) uint8_t xslot2[S > 2 ? XSTAGE : 16];
   __shared__ __attribute__((aligned(16))) uint8_t xslot3[S > 3 ? XSTAGE : 16];
-  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
-  hyb_body<NT, S, NCH, STATS>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
-                              inv_temp, part, blockIdx.y * HybShape<NT>::TP, blockIdx.x);
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * WT * kL3TileBytes];
+  hyb_body<NT, S, NCH, STATS, WT>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V,
+                                  G, inv_temp, part, blockIdx.y * HybShape<NT>::TP, blockIdx.x);
 }
 
 // The same kernel with fewer workgroups than slices: workgroup b takes slices
@@ -746,7 +807,9 @@ int hyb_grid(int V) {
 
 // ev0 / ev1 (may be NULL) are recorded on the stream right before and after
 // the launch.
-template <int NT, int S, int NCH, bool STATS = false>
+// WT = 2 pairs consecutive slices in one workgroup (G / 2 workgroups; the
+// caller keeps that at least one per CU).
+template <int NT, int S, int NCH, bool STATS = false, int WT = 1>
 int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
                       hipStream_t s, float inv_temp = 1.f, StatPart* part = nullptr,
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
@@ -754,8 +817,8 @@ int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T
   const int passes = (T + NT * 16 - 1) / (NT * 16);
   if (ev0)
     if (int32_t rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord")) return rc;
-  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS>), dim3(G, passes), dim3(kHybThreads),
-                     0, s, X, W, logits, T, hid, V, G, inv_temp, part);
+  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS, WT>), dim3(G / WT, passes),
+                     dim3(kHybThreads), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
   if (int32_t rc = launch_status("verify_logits launch")) return rc;
   return ev1 ? hip_status(hipEventRecord(ev1, s), "hipEventRecord") : ENTMTP_OK;
 }
@@ -766,6 +829,9 @@ template <bool STATS>
 bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
                          hipStream_t s, float inv_temp, StatPart* part, int32_t* rc,
                          hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
+  // large node tiles pair slices per workgroup (each X fragment read from
+  // LDS then feeds two W tiles) when that still leaves a workgroup per CU
+  const bool pair = hyb_grid(V) >= 2 * device_cus();
   auto go = [&](auto nch) {
     constexpr int NCH = decltype(nch)::value;
     if (T <= 16)
@@ -773,9 +839,11 @@ bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, in
     else if (T <= 32)
       *rc = launch_lm_hyb<2, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
     else if (T <= 64)
-      *rc = launch_lm_hyb<4, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+      *rc = pair ? launch_lm_hyb<4, kHybS4, NCH, STATS, kHybW4>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1)
+                 : launch_lm_hyb<4, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
     else
-      *rc = launch_lm_hyb<8, 2, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+      *rc = pair ? launch_lm_hyb<8, kHybS8, NCH, STATS, kHybW8>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1)
+                 : launch_lm_hyb<8, 2, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
   };
   if (hid == 4096) {              // the 7B hidden size: K loop fully unrolled
     go(std::integral_constant<int, 32>{});
