@@ -62,7 +62,7 @@ def w7b():
     return synth.lm_head_weight(1, 32000, 4096)
 
 
-@pytest.mark.parametrize("T", [27, 128])
+@pytest.mark.parametrize("T", [27, 64, 100, 128])
 def test_verify_logits_7b_full(api, w7b, T):
     say("verify_logits 7b", T)
     X = synth.hidden_rows(1, T, 4096)
@@ -157,7 +157,8 @@ def run_fused(api, X, W, inv_temp=1.0):
 
 
 @pytest.mark.parametrize("T,hid,V", [(1, 512, 1), (3, 512, 63), (16, 1024, 4097), (27, 4096, 32000),
-                                     (33, 512, 1000), (64, 512, 777), (128, 4096, 32000),
+                                     (33, 512, 1000), (64, 512, 777), (64, 4096, 32000),
+                                     (100, 4096, 32000), (128, 4096, 32000),
                                      (129, 512, 260), (7, 264, 301), (300, 2048, 100)])
 def test_verify_logits_stats_fused(api, T, hid, V):
     say("verify_logits_stats", T, hid, V)
