@@ -48,7 +48,7 @@ def parse():
     ap.add_argument("--warmup", type=int, default=50)
     ap.add_argument("--workload", default="bank5_L2048_7b",
                     choices=["bank5_L2048_7b", "tree27_L256_7b", "tree64_L4096_7b_32layer",
-                             "tree128_L8192_13b"])
+                             "tree128_L8192_13b", "batch8_gqa_v128k"])
     ap.add_argument("--pool", type=int, default=32, help="distinct per-step input sets")
     ap.add_argument("--weight-copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -108,6 +108,9 @@ def main():
     torch.cuda.set_device(dev)
     lib = api.lib
 
+    if args.workload == "batch8_gqa_v128k":
+        run_batched(args, api, synth, torch, lib)
+        return
     wl = synth.WORKLOADS[args.workload]
     Hq, Hkv, d, hid, V = wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.hidden, wl.vocab
     trees = synth.workload_trees(wl)
@@ -385,6 +388,193 @@ def main():
         "next_rows": extras,
     }
     print(json.dumps(line), flush=True)
+
+
+def run_batched(args, api, synth, torch, lib):
+    """The batched verification step: 8 sequences, each with its own tree from
+    a 5-tree bank (8..128 nodes) and its own prefix (512..16384, growing), GQA
+    32:8, vocabulary 128256.  A step, in dependency order on one stream:
+    batched tree attention, the LM head with statistics over the
+    concatenated rows, batched greedy acceptance and compaction; then the
+    host reads every sequence's (accept length, s) and moves each sequence's
+    ladder.  The hidden rows of a step are gathered from a staged pool per
+    sequence (the model would hand them over contiguous), the draft tokens
+    written from pinned memory."""
+    dev = torch.device("cuda:0")
+    wl = synth.WORKLOADS["batch8_gqa_v128k"]
+    B, Hq, Hkv, d, hid, V = 8, wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.hidden, wl.vocab
+    trees = synth.workload_trees(wl)
+    bank = api.Bank(trees)
+    Ts, n_topo, Tmax, Dmax = bank.T, len(trees), max(bank.T), max(bank.D)
+    total = args.warmup + args.steps
+    lens0 = synth.batch_prefix_lens(wl.ident, B)
+    cap = int(lens0.max()) + total * (Dmax + 1) + Tmax + 64
+    scale, theta = 1.0 / math.sqrt(d), wl.rope_theta
+    bf = torch.bfloat16
+    gen = torch.Generator(device=dev)
+
+    def randn(shape, seed, std=1.0):
+        gen.manual_seed(seed)
+        return (torch.randn(shape, generator=gen, device=dev) * std).to(bf)
+
+    t0 = time.time()
+    W = randn((V, hid), 7001, wl.w_std)
+    kcs = [torch.zeros((Hkv, cap, d), dtype=bf, device=dev) for _ in range(B)]
+    vcs = [torch.zeros((Hkv, cap, d), dtype=bf, device=dev) for _ in range(B)]
+    for b in range(B):
+        kcs[b][:, : lens0[b]] = randn((Hkv, int(lens0[b]), d), 7100 + 2 * b)
+        vcs[b][:, : lens0[b]] = randn((Hkv, int(lens0[b]), d), 7101 + 2 * b)
+    # pool: per entry, attention rows for the largest batch, and per sequence
+    # slot 128 hidden rows with a confidence regime planted (lift ~ U[11, 18]
+    # high or U[0, 11] low, a two-state chain per slot) and their argmax
+    P = 8
+    rows_max = B * Tmax
+    g_np = np.random.default_rng(7)
+    hi = g_np.random(B) < 0.5
+    pool = []
+    lg = torch.empty((Tmax, V), dtype=torch.float32, device=dev)
+    amd = torch.empty(Tmax, dtype=torch.int32, device=dev)
+    for e in range(P):
+        ent = {"q": randn((rows_max, Hq, d), 7200 + 4 * e), "kt": randn((rows_max, Hkv, d), 7201 + 4 * e),
+               "vt": randn((rows_max, Hkv, d), 7202 + 4 * e), "x": [], "am": []}
+        for b in range(B):
+            if g_np.random() >= 0.9:
+                hi[b] = not hi[b]
+            delta = g_np.uniform(11.0, 18.0) if hi[b] else g_np.uniform(0.0, 11.0)
+            x = randn((Tmax, hid), 7300 + 16 * e + b).float()
+            spike = torch.from_numpy(g_np.integers(0, V, Tmax)).to(dev)
+            x += (delta / (hid * wl.w_std ** 2)) * W.index_select(0, spike).float()
+            x = x.to(bf)
+            api.verify_logits(x, W, lg)
+            api.logit_stats(lg, 1.0, None, None, amd)
+            ent["x"].append(x)
+            ent["am"].append(amd.cpu().numpy().copy())
+        ent["x_all"] = torch.cat(ent["x"])   # [B * Tmax, hid], slot b at rows b * Tmax
+        pool.append(ent)
+    del lg
+    parents = [np.asarray(t, np.int64) for t in trees]
+    u_tab = g_np.random((total, rows_max))
+    r_tab = g_np.integers(0, V, (total, rows_max)).astype(np.int32)
+    log(f"batched workload: B={B}, bank T={Ts}, prefix {lens0.min()}..{lens0.max()}, cap={cap}; "
+        f"staged in {time.time() - t0:.1f}s")
+
+    out = torch.empty((rows_max, Hq, d), dtype=bf, device=dev)
+    aws = torch.empty(api.tree_attn_batched_workspace(B, Tmax, Hq, Hkv, d, cap), dtype=torch.uint8,
+                      device=dev)
+    part = torch.empty(lib.entmtp_stats_partials_bytes(rows_max, hid, V), dtype=torch.uint8, device=dev)
+    H = torch.empty(rows_max, device=dev)
+    p1 = torch.empty(rows_max, device=dev)
+    am = torch.empty(rows_max, dtype=torch.int32, device=dev)
+    tok_h = torch.empty(rows_max, dtype=torch.int32, pin_memory=True)
+    idx_h = torch.empty(rows_max, dtype=torch.int64, pin_memory=True)
+    tok_d = torch.empty(rows_max, dtype=torch.int32, device=dev)
+    idx_d = torch.empty(rows_max, dtype=torch.int64, device=dev)
+    cap_path = Dmax + 1
+    acc = torch.zeros(B, dtype=torch.int32, device=dev)
+    bon = torch.zeros(B, dtype=torch.int32, device=dev)
+    best = torch.zeros(B, device=dev)
+    path = torch.full((B, cap_path), -1, dtype=torch.int32, device=dev)
+    res_h = torch.empty(2 * B, dtype=torch.int32, pin_memory=True)
+    res_d = torch.empty(2 * B, dtype=torch.int32, device=dev)
+    ev_lm = (torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
+    done = torch.cuda.Event()
+    P_ = ctypes.c_void_p
+    lens = lens0.astype(np.int64).copy()
+    rung = np.zeros(B, np.int64)
+    lm_us, trace = [], []
+
+    def step(t, timed_lm):
+        e = pool[t % P]
+        topo = [int(k) for k in rung]
+        offs = np.concatenate([[0], np.cumsum([Ts[k] for k in topo])])
+        R = int(offs[-1])
+        # draft tokens and the hidden-row gather for this batch layout
+        tok = tok_h.numpy()
+        idx = idx_h.numpy()
+        for b, k in enumerate(topo):
+            o, T = int(offs[b]), Ts[k]
+            par = parents[k]
+            am_b = e["am"][b]
+            u, r = u_tab[t, o:o + T], r_tab[t, o:o + T]
+            tk = np.where(u < wl.p_acc, am_b[np.maximum(par, 0)], r)
+            tk[0] = -1
+            tok[o:o + T] = tk
+            idx[o:o + T] = b * Tmax + np.arange(T)
+        tok_d[:R].copy_(tok_h[:R], non_blocking=True)
+        idx_d[:R].copy_(idx_h[:R], non_blocking=True)
+        x = e["x_all"].index_select(0, idx_d[:R])
+        api.tree_attn_batched(bank, topo, lens.tolist(), e["q"][:R], e["kt"][:R], e["vt"][:R], kcs,
+                              vcs, scale, theta, out[:R], aws)
+        if timed_lm:
+            ev_lm[0].record()
+        rc = lib.entmtp_verify_logits_partials(P_(x.data_ptr()), P_(W.data_ptr()), R, hid, V, 1.0, None,
+                                               P_(part.data_ptr()), part.numel(),
+                                               P_(torch.cuda.current_stream().cuda_stream))
+        if rc:
+            raise RuntimeError(api.last_error())
+        if timed_lm:
+            ev_lm[1].record()
+        api.stats_finalize(part, R, V, 1.0, H, p1, am)
+        api.accept_batched(bank, topo, tok_d, am, p1, acc, path, bon, best)
+        api.kv_compact_batched(path, acc, lens.tolist(), kcs, vcs)
+        res_d[:B].copy_(acc)
+        res_d[B:].copy_(best.view(torch.int32))
+        res_h.copy_(res_d, non_blocking=True)
+        done.record()
+        done.synchronize()
+        r_ = res_h.numpy()
+        a = r_[:B].astype(np.int64)
+        s = r_[B:].view(np.float32)
+        if timed_lm:
+            lm_us.append((R, ev_lm[0].elapsed_time(ev_lm[1]) * 1e3))
+        trace.append((R, int(a.sum()) + B))
+        np.add(lens, a + 1, out=lens)
+        for b in range(B):
+            rung[b] = api.ladder_next(int(rung[b]), n_topo, float(s[b]), 0.8, 0.6)
+
+    for t in range(args.warmup):
+        step(t, False)
+    trace.clear()
+    torch.cuda.synchronize()
+    gc.disable()
+    t_start = time.perf_counter()
+    for t in range(args.warmup, total):
+        step(t, (t - args.warmup) % args.event_every == 0)
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t_start
+    gc.enable()
+    K = args.steps
+    us = elapsed / K * 1e6
+    tokens = sum(n for _, n in trace)
+    rows_mean = float(np.mean([R for R, _ in trace]))
+    lm_mean = float(np.mean([u for _, u in lm_us]))
+    lm_rows = float(np.mean([R for R, _ in lm_us]))
+    lm_bytes = V * hid * 2
+    lm_flops = 2.0 * lm_rows * V * hid
+    log(f"{K} batched steps in {elapsed:.3f}s: {us:.1f} us/step, {tokens / elapsed:.0f} tokens/s, "
+        f"mean rows {rows_mean:.1f}, LM head {lm_mean:.1f} us at {lm_rows:.0f} rows")
+    line = {
+        "metric": METRIC, "value": round(K / elapsed, 2), "unit": "steps/s", "n_gpus": 1, "steps": K,
+        "warmup": args.warmup, "ms_per_step": round(elapsed / K * 1e3, 5), "us_per_step": round(us, 2),
+        "tokens_per_s": round(tokens / elapsed, 1), "higher_is_better": True, "scaling": "weak",
+        "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": wl.name, "batch": B, "heads": Hq, "kv_heads": Hkv, "head_dim": d,
+                   "hidden": hid, "vocab": V, "prefix_len_start": [int(x) for x in lens0],
+                   "bank_T": Ts, "mean_rows_per_step": round(rows_mean, 1),
+                   "mean_tokens_per_step": round(tokens / K, 3),
+                   "scheduler": "hysteretic ladder on=0.8 off=0.6 per sequence, on the host",
+                   "parallelism": "single GPU"},
+        "roofline": {"kernel": "LM head with statistics partials over the batch's rows",
+                     "bound": "hbm", "achieved": round(lm_bytes / lm_mean / 1e3, 1),
+                     "peak": HBM_PEAK_GBPS, "unit": "GB/s",
+                     "frac": round(lm_bytes / lm_mean / 1e3 / HBM_PEAK_GBPS, 4), "traffic": None,
+                     "avg_us": round(lm_mean, 2), "mean_rows": round(lm_rows, 1),
+                     "mfma_TFLOPs": round(lm_flops / lm_mean / 1e6, 1),
+                     "mfma_frac_bf16": round(lm_flops / lm_mean / 1e6 / 2500.0, 4),
+                     "timing": "HIP events around the LM-head launch of every n-th timed step"},
+        "cpu_baseline": None,
+    }
+    print(json.dumps(line))
 
 
 def next_rows(api, synth, W, pool, hid, V, dev, reps=50):

@@ -667,8 +667,15 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t xslot2[S > 2 ? XSTAGE : 16];
   __shared__ __attribute__((aligned(16))) uint8_t xslot3[S > 3 ? XSTAGE : 16];
   __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * WT * kL3TileBytes];
+  // 1-D grid over (slice group, pass, XCD): the passes of one slice share an
+  // XCD (dispatch is round-robin over 8 XCDs) and start together, so a W
+  // stage fetched from HBM by one of them is an L2 hit for the others
+  const int passes = (T + HybShape<NT>::TP - 1) / HybShape<NT>::TP;
+  const int bid = blockIdx.x, r = bid >> 3;
+  const int pass = r % passes, slice = (r / passes) * 8 + (bid & 7);
+  if (slice >= G / WT) return;
   hyb_body<NT, S, NCH, STATS, WT>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V,
-                                  G, inv_temp, part, blockIdx.y * HybShape<NT>::TP, blockIdx.x);
+                                  G, inv_temp, part, pass * HybShape<NT>::TP, slice);
 }
 
 // The same kernel with fewer workgroups than slices: workgroup b takes slices
@@ -815,9 +822,10 @@ int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T
                       hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
   const int G = hyb_grid(V);
   const int passes = (T + NT * 16 - 1) / (NT * 16);
+  const int groups = (G / WT + 7) / 8;   // slices in groups of 8, one per XCD
   if (ev0)
     if (int32_t rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord")) return rc;
-  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS, WT>), dim3(G / WT, passes),
+  hipLaunchKernelGGL((lm_head_hyb_kernel<NT, S, NCH, STATS, WT>), dim3(groups * passes * 8),
                      dim3(kHybThreads), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
   if (int32_t rc = launch_status("verify_logits launch")) return rc;
   return ev1 ? hip_status(hipEventRecord(ev1, s), "hipEventRecord") : ENTMTP_OK;
