@@ -660,11 +660,11 @@ def lm_head_traffic(Ts):
         return None
     per = {}
     for name, v in rec["per_variant"].items():
-        if not name.rstrip(">").endswith("true"):   # the timed kernel is the statistics variant
+        targs = [x.strip() for x in name.split("<")[1].rstrip(">").split(",")]
+        if targs[3] != "true":   # the timed kernel is the statistics variant <NT, S, NCH, STATS, ...>
             continue
         kernel = name.split("<")[0].split()[-1]
-        nt = int(name.split("<")[1].split(",")[0])
-        per[(kernel, nt)] = v["fetch_bytes"] + v["write_bytes"]
+        per[(kernel, int(targs[0]))] = v["fetch_bytes"] + v["write_bytes"]
     tot = 0.0
     for T in Ts:   # the step's launch: the loop kernel up to 32 nodes, the grid kernel above
         key = (("lm_head_hyb_loop_kernel", 1 if T <= 16 else 2) if T <= 32 else

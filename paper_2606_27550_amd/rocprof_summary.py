@@ -5,6 +5,11 @@
       <copy_fetch.csv> <copy_write.csv> <copy_bytes> <out.md> <out.json> "<commands>"
 
 ``stats`` turns a --kernel-trace --stats CSV into a markdown table.
+``counters`` averages a --pmc counter collection per kernel (name filter
+optional):
+
+  python -m paper_2606_27550_amd.rocprof_summary counters <counter_collection.csv> <out.md> "<command>" [filter]
+
 ``traffic`` turns FETCH_SIZE / WRITE_SIZE counter collections (KiB per
 dispatch) into HBM bytes per launch, scaled by what the same counters read for
 a plain device copy of known size, and records them together with the hash of
@@ -88,10 +93,33 @@ def traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes, ou
         f.write("\n")
 
 
+def counters(csv_path: str, out_md: str, command: str, match: str = "") -> None:
+    """Mean of every counter per kernel (kernels whose name contains `match`)."""
+    acc = collections.defaultdict(lambda: collections.defaultdict(list))
+    for r in csv.DictReader(open(csv_path)):
+        k = short(r["Kernel_Name"])
+        if match in k:
+            acc[k][r["Counter_Name"]].append(float(r["Counter_Value"]))
+    names = sorted({c for v in acc.values() for c in v})
+    lines = [f"# Counters per dispatch: `{command}`", "",
+             "Means over the dispatches of each kernel (rocprofv3 sums each counter over the",
+             "whole device).", "",
+             "| kernel | dispatches | " + " | ".join(names) + " |",
+             "|---|---:|" + "---:|" * len(names)]
+    for k in sorted(acc):
+        n = max(len(v) for v in acc[k].values())
+        cells = [f"{sum(acc[k][c]) / len(acc[k][c]):.4g}" if acc[k][c] else "" for c in names]
+        lines.append(f"| `{k}` | {n} | " + " | ".join(cells) + " |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4])
     elif sys.argv[1] == "traffic":
         traffic(*sys.argv[2:10])
+    elif sys.argv[1] == "counters":
+        counters(*sys.argv[2:6])
     else:
         sys.exit(__doc__)
