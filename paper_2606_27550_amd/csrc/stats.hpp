@@ -51,43 +51,102 @@ __device__ __forceinline__ StatPart shfl_part(const StatPart& p, int off) {
                   __shfl_xor(p.idx, off, 64)};
 }
 
-// Merges the G partials of one row with one wavefront in a fixed order --
-// lane l folds partials l, l + 64, l + 128, ... in turn, then a butterfly
-// over the 64 lanes -- so that every lane ends with the row's partial.  Every
-// kernel that finishes statistics merges this way, so their results agree
-// bit for bit.  Two rows at a time (b_row may be NULL): the loads of both are
-// issued before either is folded.
+// One wavefront merges the G partials of each of R rows (rows[r] NULL: no
+// row) in two steps: the row maximum and its lowest index first, then Z and S
+// rebased to that maximum -- one exponential per partial.  Lane l takes
+// partials l, l + 64, l + 128, ... in that order and a butterfly combines the
+// lanes, so the result does not depend on R or on the path below; every
+// kernel that finishes statistics merges this way and they agree bit for
+// bit.  Up to 512 partials per row the loads of all R rows are issued at
+// once and kept in registers (one round trip); longer rows are read twice.
+constexpr int kMergeRegParts = 8;   // partials per lane held in registers
+
+template <int R>
+__device__ __forceinline__ void merge_rows(const StatPart* const (&rows)[R], int G, float inv_temp,
+                                           StatPart (&out)[R]) {
+  const int lane = threadIdx.x & 63;
+  const StatPart kEmpty{-INFINITY, 0.f, 0.f, 0x7fffffff};
+  float m[R];
+  int mi[R];
+  float Z[R], S[R];
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+    m[r] = -INFINITY;
+    mi[r] = 0x7fffffff;
+    Z[r] = 0.f;
+    S[r] = 0.f;
+  }
+  // d <= 0; the hardware exponential (a few ulp) is far inside the 1e-3 bar
+  // of the statistics
+  auto add = [&](const StatPart& p, float my, float& z, float& sacc) {
+    if (p.zmax != -INFINITY) {
+      const float d = p.zmax * inv_temp - my;
+      const float f = __expf(d);
+      z += p.Z * f;
+      sacc += f * (p.S + d * p.Z);
+    }
+  };
+  auto max_butterfly = [&]() {
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int off = 32; off >= 1; off >>= 1)
+        take_max(m[r], mi[r], __shfl_xor(m[r], off, 64), __shfl_xor(mi[r], off, 64));
+  };
+  if (G <= 64 * kMergeRegParts) {
+    StatPart v[R][kMergeRegParts];
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int k = 0; k < kMergeRegParts; ++k) {
+        const int g = lane + 64 * k;
+        v[r][k] = (rows[r] && g < G) ? rows[r][g] : kEmpty;
+      }
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int k = 0; k < kMergeRegParts; ++k) take_max(m[r], mi[r], v[r][k].zmax, v[r][k].idx);
+    max_butterfly();
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (m[r] != -INFINITY) {
+        const float my = m[r] * inv_temp;
+#pragma unroll
+        for (int k = 0; k < kMergeRegParts; ++k) add(v[r][k], my, Z[r], S[r]);
+      }
+  } else {
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (rows[r])
+        for (int g = lane; g < G; g += 64) take_max(m[r], mi[r], rows[r][g].zmax, rows[r][g].idx);
+    max_butterfly();
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+      if (rows[r] && m[r] != -INFINITY) {
+        const float my = m[r] * inv_temp;
+        for (int g = lane; g < G; g += 64) add(rows[r][g], my, Z[r], S[r]);
+      }
+  }
+#pragma unroll
+  for (int r = 0; r < R; ++r) {
+#pragma unroll
+    for (int off = 32; off >= 1; off >>= 1) {
+      Z[r] += __shfl_xor(Z[r], off, 64);
+      S[r] += __shfl_xor(S[r], off, 64);
+    }
+    out[r] = StatPart{m[r], Z[r], S[r], mi[r]};
+  }
+}
+
+// Two rows (b_row may be NULL), as merge_rows.
 __device__ __forceinline__ void merge_rows_wave(const StatPart* __restrict__ a_row,
                                                 const StatPart* __restrict__ b_row, int G,
                                                 float inv_temp, StatPart& a, StatPart& b) {
-  const int lane = threadIdx.x & 63;
-  a = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
-  b = a;
-  int g = lane;
-  for (; g + 192 < G; g += 256) {
-    StatPart ra[4], rb[4];
-#pragma unroll
-    for (int k = 0; k < 4; ++k) ra[k] = a_row[g + 64 * k];
-    if (b_row) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) rb[k] = b_row[g + 64 * k];
-    }
-#pragma unroll
-    for (int k = 0; k < 4; ++k) part_merge(a, ra[k], inv_temp);
-    if (b_row) {
-#pragma unroll
-      for (int k = 0; k < 4; ++k) part_merge(b, rb[k], inv_temp);
-    }
-  }
-  for (; g < G; g += 64) {
-    part_merge(a, a_row[g], inv_temp);
-    if (b_row) part_merge(b, b_row[g], inv_temp);
-  }
-#pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    part_merge(a, shfl_part(a, off), inv_temp);
-    part_merge(b, shfl_part(b, off), inv_temp);
-  }
+  const StatPart* rows[2] = {a_row, b_row};
+  StatPart o[2];
+  merge_rows<2>(rows, G, inv_temp, o);
+  a = o[0];
+  b = o[1];
 }
 
 // A merged row's statistics: entropy ln Z - S / Z and top-1 probability 1 / Z.
@@ -95,7 +154,7 @@ __device__ __forceinline__ float part_entropy(const StatPart& p) { return logf(p
 __device__ __forceinline__ float part_top1p(const StatPart& p) { return 1.f / p.Z; }
 
 // The statistics of nodes 0..T-1 by one workgroup of NTH threads, one
-// wavefront per node (two nodes per pass), written to the outputs (each may
+// wavefront per node (four nodes per pass), written to the outputs (each may
 // be NULL) and, for the workgroup's own later use, to LDS arrays s_top1p and
 // s_argmax (may be NULL).  The caller synchronises the workgroup before
 // reading the LDS arrays.
@@ -105,24 +164,29 @@ __device__ __forceinline__ void finalize_nodes(const StatPart* __restrict__ part
                                                float* __restrict__ top1p, int* __restrict__ argmax,
                                                float* s_top1p, int* s_argmax) {
   constexpr int NW = NTH / 64;
+  // rows per wavefront per pass (their loads go out together); one in a
+  // 1024-thread workgroup, whose lanes have 128 registers
+  constexpr int R = NTH >= 1024 ? 1 : 4;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
-  for (int n0 = w; n0 < T; n0 += 2 * NW) {
-    const int n1 = n0 + NW;
-    StatPart a, b;
-    merge_rows_wave(part + static_cast<size_t>(n0) * G,
-                    n1 < T ? part + static_cast<size_t>(n1) * G : nullptr, G, inv_temp, a, b);
+  for (int n0 = w; n0 < T; n0 += R * NW) {
+    const StatPart* rows[R];
+#pragma unroll
+    for (int r = 0; r < R; ++r) {
+      const int n = n0 + r * NW;
+      rows[r] = n < T ? part + static_cast<size_t>(n) * G : nullptr;
+    }
+    StatPart o[R];
+    merge_rows<R>(rows, G, inv_temp, o);
     if (lane == 0) {
-      if (entropy) entropy[n0] = part_entropy(a);
-      if (top1p) top1p[n0] = part_top1p(a);
-      if (argmax) argmax[n0] = a.idx;
-      if (s_top1p) s_top1p[n0] = part_top1p(a);
-      if (s_argmax) s_argmax[n0] = a.idx;
-      if (n1 < T) {
-        if (entropy) entropy[n1] = part_entropy(b);
-        if (top1p) top1p[n1] = part_top1p(b);
-        if (argmax) argmax[n1] = b.idx;
-        if (s_top1p) s_top1p[n1] = part_top1p(b);
-        if (s_argmax) s_argmax[n1] = b.idx;
+#pragma unroll
+      for (int r = 0; r < R; ++r) {
+        const int n = n0 + r * NW;
+        if (n >= T) break;
+        if (entropy) entropy[n] = part_entropy(o[r]);
+        if (top1p) top1p[n] = part_top1p(o[r]);
+        if (argmax) argmax[n] = o[r].idx;
+        if (s_top1p) s_top1p[n] = part_top1p(o[r]);
+        if (s_argmax) s_argmax[n] = o[r].idx;
       }
     }
   }
