@@ -779,7 +779,7 @@ __global__ __launch_bounds__(64 * kFinNodes) void stats_finalize_kernel(
   const int node = blockIdx.x * kFinNodes + (threadIdx.x >> 6);
   if (node >= T) return;   // whole wavefronts
   StatPart a, b;
-  merge_rows_wave(part + static_cast<size_t>(node) * G, nullptr, G, inv_temp, a, b);
+  merge_rows_wave(part, node, -1, G, inv_temp, a, b);
   if ((threadIdx.x & 63) == 0) {
     if (entropy) entropy[node] = part_entropy(a);
     if (top1p) top1p[node] = part_top1p(a);

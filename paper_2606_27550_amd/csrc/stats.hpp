@@ -51,8 +51,8 @@ __device__ __forceinline__ StatPart shfl_part(const StatPart& p, int off) {
                   __shfl_xor(p.idx, off, 64)};
 }
 
-// One wavefront merges the G partials of each of R rows (rows[r] NULL: no
-// row) in two steps: the row maximum and its lowest index first, then Z and S
+// One wavefront merges the G partials of each of R rows of part (row[r] < 0:
+// no row; row[0] is a row) in two steps: the row maximum and its lowest index first, then Z and S
 // rebased to that maximum -- one exponential per partial.  Lane l takes
 // partials l, l + 64, l + 128, ... in that order and a butterfly combines the
 // lanes, so the result does not depend on R or on the path below; every
@@ -61,51 +61,85 @@ __device__ __forceinline__ StatPart shfl_part(const StatPart& p, int off) {
 // once and kept in registers (one round trip); longer rows are read twice.
 constexpr int kMergeRegParts = 8;   // partials per lane held in registers
 
+// (z, index) as one key whose unsigned order is take_max's order: larger z
+// first, then the lower index (-0 is taken as +0, as take_max compares them
+// equal).  The row maximum is then a max over 64-bit keys, branch-free.
+__device__ __forceinline__ unsigned long long max_key(float z, int idx) {
+  uint32_t u = __float_as_uint(z + 0.f);
+  u = (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+  return (static_cast<unsigned long long>(u) << 32) | (0xffffffffu - static_cast<uint32_t>(idx));
+}
+
+__device__ __forceinline__ void key_parts(unsigned long long key, float& z, int& idx) {
+  const uint32_t u = static_cast<uint32_t>(key >> 32);
+  z = __uint_as_float((u & 0x80000000u) ? (u ^ 0x80000000u) : ~u);
+  idx = static_cast<int>(0xffffffffu - static_cast<uint32_t>(key));
+}
+
+__device__ __forceinline__ unsigned long long key_max(unsigned long long a, unsigned long long b) {
+  return a > b ? a : b;
+}
+
 template <int R>
-__device__ __forceinline__ void merge_rows(const StatPart* const (&rows)[R], int G, float inv_temp,
-                                           StatPart (&out)[R]) {
+__device__ __forceinline__ void merge_rows(const StatPart* __restrict__ part, const int (&row)[R],
+                                           int G, float inv_temp, StatPart (&out)[R]) {
   const int lane = threadIdx.x & 63;
   const StatPart kEmpty{-INFINITY, 0.f, 0.f, 0x7fffffff};
+  const unsigned long long kEmptyKey = max_key(-INFINITY, 0x7fffffff);
+  unsigned long long key[R];
   float m[R];
   int mi[R];
   float Z[R], S[R];
 #pragma unroll
   for (int r = 0; r < R; ++r) {
-    m[r] = -INFINITY;
-    mi[r] = 0x7fffffff;
+    key[r] = kEmptyKey;
     Z[r] = 0.f;
     S[r] = 0.f;
   }
   // d <= 0; the hardware exponential (a few ulp) is far inside the 1e-3 bar
-  // of the statistics
+  // of the statistics.  Branch-free: an empty partial adds zeros.
   auto add = [&](const StatPart& p, float my, float& z, float& sacc) {
-    if (p.zmax != -INFINITY) {
-      const float d = p.zmax * inv_temp - my;
-      const float f = __expf(d);
-      z += p.Z * f;
-      sacc += f * (p.S + d * p.Z);
-    }
+    const bool live = p.zmax != -INFINITY;
+    const float d = live ? p.zmax * inv_temp - my : 0.f;
+    const float f = live ? __expf(d) : 0.f;
+    z += p.Z * f;
+    sacc += f * (p.S + d * p.Z);
   };
   auto max_butterfly = [&]() {
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+    for (int off = 32; off >= 1; off >>= 1)
 #pragma unroll
-      for (int off = 32; off >= 1; off >>= 1)
-        take_max(m[r], mi[r], __shfl_xor(m[r], off, 64), __shfl_xor(mi[r], off, 64));
+      for (int r = 0; r < R; ++r) {
+        const uint32_t hi = __shfl_xor(static_cast<uint32_t>(key[r] >> 32), off, 64);
+        const uint32_t lo = __shfl_xor(static_cast<uint32_t>(key[r]), off, 64);
+        key[r] = key_max(key[r], (static_cast<unsigned long long>(hi) << 32) | lo);
+      }
+#pragma unroll
+    for (int r = 0; r < R; ++r) key_parts(key[r], m[r], mi[r]);
   };
   if (G <= 64 * kMergeRegParts) {
+    // unconditional loads addressed from the kernel's own pointer (clamped
+    // to an existing row and partial), so the compiler issues them back to
+    // back as global loads; entries past the row read as empty
     StatPart v[R][kMergeRegParts];
 #pragma unroll
-    for (int r = 0; r < R; ++r)
+    for (int r = 0; r < R; ++r) {
+      const StatPart* src = part + static_cast<size_t>(row[r] >= 0 ? row[r] : row[0]) * G;
 #pragma unroll
       for (int k = 0; k < kMergeRegParts; ++k) {
         const int g = lane + 64 * k;
-        v[r][k] = (rows[r] && g < G) ? rows[r][g] : kEmpty;
+        v[r][k] = src[g < G ? g : 0];
       }
+    }
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int k = 0; k < kMergeRegParts; ++k) take_max(m[r], mi[r], v[r][k].zmax, v[r][k].idx);
+      for (int k = 0; k < kMergeRegParts; ++k)
+        if (row[r] < 0 || lane + 64 * k >= G) v[r][k] = kEmpty;
+#pragma unroll
+    for (int r = 0; r < R; ++r)
+#pragma unroll
+      for (int k = 0; k < kMergeRegParts; ++k) key[r] = key_max(key[r], max_key(v[r][k].zmax, v[r][k].idx));
     max_butterfly();
 #pragma unroll
     for (int r = 0; r < R; ++r)
@@ -117,14 +151,17 @@ __device__ __forceinline__ void merge_rows(const StatPart* const (&rows)[R], int
   } else {
 #pragma unroll
     for (int r = 0; r < R; ++r)
-      if (rows[r])
-        for (int g = lane; g < G; g += 64) take_max(m[r], mi[r], rows[r][g].zmax, rows[r][g].idx);
+      if (row[r] >= 0) {
+        const StatPart* src = part + static_cast<size_t>(row[r]) * G;
+        for (int g = lane; g < G; g += 64) key[r] = key_max(key[r], max_key(src[g].zmax, src[g].idx));
+      }
     max_butterfly();
 #pragma unroll
     for (int r = 0; r < R; ++r)
-      if (rows[r] && m[r] != -INFINITY) {
+      if (row[r] >= 0 && m[r] != -INFINITY) {
+        const StatPart* src = part + static_cast<size_t>(row[r]) * G;
         const float my = m[r] * inv_temp;
-        for (int g = lane; g < G; g += 64) add(rows[r][g], my, Z[r], S[r]);
+        for (int g = lane; g < G; g += 64) add(src[g], my, Z[r], S[r]);
       }
   }
 #pragma unroll
@@ -138,13 +175,13 @@ __device__ __forceinline__ void merge_rows(const StatPart* const (&rows)[R], int
   }
 }
 
-// Two rows (b_row may be NULL), as merge_rows.
-__device__ __forceinline__ void merge_rows_wave(const StatPart* __restrict__ a_row,
-                                                const StatPart* __restrict__ b_row, int G,
-                                                float inv_temp, StatPart& a, StatPart& b) {
-  const StatPart* rows[2] = {a_row, b_row};
+// Rows a and b of part (b < 0: none), as merge_rows.
+__device__ __forceinline__ void merge_rows_wave(const StatPart* __restrict__ part, int a_row,
+                                                int b_row, int G, float inv_temp, StatPart& a,
+                                                StatPart& b) {
+  const int rows[2] = {a_row, b_row};
   StatPart o[2];
-  merge_rows<2>(rows, G, inv_temp, o);
+  merge_rows<2>(part, rows, G, inv_temp, o);
   a = o[0];
   b = o[1];
 }
@@ -169,14 +206,14 @@ __device__ __forceinline__ void finalize_nodes(const StatPart* __restrict__ part
   constexpr int R = NTH >= 1024 ? 1 : 4;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int n0 = w; n0 < T; n0 += R * NW) {
-    const StatPart* rows[R];
+    int rows[R];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const int n = n0 + r * NW;
-      rows[r] = n < T ? part + static_cast<size_t>(n) * G : nullptr;
+      rows[r] = n < T ? n : -1;
     }
     StatPart o[R];
-    merge_rows<R>(rows, G, inv_temp, o);
+    merge_rows<R>(part, rows, G, inv_temp, o);
     if (lane == 0) {
 #pragma unroll
       for (int r = 0; r < R; ++r) {
