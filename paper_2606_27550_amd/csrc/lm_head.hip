@@ -731,7 +731,7 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_dyn_small_kernel(
   }
 }
 
-template <int NCH>
+template <int NCH, int WT>
 __global__ __launch_bounds__(kHybThreads) void lm_head_dyn_large_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
     const int* __restrict__ T_dev, int hid, int V, int G, float inv_temp,
@@ -739,11 +739,11 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_dyn_large_kernel(
   constexpr int XSTAGE = HybShape<8>::TP * kL3RowBytes;
   __shared__ __attribute__((aligned(16))) uint8_t xslot0[XSTAGE];
   __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
-  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * WT * kL3TileBytes];
   const int T = __builtin_amdgcn_readfirstlane(*T_dev);
   if (T > 32)
-    hyb_body<8, 2, NCH, true>(xslot0, xslot1, xslot0, xslot1, tpose, X, W, logits, T, hid, V, G,
-                              inv_temp, part, 0, blockIdx.x);
+    hyb_body<8, 2, NCH, true, WT>(xslot0, xslot1, xslot0, xslot1, tpose, X, W, logits, T, hid, V,
+                                  G, inv_temp, part, 0, blockIdx.x);
 }
 
 // Largest vocabulary slice slice_begin() produces for G workgroups (host copy
@@ -940,6 +940,10 @@ int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w
   auto* part = static_cast<StatPart*>(partials);
   const auto* X = reinterpret_cast<const uint16_t*>(hidden);
   const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
+  // the large kernel pairs slices per workgroup (as the host-sized one) when
+  // that leaves a workgroup per CU: half the workgroups to place when it has
+  // nothing to do
+  const int large_wt = G >= 2 * device_cus() ? 2 : 1;
   auto both = [&](auto small, auto large) -> int32_t {
     if (ev0)
       if (int32_t rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord")) return rc;
@@ -947,15 +951,20 @@ int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w
                        hid, V, G, inv_temp, part);
     if (int32_t rc = launch_status("verify_logits (device-sized, small) launch")) return rc;
     if (T_max > 32) {   // some bank tree needs the large kernel
-      hipLaunchKernelGGL(large, dim3(G), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev, hid, V, G,
-                         inv_temp, part);
+      hipLaunchKernelGGL(large, dim3(G / large_wt), dim3(kHybThreads), 0, s, X, W, nullptr, T_dev,
+                         hid, V, G, inv_temp, part);
       if (int32_t rc = launch_status("verify_logits (device-sized, large) launch")) return rc;
     }
     return ev1 ? hip_status(hipEventRecord(ev1, s), "hipEventRecord") : ENTMTP_OK;
   };
-  if (hid == 32 * kL3Bk) return both(lm_head_dyn_small_kernel<32>, lm_head_dyn_large_kernel<32>);
-  if (hid == 40 * kL3Bk) return both(lm_head_dyn_small_kernel<40>, lm_head_dyn_large_kernel<40>);
-  return both(lm_head_dyn_small_kernel<0>, lm_head_dyn_large_kernel<0>);
+  if (hid == 32 * kL3Bk)
+    return large_wt == 2 ? both(lm_head_dyn_small_kernel<32>, lm_head_dyn_large_kernel<32, 2>)
+                         : both(lm_head_dyn_small_kernel<32>, lm_head_dyn_large_kernel<32, 1>);
+  if (hid == 40 * kL3Bk)
+    return large_wt == 2 ? both(lm_head_dyn_small_kernel<40>, lm_head_dyn_large_kernel<40, 2>)
+                         : both(lm_head_dyn_small_kernel<40>, lm_head_dyn_large_kernel<40, 1>);
+  return large_wt == 2 ? both(lm_head_dyn_small_kernel<0>, lm_head_dyn_large_kernel<0, 2>)
+                       : both(lm_head_dyn_small_kernel<0>, lm_head_dyn_large_kernel<0, 1>);
 }
 
 int32_t launch_stats_finalize(const void* partials, int T, int V, float inv_temp, float* entropy,
