@@ -56,6 +56,11 @@ __host__ __device__ inline int rows_padded(int G, int T) {
 // Workgroups along the query rows: groups of nt 32-row tiles.
 __host__ __device__ inline int query_groups(int nqt, int nt) { return (nqt + nt - 1) / nt; }
 
+// Query tiles per workgroup for one tree of a device-planned call: two when
+// its rows per KV head pass one tile (each tree goes to the kernel instance
+// made for it).
+__host__ __device__ inline int tree_tiles(int G, int T) { return G * T > kQTile ? 2 : 1; }
+
 __host__ __device__ inline int split_bound(int nblocks) {
   int b = nblocks / kMinBlocksPerSplit;
   b = b < 1 ? 1 : b;
@@ -157,7 +162,7 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
   q.row0 = 0;
   q.rows_pad = rows_padded(p.G, q.T);
   q.nqt = q.rows_pad / kQTile;
-  q.nqg = query_groups(q.nqt, p.nt);
+  q.nqg = query_groups(q.nqt, tree_tiles(p.G, q.T));
   const int nblocks = (q.L + q.T + KB - 1) / KB;
   const int ns = t->splits[split_bound(nblocks)];   // = split_single(nblocks, Hkv * nqg, cus)
   q.bps = (nblocks + ns - 1) / ns;
@@ -242,6 +247,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
   const SeqPlan sq = resolve(p, b);
   if (sq.T == 0) return;
+  if (p.dev && tree_tiles(p.G, sq.T) != NT) return;   // the device's tree is the other instance's
   const int bid = blockIdx.x - sq.item0;
   const int qg = (bid >> 3) % sq.nqg;
   const int gc = ((bid >> 3) / sq.nqg) * 8 + (bid & 7);
@@ -660,13 +666,7 @@ void launch_attend(const BatchArgs& a, int items, hipStream_t s) {
     hipLaunchKernelGGL(tree_attn_kernel<1>, dim3(items), dim3(kAttnThreads), 0, s, a);
 }
 
-// Query tiles per workgroup of device-planned calls on a bank: two when some
-// topology has more than one tile.
-int device_tiles(const entmtp_bank* bank, int G) {
-  for (const TopoDesc& td : bank->desc)
-    if (rows_padded(G, td.T) > kQTile) return 2;
-  return 1;
-}
+
 
 int device_cus() {
   static int cus[64] = {0};
@@ -839,14 +839,15 @@ int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, Dev
   DevAttnShape sh;
   for (const TopoDesc& td : bank->desc) {
     sh.T_max = td.T > sh.T_max ? td.T : sh.T_max;
-    const int nqg = query_groups(rows_padded(G, td.T) / kQTile, device_tiles(bank, G));
+    const int nt = tree_tiles(G, td.T);
+    const int nqg = query_groups(rows_padded(G, td.T) / kQTile, nt);
     const int max_blocks = (cap + KB - 1) / KB;
     for (int nblocks = 1; nblocks <= max_blocks; ++nblocks) {
       const int ns0 = split_single(nblocks, Hkv * nqg, cus);
       const int bps = (nblocks + ns0 - 1) / ns0;
       const int ns = (nblocks + bps - 1) / bps;
       const int items = (Hkv * ns + 7) / 8 * 8 * nqg;
-      sh.items = items > sh.items ? items : sh.items;
+      sh.items[nt] = items > sh.items[nt] ? items : sh.items[nt];
     }
   }
   sh.rows = sh.T_max;
@@ -860,7 +861,7 @@ void attn_device_splits(const entmtp_bank* bank, int Hq, int Hkv, DevTopo* topos
   const int cus = device_cus();
   const int G = Hq / Hkv;
   for (size_t k = 0; k < bank->desc.size(); ++k) {
-    const int nqg = query_groups(rows_padded(G, bank->desc[k].T) / kQTile, device_tiles(bank, G));
+    const int nqg = query_groups(rows_padded(G, bank->desc[k].T) / kQTile, tree_tiles(G, bank->desc[k].T));
     topos[k].splits[0] = 1;
     for (int b = 1; b <= kMaxSplits; ++b)
       topos[k].splits[b] = static_cast<unsigned char>(split_for_bound(b, Hkv * nqg, cus));
@@ -877,7 +878,6 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   a.topos = topos;
   a.arena = bank->arena;
   a.cus = device_cus();
-  a.nt = device_tiles(bank, Hq / Hkv);
   a.B = 1;
   a.G = Hq / Hkv;
   a.Hq = Hq;
@@ -903,8 +903,14 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
   hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
   if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
-  launch_attend(a, sh.items, s);
-  if (int32_t rc = launch_status("tree_attn launch")) return rc;
+  // one instance per tile count among the bank's trees; the one not made for
+  // the device's tree leaves at once
+  for (int nt = 1; nt <= 2; ++nt) {
+    if (sh.items[nt] == 0) continue;
+    a.nt = nt;
+    launch_attend(a, sh.items[nt], s);
+    if (int32_t rc = launch_status("tree_attn launch")) return rc;
+  }
   hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
   return launch_status("tree_attn merge launch");
 }
