@@ -274,6 +274,8 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   __shared__ __attribute__((aligned(16))) uint8_t lds[kLdsBytes];
   __shared__ uint32_t s_mask[QR][ENTMTP_MASK_WORDS + 1];
   __shared__ float s_m[kAttnWaves][QR], s_l[kAttnWaves][QR];
+  __shared__ float s_sc[kAttnWaves][QR];   // each wave's factor to the common max
+  __shared__ float s_M[QR], s_L[QR];        // a row's common max and sum
   u32x4 (*s_qf)[8][64] = reinterpret_cast<u32x4 (*)[8][64]>(lds);   // [NT][s][lane]
   uint32_t* vt = reinterpret_cast<uint32_t*>(lds + kQfBytes + wave * kVtBytes);  // [HD][VT_LD/2]
 
@@ -519,14 +521,27 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
   }
   __syncthreads();
+  // per row, once: the common max, each wave's factor to it, and the sum
+  if (tid < QR) {
+    float M = -INFINITY;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][tid]);
+    float lsum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kAttnWaves; ++w) {
+      const float sc = (s_m[w][tid] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(s_m[w][tid] - M);
+      s_sc[w][tid] = sc;
+      lsum += s_l[w][tid] * sc;
+    }
+    s_M[tid] = M;
+    s_L[tid] = lsum;
+  }
+  __syncthreads();
   float* ored = reinterpret_cast<float*>(lds);  // [slot][query][OLD]
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
     if (t > 0 && !two) break;
-    float M = -INFINITY;
-#pragma unroll
-    for (int w = 0; w < kAttnWaves; ++w) M = fmaxf(M, s_m[w][t * kQTile + li]);
-    const float myscale = (m_run[t] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(m_run[t] - M);
+    const float myscale = s_sc[wave][t * kQTile + li];
     // lane (query li, half lh) holds dims 32ct + 8j + 4lh + i in o[t][ct][4j + i]
     auto slot_at = [&](int slot, int ct, int j) {
       return reinterpret_cast<float4*>(ored + (slot * kQTile + li) * OLD + 32 * ct + 8 * j + 4 * lh);
@@ -561,15 +576,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
       const int row = (qt0 + t) * kQTile + q;
       if (row >= GT) continue;
       const int sr = t * kQTile + q;
-      float Mq = -INFINITY;
-#pragma unroll
-      for (int w = 0; w < kAttnWaves; ++w) Mq = fmaxf(Mq, s_m[w][sr]);
-      float lsum = 0.f;
-#pragma unroll
-      for (int w = 0; w < kAttnWaves; ++w) {
-        const float sc = (s_m[w][sr] == -INFINITY) ? 0.f : __builtin_amdgcn_exp2f(s_m[w][sr] - Mq);
-        lsum += s_l[w][sr] * sc;
-      }
+      const float Mq = s_M[sr], lsum = s_L[sr];
       const float4 s0 = *reinterpret_cast<const float4*>(ored + q * OLD + d4);
       const float4 s1 = *reinterpret_cast<const float4*>(ored + (kQTile + q) * OLD + d4);
       const float4 os = make_float4(s0.x + s1.x, s0.y + s1.y, s0.z + s1.z, s0.w + s1.w);
