@@ -26,6 +26,10 @@
 //     Online softmax in fp32, base 2, with a lazily raised running max (the
 //     accumulators are rescaled only when a block's max passes the reference
 //     by more than 2^8).  The four waves merge in LDS.
+//     Trees with more than 64 query rows per KV head use a second kernel
+//     whose four waves own one query tile each and walk the same key blocks,
+//     staged once per workgroup in LDS, so a block is read once per 128 rows;
+//     it stays under 256 registers per lane, two workgroups per CU.
 //  3. merge: combines the splits' (max, sum, unnormalised output) partials.
 //     Skipped when a single split covers the keys.
 #include <cfloat>
@@ -56,10 +60,11 @@ __host__ __device__ inline int rows_padded(int G, int T) {
 // Workgroups along the query rows: groups of nt 32-row tiles.
 __host__ __device__ inline int query_groups(int nqt, int nt) { return (nqt + nt - 1) / nt; }
 
-// Query tiles per workgroup for one tree of a device-planned call: two when
-// its rows per KV head pass one tile (each tree goes to the kernel instance
-// made for it).
-__host__ __device__ inline int tree_tiles(int G, int T) { return G * T > kQTile ? 2 : 1; }
+// Query tiles per workgroup for a tree: one, two (both in every wave) above
+// one tile of rows per KV head, four (one per wave) above two tiles.
+__host__ __device__ inline int tree_tiles(int G, int T) {
+  return G * T > 2 * kQTile ? 4 : (G * T > kQTile ? 2 : 1);
+}
 
 __host__ __device__ inline int split_bound(int nblocks) {
   int b = nblocks / kMinBlocksPerSplit;
@@ -86,6 +91,10 @@ __host__ __device__ inline int split_for_bound(int bound, int base_wg, int cus) 
   }
   return best;
 }
+
+// Workgroups of an instance resident per CU: two for the four-tile kernel
+// (under 256 registers per lane), one for the others.
+__host__ __device__ inline int wg_per_cu(int nt) { return nt == 4 ? 2 : 1; }
 
 __host__ __device__ inline int split_single(int nblocks, int base_wg, int cus) {
   return split_for_bound(split_bound(nblocks), base_wg, cus);
@@ -164,7 +173,7 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
   q.nqt = q.rows_pad / kQTile;
   q.nqg = query_groups(q.nqt, tree_tiles(p.G, q.T));
   const int nblocks = (q.L + q.T + KB - 1) / KB;
-  const int ns = t->splits[split_bound(nblocks)];   // = split_single(nblocks, Hkv * nqg, cus)
+  const int ns = t->splits[split_bound(nblocks)];   // = split_single(nblocks, Hkv * nqg, cus * wg_per_cu)
   q.bps = (nblocks + ns - 1) / ns;
   q.nsplit = (nblocks + q.bps - 1) / q.bps;
   q.item0 = 0;
@@ -599,6 +608,241 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   }
 }
 
+// Four query tiles per workgroup, one per wave (trees with more than 64
+// query rows per KV head): the four waves walk the same key blocks, which
+// the workgroup stages once in LDS -- K as rows, V transposed -- from
+// coalesced loads (16 lanes per 256-byte key row), double-buffered with one
+// barrier per block and two blocks in flight in registers, so a KV block is
+// read once per 128 query rows.  Each wave keeps its own tile's Q fragments,
+// softmax state and output, so no cross-wave merge is needed.
+constexpr int KROW = HD + 8;   // bf16 per staged K row (16-byte pad: rows 4 banks apart)
+
+__global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs p) {
+  const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
+  const SeqPlan sq = resolve(p, b);
+  if (sq.T == 0) return;
+  if (p.dev && tree_tiles(p.G, sq.T) != 4) return;   // the device's tree is another instance's
+  const int bid = blockIdx.x - sq.item0;
+  const int qg = (bid >> 3) % sq.nqg;
+  const int gc = ((bid >> 3) / sq.nqg) * 8 + (bid & 7);
+  if (gc >= p.Hkv * sq.nsplit) return;
+  const int g = gc / sq.nsplit, split = gc % sq.nsplit;
+  const int T = sq.T, L = sq.L, nkeys = sq.L + sq.T, rows_pad = sq.rows_pad;
+  const int nsplit = sq.nsplit;
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const int li = lane & 31, lh = lane >> 5;
+  const int GT = p.G * T;
+  const int qt = qg * 4 + wave;           // this wave's query tile
+  const bool live = qt < sq.nqt;          // (uniform per wave)
+  constexpr int QR = 4 * kQTile;
+
+  __shared__ __attribute__((aligned(16))) uint16_t s_k[2][KB][KROW];
+  __shared__ __attribute__((aligned(16))) uint32_t s_vt[2][HD * (VT_LD / 2)];
+  __shared__ uint32_t s_mask[QR][ENTMTP_MASK_WORDS + 1];
+
+  const size_t head_off = static_cast<size_t>(g) * p.cap * HD;
+  const uint16_t* kbase = sq.kc + head_off;
+  const uint16_t* vbase = sq.vc + head_off;
+  const float c = p.scale_log2;
+  const int nblocks = (nkeys + KB - 1) / KB;
+  const int blk_lo = split * sq.bps;
+  const int blk_hi = min(nblocks, blk_lo + sq.bps);
+  const int nb = blk_hi - blk_lo;
+
+  // cooperative loads of one block: K unit u = tid + 256 j -> key u / 16,
+  // 16-byte chunk u % 16; V unit tid -> key pair tid / 16, 8-dim chunk
+  // tid % 16 (both keys of the pair).  Keys past the end clamp to the last.
+  auto gload = [&](int i, u32x4 (&kr)[2], u32x4& va, u32x4& vb) {
+    const int kb = (blk_lo + min(i, nb - 1)) * KB;
+    const int last = nkeys - 1;
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int u = tid + kAttnThreads * j;
+      const int key = min(kb + (u >> 4), last);
+      kr[j] = *reinterpret_cast<const u32x4*>(kbase + static_cast<size_t>(key) * HD + 8 * (u & 15));
+    }
+    const int m = tid & 15, pp = tid >> 4;
+    const int k0 = min(kb + 2 * pp, last), k1 = min(kb + 2 * pp + 1, last);
+    va = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k0) * HD + 8 * m);
+    vb = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k1) * HD + 8 * m);
+  };
+  auto stage = [&](int buf, const u32x4 (&kr)[2], const u32x4& va, const u32x4& vb) {
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const int u = tid + kAttnThreads * j;
+      *reinterpret_cast<u32x4*>(&s_k[buf][u >> 4][8 * (u & 15)]) = kr[j];
+    }
+    const int m = tid & 15, pp = tid >> 4;
+    uint32_t* vt = s_vt[buf];
+#pragma unroll
+    for (int w = 0; w < 4; ++w) {
+      vt[(8 * m + 2 * w) * (VT_LD / 2) + pp] = __builtin_amdgcn_perm(vb[w], va[w], 0x05040100u);
+      vt[(8 * m + 2 * w + 1) * (VT_LD / 2) + pp] = __builtin_amdgcn_perm(vb[w], va[w], 0x07060302u);
+    }
+  };
+
+  u32x4 kA[2], kB[2], vaA, vbA, vaB, vbB;
+  gload(0, kA, vaA, vbA);
+  gload(1, kB, vaB, vbB);
+
+  // ancestor masks of the group's rows, and this wave's Q fragments
+  for (int u = tid; u < QR * ENTMTP_MASK_WORDS; u += kAttnThreads) {
+    const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
+    const int qrow = qg * QR + r;
+    s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+  }
+  u32x4 qf[8];
+  {
+    const int qrow = qt * kQTile + li;
+    const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD + 8 * lh;
+#pragma unroll
+    for (int s = 0; s < 8; ++s)
+      qf[s] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+  }
+  stage(0, kA, vaA, vbA);
+  gload(2, kA, vaA, vbA);
+  __syncthreads();
+
+  float m_run = -INFINITY, l_run = 0.f;
+  f32x16 o[4];
+#pragma unroll
+  for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+    for (int r = 0; r < 16; ++r) o[ct][r] = 0.f;
+
+  // block i of the split from LDS buffer buf: this wave's scores, softmax
+  // (lazily raised max, as in tree_attn_kernel) and P V
+  auto compute = [&](int i, int buf) {
+    if (!live) return;
+    const int kb = (blk_lo + i) * KB;
+    const bool plain = kb + KB <= L;
+    f32x16 sacc;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) sacc[r] = 0.f;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) {
+      const u32x4 kf = *reinterpret_cast<const u32x4*>(&s_k[buf][li][16 * s + 8 * lh]);
+      sacc = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(kf), as_bf16x8(qf[s]), sacc, 0, 0, 0);
+    }
+    float bmax = -INFINITY;
+    if (plain) {
+#pragma unroll
+      for (int r = 0; r < 16; ++r) bmax = fmaxf(bmax, sacc[r]);
+    } else {
+      uint32_t win = 0xFFFFFFFFu;
+      const int rel = kb - L;
+      const uint32_t* mrow = s_mask[wave * kQTile + li];
+      if (rel < 0) {
+        const int npre = -rel;
+        win = (0xFFFFFFFFu >> (32 - npre)) | (mrow[0] << npre);
+      } else {
+        const int wi = rel >> 5, sh = rel & 31;
+        const uint32_t lo = mrow[wi];
+        const uint32_t hi = wi + 1 < ENTMTP_MASK_WORDS ? mrow[wi + 1] : 0u;
+        win = sh ? (lo >> sh) | (hi << (32 - sh)) : lo;
+      }
+#pragma unroll
+      for (int r = 0; r < 16; ++r) {
+        const int n = 8 * (r >> 2) + 4 * lh + (r & 3);
+        const bool vis = ((win >> n) & 1u) && (kb + n < nkeys);
+        sacc[r] = vis ? sacc[r] : -INFINITY;
+        bmax = fmaxf(bmax, sacc[r]);
+      }
+    }
+    bmax = fmaxf(bmax, __shfl_xor(bmax, 32, 64));
+    const float mb = bmax * c;
+    const bool need = mb > m_run + kLazyLog2;
+    if (__any(need)) {
+      const float mn = need ? mb : m_run;
+      const float alpha = !need ? 1.f : (m_run == -INFINITY ? 0.f : __builtin_amdgcn_exp2f(m_run - mn));
+      l_run *= alpha;
+#pragma unroll
+      for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+        for (int r = 0; r < 16; ++r) o[ct][r] *= alpha;
+      m_run = mn;
+    }
+    const float mneg = m_run == -INFINITY ? 0.f : -m_run;
+    float pr[16];
+    float rsum = 0.f;
+#pragma unroll
+    for (int r = 0; r < 16; ++r) {
+      pr[r] = __builtin_amdgcn_exp2f(fmaf(sacc[r], c, mneg));
+      rsum += pr[r];
+    }
+    rsum += __shfl_xor(rsum, 32, 64);
+    l_run += rsum;
+    bf16x8 pf[2];
+#pragma unroll
+    for (int u = 0; u < 2; ++u) {
+      u32x4 w;
+#pragma unroll
+      for (int e = 0; e < 4; ++e)
+        w[e] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+                                               (f32x2{pr[8 * u + 2 * e], pr[8 * u + 2 * e + 1]}), bf16x2));
+      pf[u] = as_bf16x8(w);
+    }
+    const uint32_t* vt = s_vt[buf];
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct) {
+      const uint32_t* row = vt + (32 * ct + li) * (VT_LD / 2);
+#pragma unroll
+      for (int u = 0; u < 2; ++u) {
+        const uint2 x0 = *reinterpret_cast<const uint2*>(row + 8 * u + 2 * lh);
+        const uint2 x1 = *reinterpret_cast<const uint2*>(row + 8 * u + 4 + 2 * lh);
+        const u32x4 w = {x0.x, x0.y, x1.x, x1.y};
+        o[ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[u], o[ct], 0, 0, 0);
+      }
+    }
+  };
+
+  // block i computes from buffer i & 1 while block i + 1 is staged into the
+  // other buffer and block i + 3 streams into the freed registers
+  for (int i = 0;; i += 2) {
+    compute(i, 0);
+    if (i + 1 >= nb) break;
+    stage(1, kB, vaB, vbB);
+    gload(i + 3, kB, vaB, vbB);
+    __syncthreads();
+    compute(i + 1, 1);
+    if (i + 2 >= nb) break;
+    stage(0, kA, vaA, vbA);
+    gload(i + 4, kA, vaA, vbA);
+    __syncthreads();
+  }
+
+  // this wave's tile: the output (one split) or its partial
+  if (!live) return;
+  const int row = qt * kQTile + li;
+  if (row >= GT) return;
+  if (nsplit == 1) {
+    const int gh = row / T, node = row % T;
+    uint16_t* dst = p.out + (static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + gh) * HD;
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int j = 0; j < 4; ++j) {
+        uint2 pk;
+        pk.x = f32_to_bf16_rne(o[ct][4 * j] / l_run) | (f32_to_bf16_rne(o[ct][4 * j + 1] / l_run) << 16);
+        pk.y = f32_to_bf16_rne(o[ct][4 * j + 2] / l_run) | (f32_to_bf16_rne(o[ct][4 * j + 3] / l_run) << 16);
+        *reinterpret_cast<uint2*>(dst + 32 * ct + 8 * j + 4 * lh) = pk;
+      }
+  } else {
+    const size_t prow = sq.part_off + (static_cast<size_t>(split) * p.Hkv + g) * rows_pad + row;
+    float* dst = p.part_o + prow * HD;
+#pragma unroll
+    for (int ct = 0; ct < 4; ++ct)
+#pragma unroll
+      for (int j = 0; j < 4; ++j)
+        *reinterpret_cast<float4*>(dst + 32 * ct + 8 * j + 4 * lh) =
+            make_float4(o[ct][4 * j], o[ct][4 * j + 1], o[ct][4 * j + 2], o[ct][4 * j + 3]);
+    if (lh == 0) {
+      p.part_ml[prow * 2 + 0] = m_run;
+      p.part_ml[prow * 2 + 1] = l_run;
+    }
+  }
+}
+
 // ----------------------------------------------------------------- merge --
 
 // One half-wavefront per output row (kMergeRows rows per block): lane c <
@@ -667,7 +911,9 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
 void launch_attend(const BatchArgs& a, int items, hipStream_t s) {
-  if (a.nt == 2)
+  if (a.nt == 4)
+    hipLaunchKernelGGL(tree_attn_q4_kernel, dim3(items), dim3(kAttnThreads), 0, s, a);
+  else if (a.nt == 2)
     hipLaunchKernelGGL(tree_attn_kernel<2>, dim3(items), dim3(kAttnThreads), 0, s, a);
   else
     hipLaunchKernelGGL(tree_attn_kernel<1>, dim3(items), dim3(kAttnThreads), 0, s, a);
@@ -712,12 +958,13 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
   a.cap = cap;
   const int cus = device_cus();
   a.cus = cus;
-  a.nt = 1;   // two tiles per workgroup as soon as some sequence has more than one
+  a.nt = 1;   // the largest tile count any sequence needs
   long long work = 0;
   for (int b = 0; b < B; ++b) {
     const int T = bank->desc[topo[b]].T;
     const int nqt = rows_padded(a.G, T) / kQTile;
-    if (nqt > 1) a.nt = 2;
+    const int nt = tree_tiles(a.G, T);
+    a.nt = nt > a.nt ? nt : a.nt;
     work += static_cast<long long>(Hkv) * nqt * ((L[b] + T + KB - 1) / KB);
   }
   work = (work + a.nt - 1) / a.nt;
@@ -742,7 +989,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     const int nblocks = (q.L + q.T + KB - 1) / KB;
     int ns;
     if (B == 1) {
-      ns = split_single(nblocks, Hkv * q.nqg, cus);
+      ns = split_single(nblocks, Hkv * q.nqg, cus * wg_per_cu(a.nt));
     } else {
       ns = (nblocks + target_bps - 1) / target_bps;
       const int bound = split_bound(nblocks);
@@ -850,7 +1097,7 @@ int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, Dev
     const int nqg = query_groups(rows_padded(G, td.T) / kQTile, nt);
     const int max_blocks = (cap + KB - 1) / KB;
     for (int nblocks = 1; nblocks <= max_blocks; ++nblocks) {
-      const int ns0 = split_single(nblocks, Hkv * nqg, cus);
+      const int ns0 = split_single(nblocks, Hkv * nqg, cus * wg_per_cu(nt));
       const int bps = (nblocks + ns0 - 1) / ns0;
       const int ns = (nblocks + bps - 1) / bps;
       const int items = (Hkv * ns + 7) / 8 * 8 * nqg;
@@ -868,10 +1115,11 @@ void attn_device_splits(const entmtp_bank* bank, int Hq, int Hkv, DevTopo* topos
   const int cus = device_cus();
   const int G = Hq / Hkv;
   for (size_t k = 0; k < bank->desc.size(); ++k) {
-    const int nqg = query_groups(rows_padded(G, bank->desc[k].T) / kQTile, tree_tiles(G, bank->desc[k].T));
+    const int nt = tree_tiles(G, bank->desc[k].T);
+    const int nqg = query_groups(rows_padded(G, bank->desc[k].T) / kQTile, nt);
     topos[k].splits[0] = 1;
     for (int b = 1; b <= kMaxSplits; ++b)
-      topos[k].splits[b] = static_cast<unsigned char>(split_for_bound(b, Hkv * nqg, cus));
+      topos[k].splits[b] = static_cast<unsigned char>(split_for_bound(b, Hkv * nqg, cus * wg_per_cu(nt)));
   }
 }
 
@@ -910,9 +1158,9 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
   hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
   if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
-  // one instance per tile count among the bank's trees; the one not made for
-  // the device's tree leaves at once
-  for (int nt = 1; nt <= 2; ++nt) {
+  // one instance per tile count among the bank's trees; those not made for
+  // the device's tree leave at once
+  for (int nt = 1; nt <= 4; nt *= 2) {
     if (sh.items[nt] == 0) continue;
     a.nt = nt;
     launch_attend(a, sh.items[nt], s);
