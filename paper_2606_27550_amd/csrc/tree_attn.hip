@@ -11,25 +11,25 @@
 //     one bf16 rounding), write the tree's K/V into cache slots
 //     [L, L+T) and the rotated queries into the workspace, grouped per KV
 //     head (GQA: query rows = head-in-group x node).
-//  2. attend: flash-decoding over the cache.  A workgroup owns one
-//     (KV head, group of two 32-query tiles, key split); its four waves take
-//     interleaved 32-key blocks, each wave loading its next block while it
-//     multiplies the current one (K two blocks deep in registers, V one) and
-//     applying every block to both tiles, so a KV block is read once per 64
-//     query rows.  The tiles' fragments live once per workgroup in LDS.
-//     S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16: K comes
-//     from HBM straight into A-operand registers, V is transposed through a
-//     per-wave LDS tile, P never leaves registers (the S^T accumulator layout
-//     is re-read as the B operand of the PV product after a fixed key
+//  2. attend: flash-decoding over the cache, one of two kernels.
+//     Trees of up to 32 query rows per KV head: a workgroup owns one (KV
+//     head, 32-query tile, key split); its four waves take interleaved 32-key
+//     blocks, each wave loading its next block while it multiplies the
+//     current one (K two blocks deep in registers, V one); the tile's
+//     fragments live once per workgroup in LDS, and the four waves merge in
+//     LDS at the end.  Larger trees: a workgroup owns four tiles, one per
+//     wave, and the waves walk the same key blocks, staged once per
+//     workgroup in LDS (K as rows, V transposed), so a block is read once per
+//     128 rows; that kernel stays under 256 registers per lane, two
+//     workgroups per CU.
+//     S^T = K Q^T and O^T += V^T P^T run on v_mfma_f32_32x32x16_bf16, V
+//     transposed through LDS, P never leaving registers (the S^T accumulator
+//     layout is re-read as the B operand of the PV product after a fixed key
 //     permutation).  Blocks wholly inside the prefix skip the mask; the
 //     others take a 32-bit window cut from the node's ancestor bitmask.
 //     Online softmax in fp32, base 2, with a lazily raised running max (the
 //     accumulators are rescaled only when a block's max passes the reference
-//     by more than 2^8).  The four waves merge in LDS.
-//     Trees with more than 64 query rows per KV head use a second kernel
-//     whose four waves own one query tile each and walk the same key blocks,
-//     staged once per workgroup in LDS, so a block is read once per 128 rows;
-//     it stays under 256 registers per lane, two workgroups per CU.
+//     by more than 2^8).
 //  3. merge: combines the splits' (max, sum, unnormalised output) partials.
 //     Skipped when a single split covers the keys.
 #include <cfloat>
@@ -60,11 +60,11 @@ __host__ __device__ inline int rows_padded(int G, int T) {
 // Workgroups along the query rows: groups of nt 32-row tiles.
 __host__ __device__ inline int query_groups(int nqt, int nt) { return (nqt + nt - 1) / nt; }
 
-// Query tiles per workgroup for a tree: one, two (both in every wave) above
-// one tile of rows per KV head, four (one per wave) above two tiles.
-__host__ __device__ inline int tree_tiles(int G, int T) {
-  return G * T > 2 * kQTile ? 4 : (G * T > kQTile ? 2 : 1);
-}
+// Query tiles per workgroup for a tree: one up to one tile of rows per KV
+// head, four (one per wave) above.  (The two-tile form -- both tiles in every
+// wave -- measured slower than four tiles with two waves idle: 23.5 against
+// 19.8 us at 64 rows and prefix 4096.)
+__host__ __device__ inline int tree_tiles(int G, int T) { return G * T > kQTile ? 4 : 1; }
 
 __host__ __device__ inline int split_bound(int nblocks) {
   int b = nblocks / kMinBlocksPerSplit;
@@ -246,9 +246,10 @@ __device__ __forceinline__ void wave_lds_sync() {
   __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
 }
 
-// NT = query tiles per workgroup (1 or 2); every wave holds all NT tiles.
-template <int NT>
+// One query tile per workgroup (trees of up to 32 query rows per KV head);
+// the per-tile state below is written for NT tiles held by every wave.
 __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
+  constexpr int NT = 1;
   // blockIdx -> sequence, then (kv head, split) group and query-tile group;
   // the query groups of one (head, split) land on the same XCD (dispatch is
   // round-robin over 8 XCDs and every sequence's range starts at a multiple
@@ -256,7 +257,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
   const SeqPlan sq = resolve(p, b);
   if (sq.T == 0) return;
-  if (p.dev && tree_tiles(p.G, sq.T) != NT) return;   // the device's tree is the other instance's
+  if (p.dev && tree_tiles(p.G, sq.T) != NT) return;   // the device's tree is the other kernel's
   const int bid = blockIdx.x - sq.item0;
   const int qg = (bid >> 3) % sq.nqg;
   const int gc = ((bid >> 3) / sq.nqg) * 8 + (bid & 7);
@@ -264,8 +265,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   const int g = gc / sq.nsplit, split = gc % sq.nsplit;
   const int T = sq.T, L = sq.L, nkeys = sq.L + sq.T, rows_pad = sq.rows_pad;
   const int nsplit = sq.nsplit;
-  const int qt0 = qg * NT;                      // first query tile of the group
-  const bool two = NT == 2 && qt0 + 1 < sq.nqt;   // the group's second tile exists (uniform)
+  const int qt0 = qg * NT;   // first query tile of the group
 
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const int li = lane & 31, lh = lane >> 5;
@@ -461,7 +461,6 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     bf16x8 pf[NT][2];
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      if (t > 0 && !two) break;
       // S^T[key][query] = K Q^T
 #pragma unroll
       for (int r = 0; r < 16; ++r) sacc[t][r] = 0.f;
@@ -472,7 +471,6 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     }
 #pragma unroll
     for (int t = 0; t < NT; ++t) {
-      if (t > 0 && !two) break;
       softmax(t, sacc[t], kb, plain, pf[t]);
     }
     wave_lds_sync();  // V^T tile written by every lane
@@ -487,8 +485,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
         const u32x4 w = {x0.x, x0.y, x1.x, x1.y};
 #pragma unroll
         for (int t = 0; t < NT; ++t)
-          if (t == 0 || two)
-            o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t][u], o[t][ct], 0, 0, 0);
+          o[t][ct] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(as_bf16x8(w), pf[t][u], o[t][ct], 0, 0, 0);
       }
     }
   };
@@ -549,7 +546,6 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   float* ored = reinterpret_cast<float*>(lds);  // [slot][query][OLD]
 #pragma unroll
   for (int t = 0; t < NT; ++t) {
-    if (t > 0 && !two) break;
     const float myscale = s_sc[wave][t * kQTile + li];
     // lane (query li, half lh) holds dims 32ct + 8j + 4lh + i in o[t][ct][4j + i]
     auto slot_at = [&](int slot, int ct, int j) {
@@ -608,8 +604,8 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   }
 }
 
-// Four query tiles per workgroup, one per wave (trees with more than 64
-// query rows per KV head): the four waves walk the same key blocks, which
+// Four query tiles per workgroup, one per wave (trees with more than 32
+// query rows per KV head; waves past the tree's last tile only load): the four waves walk the same key blocks, which
 // the workgroup stages once in LDS -- K as rows, V transposed -- from
 // coalesced loads (16 lanes per 256-byte key row), double-buffered with one
 // barrier per block and two blocks in flight in registers, so a KV block is
@@ -913,10 +909,8 @@ size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 void launch_attend(const BatchArgs& a, int items, hipStream_t s) {
   if (a.nt == 4)
     hipLaunchKernelGGL(tree_attn_q4_kernel, dim3(items), dim3(kAttnThreads), 0, s, a);
-  else if (a.nt == 2)
-    hipLaunchKernelGGL(tree_attn_kernel<2>, dim3(items), dim3(kAttnThreads), 0, s, a);
   else
-    hipLaunchKernelGGL(tree_attn_kernel<1>, dim3(items), dim3(kAttnThreads), 0, s, a);
+    hipLaunchKernelGGL(tree_attn_kernel, dim3(items), dim3(kAttnThreads), 0, s, a);
 }
 
 
