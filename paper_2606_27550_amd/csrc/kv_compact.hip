@@ -14,7 +14,7 @@ namespace entmtp {
 namespace {
 
 constexpr int kCompactThreads = 256;
-constexpr int kCompactItems = 8;  // 16-byte items per thread: covers 2 * 32 rows * 256 dims
+constexpr int kCompactItems = 8;  // 16-byte items per thread at most: 2 * 32 rows * 256 dims
 
 // Sequences of one call: their caches and prefix lengths; the paths and
 // accept lengths are device arrays, one row / entry per sequence.
@@ -47,28 +47,34 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs
   const int per_tensor = (a + 1) * chunks;
   const int n_items = 2 * per_tensor;
 
-  u32x4 val[kCompactItems];
-  uint16_t* dst[kCompactItems];
-#pragma unroll
-  for (int q = 0; q < kCompactItems; ++q) {
-    const int it = threadIdx.x + q * kCompactThreads;
-    dst[q] = nullptr;
-    if (it < n_items) {
-      const int tsel = it / per_tensor, rem = it % per_tensor;
-      const int j = rem / chunks, ch = rem % chunks;
-      const int pj = p.by_value ? p.path_v[j] : path[j];
-      const int src_row = L + pj, dst_row = L + j;
-      if (src_row != dst_row && pj >= 0 && src_row < cap && dst_row < cap) {
-        uint16_t* buf = (tsel ? p.vc[b] : p.kc[b]) + base + ch * 8;
-        val[q] = *reinterpret_cast<const u32x4*>(buf + static_cast<size_t>(src_row) * d);
-        dst[q] = buf + static_cast<size_t>(dst_row) * d;
-      }
+  // the path into LDS once (one entry per thread), then the moved rows
+  // staged through LDS: every read of this (sequence, layer, head) precedes
+  // every write, and the kernel holds few registers, so it fits on a CU
+  // beside a running LM-head workgroup
+  __shared__ int s_path[ENTMTP_D_MAX + 1];
+  extern __shared__ u32x4 s_val[];   // n_items entries, sized at launch
+  const int t = threadIdx.x;
+  if (t <= a) s_path[t] = p.by_value ? p.path_v[t] : path[t];
+  __syncthreads();
+  for (int it = t; it < n_items; it += kCompactThreads) {
+    const int tsel = it / per_tensor, rem = it % per_tensor;
+    const int j = rem / chunks, ch = rem % chunks;
+    const int src_row = L + s_path[j];
+    if (s_path[j] >= 0 && src_row < cap) {
+      const uint16_t* buf = (tsel ? p.vc[b] : p.kc[b]) + base + ch * 8;
+      s_val[it] = *reinterpret_cast<const u32x4*>(buf + static_cast<size_t>(src_row) * d);
     }
   }
-  __syncthreads();  // every read of this (sequence, layer, head) precedes every write
-#pragma unroll
-  for (int q = 0; q < kCompactItems; ++q)
-    if (dst[q]) *reinterpret_cast<u32x4*>(dst[q]) = val[q];
+  __syncthreads();
+  for (int it = t; it < n_items; it += kCompactThreads) {
+    const int tsel = it / per_tensor, rem = it % per_tensor;
+    const int j = rem / chunks, ch = rem % chunks;
+    const int src_row = L + s_path[j], dst_row = L + j;
+    if (src_row != dst_row && s_path[j] >= 0 && src_row < cap && dst_row < cap) {
+      uint16_t* buf = (tsel ? p.vc[b] : p.kc[b]) + base + ch * 8;
+      *reinterpret_cast<u32x4*>(buf + static_cast<size_t>(dst_row) * d) = s_val[it];
+    }
+  }
 }
 
 int32_t check_shape(int32_t path_capacity, int32_t n_layers, int64_t layer_stride, int32_t Hkv,
@@ -88,7 +94,13 @@ int32_t check_shape(int32_t path_capacity, int32_t n_layers, int64_t layer_strid
 }
 
 int32_t launch_compact(const CompactArgs& a, int B, hipStream_t s) {
-  hipLaunchKernelGGL(kv_compact_kernel, dim3(B * a.n_layers * a.Hkv), dim3(kCompactThreads), 0, s, a);
+  // LDS for the most rows the kernel can move: the accept length given by
+  // value, else the path capacity (both clamped as in the kernel)
+  const int cap_rows = a.path_cap < ENTMTP_D_MAX + 1 ? a.path_cap : ENTMTP_D_MAX + 1;
+  int rows = a.by_value ? a.a_v + 1 : cap_rows;
+  rows = rows < 1 ? 1 : (rows > cap_rows ? cap_rows : rows);
+  const size_t lds = static_cast<size_t>(2) * rows * (a.d / 8) * sizeof(u32x4);
+  hipLaunchKernelGGL(kv_compact_kernel, dim3(B * a.n_layers * a.Hkv), dim3(kCompactThreads), lds, s, a);
   return launch_status("kv_compact launch");
 }
 
