@@ -55,7 +55,7 @@ def parse():
     ap.add_argument("--no-extras", action="store_true",
                     help="skip the timings of the typical-acceptance and frontier kernels")
     ap.add_argument("--event-every", type=int, default=8,
-                    help="time the LM head with HIP events on every n-th timed step (each "
+                    help="time the LM head with HIP events on a seeded random 1/n of the timed steps (each "
                          "event pair costs the host a few microseconds)")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
     ap.add_argument("--fixed-topo", type=int, default=-1,
@@ -83,6 +83,40 @@ def calibrate_copy():
     torch.cuda.synchronize()
     print(json.dumps({"calibration": "device copy", "bytes_read_per_copy": n,
                       "bytes_written_per_copy": n, "copies": 5}))
+
+
+class TimingEvent:
+    """A HIP timing event without the system-scope fence at record time
+    (hipEventDisableSystemFence): the bracketed kernel's results stay on the
+    device, and the fence would add its cache write-back to the bracket.
+    Created through the HIP runtime torch loaded."""
+    _hip = None
+
+    def __init__(self):
+        if TimingEvent._hip is None:
+            with open("/proc/self/maps") as f:
+                rt = sorted({l.split()[-1] for l in f if "libamdhip64" in l})
+            hip = ctypes.CDLL(rt[0])
+            hip.hipEventCreateWithFlags.argtypes = [ctypes.POINTER(ctypes.c_void_p), ctypes.c_uint]
+            hip.hipEventElapsedTime.argtypes = [ctypes.POINTER(ctypes.c_float), ctypes.c_void_p,
+                                                ctypes.c_void_p]
+            hip.hipEventDestroy.argtypes = [ctypes.c_void_p]
+            TimingEvent._hip = hip
+        self.ptr = ctypes.c_void_p()
+        rc = TimingEvent._hip.hipEventCreateWithFlags(ctypes.byref(self.ptr), 0x20000000)
+        if rc != 0:
+            raise RuntimeError(f"hipEventCreateWithFlags failed ({rc})")
+
+    def elapsed_time(self, end) -> float:
+        ms = ctypes.c_float()
+        rc = TimingEvent._hip.hipEventElapsedTime(ctypes.byref(ms), self.ptr, end.ptr)
+        if rc != 0:
+            raise RuntimeError(f"hipEventElapsedTime failed ({rc})")
+        return ms.value
+
+    def __del__(self):
+        if self._hip is not None and self.ptr:
+            self._hip.hipEventDestroy(self.ptr)
 
 
 def log(*a):
@@ -267,13 +301,11 @@ def main():
     # ---------------------------------------------------------- timed
     K = args.steps
     NE = max(1, args.event_every)
-    sampled = list(range(0, K, NE))      # timed steps whose LM head carries an event pair
-    events = [(torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True))
-              for _ in sampled]
-    for a_, b_ in events:          # torch creates an event's handle on its first record
-        a_.record()
-        b_.record()
-    ev_p = [(P_(a_.cuda_event), P_(b_.cuda_event)) for a_, b_ in events]
+    # timed steps whose LM head carries an event pair: a seeded random 1/NE of
+    # them (a fixed stride can alias with the ladder's cycle through the bank)
+    sampled = sorted(np.random.default_rng(7).choice(K, max(1, K // NE), replace=False).tolist())
+    events = [(TimingEvent(), TimingEvent()) for _ in sampled]
+    ev_p = {t: (a_.ptr, b_.ptr) for t, (a_, b_) in zip(sampled, events)}
     trace = []
     graphs, graph_steps = [], 0
     if on_gpu and args.graph:
@@ -305,8 +337,8 @@ def main():
     for g in graphs:
         chk(lib.entmtp_step_graph_launch(handles[0], g))
     for t in range(graph_steps, K):
-        trace.append(run(args.warmup + t, ev_p[t // NE] if t % NE == 0 else (None, None)))
-    events = [events[t // NE] for t in sampled]
+        trace.append(run(args.warmup + t, ev_p.get(t, (None, None))))
+    events = [ev for t, ev in zip(ev_p, events) if t >= graph_steps]
     chk(lib.entmtp_step_flush(handles[0]))   # the last timed step's compaction
     torch.cuda.synchronize()
     elapsed = time.perf_counter() - t_start
@@ -383,7 +415,7 @@ def main():
                      "algorithmic_bytes_per_launch": round(lm_bytes / len(sampled)),
                      "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T,
                      "timed_launches": len(sampled),
-                     "timing": f"HIP events around the LM-head launch of every {NE}-th timed step"},
+                     "timing": f"HIP events (no system fence) around the LM-head launch of a seeded random 1/{NE} of the timed steps, behind a launch gate"},
         "cpu_baseline": cpu,
         "next_rows": extras,
     }

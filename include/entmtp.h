@@ -555,7 +555,10 @@ void entmtp_step_destroy(entmtp_step* step);
  * LM-head weight for this step ([V][hid] bf16, 16-byte aligned; NULL: the
  * configured one).
  * ev_lm_begin / ev_lm_end: optional hipEvent_t recorded on the stream right
- * before and after the LM-head launch (NULL: none).
+ * before and after the LM-head launch (NULL: none).  With events, a one-lane
+ * gate kernel goes ahead of ev_lm_begin and holds the stream (at most 2 ms)
+ * until the host has enqueued the LM head and ev_lm_end, so the pair brackets
+ * the kernel rather than the host's launch call on an idle stream.
  * Requirements: prefix_len >= 0, prefix_len + T <= cap.
  * Errors: EINVAL (also: the previous result was not read), ERANGE, EHIP (a
  * failed launch leaves the step unusable for entmtp_step_wait until the next

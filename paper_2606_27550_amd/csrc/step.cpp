@@ -51,6 +51,11 @@ struct entmtp_step {
   hipEvent_t ev_side[kRing] = {};   // side-stream work of device-scheduled step t done
   StepMirror* host = nullptr;  // pinned, coherent
   StepMirror* dev = nullptr;   // device address of `host`
+  // launch gate for timed LM heads: a pinned, coherent word the host writes
+  // once the LM head is enqueued (its own 64-byte line)
+  uint32_t* gate_host = nullptr;
+  uint32_t* gate_dev = nullptr;
+  uint32_t gate_seq = 0;
   hipStream_t side = nullptr;  // attention chain (default priority, non-blocking)
   hipEvent_t fork = nullptr;   // caller's stream -> side stream
   hipEvent_t join = nullptr;   // side stream -> caller's stream
@@ -66,6 +71,24 @@ struct entmtp_step {
 namespace {
 
 size_t round256(size_t x) { return (x + 255) & ~size_t(255); }
+
+// The longest a launch gate holds its stream: 2 ms of the 100 MHz constant
+// clock (wall_clock64).
+constexpr uint64_t kGateTicks = 200000;
+
+// Holds the stream until the host has stored `want` to the pinned word, which
+// it does right after enqueuing the work behind the gate, or until max_ticks
+// have passed.  A timing event recorded behind the gate is therefore stamped
+// with the timed kernel already in the queue; recorded on an idle stream, it
+// would be stamped before the host's launch call and count that call's time
+// and the idle queue's dispatch latency as the kernel's.
+__global__ void launch_gate_kernel(const uint32_t* word, uint32_t want, uint64_t max_ticks) {
+  if (threadIdx.x != 0) return;
+  const uint64_t t0 = wall_clock64();
+  while (__hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != want &&
+         wall_clock64() - t0 < max_ticks)
+    __builtin_amdgcn_s_sleep(2);
+}
 
 void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
   int32_t t = 0, dd = 0;
@@ -190,6 +213,18 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
     rc = hip_status(hipHostGetDevicePointer(&d, h, 0), "hipHostGetDevicePointer");
     st->dev = static_cast<StepMirror*>(d);
   }
+  if (rc == ENTMTP_OK) {
+    void* g = nullptr;
+    rc = hip_status(hipHostMalloc(&g, 64, hipHostMallocMapped | hipHostMallocCoherent),
+                    "hipHostMalloc (launch gate)");
+    if (rc == ENTMTP_OK) {
+      st->gate_host = static_cast<uint32_t*>(g);
+      *st->gate_host = 0u;
+      void* d = nullptr;
+      rc = hip_status(hipHostGetDevicePointer(&d, g, 0), "hipHostGetDevicePointer");
+      st->gate_dev = static_cast<uint32_t*>(d);
+    }
+  }
   if (rc == ENTMTP_OK)
     rc = hip_status(hipStreamCreateWithFlags(&st->side, hipStreamNonBlocking), "hipStreamCreate");
   if (rc == ENTMTP_OK)
@@ -238,6 +273,7 @@ extern "C" void entmtp_step_destroy(entmtp_step* st) {
   if (st->fork) (void)hipEventDestroy(st->fork);
   if (st->side) (void)hipStreamDestroy(st->side);
   if (st->host) (void)hipHostFree(st->host);
+  if (st->gate_host) (void)hipHostFree(st->gate_host);
   delete st;
 }
 
@@ -327,12 +363,21 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
   // enqueued before it (the step's inputs)
   if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
 
+  // a timed LM head waits behind a launch gate that opens once it is enqueued
+  const bool gated = ev_lm_begin != nullptr;
+  if (gated) {
+    st->gate_seq = st->gate_seq + 1u == 0u ? 1u : st->gate_seq + 1u;
+    hipLaunchKernelGGL(launch_gate_kernel, dim3(1), dim3(64), 0, s, st->gate_dev, st->gate_seq,
+                       kGateTicks);
+    if (int32_t rc = launch_status("launch gate")) return rc;
+  }
   // the LM head (the longest kernel) is enqueued first, so that it is running
   // while the host enqueues the attention chain behind it
-  if (int32_t rc = launch_step_partials(hidden, w_lm ? w_lm : c.w_lm, T, c.hid, c.V, c.inv_temp,
-                                        c.logits, part, s, static_cast<hipEvent_t>(ev_lm_begin),
-                                        static_cast<hipEvent_t>(ev_lm_end)))
-    return rc;
+  const int32_t lm_rc = launch_step_partials(hidden, w_lm ? w_lm : c.w_lm, T, c.hid, c.V, c.inv_temp,
+                                             c.logits, part, s, static_cast<hipEvent_t>(ev_lm_begin),
+                                             static_cast<hipEvent_t>(ev_lm_end));
+  if (gated) __atomic_store_n(st->gate_host, st->gate_seq, __ATOMIC_RELEASE);   // open the gate
+  if (lm_rc) return lm_rc;
   const uint32_t seq = st->seq + 1u == 0u ? 1u : st->seq + 1u;   // 0 is the record's initial tag
   if (int32_t rc = launch_finalize_accept(
           st->bank, topo, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax, draft_tokens,

@@ -331,7 +331,11 @@ def check_attn(api, parent, T, L, Hq, Hkv, theta, wl=50, cap_extra=5, layer=0):
     ("single", 1, 0, 2, 2, 0.0), ("single", 1, 1, 4, 4, 10000.0), ("chain", 5, 31, 2, 2, 0.0),
     ("chain", 32, 32, 2, 2, 10000.0), ("star", 9, 33, 4, 1, 10000.0), ("random", 27, 256, 8, 8, 10000.0),
     ("random", 64, 100, 8, 2, 10000.0), ("random", 128, 0, 4, 4, 0.0), ("random", 200, 70, 4, 1, 10000.0),
-    ("random", 256, 513, 2, 2, 10000.0), ("star", 100, 1000, 4, 4, 10000.0), ("chain", 3, 4000, 8, 8, 10000.0)])
+    ("random", 256, 513, 2, 2, 10000.0), ("star", 100, 1000, 4, 4, 10000.0), ("chain", 3, 4000, 8, 8, 10000.0),
+    # four-tile kernel with idle waves: 2 tiles (40 nodes; 20 nodes x 2 heads
+    # per KV head) and 3 tiles (80 nodes)
+    ("random", 40, 300, 4, 4, 10000.0), ("random", 20, 777, 4, 2, 10000.0),
+    ("random", 80, 1500, 8, 8, 10000.0)])
 def test_tree_attn_small(api, kind, T, L, Hq, Hkv, theta):
     say("tree_attn", kind, T, L, Hq, Hkv, theta)
     if kind == "single":
