@@ -62,6 +62,9 @@ def parse():
                     help="disable the scheduler and use this bank entry every step")
     ap.add_argument("--graph", action="store_true",
                     help="with --gpu-scheduler: replay segments of steps captured as HIP graphs")
+    ap.add_argument("--no-arm", action="store_true",
+                    help="host-scheduled steps: launch each LM head only after the previous "
+                         "result is read, instead of enqueueing it ahead behind a gate")
     ap.add_argument("--gpu-scheduler", action="store_true",
                     help="run the ladder on the GPU (no result read per step) instead of on "
                          "the host; the same decisions")
@@ -275,12 +278,30 @@ def main():
                                           W_p[t % len(W_p)], e["drafts"], log_base, total, ev[0],
                                           ev[1]))
 
-    def step(t, ev=(None, None)):
+    # host-scheduled steps: while step t is in flight, step t+1's LM head is
+    # enqueued behind a gate (entmtp_step_arm) for the largest tree the ladder
+    # can reach from the current rung; launching step t+1 once the host has
+    # read step t's result and moved the ladder then opens the gate
+    arming = not args.no_arm
+    armed = [False, 0]        # armed?, the rows the armed LM head covers
+    lm_rows = []              # rows of the LM head each host-scheduled step ran
+
+    def step(t, ev=(None, None), ev_next=(None, None), arm_next=False):
         L = state["L"] if grows else L0
         topo = state["rung"]
         e = pool_p[t % P]
+        if armed[0]:   # the LM head and its events are in the queue already
+            ev = (None, None)
         chk(lib.entmtp_step_launch(handles[0], topo, L, e["q"], e["kt"], e["vt"], out_p, e["x"],
                                    W_p[t % len(W_p)], e["tok"][topo], ev[0], ev[1]))
+        lm_rows.append(armed[1] if armed[0] and Ts[topo] <= armed[1] else Ts[topo])
+        armed[0] = False
+        if arming and arm_next:
+            nx = pool_p[(t + 1) % P]
+            bound = Ts[min(topo + 1, n_topo - 1)] if args.fixed_topo < 0 else Ts[topo]
+            chk(lib.entmtp_step_arm(handles[0], nx["x"], W_p[(t + 1) % len(W_p)], bound,
+                                    ev_next[0], ev_next[1]))
+            armed[:] = [True, bound]
         chk(lib.entmtp_step_wait(handles[0], a_r, b_r, s_r, 30.0))
         a, s = a_c.value, s_c.value
         if grows:
@@ -294,7 +315,10 @@ def main():
         chk(lib.entmtp_step_device_start(handles[0], state["rung"], L0))
     run = step_gpu if on_gpu else step
     for t in range(args.warmup):
-        run(t)
+        if on_gpu:
+            run(t)
+        else:
+            run(t, arm_next=t + 1 < args.warmup)
     chk(lib.entmtp_step_flush(handles[0]))   # the last warm-up step's compaction
     torch.cuda.synchronize()
 
@@ -337,7 +361,11 @@ def main():
     for g in graphs:
         chk(lib.entmtp_step_graph_launch(handles[0], g))
     for t in range(graph_steps, K):
-        trace.append(run(args.warmup + t, ev_p.get(t, (None, None))))
+        if on_gpu:
+            trace.append(run(args.warmup + t, ev_p.get(t, (None, None))))
+        else:
+            trace.append(run(args.warmup + t, ev_p.get(t, (None, None)),
+                             ev_p.get(t + 1, (None, None)), t + 1 < K))
     events = [ev for t, ev in zip(ev_p, events) if t >= graph_steps]
     chk(lib.entmtp_step_flush(handles[0]))   # the last timed step's compaction
     torch.cuda.synchronize()
@@ -390,7 +418,8 @@ def main():
         cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta,
                            [topo for *_, topo in trace])
 
-    traffic = lm_head_traffic([T for T, *_ in trace])
+    timed_rows = lm_rows[len(lm_rows) - len(trace):] if len(lm_rows) >= len(trace) else []
+    traffic = lm_head_traffic(timed_rows or [T for T, *_ in trace])
     extras = None if args.no_extras else next_rows(api, synth, W[0], pool, hid, V, dev)
 
     line = {
@@ -407,6 +436,7 @@ def main():
                                  else f"fixed topo {args.fixed_topo}")
                    + (", on the GPU" if on_gpu else ", on the host"),
                    "T_histogram": {str(k): v for k, v in sorted(Tcount.items())},
+                   "next_lm_head_armed": bool(arming and not on_gpu),
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
         "roofline": {"kernel": "LM head with statistics partials (lm_head_hyb_loop_kernel up to 32 nodes, lm_head_hyb_kernel above)", "bound": "hbm",
@@ -415,7 +445,7 @@ def main():
                      "algorithmic_bytes_per_launch": round(lm_bytes / len(sampled)),
                      "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T,
                      "timed_launches": len(sampled),
-                     "timing": f"HIP events (no system fence) around the LM-head launch of a seeded random 1/{NE} of the timed steps, behind a launch gate"},
+                     "timing": f"HIP events (no system fence) around the LM-head launch of a seeded random 1/{NE} of the timed steps, the LM head queued behind a gate (armed during the previous step, or gated at its launch)"},
         "cpu_baseline": cpu,
         "next_rows": extras,
     }

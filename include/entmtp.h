@@ -571,6 +571,43 @@ int32_t entmtp_step_launch(entmtp_step* step, int32_t topo, int32_t prefix_len,
                            const int32_t* draft_tokens, void* ev_lm_begin, void* ev_lm_end);
 
 /*
+ * Enqueues the LM head of the next host-scheduled step ahead of its launch,
+ * so that the launch, issued once the host has read the previous result and
+ * chosen the tree (§4 "Policy"), only has to release work already in the
+ * queue.  On the configured stream, after everything enqueued so far: the
+ * fork point of the next step's cache chain, a one-lane gate kernel, and
+ * the LM head with fused statistics partials for rows [0, T_bound) of
+ * `hidden`.  The gate holds the stream until entmtp_step_wait has read the
+ * pending step's result (or the next entmtp_step_launch or entmtp_step_flush
+ * comes first), or for at most 2 ms; the LM head's inputs are fixed here, so
+ * a gate that times out only lets it start early.
+ * The next entmtp_step_launch then uses this LM head when its tree has at
+ * most T_bound nodes and it passes the same hidden and w_lm (it must pass
+ * NULL events); otherwise it opens the gate and enqueues a fresh LM head
+ * (the armed one runs unused).  With the ladder a step's tree is at most one
+ * rung above the current one, so T_bound = the next larger tree's node count
+ * always suffices; the extra rows cost little, since the LM head streams the
+ * weights once for up to 16 / 32 / 64 / 128 rows.
+ *   hidden [T_bound][hid] bf16; w_lm [V][hid] bf16 (NULL: the configured
+ *   one); T_bound in [1, the bank's largest T]; ev_lm_begin / ev_lm_end:
+ *   optional hipEvent_t recorded right before and after the LM head (behind
+ *   the gate, so the pair brackets the kernel).
+ * Ordering: the next step's cache chain starts after the work enqueued on
+ * the stream before this call, and work enqueued after it queues behind the
+ * armed LM head; so the next step's q, k_tree, v_tree, out and hidden must be
+ * ready (or enqueued) before arming.  Only its draft tokens, which the
+ * acceptance reads after the LM head, may still be enqueued in between.
+ * The armed LM head writes the configured logits buffer (if any), so the
+ * logits of the pending step are valid only until the gate opens or its
+ * time limit ends the wait.
+ * May be called while a launched step's result is pending (that is its use);
+ * not while already armed or with device-scheduled steps running
+ * (entmtp_step_device_start discards the arming).  Errors: EINVAL, ERANGE, EHIP.
+ */
+int32_t entmtp_step_arm(entmtp_step* step, const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
+                        int32_t T_bound, void* ev_lm_begin, void* ev_lm_end);
+
+/*
  * Waits for the acceptance result of the latest entmtp_step_launch by polling
  * the pinned host record (no stream synchronisation: attention may still be
  * running).  Writes the accepted draft count, the bonus token and the top-1

@@ -81,6 +81,7 @@ _SIGNATURES = {
     "entmtp_step_destroy": (None, [_c_p]),
     "entmtp_step_launch": (_c_i32, [_c_p, _c_i32, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
                                     _c_p, _c_p]),
+    "entmtp_step_arm": (_c_i32, [_c_p, _c_p, _c_p, _c_i32, _c_p, _c_p]),
     "entmtp_step_flush": (_c_i32, [_c_p]),
     "entmtp_step_wait": (_c_i32, [_c_p, ctypes.POINTER(_c_i32), ctypes.POINTER(_c_i32),
                                   ctypes.POINTER(_c_f32), ctypes.c_double]),
@@ -659,6 +660,12 @@ class Step:
         _check(lib.entmtp_step_launch(self._h, topo, prefix_len, _p(q), _p(k_tree), _p(v_tree),
                                       _p(out), _p(hidden), _p(w_lm), _p(draft_tokens), ev[0],
                                       ev[1]))
+
+    def arm(self, hidden, T_bound: int, w_lm=None, ev_lm_begin=None, ev_lm_end=None) -> None:
+        """Enqueue the next step's LM head (rows [0, T_bound) of ``hidden``)
+        behind a gate that the next ``launch`` opens."""
+        ev = [None if e is None else _c_p(e.cuda_event) for e in (ev_lm_begin, ev_lm_end)]
+        _check(lib.entmtp_step_arm(self._h, _p(hidden), _p(w_lm), T_bound, ev[0], ev[1]))
 
     def flush(self) -> None:
         _check(lib.entmtp_step_flush(self._h))

@@ -13,8 +13,9 @@
 // node by node into LDS, and the same workgroup then accepts the tree from
 // there, so no device-wide fence or arrival counter sits between the two.
 // (The workgroup is one wavefront per SIMD, so it finds room on a CU beside
-// the attention kernel.)  Larger trees merge their statistics in a kernel of
-// their own, one wavefront per node, before the acceptance kernel.
+// the attention kernel, which may still be running.)  Larger trees merge
+// their statistics in a kernel of their own, one wavefront per node, before
+// the acceptance kernel.
 #include "accept.hpp"
 #include "common.hpp"
 #include "stats.hpp"
@@ -23,6 +24,7 @@ namespace entmtp {
 namespace {
 
 constexpr int kFinAccThreads = 256;    // statistics + acceptance of one step, one workgroup
+constexpr int kPathPerThread = 4;       // path-table entries a thread carries across the merge
 constexpr int kFusedMaxT = 32;         // larger trees: a separate statistics kernel
 
 
@@ -90,14 +92,36 @@ __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
     const int* __restrict__ path_tab, int T, int D, const int* __restrict__ tok,
     int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
     float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
+  constexpr int kPathLds = kPathPerThread * kFinAccThreads;
   __shared__ float s_p1[ENTMTP_T_MAX];
   __shared__ int s_am[ENTMTP_T_MAX];
-  // the tree's own inputs are fetched while the partials merge
+  __shared__ int s_path[kPathLds];
+  // the tree's own inputs, and its path table when it fits in LDS, are
+  // fetched while the partials merge (the path rows are then read from LDS
+  // at the end instead of by a dependent global load)
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
+  const int np = T * (D + 1);
+  const bool lds_path = np <= kPathLds;
+  int pv[kPathPerThread];
+#pragma unroll
+  for (int k = 0; k < kPathPerThread; ++k) {
+    const int idx = threadIdx.x + k * kFinAccThreads;
+    pv[k] = lds_path && idx < np ? path_tab[idx] : -1;
+  }
+  // up to 32 nodes merge in one pass (eight rows per wavefront) when the LM
+  // head folded two slices per partial
   finalize_nodes<kFinAccThreads>(part, G, T, inv_temp, entropy, top1p, amax, s_p1, s_am);
+  if (lds_path) {
+#pragma unroll
+    for (int k = 0; k < kPathPerThread; ++k) {
+      const int idx = threadIdx.x + k * kFinAccThreads;
+      if (idx < np) s_path[idx] = pv[k];
+    }
+  }
   __syncthreads();
-  (void)accept_finish<kFinAccThreads>(n, greedy_ok(n, s_am, T), path_tab, T, D, s_am, s_p1,
-                                      accept_len, path_out, D + 1, bonus, best_p, mirror, seq);
+  (void)accept_finish<kFinAccThreads>(n, greedy_ok(n, s_am, T), lds_path ? s_path : path_tab, T,
+                                      D, s_am, s_p1, accept_len, path_out, D + 1, bonus, best_p,
+                                      mirror, seq);
 }
 
 // The same for a tree the device chose: the tree, its drafts and the prefix
@@ -106,7 +130,7 @@ __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
 constexpr int kFinAccDevThreads = 1024;   // any bank tree (up to 128 nodes) in at most 4 passes
 __global__ __launch_bounds__(kFinAccDevThreads) void finalize_accept_device_kernel(
     FinAccDevice dv, const uint8_t* __restrict__ arena, const StatPart* __restrict__ part, int G,
-    float inv_temp, float* __restrict__ entropy, float* __restrict__ top1p,
+    int G_small, float inv_temp, float* __restrict__ entropy, float* __restrict__ top1p,
     int* __restrict__ amax, int* __restrict__ accept_len, int* __restrict__ path_out,
     int path_cap, int* __restrict__ bonus, float* __restrict__ best_p,
     StepMirror* __restrict__ mirror, uint32_t seq) {
@@ -122,7 +146,9 @@ __global__ __launch_bounds__(kFinAccDevThreads) void finalize_accept_device_kern
   const int D = t->D;
   const int* tok = dv.drafts + static_cast<size_t>(st.rung) * dv.tree_rows;
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
-  finalize_nodes<kFinAccDevThreads>(part, G, T, inv_temp, entropy, top1p, amax, s_p1, s_am);
+  // the small-tree LM head wrote one partial per workgroup (G_small per row)
+  finalize_nodes<kFinAccDevThreads>(part, T <= kStepSmallT ? G_small : G, T, inv_temp, entropy,
+                                    top1p, amax, s_p1, s_am);
   __syncthreads();
   const int key = accept_finish<kFinAccDevThreads>(n, greedy_ok(n, s_am, T), path_tab, T, D, s_am,
                                                    s_p1, accept_len, path_out, path_cap, bonus,
@@ -253,13 +279,14 @@ int32_t launch_finalize_accept_device(const entmtp_bank* bank, const FinAccDevic
                                       uint32_t seq, hipStream_t stream) {
   hipLaunchKernelGGL(finalize_accept_device_kernel, dim3(1), dim3(kFinAccDevThreads), 0, stream, dv,
                      bank->arena, static_cast<const StatPart*>(partials), stats_slices(V),
-                     inv_temp, entropy, top1p, argmax, accept_len, path, path_capacity, bonus,
+                     step_small_parts(V), inv_temp, entropy, top1p, argmax, accept_len, path, path_capacity, bonus,
                      best_top1p, mirror, seq);
   return launch_status("finalize_accept (device-scheduled) launch");
 }
 
 int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,
-                               int32_t V, float inv_temp, float* entropy, float* top1p,
+                               int32_t n_parts, int32_t V, float inv_temp, float* entropy,
+                               float* top1p,
                                int32_t* argmax, const int32_t* draft_tokens, int32_t* accept_len,
                                int32_t* path, int32_t* bonus, float* best_top1p,
                                StepMirror* mirror, uint32_t seq, hipStream_t stream) {
@@ -271,7 +298,7 @@ int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void
                          best_top1p, mirror, seq, stream);
   }
   hipLaunchKernelGGL(finalize_accept_kernel, dim3(1), dim3(kFinAccThreads), 0, stream,
-                     static_cast<const StatPart*>(partials), stats_slices(V), inv_temp, entropy,
+                     static_cast<const StatPart*>(partials), n_parts, inv_temp, entropy,
                      top1p, argmax, bank_ptr<int>(bank, d.off_parent),
                      bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
                      bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, accept_len, path,

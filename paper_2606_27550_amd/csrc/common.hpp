@@ -173,10 +173,13 @@ int32_t launch_compact_host(const int32_t* path_host, int32_t accept_len, int32_
                             hipStream_t s);
 
 // Finishes the LM head's statistics partials for every node of tree `topo`
-// and accepts the tree (as launch_accept): one launch for trees of up to 32
-// nodes, a statistics launch and an acceptance launch for larger ones.
+// (n_parts partials per node, rows n_parts long: what the LM head launched
+// for the step wrote) and accepts the tree (as launch_accept): one launch
+// for trees of up to 32 nodes, a statistics launch and an acceptance launch
+// for larger ones.
 int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void* partials,
-                               int32_t V, float inv_temp, float* entropy, float* top1p,
+                               int32_t n_parts, int32_t V, float inv_temp, float* entropy,
+                               float* top1p,
                                int32_t* argmax, const int32_t* draft_tokens, int32_t* accept_len,
                                int32_t* path, int32_t* bonus, float* best_top1p,
                                StepMirror* mirror, uint32_t seq, hipStream_t stream);

@@ -426,7 +426,8 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
                                          const uint16_t* __restrict__ X,
                                          const uint16_t* __restrict__ W, float* __restrict__ logits,
                                          int T, int hid, int V, int G, float inv_temp,
-                                         StatPart* __restrict__ part, int j0, int sl) {
+                                         StatPart* __restrict__ part, int j0, int sl,
+                                         int pcol = -1, int pstride = 0, bool merge_prev = false) {
   using Sh = HybShape<NT>;
   static_assert(S >= 2 && S <= 4, "two to four X ring slots");
   static_assert(WT == 1 || WT == 2, "one or two W tiles per wave");
@@ -437,11 +438,16 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
   const int r1 = slice_begin(WT * sl + WT, G, V);
   if (r0 >= r1) {  // empty slices (tiny V): the whole workgroup leaves
     if constexpr (STATS)
-      if (threadIdx.x < Sh::TP && j0 + threadIdx.x < T)
+      if (threadIdx.x < Sh::TP && j0 + threadIdx.x < T) {
+        const StatPart empty{-INFINITY, 0.f, 0.f, 0x7fffffff};
+        if (pcol >= 0) {
+          if (!merge_prev) part[static_cast<size_t>(j0 + threadIdx.x) * pstride + pcol] = empty;
+        } else {
 #pragma unroll
-        for (int u = 0; u < WT; ++u)
-          part[static_cast<size_t>(j0 + threadIdx.x) * G + WT * sl + u] =
-              StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
+          for (int u = 0; u < WT; ++u)
+            part[static_cast<size_t>(j0 + threadIdx.x) * G + WT * sl + u] = empty;
+        }
+      }
     return;
   }
   const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
@@ -647,12 +653,25 @@ __device__ __forceinline__ void hyb_body(uint8_t* xslot0, uint8_t* xslot1, uint8
       StatPart acc_p = wpart[c];
 #pragma unroll
       for (int w = 1; w < kHybWaves; ++w) part_merge(acc_p, wpart[w * kStride + c], inv_temp);
-      // the workgroup's slices: the combined partial in the first, neutral
-      // partials in the others
-      part[static_cast<size_t>(j0 + c) * G + WT * sl] = acc_p;
+      if (pcol >= 0) {
+        // one partial per workgroup (column pcol of rows pstride long): a
+        // workgroup's later slices fold into the partial of its first, which
+        // this thread wrote itself
+        StatPart* dst = part + static_cast<size_t>(j0 + c) * pstride + pcol;
+        if (merge_prev) {
+          StatPart prev = *dst;
+          part_merge(prev, acc_p, inv_temp);
+          acc_p = prev;
+        }
+        *dst = acc_p;
+      } else {
+        // the workgroup's slices: the combined partial in the first, neutral
+        // partials in the others
+        part[static_cast<size_t>(j0 + c) * G + WT * sl] = acc_p;
 #pragma unroll
-      for (int u = 1; u < WT; ++u)
-        part[static_cast<size_t>(j0 + c) * G + WT * sl + u] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
+        for (int u = 1; u < WT; ++u)
+          part[static_cast<size_t>(j0 + c) * G + WT * sl + u] = StatPart{-INFINITY, 0.f, 0.f, 0x7fffffff};
+      }
     }
   }
 }
@@ -680,7 +699,8 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_kernel(
 
 // The same kernel with fewer workgroups than slices: workgroup b takes slices
 // b, b + gridDim.x, ... in turn (one resident workgroup per CU leaves the
-// other half of the CU to concurrent work).
+// other half of the CU to concurrent work) and folds them into one partial
+// per node, column b of rows gridDim.x long (half the partials to merge).
 template <int NT, int S, int NCH, bool STATS>
 __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_loop_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
@@ -694,7 +714,8 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_hyb_loop_kernel(
   for (int sl = blockIdx.x; sl < G; sl += gridDim.x) {
     if (sl != static_cast<int>(blockIdx.x)) __syncthreads();   // the previous slice is done with the LDS
     hyb_body<NT, S, NCH, STATS>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
-                                inv_temp, part, blockIdx.y * HybShape<NT>::TP, sl);
+                                inv_temp, part, blockIdx.y * HybShape<NT>::TP, sl, blockIdx.x,
+                                gridDim.x, sl != static_cast<int>(blockIdx.x));
   }
 }
 
@@ -717,17 +738,19 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_dyn_small_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t xslot3[XSTAGE];
   __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * kL3TileBytes];
   const int T = __builtin_amdgcn_readfirstlane(*T_dev);
-  if (T > 32) return;
+  if (T > kStepSmallT) return;
   // slices b, b + gridDim.x, ...: the grid is half the slices, so one
-  // workgroup per CU streams W and the attention overlapping it fits beside
+  // workgroup per CU streams W and the attention overlapping it fits beside;
+  // one partial per workgroup, as the host-sized loop kernel
   for (int sl = blockIdx.x; sl < G; sl += gridDim.x) {
-    if (sl != static_cast<int>(blockIdx.x)) __syncthreads();
+    const bool later = sl != static_cast<int>(blockIdx.x);
+    if (later) __syncthreads();
     if (T <= 16)
       hyb_body<1, 4, NCH, true>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
-                                inv_temp, part, 0, sl);
+                                inv_temp, part, 0, sl, blockIdx.x, gridDim.x, later);
     else
       hyb_body<2, 4, NCH, true>(xslot0, xslot1, xslot2, xslot3, tpose, X, W, logits, T, hid, V, G,
-                                inv_temp, part, 0, sl);
+                                inv_temp, part, 0, sl, blockIdx.x, gridDim.x, later);
   }
 }
 
@@ -741,7 +764,7 @@ __global__ __launch_bounds__(kHybThreads) void lm_head_dyn_large_kernel(
   __shared__ __attribute__((aligned(16))) uint8_t xslot1[XSTAGE];
   __shared__ __attribute__((aligned(16))) uint8_t tpose[kHybWaves * WT * kL3TileBytes];
   const int T = __builtin_amdgcn_readfirstlane(*T_dev);
-  if (T > 32)
+  if (T > kStepSmallT)
     hyb_body<8, 2, NCH, true, WT>(xslot0, xslot1, xslot0, xslot1, tpose, X, W, logits, T, hid, V,
                                   G, inv_temp, part, 0, blockIdx.x);
 }
@@ -900,13 +923,17 @@ int32_t launch_lm(const uint16_t* X, const uint16_t* W, float* logits, int T, in
 
 int stats_slices(int V) { return hyb_grid(V); }
 
+int step_small_parts(int V) { return (hyb_grid(V) + 1) / 2; }
+
 int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, int T, int hid,
-                             int V, float inv_temp, float* logits, void* partials, hipStream_t s,
-                             hipEvent_t ev0, hipEvent_t ev1) {
+                             int V, float inv_temp, float* logits, void* partials, int* n_parts,
+                             hipStream_t s, hipEvent_t ev0, hipEvent_t ev1) {
   auto* part = static_cast<StatPart*>(partials);
   const auto* X = reinterpret_cast<const uint16_t*>(hidden);
   const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
-  if (T > 32) {   // the step's configuration was checked: hid is a multiple of 4 rounds
+  *n_parts = step_small_parts(V);
+  if (T > kStepSmallT) {   // the step's configuration was checked: hid is a multiple of 4 rounds
+    *n_parts = hyb_grid(V);
     int32_t rc = ENTMTP_OK;
     if (!launch_hyb_dispatch<true>(X, W, logits, T, hid, V, s, inv_temp, part, &rc, ev0, ev1))
       return fail(ENTMTP_EINVAL, "hid = %d: no streaming LM head", hid);

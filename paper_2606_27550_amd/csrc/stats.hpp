@@ -80,7 +80,7 @@ __device__ __forceinline__ unsigned long long key_max(unsigned long long a, unsi
   return a > b ? a : b;
 }
 
-template <int R>
+template <int R, int P = kMergeRegParts>
 __device__ __forceinline__ void merge_rows(const StatPart* __restrict__ part, const int (&row)[R],
                                            int G, float inv_temp, StatPart (&out)[R]) {
   const int lane = threadIdx.x & 63;
@@ -117,16 +117,16 @@ __device__ __forceinline__ void merge_rows(const StatPart* __restrict__ part, co
 #pragma unroll
     for (int r = 0; r < R; ++r) key_parts(key[r], m[r], mi[r]);
   };
-  if (G <= 64 * kMergeRegParts) {
+  if (G <= 64 * P) {
     // unconditional loads addressed from the kernel's own pointer (clamped
     // to an existing row and partial), so the compiler issues them back to
     // back as global loads; entries past the row read as empty
-    StatPart v[R][kMergeRegParts];
+    StatPart v[R][P];
 #pragma unroll
     for (int r = 0; r < R; ++r) {
       const StatPart* src = part + static_cast<size_t>(row[r] >= 0 ? row[r] : row[0]) * G;
 #pragma unroll
-      for (int k = 0; k < kMergeRegParts; ++k) {
+      for (int k = 0; k < P; ++k) {
         const int g = lane + 64 * k;
         v[r][k] = src[g < G ? g : 0];
       }
@@ -134,19 +134,19 @@ __device__ __forceinline__ void merge_rows(const StatPart* __restrict__ part, co
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int k = 0; k < kMergeRegParts; ++k)
+      for (int k = 0; k < P; ++k)
         if (row[r] < 0 || lane + 64 * k >= G) v[r][k] = kEmpty;
 #pragma unroll
     for (int r = 0; r < R; ++r)
 #pragma unroll
-      for (int k = 0; k < kMergeRegParts; ++k) key[r] = key_max(key[r], max_key(v[r][k].zmax, v[r][k].idx));
+      for (int k = 0; k < P; ++k) key[r] = key_max(key[r], max_key(v[r][k].zmax, v[r][k].idx));
     max_butterfly();
 #pragma unroll
     for (int r = 0; r < R; ++r)
       if (m[r] != -INFINITY) {
         const float my = m[r] * inv_temp;
 #pragma unroll
-        for (int k = 0; k < kMergeRegParts; ++k) add(v[r][k], my, Z[r], S[r]);
+        for (int k = 0; k < P; ++k) add(v[r][k], my, Z[r], S[r]);
       }
   } else {
 #pragma unroll
@@ -195,15 +195,12 @@ __device__ __forceinline__ float part_top1p(const StatPart& p) { return 1.f / p.
 // be NULL) and, for the workgroup's own later use, to LDS arrays s_top1p and
 // s_argmax (may be NULL).  The caller synchronises the workgroup before
 // reading the LDS arrays.
-template <int NTH>
-__device__ __forceinline__ void finalize_nodes(const StatPart* __restrict__ part, int G, int T,
-                                               float inv_temp, float* __restrict__ entropy,
-                                               float* __restrict__ top1p, int* __restrict__ argmax,
-                                               float* s_top1p, int* s_argmax) {
+template <int NTH, int R, int P>
+__device__ __forceinline__ void finalize_rows(const StatPart* __restrict__ part, int G, int T,
+                                              float inv_temp, float* __restrict__ entropy,
+                                              float* __restrict__ top1p, int* __restrict__ argmax,
+                                              float* s_top1p, int* s_argmax) {
   constexpr int NW = NTH / 64;
-  // rows per wavefront per pass (their loads go out together); one in a
-  // 1024-thread workgroup, whose lanes have 128 registers
-  constexpr int R = NTH >= 1024 ? 1 : 4;
   const int w = threadIdx.x >> 6, lane = threadIdx.x & 63;
   for (int n0 = w; n0 < T; n0 += R * NW) {
     int rows[R];
@@ -213,7 +210,7 @@ __device__ __forceinline__ void finalize_nodes(const StatPart* __restrict__ part
       rows[r] = n < T ? n : -1;
     }
     StatPart o[R];
-    merge_rows<R>(part, rows, G, inv_temp, o);
+    merge_rows<R, P>(part, rows, G, inv_temp, o);
     if (lane == 0) {
 #pragma unroll
       for (int r = 0; r < R; ++r) {
@@ -229,6 +226,30 @@ __device__ __forceinline__ void finalize_nodes(const StatPart* __restrict__ part
   }
 }
 
+template <int NTH>
+__device__ __forceinline__ void finalize_nodes(const StatPart* __restrict__ part, int G, int T,
+                                               float inv_temp, float* __restrict__ entropy,
+                                               float* __restrict__ top1p, int* __restrict__ argmax,
+                                               float* s_top1p, int* s_argmax) {
+  // rows per wavefront per pass (their loads go out together): one in a
+  // 1024-thread workgroup, whose lanes have 128 registers; else four rows of
+  // up to 512 partials, or eight rows of up to 256 (the step's small-tree LM
+  // head folds two slices per partial), 128 registers of partials either way
+  if constexpr (NTH >= 1024) {
+    if (G <= 64 * 4)
+      finalize_rows<NTH, 1, 4>(part, G, T, inv_temp, entropy, top1p, argmax, s_top1p, s_argmax);
+    else
+      finalize_rows<NTH, 1, kMergeRegParts>(part, G, T, inv_temp, entropy, top1p, argmax, s_top1p,
+                                            s_argmax);
+  } else {
+    if (G <= 64 * 4)
+      finalize_rows<NTH, 8, 4>(part, G, T, inv_temp, entropy, top1p, argmax, s_top1p, s_argmax);
+    else
+      finalize_rows<NTH, 4, kMergeRegParts>(part, G, T, inv_temp, entropy, top1p, argmax, s_top1p,
+                                            s_argmax);
+  }
+}
+
 // The statistics of nodes 0..T-1 from the LM head's partials, one wavefront
 // per node (as entmtp_stats_finalize, arguments unchecked).
 int32_t launch_stats_finalize(const void* partials, int T, int V, float inv_temp, float* entropy,
@@ -238,14 +259,20 @@ int32_t launch_stats_finalize(const void* partials, int T, int V, float inv_temp
 // current device (its grid width).
 int stats_slices(int V);
 
+// Trees of up to kStepSmallT nodes: the step's LM head runs one workgroup per
+// two vocabulary slices and writes one partial per workgroup per node,
+// step_small_parts(V) per row (rows that long).
+constexpr int kStepSmallT = 32;
+int step_small_parts(int V);
+
 // The LM head with statistics partials inside a verification step: as
 // entmtp_verify_logits_partials (arguments checked by the step), but for trees
 // of up to 32 nodes with one workgroup per CU looping over two vocabulary
 // slices, which leaves room on every CU for the attention overlapping it.
 // ev0 / ev1 (may be NULL) are recorded right before and after the LM head.
 int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, int T, int hid,
-                             int V, float inv_temp, float* logits, void* partials, hipStream_t s,
-                             hipEvent_t ev0, hipEvent_t ev1);
+                             int V, float inv_temp, float* logits, void* partials, int* n_parts,
+                             hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
 // The LM head with statistics partials (as entmtp_verify_logits_partials,
 // no logits) for a node count the device holds in *T_dev (1 <= T <= T_max

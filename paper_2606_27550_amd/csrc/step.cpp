@@ -56,6 +56,14 @@ struct entmtp_step {
   uint32_t* gate_host = nullptr;
   uint32_t* gate_dev = nullptr;
   uint32_t gate_seq = 0;
+  // the next step's LM head, enqueued ahead of its launch behind the gate
+  // (entmtp_step_arm): the rows it covers and the inputs it reads
+  bool armed = false;
+  int32_t armed_T = 0;
+  int32_t armed_parts = 0;     // statistics partials per node it writes
+  int32_t lm_parts = 0;        // the same for the LM head of the latest launch
+  const void* armed_hidden = nullptr;
+  const void* armed_w = nullptr;
   hipStream_t side = nullptr;  // attention chain (default priority, non-blocking)
   hipEvent_t fork = nullptr;   // caller's stream -> side stream
   hipEvent_t join = nullptr;   // side stream -> caller's stream
@@ -88,6 +96,20 @@ __global__ void launch_gate_kernel(const uint32_t* word, uint32_t want, uint64_t
   while (__hip_atomic_load(word, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_SYSTEM) != want &&
          wall_clock64() - t0 < max_ticks)
     __builtin_amdgcn_s_sleep(2);
+}
+
+// Lets the gated work of the latest gate kernel run (harmless if it already
+// has, or if the gate's time limit ended the wait).
+void open_gate(entmtp_step* st) {
+  __atomic_store_n(st->gate_host, st->gate_seq, __ATOMIC_RELEASE);
+}
+
+// Enqueues a gate kernel on s with a fresh sequence number.
+int32_t enqueue_gate(entmtp_step* st, hipStream_t s) {
+  st->gate_seq = st->gate_seq + 1u == 0u ? 1u : st->gate_seq + 1u;
+  hipLaunchKernelGGL(launch_gate_kernel, dim3(1), dim3(64), 0, s, st->gate_dev, st->gate_seq,
+                     kGateTicks);
+  return launch_status("launch gate");
 }
 
 void bank_extent(const entmtp_bank* bank, int32_t* T_max, int32_t* D_max) {
@@ -266,6 +288,10 @@ extern "C" int32_t entmtp_step_create(const entmtp_bank* bank, const entmtp_step
 
 extern "C" void entmtp_step_destroy(entmtp_step* st) {
   if (!st) return;
+  if (st->armed && st->gate_host) {   // the gate kernel must be done with the word before it is freed
+    open_gate(st);
+    (void)hipStreamSynchronize(static_cast<hipStream_t>(st->cfg.stream));
+  }
   if (st->side) (void)hipStreamSynchronize(st->side);
   for (int k = 0; k < entmtp_step::kRing; ++k)
     if (st->ev_side[k]) (void)hipEventDestroy(st->ev_side[k]);
@@ -311,6 +337,7 @@ int32_t enqueue_device_compaction(entmtp_step* st, uint64_t t) {
 int32_t flush_side(entmtp_step* st) {
   ENTMTP_CHECK_ARG(!st->pending, ENTMTP_EINVAL,
                    "a launched step's result has not been read (entmtp_step_wait)");
+  if (st->armed) open_gate(st);   // an armed LM head may run now (it stays armed)
   if (int32_t rc = enqueue_due_compaction(st)) return rc;
   if (st->dev_started && st->dev_compact < st->dev_t) {   // the last device-scheduled step's
     auto s = static_cast<hipStream_t>(st->cfg.stream);
@@ -359,33 +386,51 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
   uint8_t* ws = static_cast<uint8_t*>(c.workspace);
   void* part = ws + st->part_offset;
 
-  // the side stream's work of this step starts after everything the caller
-  // enqueued before it (the step's inputs)
-  if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
-
-  // a timed LM head waits behind a launch gate that opens once it is enqueued
-  const bool gated = ev_lm_begin != nullptr;
-  if (gated) {
-    st->gate_seq = st->gate_seq + 1u == 0u ? 1u : st->gate_seq + 1u;
-    hipLaunchKernelGGL(launch_gate_kernel, dim3(1), dim3(64), 0, s, st->gate_dev, st->gate_seq,
-                       kGateTicks);
-    if (int32_t rc = launch_status("launch gate")) return rc;
+  const void* w_step = w_lm ? w_lm : c.w_lm;
+  // an armed step: the LM head waits in the stream behind the gate (with the
+  // fork recorded ahead of it); opening the gate is the whole launch, unless
+  // the tree outgrew the rows it was armed for or its inputs differ (then a
+  // fresh LM head follows it and overwrites its partials)
+  bool lm_ready = false;
+  if (st->armed) {
+    ENTMTP_CHECK_ARG(ev_lm_begin == nullptr && ev_lm_end == nullptr, ENTMTP_EINVAL,
+                     "the LM-head events of an armed step are given to entmtp_step_arm");
+    st->armed = false;
+    open_gate(st);
+    lm_ready = T <= st->armed_T && hidden == st->armed_hidden && w_step == st->armed_w;
+    st->lm_parts = st->armed_parts;
+  } else {
+    // the side stream's work of this step starts after everything the
+    // caller enqueued before it (the step's inputs)
+    if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
   }
-  // the LM head (the longest kernel) is enqueued first, so that it is running
-  // while the host enqueues the attention chain behind it
-  const int32_t lm_rc = launch_step_partials(hidden, w_lm ? w_lm : c.w_lm, T, c.hid, c.V, c.inv_temp,
-                                             c.logits, part, s, static_cast<hipEvent_t>(ev_lm_begin),
-                                             static_cast<hipEvent_t>(ev_lm_end));
-  if (gated) __atomic_store_n(st->gate_host, st->gate_seq, __ATOMIC_RELEASE);   // open the gate
-  if (lm_rc) return lm_rc;
-  const uint32_t seq = st->seq + 1u == 0u ? 1u : st->seq + 1u;   // 0 is the record's initial tag
-  if (int32_t rc = launch_finalize_accept(
-          st->bank, topo, part, c.V, c.inv_temp, c.entropy, c.top1p, c.argmax, draft_tokens,
-          c.accept_len, c.path, c.bonus, c.best_top1p, st->dev, seq, s))
-    return rc;
-  st->seq = seq;
 
-  // the cache chain on the side stream, concurrent with the above: the
+  if (!lm_ready) {
+    // a timed LM head waits behind a launch gate that opens once it is enqueued
+    const bool gated = ev_lm_begin != nullptr;
+    if (gated)
+      if (int32_t rc = enqueue_gate(st, s)) return rc;
+    // the LM head (the longest kernel) is enqueued first, so that it is
+    // running while the host enqueues the attention chain behind it
+    const int32_t lm_rc = launch_step_partials(
+        hidden, static_cast<const entmtp_bf16*>(w_step), T, c.hid, c.V, c.inv_temp, c.logits, part,
+        &st->lm_parts, s, static_cast<hipEvent_t>(ev_lm_begin), static_cast<hipEvent_t>(ev_lm_end));
+    if (gated) open_gate(st);
+    if (lm_rc) return lm_rc;
+  }
+  // the statistics merge and acceptance wait for the LM head: with one layer
+  // they are enqueued after the short attention chain (which then starts a
+  // few microseconds sooner), with many before it (whose enqueue would
+  // outlast the LM head)
+  const uint32_t seq = st->seq + 1u == 0u ? 1u : st->seq + 1u;   // 0 is the record's initial tag
+  auto finalize = [&]() {
+    return launch_finalize_accept(st->bank, topo, part, st->lm_parts, c.V, c.inv_temp, c.entropy,
+                                  c.top1p, c.argmax, draft_tokens, c.accept_len, c.path, c.bonus,
+                                  c.best_top1p, st->dev, seq, s);
+  };
+  if (c.n_layers > 1)
+    if (int32_t rc = finalize()) return rc;
+  // the cache chain on the side stream, concurrent with the LM head: the
   // previous step's compaction, then this step's attention layers
   if (int32_t rc = hip_status(hipStreamWaitEvent(st->side, st->fork, 0), "hipStreamWaitEvent"))
     return rc;
@@ -400,8 +445,48 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
                                       out + l * q_layer, ws, st->attn_bytes, st->side))
       return rc;
   }
+  if (c.n_layers == 1)
+    if (int32_t rc = finalize()) return rc;
+  st->seq = seq;
   st->pending = true;
   st->pending_L = prefix_len;
+  return ENTMTP_OK;
+}
+
+extern "C" int32_t entmtp_step_arm(entmtp_step* st, const entmtp_bf16* hidden,
+                                   const entmtp_bf16* w_lm, int32_t T_bound, void* ev_lm_begin,
+                                   void* ev_lm_end) {
+  clear_error();
+  ENTMTP_CHECK_ARG(st != nullptr, ENTMTP_EINVAL, "step is NULL");
+  ENTMTP_CHECK_ARG(!st->armed, ENTMTP_EINVAL, "the next step is armed already");
+  ENTMTP_CHECK_ARG(!st->dev_started, ENTMTP_EINVAL,
+                   "device-scheduled steps are running (their LM heads are enqueued by their launch)");
+  ENTMTP_CHECK_ARG(hidden != nullptr, ENTMTP_EINVAL, "hidden is NULL");
+  ENTMTP_CHECK_ARG(w_lm == nullptr || aligned16(w_lm), ENTMTP_EINVAL, "w_lm must be 16-byte aligned");
+  ENTMTP_CHECK_ARG(T_bound >= 1 && T_bound <= st->T_max, ENTMTP_ERANGE,
+                   "T_bound = %d outside [1, %d] (the bank's largest tree)", T_bound, st->T_max);
+  const entmtp_step_config& c = st->cfg;
+  auto s = static_cast<hipStream_t>(c.stream);
+  void* part = static_cast<uint8_t*>(c.workspace) + st->part_offset;
+  const void* w_step = w_lm ? w_lm : c.w_lm;
+  // the next step's cache chain starts after everything enqueued so far (the
+  // caller's inputs and the pending step's acceptance), not after the armed
+  // LM head
+  if (int32_t rc = hip_status(hipEventRecord(st->fork, s), "hipEventRecord (fork)")) return rc;
+  if (int32_t rc = enqueue_gate(st, s)) return rc;
+  int32_t parts = 0;
+  const int32_t rc = launch_step_partials(
+      hidden, static_cast<const entmtp_bf16*>(w_step), T_bound, c.hid, c.V, c.inv_temp, c.logits,
+      part, &parts, s, static_cast<hipEvent_t>(ev_lm_begin), static_cast<hipEvent_t>(ev_lm_end));
+  if (rc) {
+    open_gate(st);
+    return rc;
+  }
+  st->armed = true;
+  st->armed_T = T_bound;
+  st->armed_parts = parts;
+  st->armed_hidden = hidden;
+  st->armed_w = w_step;
   return ENTMTP_OK;
 }
 
@@ -446,6 +531,9 @@ extern "C" int32_t entmtp_step_wait(entmtp_step* st, int32_t* accept_len, int32_
     }
     __builtin_ia32_pause();
   }
+  // the result is known: an armed LM head (sized for any tree the caller may
+  // choose next) may start now, before the caller has moved the ladder
+  if (st->armed) open_gate(st);
   const int32_t a = static_cast<int32_t>(static_cast<uint32_t>(words[0]));
   st->pending = false;
   if (a < 0 || a > st->D_max)
@@ -484,8 +572,10 @@ extern "C" int32_t entmtp_step_device_start(entmtp_step* st, int32_t topo, int32
                    st->bank->desc[topo].T, c.cap);
   ENTMTP_CHECK_ARG(st->T_max <= 128, ENTMTP_ERANGE,
                    "device-scheduled steps support trees of up to 128 nodes (bank has %d)", st->T_max);
-  // steps before this one finish their cache work first
+  // steps before this one finish their cache work first (an armed LM head
+  // runs unused: device-scheduled steps enqueue their own)
   if (int32_t rc = flush_side(st)) return rc;
+  st->armed = false;
   DevStep* state = dev_state(st);
   hipLaunchKernelGGL(device_start_kernel, dim3(1), dim3(64), 0, static_cast<hipStream_t>(c.stream),
                      state, reinterpret_cast<const DevTopo*>(state + entmtp_step::kRing), topo,
