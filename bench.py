@@ -726,7 +726,12 @@ def lm_head_traffic(Ts):
         if targs[3] != "true":   # the timed kernel is the statistics variant <NT, S, NCH, STATS, ...>
             continue
         kernel = name.split("<")[0].split()[-1]
-        per[(kernel, int(targs[0]))] = v["fetch_bytes"] + v["write_bytes"]
+        key = (kernel, int(targs[0]))
+        # large tiles: the step pairs slices per workgroup (last argument 2);
+        # an unpaired launch of the entry points must not stand in for it
+        if key in per and len(targs) > 4 and targs[4] != "2":
+            continue
+        per[key] = v["fetch_bytes"] + v["write_bytes"]
     tot = 0.0
     for T in Ts:   # the step's launch: the loop kernel up to 32 nodes, the grid kernel above
         key = (("lm_head_hyb_loop_kernel", 1 if T <= 16 else 2) if T <= 32 else

@@ -856,13 +856,19 @@ int32_t launch_lm_hyb(const uint16_t* X, const uint16_t* W, float* logits, int T
 
 // Streaming LM head with fused statistics partials, then the per-node
 // finalize; false when the streaming kernel does not apply to hid.
+// beside: other work (the step's attention) runs beside the LM head.
 template <bool STATS>
 bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
                          hipStream_t s, float inv_temp, StatPart* part, int32_t* rc,
-                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr) {
+                         hipEvent_t ev0 = nullptr, hipEvent_t ev1 = nullptr, bool beside = false) {
   // large node tiles pair slices per workgroup (each X fragment read from
-  // LDS then feeds two W tiles) when that still leaves a workgroup per CU
+  // LDS then feeds two W tiles) when that still leaves a workgroup per CU;
+  // 128-node tiles only beside other work: alone, two unpaired workgroups
+  // per CU keep more of W in flight (the batch-8 LM head: 259 -> 247 us),
+  // but they fill the CU's LDS, and beside the 13B step's attention they lost
+  // (96 -> 106 us)
   const bool pair = hyb_grid(V) >= 2 * device_cus();
+  const bool pair128 = pair && beside;
   auto go = [&](auto nch) {
     constexpr int NCH = decltype(nch)::value;
     if (T <= 16)
@@ -873,8 +879,8 @@ bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, in
       *rc = pair ? launch_lm_hyb<4, kHybS4, NCH, STATS, kHybW4>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1)
                  : launch_lm_hyb<4, 4, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
     else
-      *rc = pair ? launch_lm_hyb<8, kHybS8, NCH, STATS, kHybW8>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1)
-                 : launch_lm_hyb<8, 2, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
+      *rc = pair128 ? launch_lm_hyb<8, kHybS8, NCH, STATS, kHybW8>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1)
+                    : launch_lm_hyb<8, 2, NCH, STATS>(X, W, logits, T, hid, V, s, inv_temp, part, ev0, ev1);
   };
   if (hid == 4096) {              // the 7B hidden size: K loop fully unrolled
     go(std::integral_constant<int, 32>{});
@@ -935,7 +941,7 @@ int32_t launch_step_partials(const entmtp_bf16* hidden, const entmtp_bf16* w_lm,
   if (T > kStepSmallT) {   // the step's configuration was checked: hid is a multiple of 4 rounds
     *n_parts = hyb_grid(V);
     int32_t rc = ENTMTP_OK;
-    if (!launch_hyb_dispatch<true>(X, W, logits, T, hid, V, s, inv_temp, part, &rc, ev0, ev1))
+    if (!launch_hyb_dispatch<true>(X, W, logits, T, hid, V, s, inv_temp, part, &rc, ev0, ev1, true))
       return fail(ENTMTP_EINVAL, "hid = %d: no streaming LM head", hid);
     return rc;
   }
