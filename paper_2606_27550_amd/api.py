@@ -616,9 +616,10 @@ class Step:
         D = max(bank.D)
         self.logits = (torch.empty((tree_rows, V), dtype=torch.float32, device=dev) if keep_logits
                        else None)
-        self.entropy = torch.empty(tree_rows, dtype=torch.float32, device=dev)
-        self.top1p = torch.empty(tree_rows, dtype=torch.float32, device=dev)
-        self.argmax = torch.empty(tree_rows, dtype=torch.int32, device=dev)
+        # zeroed: a step writes rows [0, T) only, and rows above stay defined
+        self.entropy = torch.zeros(tree_rows, dtype=torch.float32, device=dev)
+        self.top1p = torch.zeros(tree_rows, dtype=torch.float32, device=dev)
+        self.argmax = torch.zeros(tree_rows, dtype=torch.int32, device=dev)
         self.accept_len = torch.zeros(1, dtype=torch.int32, device=dev)
         self.bonus = torch.zeros(1, dtype=torch.int32, device=dev)
         self.best_top1p = torch.zeros(1, dtype=torch.float32, device=dev)
