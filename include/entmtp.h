@@ -481,8 +481,10 @@ int32_t entmtp_frontier_score(const entmtp_bank* bank, int32_t topo, const uint8
  *              fp32; argmax [tree_rows] int32   outputs of the LM head and
  *              statistics
  *   accept_len [1], bonus [1] int32, best_top1p [1] fp32, path [path_capacity]
- *              int32 (path_capacity >= 1 + the largest depth in the bank)
- *              outputs of acceptance, as for entmtp_accept
+ *              int32 (1 + the largest depth in the bank <= path_capacity <=
+ *              ENTMTP_D_MAX + 1)   outputs of acceptance, as for entmtp_accept;
+ *              every step writes all path_capacity entries (-1 past its
+ *              accept length, whatever the depth of its tree)
  *   workspace  scratch of entmtp_step_workspace() bytes, 256-byte aligned,
  *              used by this step object only (it holds attention partials,
  *              statistics partials and the device-scheduled state, which

@@ -45,9 +45,10 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_kernel(
     const int* __restrict__ parent, const int* __restrict__ depth,
     const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
     const int* __restrict__ tok, const int* __restrict__ amax, const float* __restrict__ top1p,
-    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
-    float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
-  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, D + 1,
+    int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
+    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
+    uint32_t seq) {
+  accept_core(parent, depth, mask, path_tab, T, D, tok, amax, top1p, accept_len, path_out, path_cap,
               bonus, best_p, mirror, seq);
 }
 
@@ -90,8 +91,9 @@ __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
     float* __restrict__ top1p, int* __restrict__ amax, const int* __restrict__ parent,
     const int* __restrict__ depth, const uint32_t* __restrict__ mask,
     const int* __restrict__ path_tab, int T, int D, const int* __restrict__ tok,
-    int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
-    float* __restrict__ best_p, StepMirror* __restrict__ mirror, uint32_t seq) {
+    int* __restrict__ accept_len, int* __restrict__ path_out, int path_cap,
+    int* __restrict__ bonus, float* __restrict__ best_p, StepMirror* __restrict__ mirror,
+    uint32_t seq) {
   constexpr int kPathLds = kPathPerThread * kFinAccThreads;
   __shared__ float s_p1[ENTMTP_T_MAX];
   __shared__ int s_am[ENTMTP_T_MAX];
@@ -120,8 +122,8 @@ __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
   }
   __syncthreads();
   (void)accept_finish<kFinAccThreads>(n, greedy_ok(n, s_am, T), lds_path ? s_path : path_tab, T,
-                                      D, s_am, s_p1, accept_len, path_out, D + 1, bonus, best_p,
-                                      mirror, seq);
+                                      D, s_am, s_p1, accept_len, path_out, path_cap, bonus,
+                                      best_p, mirror, seq);
 }
 
 // The same for a tree the device chose: the tree, its drafts and the prefix
@@ -260,14 +262,14 @@ namespace entmtp {
 
 int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draft_tokens,
                       const int32_t* argmax, const float* top1p, int32_t* accept_len,
-                      int32_t* path, int32_t* bonus, float* best_top1p, StepMirror* mirror,
-                      uint32_t seq, hipStream_t stream) {
+                      int32_t* path, int32_t path_capacity, int32_t* bonus, float* best_top1p,
+                      StepMirror* mirror, uint32_t seq, hipStream_t stream) {
   const TopoDesc& d = bank->desc[topo];
   hipLaunchKernelGGL(accept_kernel, dim3(1), dim3(kAcceptThreads), 0, stream,
                      bank_ptr<int>(bank, d.off_parent), bank_ptr<int>(bank, d.off_depth),
                      bank_ptr<uint32_t>(bank, d.off_mask), bank_ptr<int>(bank, d.off_path), d.T,
-                     d.D, draft_tokens, argmax, top1p, accept_len, path, bonus, best_top1p,
-                     mirror, seq);
+                     d.D, draft_tokens, argmax, top1p, accept_len, path, path_capacity, bonus,
+                     best_top1p, mirror, seq);
   return launch_status("accept launch");
 }
 
@@ -288,21 +290,22 @@ int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void
                                int32_t n_parts, int32_t V, float inv_temp, float* entropy,
                                float* top1p,
                                int32_t* argmax, const int32_t* draft_tokens, int32_t* accept_len,
-                               int32_t* path, int32_t* bonus, float* best_top1p,
-                               StepMirror* mirror, uint32_t seq, hipStream_t stream) {
+                               int32_t* path, int32_t path_capacity, int32_t* bonus,
+                               float* best_top1p, StepMirror* mirror, uint32_t seq,
+                               hipStream_t stream) {
   const TopoDesc& d = bank->desc[topo];
   if (d.T > kFusedMaxT) {
     if (int32_t rc = launch_stats_finalize(partials, d.T, V, inv_temp, entropy, top1p, argmax, stream))
       return rc;
-    return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,
-                         best_top1p, mirror, seq, stream);
+    return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path, path_capacity,
+                         bonus, best_top1p, mirror, seq, stream);
   }
   hipLaunchKernelGGL(finalize_accept_kernel, dim3(1), dim3(kFinAccThreads), 0, stream,
                      static_cast<const StatPart*>(partials), n_parts, inv_temp, entropy,
                      top1p, argmax, bank_ptr<int>(bank, d.off_parent),
                      bank_ptr<int>(bank, d.off_depth), bank_ptr<uint32_t>(bank, d.off_mask),
                      bank_ptr<int>(bank, d.off_path), d.T, d.D, draft_tokens, accept_len, path,
-                     bonus, best_top1p, mirror, seq);
+                     path_capacity, bonus, best_top1p, mirror, seq);
   return launch_status("finalize_accept launch");
 }
 
@@ -318,8 +321,9 @@ extern "C" int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo,
                    "draft_tokens, argmax, accept_len, path and bonus must be non-NULL");
   ENTMTP_CHECK_ARG(best_top1p == nullptr || top1p != nullptr, ENTMTP_EINVAL,
                    "best_top1p needs top1p");
-  return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,
-                       best_top1p, nullptr, 0u, static_cast<hipStream_t>(stream));
+  return launch_accept(bank, topo, draft_tokens, argmax, top1p, accept_len, path,
+                       bank->desc[topo].D + 1, bonus, best_top1p, nullptr, 0u,
+                       static_cast<hipStream_t>(stream));
 }
 
 extern "C" int32_t entmtp_accept_batched(const entmtp_bank* bank, int32_t B, const int32_t* topo,

@@ -127,10 +127,12 @@ static_assert(sizeof(StepMirror) == kMirrorWords * sizeof(uint64_t), "mirror lay
 // Launches the accept kernel (no argument checks beyond the bank's); with a
 // non-NULL `mirror` (device address of host memory) it also publishes the
 // result there under sequence number `seq`.
+// path_capacity entries of `path` are written (-1 past the accept length);
+// at least the tree's depth + 1, at most ENTMTP_D_MAX + 1.
 int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draft_tokens,
                       const int32_t* argmax, const float* top1p, int32_t* accept_len,
-                      int32_t* path, int32_t* bonus, float* best_top1p, StepMirror* mirror,
-                      uint32_t seq, hipStream_t stream);
+                      int32_t* path, int32_t path_capacity, int32_t* bonus, float* best_top1p,
+                      StepMirror* mirror, uint32_t seq, hipStream_t stream);
 
 // The device-scheduled form: the tree is bank entry cur->rung; the drafts of
 // bank tree k are row k of drafts [n_topo][tree_rows]; after accepting, the
@@ -181,8 +183,9 @@ int32_t launch_finalize_accept(const entmtp_bank* bank, int32_t topo, const void
                                int32_t n_parts, int32_t V, float inv_temp, float* entropy,
                                float* top1p,
                                int32_t* argmax, const int32_t* draft_tokens, int32_t* accept_len,
-                               int32_t* path, int32_t* bonus, float* best_top1p,
-                               StepMirror* mirror, uint32_t seq, hipStream_t stream);
+                               int32_t* path, int32_t path_capacity, int32_t* bonus,
+                               float* best_top1p, StepMirror* mirror, uint32_t seq,
+                               hipStream_t stream);
 
 template <typename T>
 inline const T* bank_ptr(const entmtp_bank* b, int64_t off) {

@@ -174,8 +174,9 @@ int32_t check_config(const entmtp_bank* bank, const entmtp_step_config* c, int32
                    "statistics outputs must be non-NULL and logits (if any) 16-byte aligned");
   ENTMTP_CHECK_ARG(c->accept_len && c->bonus && c->best_top1p && c->path, ENTMTP_EINVAL,
                    "acceptance outputs must be non-NULL");
-  ENTMTP_CHECK_ARG(c->path_capacity >= *D_max + 1, ENTMTP_EINVAL,
-                   "path_capacity = %d below 1 + the bank's depth %d", c->path_capacity, *D_max);
+  ENTMTP_CHECK_ARG(c->path_capacity >= *D_max + 1 && c->path_capacity <= ENTMTP_D_MAX + 1,
+                   ENTMTP_EINVAL, "path_capacity = %d outside [1 + the bank's depth %d, %d]",
+                   c->path_capacity, *D_max, ENTMTP_D_MAX + 1);
   ENTMTP_CHECK_ARG(c->tau_off <= c->tau_on, ENTMTP_EINVAL, "tau_off %g > tau_on %g",
                    static_cast<double>(c->tau_off), static_cast<double>(c->tau_on));
   return ENTMTP_OK;
@@ -425,8 +426,8 @@ extern "C" int32_t entmtp_step_launch(entmtp_step* st, int32_t topo, int32_t pre
   const uint32_t seq = st->seq + 1u == 0u ? 1u : st->seq + 1u;   // 0 is the record's initial tag
   auto finalize = [&]() {
     return launch_finalize_accept(st->bank, topo, part, st->lm_parts, c.V, c.inv_temp, c.entropy,
-                                  c.top1p, c.argmax, draft_tokens, c.accept_len, c.path, c.bonus,
-                                  c.best_top1p, st->dev, seq, s);
+                                  c.top1p, c.argmax, draft_tokens, c.accept_len, c.path,
+                                  c.path_capacity, c.bonus, c.best_top1p, st->dev, seq, s);
   };
   if (c.n_layers > 1)
     if (int32_t rc = finalize()) return rc;

@@ -178,14 +178,19 @@ def test_kv_compact_batched(api, trees):
         np.testing.assert_array_equal(host_bits(vcs[b]), rv)
 
 
-def test_batched_step_end_to_end(api, trees):
+@pytest.mark.parametrize("topo,lens,V", [
+    ([0, 1, 2, 0], [700, 64, 1500, 1023], 32000),
+    # 64- and 128-node trees: 336 rows, three 128-row LM-head passes
+    ([4, 3, 1, 4], [513, 2048, 90, 4000], 32000),
+    # the benchmark's vocabulary: 2048 statistics partials per node
+    ([4, 2], [1500, 777], 128256),
+])
+def test_batched_step_end_to_end(api, trees, topo, lens, V):
     """Attention, the LM head and statistics over the concatenated rows,
     acceptance and compaction of a batch, each sequence against the oracle's
-    step on its own rows (GQA 32:8, hidden 4096, vocab 32000 to keep the fp64
-    oracle quick; the 128k vocabulary is covered by the sampled LM-head test)."""
-    Hq, Hkv, hid, V = WL.n_heads, WL.n_kv_heads, WL.hidden, 32000
-    topo = [0, 1, 2, 0]
-    lens = [700, 64, 1500, 1023]
+    step on its own rows (GQA 32:8, hidden 4096)."""
+    Hq, Hkv, hid = WL.n_heads, WL.n_kv_heads, WL.hidden
+    say("batched step", topo, lens, V)
     B = len(topo)
     cap = max(lens) + 128 + 8
     scale = 1 / math.sqrt(D_HEAD)

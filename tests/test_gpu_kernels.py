@@ -367,6 +367,20 @@ def test_tree_attn_mask_leakage(api):
         pert = synth.AttnInputs(inp.q, kt, vt, inp.k_cache, inp.v_cache)
         out, _, _ = run_attn(api, bank, 0, pert, L, 0.1, 10000.0)
         np.testing.assert_array_equal(out[i], base[i])
+    # the other half: a node's own path does reach it.  Perturbing one node's
+    # key and value changes exactly the rows of the nodes it is an ancestor
+    # of (itself included), and leaves every other row as it was.
+    for j in (0, 3, 11, 26):
+        kt, vt = inp.k_tree.copy(), inp.v_tree.copy()
+        kt[j] = synth.f32_to_bf16_bits(g.standard_normal(kt[j].shape).astype(np.float32))
+        vt[j] = synth.f32_to_bf16_bits(g.standard_normal(vt[j].shape).astype(np.float32))
+        pert = synth.AttnInputs(inp.q, kt, vt, inp.k_cache, inp.v_cache)
+        out, _, _ = run_attn(api, bank, 0, pert, L, 0.1, 10000.0)
+        for i in range(T):
+            if j in anc[i]:
+                assert not np.array_equal(out[i], base[i]), (j, i)
+            else:
+                np.testing.assert_array_equal(out[i], base[i])
 
 
 @pytest.mark.parametrize("name,T,L,Hq,Hkv", [("7b_tree27", 27, 256, 32, 32),

@@ -139,7 +139,12 @@ def run_loop(api, n_layers, n_steps, Hq=8, Hkv=2, hid=512, V=1000, L0=40, start_
         api.accept(bank, rung, tok_d, am2, p12, a2, path2, b2, s2)
         api.kv_compact(path2, a2, L, kc2, vc2)
         torch.cuda.synchronize()
-        pairs = [(out[:, :T], out2[:, :T]), (st.argmax[:T], am2[:T]), (st.path, path2)]
+        # entmtp_accept writes its tree's D + 1 path entries; the step writes
+        # its whole path buffer (-1 past the accept length, whatever the depth
+        # of the tree before)
+        Dt = bank.D[rung]
+        pairs = [(out[:, :T], out2[:, :T]), (st.argmax[:T], am2[:T]), (st.path[:Dt + 1], path2[:Dt + 1])]
+        assert (st.path[Dt + 1:] == -1).all()
         for mine, theirs in ((st.entropy[:T], H2[:T]), (st.top1p[:T], p12[:T])):
             torch.testing.assert_close(mine, theirs, rtol=RTOL_ORDER, atol=ATOL_ORDER)
         if flush_each:
@@ -326,13 +331,14 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
     st_h = api.Step(bank, kc_h, vc_h, W, keep_logits=False, **kw)
     st_d = api.Step(bank, kc_d, vc_d, W, keep_logits=False, tau_on=0.8, tau_off=0.6, **kw)
     deltas, spikes = synth.regime_spikes(WL, n_steps, Tmax, V, hid)
-    steps = []
+    steps, host_steps = [], []
     for t in range(n_steps):
         layers, x, am, u, r = step_inputs(t, n_layers, Tmax, Hq, Hkv, d, w_bits, w64,
                                           float(deltas[t]), spikes[t])
         drafts = np.zeros((K, Tmax), np.int32)
         for k in range(K):
             drafts[k, : bank.T[k]] = synth.draft_tokens(trees[k], am, u, r, 0.7)
+        host_steps.append((layers, x, drafts))
         steps.append({"q": dev_bf16(stack(layers, "q")), "kt": dev_bf16(stack(layers, "k_tree")),
                       "vt": dev_bf16(stack(layers, "v_tree")), "x": dev_bf16(x),
                       "drafts": dev_i32(drafts)})
@@ -374,7 +380,44 @@ def test_device_scheduled_loop_matches_host_scheduled(api, n_layers, with128):
     assert int(st_d.accept_len.item()) == trace[-1][2] == int(st_h.accept_len.item())
     a_last = trace[-1][2]
     assert torch.equal(st_d.path[: a_last + 1], st_h.path[: a_last + 1])
-    assert (st_d.path[a_last + 1:] == -1).all()
+    assert (st_d.path[a_last + 1:] == -1).all() and (st_h.path[a_last + 1:] == -1).all()
+
+    # the device log replayed on the oracle, step by step from the oracle's own
+    # caches: tree and prefix as the oracle's ladder leaves them, accept length
+    # exact, s within 1e-3; a next tree that differs from the ladder's choice on
+    # the oracle's s is allowed only when that s lies within 1e-3 of a threshold
+    kc_o = [b.k_cache for b in base]
+    vc_o = [b.v_cache for b in base]
+    rung, L = rung0, L0
+    for t in range(n_steps):
+        layers, x, drafts = host_steps[t]
+        T = bank.T[rung]
+        g_s = float(log_h[t, 3:4].view(np.float32)[0])
+        assert tuple(int(v) for v in log_h[t, :2]) == (rung, L), (t, log_h[t])
+        ref = orc.verify_step(trees[rung], layers[0].q[:T], layers[0].k_tree[:T],
+                              layers[0].v_tree[:T], kc_o[0], vc_o[0], L, x[:T], w_bits,
+                              drafts[rung, :T], scale, theta)
+        assert int(log_h[t, 2]) == ref["accept_len"], t
+        assert abs(g_s - ref["s"]) <= RTOL_STATS * ref["s"] + 1e-6
+        assert np.abs(out_d[t, 0, :T].float().cpu().numpy() - ref["out"]).max() <= ATOL_BF16
+        kc_o[0], vc_o[0] = ref["k_cache"], ref["v_cache"]
+        for l in range(1, n_layers):
+            _, rk, rv = orc.tree_attention(layers[l].q[:T], layers[l].k_tree[:T],
+                                           layers[l].v_tree[:T], kc_o[l], vc_o[l], L, trees[rung],
+                                           scale, theta)
+            kc_o[l], vc_o[l] = orc.kv_compact(rk, rv, L, ref["path"])
+        L += ref["accept_len"] + 1
+        nxt = orc.ladder_next(rung, K, ref["s"], 0.8, 0.6)
+        if t + 1 < n_steps and int(log_h[t + 1, 0]) != nxt:
+            near = min(abs(ref["s"] - 0.8) / 0.8, abs(ref["s"] - 0.6) / 0.6)
+            assert near <= RTOL_STATS, (t, ref["s"])
+            nxt = int(log_h[t + 1, 0])
+        rung = nxt
+    kd = host_bits(kc_d)
+    vd = host_bits(vc_d)
+    for l in range(n_layers):
+        np.testing.assert_array_equal(kd[l][:, :L], kc_o[l][:, :L])
+        np.testing.assert_array_equal(vd[l][:, :L], vc_o[l][:, :L])
     st_h.close()
     st_d.close()
 
