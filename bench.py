@@ -2,25 +2,33 @@
 """Tree-verification step benchmark on one MI355X.
 
 A step is one pass of the whole verification hot path at batch 1:
-  host: pick the tree for this step with the hysteretic ladder (tau_on 0.8,
-        tau_off 0.6) from the previous step's top-1 probability at the
-        deepest accepted node;
+  host: pick the tree for this step (the hysteretic ladder, tau_on 0.8,
+        tau_off 0.6, over the previous step's top-1 probability at the
+        deepest accepted node; a one-tree bank always picks its tree);
   GPU:  tree attention (tree K/V appended to the cache), LM-head logits with
         fused softmax statistics -> greedy acceptance, and KV compaction, all
         enqueued by one entmtp_step_launch (the compaction of a step goes out
         with the next step's launch, on the cache stream, beside the next LM
         head);
   host: poll the pinned record acceptance publishes (accept length, s, path)
-        -- the step's one device-to-host read -- and grow the prefix by
-        accept_len + 1.
+        -- the step's one device-to-host read -- and move the prefix.
 The timed region ends with a flush, so it holds exactly K compactions.
 
-Default workload: Vicuna-7B shapes (32 x 128 heads, hidden 4096, vocab
-32000), a 5-tree bank with {1, 8, 26, 64, 128} nodes, prefix 2048 growing
-every step.  Inputs are seeded synthetic tensors staged in HBM before timing
-(a pool of per-step inputs is cycled); two copies of the LM-head weight
-alternate between steps so that the 256 MB last-level cache cannot serve the
-weight stream.
+Default workload: Vicuna-7B shapes (32 x 128 heads, hidden 4096, vocabulary
+32000), one attention layer and the LM head, a 27-node tree of depth 4 over
+a 256-token prefix, the prefix reset every step (each step verifies a fresh
+tree at the same position).  ``--workload`` selects the others: the 5-tree
+bank {1, 8, 26, 64, 128} at prefix 2048 growing every step, the 32-layer
+stack, the 13B shapes and the batch-8 GQA step.  Inputs are seeded synthetic
+tensors staged in HBM before timing (a pool of per-step inputs is cycled);
+two copies of the LM-head weight alternate between steps so that the 256 MB
+last-level cache cannot serve the weight stream.
+
+After the default run, a switching study on the 5-tree bank (prefix fixed at
+2048) compares steps whose tree the ladder picks, and steps whose tree moves
+by one rung every step, with steps on one fixed tree each, weighted by the
+same tree-size histogram; arming is the same in all runs, so the difference
+is what switching trees costs.
 
 Prints ONE JSON line.  ``--gpus N`` with N > 1 exits: the build targets one GPU.
 """
@@ -39,6 +47,9 @@ import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
 METRIC = "tree-verify steps/sec and µs/step at batch 1; achieved HBM GB/s vs peak"
+MIN_TIMED_LAUNCHES = 16
+SINGLE_WORKLOADS = ["tree27_L256_7b", "bank5_L2048_7b", "tree64_L4096_7b_32layer",
+                    "tree128_L8192_13b"]
 
 
 def parse():
@@ -46,18 +57,21 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=1000)
     ap.add_argument("--warmup", type=int, default=50)
-    ap.add_argument("--workload", default="bank5_L2048_7b",
-                    choices=["bank5_L2048_7b", "tree27_L256_7b", "tree64_L4096_7b_32layer",
-                             "tree128_L8192_13b", "batch8_gqa_v128k"])
+    ap.add_argument("--workload", default="tree27_L256_7b",
+                    choices=SINGLE_WORKLOADS + ["batch8_gqa_v128k"])
     ap.add_argument("--pool", type=int, default=32, help="distinct per-step input sets")
     ap.add_argument("--weight-copies", type=int, default=2)
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-extras", action="store_true",
-                    help="skip the timings of the typical-acceptance and frontier kernels")
+                    help="skip the switching study and the timings of the typical-acceptance, "
+                         "speculative-sampling and frontier kernels")
     ap.add_argument("--event-every", type=int, default=8,
-                    help="time the LM head with HIP events on a seeded random 1/n of the timed steps (each "
-                         "event pair costs the host a few microseconds)")
+                    help="time the LM head with HIP events on a seeded random 1/n of the timed steps "
+                         f"(at least {MIN_TIMED_LAUNCHES}; each event pair costs the host a few "
+                         "microseconds)")
     ap.add_argument("--cpu-budget-s", type=float, default=20.0)
+    ap.add_argument("--switch-steps", type=int, default=300,
+                    help="timed steps per run of the switching study")
     ap.add_argument("--fixed-topo", type=int, default=-1,
                     help="disable the scheduler and use this bank entry every step")
     ap.add_argument("--graph", action="store_true",
@@ -67,7 +81,7 @@ def parse():
                          "result is read, instead of enqueueing it ahead behind a gate")
     ap.add_argument("--gpu-scheduler", action="store_true",
                     help="run the ladder on the GPU (no result read per step) instead of on "
-                         "the host; the same decisions")
+                         "the host; the same decisions (5-tree bank workload)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 256 MiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
@@ -126,6 +140,276 @@ def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
 
 
+class SingleSeq:
+    """A single-sequence workload staged in HBM: the LM-head weight copies, the
+    per-layer caches, a pool of per-step inputs with their draft tokens for
+    every bank tree, and one step context on a stream of its own."""
+
+    def __init__(self, api, synth, torch, name, pool_size, weight_copies, cap_steps,
+                 device_prefix_fixed=False):
+        self.api, self.synth, self.torch, self.lib = api, synth, torch, api.lib
+        dev = self.dev = torch.device("cuda:0")
+        wl = self.wl = synth.WORKLOADS[name]
+        self.Hq, self.Hkv, self.d, self.hid, self.V = (wl.n_heads, wl.n_kv_heads, wl.head_dim,
+                                                       wl.hidden, wl.vocab)
+        Hq, Hkv, d, hid, V = self.Hq, self.Hkv, self.d, self.hid, self.V
+        self.trees = synth.workload_trees(wl)
+        self.bank = api.Bank(self.trees)
+        self.n_topo = len(self.trees)
+        self.Ts = self.bank.T
+        Tmax, Dmax = max(self.bank.T), max(self.bank.D)
+        self.L0 = wl.prefix_len
+        self.cap = cap = self.L0 + cap_steps * (Dmax + 1) + Tmax + 64
+        self.scale, self.theta = 1.0 / math.sqrt(d), wl.rope_theta
+        self.NL = NL = wl.n_layers
+        log(f"workload {wl.name}: bank T={self.bank.T} D={self.bank.D}, L0={self.L0}, cap={cap}")
+        t0 = time.time()
+        bf = torch.bfloat16
+
+        def to_dev(bits):
+            return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(bf).to(dev)
+
+        self.w_host = synth.lm_head_weight(wl.ident, V, hid)
+        W = [to_dev(self.w_host)]
+        for _ in range(1, weight_copies):
+            W.append(W[0].clone())
+        self.W = W
+        base = synth.attn_inputs(wl.ident, 1, Hq, Hkv, d, self.L0, cap)
+        self.kc0_host = base.k_cache[:, :self.L0].copy()
+        self.vc0_host = base.v_cache[:, :self.L0].copy()
+        self.k_cache = torch.zeros((NL, Hkv, cap, d), dtype=bf, device=dev)   # [layer][head][slot][dim]
+        self.v_cache = torch.zeros((NL, Hkv, cap, d), dtype=bf, device=dev)
+        self.k_cache[0, :, :self.L0] = to_dev(self.kc0_host)
+        self.v_cache[0, :, :self.L0] = to_dev(self.vc0_host)
+        del base
+        # further layers (the 32-layer workload): seeded N(0, 1) drawn on the
+        # GPU, a generator per layer (the oracle baseline covers one layer)
+        gen = torch.Generator(device=dev)
+
+        def randn_dev(shape, seed):
+            gen.manual_seed(seed)
+            return torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(bf)
+
+        for l in range(1, NL):
+            self.k_cache[l, :, :self.L0] = randn_dev((Hkv, self.L0, d), 1000 * wl.ident + 2 * l)
+            self.v_cache[l, :, :self.L0] = randn_dev((Hkv, self.L0, d), 1000 * wl.ident + 2 * l + 1)
+
+        # the scheduler workload plants a confidence regime in the hidden
+        # states (a lift on one token per row) so that the ladder moves
+        lifted = self.n_topo > 1
+        P = self.P = pool_size if NL == 1 else min(pool_size, 4)
+        deltas, spike_tok = synth.regime_spikes(wl.ident, P, Tmax, V, hid)
+        pool = []
+        for e in range(P):
+            a_in = synth.attn_inputs(wl.ident, Tmax, Hq, Hkv, d, 0, Tmax, step=e + 1)
+            x = synth.hidden_rows(wl.ident, Tmax, hid, step=e + 1)
+            if lifted:
+                x = synth.plant_spike(x, self.w_host, spike_tok[e], float(deltas[e]), wl.w_std)
+            u, r = synth.draft_randoms(wl.ident, Tmax, V, step=e + 1)
+            q_l, kt_l, vt_l = [to_dev(a_in.q)], [to_dev(a_in.k_tree)], [to_dev(a_in.v_tree)]
+            for l in range(1, NL):   # layer-major, as the step reads them
+                sd = 1000 * wl.ident + 100 * (e + 1) + 3 * l
+                q_l.append(randn_dev((Tmax, Hq, d), sd))
+                kt_l.append(randn_dev((Tmax, Hkv, d), sd + 1))
+                vt_l.append(randn_dev((Tmax, Hkv, d), sd + 2))
+            pool.append({"q": torch.stack(q_l), "kt": torch.stack(kt_l), "vt": torch.stack(vt_l),
+                         "x": to_dev(x), "u": u, "r": r,
+                         "host": (a_in.q, a_in.k_tree, a_in.v_tree, x)})
+        self.pool = pool
+        log(f"staged inputs in {time.time() - t0:.1f}s")
+
+        # the step loop runs on a stream of its own (non-blocking: launches on
+        # the legacy default stream cost the host more); the LM-head weight
+        # copy is passed per step; the statistics come from the LM head's
+        # accumulators, so no logits are materialised
+        self.stream = torch.cuda.Stream()
+        self.st = api.Step(self.bank, self.k_cache, self.v_cache, W[0], n_layers=NL, Hq=Hq,
+                           Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax, scale=self.scale,
+                           rope_theta=self.theta, keep_logits=False, tau_on=0.8, tau_off=0.6,
+                           device_prefix_fixed=device_prefix_fixed,
+                           cache_layer_stride=Hkv * cap * d, stream=self.stream)
+        torch.cuda.synchronize()
+        self.out = torch.empty((NL, Tmax, Hq, d), dtype=bf, device=dev)
+
+        # draft tokens: the target's greedy token at the parent with
+        # probability p_acc, computed with the library itself on each pool
+        # entry (input synthesis; the separate logits and statistics kernels,
+        # so that the counters of the timed fused kernel are not mixed with
+        # these staging launches)
+        lg = torch.empty((Tmax, V), dtype=torch.float32, device=dev)
+        for e in pool:
+            api.verify_logits(e["x"], W[0], lg)
+            api.logit_stats(lg, 1.0, None, None, self.st.argmax)
+            am = self.st.argmax.cpu().numpy()
+            e["tok"] = [synth.draft_tokens(self.trees[k], am, e["u"], e["r"], wl.p_acc)
+                        for k in range(self.n_topo)]
+            e["tok_dev"] = [torch.from_numpy(t).to(dev) for t in e["tok"]]
+            table = np.zeros((self.n_topo, Tmax), np.int32)
+            for k, t in enumerate(e["tok"]):
+                table[k, : len(t)] = t
+            e["drafts_dev"] = torch.from_numpy(table).to(dev)
+        del lg
+        torch.cuda.synchronize()
+        P_ = ctypes.c_void_p
+        self.pool_p = [{"q": P_(e["q"].data_ptr()), "kt": P_(e["kt"].data_ptr()),
+                        "vt": P_(e["vt"].data_ptr()), "x": P_(e["x"].data_ptr()),
+                        "tok": [P_(t.data_ptr()) for t in e["tok_dev"]],
+                        "drafts": P_(e["drafts_dev"].data_ptr())} for e in pool]
+        self.W_p = [P_(w.data_ptr()) for w in W]
+        self.out_p = P_(self.out.data_ptr())
+
+    def chk(self, rc):
+        if rc:
+            raise self.api.EntmtpError(rc, self.api.last_error())
+
+    def run(self, K, warmup, policy, *, grow, start_rung=0, arm=True, arm_reach=True,
+            n_events=0, on_gpu=False, graph=False, step_times=None):
+        """Runs `warmup` untimed and K timed steps.  policy(topo, s) gives the
+        next step's tree from the current one and the step's s (host-
+        scheduled steps).  grow: the prefix grows by the accepted tokens (else
+        every step verifies at L0).  arm: each next step's LM head is enqueued
+        behind a gate while the step before is pending, sized for the next
+        rung (arm_reach) or for the current tree.  n_events: timed steps whose
+        LM head carries a HIP event pair (a seeded random choice).  on_gpu:
+        the ladder runs on the GPU (entmtp_step_launch_device), optionally
+        replayed as captured graph segments (the prefix then grows unless the
+        step context was made with a fixed device prefix).  step_times: a list
+        that receives the host clock after every timed step."""
+        torch, lib = self.torch, self.lib
+        h = self.st.handle
+        Ts, n_topo, P = self.Ts, self.n_topo, self.P
+        pool_p, W_p, out_p = self.pool_p, self.W_p, self.out_p
+        total = warmup + K
+        steplog = torch.full((total, 4), -1, dtype=torch.int32, device=self.dev)
+        log_base = ctypes.c_void_p(steplog.data_ptr())
+        a_c, b_c, s_c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
+        a_r, b_r, s_r = ctypes.byref(a_c), ctypes.byref(b_c), ctypes.byref(s_c)
+        state = {"L": self.L0, "rung": start_rung}
+        armed = [False, 0]        # armed?, the rows the armed LM head covers
+        lm_rows = []              # rows of the LM head each host-scheduled step ran
+        chk = self.chk
+
+        def step_gpu(t, ev=(None, None)):
+            # nothing is read back: the next step's tree and prefix stay on the GPU
+            e = pool_p[t % P]
+            chk(lib.entmtp_step_launch_device(h, e["q"], e["kt"], e["vt"], out_p, e["x"],
+                                              W_p[t % len(W_p)], e["drafts"], log_base, total,
+                                              ev[0], ev[1]))
+
+        def step(t, ev=(None, None), ev_next=(None, None), arm_next=False):
+            L = state["L"] if grow else self.L0
+            topo = state["rung"]
+            e = pool_p[t % P]
+            if armed[0]:   # the LM head and its events are in the queue already
+                ev = (None, None)
+            chk(lib.entmtp_step_launch(h, topo, L, e["q"], e["kt"], e["vt"], out_p, e["x"],
+                                       W_p[t % len(W_p)], e["tok"][topo], ev[0], ev[1]))
+            lm_rows.append(armed[1] if armed[0] and Ts[topo] <= armed[1] else Ts[topo])
+            armed[0] = False
+            if arm and arm_next:
+                nx = pool_p[(t + 1) % P]
+                bound = Ts[min(topo + 1, n_topo - 1)] if arm_reach else Ts[topo]
+                chk(lib.entmtp_step_arm(h, nx["x"], W_p[(t + 1) % len(W_p)], bound, ev_next[0],
+                                        ev_next[1]))
+                armed[:] = [True, bound]
+            chk(lib.entmtp_step_wait(h, a_r, b_r, s_r, 30.0))
+            a, s = a_c.value, s_c.value
+            if grow:
+                state["L"] = L + a + 1
+            state["rung"] = policy(topo, s)
+            return Ts[topo], L, a, s, topo
+
+        # timed steps whose LM head carries an event pair: a seeded random
+        # choice (a fixed stride can alias with the ladder's cycle through the
+        # bank)
+        sampled = sorted(np.random.default_rng(7).choice(K, min(K, n_events), replace=False).tolist())
+        events = [(TimingEvent(), TimingEvent()) for _ in sampled]
+        ev_p = {t: (a_.ptr, b_.ptr) for t, (a_, b_) in zip(sampled, events)}
+        trace = []
+        graphs, graph_steps = [], 0
+        if on_gpu:
+            chk(lib.entmtp_step_device_start(h, state["rung"], self.L0))
+        torch.cuda.synchronize()
+        # no garbage collection inside the timed region: a full collection of
+        # the interpreter's heap stalls the host loop for tens of milliseconds
+        # (collected before the warm-up, so that the warm-up steps run right
+        # before the timed ones and the GPU does not sit idle in between)
+        gc.collect()
+        gc.disable()
+        for t in range(warmup):
+            if on_gpu:
+                step_gpu(t)
+            else:
+                step(t, arm_next=t + 1 < warmup)
+        chk(lib.entmtp_step_flush(h))   # the last warm-up step's compaction
+        if on_gpu and graph:
+            # segments of SEG steps (a whole number of input-pool and
+            # weight-copy cycles, and of the device state ring), all captured
+            # after the warm-up, before the timed region; the steps past the last whole segment
+            # run eagerly (and carry the LM-head events, which graph replays
+            # do not)
+            SEG = math.lcm(P, len(W_p), 4)
+            for g0 in range(0, K - K % SEG, SEG):
+                ts = range(warmup + g0, warmup + g0 + SEG)
+                arr = lambda vals: (ctypes.c_void_p * SEG)(*[v.value for v in vals])   # noqa: E731
+                gh = ctypes.c_void_p()
+                chk(lib.entmtp_step_device_graph(
+                    h, SEG, arr([pool_p[t % P]["q"] for t in ts]),
+                    arr([pool_p[t % P]["kt"] for t in ts]), arr([pool_p[t % P]["vt"] for t in ts]),
+                    arr([out_p] * SEG), arr([pool_p[t % P]["x"] for t in ts]),
+                    arr([W_p[t % len(W_p)] for t in ts]), arr([pool_p[t % P]["drafts"] for t in ts]),
+                    log_base, total, ctypes.byref(gh)))
+                graphs.append(gh)
+            graph_steps = len(graphs) * SEG
+            sampled = [t for t in sampled if t >= graph_steps]
+            log(f"captured {len(graphs)} graphs of {SEG} steps")
+        torch.cuda.synchronize()
+        # HIP API calls between two hipMemGetInfo calls are the timed region's
+        # (the marker a rocprofv3 API trace of this run is cut at)
+        torch.cuda.mem_get_info()
+        t_start = time.perf_counter()
+        for g in graphs:
+            chk(lib.entmtp_step_graph_launch(h, g))
+        for t in range(graph_steps, K):
+            if on_gpu:
+                step_gpu(warmup + t, ev_p.get(t, (None, None)))
+            else:
+                trace.append(step(warmup + t, ev_p.get(t, (None, None)),
+                                  ev_p.get(t + 1, (None, None)), t + 1 < K))
+            if step_times is not None:
+                step_times.append(time.perf_counter())
+        chk(lib.entmtp_step_flush(h))   # the last timed step's compaction
+        torch.cuda.synchronize()
+        elapsed = time.perf_counter() - t_start
+        torch.cuda.mem_get_info()
+        gc.enable()
+        if step_times is not None:
+            step_times.insert(0, t_start)
+        events = [ev for t, ev in zip(ev_p, events) if t >= graph_steps]
+        for g in graphs:
+            lib.entmtp_step_graph_destroy(g)
+        if on_gpu:   # the steps' (tree, prefix, accept length, s) as the GPU logged them
+            lg = steplog.cpu().numpy()[warmup:]
+            trace = [(Ts[int(r)], int(L), int(a), float(np.int32(sb).view(np.float32)), int(r))
+                     for r, L, a, sb in lg]
+            state["L"] = int(lg[-1, 1] + lg[-1, 2] + 1)
+        lm_ms = [a.elapsed_time(b) for a, b in events]
+        timed_rows = lm_rows[len(lm_rows) - len(trace):] if len(lm_rows) >= len(trace) else []
+        return {"elapsed": elapsed, "trace": trace, "lm_ms": lm_ms, "sampled": sampled,
+                "lm_rows": timed_rows, "L_end": state["L"]}
+
+
+def ladder(lib, n_topo):
+    return lambda topo, s: lib.entmtp_ladder_next(topo, n_topo, s, 0.8, 0.6)
+
+
+def histogram(vals):
+    h = {}
+    for v in vals:
+        h[v] = h.get(v, 0) + 1
+    return dict(sorted(h.items()))
+
+
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
@@ -141,249 +425,33 @@ def main():
     if args.calibrate_copy:
         calibrate_copy()
         return
-    dev = torch.device("cuda:0")
-    torch.cuda.set_device(dev)
+    torch.cuda.set_device(torch.device("cuda:0"))
     lib = api.lib
 
     if args.workload == "batch8_gqa_v128k":
         run_batched(args, api, synth, torch, lib)
         return
-    wl = synth.WORKLOADS[args.workload]
-    Hq, Hkv, d, hid, V = wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.hidden, wl.vocab
-    trees = synth.workload_trees(wl)
-    bank = api.Bank(trees)
-    n_topo = len(trees)
-    Tmax = max(bank.T)
-    Dmax = max(bank.D)
-    L0 = wl.prefix_len
     grows = args.workload == "bank5_L2048_7b"
     total_steps = args.warmup + args.steps
-    cap = L0 + (total_steps * (Dmax + 1) if grows else 0) + Tmax + 64
-    scale = 1.0 / math.sqrt(d)
-    theta = wl.rope_theta
-    log(f"workload {wl.name}: bank T={bank.T} D={bank.D}, L0={L0}, cap={cap}")
-
-    # ---------------------------------------------------------- staging
-    t0 = time.time()
-    bf = torch.bfloat16
-
-    def to_dev(bits):
-        return torch.from_numpy(np.ascontiguousarray(bits).view(np.int16)).view(bf).to(dev)
-
-    w_host = synth.lm_head_weight(wl.ident, V, hid)
-    W = [to_dev(w_host)]
-    for c in range(1, args.weight_copies):
-        W.append(W[0].clone())
-    NL = wl.n_layers
-    base = synth.attn_inputs(wl.ident, 1, Hq, Hkv, d, L0, cap)
-    kc0_host, vc0_host = base.k_cache[:, :L0].copy(), base.v_cache[:, :L0].copy()
-    k_cache = torch.zeros((NL, Hkv, cap, d), dtype=bf, device=dev)   # [layer][head][slot][dim]
-    v_cache = torch.zeros((NL, Hkv, cap, d), dtype=bf, device=dev)
-    k_cache[0, :, :L0] = to_dev(kc0_host)
-    v_cache[0, :, :L0] = to_dev(vc0_host)
-    del base
-    # further layers (the 32-layer workload): seeded N(0, 1) drawn on the GPU,
-    # a generator per layer (the oracle baseline covers single-layer work)
-    gen = torch.Generator(device=dev)
-
-    def randn_dev(shape, seed):
-        gen.manual_seed(seed)
-        return torch.randn(shape, generator=gen, device=dev, dtype=torch.float32).to(bf)
-
-    for l in range(1, NL):
-        k_cache[l, :, :L0] = randn_dev((Hkv, L0, d), 1000 * wl.ident + 2 * l)
-        v_cache[l, :, :L0] = randn_dev((Hkv, L0, d), 1000 * wl.ident + 2 * l + 1)
-
-    P = args.pool if NL == 1 else min(args.pool, 4)
-    deltas, spike_tok = synth.regime_spikes(wl.ident, P, Tmax, V, hid)
-    pool = []
-    for e in range(P):
-        a_in = synth.attn_inputs(wl.ident, Tmax, Hq, Hkv, d, 0, Tmax, step=e + 1)
-        x = synth.hidden_rows(wl.ident, Tmax, hid, step=e + 1)
-        if grows:
-            x = synth.plant_spike(x, w_host, spike_tok[e], float(deltas[e]), wl.w_std)
-        u, r = synth.draft_randoms(wl.ident, Tmax, V, step=e + 1)
-        q_l, kt_l, vt_l = [to_dev(a_in.q)], [to_dev(a_in.k_tree)], [to_dev(a_in.v_tree)]
-        for l in range(1, NL):   # layer-major, as the step reads them
-            sd = 1000 * wl.ident + 100 * (e + 1) + 3 * l
-            q_l.append(randn_dev((Tmax, Hq, d), sd))
-            kt_l.append(randn_dev((Tmax, Hkv, d), sd + 1))
-            vt_l.append(randn_dev((Tmax, Hkv, d), sd + 2))
-        pool.append({"q": torch.stack(q_l), "kt": torch.stack(kt_l), "vt": torch.stack(vt_l),
-                     "x": to_dev(x), "u": u, "r": r,
-                     "host": (a_in.q, a_in.k_tree, a_in.v_tree, x)})
-    log(f"staged inputs in {time.time() - t0:.1f}s")
-
-    # the step loop runs on a stream of its own (non-blocking: launches on the
-    # legacy default stream cost the host more); one step context, the
-    # LM-head weight copy passed per step; the statistics come from the LM
-    # head's accumulators, so no logits are materialised
-    run_stream = torch.cuda.Stream()
-    # the ladder runs on the host (one result read per step, as in the paper's
-    # loop) or, with --gpu-scheduler, on the GPU for the growing-prefix
-    # workload (the same decisions); a fixed topology is a ladder that never
-    # moves
-    on_gpu = grows and args.gpu_scheduler
-    tau_on, tau_off = (0.8, 0.6) if args.fixed_topo < 0 else (float("inf"), float("-inf"))
-    st = [api.Step(bank, k_cache, v_cache, W[0], n_layers=NL, Hq=Hq, Hkv=Hkv, d=d, cap=cap,
-                   tree_rows=Tmax, scale=scale, rope_theta=theta, keep_logits=False, tau_on=tau_on,
-                   tau_off=tau_off, cache_layer_stride=Hkv * cap * d, stream=run_stream)]
-    torch.cuda.synchronize()
-    out = torch.empty((NL, Tmax, Hq, d), dtype=bf, device=dev)
-
-    # draft tokens: the target's greedy token at the parent with prob p_acc,
-    # computed with the library itself on each pool entry (input synthesis)
-    # (the separate logits and statistics kernels, so that the counters of the
-    # timed fused kernel are not mixed with these staging launches)
-    lg = torch.empty((Tmax, V), dtype=torch.float32, device=dev)
-    for e in pool:
-        api.verify_logits(e["x"], W[0], lg)
-        api.logit_stats(lg, 1.0, None, None, st[0].argmax)
-        am = st[0].argmax.cpu().numpy()
-        e["tok"] = [synth.draft_tokens(trees[k], am, e["u"], e["r"], wl.p_acc) for k in range(n_topo)]
-        e["tok_dev"] = [torch.from_numpy(t).to(dev) for t in e["tok"]]
-        table = np.zeros((n_topo, Tmax), np.int32)
-        for k, t in enumerate(e["tok"]):
-            table[k, : len(t)] = t
-        e["drafts_dev"] = torch.from_numpy(table).to(dev)
-    del lg
-    torch.cuda.synchronize()
-
-    # ---------------------------------------------------------- raw step
-    P_ = ctypes.c_void_p
-    handles = [s_.handle for s_ in st]
-    out_p = P_(out.data_ptr())
-    pool_p = [{"q": P_(e["q"].data_ptr()), "kt": P_(e["kt"].data_ptr()), "vt": P_(e["vt"].data_ptr()),
-               "x": P_(e["x"].data_ptr()), "tok": [P_(t.data_ptr()) for t in e["tok_dev"]],
-               "drafts": P_(e["drafts_dev"].data_ptr())}
-              for e in pool]
-    W_p = [P_(w.data_ptr()) for w in W]
-    total = args.warmup + args.steps
-    steplog = torch.full((total, 4), -1, dtype=torch.int32, device=dev)
-    log_base = P_(steplog.data_ptr())
-    Ts = bank.T
-    a_c, b_c, s_c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
-    a_r, b_r, s_r = ctypes.byref(a_c), ctypes.byref(b_c), ctypes.byref(s_c)
-
-    def chk(rc):
-        if rc:
-            raise api.EntmtpError(rc, api.last_error())
-
-    state = {"L": L0, "rung": 0 if args.fixed_topo < 0 else args.fixed_topo, "s": 0.0}
-
-    def step_gpu(t, ev=(None, None)):
-        # nothing is read back: the next step's tree and prefix stay on the GPU
-        e = pool_p[t % P]
-        chk(lib.entmtp_step_launch_device(handles[0], e["q"], e["kt"], e["vt"], out_p, e["x"],
-                                          W_p[t % len(W_p)], e["drafts"], log_base, total, ev[0],
-                                          ev[1]))
-
-    # host-scheduled steps: while step t is in flight, step t+1's LM head is
-    # enqueued behind a gate (entmtp_step_arm) for the largest tree the ladder
-    # can reach from the current rung; launching step t+1 once the host has
-    # read step t's result and moved the ladder then opens the gate
-    arming = not args.no_arm
-    armed = [False, 0]        # armed?, the rows the armed LM head covers
-    lm_rows = []              # rows of the LM head each host-scheduled step ran
-
-    def step(t, ev=(None, None), ev_next=(None, None), arm_next=False):
-        L = state["L"] if grows else L0
-        topo = state["rung"]
-        e = pool_p[t % P]
-        if armed[0]:   # the LM head and its events are in the queue already
-            ev = (None, None)
-        chk(lib.entmtp_step_launch(handles[0], topo, L, e["q"], e["kt"], e["vt"], out_p, e["x"],
-                                   W_p[t % len(W_p)], e["tok"][topo], ev[0], ev[1]))
-        lm_rows.append(armed[1] if armed[0] and Ts[topo] <= armed[1] else Ts[topo])
-        armed[0] = False
-        if arming and arm_next:
-            nx = pool_p[(t + 1) % P]
-            bound = Ts[min(topo + 1, n_topo - 1)] if args.fixed_topo < 0 else Ts[topo]
-            chk(lib.entmtp_step_arm(handles[0], nx["x"], W_p[(t + 1) % len(W_p)], bound,
-                                    ev_next[0], ev_next[1]))
-            armed[:] = [True, bound]
-        chk(lib.entmtp_step_wait(handles[0], a_r, b_r, s_r, 30.0))
-        a, s = a_c.value, s_c.value
-        if grows:
-            state["L"] = L + a + 1
-        if args.fixed_topo < 0:
-            state["rung"] = lib.entmtp_ladder_next(topo, n_topo, s, 0.8, 0.6)
-        return Ts[topo], L, a, s, topo
-
-    # ---------------------------------------------------------- warmup
-    if on_gpu:
-        chk(lib.entmtp_step_device_start(handles[0], state["rung"], L0))
-    run = step_gpu if on_gpu else step
-    for t in range(args.warmup):
-        if on_gpu:
-            run(t)
-        else:
-            run(t, arm_next=t + 1 < args.warmup)
-    chk(lib.entmtp_step_flush(handles[0]))   # the last warm-up step's compaction
-    torch.cuda.synchronize()
-
-    # ---------------------------------------------------------- timed
+    run = SingleSeq(api, synth, torch, args.workload, args.pool, args.weight_copies,
+                    total_steps if grows else 0, device_prefix_fixed=not grows)
+    wl, bank = run.wl, run.bank
+    Hq, Hkv, d, hid, V, NL = run.Hq, run.Hkv, run.d, run.hid, run.V, run.NL
+    on_gpu = args.gpu_scheduler
+    fixed = args.fixed_topo >= 0
+    policy = (lambda topo, s: args.fixed_topo) if fixed else ladder(lib, run.n_topo)
     K = args.steps
-    NE = max(1, args.event_every)
-    # timed steps whose LM head carries an event pair: a seeded random 1/NE of
-    # them (a fixed stride can alias with the ladder's cycle through the bank)
-    sampled = sorted(np.random.default_rng(7).choice(K, max(1, K // NE), replace=False).tolist())
-    events = [(TimingEvent(), TimingEvent()) for _ in sampled]
-    ev_p = {t: (a_.ptr, b_.ptr) for t, (a_, b_) in zip(sampled, events)}
-    trace = []
-    graphs, graph_steps = [], 0
-    if on_gpu and args.graph:
-        # segments of SEG steps (a whole number of input-pool and weight-copy
-        # cycles, and of the device state ring), all captured before the timed
-        # region; the steps past the last whole segment run eagerly (and carry
-        # the LM-head events, which graph replays do not)
-        SEG = math.lcm(P, len(W_p), 4)
-        for g0 in range(0, K - K % SEG, SEG):
-            ts = range(args.warmup + g0, args.warmup + g0 + SEG)
-            arr = lambda vals: (ctypes.c_void_p * SEG)(*[v.value for v in vals])   # noqa: E731
-            h = ctypes.c_void_p()
-            chk(lib.entmtp_step_device_graph(
-                handles[0], SEG, arr([pool_p[t % P]["q"] for t in ts]),
-                arr([pool_p[t % P]["kt"] for t in ts]), arr([pool_p[t % P]["vt"] for t in ts]),
-                arr([out_p] * SEG), arr([pool_p[t % P]["x"] for t in ts]),
-                arr([W_p[t % len(W_p)] for t in ts]), arr([pool_p[t % P]["drafts"] for t in ts]),
-                log_base, total, ctypes.byref(h)))
-            graphs.append(h)
-        graph_steps = len(graphs) * SEG
-        sampled = [t for t in sampled if t >= graph_steps]
-        log(f"captured {len(graphs)} graphs of {SEG} steps")
-    torch.cuda.synchronize()
-    # no garbage collection inside the timed region: a full collection of the
-    # interpreter's heap stalls the host loop for tens of milliseconds
-    gc.collect()
-    gc.disable()
-    t_start = time.perf_counter()
-    for g in graphs:
-        chk(lib.entmtp_step_graph_launch(handles[0], g))
-    for t in range(graph_steps, K):
-        if on_gpu:
-            trace.append(run(args.warmup + t, ev_p.get(t, (None, None))))
-        else:
-            trace.append(run(args.warmup + t, ev_p.get(t, (None, None)),
-                             ev_p.get(t + 1, (None, None)), t + 1 < K))
-    events = [ev for t, ev in zip(ev_p, events) if t >= graph_steps]
-    chk(lib.entmtp_step_flush(handles[0]))   # the last timed step's compaction
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t_start
-    gc.enable()
-    for g in graphs:
-        lib.entmtp_step_graph_destroy(g)
-    if on_gpu:   # the steps' (tree, prefix, accept length, s) as the GPU logged them
-        lg = steplog.cpu().numpy()[args.warmup:]
-        trace = [(bank.T[int(r)], int(L), int(a), float(np.int32(sb).view(np.float32)), int(r))
-                 for r, L, a, sb in lg]
-        state["L"] = int(lg[-1, 1] + lg[-1, 2] + 1)
-
-    lm_ms = [a.elapsed_time(b) for a, b in events]
+    n_events = max(MIN_TIMED_LAUNCHES, K // max(1, args.event_every))
+    res = run.run(K, args.warmup, policy, grow=grows, start_rung=max(args.fixed_topo, 0),
+                  arm=not args.no_arm, arm_reach=not fixed, n_events=n_events, on_gpu=on_gpu,
+                  graph=args.graph)
+    elapsed, trace, lm_ms = res["elapsed"], res["trace"], res["lm_ms"]
+    sampled = [t for t in res["sampled"]]
     by_T = {}
     for (T, *_), ms in zip([trace[t] for t in sampled], lm_ms):
         by_T.setdefault(T, []).append(ms)
     lm_us_by_T = {str(T): round(float(np.mean(v)) * 1e3, 2) for T, v in sorted(by_T.items())}
+
     # algorithmic bytes (what the method must move; fp32 logits excluded)
     def step_bytes(T, L, a):
         w = V * hid * 2
@@ -402,25 +470,26 @@ def main():
     us = elapsed / K * 1e6
     hbm = bytes_total / elapsed / 1e9
     lm_gbps = lm_bytes / lm_s / 1e9
-    Tcount = {}
-    for T, *_ in trace:
-        Tcount[T] = Tcount.get(T, 0) + 1
+    Tcount = histogram(T for T, *_ in trace)
     accept_mean = float(np.mean([a + 1 for _, _, a, _, _ in trace]))
     switches = sum(1 for i in range(1, len(trace)) if trace[i][4] != trace[i - 1][4])
     log(f"{K} steps in {elapsed:.3f}s: {us:.1f} us/step, {hbm:.0f} GB/s algorithmic; "
-        f"LM head {np.mean(lm_ms) * 1e3:.1f} us avg, {lm_gbps:.0f} GB/s; T histogram {Tcount}; "
-        f"mean tokens/step {accept_mean:.3f}; switches {switches}; final L {state['L']}; "
-        f"LM head us by T {lm_us_by_T}")
+        f"LM head {np.mean(lm_ms) * 1e3:.1f} us avg over {len(lm_ms)} launches, {lm_gbps:.0f} GB/s; "
+        f"T histogram {Tcount}; mean tokens/step {accept_mean:.3f}; switches {switches}; "
+        f"final L {res['L_end']}; LM head us by T {lm_us_by_T}")
 
-    # ---------------------------------------------------------- cpu baseline
     cpu = None
     if not args.no_cpu_baseline and NL == 1:
-        cpu = cpu_baseline(args, wl, trees, pool, w_host, kc0_host, vc0_host, cap, scale, theta,
-                           [topo for *_, topo in trace])
-
-    timed_rows = lm_rows[len(lm_rows) - len(trace):] if len(lm_rows) >= len(trace) else []
-    traffic = lm_head_traffic(timed_rows or [T for T, *_ in trace])
-    extras = None if args.no_extras else next_rows(api, synth, W[0], pool, hid, V, dev)
+        cpu = cpu_baseline(args, run, [topo for *_, topo in trace])
+    traffic = lm_head_traffic(res["lm_rows"] or [T for T, *_ in trace])
+    extras, switching = None, None
+    if not args.no_extras:
+        extras = next_rows(api, synth, run.W[0], run.pool, hid, V, run.dev)
+        if args.workload == "tree27_L256_7b":
+            del run
+            gc.collect()
+            torch.cuda.empty_cache()
+            switching = switch_study(args, api, synth, torch)
 
     line = {
         "metric": METRIC, "value": round(steps_per_s, 2), "unit": "steps/s", "n_gpus": 1,
@@ -429,27 +498,85 @@ def main():
         "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
         "hbm_GBps_algorithmic": round(hbm, 1), "hbm_frac": round(hbm / HBM_PEAK_GBPS, 4),
         "config": {"workload": wl.name, "batch": 1, "layers": NL, "heads": Hq, "kv_heads": Hkv,
-                   "head_dim": d,
-                   "hidden": hid, "vocab": V, "prefix_len_start": L0,
-                   "prefix_len_end": state["L"], "bank_T": bank.T,
-                   "scheduler": ("hysteretic ladder on=0.8 off=0.6" if args.fixed_topo < 0
+                   "head_dim": d, "hidden": hid, "vocab": V, "prefix_len_start": wl.prefix_len,
+                   "prefix_len_end": res["L_end"] if grows else wl.prefix_len,
+                   "prefix": "growing by the accepted tokens" if grows else "reset every step",
+                   "bank_T": bank.T,
+                   "scheduler": ("hysteretic ladder on=0.8 off=0.6" if not fixed
                                  else f"fixed topo {args.fixed_topo}")
                    + (", on the GPU" if on_gpu else ", on the host"),
-                   "T_histogram": {str(k): v for k, v in sorted(Tcount.items())},
-                   "next_lm_head_armed": bool(arming and not on_gpu),
+                   "T_histogram": {str(k): v for k, v in Tcount.items()},
+                   "next_lm_head_armed": bool(not args.no_arm and not on_gpu),
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
-        "roofline": {"kernel": "LM head with statistics partials (lm_head_hyb_loop_kernel up to 32 nodes, lm_head_hyb_kernel above)", "bound": "hbm",
-                     "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS, "unit": "GB/s",
-                     "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "algorithmic_bytes_per_launch": round(lm_bytes / len(sampled)),
+        "roofline": {"kernel": "LM head with statistics partials (lm_head_hyb_loop_kernel up to 32 nodes, lm_head_hyb_kernel above)",
+                     "bound": "hbm", "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS,
+                     "unit": "GB/s", "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
+                     "algorithmic_bytes_per_launch": round(lm_bytes / max(1, len(sampled))),
                      "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T,
-                     "timed_launches": len(sampled),
-                     "timing": f"HIP events (no system fence) around the LM-head launch of a seeded random 1/{NE} of the timed steps, the LM head queued behind a gate (armed during the previous step, or gated at its launch)"},
+                     "timed_launches": len(lm_ms),
+                     "timing": "HIP events (no system fence) on the step stream around the LM-head "
+                               f"launch of a seeded random {len(lm_ms)} of the {K} timed steps, the "
+                               "LM head queued behind a gate (armed during the previous step, or "
+                               "gated at its launch)"},
         "cpu_baseline": cpu,
+        "switching": switching,
         "next_rows": extras,
     }
     print(json.dumps(line), flush=True)
+
+
+def switch_study(args, api, synth, torch):
+    """What switching trees costs: the 5-tree bank at prefix 2048 (reset every
+    step), (a) the ladder's own choices, (b) a tree one rung up or down every
+    step (a reflecting walk: a switch at every step), and (c) one fixed tree
+    per run, every run armed the same way (the next step's LM head sized for
+    the next rung).  Overheads are the runs' step times minus the fixed-tree
+    step times weighted by the same tree-size histogram."""
+    lib = api.lib
+    K, W = args.switch_steps, max(10, args.switch_steps // 10)
+    run = SingleSeq(api, synth, torch, "bank5_L2048_7b", args.pool, args.weight_copies, 0)
+    n, Ts = run.n_topo, run.Ts
+    us = lambda r: r["elapsed"] / K * 1e6   # noqa: E731
+    lad = run.run(K, W, ladder(lib, n), grow=False)
+    g = np.random.default_rng(11)
+
+    def walk(topo, s):
+        if topo == 0:
+            return 1
+        if topo == n - 1:
+            return n - 2
+        return topo + (1 if g.random() < 0.5 else -1)
+
+    wk = run.run(K, W, walk, grow=False, start_rung=n // 2)
+    fixed_us = {}
+    for r in range(n):
+        fixed_us[Ts[r]] = us(run.run(K, W, lambda topo, s, r=r: r, grow=False, start_rung=r))
+    lad2 = run.run(K, W, ladder(lib, n), grow=False)
+
+    def summary(res):
+        hist = histogram(T for T, *_ in res["trace"])
+        weighted = sum(c * fixed_us[T] for T, c in hist.items()) / K
+        sw = sum(1 for i in range(1, K) if res["trace"][i][4] != res["trace"][i - 1][4])
+        return hist, weighted, sw
+
+    h_l, w_l, sw_l = summary(lad)
+    h_w, w_w, sw_w = summary(wk)
+    h_l2, w_l2, _ = summary(lad2)
+    lad_over = 0.5 * ((us(lad) - w_l) + (us(lad2) - w_l2))
+    out = {"workload": "bank5_L2048_7b", "prefix": "2048, reset every step", "steps_per_run": K,
+           "arming": "every run: next LM head sized for the next rung",
+           "fixed_tree_us": {str(T): round(v, 2) for T, v in fixed_us.items()},
+           "ladder_us": [round(us(lad), 2), round(us(lad2), 2)],
+           "ladder_switches": sw_l, "ladder_T_histogram": {str(k): v for k, v in h_l.items()},
+           "ladder_fixed_weighted_us": [round(w_l, 2), round(w_l2, 2)],
+           "switch_overhead_us": round(lad_over, 2),
+           "walk_us": round(us(wk), 2), "walk_switches": sw_w,
+           "walk_T_histogram": {str(k): v for k, v in h_w.items()},
+           "walk_fixed_weighted_us": round(w_w, 2),
+           "walk_overhead_us": round(us(wk) - w_w, 2)}
+    log("switching study", json.dumps(out))
+    return out
 
 
 def run_batched(args, api, synth, torch, lib):
@@ -742,40 +869,67 @@ def lm_head_traffic(Ts):
     return round(tot / len(Ts))
 
 
-def cpu_baseline(args, wl, trees, pool, w_host, kc0, vc0, cap, scale, theta, topo_seq):
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
+
+
+def cpu_baseline(args, run, topo_seq):
     """The oracle, as it stands, on a bounded sample of the same workload: the
-    timed run's own sequence of trees, from its start, until the time budget."""
+    timed run's own sequence of trees, from its start, at the starting prefix,
+    until the time budget (at least three steps; the median step time is
+    reported), then the first tree of that sequence on one host thread."""
     from oracle import entmtp_oracle as orc
     try:
-        from threadpoolctl import threadpool_info
+        from threadpoolctl import threadpool_info, threadpool_limits
         threads = max([i.get("num_threads", 1) for i in threadpool_info()] or [1])
     except Exception:
+        threadpool_limits = None
         threads = os.cpu_count() or 1
+    wl, trees, pool = run.wl, run.trees, run.pool
     Hkv, d, L0 = wl.n_kv_heads, wl.head_dim, wl.prefix_len
-    # sample: the trees the GPU run chose, in order, at the starting prefix
     order = list(topo_seq) or list(range(len(trees)))
-    done, t0 = [], time.perf_counter()
     kc = np.zeros((Hkv, L0 + 256, d), np.uint16)
     vc = np.zeros_like(kc)
-    kc[:, :L0], vc[:, :L0] = kc0, vc0
-    for i, k in enumerate(order):
+    kc[:, :L0], vc[:, :L0] = run.kc0_host, run.vc0_host
+
+    def one(i, k):
         e = pool[i % len(pool)]
         q, kt, vt, x = e["host"]
         T = len(trees[k])
-        orc.verify_step(trees[k], q[:T], kt[:T], vt[:T], kc, vc, L0, x[:T], w_host,
-                        e["tok"][k], scale, theta)
-        done.append(T)
-        if time.perf_counter() - t0 > args.cpu_budget_s:
+        t0 = time.perf_counter()
+        orc.verify_step(trees[k], q[:T], kt[:T], vt[:T], kc, vc, L0, x[:T], run.w_host,
+                        e["tok"][k], run.scale, run.theta)
+        return time.perf_counter() - t0
+
+    times, done = [], []
+    for i, k in enumerate(order):
+        times.append(one(i, k))
+        done.append(len(trees[k]))
+        if sum(times) > args.cpu_budget_s and len(times) >= 3:
             break
-    el = time.perf_counter() - t0
-    hist = {}
-    for T in done:
-        hist[T] = hist.get(T, 0) + 1
-    return {"value": round(len(done) / el, 4), "unit": "steps/s", "cores": threads,
-            "kind": "oracle",
+    one_thread = []
+    if threadpool_limits is not None:
+        with threadpool_limits(limits=1):
+            while len(one_thread) < 3 and sum(one_thread) < args.cpu_budget_s / 2:
+                one_thread.append(one(0, order[0]))
+    hist = histogram(done)
+    med = float(np.median(times))
+    return {"value": round(1.0 / med, 4), "unit": "steps/s", "cores": threads, "kind": "oracle",
+            "affinity_cores": len(os.sched_getaffinity(0)), "cpu_model": cpu_model(),
+            "median_step_s": round(med, 4),
+            "value_1thread": round(1.0 / float(np.median(one_thread)), 4) if one_thread else None,
+            "steps_1thread": len(one_thread),
             "sample": f"the first {len(done)} steps of the timed run's tree sequence of {wl.name} "
-                      f"(tree-size histogram {dict(sorted(hist.items()))}) at prefix {L0}, "
-                      f"{el:.1f}s; fp64 numpy/BLAS on host cores"}
+                      f"(tree-size histogram {hist}) at prefix {L0}, {sum(times):.1f}s, value = 1 / "
+                      f"median step time; fp64 numpy/BLAS on {threads} host threads; value_1thread: "
+                      f"{len(one_thread)} steps of tree {order[0]} on one thread"}
 
 
 if __name__ == "__main__":

@@ -492,6 +492,10 @@ int32_t entmtp_frontier_score(const entmtp_bank* bank, int32_t topo, const uint8
  *   stream     the HIP stream every launch goes to (NULL: the null stream)
  *   tau_on, tau_off   thresholds of the hysteretic ladder (§4 "Policy") for
  *              device-scheduled steps, tau_off <= tau_on (unused otherwise)
+ *   device_prefix_fixed   0: device-scheduled steps advance the prefix by the
+ *              accepted tokens (the decode loop); 1: every device-scheduled
+ *              step verifies at the prefix length entmtp_step_device_start
+ *              set (a fixed position, for measuring one shape)
  */
 typedef struct entmtp_step_config {
   int32_t n_layers, Hq, Hkv, d, cap, tree_rows;
@@ -515,6 +519,7 @@ typedef struct entmtp_step_config {
   size_t workspace_bytes;
   void* stream;
   float tau_on, tau_off;
+  int32_t device_prefix_fixed;
 } entmtp_step_config;
 
 typedef struct entmtp_step entmtp_step;
@@ -662,8 +667,11 @@ int32_t entmtp_step_flush(entmtp_step* step);
  *   log     device int32[log_rows][4] or NULL: row (step index since
  *           entmtp_step_device_start) % log_rows receives (tree, prefix
  *           length, accept_len, s as float bits) of the step
- * The caller sizes cap for the whole run (prefix growth included); a step
- * whose prefix length plus tree would exceed cap computes no attention.
+ * The caller sizes cap for the whole run (prefix growth included).  A step
+ * whose prefix length plus tree would exceed cap computes no attention; it
+ * and every later step of the run keep the tree and prefix length they had,
+ * and their log rows carry accept length -1 (the host reads the overflow
+ * there).
  * Errors: EINVAL (no entmtp_step_device_start yet), EHIP.
  */
 int32_t entmtp_step_device_start(entmtp_step* step, int32_t topo, int32_t prefix_len);

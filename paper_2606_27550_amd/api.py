@@ -31,7 +31,8 @@ class StepConfig(ctypes.Structure):
                 ("logits", _c_p), ("entropy", _c_p), ("top1p", _c_p), ("argmax", _c_p),
                 ("accept_len", _c_p), ("bonus", _c_p), ("best_top1p", _c_p), ("path", _c_p),
                 ("path_capacity", _c_i32), ("workspace", _c_p), ("workspace_bytes", _c_sz),
-                ("stream", _c_p), ("tau_on", _c_f32), ("tau_off", _c_f32)]
+                ("stream", _c_p), ("tau_on", _c_f32), ("tau_off", _c_f32),
+                ("device_prefix_fixed", _c_i32)]
 
 
 # name -> (restype, argtypes), mirroring include/entmtp.h
@@ -609,7 +610,8 @@ class Step:
 
     def __init__(self, bank: Bank, k_cache, v_cache, w_lm, *, n_layers=1, Hq, Hkv, d=HEAD_DIM,
                  cap, tree_rows, scale, rope_theta, inv_temp=1.0, cache_layer_stride=0,
-                 keep_logits=True, tau_on=0.8, tau_off=0.6, stream=None):
+                 keep_logits=True, tau_on=0.8, tau_off=0.6, device_prefix_fixed=False,
+                 stream=None):
         import torch
         dev = k_cache.device
         V, hid = w_lm.shape
@@ -634,7 +636,8 @@ class Step:
                        self.entropy.data_ptr(),
                        self.top1p.data_ptr(), self.argmax.data_ptr(), self.accept_len.data_ptr(),
                        self.bonus.data_ptr(), self.best_top1p.data_ptr(), self.path.data_ptr(),
-                       D + 1, None, 0, _stream(stream).value, tau_on, tau_off)
+                       D + 1, None, 0, _stream(stream).value, tau_on, tau_off,
+                       int(bool(device_prefix_fixed)))
         need = int(lib.entmtp_step_workspace(bank.handle, ctypes.byref(c)))
         if need == 0:
             _check(lib.entmtp_step_create(bank.handle, ctypes.byref(c), ctypes.byref(_c_p())))

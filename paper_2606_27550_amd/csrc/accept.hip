@@ -163,18 +163,21 @@ __global__ __launch_bounds__(kFinAccDevThreads) void finalize_accept_device_kern
   if (threadIdx.x == 0) {
     const int a = key >> 10, best = 1023 - (key & 1023);
     const float s = s_p1[best];
-    const int next = ladder_step(st.rung, dv.n_topo, s, dv.tau_on, dv.tau_off);
+    // a step beyond the cache verified nothing: stop where it is
+    const bool over = st.overflow != 0 || st.L + st.T > dv.cap;
+    const int next = over ? st.rung : ladder_step(st.rung, dv.n_topo, s, dv.tau_on, dv.tau_off);
     DevStep nx;
     nx.rung = next;
     nx.T = dv.topos[next].T;
-    nx.L = st.L + a + 1;
+    nx.L = over || dv.prefix_fixed ? st.L : st.L + a + 1;
     nx.step = st.step + 1;
+    nx.overflow = over ? 1 : 0;
     *dv.next = nx;
     if (dv.log) {
       int32_t* row = dv.log + 4 * static_cast<size_t>(st.step % dv.log_rows);
       row[0] = st.rung;
       row[1] = st.L;
-      row[2] = a;
+      row[2] = over ? -1 : a;
       row[3] = __float_as_int(s);
     }
   }

@@ -60,10 +60,11 @@ int32_t check_device_bank(const entmtp_bank* bank, int32_t topo);
 // policy moved next to the statistics it reads): one slot per step parity,
 // the step with parity p reads slot p and its acceptance writes slot p ^ 1.
 struct DevStep {
-  int rung;   // bank index of the step's tree
-  int T;      // its node count
-  int L;      // prefix length
-  int step;   // steps since the device state was started
+  int rung;      // bank index of the step's tree
+  int T;         // its node count
+  int L;         // prefix length
+  int step;      // steps since the device state was started
+  int overflow;  // sticky: a step's prefix plus tree exceeded the cache (no attention since)
 };
 
 // A bank tree as the device-scheduled kernels find it: sizes and byte
@@ -140,13 +141,18 @@ int32_t launch_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
 // {rung', T', L + accept_len + 1}; log (4 ints, may be NULL) receives
 // (rung, L, accept_len, s bits) in row cur->step % log_rows of a
 // [log_rows][4] array; user_accept_len / user_path (may be NULL) receive
-// copies of the accept length and path.
+// copies of the accept length and path.  prefix_fixed: the next step keeps
+// prefix length L (every step verifies at the same position).  A step whose
+// L + T exceeds cap (its attention computed nothing) sets the sticky overflow
+// flag: from then on the prefix and tree stay where they are and the log
+// records accept length -1.
 struct FinAccDevice {
   const DevStep* cur;
   DevStep* next;
   const DevTopo* topos;
   const int32_t* drafts;
   int32_t tree_rows, n_topo;
+  int32_t cap, prefix_fixed;
   float tau_on, tau_off;
   int32_t* log;
   int32_t log_rows;

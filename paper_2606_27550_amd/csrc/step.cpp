@@ -177,6 +177,8 @@ int32_t check_config(const entmtp_bank* bank, const entmtp_step_config* c, int32
   ENTMTP_CHECK_ARG(c->path_capacity >= *D_max + 1 && c->path_capacity <= ENTMTP_D_MAX + 1,
                    ENTMTP_EINVAL, "path_capacity = %d outside [1 + the bank's depth %d, %d]",
                    c->path_capacity, *D_max, ENTMTP_D_MAX + 1);
+  ENTMTP_CHECK_ARG(c->device_prefix_fixed == 0 || c->device_prefix_fixed == 1, ENTMTP_EINVAL,
+                   "device_prefix_fixed = %d must be 0 or 1", c->device_prefix_fixed);
   ENTMTP_CHECK_ARG(c->tau_off <= c->tau_on, ENTMTP_EINVAL, "tau_off %g > tau_on %g",
                    static_cast<double>(c->tau_off), static_cast<double>(c->tau_on));
   return ENTMTP_OK;
@@ -558,7 +560,7 @@ extern "C" int32_t entmtp_step_wait(entmtp_step* st, int32_t* accept_len, int32_
 namespace {
 
 __global__ void device_start_kernel(DevStep* state, const DevTopo* topos, int rung, int L) {
-  if (threadIdx.x == 0) state[0] = DevStep{rung, topos[rung].T, L, 0};
+  if (threadIdx.x == 0) state[0] = DevStep{rung, topos[rung].T, L, 0, 0};
 }
 
 }  // namespace
@@ -639,6 +641,8 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   dv.drafts = drafts;
   dv.tree_rows = c.tree_rows;
   dv.n_topo = static_cast<int32_t>(st->bank->desc.size());
+  dv.cap = c.cap;
+  dv.prefix_fixed = c.device_prefix_fixed;
   dv.tau_on = c.tau_on;
   dv.tau_off = c.tau_off;
   dv.log = log;

@@ -10,6 +10,12 @@ optional):
 
   python -m paper_2606_27550_amd.rocprof_summary counters <counter_collection.csv> <out.md> "<command>" [filter]
 
+``apiwindow`` counts the HIP and HSA API calls of a --hip-trace --hsa-trace run
+inside the benchmark's timed region (between its last two hipMemGetInfo
+calls) and lists every code-object load or compile call of the whole run:
+
+  python -m paper_2606_27550_amd.rocprof_summary apiwindow <hip_api_trace.csv> <hsa_api_trace.csv> <out.md> "<command>"
+
 ``traffic`` turns FETCH_SIZE / WRITE_SIZE counter collections (KiB per
 dispatch) into HBM bytes per launch, scaled by what the same counters read for
 a plain device copy of known size, and records them together with the hash of
@@ -114,6 +120,57 @@ def counters(csv_path: str, out_md: str, command: str, match: str = "") -> None:
         f.write("\n".join(lines) + "\n")
 
 
+# HIP / HSA calls that load, register or compile code objects
+LOADERS = ("hipModuleLoad", "hipModuleLoadData", "hipModuleLoadDataEx", "hipModuleGetFunction",
+           "hipModuleUnload", "hiprtc", "__hipRegisterFatBinary", "__hipRegisterFunction",
+           "hsa_executable_load_agent_code_object", "hsa_executable_load_program_code_object",
+           "hsa_code_object_reader_create_from_memory", "hsa_code_object_reader_create_from_file",
+           "hsa_executable_create", "hsa_executable_create_alt", "hsa_executable_freeze",
+           "hsa_code_object_deserialize", "hsa_ext_program")
+
+
+def _api_rows(csv_path):
+    out = []
+    for r in csv.DictReader(open(csv_path)):
+        name = r.get("Function") or r.get("Operation") or r.get("Name") or ""
+        out.append((name, int(r["Start_Timestamp"]), int(r["End_Timestamp"])))
+    return out
+
+
+def apiwindow(hip_csv: str, hsa_csv: str, out_md: str, command: str) -> None:
+    hip = _api_rows(hip_csv)
+    hsa = _api_rows(hsa_csv) if hsa_csv and os.path.exists(hsa_csv) else []
+    marks = sorted(t0 for n, t0, _ in hip if n == "hipMemGetInfo")
+    if len(marks) < 2:
+        raise SystemExit("no timed-region markers (hipMemGetInfo) in the HIP trace")
+    w0, w1 = marks[-2], marks[-1]
+    inside = collections.Counter()
+    for n, t0, _ in hip + hsa:
+        if w0 < t0 < w1:
+            inside[n] += 1
+    loads = [(n, t0) for n, t0, _ in hip + hsa if n.startswith(LOADERS)]
+    loads_inside = [(n, t0) for n, t0 in loads if w0 < t0 < w1]
+    lines = [f"# HIP / HSA API calls in the timed region: `{command}`", "",
+             "rocprofv3 --hip-trace --hsa-trace.  The timed region is the interval between the",
+             "benchmark's last two hipMemGetInfo calls, made right before the timed steps start",
+             "and right after the final synchronisation.", "",
+             f"Timed region: {(w1 - w0) / 1e6:.3f} ms.  Code-object load, registration or compile",
+             f"calls in the whole run: {len(loads)}; inside the timed region: {len(loads_inside)}.", ""]
+    if loads:
+        by = collections.Counter(n for n, _ in loads)
+        lines += ["| code-object call (whole run) | calls | last call, ms before the timed region |",
+                  "|---|---:|---:|"]
+        for n, c in sorted(by.items()):
+            last = max(t0 for m, t0 in loads if m == n)
+            lines.append(f"| `{n}` | {c} | {(w0 - last) / 1e6:.1f} |")
+        lines.append("")
+    lines += ["| API call inside the timed region | calls |", "|---|---:|"]
+    for n, c in sorted(inside.items(), key=lambda kv: -kv[1]):
+        lines.append(f"| `{n}` | {c} |")
+    with open(out_md, "w") as f:
+        f.write("\n".join(lines) + "\n")
+
+
 if __name__ == "__main__":
     if sys.argv[1] == "stats":
         stats(sys.argv[2], sys.argv[3], sys.argv[4])
@@ -121,5 +178,7 @@ if __name__ == "__main__":
         traffic(*sys.argv[2:10])
     elif sys.argv[1] == "counters":
         counters(*sys.argv[2:6])
+    elif sys.argv[1] == "apiwindow":
+        apiwindow(*sys.argv[2:6])
     else:
         sys.exit(__doc__)

@@ -223,3 +223,26 @@ def test_frontier_tree_matches_oracle():
         joint, in_tree = api.frontier_tree(parent, D)
         ref, ref_in = orc.joint_tree(parent, D)
         assert joint == ref and in_tree == [int(x) for x in ref_in]
+
+
+def test_step_config_layout_matches_header(tmp_path):
+    """The binding's entmtp_step_config mirror has the header's field offsets
+    and size (checked by compiling the header with the host C compiler)."""
+    import ctypes
+    import shutil
+    import subprocess
+    cc = shutil.which("gcc") or shutil.which("cc")
+    if cc is None:
+        pytest.skip("no host C compiler")
+    from paper_2606_27550_amd.api import StepConfig
+    names = [f for f, _ in StepConfig._fields_]
+    src = tmp_path / "layout.c"
+    src.write_text('#include <stdio.h>\n#include <stddef.h>\n#include "entmtp.h"\nint main(void) {\n'
+                   + "".join(f'  printf("%zu\\n", offsetof(entmtp_step_config, {n}));\n' for n in names)
+                   + '  printf("%zu\\n", sizeof(entmtp_step_config));\n  return 0;\n}\n')
+    exe = tmp_path / "layout"
+    subprocess.run([cc, "-I", os.path.join(ROOT, "include"), str(src), "-o", str(exe)], check=True)
+    got = [int(v) for v in subprocess.run([str(exe)], capture_output=True, text=True,
+                                          check=True).stdout.split()]
+    want = [getattr(StepConfig, n).offset for n in names] + [ctypes.sizeof(StepConfig)]
+    assert got == want

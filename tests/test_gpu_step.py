@@ -557,3 +557,95 @@ def test_device_step_graph_replays_match_eager_steps(api):
     graph.close()
     st_e.close()
     st_g.close()
+
+
+def test_device_scheduled_fixed_prefix_and_cache_overflow(api):
+    """(1) With device_prefix_fixed every device-scheduled step verifies at the
+    prefix length it started with: the log's prefix column stays put, and the
+    steps equal host-scheduled steps launched at that prefix (trees, accept
+    lengths, s and caches bit for bit).  (2) A run whose prefix outgrows the
+    cache (one fixed 64-node tree): the first step whose prefix plus tree
+    exceeds the capacity, and every step after it, logs accept length -1 and
+    keeps its tree and prefix length; the steps before it log as usual."""
+    Hq, Hkv, d, hid, V, L0, n_steps = 8, 2, 128, 512, 1000, 40, 8
+    theta, scale = 10000.0, 1 / math.sqrt(128)
+    trees = bank_trees()
+    bank = api.Bank(trees)
+    K, Tmax = len(trees), max(bank.T)
+    w_bits = synth.lm_head_weight(WL, V, hid, std=W_STD)
+    w64 = orc.bf16_to_f64(w_bits)
+    W = dev_bf16(w_bits)
+    deltas, spikes = synth.regime_spikes(WL, n_steps, Tmax, V, hid)
+    steps = []
+    for t in range(n_steps):
+        layers, x, am, u, r = step_inputs(t, 1, Tmax, Hq, Hkv, d, w_bits, w64, float(deltas[t]),
+                                          spikes[t])
+        drafts = np.zeros((K, Tmax), np.int32)
+        for k in range(K):
+            drafts[k, : bank.T[k]] = synth.draft_tokens(trees[k], am, u, r, 0.7)
+        steps.append({"q": dev_bf16(layers[0].q), "kt": dev_bf16(layers[0].k_tree),
+                      "vt": dev_bf16(layers[0].v_tree), "x": dev_bf16(x), "drafts": dev_i32(drafts)})
+    out = torch.zeros((Tmax, Hq, d), dtype=torch.bfloat16, device="cuda")
+
+    # (1) fixed prefix, host- and device-scheduled
+    cap = L0 + Tmax + 8
+    base = synth.attn_inputs(WL, 1, Hq, Hkv, d, L0, cap)
+    kc_h, vc_h = dev_bf16(base.k_cache), dev_bf16(base.v_cache)
+    kc_d, vc_d = kc_h.clone(), vc_h.clone()
+    kw = dict(Hq=Hq, Hkv=Hkv, d=d, cap=cap, tree_rows=Tmax, scale=scale, rope_theta=theta,
+              keep_logits=False)
+    st_h = api.Step(bank, kc_h, vc_h, W, **kw)
+    st_d = api.Step(bank, kc_d, vc_d, W, device_prefix_fixed=True, **kw)
+    rung, trace = 0, []
+    for e in steps:
+        st_h.launch(rung, L0, e["q"], e["kt"], e["vt"], out, e["x"], e["drafts"][rung])
+        a, bonus, s = st_h.wait(timeout_s=60.0)
+        trace.append((rung, L0, a, s))
+        rung = api.ladder_next(rung, K, s, 0.8, 0.6)
+    st_h.flush()
+    log = torch.full((n_steps, 4), -7, dtype=torch.int32, device="cuda")
+    st_d.device_start(0, L0)
+    for e in steps:
+        st_d.launch_device(e["q"], e["kt"], e["vt"], out, e["x"], e["drafts"], log)
+    st_d.flush()
+    torch.cuda.synchronize()
+    log_h = log.cpu().numpy()
+    say("fixed prefix: host trace", [(r_, a_) for r_, _, a_, _ in trace])
+    for t, (r_, L_, a_, s_) in enumerate(trace):
+        assert tuple(log_h[t, :3]) == (r_, L_, a_), (t, log_h[t])
+        assert log_h[t, 3:4].view(np.float32)[0] == np.float32(s_)
+    assert len({r_ for r_, *_ in trace}) >= 2
+    assert torch.equal(kc_h.view(torch.int16), kc_d.view(torch.int16))
+    assert torch.equal(vc_h.view(torch.int16), vc_d.view(torch.int16))
+    st_h.close()
+    st_d.close()
+
+    # (2) growing prefix, one fixed tree (thresholds that never move the
+    # ladder), a cache four slots larger than the first step needs
+    rung = 3
+    cap = L0 + bank.T[rung] + 4
+    base = synth.attn_inputs(WL, 1, Hq, Hkv, d, L0, cap)
+    kc, vc = dev_bf16(base.k_cache), dev_bf16(base.v_cache)
+    st = api.Step(bank, kc, vc, W, tau_on=float("inf"), tau_off=float("-inf"),
+                  **dict(kw, cap=cap))
+    log = torch.full((n_steps, 4), -7, dtype=torch.int32, device="cuda")
+    st.device_start(rung, L0)
+    for e in steps:
+        st.launch_device(e["q"], e["kt"], e["vt"], out, e["x"], e["drafts"], log)
+    st.flush()
+    torch.cuda.synchronize()
+    log_h = log.cpu().numpy()
+    say("overflow run log", log_h[:, :3].tolist())
+    L, over = L0, False
+    for t in range(n_steps):
+        r_, L_, a_ = (int(v) for v in log_h[t, :3])
+        assert (r_, L_) == (rung, L), (t, log_h[t])
+        over = over or L + bank.T[rung] > cap
+        if over:
+            assert a_ == -1, (t, log_h[t])
+        else:
+            assert 0 <= a_ <= bank.D[rung], (t, log_h[t])
+            L += a_ + 1
+    assert over                                  # the run did outgrow the cache
+    np.testing.assert_array_equal(host_bits(kc)[:, :L0], base.k_cache[:, :L0])   # prefix intact
+    st.close()
