@@ -166,6 +166,31 @@ int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const entmtp_bf1
                          void* workspace, size_t workspace_bytes, void* stream);
 
 /*
+ * Allocation-free form of entmtp_tree_attn, for callers that cannot allocate
+ * device memory (code under HIP graph capture, serving loops or harnesses
+ * that forbid allocation).  Same arguments, computation and outputs as
+ * entmtp_tree_attn, without the workspace: the call uses a static device
+ * array of ENTMTP_NOALLOC_SCRATCH_BYTES that the library holds on every
+ * device it runs on until the process ends (its device address is looked up
+ * once per device, on the first call made with that device current).
+ * It accepts exactly the calls with
+ *   entmtp_tree_attn_workspace(T, Hq, Hkv, d, prefix_len) <= ENTMTP_NOALLOC_SCRATCH_BYTES
+ * and rejects any other with ENOSPC before launching anything.  It allocates
+ * and frees nothing.  The array keeps the last call's contents; nothing in it
+ * has to start at zero (every call writes what it reads).  All calls on one
+ * device share the array: calls that can overlap on one device (on streams
+ * not ordered with each other, or from several host threads) race, and the
+ * caller must order them.
+ * Errors: EINVAL, ERANGE, ENOSPC (sizes beyond the array), EHIP.
+ */
+#define ENTMTP_NOALLOC_SCRATCH_BYTES (96u * 1024u * 1024u)
+int32_t entmtp_tree_attn_noalloc(const entmtp_bank* bank, int32_t topo, const entmtp_bf16* q,
+                                 const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                                 entmtp_bf16* k_cache, entmtp_bf16* v_cache, int32_t cap,
+                                 int32_t prefix_len, int32_t Hq, int32_t Hkv, int32_t d,
+                                 float scale, float rope_theta, entmtp_bf16* out, void* stream);
+
+/*
  * Batched form: B sequences (1 <= B <= ENTMTP_B_MAX), each with its own tree
  * (topo[b]), prefix length (prefix_len[b]) and cache (k_caches[b],
  * v_caches[b], each [Hkv][cap][d] bf16) -- the per-sequence tree choice of §4

@@ -48,6 +48,9 @@ _SIGNATURES = {
     "entmtp_tree_attn_workspace": (_c_sz, [_c_i32, _c_i32, _c_i32, _c_i32, _c_i32]),
     "entmtp_tree_attn": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32, _c_i32,
                                   _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p, _c_sz, _c_p]),
+    "entmtp_tree_attn_noalloc": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32,
+                                          _c_i32, _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p,
+                                          _c_p]),
     "entmtp_tree_attn_batched_workspace": (_c_sz, [_c_i32] * 6),
     "entmtp_tree_attn_batched": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
                                           _c_i32, _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p,
@@ -276,6 +279,32 @@ def tree_attn(bank: Bank, topo: int, q, k_tree, v_tree, k_cache, v_cache, prefix
                                 _p(v_cache), cap, prefix_len, Hq, Hkv, d, scale, rope_theta,
                                 _p(out), _p(workspace), workspace.numel() * workspace.element_size(),
                                 _stream(stream)))
+
+
+NOALLOC_SCRATCH_BYTES = 96 * 1024 * 1024   # ENTMTP_NOALLOC_SCRATCH_BYTES
+
+
+def tree_attn_noalloc(bank: Bank, topo: int, q, k_tree, v_tree, k_cache, v_cache, prefix_len: int,
+                      scale: float, rope_theta: float, out, stream=None) -> None:
+    """tree_attn without a workspace argument (the library's static scratch):
+    for callers that cannot allocate; calls that can overlap on one device
+    must be ordered by the caller."""
+    import torch
+    _need(0 <= topo < len(bank), "topo out of range")
+    T = bank.T[topo]
+    _need(q.dim() == 3 and k_cache.dim() == 3, "q and caches are 3-D")
+    _, Hq, d = q.shape
+    Hkv, cap, _ = k_cache.shape
+    bf = torch.bfloat16
+    _dev(q, "q", bf, (T, Hq, d))
+    _dev(k_tree, "k_tree", bf, (T, Hkv, d))
+    _dev(v_tree, "v_tree", bf, (T, Hkv, d))
+    _dev(k_cache, "k_cache", bf, (Hkv, cap, d))
+    _dev(v_cache, "v_cache", bf, (Hkv, cap, d))
+    _dev(out, "out", bf, (T, Hq, d))
+    _check(lib.entmtp_tree_attn_noalloc(bank.handle, topo, _p(q), _p(k_tree), _p(v_tree),
+                                        _p(k_cache), _p(v_cache), cap, prefix_len, Hq, Hkv, d,
+                                        scale, rope_theta, _p(out), _stream(stream)))
 
 
 def _host_i32(values):

@@ -33,6 +33,7 @@
 //  3. merge: combines the splits' (max, sum, unnormalised output) partials.
 //     Skipped when a single split covers the keys.
 #include <cfloat>
+#include <mutex>
 
 #include "common.hpp"
 
@@ -1166,6 +1167,41 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
 
 }  // namespace entmtp
 
+// Workspace of entmtp_tree_attn_noalloc, for callers that cannot allocate:
+// one array per device, held until the process ends.  Host code never
+// passes `scratch` itself to a kernel (in host code the name is a host-side
+// stand-in): it takes the device address looked up below.
+static __device__ __align__(256) uint8_t scratch[ENTMTP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxScratchDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_dev[kMaxScratchDevices] = {};
+
+// Device address of `scratch` on the current device, looked up (with that
+// device current) the first time a call runs on it.
+int32_t scratch_address(void** out) {
+  int dev = -1;
+  if (int32_t rc = entmtp::hip_status(hipGetDevice(&dev), "hipGetDevice")) return rc;
+  ENTMTP_CHECK_ARG(dev >= 0 && dev < kMaxScratchDevices, ENTMTP_EINVAL,
+                   "device %d outside the %d devices the static scratch is tracked for", dev,
+                   kMaxScratchDevices);
+  std::lock_guard<std::mutex> lock(g_scratch_mu);
+  if (g_scratch_dev[dev] == nullptr) {
+    void* p = nullptr;
+    if (int32_t rc = entmtp::hip_status(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)),
+                                        "hipGetSymbolAddress (static scratch)"))
+      return rc;
+    ENTMTP_CHECK_ARG(p != nullptr, ENTMTP_EHIP, "hipGetSymbolAddress returned NULL for the scratch");
+    g_scratch_dev[dev] = p;
+  }
+  *out = g_scratch_dev[dev];
+  return ENTMTP_OK;
+}
+
+}  // namespace
+
 using namespace entmtp;
 
 extern "C" size_t entmtp_tree_attn_workspace(int32_t T, int32_t Hq, int32_t Hkv, int32_t d,
@@ -1205,6 +1241,37 @@ extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const
   a.vt = v_tree;
   a.out = out;
   return launch_call(a, sh, workspace, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int32_t entmtp_tree_attn_noalloc(const entmtp_bank* bank, int32_t topo,
+                                            const entmtp_bf16* q, const entmtp_bf16* k_tree,
+                                            const entmtp_bf16* v_tree, entmtp_bf16* k_cache,
+                                            entmtp_bf16* v_cache, int32_t cap, int32_t prefix_len,
+                                            int32_t Hq, int32_t Hkv, int32_t d, float scale,
+                                            float rope_theta, entmtp_bf16* out, void* stream) {
+  clear_error();
+  if (int32_t rc = check_sequence(bank, topo, prefix_len, k_cache, v_cache, cap, 0)) return rc;
+  // (the workspace check of check_common is met by the static array)
+  if (int32_t rc = check_common(Hq, Hkv, d, scale, rope_theta, q, k_tree, v_tree, out, scratch))
+    return rc;
+  const int T = bank->desc[topo].T;
+  // the bound entmtp_tree_attn_workspace() states covers every plan of the
+  // call, so an accepted call stays inside the array
+  const size_t need = workspace_bytes(T, Hq, Hkv, prefix_len);
+  ENTMTP_CHECK_ARG(need <= ENTMTP_NOALLOC_SCRATCH_BYTES, ENTMTP_ENOSPC,
+                   "the call needs %zu bytes of workspace, the static scratch holds %zu", need,
+                   static_cast<size_t>(ENTMTP_NOALLOC_SCRATCH_BYTES));
+  void* ws = nullptr;
+  if (int32_t rc = scratch_address(&ws)) return rc;
+  BatchArgs a;
+  const CallShape sh = plan_call(bank, 1, &topo, &prefix_len, &k_cache, &v_cache, cap, Hq, Hkv, a);
+  a.scale_log2 = scale * 1.4426950408889634f;
+  a.theta = static_cast<double>(rope_theta);
+  a.q = q;
+  a.kt = k_tree;
+  a.vt = v_tree;
+  a.out = out;
+  return launch_call(a, sh, ws, static_cast<hipStream_t>(stream));
 }
 
 extern "C" int32_t entmtp_tree_attn_batched(
