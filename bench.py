@@ -263,14 +263,16 @@ class SingleSeq:
             raise self.api.EntmtpError(rc, self.api.last_error())
 
     def run(self, K, warmup, policy, *, grow, start_rung=0, arm=True, arm_reach=True,
-            n_events=0, on_gpu=False, graph=False, step_times=None):
+            n_events=0, event_pass=0, on_gpu=False, graph=False, step_times=None):
         """Runs `warmup` untimed and K timed steps.  policy(topo, s) gives the
         next step's tree from the current one and the step's s (host-
         scheduled steps).  grow: the prefix grows by the accepted tokens (else
         every step verifies at L0).  arm: each next step's LM head is enqueued
         behind a gate while the step before is pending, sized for the next
         rung (arm_reach) or for the current tree.  n_events: timed steps whose
-        LM head carries a HIP event pair (a seeded random choice).  on_gpu:
+        LM head carries a HIP event pair (a seeded random choice);
+        event_pass: steps run right after the timed region (same loop, inputs
+        and state, outside the timing) whose LM heads all carry event pairs.  on_gpu:
         the ladder runs on the GPU (entmtp_step_launch_device), optionally
         replayed as captured graph segments (the prefix then grows unless the
         step context was made with a fixed device prefix).  step_times: a list
@@ -279,7 +281,7 @@ class SingleSeq:
         h = self.st.handle
         Ts, n_topo, P = self.Ts, self.n_topo, self.P
         pool_p, W_p, out_p = self.pool_p, self.W_p, self.out_p
-        total = warmup + K
+        total = warmup + K + event_pass
         steplog = torch.full((total, 4), -1, dtype=torch.int32, device=self.dev)
         log_base = ctypes.c_void_p(steplog.data_ptr())
         a_c, b_c, s_c = ctypes.c_int32(), ctypes.c_int32(), ctypes.c_float()
@@ -344,11 +346,11 @@ class SingleSeq:
         chk(lib.entmtp_step_flush(h))   # the last warm-up step's compaction
         if on_gpu and graph:
             # segments of SEG steps (a whole number of input-pool and
-            # weight-copy cycles, and of the device state ring), all captured
+            # weight-copy cycles, and of the 16-slot device state ring), all captured
             # after the warm-up, before the timed region; the steps past the last whole segment
             # run eagerly (and carry the LM-head events, which graph replays
             # do not)
-            SEG = math.lcm(P, len(W_p), 4)
+            SEG = math.lcm(P, len(W_p), 16)
             for g0 in range(0, K - K % SEG, SEG):
                 ts = range(warmup + g0, warmup + g0 + SEG)
                 arr = lambda vals: (ctypes.c_void_p * SEG)(*[v.value for v in vals])   # noqa: E731
@@ -382,21 +384,41 @@ class SingleSeq:
         torch.cuda.synchronize()
         elapsed = time.perf_counter() - t_start
         torch.cuda.mem_get_info()
-        gc.enable()
         if step_times is not None:
             step_times.insert(0, t_start)
         events = [ev for t, ev in zip(ev_p, events) if t >= graph_steps]
         for g in graphs:
             lib.entmtp_step_graph_destroy(g)
+        n_timed_rows = len(lm_rows)
+        # the event pass: every LM head bracketed, outside the timed region
+        pass_events = [(TimingEvent(), TimingEvent()) for _ in range(event_pass)]
+        pass_trace = []
+        for j in range(event_pass):
+            t = warmup + K + j
+            ev = (pass_events[j][0].ptr, pass_events[j][1].ptr)
+            if on_gpu:
+                step_gpu(t, ev)
+            else:
+                nxt = (pass_events[j + 1][0].ptr, pass_events[j + 1][1].ptr) if j + 1 < event_pass \
+                    else (None, None)
+                pass_trace.append(step(t, ev, nxt, j + 1 < event_pass))
+        if event_pass:
+            chk(lib.entmtp_step_flush(h))
+            torch.cuda.synchronize()
+        gc.enable()
         if on_gpu:   # the steps' (tree, prefix, accept length, s) as the GPU logged them
-            lg = steplog.cpu().numpy()[warmup:]
-            trace = [(Ts[int(r)], int(L), int(a), float(np.int32(sb).view(np.float32)), int(r))
-                     for r, L, a, sb in lg]
-            state["L"] = int(lg[-1, 1] + lg[-1, 2] + 1)
+            lg = steplog.cpu().numpy()
+            rows = [(Ts[int(r)], int(L), int(a), float(np.int32(sb).view(np.float32)), int(r))
+                    for r, L, a, sb in lg]
+            trace = rows[warmup:warmup + K]
+            pass_trace = rows[warmup + K:]
+            state["L"] = int(lg[warmup + K - 1, 1] + lg[warmup + K - 1, 2] + 1)
         lm_ms = [a.elapsed_time(b) for a, b in events]
-        timed_rows = lm_rows[len(lm_rows) - len(trace):] if len(lm_rows) >= len(trace) else []
+        pass_ms = [a.elapsed_time(b) for a, b in pass_events]
+        timed_rows = lm_rows[n_timed_rows - len(trace):n_timed_rows] if n_timed_rows >= len(trace) else []
         return {"elapsed": elapsed, "trace": trace, "lm_ms": lm_ms, "sampled": sampled,
-                "lm_rows": timed_rows, "L_end": state["L"]}
+                "lm_rows": timed_rows, "L_end": state["L"], "pass_ms": pass_ms,
+                "pass_T": [T for T, *_ in pass_trace]}
 
 
 def ladder(lib, n_topo):
@@ -441,14 +463,18 @@ def main():
     fixed = args.fixed_topo >= 0
     policy = (lambda topo, s: args.fixed_topo) if fixed else ladder(lib, run.n_topo)
     K = args.steps
-    n_events = max(MIN_TIMED_LAUNCHES, K // max(1, args.event_every))
+    n_events = max(1, K // max(1, args.event_every))
     res = run.run(K, args.warmup, policy, grow=grows, start_rung=max(args.fixed_topo, 0),
-                  arm=not args.no_arm, arm_reach=not fixed, n_events=n_events, on_gpu=on_gpu,
-                  graph=args.graph)
-    elapsed, trace, lm_ms = res["elapsed"], res["trace"], res["lm_ms"]
+                  arm=not args.no_arm, arm_reach=not fixed, n_events=n_events,
+                  event_pass=MIN_TIMED_LAUNCHES, on_gpu=on_gpu, graph=args.graph)
+    elapsed, trace = res["elapsed"], res["trace"]
     sampled = [t for t in res["sampled"]]
+    # LM-head durations: the timed region's sample, then the event pass
+    lm_T = [trace[t][0] for t in sampled][:len(res["lm_ms"])] + res["pass_T"]
+    lm_ms = res["lm_ms"] + res["pass_ms"]
+    n_in_region = len(res["lm_ms"])
     by_T = {}
-    for (T, *_), ms in zip([trace[t] for t in sampled], lm_ms):
+    for T, ms in zip(lm_T, lm_ms):
         by_T.setdefault(T, []).append(ms)
     lm_us_by_T = {str(T): round(float(np.mean(v)) * 1e3, 2) for T, v in sorted(by_T.items())}
 
@@ -464,7 +490,7 @@ def main():
         return w + kv + tree_in + tree_kv_out + att_out + compact + stats
 
     bytes_total = sum(step_bytes(T, L, a) for T, L, a, _, _ in trace)
-    lm_bytes = sum(V * hid * 2 + trace[t][0] * hid * 2 for t in sampled)
+    lm_bytes = sum(V * hid * 2 + T * hid * 2 for T in lm_T)
     lm_s = sum(lm_ms) / 1e3
     steps_per_s = K / elapsed
     us = elapsed / K * 1e6
@@ -509,16 +535,18 @@ def main():
                    "next_lm_head_armed": bool(not args.no_arm and not on_gpu),
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
-        "roofline": {"kernel": "LM head with statistics partials (lm_head_hyb_loop_kernel up to 32 nodes, lm_head_hyb_kernel above)",
+        "roofline": {"kernel": "LM head with statistics partials (lm_head_pair_kernel up to 32 nodes, lm_head_hyb_kernel above)",
                      "bound": "hbm", "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
-                     "algorithmic_bytes_per_launch": round(lm_bytes / max(1, len(sampled))),
+                     "algorithmic_bytes_per_launch": round(lm_bytes / max(1, len(lm_T))),
                      "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T,
-                     "timed_launches": len(lm_ms),
+                     "timed_launches": len(lm_ms), "timed_launches_in_region": n_in_region,
                      "timing": "HIP events (no system fence) on the step stream around the LM-head "
-                               f"launch of a seeded random {len(lm_ms)} of the {K} timed steps, the "
-                               "LM head queued behind a gate (armed during the previous step, or "
-                               "gated at its launch)"},
+                               f"launch of a seeded random {n_in_region} of the {K} timed steps and "
+                               f"of all {len(lm_ms) - n_in_region} steps of an event pass run right "
+                               "after the timed region (same loop, inputs and state); the LM head "
+                               "queued behind the previous step's publish kernel or a launch gate, "
+                               "so that each pair brackets the kernel"},
         "cpu_baseline": cpu,
         "switching": switching,
         "next_rows": extras,
@@ -850,18 +878,21 @@ def lm_head_traffic(Ts):
     per = {}
     for name, v in rec["per_variant"].items():
         targs = [x.strip() for x in name.split("<")[1].rstrip(">").split(",")]
-        if targs[3] != "true":   # the timed kernel is the statistics variant <NT, S, NCH, STATS, ...>
-            continue
         kernel = name.split("<")[0].split()[-1]
-        key = (kernel, int(targs[0]))
-        # large tiles: the step pairs slices per workgroup (last argument 2);
-        # an unpaired launch of the entry points must not stand in for it
-        if key in per and len(targs) > 4 and targs[4] != "2":
+        if kernel == "lm_head_pair_kernel":            # <NT, NCH>: up to 32 nodes
+            key = (kernel, int(targs[0]))
+        elif kernel == "lm_head_hyb_kernel" and targs[3] == "true":   # <NT, S, NCH, STATS, WT>
+            key = (kernel, int(targs[0]))
+            # large tiles: the step pairs slices per workgroup (last argument
+            # 2); an unpaired launch of the entry points must not stand in
+            if key in per and len(targs) > 4 and targs[4] != "2":
+                continue
+        else:
             continue
         per[key] = v["fetch_bytes"] + v["write_bytes"]
     tot = 0.0
-    for T in Ts:   # the step's launch: the loop kernel up to 32 nodes, the grid kernel above
-        key = (("lm_head_hyb_loop_kernel", 1 if T <= 16 else 2) if T <= 32 else
+    for T in Ts:   # the step's launch: the pair kernel up to 32 nodes, the grid kernel above
+        key = (("lm_head_pair_kernel", 1 if T <= 16 else 2) if T <= 32 else
                ("lm_head_hyb_kernel", 4 if T <= 64 else 8))
         if key not in per:
             return None

@@ -708,7 +708,7 @@ int32_t entmtp_step_launch_device(entmtp_step* step, const entmtp_bf16* q,
 
 /*
  * A segment of device-scheduled steps as one HIP graph: since such steps read
- * nothing back, n_steps of them (a multiple of 4, the depth of the device
+ * nothing back, n_steps of them (a multiple of 16, the depth of the device
  * state ring) are captured from the configured stream (which must not be the
  * null stream) with their per-step inputs -- host arrays of n_steps device
  * pointers, w_lm may be NULL (the configured weight) -- and a final flush, so
@@ -716,7 +716,9 @@ int32_t entmtp_step_launch_device(entmtp_step* step, const entmtp_bf16* q,
  * entmtp_step_graph_launch then runs the segment's steps on the configured
  * stream, continuing from whatever tree and prefix length the device state
  * holds (the log rows follow the device's step count); replays of one graph
- * may follow each other and eager steps.  *graph receives an opaque handle;
+ * may follow each other, and eager steps whose number is a multiple of 16
+ * (entmtp_step_graph_launch returns EINVAL otherwise: the segment's steps
+ * read fixed ring slots).  *graph receives an opaque handle;
  * release it with entmtp_step_graph_destroy.  Requires
  * entmtp_step_device_start first.  Errors: EINVAL, ERANGE, EHIP.
  */

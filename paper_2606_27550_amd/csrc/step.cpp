@@ -42,8 +42,16 @@ struct entmtp_step {
   size_t ring_offset = 0;      // and the acceptance ring: kRing x (accept_len, path[path_capacity])
   DevAttnShape dshape;         // attention grids for a tree chosen on the device
   // device-scheduled steps: step t reads state slot t % kRing and writes slot
-  // (t + 1) % kRing; its accept length and path go to ring slot t % kRing
-  static constexpr int kRing = 4;
+  // (t + 1) % kRing; its accept length and path go to ring slot t % kRing.
+  // Before step t's acceptance writes those slots, the side stream must be
+  // done with their previous users (its work of step t + 2 - kRing); the
+  // caller's stream waits for the side stream's step t - kWaitLag at every
+  // kWaitEvery-th step, which covers the kWaitEvery steps from there
+  // (t + kWaitEvery - 1 + 2 - kRing <= t - kWaitLag) with one wait packet.
+  static constexpr int kRing = 16;
+  static constexpr int kWaitEvery = 8;
+  static constexpr int kWaitLag = 4;
+  static_assert(kWaitEvery + 1 - kRing <= -kWaitLag, "ring too shallow for the wait cadence");
   bool dev_started = false;
   uint64_t dev_t = 0;          // steps launched since entmtp_step_device_start
   uint64_t dev_compact = 0;    // steps whose compaction has been enqueued
@@ -627,11 +635,13 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
                                             static_cast<hipEvent_t>(ev_lm_begin),
                                             static_cast<hipEvent_t>(ev_lm_end)))
     return rc;
-  // step t writes state slot t+1 and ring slot t: the side stream must be
-  // done with step t-2 (whose compaction read slot t-2 and ring slot t-2, and
-  // whose predecessor's compaction read slot t-3 = t+1 mod R)
-  if (t >= st->dev_sync_t + 2)   // (earlier steps: joined by a flush already)
-    if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->ev_side[(t - 2) % R], 0),
+  // step t writes state slot t+1 and ring slot t, which the side stream's
+  // work of step t+2-R read last: one wait for its step t-kWaitLag every
+  // kWaitEvery steps covers that (steps whose side work a flush has joined
+  // need none)
+  constexpr uint64_t E = entmtp_step::kWaitEvery, LAG = entmtp_step::kWaitLag;
+  if (t % E == 0 && t >= st->dev_sync_t + LAG)
+    if (int32_t rc = hip_status(hipStreamWaitEvent(s, st->ev_side[(t - LAG) % R], 0),
                                 "hipStreamWaitEvent"))
       return rc;
   FinAccDevice dv;
@@ -676,6 +686,17 @@ extern "C" int32_t entmtp_step_launch_device(entmtp_step* st, const entmtp_bf16*
   return ENTMTP_OK;
 }
 
+namespace {
+
+// A captured segment and the ring slot its first step reads (the device
+// state must sit in that slot when the segment is replayed).
+struct StepGraph {
+  hipGraphExec_t exec;
+  int slot;
+};
+
+}  // namespace
+
 extern "C" int32_t entmtp_step_device_graph(entmtp_step* st, int32_t n_steps,
                                             const entmtp_bf16* const* q,
                                             const entmtp_bf16* const* k_tree,
@@ -699,6 +720,7 @@ extern "C" int32_t entmtp_step_device_graph(entmtp_step* st, int32_t n_steps,
   auto s = static_cast<hipStream_t>(st->cfg.stream);
   // the segment starts from a joined state, so it depends on nothing outside it
   if (int32_t rc = flush_side(st)) return rc;
+  const int slot = static_cast<int>(st->dev_t % entmtp_step::kRing);
   if (int32_t rc = hip_status(hipStreamBeginCapture(s, hipStreamCaptureModeRelaxed),
                               "hipStreamBeginCapture"))
     return rc;
@@ -716,18 +738,26 @@ extern "C" int32_t entmtp_step_device_graph(entmtp_step* st, int32_t n_steps,
     rc = hip_status(hipGraphInstantiate(&exec, g, nullptr, nullptr, 0), "hipGraphInstantiate");
   if (g) (void)hipGraphDestroy(g);
   if (rc != ENTMTP_OK) return rc;
-  *graph = exec;
+  *graph = new StepGraph{exec, slot};
   return ENTMTP_OK;
 }
 
 extern "C" int32_t entmtp_step_graph_launch(entmtp_step* st, void* graph) {
   clear_error();
   ENTMTP_CHECK_ARG(st != nullptr && graph != nullptr, ENTMTP_EINVAL, "step or graph is NULL");
-  return hip_status(hipGraphLaunch(static_cast<hipGraphExec_t>(graph),
-                                   static_cast<hipStream_t>(st->cfg.stream)),
+  const auto* g = static_cast<const StepGraph*>(graph);
+  const int now = static_cast<int>(st->dev_t % entmtp_step::kRing);
+  ENTMTP_CHECK_ARG(now == g->slot, ENTMTP_EINVAL,
+                   "the device state is in ring slot %d, the segment starts at slot %d: eager "
+                   "steps between replays must number a multiple of %d", now, g->slot,
+                   entmtp_step::kRing);
+  return hip_status(hipGraphLaunch(g->exec, static_cast<hipStream_t>(st->cfg.stream)),
                     "hipGraphLaunch");
 }
 
 extern "C" void entmtp_step_graph_destroy(void* graph) {
-  if (graph) (void)hipGraphExecDestroy(static_cast<hipGraphExec_t>(graph));
+  if (!graph) return;
+  auto* g = static_cast<StepGraph*>(graph);
+  (void)hipGraphExecDestroy(g->exec);
+  delete g;
 }
