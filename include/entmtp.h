@@ -319,8 +319,13 @@ int32_t entmtp_accept(const entmtp_bank* bank, int32_t topo, const int32_t* draf
  * the rule is the published typical acceptance of Medusa/Hydra).  Node i >= 1
  * is locally acceptable when its draft token's probability under its parent's
  * distribution p = softmax(z[parent] * inv_temp) exceeds
- * min(eps, alpha * exp(-H(p))); the longest accepted path, bonus token and
- * outputs are then as for entmtp_accept.
+ * min(eps, alpha * exp(-H(p))), and accepted when every ancestor is too.
+ * The answer is the deepest accepted node; among several of that depth, the
+ * one whose path's draft tokens are jointly most likely (largest sum of
+ * log p(draft) from the root, decided in fp32; then the lowest index), the
+ * published rule's choice among equally long candidates.  Outputs (accept
+ * length, path with -1 past it, bonus = argmax at the chosen node,
+ * best_top1p) are as for entmtp_accept; path has D + 1 entries.
  *
  * entmtp_draft_logits computes what the test needs beyond the statistics:
  * z_draft[i] = X[parent(i)] . W[draft_tokens[i]] and z_top[i] = X[parent(i)] .
@@ -452,6 +457,28 @@ int32_t entmtp_accept_stochastic(const entmtp_bank* bank, int32_t topo,
 /* Acceptance frontier (§3.1, Algorithm 1: the scoring step of the greedy     */
 /* offline tree search)                                                       */
 /* ------------------------------------------------------------------------ */
+
+/*
+ * NextChildren(T, D) of Algorithm 1 (§3.1; the paper does not spell it out):
+ * every node of T whose depth is below max_depth, the root included, proposes
+ * its next-ranked child (rank = its current number of children, the greedy
+ * tree-growing step of Medusa/Hydra tree lists).  Builds the joint tree
+ * T u F that entmtp_frontier_score scores: T's nodes keep their indices, the
+ * candidates follow in node order of their parents.  Host only.
+ *   parent       HOST int32[T], parent[0] = -1, 0 <= parent[i] < i
+ *   T            1 <= T
+ *   max_depth    D >= 0 (a candidate's depth is at most D)
+ *   joint_parent HOST int32[joint_capacity] out: the parent array of T u F
+ *   in_tree      HOST uint8[joint_capacity] out (may be NULL): 1 for T's nodes,
+ *                0 for the candidates
+ *   joint_T      HOST int32 out: T + |F|
+ * Errors: EINVAL (NULL pointer, bad parent array, max_depth < 0), ENOSPC
+ * (T + |F| > joint_capacity; *joint_T still receives T + |F| and nothing
+ * else is written).
+ */
+int32_t entmtp_frontier_tree(const int32_t* parent, int32_t T, int32_t max_depth,
+                             int32_t* joint_parent, uint8_t* in_tree, int32_t joint_capacity,
+                             int32_t* joint_T);
 
 /*
  * Scores every one-node augmentation T u {nu} of a draft tree T from one

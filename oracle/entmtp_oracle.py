@@ -321,8 +321,12 @@ def accept_typical(parent: Sequence[int], draft_tokens: Sequence[int], z, inv_te
     Node i >= 1 is locally acceptable when its draft token's probability under
     its parent's distribution p = softmax(z[parent] * inv_temp) exceeds
     min(eps, alpha * exp(-H(p))); it is accepted when its parent is accepted
-    too (the root always is).  The answer is the deepest accepted node (lowest
-    index among equals); the bonus token is the argmax at that node.
+    too (the root always is).  The answer is the deepest accepted node; where
+    several accepted nodes share that depth (siblings often pass together
+    under this rule), the published rule keeps the candidate whose accepted
+    tokens are jointly most likely: the largest sum of log p_draft over the
+    node's root-to-node path, then the lowest index.  The bonus token is the
+    argmax at the chosen node.
 
     z: the tree's logits [T][V].  Returns (a, path, bonus, best, p_draft,
     threshold) with p_draft[i] the draft token's probability under node i's
@@ -342,9 +346,16 @@ def accept_typical(parent: Sequence[int], draft_tokens: Sequence[int], z, inv_te
         depth[i] = depth[parent[i]] + 1
         p_draft[i] = float(probs[parent[i]][int(draft_tokens[i])])
         ok[i] = ok[parent[i]] and p_draft[i] > thr[parent[i]]
-    best = 0
-    for i in range(T):
-        if ok[i] and depth[i] > depth[best]:
+    # joint log-likelihood of each accepted node's path (the root contributes 0)
+    loglik = [0.0] * T
+    for i in range(1, T):
+        if ok[i]:
+            loglik[i] = loglik[parent[i]] + math.log(p_draft[i])
+    a = max(depth[i] for i in range(T) if ok[i])
+    deepest = [i for i in range(T) if ok[i] and depth[i] == a]
+    best = deepest[0]
+    for i in deepest[1:]:          # ascending index: a later node must be strictly more likely
+        if loglik[i] > loglik[best]:
             best = i
     path = ancestors_or_self(parent, best)
     bonus = int(np.argmax(np.asarray(z[best], dtype=np.float64)))

@@ -73,6 +73,7 @@ _SIGNATURES = {
                                      _c_p]),
     "entmtp_accept_typical": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_f32,
                                        _c_f32, _c_f32, _c_p, _c_p, _c_p, _c_p, _c_p]),
+    "entmtp_frontier_tree": (_c_i32, [_c_p, _c_i32, _c_i32, _c_p, _c_p, _c_i32, ctypes.POINTER(_c_i32)]),
     "entmtp_frontier_score": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p,
                                        _c_p]),
     "entmtp_accept_stochastic": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_i32, _c_f32, _c_p,
@@ -535,16 +536,20 @@ def accept_typical(bank: Bank, topo: int, draft_tokens, argmax, z_draft, z_top, 
 
 
 def frontier_tree(parent, max_depth: int):
-    """The joint tree T u F of the offline search's scoring step (host
-    bookkeeping): every node of T whose depth is below max_depth, the root
-    included, proposes its next-ranked child; the candidates follow T's nodes
-    in node order.  Returns (parent list of T u F, in_tree list of 0/1)."""
-    depth = [0] * len(parent)
-    for i in range(1, len(parent)):
-        _need(0 <= parent[i] < i, "parents precede their children")
-        depth[i] = depth[parent[i]] + 1
-    cands = [p for p, dp in enumerate(depth) if dp < max_depth]
-    return list(parent) + cands, [1] * len(parent) + [0] * len(cands)
+    """The joint tree T u F of the offline search's scoring step
+    (entmtp_frontier_tree): every node of T whose depth is below max_depth,
+    the root included, proposes its next-ranked child; the candidates follow
+    T's nodes in node order.  Returns (parent list of T u F, in_tree list of
+    0/1)."""
+    T = len(parent)
+    _need(T >= 1, "the tree has a root")
+    src = (_c_i32 * T)(*[int(p) for p in parent])
+    cap = 2 * T
+    joint = (_c_i32 * cap)()
+    in_tree = (ctypes.c_uint8 * cap)()
+    n = _c_i32(0)
+    _check(lib.entmtp_frontier_tree(src, T, int(max_depth), joint, in_tree, cap, ctypes.byref(n)))
+    return list(joint[: n.value]), list(in_tree[: n.value])
 
 
 def frontier_score(bank: Bank, topo: int, in_tree, sums, best, local_ok=None, draft_tokens=None,

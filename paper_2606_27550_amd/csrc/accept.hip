@@ -233,8 +233,18 @@ __global__ __launch_bounds__(64) void draft_logits_kernel(
 
 // Typical acceptance: node i >= 1 is locally acceptable when its draft
 // token's probability under the parent's temperature-scaled distribution,
-// exp((z_draft - z_top) * inv_temp) * top1p[parent], exceeds
-// min(eps, alpha * exp(-entropy[parent])).
+// p_i = exp((z_draft - z_top) * inv_temp) * top1p[parent], exceeds
+// min(eps, alpha * exp(-entropy[parent])).  Among the deepest accepted nodes
+// the one whose path's drafts are jointly most likely wins (largest sum of
+// log p over its root-to-node path, then the lowest index): under this rule
+// several siblings often pass together.  The key packs depth (5 bits), the
+// order-preserving bits of that fp32 sum and 1023 - index into 64 bits, so
+// one maximum over the workgroup makes the choice.
+__device__ __forceinline__ uint64_t float_order_bits(float f) {
+  const uint32_t u = __float_as_uint(f);
+  return (u & 0x80000000u) ? ~u : (u | 0x80000000u);
+}
+
 __global__ __launch_bounds__(kAcceptThreads) void accept_typical_kernel(
     const int* __restrict__ parent, const int* __restrict__ depth,
     const uint32_t* __restrict__ mask, const int* __restrict__ path_tab, int T, int D,
@@ -243,9 +253,13 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_typical_kernel(
     const float* __restrict__ top1p, float inv_temp, float eps, float alpha,
     int* __restrict__ accept_len, int* __restrict__ path_out, int* __restrict__ bonus,
     float* __restrict__ best_p) {
+  __shared__ float s_logp[kAcceptThreads];
+  __shared__ uint32_t matched[ENTMTP_MASK_WORDS];
+  __shared__ uint64_t s_key[kAcceptThreads / 64];
   const NodeIn n = accept_load(parent, depth, mask, tok, T);
   const int i = threadIdx.x;
   bool ok = false;
+  float logp = 0.f;
   if (i == 0) {
     ok = true;
   } else if (i < T) {
@@ -253,9 +267,45 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_typical_kernel(
     const float pd = expf((z_draft[i] - z_top[i]) * inv_temp) * top1p[p];
     const float thr = fminf(eps, alpha * expf(-entropy[p]));
     ok = pd > thr;
+    logp = ok ? logf(pd) : 0.f;   // pd > thr >= 0 for every node whose value is read
   }
-  (void)accept_finish(n, ok, path_tab, T, D, amax, top1p, accept_len, path_out, D + 1, bonus,
-                      best_p, nullptr, 0u);
+  s_logp[i] = logp;
+  if (i < ENTMTP_MASK_WORDS) matched[i] = 0u;
+  __syncthreads();
+  if (i < T && ok) atomicOr(&matched[i >> 5], 1u << (i & 31));
+  __syncthreads();
+  uint64_t key = 0u;   // below every accepted node's key (the root's is > 0)
+  if (i < T) {
+    bool acc = true;
+#pragma unroll
+    for (int w = 0; w < ENTMTP_MASK_WORDS; ++w) acc = acc && ((n.mask[w] & ~matched[w]) == 0u);
+    if (acc) {
+      float ll = 0.f;   // root to node, as the path is walked
+      for (int j = 1; j <= n.depth; ++j) ll += s_logp[path_tab[i * (D + 1) + j]];
+      key = (static_cast<uint64_t>(n.depth) << 42) | (float_order_bits(ll) << 10) |
+            static_cast<uint64_t>(1023 - i);
+    }
+  }
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    const uint32_t lo = __shfl_xor(static_cast<uint32_t>(key), off, 64);
+    const uint32_t hi = __shfl_xor(static_cast<uint32_t>(key >> 32), off, 64);
+    const uint64_t other = (static_cast<uint64_t>(hi) << 32) | lo;
+    key = other > key ? other : key;
+  }
+  if ((i & 63) == 0) s_key[i >> 6] = key;
+  __syncthreads();
+  key = s_key[0];
+#pragma unroll
+  for (int w = 1; w < kAcceptThreads / 64; ++w) key = s_key[w] > key ? s_key[w] : key;
+  const int best = 1023 - static_cast<int>(key & 1023u);
+  const int a = static_cast<int>(key >> 42);
+  if (i <= D) path_out[i] = (i <= a) ? path_tab[best * (D + 1) + i] : -1;
+  if (i == 0) {
+    *accept_len = a;
+    *bonus = amax[best];
+    if (best_p) *best_p = top1p[best];
+  }
 }
 
 }  // namespace

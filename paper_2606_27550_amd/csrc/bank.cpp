@@ -221,3 +221,41 @@ extern "C" int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, fl
                    static_cast<double>(tau_off), static_cast<double>(tau_on));
   return ladder_step(rung, n_rungs, s, tau_on, tau_off);
 }
+
+// NextChildren(T, D) of Algorithm 1 and the joint tree T u F built from it:
+// a node's next-ranked child hangs under it, so each node of depth below D
+// contributes exactly one candidate, appended in node order.
+extern "C" int32_t entmtp_frontier_tree(const int32_t* parent, int32_t T, int32_t max_depth,
+                                        int32_t* joint_parent, uint8_t* in_tree,
+                                        int32_t joint_capacity, int32_t* joint_T) {
+  clear_error();
+  ENTMTP_CHECK_ARG(parent && joint_parent && joint_T, ENTMTP_EINVAL,
+                   "parent, joint_parent and joint_T must be non-NULL");
+  ENTMTP_CHECK_ARG(T >= 1, ENTMTP_EINVAL, "T = %d < 1", T);
+  ENTMTP_CHECK_ARG(max_depth >= 0, ENTMTP_EINVAL, "max_depth = %d < 0", max_depth);
+  ENTMTP_CHECK_ARG(parent[0] == -1, ENTMTP_EINVAL, "parent[0] = %d, the root's must be -1", parent[0]);
+  std::vector<int32_t> depth(static_cast<size_t>(T), 0);
+  int32_t n_cand = 0;
+  for (int32_t i = 0; i < T; ++i) {
+    if (i > 0) {
+      ENTMTP_CHECK_ARG(parent[i] >= 0 && parent[i] < i, ENTMTP_EINVAL,
+                       "parent[%d] = %d: parents must precede their children", i, parent[i]);
+      depth[i] = depth[parent[i]] + 1;
+    }
+    n_cand += depth[i] < max_depth ? 1 : 0;
+  }
+  *joint_T = T + n_cand;
+  ENTMTP_CHECK_ARG(T + n_cand <= joint_capacity, ENTMTP_ENOSPC,
+                   "joint tree has %d nodes, capacity %d", T + n_cand, joint_capacity);
+  int32_t k = T;
+  for (int32_t i = 0; i < T; ++i) {
+    joint_parent[i] = parent[i];
+    if (in_tree) in_tree[i] = 1u;
+    if (depth[i] < max_depth) {
+      joint_parent[k] = i;
+      if (in_tree) in_tree[k] = 0u;
+      ++k;
+    }
+  }
+  return ENTMTP_OK;
+}

@@ -213,8 +213,8 @@ def test_ladder_matches_oracle():
 
 
 def test_frontier_tree_matches_oracle():
-    """The binding's host bookkeeping of the joint tree T u F against the
-    oracle's NextChildren."""
+    """entmtp_frontier_tree (the joint tree T u F, through the C ABI) against
+    the oracle's NextChildren."""
     rng = np.random.default_rng(5)
     for _ in range(200):
         n = int(rng.integers(1, 30))
@@ -223,6 +223,25 @@ def test_frontier_tree_matches_oracle():
         joint, in_tree = api.frontier_tree(parent, D)
         ref, ref_in = orc.joint_tree(parent, D)
         assert joint == ref and in_tree == [int(x) for x in ref_in]
+
+
+def test_frontier_tree_errors():
+    import ctypes
+    lib = api.lib
+    parent = (ctypes.c_int32 * 4)(-1, 0, 0, 1)
+    out = (ctypes.c_int32 * 8)()
+    flags = (ctypes.c_uint8 * 8)()
+    n = ctypes.c_int32(0)
+    # depth 2 admits candidates under nodes 0, 1, 2 (depths 0, 1, 1): 7 nodes
+    assert lib.entmtp_frontier_tree(parent, 4, 2, out, flags, 8, ctypes.byref(n)) == 0
+    assert n.value == 7 and list(out[:7]) == [-1, 0, 0, 1, 0, 1, 2]
+    assert list(flags[:7]) == [1, 1, 1, 1, 0, 0, 0]
+    assert lib.entmtp_frontier_tree(parent, 4, 2, out, None, 6, ctypes.byref(n)) == api.ENOSPC
+    assert n.value == 7
+    bad = (ctypes.c_int32 * 3)(-1, 0, 2)       # a parent that does not precede its child
+    assert lib.entmtp_frontier_tree(bad, 3, 2, out, flags, 8, ctypes.byref(n)) == api.EINVAL
+    assert lib.entmtp_frontier_tree(parent, 4, -1, out, flags, 8, ctypes.byref(n)) == api.EINVAL
+    assert lib.entmtp_frontier_tree(None, 4, 2, out, flags, 8, ctypes.byref(n)) == api.EINVAL
 
 
 def test_step_config_layout_matches_header(tmp_path):

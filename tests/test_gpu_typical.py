@@ -52,6 +52,37 @@ def separated_drafts(parent, z, am, g, V):
     return tok
 
 
+def deepest_loglik(parent, p, thr):
+    """The accepted nodes of the greatest depth and the fp64 log-likelihood
+    of each one's path (the quantity the tie-break compares)."""
+    T = len(parent)
+    acc, depth, ll = [True] + [False] * (T - 1), [0] * T, [0.0] * T
+    for i in range(1, T):
+        depth[i] = depth[parent[i]] + 1
+        acc[i] = acc[parent[i]] and p[i] > thr[parent[i]]
+        if acc[i]:
+            ll[i] = ll[parent[i]] + np.log(p[i])
+    top = max(depth[i] for i in range(T) if acc[i])
+    return [(i, ll[i]) for i in range(T) if acc[i] and depth[i] == top]
+
+
+def tie_separated(parent, tok, p, thr, gap=1e-3):
+    """fp32 and fp64 choose the same node among the deepest: the winner's
+    path log-likelihood leads every other by `gap`, or the runners-up are
+    exact copies of it (the same draft tokens along the same parents)."""
+    c = sorted(deepest_loglik(parent, p, thr), key=lambda x: -x[1])
+    if len(c) < 2:
+        return True
+    best = c[0]
+    for i, l in c[1:]:
+        if best[1] - l >= gap:
+            continue
+        same = tok[i] == tok[best[0]] and parent[i] == parent[best[0]]
+        if not same:
+            return False
+    return True
+
+
 def run_typical(api, parent, X, W, tok):
     T, hid = X.shape
     V = W.shape[0]
@@ -89,8 +120,13 @@ def test_typical_acceptance_matches_oracle(api, T, depth, hid, V, spike):
         X = margin_hidden(40 + T, T, W)
     z = orc.verify_logits(X, W).astype(np.float32).astype(np.float64)
     am = z.argmax(axis=1)
-    tok = separated_drafts(parent, z, am, g, V)
-    ra, rpath, rbonus, rbest, rp, rthr = orc.accept_typical(parent, tok, z, INV_T, EPS, ALPHA)
+    for _ in range(50):
+        tok = separated_drafts(parent, z, am, g, V)
+        ra, rpath, rbonus, rbest, rp, rthr = orc.accept_typical(parent, tok, z, INV_T, EPS, ALPHA)
+        if tie_separated(parent, tok, rp, rthr):
+            break
+    else:
+        raise RuntimeError("no draft set with a separated choice among the deepest nodes")
     local = rp[1:] > rthr[np.asarray(parent[1:])]
     beyond_greedy = sum(1 for i in range(1, T) if local[i - 1] and tok[i] != am[parent[i]])
     assert 0 < local.sum() < T - 1 or T < 16
@@ -107,6 +143,33 @@ def test_typical_acceptance_matches_oracle(api, T, depth, hid, V, spike):
     for i in range(1, T):
         assert abs(zd[i] - Xf[parent[i]] @ Wf[tok[i]]) <= 1e-4 * max(1.0, abs(z).max())
         assert abs(zt[i] - Xf[parent[i]] @ Wf[am[parent[i]]]) <= 1e-4 * max(1.0, abs(z).max())
+
+
+@pytest.mark.parametrize("T,depth,hid,V", [(27, 4, 512, 1000), (64, 5, 1024, 4000), (128, 6, 4096, 32000)])
+def test_typical_chooses_the_most_likely_deepest_path(api, T, depth, hid, V):
+    """Flat rows (small hidden states): nearly every draft passes, many nodes
+    share the greatest depth, and the choice among them is the path whose
+    drafts are jointly most likely, not the lowest index."""
+    say("typical tie-break", T, hid, V)
+    g = np.random.default_rng(7 * T + V)
+    parent = synth.uniform_attach_tree(70 + T, T, depth)
+    W = synth.lm_head_weight(70 + T, V, hid, std=0.05)
+    X = margin_hidden(70 + T, T, W)
+    z = orc.verify_logits(X, W).astype(np.float32).astype(np.float64)
+    am = z.argmax(axis=1)
+    for _ in range(50):
+        tok = separated_drafts(parent, z, am, g, V)
+        ra, rpath, rbonus, rbest, rp, rthr = orc.accept_typical(parent, tok, z, INV_T, EPS, ALPHA)
+        cands = deepest_loglik(parent, rp, rthr)
+        if len(cands) > 1 and rbest != cands[0][0] and tie_separated(parent, tok, rp, rthr):
+            break
+    else:
+        raise RuntimeError("no draft set whose deepest tie the likelihood decides")
+    a, path, bonus, best, *_ = run_typical(api, parent, X, W, tok)
+    say(f"  accept {a} (oracle {ra}), chosen {rbest} among {[c for c, _ in cands]}")
+    assert (a, bonus) == (ra, rbonus)
+    assert path[: a + 1].tolist() == list(rpath)
+    assert (path[a + 1:] == -1).all()
 
 
 def test_typical_equals_greedy_on_peaked_rows(api):

@@ -1,6 +1,7 @@
 """Pins of the oracle's typical acceptance (not the GPU): degenerate
 thresholds, closed forms for uniform logits, equivalence with greedy
-acceptance on peaked distributions, and a hand-worked three-token example."""
+acceptance on peaked distributions, hand-worked examples, and the choice
+among equally deep accepted nodes checked by brute force."""
 import math
 
 import numpy as np
@@ -63,7 +64,13 @@ def test_hand_worked_three_token_example():
     # eps 0.09: threshold 0.09, every child (0.6, 0.3, 0.1) passes
     a, path, bonus, best, p, thr = orc.accept_typical(parent, tok, z, 1.0, 0.09, 0.3)
     assert np.allclose(p[1:], [0.6, 0.3, 0.1]) and abs(thr[0] - 0.09) < 1e-12
-    assert (a, best) == (1, 1) and bonus == 0            # lowest index among the depth-1 nodes
+    assert (a, best) == (1, 1) and bonus == 0            # the most likely depth-1 node (0.6)
+    # the same children with their tokens permuted: the 0.6 child is node 2
+    a, path, _, best, p, _ = orc.accept_typical(parent, [0, 2, 0, 1], z, 1.0, 0.09, 0.3)
+    assert np.allclose(p[1:], [0.1, 0.6, 0.3]) and (a, best, list(path)) == (1, 2, [0, 2])
+    # equal tokens are equally likely: the lowest index wins
+    a, _, _, best, _, _ = orc.accept_typical(parent, [0, 1, 1, 2], z, 1.0, 0.09, 0.3)
+    assert (a, best) == (1, 1)
     # eps 0.2: threshold 0.3 * exp(-H) = 0.1222; the 0.1 child fails, 0.3 passes
     a, _, _, _, _, thr = orc.accept_typical(parent, [0, 2, 2, 1], z, 1.0, 0.2, 0.3)
     assert abs(thr[0] - 0.3 * math.exp(-H)) < 1e-12 and a == 1
@@ -89,3 +96,53 @@ def test_threshold_is_the_parents_and_strict():
     z = np.zeros((2, 10))
     a, _, _, _, p, thr = orc.accept_typical(parent, [0, 3], z, 1.0, 0.1, 5.0)
     assert p[1] == 0.1 and thr[0] == 0.1 and a == 0
+
+
+def test_deepest_tie_goes_to_the_most_likely_path():
+    # parent = [-1, 0, 0, 1, 2]: nodes 1, 2 at depth 1, node 3 under 1, node 4 under 2.
+    # root p = (0.6, 0.3, 0.1); node 1 p = (0.7, 0.2, 0.1); node 2 p = (0.4, 0.35, 0.25)
+    parent = [-1, 0, 0, 1, 2]
+    z = np.log(np.array([[0.6, 0.3, 0.1], [0.7, 0.2, 0.1], [0.4, 0.35, 0.25],
+                         [1 / 3, 1 / 3, 1 / 3], [1 / 3, 1 / 3, 1 / 3]]))
+    # node 1 drafts token 1 (0.3), node 2 token 0 (0.6); node 3 token 0 under
+    # node 1 (0.7), node 4 token 0 under node 2 (0.4).  Both depth-2 nodes pass
+    # (threshold <= 0.09); their paths: 0.3 * 0.7 = 0.21 < 0.6 * 0.4 = 0.24, so
+    # node 4 is chosen although its own token is the less likely one
+    a, path, bonus, best, p, _ = orc.accept_typical(parent, [0, 1, 0, 0, 0], z, 1.0, 0.09, 0.3)
+    assert np.allclose(p[1:], [0.3, 0.6, 0.7, 0.4])
+    assert (a, best, list(path), bonus) == (2, 4, [0, 2, 4], 0)
+    # node 3's token made 0.9 likely: 0.27 > 0.24, node 3 wins
+    z[1] = np.log([0.9, 0.05, 0.05])
+    a, path, _, best, _, _ = orc.accept_typical(parent, [0, 1, 0, 0, 0], z, 1.0, 0.09, 0.3)
+    assert (a, best, list(path)) == (2, 3, [0, 1, 3])
+
+
+def test_choice_among_deepest_matches_brute_force():
+    """The chosen node maximises the product of its path's draft
+    probabilities (computed here as a product, not as a sum of logs) over
+    every accepted node of the greatest depth, lowest index on ties."""
+    V = 6
+    for seed in range(40):
+        g = np.random.default_rng(300 + seed)
+        T = int(g.integers(2, 30))
+        parent = synth.uniform_attach_tree(300 + seed, T, int(g.integers(1, min(5, T))))
+        z = g.standard_normal((T, V)) * 0.3         # flat rows: many siblings pass together
+        tok = g.integers(0, V, T)
+        a, path, _, best, p, thr = orc.accept_typical(parent, tok, z, 1.0, 0.09, 0.3)
+        acc = [True] + [False] * (T - 1)
+        for i in range(1, T):
+            acc[i] = acc[parent[i]] and p[i] > thr[parent[i]]
+        depth = [0] * T
+        for i in range(1, T):
+            depth[i] = depth[parent[i]] + 1
+        top = max(depth[i] for i in range(T) if acc[i])
+        def prob(i):
+            out = 1.0
+            while i != 0:
+                out *= p[i]
+                i = parent[i]
+            return out
+        cands = [i for i in range(T) if acc[i] and depth[i] == top]
+        want = min(cands, key=lambda i: (-prob(i), i))
+        assert (a, best) == (top, want), (seed, cands)
+        assert list(path) == orc.ancestors_or_self(parent, want)
