@@ -442,14 +442,16 @@ def stats_partials_bytes(T: int, hid: int, V: int) -> int:
 
 
 def verify_logits_partials(hidden, w_lm, logits, inv_temp: float, partials, stream=None) -> None:
-    """First half of verify_logits_stats: logits plus per-slice statistics partials."""
+    """First half of verify_logits_stats: per-slice statistics partials, and
+    the logits unless ``logits`` is None."""
     import torch
     _need(hidden.dim() == 2 and w_lm.dim() == 2, "hidden and w_lm are 2-D")
     T, hid = hidden.shape
     V = w_lm.shape[0]
     _dev(hidden, "hidden", torch.bfloat16, (T, hid))
     _dev(w_lm, "w_lm", torch.bfloat16, (V, hid))
-    _dev(logits, "logits", torch.float32, (T, V))
+    if logits is not None:
+        _dev(logits, "logits", torch.float32, (T, V))
     _need(partials.is_cuda and partials.is_contiguous(), "partials must be a contiguous GPU tensor")
     _check(lib.entmtp_verify_logits_partials(_p(hidden), _p(w_lm), T, hid, V, inv_temp, _p(logits),
                                              _p(partials), partials.numel() * partials.element_size(),

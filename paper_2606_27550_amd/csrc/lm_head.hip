@@ -42,6 +42,7 @@
 
 #include "common.hpp"
 #include "stats.hpp"
+#include "stream_pipe.hpp"
 
 namespace entmtp {
 namespace {
@@ -50,11 +51,6 @@ constexpr int kLmThreads = 256;
 constexpr int kLmWaves = kLmThreads / 64;
 constexpr int kLmTiles = 2;                         // 16-row tiles per wave
 constexpr int kLmRowsPerBlock = 16 * kLmTiles * kLmWaves;  // 128
-
-__device__ __forceinline__ int slice_begin(int b, int G, int V) {
-  if (b >= G) return V;
-  return static_cast<int>((static_cast<long long>(V) * b / G) & ~3ll);
-}
 
 template <int NT, int BK>
 __global__ __launch_bounds__(kLmThreads) void lm_head_kernel(
@@ -205,34 +201,6 @@ constexpr int kL3Threads = 64 * kL3Waves;
 constexpr int kL3Bk = 128;                 // k per stage
 constexpr int kL3RowBytes = kL3Bk * 2;     // 256
 constexpr int kL3TileBytes = 16 * kL3RowBytes;
-
-// s_waitcnt vmcnt(N) lgkmcnt(0) (gfx9 encoding; expcnt not waited on): this
-// wave's direct-to-LDS loads older than the last N have landed and its own
-// LDS reads are complete.
-template <int N>
-__device__ __forceinline__ void wait_vmcnt() {
-  static_assert(N >= 0 && N < 64, "vmcnt range");
-  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (0 << 8));
-}
-
-// One direct global->LDS copy of 16 bytes per lane: lane l's bytes land at
-// lds + 16 * l (lds is wave-uniform).  Kept in a device-only function: in a
-// kernel's (host+device) lambda this gfx950 builtin would keep the compiler
-// from emitting the kernel's host launch stub.
-__device__ __forceinline__ void lds_dma16(const void* src, void* lds) {
-  __builtin_amdgcn_global_load_lds(src, lds, 16, 0, 0);
-}
-
-// Workgroup barrier without a memory-model fence.  __syncthreads() would add
-// a release fence, which waits for every outstanding load (the LDS-DMA
-// stages count as LDS writes) and so drains the pipeline; here the waits are
-// explicit (wait_vmcnt) and the empty asm statements only stop the compiler
-// from moving LDS accesses across the barrier.
-__device__ __forceinline__ void stage_barrier() {
-  asm volatile("" ::: "memory");
-  __builtin_amdgcn_s_barrier();
-  asm volatile("" ::: "memory");
-}
 
 template <int NT>
 struct L3Shape {
@@ -863,6 +831,17 @@ bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, in
   // per CU keep more of W in flight (the batch-8 LM head: 259 -> 247 us),
   // but they fill the CU's LDS, and beside the 13B step's attention they lost
   // (96 -> 106 us)
+  // many rows: the tiled contraction reads W once per 128 rows with each
+  // LDS byte feeding more products
+  if (lm_gemm_takes(T, hid, hyb_grid(V), device_cus())) {
+    if (ev0)
+      if ((*rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord"))) return true;
+    *rc = launch_lm_gemm(reinterpret_cast<const entmtp_bf16*>(X),
+                         reinterpret_cast<const entmtp_bf16*>(W), logits, T, hid, V, hyb_grid(V),
+                         inv_temp, STATS ? part : nullptr, s);
+    if (*rc == ENTMTP_OK && ev1) *rc = hip_status(hipEventRecord(ev1, s), "hipEventRecord");
+    return true;
+  }
   const bool pair = hyb_grid(V) >= 2 * device_cus();
   const bool pair128 = pair && beside;
   auto go = [&](auto nch) {

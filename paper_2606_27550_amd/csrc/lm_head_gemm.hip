@@ -1,0 +1,392 @@
+// LM head over many rows: the verification logits of §2.3 for a batch of
+// trees verified together (up to hundreds of rows), as a tiled MFMA
+// contraction.
+//
+// With hundreds of rows the product logits = X W^T is no longer a skinny
+// stream: at 544 rows and a 128256-entry vocabulary it holds 571 GFLOP for
+// 1.05 GB of W, so it is bound by the matrix cores, not HBM.  The streaming
+// kernels take at most 128 rows per pass and stage W through registers of
+// one wave per 16 rows; this kernel gives a workgroup a 256-row vocabulary
+// block (four of the streaming grid's slices) and 128 rows of X, shared
+// through LDS, so each LDS byte feeds 64 to 128 products:
+//  * four waves in a 2 x 2 grid over the 256 x 128 output tile, each
+//    accumulating a 128 x 64 sub-tile with v_mfma_f32_16x16x32_bf16;
+//  * K advances in stages of 64: each wave loads its share of a stage's W
+//    and X rows into VGPRs (8 rows x 128 bytes per instruction) two stages
+//    ahead of storing them into one of three LDS slots, two stages ahead of
+//    their use (direct global->LDS copies measured at a third of the rate
+//    this tile consumes; 16 rows x 64 bytes per instruction at two thirds);
+//  * within a 128-byte row the eight 16-byte chunks are stored XOR-swizzled
+//    by the row's place in its 16-row group, so the MFMA fragment reads
+//    (16 rows, one chunk) spread over all LDS banks;
+//  * the stores, loads and fragment reads of a stage are interleaved one by
+//    one with its products, and a k-step's fragments are read during the
+//    previous k-step; one LDS wait and one barrier per stage;
+//  * the passes of one vocabulary block run on one XCD (dispatch is
+//    round-robin), so W fetched by one pass is an L2 hit for the others;
+//  * with statistics the epilogue reduces each row's accumulators over the
+//    block into one partial (the streaming kernels' layout: the block's
+//    partial in its first slice, neutral partials in the other three), so
+//    the statistics merge is unchanged.
+// Hidden sizes 4096 and 5120 (the stage count is a template parameter).
+#include <type_traits>
+
+#include "common.hpp"
+#include "stats.hpp"
+#include "stream_pipe.hpp"
+
+namespace entmtp {
+namespace {
+
+constexpr int kGemmThreads = 256;   // four waves, 2 x 2 over the output tile
+constexpr int kGemmSlices = 4;      // streaming-grid slices (at most 64 rows each) per block
+constexpr int kGemmBM = 64 * kGemmSlices;
+constexpr int kGemmBN = 128;        // rows of X per pass
+constexpr int kGemmBK = 64;         // k per stage: two MFMA k-steps, 128-byte rows
+constexpr int kGemmMinRows = 128;   // the streaming kernels' largest pass
+constexpr int kGemmSlots = 3;       // LDS stages: multiplied, read, written
+constexpr int kGemmD = 2;           // stages of loads held in VGPRs ahead of their store
+
+template <int BN>
+struct GemmShape {
+  static constexpr int ROWB = kGemmBK * 2;        // bytes of a row per stage
+  static constexpr int CH = ROWB / 16;            // 16-byte chunks per row
+  static constexpr int RPI = 64 / CH;             // rows per load instruction (8)
+  static constexpr int A_BYTES = kGemmBM * ROWB;  // W block
+  static constexpr int B_BYTES = BN * ROWB;       // X block
+  static constexpr int SLOT = A_BYTES + B_BYTES;
+  static constexpr int AI = kGemmBM / RPI / 4;    // W loads per wave per stage
+  static constexpr int BI = BN / RPI / 4;         // X loads per wave per stage
+  static constexpr int LI = AI + BI;
+  static constexpr int WM = kGemmBM / 2, WN = BN / 2;   // wave sub-tile
+  static constexpr int MI = WM / 16, NI = WN / 16;
+  static constexpr int NF = MI + NI;              // fragments per k-step
+  static_assert(BN % (4 * RPI) == 0 && AI % 2 == 0 && BI % 2 == 0, "loads split evenly");
+  static_assert(kGemmSlots * SLOT <= 160 * 1024, "slots fit in LDS");
+};
+
+// Slot of 16-byte chunk c of row r (eight chunks per row) is c ^ swz(r).  A
+// fragment read takes one chunk of 16 consecutive rows; rows r, r + 2, r + 4,
+// r + 6 share banks (128-byte rows, 256-byte bank period) unless their slots
+// differ, and LDS serving 8 lanes per cycle also needs rows r .. r + 7
+// apart: (r & 7) ^ ((r >> 3) & 1) over the row's place in its 16-row group
+// gives both (a function of r mod 16 only, so stores and reads agree for
+// every 16-row block).
+__device__ __forceinline__ int chunk_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+
+// s_waitcnt lgkmcnt(N) alone (vmcnt and expcnt left at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_lds_but() {
+  static_assert(N >= 0 && N < 16, "lgkmcnt range");
+  __builtin_amdgcn_s_waitcnt(0xC07F | (N << 8));
+}
+__device__ __forceinline__ void wait_lds() { wait_lds_but<0>(); }
+
+// Waits out the latency of the last MFMAs before their accumulators are
+// read (32 wait states: the longest 16x16x32 result latency is 16 passes of
+// four cycles, of which the issue of the following instructions covers the
+// rest).
+__device__ __forceinline__ void mfma_drain() {
+  asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
+}
+
+template <int BN, int NST, bool STATS>
+__global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
+  using Sh = GemmShape<BN>;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kGemmSlots * Sh::SLOT];
+
+  // 1-D grid over (block group, pass, XCD): the passes of one vocabulary
+  // block are consecutive workgroups of one XCD
+  const int groups = (G + kGemmSlices - 1) / kGemmSlices;
+  const int passes = (T + BN - 1) / BN;
+  const int bid = blockIdx.x, r8 = bid >> 3;
+  const int pass = r8 % passes, grp = (r8 / passes) * 8 + (bid & 7);
+  if (grp >= groups) return;
+  const int j0 = pass * BN;
+  const int r0 = slice_begin(kGemmSlices * grp, G, V);
+  const int r1 = slice_begin(kGemmSlices * grp + kGemmSlices, G, V);
+  const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+  const StatPart empty{-INFINITY, 0.f, 0.f, 0x7fffffff};
+  if (r0 >= r1) {   // empty block (tiny V): neutral partials only
+    if constexpr (STATS)
+      for (int c = tid; c < BN; c += kGemmThreads)
+        if (j0 + c < T)
+          for (int u = 0; u < kGemmSlices && kGemmSlices * grp + u < G; ++u)
+            part[static_cast<size_t>(j0 + c) * G + kGemmSlices * grp + u] = empty;
+    return;
+  }
+
+  // load instruction q of a wave covers rows (wave * n + q) * 8 .. + 7 of
+  // the block (n = AI for W, BI for X); lane l takes chunk l % 8 of row l / 8
+  // and stores it at slot (l % 8) ^ swz(row).  W rows past the block load
+  // the next block's rows (or the last row of W), X rows past T the pass's
+  // first row: in bounds, and never stored.
+  const int lrow = lane >> 3, lch = lane & 7;
+  uint32_t src[Sh::LI];   // byte offsets from W (q < AI) or X
+#pragma unroll
+  for (int q = 0; q < Sh::AI; ++q) {
+    const int row = min(r0 + (wave * Sh::AI + q) * Sh::RPI + lrow, V - 1);
+    src[q] = (static_cast<uint32_t>(row) * hid + 8 * lch) * 2u;
+  }
+#pragma unroll
+  for (int q = 0; q < Sh::BI; ++q) {
+    const int rr = (wave * Sh::BI + q) * Sh::RPI + lrow;
+    const int node = j0 + rr < T ? j0 + rr : j0;
+    src[Sh::AI + q] = (static_cast<uint32_t>(node) * hid + 8 * lch) * 2u;
+  }
+  // LDS byte offset of the lane's chunk for load q (rows of one instruction
+  // are 8 apart within the block, so the swizzle depends on q's parity)
+  auto dst_of = [&](int q) {
+    const int rr = q < Sh::AI ? (wave * Sh::AI + q) * Sh::RPI + lrow
+                              : (wave * Sh::BI + q - Sh::AI) * Sh::RPI + lrow;
+    return (q < Sh::AI ? 0 : Sh::A_BYTES) + rr * Sh::ROWB + ((lch ^ chunk_swz(rr)) << 4);
+  };
+  // blocks walk K in rotated order, so that CUs do not all stream the same
+  // column band of W at once
+  const int rot = static_cast<int>((static_cast<unsigned>(grp) * 7u) % static_cast<unsigned>(NST));
+  const uint8_t* const Wb = reinterpret_cast<const uint8_t*>(W);
+  const uint8_t* const Xb = reinterpret_cast<const uint8_t*>(X);
+  u32x4 pre[kGemmD][Sh::LI];
+  // load q of stage `stage` (clamped to the last stage)
+  auto load_one = [&](u32x4& r, int q, int stage) {
+    int ks = (stage < NST ? stage : NST - 1) + rot;
+    ks = ks >= NST ? ks - NST : ks;
+    const uint32_t off = src[q] + static_cast<uint32_t>(ks * Sh::ROWB);
+    // W is streamed once: keep it out of the caches' way; X is re-read
+    if (q < Sh::AI)
+      r = __builtin_nontemporal_load(reinterpret_cast<const u32x4*>(Wb + off));
+    else
+      r = *reinterpret_cast<const u32x4*>(Xb + off);
+  };
+
+  const int lr = lane & 15, lg = lane >> 4;
+  const int wm = wave & 1, wn = wave >> 1;
+  // fragment f of k-step j: W block f (f < MI) rows wm*WM + 16f + lr, or X
+  // block f - MI rows wn*WN + 16(f - MI) + lr; chunk 4j + lg
+  auto read_one = [&](bf16x8& out, const uint8_t* slot, int j, int f) {
+    const int row = f < Sh::MI ? wm * Sh::WM + 16 * f + lr : wn * Sh::WN + 16 * (f - Sh::MI) + lr;
+    const int off = (f < Sh::MI ? 0 : Sh::A_BYTES) + row * Sh::ROWB + (((4 * j + lg) ^ chunk_swz(lr)) << 4);
+    out = as_bf16x8(*reinterpret_cast<const u32x4*>(slot + off));
+  };
+
+  f32x4 acc[Sh::MI][Sh::NI];
+#pragma unroll
+  for (int mi = 0; mi < Sh::MI; ++mi)
+#pragma unroll
+    for (int ni = 0; ni < Sh::NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
+  bf16x8 frag[2][Sh::NF];
+  // The products accumulate in place in AGPRs, written as inline assembly:
+  // with the builtin the compiler renamed the accumulators from one step to
+  // the next and spent a move per accumulator register per loop trip
+  // undoing it.  The "memory" clobber keeps the step's loads, stores and
+  // fragment reads where the source puts them among the products.  Nothing
+  // reads an accumulator between products; mfma_drain() covers the window
+  // before the epilogue reads them.
+  auto mfma_one = [&](int buf, int i) {
+    const int mi = i / Sh::NI, ni = i % Sh::NI;
+    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                 : "+a"(acc[mi][ni])
+                 : "v"(frag[buf][mi]), "v"(frag[buf][Sh::MI + ni])
+                 : "memory");
+  };
+  // the fragments in the order the products need them: X blocks (every
+  // product of the first W block uses one), then W blocks
+  auto frag_at = [&](int n) { return n < Sh::NI ? Sh::MI + n : n - Sh::NI; };
+
+  // Stage s is loaded into pre[s % D] at step s - 2 - D (the prologue for
+  // the first ones), stored into slot s % 3 at step s - 2, its first k-step's
+  // fragments read during step s - 1, its second's during step s, and it is
+  // multiplied at step s.  A slot is overwritten two steps after its last
+  // fragments were read, behind a barrier.  Loads past the last stage
+  // re-load it.
+#pragma unroll
+  for (int k = 0; k < kGemmD; ++k)
+#pragma unroll
+    for (int q = 0; q < Sh::LI; ++q) load_one(pre[k][q], q, k);
+#pragma unroll
+  for (int k = 0; k < 2; ++k)
+#pragma unroll
+    for (int q = 0; q < Sh::LI; ++q) {
+      *reinterpret_cast<u32x4*>(ring + k * Sh::SLOT + dst_of(q)) = pre[k % kGemmD][q];
+      load_one(pre[k % kGemmD][q], q, kGemmD + k);
+    }
+  wait_lds();
+  stage_barrier();
+#pragma unroll
+  for (int n = 0; n < Sh::NF; ++n) read_one(frag[0][frag_at(n)], ring, 0, frag_at(n));
+  mfma_drain();   // the accumulators' zeroing precedes their first product
+
+  // Step c, K = c mod 6 (slot and load set depend on K only).  Each k-step
+  // runs its products in groups of (product, store, product, load, product,
+  // read, product, read, product): half the stores of stage c + 2 and the
+  // loads of stage c + 2 + D that refill their registers, and the fragments
+  // of the next k-step (stage c's second in k-step 0, stage c + 1's first in
+  // k-step 1).  Issued in one burst the LDS accesses filled the LDS queue
+  // and the wave stalled there with the matrix pipe idle.  Every store is
+  // followed by exactly two reads, so lgkmcnt(2) at the end means the
+  // step's stores have landed.
+  constexpr int kMma = Sh::MI * Sh::NI;
+  constexpr int kHalf = Sh::LI / 2;
+  static_assert(2 * kHalf == Sh::NF && 5 * kHalf <= kMma, "one group per store");
+  auto kstep = [&](int j, uint8_t* wslot, u32x4 (&pr)[Sh::LI], const uint8_t* rslot, int rj,
+                   int c) {
+#pragma unroll
+    for (int g = 0; g < kHalf; ++g) {
+      const int q = j * kHalf + g;
+      mfma_one(j, 5 * g);
+      *reinterpret_cast<u32x4*>(wslot + dst_of(q)) = pr[q];
+      mfma_one(j, 5 * g + 1);
+      load_one(pr[q], q, c + 2 + kGemmD);
+      mfma_one(j, 5 * g + 2);
+      read_one(frag[j ^ 1][frag_at(2 * g)], rslot, rj, frag_at(2 * g));
+      mfma_one(j, 5 * g + 3);
+      read_one(frag[j ^ 1][frag_at(2 * g + 1)], rslot, rj, frag_at(2 * g + 1));
+      mfma_one(j, 5 * g + 4);
+    }
+#pragma unroll
+    for (int i = 5 * kHalf; i < kMma; ++i) mfma_one(j, i);
+  };
+  auto step = [&](auto kc, int c) {
+    constexpr int K = decltype(kc)::value;
+    uint8_t* wslot = ring + ((K + 2) % kGemmSlots) * Sh::SLOT;
+    u32x4 (&pr)[Sh::LI] = pre[(K + 2) % kGemmD];
+    kstep(0, wslot, pr, ring + (K % kGemmSlots) * Sh::SLOT, 1, c);
+    kstep(1, wslot, pr, ring + ((K + 1) % kGemmSlots) * Sh::SLOT, 0, c);
+    wait_lds_but<2>();
+    stage_barrier();
+  };
+  static_assert(6 % kGemmD == 0, "six steps return slots and load sets to their start");
+  using I0 = std::integral_constant<int, 0>;
+  using I1 = std::integral_constant<int, 1>;
+  using I2 = std::integral_constant<int, 2>;
+  using I3 = std::integral_constant<int, 3>;
+  using I4 = std::integral_constant<int, 4>;
+  using I5 = std::integral_constant<int, 5>;
+  constexpr int kRounds = NST / 6;
+  for (int c = 0; c < 6 * kRounds; c += 6) {
+    step(I0{}, c);
+    step(I1{}, c + 1);
+    step(I2{}, c + 2);
+    step(I3{}, c + 3);
+    step(I4{}, c + 4);
+    step(I5{}, c + 5);
+  }
+  constexpr int kTail = NST - 6 * kRounds;
+  if constexpr (kTail > 0) step(I0{}, 6 * kRounds);
+  if constexpr (kTail > 1) step(I1{}, 6 * kRounds + 1);
+  if constexpr (kTail > 2) step(I2{}, 6 * kRounds + 2);
+  if constexpr (kTail > 3) step(I3{}, 6 * kRounds + 3);
+  if constexpr (kTail > 4) step(I4{}, 6 * kRounds + 4);
+  mfma_drain();
+
+  const int vbase = r0 + wm * Sh::WM + 4 * lg;   // first of the lane's rows in block mi = 0
+  if (logits) {
+    const bool vec_ok = (V & 3) == 0;
+#pragma unroll
+    for (int mi = 0; mi < Sh::MI; ++mi) {
+      const int v = vbase + 16 * mi;
+      // one block row at a time: the scheduler would otherwise pull every
+      // accumulator out of the AGPRs at once and spill
+      __builtin_amdgcn_sched_barrier(0);
+#pragma unroll
+      for (int ni = 0; ni < Sh::NI; ++ni) {
+        const int node = j0 + wn * Sh::WN + 16 * ni + lr;
+        if (node >= T) continue;
+        float* dst = logits + static_cast<size_t>(node) * V + v;
+        if (vec_ok && v + 3 < r1) {
+          *reinterpret_cast<f32x4*>(dst) = acc[mi][ni];
+        } else {
+#pragma unroll
+          for (int r = 0; r < 4; ++r)
+            if (v + r < r1) dst[r] = acc[mi][ni][r];
+        }
+      }
+    }
+  }
+  if constexpr (STATS) {
+    // per row: the wave's partial over its 128 vocabulary rows (lane, then
+    // the four lane groups), then the two waves of a row in LDS
+    StatPart* wpart = reinterpret_cast<StatPart*>(ring);   // [2][BN]
+#pragma unroll
+    for (int ni = 0; ni < Sh::NI; ++ni) {
+      __builtin_amdgcn_sched_barrier(0);   // one node column at a time (as above)
+      StatPart p = empty;
+#pragma unroll
+      for (int mi = 0; mi < Sh::MI; ++mi)
+#pragma unroll
+        for (int r = 0; r < 4; ++r)
+          if (vbase + 16 * mi + r < r1) take_max(p.zmax, p.idx, acc[mi][ni][r], vbase + 16 * mi + r);
+#pragma unroll
+      for (int off = 16; off <= 32; off <<= 1)
+        take_max(p.zmax, p.idx, __shfl_xor(p.zmax, off, 64), __shfl_xor(p.idx, off, 64));
+      if (p.zmax != -INFINITY) {
+        const float my = p.zmax * inv_temp;
+#pragma unroll
+        for (int mi = 0; mi < Sh::MI; ++mi)
+#pragma unroll
+          for (int r = 0; r < 4; ++r) {
+            if (vbase + 16 * mi + r < r1) {
+              const float y = acc[mi][ni][r] * inv_temp - my;
+              const float e = expf(y);
+              p.Z += e;
+              if (e > 0.f) p.S += y * e;
+            }
+          }
+      }
+#pragma unroll
+      for (int off = 16; off <= 32; off <<= 1) {
+        p.Z += __shfl_xor(p.Z, off, 64);
+        p.S += __shfl_xor(p.S, off, 64);
+      }
+      if (lg == 0) wpart[wm * BN + wn * Sh::WN + 16 * ni + lr] = p;
+    }
+    __syncthreads();
+    for (int c = tid; c < BN; c += kGemmThreads) {
+      if (j0 + c >= T) continue;
+      StatPart q = wpart[c];
+      part_merge(q, wpart[BN + c], inv_temp);
+      StatPart* dst = part + static_cast<size_t>(j0 + c) * G + kGemmSlices * grp;
+      dst[0] = q;
+#pragma unroll
+      for (int u = 1; u < kGemmSlices; ++u)
+        if (kGemmSlices * grp + u < G) dst[u] = empty;
+    }
+  }
+}
+
+template <int NST, bool STATS>
+int32_t launch_gemm(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
+                    int G, float inv_temp, StatPart* part, hipStream_t s) {
+  const int groups = (G + kGemmSlices - 1) / kGemmSlices;
+  const int passes = (T + kGemmBN - 1) / kGemmBN;
+  const int blocks = (groups + 7) / 8 * passes * 8;
+  hipLaunchKernelGGL((lm_head_gemm_kernel<kGemmBN, NST, STATS>), dim3(blocks), dim3(kGemmThreads),
+                     0, s, X, W, logits, T, hid, V, G, inv_temp, part);
+  return launch_status("verify_logits (tiled) launch");
+}
+
+}  // namespace
+
+bool lm_gemm_takes(int T, int hid, int G, int cus) {
+  if ((hid != 64 * kGemmBK && hid != 80 * kGemmBK) || G % kGemmSlices != 0) return false;
+  // more than one streaming pass of 128 rows, or a vocabulary large enough
+  // for a block per CU (128256 entries: 501 blocks; 32000: 125, which
+  // leaves half the CUs idle while the streaming kernel keeps them all busy)
+  return T > kGemmMinRows || (T > kGemmMinRows / 2 && G / kGemmSlices >= cus);
+}
+
+int32_t launch_lm_gemm(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, float* logits, int T,
+                       int hid, int V, int G, float inv_temp, void* partials, hipStream_t s) {
+  const auto* X = reinterpret_cast<const uint16_t*>(hidden);
+  const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
+  auto* part = static_cast<StatPart*>(partials);
+  if (hid == 64 * kGemmBK)
+    return part ? launch_gemm<64, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
+                : launch_gemm<64, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
+  return part ? launch_gemm<80, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
+              : launch_gemm<80, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
+}
+
+}  // namespace entmtp

@@ -281,4 +281,12 @@ int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w
                                  const int* T_dev, int T_max, int hid, int V, float inv_temp,
                                  void* partials, hipStream_t s, hipEvent_t ev0, hipEvent_t ev1);
 
+// The LM head over many rows as a tiled contraction (lm_head_gemm.hip): true
+// when it takes T rows of hidden size hid for a streaming grid of G slices on
+// a device with `cus` compute units; it then writes the streaming kernels'
+// partial layout (G per row).
+bool lm_gemm_takes(int T, int hid, int G, int cus);
+int32_t launch_lm_gemm(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, float* logits, int T,
+                       int hid, int V, int G, float inv_temp, void* partials, hipStream_t s);
+
 }  // namespace entmtp

@@ -1,0 +1,102 @@
+"""GPU parity of the tiled LM head (the kernel that takes batches of many
+rows: more than 128, or more than 64 at a 128256-entry vocabulary) against
+the oracle: logits within 1e-4 of the largest |logit|, argmax bit-exact where
+the top-2 gap exceeds fp32 accumulation error, entropy and top-1 probability
+within relative 1e-3, at both temperatures, through the partials + finalize
+entry points the batched step uses and through the logits-only entry point.
+"""
+import numpy as np
+import pytest
+
+torch = pytest.importorskip("torch")
+
+from oracle import entmtp_oracle as orc  # noqa: E402
+from paper_2606_27550_amd import synth  # noqa: E402
+from tests.helpers import dev_bf16  # noqa: E402
+
+pytestmark = pytest.mark.gpu
+
+RTOL_STATS = 1e-3
+
+
+@pytest.fixture(scope="module")
+def api():
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    from paper_2606_27550_amd import api as _api
+    return _api
+
+
+def say(*a):
+    print("[gpu-test]", *a, flush=True)
+
+
+_W = {}
+
+
+def weight(V, hid):
+    """One seeded weight per shape, shared by consecutive cases (1 GB at
+    128k x 4096, the slowest input to draw)."""
+    if (V, hid) not in _W:
+        _W.clear()
+        _W[(V, hid)] = (synth.lm_head_weight(30 + hid // 1024, V, hid), None)
+    w, wd = _W[(V, hid)]
+    if wd is None:
+        wd = dev_bf16(w)
+        _W[(V, hid)] = (w, wd)
+    return w, wd
+
+
+def check_rows(api, X, w, wd, with_logits=True):
+    T, hid = X.shape
+    V = w.shape[0]
+    ref = orc.verify_logits(X, w)                       # fp64 [T, V]
+    gap = np.sort(ref, axis=1)
+    safe = (gap[:, -1] - gap[:, -2]) > 1e-4
+    assert safe.mean() > 0.9
+    Xd = dev_bf16(X)
+    ws = torch.empty(api.stats_partials_bytes(T, hid, V), dtype=torch.uint8, device="cuda")
+    for it in (1.0, 1 / 0.7):
+        z = torch.full((T, V), float("nan"), device="cuda") if with_logits else None
+        H, p1 = torch.empty(T, device="cuda"), torch.empty(T, device="cuda")
+        am = torch.empty(T, dtype=torch.int32, device="cuda")
+        api.verify_logits_partials(Xd, wd, z, it, ws)
+        api.stats_finalize(ws, T, V, it, H, p1, am)
+        torch.cuda.synchronize()
+        if with_logits:
+            err = np.abs(z.cpu().numpy() - ref).max()
+            assert err <= 1e-4 * max(1.0, np.abs(ref).max()), err
+        rH, rp1, ram = orc.logit_stats(ref.astype(np.float32), it)
+        H, p1, am = H.cpu().numpy(), p1.cpu().numpy(), am.cpu().numpy()
+        np.testing.assert_array_equal(am[safe], ram[safe])
+        assert np.all(np.abs(H - rH) <= RTOL_STATS * np.abs(rH) + 1e-6), np.abs(H - rH).max()
+        assert np.all(np.abs(p1 - rp1) <= RTOL_STATS * np.abs(rp1) + 1e-6), np.abs(p1 - rp1).max()
+
+
+def test_tiled_lm_head_logits_only_sampled(api):
+    """entmtp_verify_logits (no statistics) at the batched workload's row
+    counts: sampled columns, the vocabulary's ends included."""
+    V, hid = 128256, 4096
+    w, wd = weight(V, hid)
+    cols = np.unique(np.concatenate([np.random.default_rng(3).integers(0, V, 300),
+                                     [0, 1, 2, 3, 255, 256, V - 4, V - 3, V - 2, V - 1]]))
+    for T in (72, 300):
+        say("tiled LM head logits only", T)
+        X = synth.hidden_rows(60 + T, T, hid)
+        out = torch.full((T, V), float("nan"), device="cuda")
+        api.verify_logits(dev_bf16(X), wd, out)
+        ref = orc.verify_logits_rows(X, w, cols)
+        got = out.cpu().numpy()
+        assert not np.isnan(got).any()
+        err = np.abs(got[:, cols] - ref).max()
+        assert err <= 1e-4 * max(1.0, np.abs(ref).max()), err
+
+
+@pytest.mark.parametrize("T,hid,V", [(65, 4096, 128256), (90, 4096, 128256), (129, 4096, 128256),
+                                     (400, 4096, 128256), (200, 4096, 32000), (257, 4096, 32000),
+                                     (129, 5120, 32000), (300, 5120, 32000)])
+def test_tiled_lm_head_statistics(api, T, hid, V):
+    say("tiled LM head + statistics", T, hid, V)
+    w, wd = weight(V, hid)
+    X = synth.hidden_rows(40 + T, T, hid)
+    check_rows(api, X, w, wd, with_logits=T * V <= 257 * 32000)
