@@ -838,7 +838,7 @@ bool launch_hyb_dispatch(const uint16_t* X, const uint16_t* W, float* logits, in
       if ((*rc = hip_status(hipEventRecord(ev0, s), "hipEventRecord"))) return true;
     *rc = launch_lm_gemm(reinterpret_cast<const entmtp_bf16*>(X),
                          reinterpret_cast<const entmtp_bf16*>(W), logits, T, hid, V, hyb_grid(V),
-                         inv_temp, STATS ? part : nullptr, s);
+                         inv_temp, STATS ? part : nullptr, device_cus(), s);
     if (*rc == ENTMTP_OK && ev1) *rc = hip_status(hipEventRecord(ev1, s), "hipEventRecord");
     return true;
   }

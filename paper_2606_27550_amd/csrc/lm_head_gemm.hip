@@ -39,26 +39,28 @@ namespace entmtp {
 namespace {
 
 constexpr int kGemmThreads = 256;   // four waves, 2 x 2 over the output tile
-constexpr int kGemmSlices = 4;      // streaming-grid slices (at most 64 rows each) per block
-constexpr int kGemmBM = 64 * kGemmSlices;
 constexpr int kGemmBN = 128;        // rows of X per pass
 constexpr int kGemmBK = 64;         // k per stage: two MFMA k-steps, 128-byte rows
 constexpr int kGemmMinRows = 128;   // the streaming kernels' largest pass
 constexpr int kGemmSlots = 3;       // LDS stages: multiplied, read, written
 constexpr int kGemmD = 2;           // stages of loads held in VGPRs ahead of their store
 
-template <int BN>
+// BM vocabulary rows per block: BM / 64 of the streaming grid's slices (at
+// most 64 rows each), 256 when the vocabulary gives every CU a block (128256
+// entries: 501 blocks), else 128 (32000: 250).
+template <int BM, int BN>
 struct GemmShape {
+  static constexpr int SLICES = BM / 64;
   static constexpr int ROWB = kGemmBK * 2;        // bytes of a row per stage
   static constexpr int CH = ROWB / 16;            // 16-byte chunks per row
   static constexpr int RPI = 64 / CH;             // rows per load instruction (8)
-  static constexpr int A_BYTES = kGemmBM * ROWB;  // W block
+  static constexpr int A_BYTES = BM * ROWB;       // W block
   static constexpr int B_BYTES = BN * ROWB;       // X block
   static constexpr int SLOT = A_BYTES + B_BYTES;
-  static constexpr int AI = kGemmBM / RPI / 4;    // W loads per wave per stage
+  static constexpr int AI = BM / RPI / 4;         // W loads per wave per stage
   static constexpr int BI = BN / RPI / 4;         // X loads per wave per stage
   static constexpr int LI = AI + BI;
-  static constexpr int WM = kGemmBM / 2, WN = BN / 2;   // wave sub-tile
+  static constexpr int WM = BM / 2, WN = BN / 2;   // wave sub-tile
   static constexpr int MI = WM / 16, NI = WN / 16;
   static constexpr int NF = MI + NI;              // fragments per k-step
   static_assert(BN % (4 * RPI) == 0 && AI % 2 == 0 && BI % 2 == 0, "loads split evenly");
@@ -90,31 +92,32 @@ __device__ __forceinline__ void mfma_drain() {
   asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
 }
 
-template <int BN, int NST, bool STATS>
+template <int BM, int BN, int NST, bool STATS>
 __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
     int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
-  using Sh = GemmShape<BN>;
+  using Sh = GemmShape<BM, BN>;
+  constexpr int kSlices = Sh::SLICES;
   __shared__ __attribute__((aligned(16))) uint8_t ring[kGemmSlots * Sh::SLOT];
 
   // 1-D grid over (block group, pass, XCD): the passes of one vocabulary
   // block are consecutive workgroups of one XCD
-  const int groups = (G + kGemmSlices - 1) / kGemmSlices;
+  const int groups = (G + kSlices - 1) / kSlices;
   const int passes = (T + BN - 1) / BN;
   const int bid = blockIdx.x, r8 = bid >> 3;
   const int pass = r8 % passes, grp = (r8 / passes) * 8 + (bid & 7);
   if (grp >= groups) return;
   const int j0 = pass * BN;
-  const int r0 = slice_begin(kGemmSlices * grp, G, V);
-  const int r1 = slice_begin(kGemmSlices * grp + kGemmSlices, G, V);
+  const int r0 = slice_begin(kSlices * grp, G, V);
+  const int r1 = slice_begin(kSlices * grp + kSlices, G, V);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const StatPart empty{-INFINITY, 0.f, 0.f, 0x7fffffff};
   if (r0 >= r1) {   // empty block (tiny V): neutral partials only
     if constexpr (STATS)
       for (int c = tid; c < BN; c += kGemmThreads)
         if (j0 + c < T)
-          for (int u = 0; u < kGemmSlices && kGemmSlices * grp + u < G; ++u)
-            part[static_cast<size_t>(j0 + c) * G + kGemmSlices * grp + u] = empty;
+          for (int u = 0; u < kSlices && kSlices * grp + u < G; ++u)
+            part[static_cast<size_t>(j0 + c) * G + kSlices * grp + u] = empty;
     return;
   }
 
@@ -220,7 +223,7 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
 
   // Step c, K = c mod 6 (slot and load set depend on K only).  Each k-step
   // runs its products in groups of (product, store, product, load, product,
-  // read, product, read, product): half the stores of stage c + 2 and the
+  // read, product, read, products): half the stores of stage c + 2 and the
   // loads of stage c + 2 + D that refill their registers, and the fragments
   // of the next k-step (stage c's second in k-step 0, stage c + 1's first in
   // k-step 1).  Issued in one burst the LDS accesses filled the LDS queue
@@ -229,24 +232,24 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   // step's stores have landed.
   constexpr int kMma = Sh::MI * Sh::NI;
   constexpr int kHalf = Sh::LI / 2;
-  static_assert(2 * kHalf == Sh::NF && 5 * kHalf <= kMma, "one group per store");
+  static_assert(2 * kHalf == Sh::NF && 4 * kHalf <= kMma, "one group per store");
   auto kstep = [&](int j, uint8_t* wslot, u32x4 (&pr)[Sh::LI], const uint8_t* rslot, int rj,
                    int c) {
 #pragma unroll
     for (int g = 0; g < kHalf; ++g) {
       const int q = j * kHalf + g;
-      mfma_one(j, 5 * g);
+      const int lo = kMma * g / kHalf, hi = kMma * (g + 1) / kHalf;   // this group's products
+      mfma_one(j, lo);
       *reinterpret_cast<u32x4*>(wslot + dst_of(q)) = pr[q];
-      mfma_one(j, 5 * g + 1);
+      mfma_one(j, lo + 1);
       load_one(pr[q], q, c + 2 + kGemmD);
-      mfma_one(j, 5 * g + 2);
+      mfma_one(j, lo + 2);
       read_one(frag[j ^ 1][frag_at(2 * g)], rslot, rj, frag_at(2 * g));
-      mfma_one(j, 5 * g + 3);
+      mfma_one(j, lo + 3);
       read_one(frag[j ^ 1][frag_at(2 * g + 1)], rslot, rj, frag_at(2 * g + 1));
-      mfma_one(j, 5 * g + 4);
-    }
 #pragma unroll
-    for (int i = 5 * kHalf; i < kMma; ++i) mfma_one(j, i);
+      for (int i = lo + 4; i < hi; ++i) mfma_one(j, i);
+    }
   };
   auto step = [&](auto kc, int c) {
     constexpr int K = decltype(kc)::value;
@@ -347,46 +350,55 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
       if (j0 + c >= T) continue;
       StatPart q = wpart[c];
       part_merge(q, wpart[BN + c], inv_temp);
-      StatPart* dst = part + static_cast<size_t>(j0 + c) * G + kGemmSlices * grp;
+      StatPart* dst = part + static_cast<size_t>(j0 + c) * G + kSlices * grp;
       dst[0] = q;
 #pragma unroll
-      for (int u = 1; u < kGemmSlices; ++u)
-        if (kGemmSlices * grp + u < G) dst[u] = empty;
+      for (int u = 1; u < kSlices; ++u)
+        if (kSlices * grp + u < G) dst[u] = empty;
     }
   }
 }
 
-template <int NST, bool STATS>
+template <int BM, int NST, bool STATS>
 int32_t launch_gemm(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
                     int G, float inv_temp, StatPart* part, hipStream_t s) {
-  const int groups = (G + kGemmSlices - 1) / kGemmSlices;
+  constexpr int kSlices = BM / 64;
+  const int groups = (G + kSlices - 1) / kSlices;
   const int passes = (T + kGemmBN - 1) / kGemmBN;
   const int blocks = (groups + 7) / 8 * passes * 8;
-  hipLaunchKernelGGL((lm_head_gemm_kernel<kGemmBN, NST, STATS>), dim3(blocks), dim3(kGemmThreads),
-                     0, s, X, W, logits, T, hid, V, G, inv_temp, part);
+  hipLaunchKernelGGL((lm_head_gemm_kernel<BM, kGemmBN, NST, STATS>), dim3(blocks),
+                     dim3(kGemmThreads), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
   return launch_status("verify_logits (tiled) launch");
+}
+
+template <int NST>
+int32_t launch_gemm_bm(bool wide, const uint16_t* X, const uint16_t* W, float* logits, int T,
+                       int hid, int V, int G, float inv_temp, StatPart* part, hipStream_t s) {
+  if (wide)
+    return part ? launch_gemm<256, NST, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
+                : launch_gemm<256, NST, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
+  return part ? launch_gemm<128, NST, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
+              : launch_gemm<128, NST, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
 }
 
 }  // namespace
 
 bool lm_gemm_takes(int T, int hid, int G, int cus) {
-  if ((hid != 64 * kGemmBK && hid != 80 * kGemmBK) || G % kGemmSlices != 0) return false;
-  // more than one streaming pass of 128 rows, or a vocabulary large enough
-  // for a block per CU (128256 entries: 501 blocks; 32000: 125, which
-  // leaves half the CUs idle while the streaming kernel keeps them all busy)
-  return T > kGemmMinRows || (T > kGemmMinRows / 2 && G / kGemmSlices >= cus);
+  if ((hid != 64 * kGemmBK && hid != 80 * kGemmBK) || G % 4 != 0) return false;
+  // more than one streaming pass of 128 rows, or more than 64 rows and a
+  // block per CU
+  return T > kGemmMinRows || (T > kGemmMinRows / 2 && G / 2 >= cus);
 }
 
 int32_t launch_lm_gemm(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, float* logits, int T,
-                       int hid, int V, int G, float inv_temp, void* partials, hipStream_t s) {
+                       int hid, int V, int G, float inv_temp, void* partials, int cus,
+                       hipStream_t s) {
   const auto* X = reinterpret_cast<const uint16_t*>(hidden);
   const auto* W = reinterpret_cast<const uint16_t*>(w_lm);
   auto* part = static_cast<StatPart*>(partials);
-  if (hid == 64 * kGemmBK)
-    return part ? launch_gemm<64, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
-                : launch_gemm<64, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
-  return part ? launch_gemm<80, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
-              : launch_gemm<80, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
+  const bool wide = G / 4 >= cus;   // 256-row blocks still give every CU one
+  if (hid == 64 * kGemmBK) return launch_gemm_bm<64>(wide, X, W, logits, T, hid, V, G, inv_temp, part, s);
+  return launch_gemm_bm<80>(wide, X, W, logits, T, hid, V, G, inv_temp, part, s);
 }
 
 }  // namespace entmtp

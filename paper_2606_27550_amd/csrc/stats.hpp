@@ -287,6 +287,7 @@ int32_t launch_partials_device_T(const entmtp_bf16* hidden, const entmtp_bf16* w
 // partial layout (G per row).
 bool lm_gemm_takes(int T, int hid, int G, int cus);
 int32_t launch_lm_gemm(const entmtp_bf16* hidden, const entmtp_bf16* w_lm, float* logits, int T,
-                       int hid, int V, int G, float inv_temp, void* partials, hipStream_t s);
+                       int hid, int V, int G, float inv_temp, void* partials, int cus,
+                       hipStream_t s);
 
 }  // namespace entmtp
