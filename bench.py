@@ -2,16 +2,20 @@
 """Tree-verification step benchmark on one MI355X.
 
 A step is one pass of the whole verification hot path at batch 1:
-  host: pick the tree for this step (the hysteretic ladder, tau_on 0.8,
-        tau_off 0.6, over the previous step's top-1 probability at the
-        deepest accepted node; a one-tree bank always picks its tree);
+  pick the tree for this step (the hysteretic ladder, tau_on 0.8, tau_off 0.6,
+        over the previous step's top-1 probability at the deepest accepted
+        node; a one-tree bank always picks its tree);
   GPU:  tree attention (tree K/V appended to the cache), LM-head logits with
-        fused softmax statistics -> greedy acceptance, and KV compaction, all
-        enqueued by one entmtp_step_launch (the compaction of a step goes out
-        with the next step's launch, on the cache stream, beside the next LM
-        head);
-  host: poll the pinned record acceptance publishes (accept length, s, path)
-        -- the step's one device-to-host read -- and move the prefix.
+        fused softmax statistics -> greedy acceptance, and KV compaction (the
+        compaction of a step goes out with the next step's launch, on the
+        cache stream, beside the next LM head).
+The ladder runs either on the GPU, in the acceptance kernel, which leaves the
+next step's tree and prefix in device memory (device-scheduled steps: the
+host enqueues step after step and reads nothing back), or on the host, which
+polls the pinned record acceptance publishes (accept length, s, path) -- the
+step's one device-to-host read -- moves the prefix and launches the next step
+(whose LM head it enqueued ahead, behind a gate).  The default workload runs
+device-scheduled and reports the host-scheduled loop beside it.
 The timed region ends with a flush, so it holds exactly K compactions.
 
 Default workload: Vicuna-7B shapes (32 x 128 heads, hidden 4096, vocabulary
@@ -79,9 +83,13 @@ def parse():
     ap.add_argument("--no-arm", action="store_true",
                     help="host-scheduled steps: launch each LM head only after the previous "
                          "result is read, instead of enqueueing it ahead behind a gate")
-    ap.add_argument("--gpu-scheduler", action="store_true",
-                    help="run the ladder on the GPU (no result read per step) instead of on "
-                         "the host; the same decisions (5-tree bank workload)")
+    ap.add_argument("--scheduler", choices=["auto", "gpu", "host"], default="auto",
+                    help="where the ladder runs: on the GPU (no result read per step, the next "
+                         "step's tree and prefix stay in device memory) or on the host (one "
+                         "record read per step); auto: the GPU for the 27-node workload, whose "
+                         "timed loop is then followed by a host-scheduled run reported beside "
+                         "it, the host for the others")
+    ap.add_argument("--gpu-scheduler", action="store_true", help="same as --scheduler gpu")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 256 MiB device copies (reference for HBM byte counters)")
     return ap.parse_args()
@@ -459,7 +467,10 @@ def main():
                     total_steps if grows else 0, device_prefix_fixed=not grows)
     wl, bank = run.wl, run.bank
     Hq, Hkv, d, hid, V, NL = run.Hq, run.Hkv, run.d, run.hid, run.V, run.NL
-    on_gpu = args.gpu_scheduler
+    sched = "gpu" if args.gpu_scheduler else args.scheduler
+    if sched == "auto":
+        sched = "gpu" if args.workload == "tree27_L256_7b" else "host"
+    on_gpu = sched == "gpu"
     fixed = args.fixed_topo >= 0
     policy = (lambda topo, s: args.fixed_topo) if fixed else ladder(lib, run.n_topo)
     K = args.steps
@@ -504,6 +515,20 @@ def main():
         f"T histogram {Tcount}; mean tokens/step {accept_mean:.3f}; switches {switches}; "
         f"final L {res['L_end']}; LM head us by T {lm_us_by_T}")
 
+    # the other scheduling mode on the same workload, same step count
+    other = None
+    if args.scheduler == "auto" and on_gpu and not args.graph:
+        gc.collect()
+        r2 = run.run(K, args.warmup, policy, grow=grows, start_rung=max(args.fixed_topo, 0),
+                     arm=not args.no_arm, arm_reach=not fixed, n_events=0, event_pass=0,
+                     on_gpu=False)
+        other = {"scheduler": "host (one result record read per step, next LM head armed)",
+                 "us_per_step": round(r2["elapsed"] / K * 1e6, 2),
+                 "steps_per_s": round(K / r2["elapsed"], 2),
+                 "hbm_frac": round(sum(step_bytes(T, L, a) for T, L, a, _, _ in r2["trace"])
+                                   / r2["elapsed"] / 1e9 / HBM_PEAK_GBPS, 4)}
+        log(f"host-scheduled: {other['us_per_step']} us/step")
+
     cpu = None
     if not args.no_cpu_baseline and NL == 1:
         cpu = cpu_baseline(args, run, [topo for *_, topo in trace])
@@ -535,7 +560,11 @@ def main():
                    "next_lm_head_armed": bool(not args.no_arm and not on_gpu),
                    "mean_tokens_per_step": round(accept_mean, 4), "topology_switches": switches,
                    "weight_copies": args.weight_copies, "parallelism": "single GPU"},
-        "roofline": {"kernel": "LM head with statistics partials (lm_head_pair_kernel up to 32 nodes, lm_head_hyb_kernel above)",
+        "roofline": {"kernel": ("LM head with statistics partials: "
+                                + ("lm_head_dyn_small_kernel (tree sized on the GPU) up to 32 nodes, "
+                                   "lm_head_dyn_large_kernel above" if on_gpu else
+                                   "lm_head_pair_kernel up to 32 nodes, lm_head_hyb_kernel up to 64, "
+                                   "lm_head_gemm_kernel above")),
                      "bound": "hbm", "achieved": round(lm_gbps, 1), "peak": HBM_PEAK_GBPS,
                      "unit": "GB/s", "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": round(lm_bytes / max(1, len(lm_T))),
@@ -548,6 +577,7 @@ def main():
                                "queued behind the previous step's publish kernel or a launch gate, "
                                "so that each pair brackets the kernel"},
         "cpu_baseline": cpu,
+        "other_scheduler": other,
         "switching": switching,
         "next_rows": extras,
     }
