@@ -142,8 +142,8 @@ size_t entmtp_tree_attn_workspace(int32_t T, int32_t Hq, int32_t Hkv, int32_t d,
  *            [0, prefix_len) hold the prefix (keys already rotated).
  *   out      [T][Hq][d] bf16.
  *   workspace  device scratch of at least entmtp_tree_attn_workspace() bytes;
- *            it holds the rotated queries and split partials of one call, so
- *            calls that share a workspace must be ordered, never concurrent.
+ *            it holds the split partials of one call, so calls that share a
+ *            workspace must be ordered, never concurrent.
  *
  * The call writes the tree's keys and values into cache slots
  * [prefix_len, prefix_len + T) and computes, for node i and query head h

@@ -90,7 +90,7 @@ __host__ __device__ inline int ladder_step(int rung, int n_rungs, float s, float
 // Grids of the attention for a tree chosen on the device: sized for the
 // largest plan any bank tree can need at prefix lengths up to cap - T.
 struct DevAttnShape {
-  int rows = 0, merge_blocks = 0, T_max = 0;
+  int rows = 0, merge_blocks = 0, T_max = 0, D_max = 0;
   int items[5] = {0, 0, 0, 0, 0};   // attend workgroups of the instance with 1 / 2 / 4 query tiles
   size_t need = 0;   // workspace bytes
 };

@@ -6,12 +6,14 @@
 // tree attends to the whole prefix and to the nodes on its own root-to-node
 // path; it sits at sequence position prefix_len + depth(i).
 //
-// Three kernels, all on the caller's stream:
-//  1. prep: rotate q and the tree's keys to their positions (fp64 angles,
-//     one bf16 rounding), write the tree's K/V into cache slots
-//     [L, L+T) and the rotated queries into the workspace, grouped per KV
-//     head (GQA: query rows = head-in-group x node).
-//  2. attend: flash-decoding over the cache, one of two kernels.
+// Two kernels, both on the caller's stream:
+//  1. attend: flash-decoding over the cache, one of two kernels.  The
+//     queries and the tree's keys are rotated to their positions as they are
+//     loaded (fp64 angles from a per-workgroup LDS table over the tree's
+//     depths, one bf16 rounding); the tree's keys and values come from the
+//     step's inputs rather than the cache, and the workgroups of the first
+//     query group write them (keys rotated) into cache slots [L, L+T) for
+//     the steps after this one.
 //     Trees of up to 32 query rows per KV head: a workgroup owns one (KV
 //     head, 32-query tile, key split); its four waves take interleaved 32-key
 //     blocks, each wave loading its next block while it multiplies the
@@ -30,9 +32,10 @@
 //     Online softmax in fp32, base 2, with a lazily raised running max (the
 //     accumulators are rescaled only when a block's max passes the reference
 //     by more than 2^8).
-//  3. merge: combines the splits' (max, sum, unnormalised output) partials.
+//  2. merge: combines the splits' (max, sum, unnormalised output) partials.
 //     Skipped when a single split covers the keys.
 #include <cfloat>
+#include <cmath>
 #include <mutex>
 
 #include "common.hpp"
@@ -110,10 +113,10 @@ struct SeqPlan {
   const uint32_t* mask;    // [T][ENTMTP_MASK_WORDS] its tree's ancestor bitmask
   const int* depth;        // [T]
   int T, L, row0;          // nodes, prefix length, first row in the concatenated q / out
+  int D;                   // depth of the tree's deepest node
   int rows_pad, nqt, nqg, nsplit, bps;   // padded rows, query tiles, query groups, splits
   int item0;               // first attend workgroup of the sequence
   int merge0;              // first merge block of the sequence
-  long long qrot_off;      // element offset of its rotated queries in the workspace
   long long part_off;      // row offset of its split partials
 };
 
@@ -130,15 +133,16 @@ struct BatchArgs {
   int nt;                  // query tiles per workgroup of the launched kernel (1 or 2)
   int B, G, Hq, Hkv, cap;
   float scale_log2;
-  double theta;
+  double theta;            // rotation base (0: no rotation)
+  double freq[HD / 2];     // theta^(-2c/d) of pair c, computed on the host
   const uint16_t* q;       // [rows][Hq][HD] (rows = sum of T, sequence after sequence)
   const uint16_t* kt;      // [rows][Hkv][HD]
   const uint16_t* vt;
-  uint16_t* qrot;          // workspace
   float* part_o;           // [part rows][HD]
   float* part_ml;          // [part rows][2]
   uint16_t* out;           // [rows][Hq][HD]
 };
+static_assert(sizeof(BatchArgs) <= 4096, "kernel arguments are limited to 4 KB");
 
 // Sequence that owns index `x` of a grid whose per-sequence ranges start at
 // `first(b)` (uniform per workgroup; at most kMaxSeqs steps).
@@ -159,6 +163,7 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
   const DevTopo* t = p.topos + st.rung;   // read in place (no local copy to index)
   q.T = st.T;
   q.L = st.L;
+  q.D = t->D;
   if (q.L < 0 || q.T < 1 || q.L + q.T > p.cap) {   // outside the cache: no attention at all
     q.T = 0;
     q.L = 0;
@@ -179,64 +184,108 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
   q.nsplit = (nblocks + q.bps - 1) / q.bps;
   q.item0 = 0;
   q.merge0 = 0;
-  q.qrot_off = 0;
   q.part_off = 0;
   return q;
 }
 
-// ------------------------------------------------------------------ prep --
+// ------------------------------------------------------------------ RoPE --
 
-__global__ __launch_bounds__(256) void attn_prep_kernel(BatchArgs p) {
-  // grid (sum of T, chunks): block (row, y) takes items [256 y, 256 y + 256)
-  // of its node's list: Hq*64 query pairs, then Hkv*64 key pairs, then
-  // Hkv*16 16-byte value chunks
-  constexpr int HALF = HD / 2;
-  const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.row0; });
-  const SeqPlan sq = resolve(p, b);
-  const int row = blockIdx.x;
-  const int i = row - sq.row0;
-  if (i >= sq.T) return;   // device-planned grids cover the largest tree
-  const int u = blockIdx.y * blockDim.x + threadIdx.x;
-  const int Hq = p.Hq, Hkv = p.Hkv, G = p.G, T = sq.T, L = sq.L, cap = p.cap;
-  const int nq = Hq * HALF, nk = Hkv * HALF, nv = Hkv * (HD / 8);
-  // the block's node sits at one position, so its HALF rotation angles are
-  // shared by every head: computed once per block
-  __shared__ double s_cos[HALF], s_sin[HALF];
-  if (p.theta > 0.0) {
-    if (threadIdx.x < HALF) {
-      // position prefix_len + depth(i), pair (c, c + d/2) turned by pos * theta^(-2c/d)
-      const int c = threadIdx.x;
-      const double pos = static_cast<double>(L) + static_cast<double>(sq.depth[i]);
-      const double ang = pos * pow(p.theta, -2.0 * c / HD);
-      sincos(ang, &s_sin[c], &s_cos[c]);
+// Angles of a tree's positions: tab[d * 64 + c] = (cos, sin) of the turn of
+// pair (c, c + 64) at position L + d, d = 0..D, in fp64 (pos * freq[c],
+// freq[c] = theta^(-2c/d) from the host), followed by the same table in
+// fp32 (for the queries), filled by the workgroup's threads (a multiple of
+// 64: each keeps one pair's frequency).  The tables live in the kernel's
+// dynamic LDS, sized by the host for the deepest tree of the launch.
+constexpr int kRopePairs = HD / 2;
+inline size_t rope_lds_bytes(int D, double theta) {
+  return theta > 0.0 ? static_cast<size_t>(D + 1) * kRopePairs * (sizeof(double2) + sizeof(float2)) : 0;
+}
+__device__ __forceinline__ const float2* rope_table_f32(const double2* tab, int D) {
+  return reinterpret_cast<const float2*>(tab + (D + 1) * kRopePairs);
+}
+inline void set_rope(BatchArgs& a, float rope_theta) {
+  a.theta = static_cast<double>(rope_theta);
+  for (int c = 0; c < kRopePairs; ++c) a.freq[c] = a.theta > 0.0 ? std::pow(a.theta, -2.0 * c / HD) : 0.0;
+}
+__device__ __forceinline__ void rope_table(double2* tab, int D, int L, const double* freq) {
+  const int c = threadIdx.x % kRopePairs;
+  const double f = freq[c];
+  for (int d = threadIdx.x / kRopePairs; d <= D; d += blockDim.x / kRopePairs) {
+    const double pos = static_cast<double>(L) + static_cast<double>(d);
+    double sn, cs;
+    sincos(pos * f, &sn, &cs);
+    tab[d * kRopePairs + c] = make_double2(cs, sn);
+    reinterpret_cast<float2*>(tab + (D + 1) * kRopePairs)[d * kRopePairs + c] =
+        make_float2(static_cast<float>(cs), static_cast<float>(sn));
+  }
+}
+
+// Turns the 8 pairs (c0 + e, c0 + e + 64), e < 8, whose halves lo / hi hold
+// (bf16), by the angles at t[c0 .. c0 + 7] (t = the position's table row):
+// lo cos - hi sin and hi cos + lo sin in fp64 (each product rounded, then
+// the sum: no fused multiply-add), each rounded to bf16 once.
+__device__ __forceinline__ void rope_pairs(u32x4& lo, u32x4& hi, const double2* t) {
+#pragma clang fp contract(off)
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t nl = 0u, nh = 0u;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const double2 a = t[2 * w + h];
+      const double x = bf16_to_f64(static_cast<uint16_t>(lo[w] >> (16 * h)));
+      const double y = bf16_to_f64(static_cast<uint16_t>(hi[w] >> (16 * h)));
+      nl |= f64_to_bf16_rne(x * a.x - y * a.y) << (16 * h);
+      nh |= f64_to_bf16_rne(y * a.x + x * a.y) << (16 * h);
     }
-    __syncthreads();
+    lo[w] = nl;
+    hi[w] = nh;
   }
-  if (u >= nq + nk + nv) return;
-  if (u >= nq + nk) {  // value copy -> cache slot L + i
-    const int w = u - nq - nk;
-    const int g = w / (HD / 8), c8 = w % (HD / 8);
-    *reinterpret_cast<u32x4*>(sq.vc + (static_cast<size_t>(g) * cap + L + i) * HD + 8 * c8) =
-        *reinterpret_cast<const u32x4*>(p.vt + (static_cast<size_t>(row) * Hkv + g) * HD + 8 * c8);
-    return;
+}
+
+// The same turn in fp32 with fp32 angles, rounded to bf16 by the hardware
+// (for the queries, which only enter bf16 products: the cache keeps the
+// fp64 form's keys).
+__device__ __forceinline__ void rope_pairs_f32(u32x4& lo, u32x4& hi, const float2* t) {
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    const float2 a0 = t[2 * w], a1 = t[2 * w + 1];
+    const float x0 = bf16_lo(lo[w]), x1 = bf16_hi(lo[w]);
+    const float y0 = bf16_lo(hi[w]), y1 = bf16_hi(hi[w]);
+    lo[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+                                             (f32x2{x0 * a0.x - y0 * a0.y, x1 * a1.x - y1 * a1.y}), bf16x2));
+    hi[w] = __builtin_bit_cast(uint32_t, __builtin_convertvector(
+                                             (f32x2{y0 * a0.x + x0 * a0.y, y1 * a1.x + x1 * a1.y}), bf16x2));
   }
-  const bool is_q = u < nq;
-  const int w = is_q ? u : u - nq;
-  const int head = w / HALF, c = w % HALF;
-  const uint16_t* src = (is_q ? p.q + (static_cast<size_t>(row) * Hq + head) * HD
-                              : p.kt + (static_cast<size_t>(row) * Hkv + head) * HD);
-  uint16_t* dst = is_q ? p.qrot + sq.qrot_off +
-                             (static_cast<size_t>(head / G) * sq.rows_pad + (head % G) * T + i) * HD
-                       : sq.kc + (static_cast<size_t>(head) * cap + L + i) * HD;
-  if (p.theta > 0.0) {
-    const double sn = s_sin[c], cs = s_cos[c];
-    const double lo = bf16_to_f64(src[c]), hi = bf16_to_f64(src[c + HALF]);
-    dst[c] = static_cast<uint16_t>(f64_to_bf16_rne(lo * cs - hi * sn));
-    dst[c + HALF] = static_cast<uint16_t>(f64_to_bf16_rne(hi * cs + lo * sn));
-  } else {
-    dst[c] = src[c];
-    dst[c + HALF] = src[c + HALF];
+}
+
+// One half of a pair whose other half sits in lane ^ 8 (a key row loaded as
+// 16 lanes x 16 bytes: chunk m holds dims 8m .. 8m + 7): the rotated chunk,
+// only this lane's half computed -- mine cos - other sin for the first half,
+// mine cos + other sin for the second (the same rounded steps as
+// rope_pairs).  Every lane must call it (shuffles); `on` selects the lanes
+// that rotate.
+__device__ __forceinline__ u32x4 rope_half(const u32x4& mine, int m, bool on, const double2* t) {
+#pragma clang fp contract(off)
+  u32x4 other;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) other[w] = static_cast<uint32_t>(__shfl_xor(static_cast<int>(mine[w]), 8, 64));
+  if (!on) return mine;
+  const double2* a = t + 8 * (m & 7);
+  u32x4 out;
+#pragma unroll
+  for (int w = 0; w < 4; ++w) {
+    uint32_t r = 0u;
+#pragma unroll
+    for (int h = 0; h < 2; ++h) {
+      const double2 cs = a[2 * w + h];
+      const double x = bf16_to_f64(static_cast<uint16_t>(mine[w] >> (16 * h)));
+      const double y = bf16_to_f64(static_cast<uint16_t>(other[w] >> (16 * h)));
+      const double sn = m < 8 ? -cs.y : cs.y;
+      r |= f64_to_bf16_rne(x * cs.x + y * sn) << (16 * h);
+    }
+    out[w] = r;
   }
+  return out;
 }
 
 // ---------------------------------------------------------------- attend --
@@ -286,6 +335,7 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   __shared__ float s_m[kAttnWaves][QR], s_l[kAttnWaves][QR];
   __shared__ float s_sc[kAttnWaves][QR];   // each wave's factor to the common max
   __shared__ float s_M[QR], s_L[QR];        // a row's common max and sum
+  extern __shared__ __attribute__((aligned(16))) double2 s_rope[];   // angles of the tree's positions
   u32x4 (*s_qf)[8][64] = reinterpret_cast<u32x4 (*)[8][64]>(lds);   // [NT][s][lane]
   uint32_t* vt = reinterpret_cast<uint32_t*>(lds + kQfBytes + wave * kVtBytes);  // [HD][VT_LD/2]
 
@@ -297,13 +347,23 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   const int blk_lo = split * sq.bps;
   const int blk_hi = min(nblocks, blk_lo + sq.bps);
 
-  // K/V of one block into registers.  Keys past the end are clamped to the
-  // last key (finite data whose probabilities are zero), so every load is
-  // unconditional and the compiler's wait counts stay exact.
+  // K/V of one block into registers: prefix keys from the cache, the tree's
+  // keys (slots L and up, not yet rotated) and values from the step's
+  // inputs.  Keys past the end are clamped to the last key (finite data
+  // whose probabilities are zero), so every load is unconditional and the
+  // compiler's wait counts stay exact.
+  auto krow = [&](int key) {
+    return key < L ? kbase + static_cast<size_t>(key) * HD
+                   : p.kt + (static_cast<size_t>(sq.row0 + key - L) * p.Hkv + g) * HD;
+  };
+  auto vrow = [&](int key) {
+    return key < L ? vbase + static_cast<size_t>(key) * HD
+                   : p.vt + (static_cast<size_t>(sq.row0 + key - L) * p.Hkv + g) * HD;
+  };
   auto load_k = [&](int blk, u32x4 (&kf)[8]) {
     const int kb = blk * KB;
     const int key = min(kb + li, nkeys - 1);
-    const uint16_t* kp = kbase + static_cast<size_t>(key) * HD + 8 * lh;
+    const uint16_t* kp = krow(key) + 8 * lh;
 #pragma unroll
     for (int s = 0; s < 8; ++s) kf[s] = *reinterpret_cast<const u32x4*>(kp + 16 * s);
   };
@@ -316,10 +376,15 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
       const int u = lane + 64 * k;
       const int pp = u & 15, m = u >> 4;
       const int k0 = min(kb + 2 * pp, last), k1 = min(kb + 2 * pp + 1, last);
-      va[k] = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k0) * HD + 8 * m);
-      vb[k] = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k1) * HD + 8 * m);
+      va[k] = *reinterpret_cast<const u32x4*>(vrow(k0) + 8 * m);
+      vb[k] = *reinterpret_cast<const u32x4*>(vrow(k1) + 8 * m);
     }
   };
+  // the first query group's workgroups keep the tree's keys and values in
+  // the cache (slots L .. L + T - 1) for the steps after this one
+  const bool keeper = qg == 0;
+  uint16_t* const kc_head = sq.kc + head_off;
+  uint16_t* const vc_head = sq.vc + head_off;
 
   // the wave's first block is requested before the prologue, so its latency
   // overlaps the staging of the queries
@@ -331,22 +396,40 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     load_v(cur, v0, v1);
   }
 
+  // Q^T B-operand fragments, the same for the four waves (they split keys,
+  // not queries), staged once in LDS: lane (query li, half lh) of tile t
+  // reads d = 16s + 8lh + e from slot [t][s][lane].  Query row r of KV head
+  // g is (head g * G + r / T, node r % T); thread (s, ln) loads chunks s and
+  // s + 4 of its row (the two halves of pairs 16s + 8lh + e), requested
+  // here and rotated once the angle table is built.
+  static_assert(NT * 4 * 64 == kAttnThreads, "one thread per pair of Q chunks");
+  const int qs = (tid >> 6) & 3, qhl = (tid >> 5) & 1;
+  const int qrow = qt0 * kQTile + li;
+  const bool qlive = qrow < GT;
+  u32x4 qlo{0u, 0u, 0u, 0u}, qhi{0u, 0u, 0u, 0u};
+  int qdepth = 0;
+  if (qlive) {
+    const int node = qrow % T;
+    const uint16_t* qp = p.q + (static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + qrow / T) * HD +
+                         8 * qhl + 16 * qs;
+    qlo = *reinterpret_cast<const u32x4*>(qp);
+    qhi = *reinterpret_cast<const u32x4*>(qp + HD / 2);
+    qdepth = sq.depth[node];
+  }
   // ancestor masks of the group's query rows (padding rows see every key)
   for (int u = tid; u < QR * ENTMTP_MASK_WORDS; u += kAttnThreads) {
     const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
-    const int qrow = qt0 * kQTile + r;
-    s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+    const int mrow = qt0 * kQTile + r;
+    s_mask[r][w] = mrow < GT ? sq.mask[(mrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
   }
-  // Q^T B-operand fragments, the same for the four waves (they split keys,
-  // not queries), staged once in LDS: lane (query li, half lh) of tile t
-  // reads d = 16s + 8lh + e from slot [t][s][lane]
-  for (int x = tid; x < NT * 8 * 64; x += kAttnThreads) {
-    const int t = x >> 9, s = (x >> 6) & 7, ln = x & 63;
-    const int qrow = (qt0 + t) * kQTile + (ln & 31);
-    const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD +
-                         8 * (ln >> 5) + 16 * s;
-    s_qf[t][s][ln] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp) : u32x4{0u, 0u, 0u, 0u};
+  const bool rope = p.theta > 0.0;
+  if (rope) {
+    rope_table(s_rope, sq.D, L, p.freq);
+    __syncthreads();
+    if (qlive) rope_pairs_f32(qlo, qhi, rope_table_f32(s_rope, sq.D) + qdepth * kRopePairs + 16 * qs + 8 * qhl);
   }
+  s_qf[0][qs][lane] = qlo;
+  s_qf[0][qs + 4][lane] = qhi;
   __syncthreads();
 
   // running (max, sum) per query in base-2 scaled units and the output
@@ -367,8 +450,19 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   }
 
   // a block's V into this wave's V^T tile: word (dim, key pair) packs the
-  // pair's two bf16 values of that dim
-  auto stage_v = [&](const u32x4 (&va)[4], const u32x4 (&vb)[4]) {
+  // pair's two bf16 values of that dim (and the tree's values into the cache)
+  auto stage_v = [&](int blk, const u32x4 (&va)[4], const u32x4 (&vb)[4]) {
+    if (keeper && blk * KB + KB > L) {
+      const int kb = blk * KB;
+#pragma unroll
+      for (int k = 0; k < 4; ++k) {
+        const int u = lane + 64 * k;
+        const int pp = u & 15, m = u >> 4;
+        const int k0 = kb + 2 * pp, k1 = k0 + 1;
+        if (k0 >= L && k0 < nkeys) *reinterpret_cast<u32x4*>(vc_head + static_cast<size_t>(k0) * HD + 8 * m) = va[k];
+        if (k1 >= L && k1 < nkeys) *reinterpret_cast<u32x4*>(vc_head + static_cast<size_t>(k1) * HD + 8 * m) = vb[k];
+      }
+    }
     wave_lds_sync();  // previous block's V^T reads are done
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
@@ -455,9 +549,24 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
 
   // the block's scores, softmax and P V for the group's tiles (V from the
   // staged tile, each V^T fragment read once for all tiles)
-  auto attend = [&](int blk, const u32x4 (&kf)[8]) {
+  auto attend = [&](int blk, u32x4 (&kf)[8]) {
     const int kb = blk * KB;
     const bool plain = kb + KB <= L;
+    if (!plain) {   // the tree's keys: rotate, and keep them in the cache
+      const int key = min(kb + li, nkeys - 1);
+      if (key >= L) {
+        if (rope) {
+          const double2* tr = s_rope + sq.depth[key - L] * kRopePairs + 8 * lh;
+#pragma unroll
+          for (int s = 0; s < 4; ++s) rope_pairs(kf[s], kf[s + 4], tr + 16 * s);
+        }
+        if (keeper && kb + li < nkeys) {
+#pragma unroll
+          for (int s = 0; s < 8; ++s)
+            *reinterpret_cast<u32x4*>(kc_head + static_cast<size_t>(key) * HD + 8 * lh + 16 * s) = kf[s];
+        }
+      }
+    }
     f32x16 sacc[NT];
     bf16x8 pf[NT][2];
 #pragma unroll
@@ -500,14 +609,14 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
       const int nb = cur + kAttnWaves;
       const int nbc = nb < blk_hi ? nb : cur;
       load_k(nbc, kB);
-      stage_v(v0, v1);
+      stage_v(cur, v0, v1);
       load_v(nbc, v0, v1);
       attend(cur, kA);
       if (nb >= blk_hi) break;
       const int nb2 = nb + kAttnWaves;
       const int nb2c = nb2 < blk_hi ? nb2 : nb;
       load_k(nb2c, kA);
-      stage_v(v0, v1);
+      stage_v(nb, v0, v1);
       load_v(nb2c, v0, v1);
       attend(nb, kB);
       if (nb2 >= blk_hi) break;
@@ -636,16 +745,32 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
   __shared__ __attribute__((aligned(16))) uint16_t s_k[2][KB][KROW];
   __shared__ __attribute__((aligned(16))) uint32_t s_vt[2][HD * (VT_LD / 2)];
   __shared__ uint32_t s_mask[QR][ENTMTP_MASK_WORDS + 1];
+  extern __shared__ __attribute__((aligned(16))) double2 s_rope[];   // angles of the tree's positions
 
   const size_t head_off = static_cast<size_t>(g) * p.cap * HD;
-  const uint16_t* kbase = sq.kc + head_off;
-  const uint16_t* vbase = sq.vc + head_off;
+  uint16_t* const kc_head = sq.kc + head_off;
+  uint16_t* const vc_head = sq.vc + head_off;
+  const uint16_t* kbase = kc_head;
+  const uint16_t* vbase = vc_head;
   const float c = p.scale_log2;
   const int nblocks = (nkeys + KB - 1) / KB;
   const int blk_lo = split * sq.bps;
   const int blk_hi = min(nblocks, blk_lo + sq.bps);
   const int nb = blk_hi - blk_lo;
+  const bool rope = p.theta > 0.0;
+  // the first query group's workgroups keep the tree's keys (rotated) and
+  // values in the cache (slots L .. L + T - 1) for the steps after this one
+  const bool keeper = qg == 0;
 
+  // prefix keys from the cache, the tree's keys and values from the inputs
+  auto krow = [&](int key) {
+    return key < L ? kbase + static_cast<size_t>(key) * HD
+                   : p.kt + (static_cast<size_t>(sq.row0 + key - L) * p.Hkv + g) * HD;
+  };
+  auto vrow = [&](int key) {
+    return key < L ? vbase + static_cast<size_t>(key) * HD
+                   : p.vt + (static_cast<size_t>(sq.row0 + key - L) * p.Hkv + g) * HD;
+  };
   // cooperative loads of one block: K unit u = tid + 256 j -> key u / 16,
   // 16-byte chunk u % 16; V unit tid -> key pair tid / 16, 8-dim chunk
   // tid % 16 (both keys of the pair).  Keys past the end clamp to the last.
@@ -656,14 +781,37 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
     for (int j = 0; j < 2; ++j) {
       const int u = tid + kAttnThreads * j;
       const int key = min(kb + (u >> 4), last);
-      kr[j] = *reinterpret_cast<const u32x4*>(kbase + static_cast<size_t>(key) * HD + 8 * (u & 15));
+      kr[j] = *reinterpret_cast<const u32x4*>(krow(key) + 8 * (u & 15));
     }
     const int m = tid & 15, pp = tid >> 4;
     const int k0 = min(kb + 2 * pp, last), k1 = min(kb + 2 * pp + 1, last);
-    va = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k0) * HD + 8 * m);
-    vb = *reinterpret_cast<const u32x4*>(vbase + static_cast<size_t>(k1) * HD + 8 * m);
+    va = *reinterpret_cast<const u32x4*>(vrow(k0) + 8 * m);
+    vb = *reinterpret_cast<const u32x4*>(vrow(k1) + 8 * m);
   };
-  auto stage = [&](int buf, const u32x4 (&kr)[2], const u32x4& va, const u32x4& vb) {
+  // block i's registers into LDS buffer buf; a block that holds tree keys
+  // rotates them first (the pair's other half sits in lane ^ 8) and the
+  // keeper writes them and their values to the cache
+  auto stage = [&](int buf, int i, u32x4 (&kr)[2], const u32x4& va, const u32x4& vb) {
+    const int kb = (blk_lo + min(i, nb - 1)) * KB;
+    if (kb + KB > L) {
+#pragma unroll
+      for (int j = 0; j < 2; ++j) {
+        const int u = tid + kAttnThreads * j;
+        const int key = kb + (u >> 4);
+        const int kk = min(key, nkeys - 1);
+        if (rope)
+          kr[j] = rope_half(kr[j], u & 15, kk >= L, s_rope + sq.depth[max(kk - L, 0)] * kRopePairs);
+        if (keeper && key >= L && key < nkeys)
+          *reinterpret_cast<u32x4*>(kc_head + static_cast<size_t>(key) * HD +
+                                    8 * (u & 15)) = kr[j];
+      }
+      const int m = tid & 15, pp = tid >> 4;
+      const int k0 = kb + 2 * pp, k1 = k0 + 1;
+      if (keeper && k0 >= L && k0 < nkeys)
+        *reinterpret_cast<u32x4*>(vc_head + static_cast<size_t>(k0) * HD + 8 * m) = va;
+      if (keeper && k1 >= L && k1 < nkeys)
+        *reinterpret_cast<u32x4*>(vc_head + static_cast<size_t>(k1) * HD + 8 * m) = vb;
+    }
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
       const int u = tid + kAttnThreads * j;
@@ -682,21 +830,38 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
   gload(0, kA, vaA, vbA);
   gload(1, kB, vaB, vbB);
 
-  // ancestor masks of the group's rows, and this wave's Q fragments
+  // this wave's Q fragments: query row r of KV head g is (head g * G + r / T,
+  // node r % T); chunks s and s + 4 hold the two halves of pairs
+  // 16s + 8lh + e, rotated once the angle table is built
+  u32x4 qf[8];
+  const int qrow = qt * kQTile + li;
+  const bool qlive = qrow < GT;
+  int qdepth = 0;
+#pragma unroll
+  for (int s = 0; s < 8; ++s) qf[s] = u32x4{0u, 0u, 0u, 0u};
+  if (qlive) {
+    const int node = qrow % T;
+    const uint16_t* qp = p.q + (static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + qrow / T) * HD + 8 * lh;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s);
+    qdepth = sq.depth[node];
+  }
+  // ancestor masks of the group's rows
   for (int u = tid; u < QR * ENTMTP_MASK_WORDS; u += kAttnThreads) {
     const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
-    const int qrow = qg * QR + r;
-    s_mask[r][w] = qrow < GT ? sq.mask[(qrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+    const int mrow = qg * QR + r;
+    s_mask[r][w] = mrow < GT ? sq.mask[(mrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
   }
-  u32x4 qf[8];
-  {
-    const int qrow = qt * kQTile + li;
-    const uint16_t* qp = p.qrot + sq.qrot_off + (static_cast<size_t>(g) * rows_pad + qrow) * HD + 8 * lh;
+  if (rope) {
+    rope_table(s_rope, sq.D, L, p.freq);
+    __syncthreads();
+    if (qlive) {
+      const float2* tr = rope_table_f32(s_rope, sq.D) + qdepth * kRopePairs + 8 * lh;
 #pragma unroll
-    for (int s = 0; s < 8; ++s)
-      qf[s] = qrow < GT ? *reinterpret_cast<const u32x4*>(qp + 16 * s) : u32x4{0u, 0u, 0u, 0u};
+      for (int s = 0; s < 4; ++s) rope_pairs_f32(qf[s], qf[s + 4], tr + 16 * s);
+    }
   }
-  stage(0, kA, vaA, vbA);
+  stage(0, 0, kA, vaA, vbA);
   gload(2, kA, vaA, vbA);
   __syncthreads();
 
@@ -798,12 +963,12 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
   for (int i = 0;; i += 2) {
     compute(i, 0);
     if (i + 1 >= nb) break;
-    stage(1, kB, vaB, vbB);
+    stage(1, i + 1, kB, vaB, vbB);
     gload(i + 3, kB, vaB, vbB);
     __syncthreads();
     compute(i + 1, 1);
     if (i + 2 >= nb) break;
-    stage(0, kA, vaA, vbA);
+    stage(0, i + 2, kA, vaA, vbA);
     gload(i + 4, kA, vaA, vbA);
     __syncthreads();
   }
@@ -907,11 +1072,12 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
-void launch_attend(const BatchArgs& a, int items, hipStream_t s) {
+// lds: bytes of the rotation table (rope_lds_bytes of the deepest tree)
+void launch_attend(const BatchArgs& a, int items, size_t lds, hipStream_t s) {
   if (a.nt == 4)
-    hipLaunchKernelGGL(tree_attn_q4_kernel, dim3(items), dim3(kAttnThreads), 0, s, a);
+    hipLaunchKernelGGL(tree_attn_q4_kernel, dim3(items), dim3(kAttnThreads), lds, s, a);
   else
-    hipLaunchKernelGGL(tree_attn_kernel, dim3(items), dim3(kAttnThreads), 0, s, a);
+    hipLaunchKernelGGL(tree_attn_kernel, dim3(items), dim3(kAttnThreads), lds, s, a);
 }
 
 
@@ -930,7 +1096,8 @@ int device_cus() {
 
 // Grid sizes of one call.
 struct CallShape {
-  int rows = 0;          // concatenated tree rows (prep grid)
+  int rows = 0;          // concatenated tree rows
+  int D = 0;             // depth of the deepest tree
   int items = 0;         // attend workgroups
   int merge_blocks = 0;  // merge blocks
   size_t need = 0;       // workspace bytes
@@ -939,7 +1106,7 @@ struct CallShape {
 // Plans the sequences of one call: per-sequence split counts (a lone
 // sequence fills the CUs by itself; a batch shares one blocks-per-split
 // target sized to about four workgroups per CU), grid ranges and the packed
-// workspace layout (rotated queries, output partials, (max, sum) partials).
+// workspace layout (output partials, then (max, sum) partials).
 CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const int32_t* L,
                     entmtp_bf16* const* kc, entmtp_bf16* const* vc, int cap, int Hq, int Hkv,
                     BatchArgs& a) {
@@ -967,7 +1134,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
   const int target_bps = static_cast<int>(per_wg > kMinBlocksPerSplit ? per_wg : kMinBlocksPerSplit);
 
   CallShape sh;
-  long long qrot = 0, part_rows = 0;
+  long long part_rows = 0;
   for (int b = 0; b < B; ++b) {
     const TopoDesc& td = bank->desc[topo[b]];
     SeqPlan& q = a.s[b];
@@ -976,6 +1143,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     q.mask = bank_ptr<uint32_t>(bank, td.off_mask);
     q.depth = bank_ptr<int>(bank, td.off_depth);
     q.T = td.T;
+    q.D = td.D;
     q.L = L[b];
     q.row0 = sh.rows;
     q.rows_pad = rows_padded(a.G, q.T);
@@ -994,40 +1162,32 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     q.nsplit = (nblocks + q.bps - 1) / q.bps;
     q.item0 = sh.items;
     q.merge0 = sh.merge_blocks;
-    q.qrot_off = qrot;
     q.part_off = part_rows;
     sh.rows += q.T;
+    sh.D = q.D > sh.D ? q.D : sh.D;
     sh.items += (Hkv * q.nsplit + 7) / 8 * 8 * q.nqg;
     if (q.nsplit > 1) {
       sh.merge_blocks += (Hkv * a.G * q.T + kMergeRows - 1) / kMergeRows;
       part_rows += static_cast<long long>(q.nsplit) * Hkv * q.rows_pad;
     }
-    qrot += static_cast<long long>(Hkv) * q.rows_pad * HD;
   }
-  const size_t qb = static_cast<size_t>(qrot) * 2;
   const size_t po = static_cast<size_t>(part_rows) * HD * 4;
   const size_t pml = static_cast<size_t>(part_rows) * 2 * 4;
-  sh.need = al256(qb) + al256(po) + al256(pml);
+  sh.need = al256(po) + al256(pml);
   return sh;
 }
 
-// Points the planned call at its workspace and launches prep, attend and
-// (when some sequence has several splits) merge.
+// Points the planned call at its workspace and launches attend and (when
+// some sequence has several splits) merge.
 int32_t launch_call(BatchArgs& a, const CallShape& sh, void* workspace, hipStream_t s) {
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  long long qrot = 0, part_rows = 0;
-  for (int b = 0; b < a.B; ++b) {
-    qrot += static_cast<long long>(a.Hkv) * a.s[b].rows_pad * HD;
+  long long part_rows = 0;
+  for (int b = 0; b < a.B; ++b)
     if (a.s[b].nsplit > 1) part_rows += static_cast<long long>(a.s[b].nsplit) * a.Hkv * a.s[b].rows_pad;
-  }
-  const size_t qb = static_cast<size_t>(qrot) * 2, po = static_cast<size_t>(part_rows) * HD * 4;
-  a.qrot = reinterpret_cast<uint16_t*>(ws);
-  a.part_o = reinterpret_cast<float*>(ws + al256(qb));
-  a.part_ml = reinterpret_cast<float*>(ws + al256(qb) + al256(po));
-  const int prep_items = (a.Hq + a.Hkv) * (HD / 2) + a.Hkv * (HD / 8);
-  hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
-  if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
-  launch_attend(a, sh.items, s);
+  const size_t po = static_cast<size_t>(part_rows) * HD * 4;
+  a.part_o = reinterpret_cast<float*>(ws);
+  a.part_ml = reinterpret_cast<float*>(ws + al256(po));
+  launch_attend(a, sh.items, rope_lds_bytes(sh.D, a.theta), s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
   if (sh.merge_blocks > 0) {
     hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
@@ -1043,8 +1203,7 @@ size_t workspace_bytes(int T, int Hq, int Hkv, int L) {
   const int rows_pad = rows_padded(G, T);
   const int nblocks = (L + T + KB - 1) / KB;
   const size_t bound = split_bound(nblocks);
-  return al256(static_cast<size_t>(Hkv) * rows_pad * HD * 2) +
-         al256(bound * Hkv * rows_pad * HD * 4) + al256(bound * Hkv * rows_pad * 2 * 4);
+  return al256(bound * Hkv * rows_pad * HD * 4) + al256(bound * Hkv * rows_pad * 2 * 4);
 }
 
 // Checks shared by the single and batched entry points.
@@ -1088,6 +1247,7 @@ int32_t attn_device_shape(const entmtp_bank* bank, int Hq, int Hkv, int cap, Dev
   DevAttnShape sh;
   for (const TopoDesc& td : bank->desc) {
     sh.T_max = td.T > sh.T_max ? td.T : sh.T_max;
+    sh.D_max = td.D > sh.D_max ? td.D : sh.D_max;
     const int nt = tree_tiles(G, td.T);
     const int nqg = query_groups(rows_padded(G, td.T) / kQTile, nt);
     const int max_blocks = (cap + KB - 1) / KB;
@@ -1136,7 +1296,7 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   a.s[0].kc = k_cache;
   a.s[0].vc = v_cache;
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.theta = static_cast<double>(rope_theta);
+  set_rope(a, rope_theta);
   a.q = q;
   a.kt = k_tree;
   a.vt = v_tree;
@@ -1144,21 +1304,16 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   // the workspace regions at the bounds workspace_bytes() sizes them with
   const int rows_pad = rows_padded(a.G, sh.T_max);
   const size_t bound = split_bound((cap + sh.T_max + KB - 1) / KB);
-  const size_t qb = static_cast<size_t>(Hkv) * rows_pad * HD * 2;
   const size_t po = bound * Hkv * rows_pad * HD * 4;
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  a.qrot = reinterpret_cast<uint16_t*>(ws);
-  a.part_o = reinterpret_cast<float*>(ws + al256(qb));
-  a.part_ml = reinterpret_cast<float*>(ws + al256(qb) + al256(po));
-  const int prep_items = (Hq + Hkv) * (HD / 2) + Hkv * (HD / 8);
-  hipLaunchKernelGGL(attn_prep_kernel, dim3(sh.rows, (prep_items + 255) / 256), dim3(256), 0, s, a);
-  if (int32_t rc = launch_status("tree_attn prep launch")) return rc;
+  a.part_o = reinterpret_cast<float*>(ws);
+  a.part_ml = reinterpret_cast<float*>(ws + al256(po));
   // one instance per tile count among the bank's trees; those not made for
   // the device's tree leave at once
   for (int nt = 1; nt <= 4; nt *= 2) {
     if (sh.items[nt] == 0) continue;
     a.nt = nt;
-    launch_attend(a, sh.items[nt], s);
+    launch_attend(a, sh.items[nt], rope_lds_bytes(sh.D_max, a.theta), s);
     if (int32_t rc = launch_status("tree_attn launch")) return rc;
   }
   hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
@@ -1235,7 +1390,7 @@ extern "C" int32_t entmtp_tree_attn(const entmtp_bank* bank, int32_t topo, const
   BatchArgs a;
   const CallShape sh = plan_call(bank, 1, &topo, &prefix_len, &k_cache, &v_cache, cap, Hq, Hkv, a);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.theta = static_cast<double>(rope_theta);
+  set_rope(a, rope_theta);
   a.q = q;
   a.kt = k_tree;
   a.vt = v_tree;
@@ -1266,7 +1421,7 @@ extern "C" int32_t entmtp_tree_attn_noalloc(const entmtp_bank* bank, int32_t top
   BatchArgs a;
   const CallShape sh = plan_call(bank, 1, &topo, &prefix_len, &k_cache, &v_cache, cap, Hq, Hkv, a);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.theta = static_cast<double>(rope_theta);
+  set_rope(a, rope_theta);
   a.q = q;
   a.kt = k_tree;
   a.vt = v_tree;
@@ -1295,7 +1450,7 @@ extern "C" int32_t entmtp_tree_attn_batched(
   ENTMTP_CHECK_ARG(ws_bytes >= sh.need, ENTMTP_ENOSPC, "workspace has %zu bytes, needs %zu",
                    ws_bytes, sh.need);
   a.scale_log2 = scale * 1.4426950408889634f;
-  a.theta = static_cast<double>(rope_theta);
+  set_rope(a, rope_theta);
   a.q = q;
   a.kt = k_tree;
   a.vt = v_tree;

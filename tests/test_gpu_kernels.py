@@ -335,7 +335,9 @@ def check_attn(api, parent, T, L, Hq, Hkv, theta, wl=50, cap_extra=5, layer=0):
     # four-tile kernel with idle waves: 2 tiles (40 nodes; 20 nodes x 2 heads
     # per KV head) and 3 tiles (80 nodes)
     ("random", 40, 300, 4, 4, 10000.0), ("random", 20, 777, 4, 2, 10000.0),
-    ("random", 80, 1500, 8, 8, 10000.0)])
+    ("random", 80, 1500, 8, 8, 10000.0),
+    # the deepest tree in the four-tile kernel (32 levels of angles in LDS)
+    ("chain", 32, 50, 8, 2, 10000.0)])
 def test_tree_attn_small(api, kind, T, L, Hq, Hkv, theta):
     say("tree_attn", kind, T, L, Hq, Hkv, theta)
     if kind == "single":
