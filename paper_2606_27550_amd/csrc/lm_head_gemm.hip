@@ -312,7 +312,14 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   }
   if constexpr (STATS) {
     // per row: the wave's partial over its 128 vocabulary rows (lane, then
-    // the four lane groups), then the two waves of a row in LDS
+    // the four lane groups), then the two waves of a row in LDS.  A lane
+    // visits its rows in increasing order, so within the lane a strictly
+    // larger value is the only update the lowest-index rule needs.  The
+    // sums run in base 2 (one hardware exponential per logit): with
+    // y2 = log2(e) (inv_temp z - my), Z = sum 2^y2 and S = ln 2 sum y2 2^y2.
+    constexpr float kLog2e = 1.44269504088896341f, kLn2 = 0.69314718055994531f;
+    const float it2 = inv_temp * kLog2e;
+    const bool full = r1 - r0 == BM;   // every row of the block is a vocabulary row
     StatPart* wpart = reinterpret_cast<StatPart*>(ring);   // [2][BN]
 #pragma unroll
     for (int ni = 0; ni < Sh::NI; ++ni) {
@@ -321,24 +328,32 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
 #pragma unroll
       for (int mi = 0; mi < Sh::MI; ++mi)
 #pragma unroll
-        for (int r = 0; r < 4; ++r)
-          if (vbase + 16 * mi + r < r1) take_max(p.zmax, p.idx, acc[mi][ni][r], vbase + 16 * mi + r);
+        for (int r = 0; r < 4; ++r) {
+          const int v = vbase + 16 * mi + r;
+          if ((full || v < r1) && acc[mi][ni][r] > p.zmax) {
+            p.zmax = acc[mi][ni][r];
+            p.idx = v;
+          }
+        }
 #pragma unroll
       for (int off = 16; off <= 32; off <<= 1)
         take_max(p.zmax, p.idx, __shfl_xor(p.zmax, off, 64), __shfl_xor(p.idx, off, 64));
       if (p.zmax != -INFINITY) {
-        const float my = p.zmax * inv_temp;
+        const float my2 = p.zmax * it2;
+        float Z = 0.f, S2 = 0.f;
 #pragma unroll
         for (int mi = 0; mi < Sh::MI; ++mi)
 #pragma unroll
           for (int r = 0; r < 4; ++r) {
-            if (vbase + 16 * mi + r < r1) {
-              const float y = acc[mi][ni][r] * inv_temp - my;
-              const float e = expf(y);
-              p.Z += e;
-              if (e > 0.f) p.S += y * e;
+            if (full || vbase + 16 * mi + r < r1) {
+              const float y2 = fmaf(acc[mi][ni][r], it2, -my2);
+              const float e = __builtin_amdgcn_exp2f(y2);
+              Z += e;
+              S2 = fmaf(y2, e, S2);
             }
           }
+        p.Z = Z;
+        p.S = S2 * kLn2;
       }
 #pragma unroll
       for (int off = 16; off <= 32; off <<= 1) {
