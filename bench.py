@@ -532,7 +532,7 @@ def main():
     cpu = None
     if not args.no_cpu_baseline and NL == 1:
         cpu = cpu_baseline(args, run, [topo for *_, topo in trace])
-    traffic = lm_head_traffic(res["lm_rows"] or [T for T, *_ in trace])
+    traffic = lm_head_traffic(res["lm_rows"] or [T for T, *_ in trace], on_gpu)
     extras, switching = None, None
     if not args.no_extras:
         extras = next_rows(api, synth, run.W[0], run.pool, hid, V, run.dev)
@@ -893,10 +893,11 @@ def next_rows(api, synth, W, pool, hid, V, dev, reps=50):
     return out
 
 
-def lm_head_traffic(Ts):
+def lm_head_traffic(Ts, on_gpu=False):
     """Measured HBM bytes per LM-head launch (FETCH_SIZE + WRITE_SIZE, scaled by
     a device-copy calibration) for this step mix, from the committed counter
-    record -- or None when the kernel source changed since it was taken."""
+    record -- or None when the kernel sources changed since it was taken or
+    the record lacks a kernel the mix launches."""
     from paper_2606_27550_amd import rocprof_summary
     path = os.path.join(os.path.dirname(os.path.abspath(__file__)), "profiles", "lm_head_traffic.json")
     try:
@@ -917,13 +918,23 @@ def lm_head_traffic(Ts):
             # 2); an unpaired launch of the entry points must not stand in
             if key in per and len(targs) > 4 and targs[4] != "2":
                 continue
+        elif kernel == "lm_head_gemm_kernel" and targs[-1] == "true":   # <BM, BN, NST, STATS>
+            key = (kernel, 0)
+        elif kernel in ("lm_head_dyn_small_kernel", "lm_head_dyn_large_kernel"):
+            key = (kernel, 0)
         else:
             continue
         per[key] = v["fetch_bytes"] + v["write_bytes"]
     tot = 0.0
-    for T in Ts:   # the step's launch: the pair kernel up to 32 nodes, the grid kernel above
-        key = (("lm_head_pair_kernel", 1 if T <= 16 else 2) if T <= 32 else
-               ("lm_head_hyb_kernel", 4 if T <= 64 else 8))
+    for T in Ts:
+        if on_gpu:   # the device-sized kernels: the small one up to 32 nodes
+            key = ("lm_head_dyn_small_kernel" if T <= 32 else "lm_head_dyn_large_kernel", 0)
+        elif T <= 32:
+            key = ("lm_head_pair_kernel", 1 if T <= 16 else 2)
+        elif T <= 64:
+            key = ("lm_head_hyb_kernel", 4)
+        else:   # the tiled kernel where it takes the launch, else the 128-node streaming tile
+            key = ("lm_head_gemm_kernel", 0) if ("lm_head_gemm_kernel", 0) in per else ("lm_head_hyb_kernel", 8)
         if key not in per:
             return None
         tot += per[key]

@@ -31,12 +31,18 @@ import os
 import sys
 
 PKG = os.path.dirname(os.path.abspath(__file__))
-LM_HEAD_SRC = os.path.join(PKG, "csrc", "lm_head.hip")
+LM_HEAD_SRCS = [os.path.join(PKG, "csrc", f) for f in
+                ("lm_head.hip", "lm_head_gemm.hip", "stats.hpp", "stream_pipe.hpp")]
 
 
 def lm_head_source_hash() -> str:
-    with open(LM_HEAD_SRC, "rb") as f:
-        return hashlib.sha256(f.read()).hexdigest()
+    """sha256 over the LM-head kernel sources (the streaming, tiled and
+    device-sized kernels and their shared helpers)."""
+    h = hashlib.sha256()
+    for path in LM_HEAD_SRCS:
+        with open(path, "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
 
 
 def short(name: str) -> str:
@@ -59,17 +65,25 @@ def stats(csv_path: str, out_md: str, command: str) -> None:
         f.write("\n".join(lines) + "\n")
 
 
-def _counter(csv_path: str):
+def _counters(csv_paths):
     acc = collections.defaultdict(list)
-    for r in csv.DictReader(open(csv_path)):
-        acc[short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
+    for path in csv_paths:
+        for r in csv.DictReader(open(path)):
+            acc[short(r["Kernel_Name"])].append(float(r["Counter_Value"]))
     return {k: sum(v) / len(v) for k, v in acc.items()}, {k: len(v) for k, v in acc.items()}
+
+
+def _counter(csv_path: str):
+    return _counters([csv_path])
 
 
 def traffic(fetch_csv, write_csv, copy_fetch_csv, copy_write_csv, copy_bytes, out_md, out_json,
             commands) -> None:
-    fetch, n_fetch = _counter(fetch_csv)
-    write, _ = _counter(write_csv)
+    """fetch_csv / write_csv may each list several collections (comma
+    separated, one per workload run); a kernel seen in several keeps the
+    mean over all its dispatches."""
+    fetch, n_fetch = _counters(fetch_csv.split(","))
+    write, _ = _counters(write_csv.split(","))
     cf, _ = _counter(copy_fetch_csv)
     cw, _ = _counter(copy_write_csv)
     copy_kib = float(copy_bytes) / 1024.0
