@@ -50,6 +50,7 @@ import time
 import numpy as np
 
 HBM_PEAK_GBPS = 8000.0
+MFMA_PEAK_BF16_TFLOPS = 2500.0   # MI355X dense bf16 matrix peak
 METRIC = "tree-verify steps/sec and µs/step at batch 1; achieved HBM GB/s vs peak"
 MIN_TIMED_LAUNCHES = 16
 SINGLE_WORKLOADS = ["tree27_L256_7b", "bank5_L2048_7b", "tree64_L4096_7b_32layer",
@@ -502,6 +503,7 @@ def main():
 
     bytes_total = sum(step_bytes(T, L, a) for T, L, a, _, _ in trace)
     lm_bytes = sum(V * hid * 2 + T * hid * 2 for T in lm_T)
+    lm_flops = sum(2.0 * T * V * hid for T in lm_T)
     lm_s = sum(lm_ms) / 1e3
     steps_per_s = K / elapsed
     us = elapsed / K * 1e6
@@ -569,6 +571,8 @@ def main():
                      "unit": "GB/s", "frac": round(lm_gbps / HBM_PEAK_GBPS, 4), "traffic": traffic,
                      "algorithmic_bytes_per_launch": round(lm_bytes / max(1, len(lm_T))),
                      "avg_us": round(float(np.mean(lm_ms)) * 1e3, 2), "avg_us_by_T": lm_us_by_T,
+                     "mfma_TFLOPs": round(lm_flops / lm_s / 1e12, 1),
+                     "mfma_frac_bf16": round(lm_flops / lm_s / 1e12 / MFMA_PEAK_BF16_TFLOPS, 4),
                      "timed_launches": len(lm_ms), "timed_launches_in_region": n_in_region,
                      "timing": "HIP events (no system fence) on the step stream around the LM-head "
                                f"launch of a seeded random {n_in_region} of the {K} timed steps and "
@@ -817,7 +821,7 @@ def run_batched(args, api, synth, torch, lib):
                      "frac": round(lm_bytes / lm_mean / 1e3 / HBM_PEAK_GBPS, 4), "traffic": None,
                      "avg_us": round(lm_mean, 2), "mean_rows": round(lm_rows, 1),
                      "mfma_TFLOPs": round(lm_flops / lm_mean / 1e6, 1),
-                     "mfma_frac_bf16": round(lm_flops / lm_mean / 1e6 / 2500.0, 4),
+                     "mfma_frac_bf16": round(lm_flops / lm_mean / 1e6 / MFMA_PEAK_BF16_TFLOPS, 4),
                      "timing": "HIP events around the LM-head launch of every n-th timed step"},
         "cpu_baseline": None,
     }
