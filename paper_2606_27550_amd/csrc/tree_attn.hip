@@ -207,9 +207,11 @@ inline void set_rope(BatchArgs& a, float rope_theta) {
   a.theta = static_cast<double>(rope_theta);
   for (int c = 0; c < kRopePairs; ++c) a.freq[c] = a.theta > 0.0 ? std::pow(a.theta, -2.0 * c / HD) : 0.0;
 }
-__device__ __forceinline__ void rope_table(double2* tab, int D, int L, const double* freq) {
+// f: this thread's pair frequency, freq[threadIdx.x % 64], loaded by the
+// caller ahead of its bulk loads (a load issued behind them would wait for
+// them).
+__device__ __forceinline__ void rope_table(double2* tab, int D, int L, double f) {
   const int c = threadIdx.x % kRopePairs;
-  const double f = freq[c];
   for (int d = threadIdx.x / kRopePairs; d <= D; d += blockDim.x / kRopePairs) {
     const double pos = static_cast<double>(L) + static_cast<double>(d);
     double sn, cs;
@@ -386,8 +388,35 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   uint16_t* const kc_head = sq.kc + head_off;
   uint16_t* const vc_head = sq.vc + head_off;
 
-  // the wave's first block is requested before the prologue, so its latency
-  // overlaps the staging of the queries
+  // Q^T B-operand fragments, the same for the four waves (they split keys,
+  // not queries), staged once in LDS: lane (query li, half lh) of tile t
+  // reads d = 16s + 8lh + e from slot [t][s][lane].  Query row r of KV head
+  // g is (head g * G + r / T, node r % T); thread (s, ln) loads chunks s and
+  // s + 4 of its row (the two halves of pairs 16s + 8lh + e).  These small
+  // loads (and the masks, the depth and the pair frequency) are requested
+  // first and unconditionally (rows past the tree read row 0 and are never
+  // stored): behind the waves' first K/V blocks they would wait for every
+  // workgroup's burst.
+  static_assert(NT * 4 * 64 == kAttnThreads, "one thread per pair of Q chunks");
+  const int qs = (tid >> 6) & 3, qhl = (tid >> 5) & 1;
+  const int qrow = qt0 * kQTile + li;
+  const bool qlive = qrow < GT;
+  const int qnode = qlive ? qrow % T : 0;
+  u32x4 qlo, qhi;
+  {
+    const uint16_t* qp = p.q + (static_cast<size_t>(sq.row0 + qnode) * p.Hq + g * p.G + (qlive ? qrow / T : 0)) * HD +
+                         8 * qhl + 16 * qs;
+    qlo = *reinterpret_cast<const u32x4*>(qp);
+    qhi = *reinterpret_cast<const u32x4*>(qp + HD / 2);
+  }
+  const int qdepth = sq.depth[qnode];
+  static_assert(QR * ENTMTP_MASK_WORDS == kAttnThreads, "one mask word per thread");
+  const int mrow = qt0 * kQTile + tid / ENTMTP_MASK_WORDS;
+  const uint32_t mword = sq.mask[(mrow < GT ? mrow % T : 0) * ENTMTP_MASK_WORDS + tid % ENTMTP_MASK_WORDS];
+  const double freq = p.freq[tid % kRopePairs];
+
+  // the wave's first block is requested before the rest of the prologue, so
+  // its latency overlaps the staging of the queries
   const bool active = blk_lo + wave < blk_hi;
   u32x4 kA[8], kB[8], v0[4], v1[4];
   int cur = blk_lo + wave;
@@ -396,40 +425,17 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
     load_v(cur, v0, v1);
   }
 
-  // Q^T B-operand fragments, the same for the four waves (they split keys,
-  // not queries), staged once in LDS: lane (query li, half lh) of tile t
-  // reads d = 16s + 8lh + e from slot [t][s][lane].  Query row r of KV head
-  // g is (head g * G + r / T, node r % T); thread (s, ln) loads chunks s and
-  // s + 4 of its row (the two halves of pairs 16s + 8lh + e), requested
-  // here and rotated once the angle table is built.
-  static_assert(NT * 4 * 64 == kAttnThreads, "one thread per pair of Q chunks");
-  const int qs = (tid >> 6) & 3, qhl = (tid >> 5) & 1;
-  const int qrow = qt0 * kQTile + li;
-  const bool qlive = qrow < GT;
-  u32x4 qlo{0u, 0u, 0u, 0u}, qhi{0u, 0u, 0u, 0u};
-  int qdepth = 0;
-  if (qlive) {
-    const int node = qrow % T;
-    const uint16_t* qp = p.q + (static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + qrow / T) * HD +
-                         8 * qhl + 16 * qs;
-    qlo = *reinterpret_cast<const u32x4*>(qp);
-    qhi = *reinterpret_cast<const u32x4*>(qp + HD / 2);
-    qdepth = sq.depth[node];
-  }
-  // ancestor masks of the group's query rows (padding rows see every key)
-  for (int u = tid; u < QR * ENTMTP_MASK_WORDS; u += kAttnThreads) {
-    const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
-    const int mrow = qt0 * kQTile + r;
-    s_mask[r][w] = mrow < GT ? sq.mask[(mrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
-  }
+  // ancestor masks of the group's query rows (padding rows see every key),
+  // the angle table, and the rotated Q fragments into LDS
+  s_mask[tid / ENTMTP_MASK_WORDS][tid % ENTMTP_MASK_WORDS] = mrow < GT ? mword : 0xFFFFFFFFu;
   const bool rope = p.theta > 0.0;
   if (rope) {
-    rope_table(s_rope, sq.D, L, p.freq);
+    rope_table(s_rope, sq.D, L, freq);
     __syncthreads();
     if (qlive) rope_pairs_f32(qlo, qhi, rope_table_f32(s_rope, sq.D) + qdepth * kRopePairs + 16 * qs + 8 * qhl);
   }
-  s_qf[0][qs][lane] = qlo;
-  s_qf[0][qs + 4][lane] = qhi;
+  s_qf[0][qs][lane] = qlive ? qlo : u32x4{0u, 0u, 0u, 0u};
+  s_qf[0][qs + 4][lane] = qlive ? qhi : u32x4{0u, 0u, 0u, 0u};
   __syncthreads();
 
   // running (max, sum) per query in base-2 scaled units and the output
@@ -826,34 +832,48 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
     }
   };
 
+  // The small loads go first (this wave's Q fragments, its rows' depths and
+  // the group's masks, all unconditional: rows past the tree read row 0 and
+  // are never stored): requested after the first two K/V blocks they waited
+  // behind every workgroup's 32 KB burst (measured: a 6 us prologue).
+  // Query row r of KV head g is (head g * G + r / T, node r % T); chunks s
+  // and s + 4 hold the two halves of pairs 16s + 8lh + e.
+  u32x4 qf[8];
+  const int qrow = qt * kQTile + li;
+  const bool qlive = qrow < GT;
+  const int qnode = qlive ? qrow % T : 0;
+  {
+    const uint16_t* qp = p.q + (static_cast<size_t>(sq.row0 + qnode) * p.Hq + g * p.G + (qlive ? qrow / T : 0)) * HD +
+                         8 * lh;
+#pragma unroll
+    for (int s = 0; s < 8; ++s) qf[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s);
+  }
+  const int qdepth = sq.depth[qnode];
+  constexpr int kMaskPer = QR * ENTMTP_MASK_WORDS / kAttnThreads;
+  static_assert(kMaskPer * kAttnThreads == QR * ENTMTP_MASK_WORDS, "mask words fill the threads");
+  uint32_t mw[kMaskPer];
+#pragma unroll
+  for (int j = 0; j < kMaskPer; ++j) {
+    const int u = tid + kAttnThreads * j;
+    const int mrow = qg * QR + u / ENTMTP_MASK_WORDS;
+    mw[j] = sq.mask[(mrow < GT ? mrow % T : 0) * ENTMTP_MASK_WORDS + u % ENTMTP_MASK_WORDS];
+  }
+  const double freq = p.freq[tid % kRopePairs];
+
   u32x4 kA[2], kB[2], vaA, vbA, vaB, vbB;
   gload(0, kA, vaA, vbA);
   gload(1, kB, vaB, vbB);
 
-  // this wave's Q fragments: query row r of KV head g is (head g * G + r / T,
-  // node r % T); chunks s and s + 4 hold the two halves of pairs
-  // 16s + 8lh + e, rotated once the angle table is built
-  u32x4 qf[8];
-  const int qrow = qt * kQTile + li;
-  const bool qlive = qrow < GT;
-  int qdepth = 0;
+  // ancestor masks of the group's rows (padding rows see every key), the
+  // angle table and this wave's rotated Q fragments, while the blocks arrive
 #pragma unroll
-  for (int s = 0; s < 8; ++s) qf[s] = u32x4{0u, 0u, 0u, 0u};
-  if (qlive) {
-    const int node = qrow % T;
-    const uint16_t* qp = p.q + (static_cast<size_t>(sq.row0 + node) * p.Hq + g * p.G + qrow / T) * HD + 8 * lh;
-#pragma unroll
-    for (int s = 0; s < 8; ++s) qf[s] = *reinterpret_cast<const u32x4*>(qp + 16 * s);
-    qdepth = sq.depth[node];
-  }
-  // ancestor masks of the group's rows
-  for (int u = tid; u < QR * ENTMTP_MASK_WORDS; u += kAttnThreads) {
-    const int r = u / ENTMTP_MASK_WORDS, w = u % ENTMTP_MASK_WORDS;
-    const int mrow = qg * QR + r;
-    s_mask[r][w] = mrow < GT ? sq.mask[(mrow % T) * ENTMTP_MASK_WORDS + w] : 0xFFFFFFFFu;
+  for (int j = 0; j < kMaskPer; ++j) {
+    const int u = tid + kAttnThreads * j;
+    const int r = u / ENTMTP_MASK_WORDS;
+    s_mask[r][u % ENTMTP_MASK_WORDS] = qg * QR + r < GT ? mw[j] : 0xFFFFFFFFu;
   }
   if (rope) {
-    rope_table(s_rope, sq.D, L, p.freq);
+    rope_table(s_rope, sq.D, L, freq);
     __syncthreads();
     if (qlive) {
       const float2* tr = rope_table_f32(s_rope, sq.D) + qdepth * kRopePairs + 8 * lh;
