@@ -1028,10 +1028,14 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
 // ----------------------------------------------------------------- merge --
 
 // One half-wavefront per output row (kMergeRows rows per block): lane c <
-// nsplit reads split c's (max, sum), the group reduces them to the common max
-// and the normalised split weights, then each lane combines four dims of
-// every split's partial output (independent float4 loads, unrolled).
+// nsplit reads split c's (max, sum) and every lane then requests its four
+// dims of the first kMergeBatch splits' partial outputs at once (one memory
+// latency instead of one per four splits: the kernel's time was those
+// rounds), the group reduces the (max, sum) pairs to the common max and the
+// normalised split weights, and combines; splits past the batch follow four
+// at a time.
 constexpr int kMergeRows = 8;
+constexpr int kMergeBatch = 16;   // splits whose partials are requested together
 constexpr int kMergeThreads = 32 * kMergeRows;
 static_assert(kMaxSplits <= 32, "a half-wavefront holds one lane per split");
 
@@ -1054,6 +1058,11 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
     mc = ml.x;
     lc = ml.y;
   }
+  const int d4 = 4 * lane;
+  float4 ob[kMergeBatch];
+#pragma unroll
+  for (int c = 0; c < kMergeBatch; ++c)
+    ob[c] = *reinterpret_cast<const float4*>(p.part_o + prow_of(min(c, nsplit - 1)) * HD + d4);
   float M = mc;
 #pragma unroll
   for (int off = 16; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 32));
@@ -1062,9 +1071,16 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
 #pragma unroll
   for (int off = 16; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off, 32);
   const float wn = w / lsum;   // the split's share of the row
-  const int d4 = 4 * lane;
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
-  for (int c0 = 0; c0 < nsplit; c0 += 4) {   // four splits' loads in flight at a time
+#pragma unroll
+  for (int c = 0; c < kMergeBatch; ++c) {
+    const float wc = c < nsplit ? __shfl(wn, c, 32) : 0.f;
+    acc.x += wc * ob[c].x;
+    acc.y += wc * ob[c].y;
+    acc.z += wc * ob[c].z;
+    acc.w += wc * ob[c].w;
+  }
+  for (int c0 = kMergeBatch; c0 < nsplit; c0 += 4) {   // four splits' loads in flight at a time
     float4 o[4];
     float wc[4];
 #pragma unroll
