@@ -530,6 +530,16 @@ def main():
                  "hbm_frac": round(sum(step_bytes(T, L, a) for T, L, a, _, _ in r2["trace"])
                                    / r2["elapsed"] / 1e9 / HBM_PEAK_GBPS, 4)}
         log(f"host-scheduled: {other['us_per_step']} us/step")
+        # the same device-scheduled steps replayed as captured HIP graph
+        # segments (no host launches inside a segment)
+        gc.collect()
+        r3 = run.run(K, args.warmup, policy, grow=grows, start_rung=max(args.fixed_topo, 0),
+                     arm=not args.no_arm, arm_reach=not fixed, n_events=0, event_pass=0,
+                     on_gpu=True, graph=True)
+        other["graph_replay"] = {"scheduler": "GPU, steps replayed as captured HIP graph segments",
+                                 "us_per_step": round(r3["elapsed"] / K * 1e6, 2),
+                                 "steps_per_s": round(K / r3["elapsed"], 2)}
+        log(f"device-scheduled, graph replay: {other['graph_replay']['us_per_step']} us/step")
 
     cpu = None
     if not args.no_cpu_baseline and NL == 1:
