@@ -9,8 +9,10 @@
 // one wave per 16 rows; this kernel gives a workgroup a 256-row vocabulary
 // block (four of the streaming grid's slices) and 128 rows of X, shared
 // through LDS, so each LDS byte feeds 64 to 128 products:
-//  * four waves in a 2 x 2 grid over the 256 x 128 output tile, each
-//    accumulating a 128 x 64 sub-tile with v_mfma_f32_16x16x32_bf16;
+//  * eight waves in a 4 x 2 grid over the 256 x 128 output tile (two per
+//    SIMD, so one issues products while the other waits), each accumulating
+//    a 64 x 64 sub-tile with v_mfma_f32_16x16x32_bf16 (128-row blocks: four
+//    waves, 2 x 2);
 //  * K advances in stages of 64: each wave loads its share of a stage's W
 //    and X rows into VGPRs (8 rows x 128 bytes per instruction) two stages
 //    ahead of storing them into one of three LDS slots, two stages ahead of
@@ -38,7 +40,6 @@
 namespace entmtp {
 namespace {
 
-constexpr int kGemmThreads = 256;   // four waves, 2 x 2 over the output tile
 constexpr int kGemmBN = 128;        // rows of X per pass
 constexpr int kGemmBK = 64;         // k per stage: two MFMA k-steps, 128-byte rows
 constexpr int kGemmMinRows = 128;   // the streaming kernels' largest pass
@@ -48,8 +49,11 @@ constexpr int kGemmD = 2;           // stages of loads held in VGPRs ahead of th
 // BM vocabulary rows per block: BM / 64 of the streaming grid's slices (at
 // most 64 rows each), 256 when the vocabulary gives every CU a block (128256
 // entries: 501 blocks), else 128 (32000: 250).
-template <int BM, int BN>
+// NW waves: NW / 2 along the vocabulary rows, two along the rows of X.
+template <int BM, int BN, int NW>
 struct GemmShape {
+  static constexpr int THREADS = 64 * NW;
+  static constexpr int WMW = NW / 2;              // waves along M
   static constexpr int SLICES = BM / 64;
   static constexpr int ROWB = kGemmBK * 2;        // bytes of a row per stage
   static constexpr int CH = ROWB / 16;            // 16-byte chunks per row
@@ -57,13 +61,18 @@ struct GemmShape {
   static constexpr int A_BYTES = BM * ROWB;       // W block
   static constexpr int B_BYTES = BN * ROWB;       // X block
   static constexpr int SLOT = A_BYTES + B_BYTES;
-  static constexpr int AI = BM / RPI / 4;         // W loads per wave per stage
-  static constexpr int BI = BN / RPI / 4;         // X loads per wave per stage
+  static constexpr int AI = BM / RPI / NW;        // W loads per wave per stage
+  static constexpr int BI = BN / RPI / NW;        // X loads per wave per stage
   static constexpr int LI = AI + BI;
-  static constexpr int WM = BM / 2, WN = BN / 2;   // wave sub-tile
+  static constexpr int WM = BM / WMW, WN = BN / 2;   // wave sub-tile
   static constexpr int MI = WM / 16, NI = WN / 16;
   static constexpr int NF = MI + NI;              // fragments per k-step
-  static_assert(BN % (4 * RPI) == 0 && AI % 2 == 0 && BI % 2 == 0, "loads split evenly");
+  // Accumulators in AGPRs when a wave's 128 x 64 sub-tile needs 128 of them
+  // beside ~220 VGPRs (one wave per SIMD); with two waves per SIMD the
+  // compiler halves the 256-register budget between the two files once
+  // AGPRs are used, so 64 x 64 sub-tiles keep theirs in VGPRs.
+  static constexpr bool ACC_AGPR = NW == 4;
+  static_assert(BN % (NW * RPI) == 0 && AI % 2 == 0 && BI % 2 == 0, "loads split evenly");
   static_assert(kGemmSlots * SLOT <= 160 * 1024, "slots fit in LDS");
 };
 
@@ -86,6 +95,15 @@ __device__ __forceinline__ void wait_lds_but() {
 }
 __device__ __forceinline__ void wait_lds() { wait_lds_but<0>(); }
 
+// True when each of h groups of m products (split as evenly as integer
+// division gives) has a product ahead of each of its accesses: a store, a
+// load and its share of f fragment reads.
+constexpr bool gemm_groups_fit(int m, int h, int f) {
+  for (int g = 0; g < h; ++g)
+    if (2 + f * (g + 1) / h - f * g / h > m * (g + 1) / h - m * g / h) return false;
+  return true;
+}
+
 // Waits out the latency of the last MFMAs before their accumulators are
 // read (32 wait states: the longest 16x16x32 result latency is 16 passes of
 // four cycles, of which the issue of the following instructions covers the
@@ -94,11 +112,11 @@ __device__ __forceinline__ void mfma_drain() {
   asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
 }
 
-template <int BM, int BN, int NST, bool STATS>
-__global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
+template <int BM, int BN, int NW, int NST, bool STATS>
+__global__ __launch_bounds__(64 * NW) void lm_head_gemm_kernel(
     const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
     int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
-  using Sh = GemmShape<BM, BN>;
+  using Sh = GemmShape<BM, BN, NW>;
   constexpr int kSlices = Sh::SLICES;
   __shared__ __attribute__((aligned(16))) uint8_t ring[kGemmSlots * Sh::SLOT];
 
@@ -116,7 +134,7 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   const StatPart empty{-INFINITY, 0.f, 0.f, 0x7fffffff};
   if (r0 >= r1) {   // empty block (tiny V): neutral partials only
     if constexpr (STATS)
-      for (int c = tid; c < BN; c += kGemmThreads)
+      for (int c = tid; c < BN; c += Sh::THREADS)
         if (j0 + c < T)
           for (int u = 0; u < kSlices && kSlices * grp + u < G; ++u)
             part[static_cast<size_t>(j0 + c) * G + kSlices * grp + u] = empty;
@@ -167,7 +185,7 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   };
 
   const int lr = lane & 15, lg = lane >> 4;
-  const int wm = wave & 1, wn = wave >> 1;
+  const int wm = wave % Sh::WMW, wn = wave / Sh::WMW;
   // fragment f of k-step j: W block f (f < MI) rows wm*WM + 16f + lr, or X
   // block f - MI rows wn*WN + 16(f - MI) + lr; chunk 4j + lg
   auto read_one = [&](bf16x8& out, const uint8_t* slot, int j, int f) {
@@ -191,10 +209,16 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   // before the epilogue reads them.
   auto mfma_one = [&](int buf, int i) {
     const int mi = i / Sh::NI, ni = i % Sh::NI;
-    asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
-                 : "+a"(acc[mi][ni])
-                 : "v"(frag[buf][mi]), "v"(frag[buf][Sh::MI + ni])
-                 : "memory");
+    if constexpr (Sh::ACC_AGPR)
+      asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                   : "+a"(acc[mi][ni])
+                   : "v"(frag[buf][mi]), "v"(frag[buf][Sh::MI + ni])
+                   : "memory");
+    else
+      asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
+                   : "+v"(acc[mi][ni])
+                   : "v"(frag[buf][mi]), "v"(frag[buf][Sh::MI + ni])
+                   : "memory");
   };
   // the fragments in the order the products need them: X blocks (every
   // product of the first W block uses one), then W blocks
@@ -223,34 +247,38 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   for (int n = 0; n < Sh::NF; ++n) read_one(frag[0][frag_at(n)], ring, 0, frag_at(n));
   mfma_drain();   // the accumulators' zeroing precedes their first product
 
-  // Step c, K = c mod 6 (slot and load set depend on K only).  Each k-step
-  // runs its products in groups of (product, store, product, load, product,
-  // read, product, read, products): half the stores of stage c + 2 and the
-  // loads of stage c + 2 + D that refill their registers, and the fragments
-  // of the next k-step (stage c's second in k-step 0, stage c + 1's first in
-  // k-step 1).  Issued in one burst the LDS accesses filled the LDS queue
-  // and the wave stalled there with the matrix pipe idle.  Every store is
-  // followed by exactly two reads, so lgkmcnt(2) at the end means the
-  // step's stores have landed.
+  // Step c, K = c mod 6 (slot and load set depend on K only).  A k-step's
+  // products run in LI / 2 groups; after the products of group g, one at a
+  // time: a store of stage c + 2 (half of them per k-step), the load of
+  // stage c + 2 + D that refills its registers, and the group's share of the
+  // fragments of the next k-step (stage c's second in k-step 0, stage c + 1's
+  // first in k-step 1).  Issued in one burst the LDS accesses filled the LDS
+  // queue and the wave stalled there with the matrix pipe idle.  The last
+  // group's reads follow the step's last store, so lgkmcnt(kTailReads) at the
+  // end means the step's stores have landed.
   constexpr int kMma = Sh::MI * Sh::NI;
   constexpr int kHalf = Sh::LI / 2;
-  static_assert(2 * kHalf == Sh::NF && 4 * kHalf <= kMma, "one group per store");
+  constexpr int kTailReads = Sh::NF - Sh::NF * (kHalf - 1) / kHalf;
+  static_assert(gemm_groups_fit(kMma, kHalf, Sh::NF) && kTailReads < 16,
+                "every group's accesses follow products of its own");
   auto kstep = [&](int j, uint8_t* wslot, u32x4 (&pr)[Sh::LI], const uint8_t* rslot, int rj,
                    int c) {
 #pragma unroll
     for (int g = 0; g < kHalf; ++g) {
       const int q = j * kHalf + g;
       const int lo = kMma * g / kHalf, hi = kMma * (g + 1) / kHalf;   // this group's products
+      const int f0 = Sh::NF * g / kHalf, f1 = Sh::NF * (g + 1) / kHalf;   // and fragments
       mfma_one(j, lo);
       *reinterpret_cast<u32x4*>(wslot + dst_of(q)) = pr[q];
       mfma_one(j, lo + 1);
       load_one(pr[q], q, c + 2 + kGemmD);
-      mfma_one(j, lo + 2);
-      read_one(frag[j ^ 1][frag_at(2 * g)], rslot, rj, frag_at(2 * g));
-      mfma_one(j, lo + 3);
-      read_one(frag[j ^ 1][frag_at(2 * g + 1)], rslot, rj, frag_at(2 * g + 1));
 #pragma unroll
-      for (int i = lo + 4; i < hi; ++i) mfma_one(j, i);
+      for (int f = f0; f < f1; ++f) {
+        mfma_one(j, lo + 2 + f - f0);
+        read_one(frag[j ^ 1][frag_at(f)], rslot, rj, frag_at(f));
+      }
+#pragma unroll
+      for (int i = lo + 2 + f1 - f0; i < hi; ++i) mfma_one(j, i);
     }
   };
   auto step = [&](auto kc, int c) {
@@ -259,7 +287,7 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
     u32x4 (&pr)[Sh::LI] = pre[(K + 2) % kGemmD];
     kstep(0, wslot, pr, ring + (K % kGemmSlots) * Sh::SLOT, 1, c);
     kstep(1, wslot, pr, ring + ((K + 1) % kGemmSlots) * Sh::SLOT, 0, c);
-    wait_lds_but<2>();
+    wait_lds_but<kTailReads>();
     stage_barrier();
   };
   static_assert(6 % kGemmD == 0, "six steps return slots and load sets to their start");
@@ -311,8 +339,8 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
     }
   }
   if constexpr (STATS) {
-    // per row: the wave's partial over its 128 vocabulary rows (lane, then
-    // the four lane groups), then the two waves of a row in LDS.  A lane
+    // per row: the wave's partial over its WM vocabulary rows (lane, then
+    // the four lane groups), then the row's NW / 2 waves in LDS.  A lane
     // visits its rows in increasing order, so within the lane a strictly
     // larger value is the only update the lowest-index rule needs.  The
     // sums run in base 2 (one hardware exponential per logit): with
@@ -320,7 +348,7 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
     constexpr float kLog2e = 1.44269504088896341f, kLn2 = 0.69314718055994531f;
     const float it2 = inv_temp * kLog2e;
     const bool full = r1 - r0 == BM;   // every row of the block is a vocabulary row
-    StatPart* wpart = reinterpret_cast<StatPart*>(ring);   // [2][BN]
+    StatPart* wpart = reinterpret_cast<StatPart*>(ring);   // [WMW][BN]
 #pragma unroll
     for (int ni = 0; ni < Sh::NI; ++ni) {
       __builtin_amdgcn_sched_barrier(0);   // one node column at a time (as above)
@@ -363,10 +391,11 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
       if (lg == 0) wpart[wm * BN + wn * Sh::WN + 16 * ni + lr] = p;
     }
     __syncthreads();
-    for (int c = tid; c < BN; c += kGemmThreads) {
+    for (int c = tid; c < BN; c += Sh::THREADS) {
       if (j0 + c >= T) continue;
       StatPart q = wpart[c];
-      part_merge(q, wpart[BN + c], inv_temp);
+#pragma unroll
+      for (int w = 1; w < Sh::WMW; ++w) part_merge(q, wpart[w * BN + c], inv_temp);
       StatPart* dst = part + static_cast<size_t>(j0 + c) * G + kSlices * grp;
       dst[0] = q;
 #pragma unroll
@@ -376,26 +405,30 @@ __global__ __launch_bounds__(kGemmThreads) void lm_head_gemm_kernel(
   }
 }
 
-template <int BM, int NST, bool STATS>
+template <int BM, int NW, int NST, bool STATS>
 int32_t launch_gemm(const uint16_t* X, const uint16_t* W, float* logits, int T, int hid, int V,
                     int G, float inv_temp, StatPart* part, hipStream_t s) {
   constexpr int kSlices = BM / 64;
   const int groups = (G + kSlices - 1) / kSlices;
   const int passes = (T + kGemmBN - 1) / kGemmBN;
   const int blocks = (groups + 7) / 8 * passes * 8;
-  hipLaunchKernelGGL((lm_head_gemm_kernel<BM, kGemmBN, NST, STATS>), dim3(blocks),
-                     dim3(kGemmThreads), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
+  hipLaunchKernelGGL((lm_head_gemm_kernel<BM, kGemmBN, NW, NST, STATS>), dim3(blocks),
+                     dim3(64 * NW), 0, s, X, W, logits, T, hid, V, G, inv_temp, part);
   return launch_status("verify_logits (tiled) launch");
 }
+
+// 256-row blocks: eight waves (4 x 2, two per SIMD) measured 2-3 % faster
+// than four (2 x 2) at 90-544 rows.
+constexpr int kWideWaves = 8;
 
 template <int NST>
 int32_t launch_gemm_bm(bool wide, const uint16_t* X, const uint16_t* W, float* logits, int T,
                        int hid, int V, int G, float inv_temp, StatPart* part, hipStream_t s) {
   if (wide)
-    return part ? launch_gemm<256, NST, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
-                : launch_gemm<256, NST, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
-  return part ? launch_gemm<128, NST, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
-              : launch_gemm<128, NST, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
+    return part ? launch_gemm<256, kWideWaves, NST, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
+                : launch_gemm<256, kWideWaves, NST, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
+  return part ? launch_gemm<128, 4, NST, true>(X, W, logits, T, hid, V, G, inv_temp, part, s)
+              : launch_gemm<128, 4, NST, false>(X, W, logits, T, hid, V, G, inv_temp, nullptr, s);
 }
 
 }  // namespace
