@@ -26,6 +26,9 @@
 //    previous k-step; one LDS wait and one barrier per stage;
 //  * the passes of one vocabulary block run on one XCD (dispatch is
 //    round-robin), so W fetched by one pass is an L2 hit for the others;
+//  * each wave runs a form of the tile specialised to the number of its
+//    16-row X blocks that hold rows of the batch, so the last pass of a
+//    ragged batch (16 of 128 rows at 400) skips the padding's products;
 //  * with statistics the epilogue reduces each row's accumulators over the
 //    block into one partial (the streaming kernels' layout: the block's
 //    partial in its first slice, neutral partials in the other three), so
@@ -112,35 +115,20 @@ __device__ __forceinline__ void mfma_drain() {
   asm volatile("s_nop 15\n\ts_nop 15" ::: "memory");
 }
 
-template <int BM, int BN, int NW, int NST, bool STATS>
-__global__ __launch_bounds__(64 * NW) void lm_head_gemm_kernel(
-    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
-    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
+// The workgroup's tile (vocabulary rows [r0, r1), batch rows from j0),
+// with NA = the number of the wave's 16-row X blocks that hold rows of the
+// batch: the last pass of a ragged batch leaves out the products of the
+// others (loads, stores, fragment reads and barriers are the same in every
+// form, so the waves of a workgroup stay in step).
+template <int BM, int BN, int NW, int NST, bool STATS, int NA>
+__device__ __forceinline__ void gemm_tile(
+    uint8_t* __restrict__ ring, const uint16_t* __restrict__ X, const uint16_t* __restrict__ W,
+    float* __restrict__ logits, int T, int hid, int V, int G, float inv_temp,
+    StatPart* __restrict__ part, int grp, int j0, int r0, int r1) {
   using Sh = GemmShape<BM, BN, NW>;
   constexpr int kSlices = Sh::SLICES;
-  __shared__ __attribute__((aligned(16))) uint8_t ring[kGemmSlots * Sh::SLOT];
-
-  // 1-D grid over (block group, pass, XCD): the passes of one vocabulary
-  // block are consecutive workgroups of one XCD
-  const int groups = (G + kSlices - 1) / kSlices;
-  const int passes = (T + BN - 1) / BN;
-  const int bid = blockIdx.x, r8 = bid >> 3;
-  const int pass = r8 % passes, grp = (r8 / passes) * 8 + (bid & 7);
-  if (grp >= groups) return;
-  const int j0 = pass * BN;
-  const int r0 = slice_begin(kSlices * grp, G, V);
-  const int r1 = slice_begin(kSlices * grp + kSlices, G, V);
   const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
   const StatPart empty{-INFINITY, 0.f, 0.f, 0x7fffffff};
-  if (r0 >= r1) {   // empty block (tiny V): neutral partials only
-    if constexpr (STATS)
-      for (int c = tid; c < BN; c += Sh::THREADS)
-        if (j0 + c < T)
-          for (int u = 0; u < kSlices && kSlices * grp + u < G; ++u)
-            part[static_cast<size_t>(j0 + c) * G + kSlices * grp + u] = empty;
-    return;
-  }
-
   // load instruction q of a wave covers rows (wave * n + q) * 8 .. + 7 of
   // the block (n = AI for W, BI for X); lane l takes chunk l % 8 of row l / 8
   // and stores it at slot (l % 8) ^ swz(row).  W rows past the block load
@@ -200,7 +188,7 @@ __global__ __launch_bounds__(64 * NW) void lm_head_gemm_kernel(
 #pragma unroll
     for (int ni = 0; ni < Sh::NI; ++ni) acc[mi][ni] = f32x4{0.f, 0.f, 0.f, 0.f};
   bf16x8 frag[2][Sh::NF];
-  // The products accumulate in place in AGPRs, written as inline assembly:
+  // The products accumulate in place (AGPRs or VGPRs), as inline assembly:
   // with the builtin the compiler renamed the accumulators from one step to
   // the next and spent a move per accumulator register per loop trip
   // undoing it.  The "memory" clobber keeps the step's loads, stores and
@@ -209,6 +197,7 @@ __global__ __launch_bounds__(64 * NW) void lm_head_gemm_kernel(
   // before the epilogue reads them.
   auto mfma_one = [&](int buf, int i) {
     const int mi = i / Sh::NI, ni = i % Sh::NI;
+    if (ni >= NA) return;   // an X block wholly past the batch
     if constexpr (Sh::ACC_AGPR)
       asm volatile("v_mfma_f32_16x16x32_bf16 %0, %1, %2, %0"
                    : "+a"(acc[mi][ni])
@@ -402,6 +391,56 @@ __global__ __launch_bounds__(64 * NW) void lm_head_gemm_kernel(
       for (int u = 1; u < kSlices; ++u)
         if (kSlices * grp + u < G) dst[u] = empty;
     }
+  }
+}
+
+template <int BM, int BN, int NW, int NST, bool STATS>
+__global__ __launch_bounds__(64 * NW) void lm_head_gemm_kernel(
+    const uint16_t* __restrict__ X, const uint16_t* __restrict__ W, float* __restrict__ logits,
+    int T, int hid, int V, int G, float inv_temp, StatPart* __restrict__ part) {
+  using Sh = GemmShape<BM, BN, NW>;
+  constexpr int kSlices = Sh::SLICES;
+  __shared__ __attribute__((aligned(16))) uint8_t ring[kGemmSlots * Sh::SLOT];
+
+  // 1-D grid over (block group, pass, XCD): the passes of one vocabulary
+  // block are consecutive workgroups of one XCD
+  const int groups = (G + kSlices - 1) / kSlices;
+  const int passes = (T + BN - 1) / BN;
+  const int bid = blockIdx.x, r8 = bid >> 3;
+  const int pass = r8 % passes, grp = (r8 / passes) * 8 + (bid & 7);
+  if (grp >= groups) return;
+  const int j0 = pass * BN;
+  const int r0 = slice_begin(kSlices * grp, G, V);
+  const int r1 = slice_begin(kSlices * grp + kSlices, G, V);
+  const int tid = threadIdx.x, wave = tid >> 6;
+  const StatPart empty{-INFINITY, 0.f, 0.f, 0x7fffffff};
+  if (r0 >= r1) {   // empty block (tiny V): neutral partials only
+    if constexpr (STATS)
+      for (int c = tid; c < BN; c += Sh::THREADS)
+        if (j0 + c < T)
+          for (int u = 0; u < kSlices && kSlices * grp + u < G; ++u)
+            part[static_cast<size_t>(j0 + c) * G + kSlices * grp + u] = empty;
+    return;
+  }
+  // live X blocks of the wave (wave-uniform)
+  const int na = __builtin_amdgcn_readfirstlane(
+      min(max((T - j0 - (wave / Sh::WMW) * Sh::WN + 15) / 16, 0), Sh::NI));
+  static_assert(Sh::NI == 4, "one form per live X block count");
+  switch (na) {
+    case 0:
+      gemm_tile<BM, BN, NW, NST, STATS, 0>(ring, X, W, logits, T, hid, V, G, inv_temp, part, grp, j0, r0, r1);
+      break;
+    case 1:
+      gemm_tile<BM, BN, NW, NST, STATS, 1>(ring, X, W, logits, T, hid, V, G, inv_temp, part, grp, j0, r0, r1);
+      break;
+    case 2:
+      gemm_tile<BM, BN, NW, NST, STATS, 2>(ring, X, W, logits, T, hid, V, G, inv_temp, part, grp, j0, r0, r1);
+      break;
+    case 3:
+      gemm_tile<BM, BN, NW, NST, STATS, 3>(ring, X, W, logits, T, hid, V, G, inv_temp, part, grp, j0, r0, r1);
+      break;
+    default:
+      gemm_tile<BM, BN, NW, NST, STATS, 4>(ring, X, W, logits, T, hid, V, G, inv_temp, part, grp, j0, r0, r1);
   }
 }
 

@@ -93,9 +93,12 @@ def test_tiled_lm_head_logits_only_sampled(api):
 
 
 @pytest.mark.parametrize("T,hid,V", [(65, 4096, 128256), (90, 4096, 128256), (129, 4096, 128256),
-                                     (400, 4096, 128256), (200, 4096, 32000), (257, 4096, 32000),
+                                     (400, 4096, 128256), (148, 4096, 32000), (200, 4096, 32000),
+                                     (257, 4096, 32000),
                                      (129, 5120, 32000), (300, 5120, 32000)])
 def test_tiled_lm_head_statistics(api, T, hid, V):
+    """Row counts chosen so that the last pass of 128 rows leaves each wave
+    every number (0-4) of live 16-row blocks at both tile shapes."""
     say("tiled LM head + statistics", T, hid, V)
     w, wd = weight(V, hid)
     X = synth.hidden_rows(40 + T, T, hid)
