@@ -75,12 +75,14 @@ def check_rows(api, X, w, wd, with_logits=True):
 
 def test_tiled_lm_head_logits_only_sampled(api):
     """entmtp_verify_logits (no statistics) at the batched workload's row
-    counts: sampled columns, the vocabulary's ends included."""
+    counts and past 256 rows (300 and 340 leave the waves 3 and 2 live
+    16-row blocks in the last pass): sampled columns, the vocabulary's ends
+    included."""
     V, hid = 128256, 4096
     w, wd = weight(V, hid)
     cols = np.unique(np.concatenate([np.random.default_rng(3).integers(0, V, 300),
                                      [0, 1, 2, 3, 255, 256, V - 4, V - 3, V - 2, V - 1]]))
-    for T in (72, 300):
+    for T in (72, 300, 340):
         say("tiled LM head logits only", T)
         X = synth.hidden_rows(60 + T, T, hid)
         out = torch.full((T, V), float("nan"), device="cuda")
