@@ -32,7 +32,9 @@
 //     Online softmax in fp32, base 2, with a lazily raised running max (the
 //     accumulators are rescaled only when a block's max passes the reference
 //     by more than 2^8).
-//  2. merge: combines the splits' (max, sum, unnormalised output) partials.
+//  2. merge: combines the splits' partials: (max, sum) in fp32 and the
+//     output normalised by its sum, in bf16 (half the bytes of fp32; a
+//     normalised partial stays within the range of the values).
 //     Skipped when a single split covers the keys.
 #include <cfloat>
 #include <cmath>
@@ -138,7 +140,7 @@ struct BatchArgs {
   const uint16_t* q;       // [rows][Hq][HD] (rows = sum of T, sequence after sequence)
   const uint16_t* kt;      // [rows][Hkv][HD]
   const uint16_t* vt;
-  float* part_o;           // [part rows][HD]
+  uint16_t* part_o;        // [part rows][HD] bf16: the split's output, normalised by its sum
   float* part_ml;          // [part rows][2]
   uint16_t* out;           // [rows][Hq][HD]
 };
@@ -710,7 +712,11 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
         *reinterpret_cast<uint2*>(p.out + (static_cast<size_t>(sq.row0 + node) * p.Hq + h) * HD + d4) = pk;
       } else {
         const size_t prow = sq.part_off + (static_cast<size_t>(split) * p.Hkv + g) * rows_pad + row;
-        *reinterpret_cast<float4*>(p.part_o + prow * HD + d4) = os;
+        const float il = lsum > 0.f ? 1.f / lsum : 0.f;   // 0: no key of the split is visible
+        uint2 pk;
+        pk.x = f32_to_bf16_rne(os.x * il) | (f32_to_bf16_rne(os.y * il) << 16);
+        pk.y = f32_to_bf16_rne(os.z * il) | (f32_to_bf16_rne(os.w * il) << 16);
+        *reinterpret_cast<uint2*>(p.part_o + prow * HD + d4) = pk;
         if (d4 == 0) {
           p.part_ml[prow * 2 + 0] = Mq;
           p.part_ml[prow * 2 + 1] = lsum;
@@ -1011,13 +1017,17 @@ __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs
       }
   } else {
     const size_t prow = sq.part_off + (static_cast<size_t>(split) * p.Hkv + g) * rows_pad + row;
-    float* dst = p.part_o + prow * HD;
+    uint16_t* dst = p.part_o + prow * HD;
+    const float il = l_run > 0.f ? 1.f / l_run : 0.f;   // 0: no key of the split is visible
 #pragma unroll
     for (int ct = 0; ct < 4; ++ct)
 #pragma unroll
-      for (int j = 0; j < 4; ++j)
-        *reinterpret_cast<float4*>(dst + 32 * ct + 8 * j + 4 * lh) =
-            make_float4(o[ct][4 * j], o[ct][4 * j + 1], o[ct][4 * j + 2], o[ct][4 * j + 3]);
+      for (int j = 0; j < 4; ++j) {
+        uint2 pk;
+        pk.x = f32_to_bf16_rne(o[ct][4 * j] * il) | (f32_to_bf16_rne(o[ct][4 * j + 1] * il) << 16);
+        pk.y = f32_to_bf16_rne(o[ct][4 * j + 2] * il) | (f32_to_bf16_rne(o[ct][4 * j + 3] * il) << 16);
+        *reinterpret_cast<uint2*>(dst + 32 * ct + 8 * j + 4 * lh) = pk;
+      }
     if (lh == 0) {
       p.part_ml[prow * 2 + 0] = m_run;
       p.part_ml[prow * 2 + 1] = l_run;
@@ -1059,10 +1069,10 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
     lc = ml.y;
   }
   const int d4 = 4 * lane;
-  float4 ob[kMergeBatch];
+  uint2 ob[kMergeBatch];
 #pragma unroll
   for (int c = 0; c < kMergeBatch; ++c)
-    ob[c] = *reinterpret_cast<const float4*>(p.part_o + prow_of(min(c, nsplit - 1)) * HD + d4);
+    ob[c] = *reinterpret_cast<const uint2*>(p.part_o + prow_of(min(c, nsplit - 1)) * HD + d4);
   float M = mc;
 #pragma unroll
   for (int off = 16; off >= 1; off >>= 1) M = fmaxf(M, __shfl_xor(M, off, 32));
@@ -1070,32 +1080,27 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
   float lsum = lc * w;
 #pragma unroll
   for (int off = 16; off >= 1; off >>= 1) lsum += __shfl_xor(lsum, off, 32);
-  const float wn = w / lsum;   // the split's share of the row
+  const float wn = w * lc / lsum;   // the split's share of the row
   float4 acc = make_float4(0.f, 0.f, 0.f, 0.f);
+  auto add = [&](float wc, uint2 v) {
+    acc.x += wc * __uint_as_float(v.x << 16);
+    acc.y += wc * __uint_as_float(v.x & 0xffff0000u);
+    acc.z += wc * __uint_as_float(v.y << 16);
+    acc.w += wc * __uint_as_float(v.y & 0xffff0000u);
+  };
 #pragma unroll
-  for (int c = 0; c < kMergeBatch; ++c) {
-    const float wc = c < nsplit ? __shfl(wn, c, 32) : 0.f;
-    acc.x += wc * ob[c].x;
-    acc.y += wc * ob[c].y;
-    acc.z += wc * ob[c].z;
-    acc.w += wc * ob[c].w;
-  }
+  for (int c = 0; c < kMergeBatch; ++c) add(c < nsplit ? __shfl(wn, c, 32) : 0.f, ob[c]);
   for (int c0 = kMergeBatch; c0 < nsplit; c0 += 4) {   // four splits' loads in flight at a time
-    float4 o[4];
+    uint2 o[4];
     float wc[4];
 #pragma unroll
     for (int k = 0; k < 4; ++k) {
       const int c = min(c0 + k, nsplit - 1);
       wc[k] = c0 + k < nsplit ? __shfl(wn, c, 32) : 0.f;
-      o[k] = *reinterpret_cast<const float4*>(p.part_o + prow_of(c) * HD + d4);
+      o[k] = *reinterpret_cast<const uint2*>(p.part_o + prow_of(c) * HD + d4);
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      acc.x += wc[k] * o[k].x;
-      acc.y += wc[k] * o[k].y;
-      acc.z += wc[k] * o[k].z;
-      acc.w += wc[k] * o[k].w;
-    }
+    for (int k = 0; k < 4; ++k) add(wc[k], o[k]);
   }
   const int gh = row / sq.T, node = row % sq.T;
   uint2 pk;
@@ -1207,7 +1212,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
       part_rows += static_cast<long long>(q.nsplit) * Hkv * q.rows_pad;
     }
   }
-  const size_t po = static_cast<size_t>(part_rows) * HD * 4;
+  const size_t po = static_cast<size_t>(part_rows) * HD * sizeof(uint16_t);
   const size_t pml = static_cast<size_t>(part_rows) * 2 * 4;
   sh.need = al256(po) + al256(pml);
   return sh;
@@ -1220,8 +1225,8 @@ int32_t launch_call(BatchArgs& a, const CallShape& sh, void* workspace, hipStrea
   long long part_rows = 0;
   for (int b = 0; b < a.B; ++b)
     if (a.s[b].nsplit > 1) part_rows += static_cast<long long>(a.s[b].nsplit) * a.Hkv * a.s[b].rows_pad;
-  const size_t po = static_cast<size_t>(part_rows) * HD * 4;
-  a.part_o = reinterpret_cast<float*>(ws);
+  const size_t po = static_cast<size_t>(part_rows) * HD * sizeof(uint16_t);
+  a.part_o = reinterpret_cast<uint16_t*>(ws);
   a.part_ml = reinterpret_cast<float*>(ws + al256(po));
   launch_attend(a, sh.items, rope_lds_bytes(sh.D, a.theta), s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
@@ -1239,7 +1244,7 @@ size_t workspace_bytes(int T, int Hq, int Hkv, int L) {
   const int rows_pad = rows_padded(G, T);
   const int nblocks = (L + T + KB - 1) / KB;
   const size_t bound = split_bound(nblocks);
-  return al256(bound * Hkv * rows_pad * HD * 4) + al256(bound * Hkv * rows_pad * 2 * 4);
+  return al256(bound * Hkv * rows_pad * HD * sizeof(uint16_t)) + al256(bound * Hkv * rows_pad * 2 * 4);
 }
 
 // Checks shared by the single and batched entry points.
@@ -1340,9 +1345,9 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
   // the workspace regions at the bounds workspace_bytes() sizes them with
   const int rows_pad = rows_padded(a.G, sh.T_max);
   const size_t bound = split_bound((cap + sh.T_max + KB - 1) / KB);
-  const size_t po = bound * Hkv * rows_pad * HD * 4;
+  const size_t po = bound * Hkv * rows_pad * HD * sizeof(uint16_t);
   uint8_t* ws = static_cast<uint8_t*>(workspace);
-  a.part_o = reinterpret_cast<float*>(ws);
+  a.part_o = reinterpret_cast<uint16_t*>(ws);
   a.part_ml = reinterpret_cast<float*>(ws + al256(po));
   // one instance per tile count among the bank's trees; those not made for
   // the device's tree leave at once

@@ -92,10 +92,10 @@ def test_noalloc_matches_workspace_entry_point(api):
 
 
 def test_noalloc_rejects_sizes_beyond_the_scratch(api):
-    # a 256-node tree at prefix 8192 with 32 heads: its workspace bound is
-    # larger than the static array, so the call returns ENOSPC on the host
-    # and launches nothing
-    T, L, H = 256, 8192, 32
+    # a 256-node tree at prefix 8192 with 64 heads: its workspace bound
+    # (132 MiB) is larger than the static array, so the call returns ENOSPC
+    # on the host and launches nothing
+    T, L, H = 256, 8192, 64
     parent = synth.uniform_attach_tree(9, T, 8)
     bank = api.Bank([parent])
     assert api.tree_attn_workspace(T, H, H, D, L) > api.NOALLOC_SCRATCH_BYTES
