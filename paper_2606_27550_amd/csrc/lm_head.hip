@@ -765,8 +765,15 @@ __global__ __launch_bounds__(64 * kFinNodes) void stats_finalize_kernel(
     float* __restrict__ top1p, int* __restrict__ argmax) {
   const int node = blockIdx.x * kFinNodes + (threadIdx.x >> 6);
   if (node >= T) return;   // whole wavefronts
-  StatPart a, b;
-  merge_rows_wave(part, node, -1, G, inv_temp, a, b);
+  // up to 2048 partials per row (a 128256-entry vocabulary writes 2004) in
+  // registers, 32 per lane, so the row's loads go out together
+  const int rows[1] = {node};
+  StatPart o[1];
+  if (G <= 64 * kMergeRegParts)
+    merge_rows<1>(part, rows, G, inv_temp, o);
+  else
+    merge_rows<1, 4 * kMergeRegParts>(part, rows, G, inv_temp, o);
+  const StatPart& a = o[0];
   if ((threadIdx.x & 63) == 0) {
     if (entropy) entropy[node] = part_entropy(a);
     if (top1p) top1p[node] = part_top1p(a);

@@ -57,8 +57,9 @@ __device__ __forceinline__ StatPart shfl_part(const StatPart& p, int off) {
 // partials l, l + 64, l + 128, ... in that order and a butterfly combines the
 // lanes, so the result does not depend on R or on the path below; every
 // kernel that finishes statistics merges this way and they agree bit for
-// bit.  Up to 512 partials per row the loads of all R rows are issued at
-// once and kept in registers (one round trip); longer rows are read twice.
+// bit.  Up to 64 P partials per row (512 by default) the loads of all R
+// rows are issued at once and kept in registers (one round trip); longer
+// rows are read twice.
 constexpr int kMergeRegParts = 8;   // partials per lane held in registers
 
 // (z, index) as one key whose unsigned order is take_max's order: larger z
