@@ -659,8 +659,10 @@ def run_batched(args, api, synth, torch, lib):
     concatenated rows, batched greedy acceptance and compaction; then the
     host reads every sequence's (accept length, s) and moves each sequence's
     ladder.  The hidden rows of a step are gathered from a staged pool per
-    sequence (the model would hand them over contiguous), the draft tokens
-    written from pinned memory."""
+    sequence (the model would hand them over contiguous); the draft tokens
+    of every (step, sequence, tree) are drawn before the timed region and a
+    step's are written from pinned memory; the attention is issued first, as
+    it needs neither."""
     dev = torch.device("cuda:0")
     wl = synth.WORKLOADS["batch8_gqa_v128k"]
     B, Hq, Hkv, d, hid, V = 8, wl.n_heads, wl.n_kv_heads, wl.head_dim, wl.hidden, wl.vocab
@@ -716,6 +718,26 @@ def run_batched(args, api, synth, torch, lib):
     parents = [np.asarray(t, np.int64) for t in trees]
     u_tab = g_np.random((total, rows_max))
     r_tab = g_np.integers(0, V, (total, rows_max)).astype(np.int32)
+    # draft tokens of every (step, sequence, tree) and the hidden-row indices
+    # of every (sequence, tree), drawn before the timed region (the drafter's
+    # output is an input of the step): node i of sequence b takes the
+    # target's argmax at its parent with probability p_acc, else a random
+    # token (draws from the sequence's slot b * Tmax ..)
+    tok_pre = []
+    for t in range(total):
+        per_b = []
+        for b in range(B):
+            am_b = pool[t % P]["am"][b]
+            u, r = u_tab[t, b * Tmax:(b + 1) * Tmax], r_tab[t, b * Tmax:(b + 1) * Tmax]
+            per_k = []
+            for k, par in enumerate(parents):
+                T = Ts[k]
+                tk = np.where(u[:T] < wl.p_acc, am_b[np.maximum(par, 0)], r[:T]).astype(np.int32)
+                tk[0] = -1
+                per_k.append(tk)
+            per_b.append(per_k)
+        tok_pre.append(per_b)
+    idx_pre = [[b * Tmax + np.arange(Ts[k], dtype=np.int64) for k in range(n_topo)] for b in range(B)]
     log(f"batched workload: B={B}, bank T={Ts}, prefix {lens0.min()}..{lens0.max()}, cap={cap}; "
         f"staged in {time.time() - t0:.1f}s")
 
@@ -747,25 +769,15 @@ def run_batched(args, api, synth, torch, lib):
     def step(t, timed_lm):
         e = pool[t % P]
         topo = [int(k) for k in rung]
-        offs = np.concatenate([[0], np.cumsum([Ts[k] for k in topo])])
-        R = int(offs[-1])
+        R = sum(Ts[k] for k in topo)
         # draft tokens and the hidden-row gather for this batch layout
-        tok = tok_h.numpy()
-        idx = idx_h.numpy()
-        for b, k in enumerate(topo):
-            o, T = int(offs[b]), Ts[k]
-            par = parents[k]
-            am_b = e["am"][b]
-            u, r = u_tab[t, o:o + T], r_tab[t, o:o + T]
-            tk = np.where(u < wl.p_acc, am_b[np.maximum(par, 0)], r)
-            tk[0] = -1
-            tok[o:o + T] = tk
-            idx[o:o + T] = b * Tmax + np.arange(T)
+        tok_h.numpy()[:R] = np.concatenate([tok_pre[t][b][k] for b, k in enumerate(topo)])
+        idx_h.numpy()[:R] = np.concatenate([idx_pre[b][k] for b, k in enumerate(topo)])
+        api.tree_attn_batched(bank, topo, lens.tolist(), e["q"][:R], e["kt"][:R], e["vt"][:R], kcs,
+                              vcs, scale, theta, out[:R], aws)
         tok_d[:R].copy_(tok_h[:R], non_blocking=True)
         idx_d[:R].copy_(idx_h[:R], non_blocking=True)
         x = e["x_all"].index_select(0, idx_d[:R])
-        api.tree_attn_batched(bank, topo, lens.tolist(), e["q"][:R], e["kt"][:R], e["vt"][:R], kcs,
-                              vcs, scale, theta, out[:R], aws)
         if timed_lm:
             ev_lm[0].record()
         rc = lib.entmtp_verify_logits_partials(P_(x.data_ptr()), P_(W.data_ptr()), R, hid, V, 1.0, None,
