@@ -944,7 +944,7 @@ def lm_head_traffic(Ts, on_gpu=False):
             # 2); an unpaired launch of the entry points must not stand in
             if key in per and len(targs) > 4 and targs[4] != "2":
                 continue
-        elif kernel == "lm_head_gemm_kernel" and targs[-1] == "true":   # <BM, BN, NST, STATS>
+        elif kernel == "lm_head_gemm_kernel" and targs[-1] == "true":   # <BM, BN, NW, NST, STATS>
             key = (kernel, 0)
         elif kernel in ("lm_head_dyn_small_kernel", "lm_head_dyn_large_kernel"):
             key = (kernel, 0)
