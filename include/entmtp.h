@@ -217,6 +217,44 @@ int32_t entmtp_tree_attn_batched(const entmtp_bank* bank, int32_t B, const int32
                                  float rope_theta, entmtp_bf16* out, void* workspace,
                                  size_t workspace_bytes, void* stream);
 
+/*
+ * Batched form with the per-sequence choices in DEVICE memory (the
+ * per-sequence tree choice of §4 made on the GPU, or by a caller that keeps
+ * its schedule there): topo[B], prefix_len[B] and row_off[B + 1] are device
+ * int32 arrays read by the kernels, so the call never waits for them;
+ * sequence b's tree rows are rows row_off[b] .. row_off[b] + T - 1 of q /
+ * k_tree / v_tree / out (T = its tree's size; they must lie in
+ * [row_off[b], row_off[b + 1]), so sequences may leave gaps), which hold
+ * rows_cap rows.  k_caches / v_caches are HOST
+ * arrays of B device pointers, each [Hkv][cap][d] bf16.  Each sequence is
+ * computed exactly as entmtp_tree_attn_batched computes it for the same
+ * trees and prefix lengths (the kernels derive the same plan).  The grids
+ * are sized on the host for the bank's largest plan (trees up to the
+ * bank's largest, prefix lengths up to cap - T).  A sequence whose topo[b]
+ * lies outside the bank, whose prefix_len[b] is negative or leaves fewer
+ * than T free cache slots, or whose tree rows do not lie in [row_off[b],
+ * row_off[b + 1]) and rows_cap computes nothing (its out rows and cache are
+ * left as they were); the host cannot see device values, so that is not an
+ * error.
+ *   workspace  device scratch of at least
+ *              entmtp_tree_attn_batched_device_workspace(bank, B, Hq, Hkv, d,
+ *              cap) bytes (0 for invalid arguments).
+ * Requirements: the bank names at most 32 trees; otherwise as
+ * entmtp_tree_attn_batched.
+ * Errors (host-checked): EINVAL, ERANGE, ENOSPC, EHIP.
+ */
+size_t entmtp_tree_attn_batched_device_workspace(const entmtp_bank* bank, int32_t B, int32_t Hq,
+                                                 int32_t Hkv, int32_t d, int32_t cap);
+int32_t entmtp_tree_attn_batched_device(const entmtp_bank* bank, int32_t B, const int32_t* topo,
+                                        const int32_t* prefix_len, const int32_t* row_off,
+                                        int32_t rows_cap, const entmtp_bf16* q,
+                                        const entmtp_bf16* k_tree, const entmtp_bf16* v_tree,
+                                        entmtp_bf16* const* k_caches,
+                                        entmtp_bf16* const* v_caches, int32_t cap, int32_t Hq,
+                                        int32_t Hkv, int32_t d, float scale, float rope_theta,
+                                        entmtp_bf16* out, void* workspace,
+                                        size_t workspace_bytes, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* LM-head verification logits (§2.2: next-token distribution softmax(W h);  */
 /* §2.3: one verification pass for all tree nodes).                           */
@@ -366,6 +404,27 @@ int32_t entmtp_accept_batched(const entmtp_bank* bank, int32_t B, const int32_t*
                               int32_t path_capacity, int32_t* bonus, float* best_top1p,
                               void* stream);
 
+/*
+ * Batched form with the trees and rows in DEVICE memory: topo[B] and
+ * row_off[B + 1] are device int32 arrays; sequence b's rows of draft_tokens,
+ * argmax and top1p are row_off[b] .. row_off[b] + T - 1 (within
+ * [row_off[b], row_off[b + 1]) and the rows_cap rows they hold).  Outputs as
+ * entmtp_accept_batched (equal for the same trees and rows).  A sequence
+ * whose topo[b] lies outside the bank, whose tree rows do not lie in
+ * [row_off[b], row_off[b + 1]) and rows_cap, or whose tree's depth + 1
+ * exceeds path_capacity is not verified: accept_len[b] = -1, bonus[b] = -1,
+ * its path row -1 and best_top1p[b] = 0 (entmtp_kv_compact_batched_device
+ * then moves nothing for it).
+ * Requirements: the bank names at most 32 trees, 1 <= path_capacity <= 256.
+ * Errors (host-checked): EINVAL, ERANGE, EHIP.
+ */
+int32_t entmtp_accept_batched_device(const entmtp_bank* bank, int32_t B, const int32_t* topo,
+                                     const int32_t* row_off, int32_t rows_cap,
+                                     const int32_t* draft_tokens, const int32_t* argmax,
+                                     const float* top1p, int32_t* accept_len, int32_t* path,
+                                     int32_t path_capacity, int32_t* bonus, float* best_top1p,
+                                     void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* KV-cache update of the accepted path (§3.2 decode loop).                   */
 /* ------------------------------------------------------------------------ */
@@ -406,6 +465,20 @@ int32_t entmtp_kv_compact_batched(int32_t B, const int32_t* path, int32_t path_c
                                   entmtp_bf16* const* k_caches, entmtp_bf16* const* v_caches,
                                   int32_t n_layers, int64_t layer_stride, int32_t Hkv,
                                   int32_t cap, int32_t d, void* stream);
+
+/*
+ * Batched form with the prefix lengths in DEVICE memory: prefix_len[B] is a
+ * device int32 array (k_caches / v_caches stay HOST arrays of device
+ * pointers); otherwise as entmtp_kv_compact_batched.  A sequence whose
+ * prefix_len[b] is negative is left unchanged.
+ * Errors (host-checked): EINVAL, EHIP.
+ */
+int32_t entmtp_kv_compact_batched_device(int32_t B, const int32_t* path, int32_t path_capacity,
+                                         const int32_t* accept_len, const int32_t* prefix_len,
+                                         entmtp_bf16* const* k_caches,
+                                         entmtp_bf16* const* v_caches, int32_t n_layers,
+                                         int64_t layer_stride, int32_t Hkv, int32_t cap,
+                                         int32_t d, void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Scheduler policy (§4 "Policy"), host only.                                 */

@@ -55,10 +55,18 @@ _SIGNATURES = {
     "entmtp_tree_attn_batched": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p,
                                           _c_i32, _c_i32, _c_i32, _c_i32, _c_f32, _c_f32, _c_p, _c_p,
                                           _c_sz, _c_p]),
+    "entmtp_tree_attn_batched_device_workspace": (_c_sz, [_c_p] + [_c_i32] * 5),
+    "entmtp_tree_attn_batched_device": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_i32, _c_p, _c_p,
+                                                 _c_p, _c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_i32,
+                                                 _c_f32, _c_f32, _c_p, _c_p, _c_sz, _c_p]),
     "entmtp_accept_batched": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_p, _c_p, _c_i32,
                                        _c_p, _c_p, _c_p]),
+    "entmtp_accept_batched_device": (_c_i32, [_c_p, _c_i32, _c_p, _c_p, _c_i32, _c_p, _c_p, _c_p,
+                                              _c_p, _c_p, _c_i32, _c_p, _c_p, _c_p]),
     "entmtp_kv_compact_batched": (_c_i32, [_c_i32, _c_p, _c_i32, _c_p, _c_p, _c_p, _c_p, _c_i32,
                                            _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
+    "entmtp_kv_compact_batched_device": (_c_i32, [_c_i32, _c_p, _c_i32, _c_p, _c_p, _c_p, _c_p,
+                                                  _c_i32, _c_i64, _c_i32, _c_i32, _c_i32, _c_p]),
     "entmtp_verify_logits": (_c_i32, [_c_p, _c_p, _c_i32, _c_i32, _c_i32, _c_p, _c_p]),
     "entmtp_logit_stats": (_c_i32, [_c_p, _c_i32, _c_i32, _c_f32, _c_p, _c_p, _c_p, _c_p]),
     "entmtp_verify_logits_stats_workspace": (_c_sz, [_c_i32, _c_i32, _c_i32]),
@@ -350,6 +358,92 @@ def tree_attn_batched(bank: Bank, topo, prefix_len, q, k_tree, v_tree, k_caches,
                                         vp, cap, Hq, Hkv, d, scale, rope_theta, _p(out),
                                         _p(workspace), workspace.numel() * workspace.element_size(),
                                         _stream(stream)))
+
+
+def tree_attn_batched_device_workspace(bank: Bank, B: int, Hq: int, Hkv: int, d: int,
+                                       cap: int) -> int:
+    return int(lib.entmtp_tree_attn_batched_device_workspace(bank.handle, B, Hq, Hkv, d, cap))
+
+
+def tree_attn_batched_device(bank: Bank, topo, prefix_len, row_off, q, k_tree, v_tree, k_caches,
+                             v_caches, scale: float, rope_theta: float, out, workspace,
+                             stream=None) -> None:
+    """topo [B], prefix_len [B] and row_off [B+1]: int32 GPU tensors read by
+    the kernels; q / k_tree / v_tree / out hold rows_cap = q.shape[0] rows;
+    one [Hkv,cap,d] cache pair per sequence."""
+    import torch
+    B = len(k_caches)
+    _need(1 <= B <= B_MAX and len(v_caches) == B, "one cache pair per sequence")
+    _dev(topo, "topo", torch.int32, min_numel=B)
+    _dev(prefix_len, "prefix_len", torch.int32, min_numel=B)
+    _dev(row_off, "row_off", torch.int32, min_numel=B + 1)
+    rows, Hq, d = q.shape
+    Hkv = k_tree.shape[1]
+    _dev(q, "q", torch.bfloat16, (rows, Hq, d))
+    _dev(k_tree, "k_tree", torch.bfloat16, (rows, Hkv, d))
+    _dev(v_tree, "v_tree", torch.bfloat16, (rows, Hkv, d))
+    _dev(out, "out", torch.bfloat16, (rows, Hq, d))
+    cap = k_caches[0].shape[1]
+    for kc, vc in zip(k_caches, v_caches):
+        _dev(kc, "k_cache", torch.bfloat16, (Hkv, cap, d))
+        _dev(vc, "v_cache", torch.bfloat16, (Hkv, cap, d))
+    _need(workspace.is_cuda and workspace.is_contiguous(), "workspace must be a contiguous GPU tensor")
+    kp, vp = _host_ptrs(k_caches), _host_ptrs(v_caches)
+    _check(lib.entmtp_tree_attn_batched_device(bank.handle, B, _p(topo), _p(prefix_len), _p(row_off),
+                                               rows, _p(q), _p(k_tree), _p(v_tree), kp, vp, cap, Hq,
+                                               Hkv, d, scale, rope_theta, _p(out), _p(workspace),
+                                               workspace.numel() * workspace.element_size(),
+                                               _stream(stream)))
+
+
+def accept_batched_device(bank: Bank, topo, row_off, draft_tokens, argmax, top1p, accept_len, path,
+                          bonus, best_top1p=None, stream=None) -> None:
+    """topo [B] and row_off [B+1]: int32 GPU tensors; the per-node arrays hold
+    rows_cap = draft_tokens.numel() rows; path is [B, path_capacity]."""
+    import torch
+    B = path.shape[0] if path.dim() == 2 else 0
+    _need(1 <= B <= B_MAX, "path is [B, path_capacity] with 1 <= B <= 16")
+    _dev(topo, "topo", torch.int32, min_numel=B)
+    _dev(row_off, "row_off", torch.int32, min_numel=B + 1)
+    _dev(draft_tokens, "draft_tokens", torch.int32)
+    rows = draft_tokens.numel()
+    _dev(argmax, "argmax", torch.int32, min_numel=rows)
+    if top1p is not None:
+        _dev(top1p, "top1p", torch.float32, min_numel=rows)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=B)
+    _dev(bonus, "bonus", torch.int32, min_numel=B)
+    if best_top1p is not None:
+        _dev(best_top1p, "best_top1p", torch.float32, min_numel=B)
+    _dev(path, "path", torch.int32)
+    _check(lib.entmtp_accept_batched_device(bank.handle, B, _p(topo), _p(row_off), rows,
+                                            _p(draft_tokens), _p(argmax), _p(top1p), _p(accept_len),
+                                            _p(path), path.shape[1], _p(bonus), _p(best_top1p),
+                                            _stream(stream)))
+
+
+def kv_compact_batched_device(path, accept_len, prefix_len, k_caches, v_caches,
+                              stream=None) -> None:
+    """As kv_compact_batched with prefix_len [B] an int32 GPU tensor."""
+    import torch
+    B = len(k_caches)
+    _need(1 <= B <= B_MAX and len(v_caches) == B, "one cache pair per sequence")
+    _need(path.dim() == 2 and path.shape[0] == B, "path is [B, path_capacity]")
+    _dev(path, "path", torch.int32)
+    _dev(accept_len, "accept_len", torch.int32, min_numel=B)
+    _dev(prefix_len, "prefix_len", torch.int32, min_numel=B)
+    shape = k_caches[0].shape
+    for kc, vc in zip(k_caches, v_caches):
+        _need(kc.shape == shape and vc.shape == shape, "caches of equal shapes")
+        _dev(kc, "k_cache", torch.bfloat16)
+        _dev(vc, "v_cache", torch.bfloat16)
+    if len(shape) == 3:
+        n_layers, (Hkv, cap, d) = 1, shape
+    else:
+        n_layers, Hkv, cap, d = shape
+    kp, vp = _host_ptrs(k_caches), _host_ptrs(v_caches)
+    _check(lib.entmtp_kv_compact_batched_device(B, _p(path), path.shape[1], _p(accept_len),
+                                                _p(prefix_len), kp, vp, n_layers, Hkv * cap * d,
+                                                Hkv, cap, d, _stream(stream)))
 
 
 def accept_batched(bank: Bank, topo, draft_tokens, argmax, top1p, accept_len, path, bonus,

@@ -86,6 +86,54 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_batched_kernel(AcceptBa
               p.best ? p.best + b : nullptr, nullptr, 0u);
 }
 
+// A batch whose trees and rows are device arrays (topo[b], row_off[b]):
+// every bank tree's arrays travel in the kernel arguments.
+constexpr int kMaxTreesAccept = 32;
+struct AcceptBatchDev {
+  AcceptSeq trees[kMaxTreesAccept];   // row0 unused
+  const int* topo;
+  const int* row_off;                 // [B + 1]
+  int rows_cap, n_trees;
+  const int* tok;
+  const int* amax;
+  const float* top1p;
+  int* accept_len;
+  int* path;
+  int path_cap;
+  int* bonus;
+  float* best;
+};
+
+static_assert(sizeof(AcceptBatchDev) <= 4096, "kernel arguments are limited to 4 KB");
+
+// Workgroup b accepts sequence b's tree.  A sequence whose tree index lies
+// outside the bank, whose tree rows [row_off[b], row_off[b] + T) do not lie
+// in [row_off[b], row_off[b + 1]) and the row capacity, or whose tree is
+// deeper than the path rows hold is not verified: accept length -1, path and
+// bonus -1 (compaction then moves nothing).
+__global__ __launch_bounds__(kAcceptThreads) void accept_batched_device_kernel(AcceptBatchDev p) {
+  const int b = blockIdx.x;
+  const int tr = p.topo[b], r0 = p.row_off[b], r1 = p.row_off[b + 1];
+  const bool named = tr >= 0 && tr < p.n_trees;
+  const int T = p.trees[named ? tr : 0].T;
+  const bool ok = named && r0 >= 0 && r0 + T <= r1 && r0 + T <= p.rows_cap &&
+                  p.trees[named ? tr : 0].D + 1 <= p.path_cap;
+  int* path = p.path + static_cast<size_t>(b) * p.path_cap;
+  if (!ok) {
+    for (int i = threadIdx.x; i < p.path_cap; i += blockDim.x) path[i] = -1;
+    if (threadIdx.x == 0) {
+      p.accept_len[b] = -1;
+      p.bonus[b] = -1;
+      if (p.best) p.best[b] = 0.f;
+    }
+    return;
+  }
+  const AcceptSeq& q = p.trees[tr];
+  accept_core(q.parent, q.depth, q.mask, q.path_tab, q.T, q.D, p.tok + r0, p.amax + r0,
+              p.top1p ? p.top1p + r0 : nullptr, p.accept_len + b, path, p.path_cap, p.bonus + b,
+              p.best ? p.best + b : nullptr, nullptr, 0u);
+}
+
 // Statistics of every node of the tree from the LM head's partials, then the
 // acceptance of the tree, by one workgroup of kFinAccThreads threads.
 __global__ __launch_bounds__(kFinAccThreads) void finalize_accept_kernel(
@@ -420,6 +468,52 @@ extern "C" int32_t entmtp_accept_batched(const entmtp_bank* bank, int32_t B, con
   hipLaunchKernelGGL(accept_batched_kernel, dim3(B), dim3(kAcceptThreads), 0,
                      static_cast<hipStream_t>(stream), a);
   return launch_status("accept_batched launch");
+}
+
+extern "C" int32_t entmtp_accept_batched_device(const entmtp_bank* bank, int32_t B,
+                                                const int32_t* topo, const int32_t* row_off,
+                                                int32_t rows_cap, const int32_t* draft_tokens,
+                                                const int32_t* argmax, const float* top1p,
+                                                int32_t* accept_len, int32_t* path,
+                                                int32_t path_capacity, int32_t* bonus,
+                                                float* best_top1p, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(B >= 1 && B <= ENTMTP_B_MAX, ENTMTP_EINVAL, "B = %d outside [1, %d]", B,
+                   ENTMTP_B_MAX);
+  if (int32_t rc = check_device_bank(bank, 0)) return rc;
+  ENTMTP_CHECK_ARG(static_cast<int>(bank->desc.size()) <= kMaxTreesAccept, ENTMTP_ERANGE,
+                   "a device-planned batch names at most %d bank trees (bank has %zu)",
+                   kMaxTreesAccept, bank->desc.size());
+  ENTMTP_CHECK_ARG(topo && row_off, ENTMTP_EINVAL, "topo and row_off must be non-NULL device arrays");
+  ENTMTP_CHECK_ARG(rows_cap >= 1, ENTMTP_EINVAL, "rows_cap = %d < 1", rows_cap);
+  ENTMTP_CHECK_ARG(draft_tokens && argmax && accept_len && path && bonus, ENTMTP_EINVAL,
+                   "draft_tokens, argmax, accept_len, path and bonus must be non-NULL");
+  ENTMTP_CHECK_ARG(best_top1p == nullptr || top1p != nullptr, ENTMTP_EINVAL,
+                   "best_top1p needs top1p");
+  ENTMTP_CHECK_ARG(path_capacity >= 1 && path_capacity <= kAcceptThreads, ENTMTP_EINVAL,
+                   "path_capacity = %d outside [1, %d]", path_capacity, kAcceptThreads);
+  AcceptBatchDev a;
+  a.n_trees = static_cast<int>(bank->desc.size());
+  for (int k = 0; k < a.n_trees; ++k) {
+    const TopoDesc& d = bank->desc[k];
+    a.trees[k] = AcceptSeq{bank_ptr<int>(bank, d.off_parent), bank_ptr<int>(bank, d.off_depth),
+                           bank_ptr<uint32_t>(bank, d.off_mask), bank_ptr<int>(bank, d.off_path),
+                           d.T, d.D, 0};
+  }
+  a.topo = topo;
+  a.row_off = row_off;
+  a.rows_cap = rows_cap;
+  a.tok = draft_tokens;
+  a.amax = argmax;
+  a.top1p = top1p;
+  a.accept_len = accept_len;
+  a.path = path;
+  a.path_cap = path_capacity;
+  a.bonus = bonus;
+  a.best = best_top1p;
+  hipLaunchKernelGGL(accept_batched_device_kernel, dim3(B), dim3(kAcceptThreads), 0,
+                     static_cast<hipStream_t>(stream), a);
+  return launch_status("accept_batched (device arrays) launch");
 }
 
 extern "C" int32_t entmtp_draft_logits(const entmtp_bank* bank, int32_t topo,

@@ -25,6 +25,7 @@ struct CompactArgs {
   const int* path;       // [B][path_cap]
   const int* accept_len; // [B]
   const DevStep* dev;    // when set, sequence 0's prefix length is dev->L
+  const int* L_dev;      // when set, sequence b's prefix length is L_dev[b] (device)
   long long layer_stride;
   int path_cap, n_layers, Hkv, cap, d;
   int by_value;          // 1: one sequence whose path and accept length are below
@@ -37,7 +38,8 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs
   const int per_seq = p.n_layers * p.Hkv;
   const int b = blockIdx.x / per_seq, rest = blockIdx.x % per_seq;
   const int layer = rest / p.Hkv, g = rest % p.Hkv;
-  const int d = p.d, cap = p.cap, L = p.dev ? p.dev->L : p.L[b];
+  const int d = p.d, cap = p.cap, L = p.dev ? p.dev->L : (p.L_dev ? p.L_dev[b] : p.L[b]);
+  if (L < 0) return;   // (a device-held prefix length the host could not check)
   const int* path = p.path + static_cast<size_t>(b) * p.path_cap;
   const size_t base = static_cast<size_t>(layer) * p.layer_stride + static_cast<size_t>(g) * cap * d;
   int a = p.by_value ? p.a_v : p.accept_len[b];
@@ -199,6 +201,42 @@ extern "C" int32_t entmtp_kv_compact_batched(int32_t B, const int32_t* path, int
     a.vc[b] = v_caches[b];
     a.L[b] = prefix_len[b];
   }
+  a.path = path;
+  a.accept_len = accept_len;
+  a.layer_stride = static_cast<long long>(layer_stride);
+  a.path_cap = path_capacity;
+  a.n_layers = n_layers;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  a.d = d;
+  return launch_compact(a, B, static_cast<hipStream_t>(stream));
+}
+
+extern "C" int32_t entmtp_kv_compact_batched_device(int32_t B, const int32_t* path,
+                                                    int32_t path_capacity,
+                                                    const int32_t* accept_len,
+                                                    const int32_t* prefix_len,
+                                                    entmtp_bf16* const* k_caches,
+                                                    entmtp_bf16* const* v_caches,
+                                                    int32_t n_layers, int64_t layer_stride,
+                                                    int32_t Hkv, int32_t cap, int32_t d,
+                                                    void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(B >= 1 && B <= ENTMTP_B_MAX, ENTMTP_EINVAL, "B = %d outside [1, %d]", B,
+                   ENTMTP_B_MAX);
+  ENTMTP_CHECK_ARG(path && accept_len && prefix_len, ENTMTP_EINVAL,
+                   "path, accept_len and prefix_len must be non-NULL device arrays");
+  ENTMTP_CHECK_ARG(k_caches && v_caches, ENTMTP_EINVAL,
+                   "k_caches and v_caches must be non-NULL host arrays");
+  if (int32_t rc = check_shape(path_capacity, n_layers, layer_stride, Hkv, cap, d)) return rc;
+  CompactArgs a{};
+  for (int b = 0; b < B; ++b) {
+    ENTMTP_CHECK_ARG(k_caches[b] && v_caches[b] && aligned16(k_caches[b]) && aligned16(v_caches[b]),
+                     ENTMTP_EINVAL, "sequence %d: caches must be non-NULL and 16-byte aligned", b);
+    a.kc[b] = k_caches[b];
+    a.vc[b] = v_caches[b];
+  }
+  a.L_dev = prefix_len;
   a.path = path;
   a.accept_len = accept_len;
   a.layer_stride = static_cast<long long>(layer_stride);

@@ -117,13 +117,31 @@ struct SeqPlan {
   int T, L, row0;          // nodes, prefix length, first row in the concatenated q / out
   int D;                   // depth of the tree's deepest node
   int rows_pad, nqt, nqg, nsplit, bps;   // padded rows, query tiles, query groups, splits
+  int nt;                  // query tiles per workgroup the call's plan gives it
   int item0;               // first attend workgroup of the sequence
   int merge0;              // first merge block of the sequence
   long long part_off;      // row offset of its split partials
 };
 
+// A bank tree as a device-planned batch finds it (kernel arguments).
+struct TreeHdr {
+  int T, D, off_mask, off_depth;
+};
+constexpr int kMaxTreesArg = 32;   // bank trees a device-planned batch can name
+
 struct BatchArgs {
   SeqPlan s[kMaxSeqs];
+  // device-planned batch: sequence b's tree, prefix length and first row
+  // come from device arrays (topo_dev[b], len_dev[b], row_off_dev[b]); the
+  // host fixed its caches and its grid, merge and partial ranges (at strides
+  // sized for the bank's largest plan), and every workgroup derives the
+  // plan the host would have made (plan_call) from those arrays
+  const int32_t* topo_dev;
+  const int32_t* len_dev;
+  const int32_t* row_off_dev;   // [B + 1]
+  int rows_cap;                 // rows q / k_tree / v_tree / out hold
+  int n_trees;
+  TreeHdr trees[kMaxTreesArg];
   // device-planned single sequence (a tree chosen on the GPU): when dev is
   // set, sequence 0's tree, prefix length and split plan come from *dev, the
   // bank descriptors and the CU count, and the grids are sized for the
@@ -187,6 +205,78 @@ __device__ __forceinline__ SeqPlan resolve(const BatchArgs& p, int b) {
   q.item0 = 0;
   q.merge0 = 0;
   q.part_off = 0;
+  return q;
+}
+
+// Plan of sequence b of a device-planned batch.  Lane i of each wavefront
+// reads sequence i's entries; a sequence whose tree index lies outside the
+// bank, whose prefix length is negative or leaves no room for its tree in
+// the cache, or whose tree rows [row_off[b], row_off[b] + T) do not lie in
+// [row_off[b], row_off[b + 1]) and the row capacity has no work (T = 0) and
+// counts for nothing in the batch plan.
+// The rest is plan_call's arithmetic: the batch's tile count is the largest
+// any sequence needs, and a batch of several shares one blocks-per-split
+// target.  Called by whole wavefronts.
+__device__ __forceinline__ SeqPlan resolve_batch(const BatchArgs& p, int b) {
+  SeqPlan q = p.s[b];   // caches and the fixed ranges
+  const int lane = threadIdx.x & 63;
+  int tr = -1, L = -1, r0 = -1, r1 = -1;
+  if (lane < p.B) {
+    tr = p.topo_dev[lane];
+    L = p.len_dev[lane];
+    r0 = p.row_off_dev[lane];
+    r1 = p.row_off_dev[lane + 1];
+  }
+  const bool named = lane < p.B && tr >= 0 && tr < p.n_trees;
+  int T = 0;
+  if (named) T = p.trees[tr].T;   // only lanes holding a bank index read the table
+  const bool ok = named && L >= 0 && static_cast<long long>(L) + T <= p.cap && r0 >= 0 &&
+                  r0 + T <= r1 && r0 + T <= p.rows_cap;
+  if (!ok) T = 0;
+  const int nblocks = T ? (L + T + KB - 1) / KB : 0;
+  int nt = T ? tree_tiles(p.G, T) : 1;
+  long long work = T ? static_cast<long long>(p.Hkv) * (rows_padded(p.G, T) / kQTile) * nblocks : 0;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) {
+    nt = max(nt, __shfl_xor(nt, off, 64));
+    work += __shfl_xor(work, off, 64);
+  }
+  const int Tb = __shfl(T, b, 64);
+  if (Tb == 0) {
+    q.T = 0;
+    q.L = 0;
+    q.nsplit = 1;
+    q.nqt = 0;
+    q.nqg = 0;
+    q.nt = nt;
+    return q;
+  }
+  const int trb = __shfl(tr, b, 64);
+  const TreeHdr& h = p.trees[trb];
+  q.T = Tb;
+  q.L = __shfl(L, b, 64);
+  q.row0 = __shfl(r0, b, 64);
+  q.D = h.D;
+  q.mask = reinterpret_cast<const uint32_t*>(p.arena + h.off_mask);
+  q.depth = reinterpret_cast<const int*>(p.arena + h.off_depth);
+  q.nt = nt;
+  q.rows_pad = rows_padded(p.G, q.T);
+  q.nqt = q.rows_pad / kQTile;
+  q.nqg = query_groups(q.nqt, nt);
+  const int nb = (q.L + q.T + KB - 1) / KB;
+  int ns;
+  if (p.B == 1) {
+    ns = split_single(nb, p.Hkv * q.nqg, p.cus * wg_per_cu(nt));
+  } else {
+    work = (work + nt - 1) / nt;
+    const long long per_wg = (work + 4LL * p.cus - 1) / (4LL * p.cus);
+    const int target_bps = static_cast<int>(per_wg > kMinBlocksPerSplit ? per_wg : kMinBlocksPerSplit);
+    ns = (nb + target_bps - 1) / target_bps;
+    const int bound = split_bound(nb);
+    ns = ns < 1 ? 1 : (ns > bound ? bound : ns);
+  }
+  q.bps = (nb + ns - 1) / ns;
+  q.nsplit = (nb + q.bps - 1) / q.bps;
   return q;
 }
 
@@ -302,6 +392,9 @@ __device__ __forceinline__ void wave_lds_sync() {
 
 // One query tile per workgroup (trees of up to 32 query rows per KV head);
 // the per-tile state below is written for NT tiles held by every wave.
+// DEVB: a device-planned batch (its own instantiation, so the host-planned
+// and single device-planned forms keep their registers).
+template <bool DEVB>
 __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   constexpr int NT = 1;
   // blockIdx -> sequence, then (kv head, split) group and query-tile group;
@@ -309,9 +402,9 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
   // round-robin over 8 XCDs and every sequence's range starts at a multiple
   // of 8), so their K/V reads share that XCD's L2.
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
-  const SeqPlan sq = resolve(p, b);
+  const SeqPlan sq = DEVB ? resolve_batch(p, b) : resolve(p, b);
   if (sq.T == 0) return;
-  if (p.dev && tree_tiles(p.G, sq.T) != NT) return;   // the device's tree is the other kernel's
+  if (DEVB ? sq.nt != NT : (p.dev && tree_tiles(p.G, sq.T) != NT)) return;   // another instance's
   const int bid = blockIdx.x - sq.item0;
   const int qg = (bid >> 3) % sq.nqg;
   const int gc = ((bid >> 3) / sq.nqg) * 8 + (bid & 7);
@@ -735,11 +828,12 @@ __global__ __launch_bounds__(kAttnThreads) void tree_attn_kernel(BatchArgs p) {
 // softmax state and output, so no cross-wave merge is needed.
 constexpr int KROW = HD + 8;   // bf16 per staged K row (16-byte pad: rows 4 banks apart)
 
+template <bool DEVB>
 __global__ __launch_bounds__(kAttnThreads, 2) void tree_attn_q4_kernel(BatchArgs p) {
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.item0; });
-  const SeqPlan sq = resolve(p, b);
+  const SeqPlan sq = DEVB ? resolve_batch(p, b) : resolve(p, b);
   if (sq.T == 0) return;
-  if (p.dev && tree_tiles(p.G, sq.T) != 4) return;   // the device's tree is another instance's
+  if (DEVB ? sq.nt != 4 : (p.dev && tree_tiles(p.G, sq.T) != 4)) return;   // another instance's
   const int bid = blockIdx.x - sq.item0;
   const int qg = (bid >> 3) % sq.nqg;
   const int gc = ((bid >> 3) / sq.nqg) * 8 + (bid & 7);
@@ -1049,9 +1143,10 @@ constexpr int kMergeBatch = 16;   // splits whose partials are requested togethe
 constexpr int kMergeThreads = 32 * kMergeRows;
 static_assert(kMaxSplits <= 32, "a half-wavefront holds one lane per split");
 
+template <bool DEVB>
 __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) {
   const int b = seq_of(p, static_cast<int>(blockIdx.x), [](const SeqPlan& q) { return q.merge0; });
-  const SeqPlan sq = resolve(p, b);
+  const SeqPlan sq = DEVB ? resolve_batch(p, b) : resolve(p, b);
   if (sq.nsplit == 1 || sq.T == 0) return;   // written by the attend kernel, or nothing to do
   const int GT = p.G * sq.T;
   const int local = (blockIdx.x - sq.merge0) * kMergeRows + (threadIdx.x >> 5);
@@ -1114,11 +1209,12 @@ __global__ __launch_bounds__(kMergeThreads) void attn_merge_kernel(BatchArgs p) 
 size_t al256(size_t x) { return (x + 255) & ~size_t(255); }
 
 // lds: bytes of the rotation table (rope_lds_bytes of the deepest tree)
+template <bool DEVB = false>
 void launch_attend(const BatchArgs& a, int items, size_t lds, hipStream_t s) {
   if (a.nt == 4)
-    hipLaunchKernelGGL(tree_attn_q4_kernel, dim3(items), dim3(kAttnThreads), lds, s, a);
+    hipLaunchKernelGGL(tree_attn_q4_kernel<DEVB>, dim3(items), dim3(kAttnThreads), lds, s, a);
   else
-    hipLaunchKernelGGL(tree_attn_kernel, dim3(items), dim3(kAttnThreads), lds, s, a);
+    hipLaunchKernelGGL(tree_attn_kernel<DEVB>, dim3(items), dim3(kAttnThreads), lds, s, a);
 }
 
 
@@ -1154,6 +1250,9 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
   a.dev = nullptr;
   a.topos = nullptr;
   a.arena = nullptr;
+  a.topo_dev = nullptr;
+  a.len_dev = nullptr;
+  a.row_off_dev = nullptr;
   a.B = B;
   a.G = Hq / Hkv;
   a.Hq = Hq;
@@ -1190,6 +1289,7 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
     q.rows_pad = rows_padded(a.G, q.T);
     q.nqt = q.rows_pad / kQTile;
     q.nqg = query_groups(q.nqt, a.nt);
+    q.nt = a.nt;
     const int nblocks = (q.L + q.T + KB - 1) / KB;
     int ns;
     if (B == 1) {
@@ -1231,7 +1331,7 @@ int32_t launch_call(BatchArgs& a, const CallShape& sh, void* workspace, hipStrea
   launch_attend(a, sh.items, rope_lds_bytes(sh.D, a.theta), s);
   if (int32_t rc = launch_status("tree_attn launch")) return rc;
   if (sh.merge_blocks > 0) {
-    hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
+    hipLaunchKernelGGL(attn_merge_kernel<false>, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
     if (int32_t rc = launch_status("tree_attn merge launch")) return rc;
   }
   return ENTMTP_OK;
@@ -1357,8 +1457,43 @@ int32_t launch_attn_device(const entmtp_bank* bank, const DevStep* dev, const De
     launch_attend(a, sh.items[nt], rope_lds_bytes(sh.D_max, a.theta), s);
     if (int32_t rc = launch_status("tree_attn launch")) return rc;
   }
-  hipLaunchKernelGGL(attn_merge_kernel, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
+  hipLaunchKernelGGL(attn_merge_kernel<false>, dim3(sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
   return launch_status("tree_attn merge launch");
+}
+
+// Fixed per-sequence ranges of a device-planned batch: each sequence slot
+// gets the grid, merge blocks and partial rows of the largest plan any bank
+// tree can need at prefix lengths up to cap - T, for either tile count.
+struct BatchDevShape {
+  int items[5] = {0, 0, 0, 0, 0};   // attend workgroups per sequence, instance with 1 / 4 tiles
+  int merge_blocks = 0;             // merge blocks per sequence
+  long long part_rows = 0;          // partial rows per sequence
+  int D_max = 0;
+  size_t need = 0;                  // workspace bytes for B sequences
+};
+
+BatchDevShape batch_dev_shape(const entmtp_bank* bank, int B, int Hq, int Hkv, int cap) {
+  BatchDevShape sh;
+  const int G = Hq / Hkv;
+  const int bound = split_bound((cap + KB - 1) / KB);
+  int T_max = 0;
+  bool any_small = false;
+  for (const TopoDesc& td : bank->desc) {
+    T_max = td.T > T_max ? td.T : T_max;
+    sh.D_max = td.D > sh.D_max ? td.D : sh.D_max;
+    any_small = any_small || tree_tiles(G, td.T) == 1;
+    // the four-tile instance serves every tree (a batch takes its largest
+    // tile count); the one-tile instance only batches of small trees
+    const int nqt = rows_padded(G, td.T) / kQTile;
+    const int items4 = (Hkv * bound + 7) / 8 * 8 * query_groups(nqt, 4);
+    sh.items[4] = items4 > sh.items[4] ? items4 : sh.items[4];
+  }
+  if (any_small) sh.items[1] = (Hkv * bound + 7) / 8 * 8;
+  sh.merge_blocks = (Hkv * G * T_max + kMergeRows - 1) / kMergeRows;
+  sh.part_rows = static_cast<long long>(bound) * Hkv * rows_padded(G, T_max);
+  const size_t rows = static_cast<size_t>(B) * sh.part_rows;
+  sh.need = al256(rows * HD * sizeof(uint16_t)) + al256(rows * 2 * 4);
+  return sh;
 }
 
 }  // namespace entmtp
@@ -1497,4 +1632,88 @@ extern "C" int32_t entmtp_tree_attn_batched(
   a.vt = v_tree;
   a.out = out;
   return launch_call(a, sh, workspace, static_cast<hipStream_t>(stream));
+}
+
+extern "C" size_t entmtp_tree_attn_batched_device_workspace(const entmtp_bank* bank, int32_t B,
+                                                            int32_t Hq, int32_t Hkv, int32_t d,
+                                                            int32_t cap) {
+  if (!bank || bank->desc.empty() || B < 1 || B > ENTMTP_B_MAX || Hq < 1 || Hkv < 1 ||
+      Hq % Hkv || d != HD || cap < 1)
+    return 0;
+  return batch_dev_shape(bank, B, Hq, Hkv, cap).need;
+}
+
+extern "C" int32_t entmtp_tree_attn_batched_device(
+    const entmtp_bank* bank, int32_t B, const int32_t* topo, const int32_t* prefix_len,
+    const int32_t* row_off, int32_t rows_cap, const entmtp_bf16* q, const entmtp_bf16* k_tree,
+    const entmtp_bf16* v_tree, entmtp_bf16* const* k_caches, entmtp_bf16* const* v_caches,
+    int32_t cap, int32_t Hq, int32_t Hkv, int32_t d, float scale, float rope_theta,
+    entmtp_bf16* out, void* workspace, size_t ws_bytes, void* stream) {
+  clear_error();
+  ENTMTP_CHECK_ARG(B >= 1 && B <= ENTMTP_B_MAX, ENTMTP_EINVAL, "B = %d outside [1, %d]", B,
+                   ENTMTP_B_MAX);
+  if (int32_t rc = check_device_bank(bank, 0)) return rc;
+  ENTMTP_CHECK_ARG(static_cast<int>(bank->desc.size()) <= kMaxTreesArg, ENTMTP_ERANGE,
+                   "a device-planned batch names at most %d bank trees (bank has %zu)",
+                   kMaxTreesArg, bank->desc.size());
+  ENTMTP_CHECK_ARG(topo && prefix_len && row_off, ENTMTP_EINVAL,
+                   "topo, prefix_len and row_off must be non-NULL device arrays");
+  ENTMTP_CHECK_ARG(k_caches && v_caches, ENTMTP_EINVAL,
+                   "k_caches and v_caches must be non-NULL host arrays");
+  ENTMTP_CHECK_ARG(rows_cap >= 1, ENTMTP_EINVAL, "rows_cap = %d < 1", rows_cap);
+  ENTMTP_CHECK_ARG(cap >= 1, ENTMTP_EINVAL, "cap = %d < 1", cap);
+  for (int b = 0; b < B; ++b)
+    ENTMTP_CHECK_ARG(k_caches[b] && v_caches[b] && aligned16(k_caches[b]) && aligned16(v_caches[b]),
+                     ENTMTP_EINVAL, "sequence %d: caches must be non-NULL and 16-byte aligned", b);
+  if (int32_t rc = check_common(Hq, Hkv, d, scale, rope_theta, q, k_tree, v_tree, out, workspace))
+    return rc;
+  const BatchDevShape sh = batch_dev_shape(bank, B, Hq, Hkv, cap);
+  ENTMTP_CHECK_ARG(ws_bytes >= sh.need, ENTMTP_ENOSPC, "workspace has %zu bytes, needs %zu",
+                   ws_bytes, sh.need);
+  BatchArgs a{};
+  a.topo_dev = topo;
+  a.len_dev = prefix_len;
+  a.row_off_dev = row_off;
+  a.rows_cap = rows_cap;
+  a.n_trees = static_cast<int>(bank->desc.size());
+  for (int k = 0; k < a.n_trees; ++k) {
+    const TopoDesc& td = bank->desc[k];
+    ENTMTP_CHECK_ARG(td.off_mask <= INT32_MAX && td.off_depth <= INT32_MAX, ENTMTP_ERANGE,
+                     "bank arena offsets past 2 GiB");
+    a.trees[k] = TreeHdr{td.T, td.D, static_cast<int>(td.off_mask), static_cast<int>(td.off_depth)};
+  }
+  a.arena = bank->arena;
+  a.cus = device_cus();
+  a.B = B;
+  a.G = Hq / Hkv;
+  a.Hq = Hq;
+  a.Hkv = Hkv;
+  a.cap = cap;
+  a.scale_log2 = scale * 1.4426950408889634f;
+  set_rope(a, rope_theta);
+  a.q = q;
+  a.kt = k_tree;
+  a.vt = v_tree;
+  a.out = out;
+  const size_t rows = static_cast<size_t>(B) * sh.part_rows;
+  uint8_t* ws = static_cast<uint8_t*>(workspace);
+  a.part_o = reinterpret_cast<uint16_t*>(ws);
+  a.part_ml = reinterpret_cast<float*>(ws + al256(rows * HD * sizeof(uint16_t)));
+  for (int b = 0; b < B; ++b) {
+    a.s[b].kc = k_caches[b];
+    a.s[b].vc = v_caches[b];
+    a.s[b].merge0 = b * sh.merge_blocks;
+    a.s[b].part_off = b * sh.part_rows;
+  }
+  const hipStream_t s = static_cast<hipStream_t>(stream);
+  // one instance per tile count; a batch's workgroups in the other leave at once
+  for (int nt = 1; nt <= 4; nt *= 4) {
+    if (sh.items[nt] == 0) continue;
+    a.nt = nt;
+    for (int b = 0; b < B; ++b) a.s[b].item0 = b * sh.items[nt];
+    launch_attend<true>(a, B * sh.items[nt], rope_lds_bytes(sh.D_max, a.theta), s);
+    if (int32_t rc = launch_status("tree_attn (device-planned batch) launch")) return rc;
+  }
+  hipLaunchKernelGGL(attn_merge_kernel<true>, dim3(B * sh.merge_blocks), dim3(kMergeThreads), 0, s, a);
+  return launch_status("tree_attn (device-planned batch) merge launch");
 }

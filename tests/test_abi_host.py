@@ -79,6 +79,50 @@ def test_bank_limits_accepted():
     api.Bank([[-1] + [0] * 255, [-1] + list(range(31))], device=None)
 
 
+def test_device_array_batched_calls_reject_bad_arguments_without_launching():
+    """The batched calls that read their per-sequence choices from device
+    memory check everything the host can see before any launch."""
+    lib = api.lib
+    host_bank = api.Bank([[-1, 0], [-1, 0, 0, 1]], device=None)
+    p = ctypes.c_void_p(16)                      # never dereferenced: validation fails first
+    ptrs = (ctypes.c_void_p * 2)(16, 16)
+    nulls = (ctypes.c_void_p * 2)(16, None)
+    for B in (0, api.B_MAX + 1):
+        assert lib.entmtp_tree_attn_batched_device(host_bank.handle, B, p, p, p, 8, p, p, p, ptrs, ptrs,
+                                                   100, 32, 8, 128, 0.1, 0.0, p, p, 1 << 20,
+                                                   None) == api.EINVAL
+        assert lib.entmtp_accept_batched_device(host_bank.handle, B, p, p, 8, p, p, None, p, p, 4, p,
+                                                None, None) == api.EINVAL
+        assert lib.entmtp_kv_compact_batched_device(B, p, 4, p, p, ptrs, ptrs, 1, 0, 8, 100, 128,
+                                                    None) == api.EINVAL
+    rc = lib.entmtp_tree_attn_batched_device(host_bank.handle, 2, p, p, p, 8, p, p, p, ptrs, ptrs, 100,
+                                             32, 8, 128, 0.1, 0.0, p, p, 1 << 20, None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
+    rc = lib.entmtp_accept_batched_device(host_bank.handle, 2, p, p, 8, p, p, None, p, p, 4, p, None,
+                                          None)
+    assert rc == api.EINVAL and "arena" in api.last_error()
+    # compaction needs no bank: its device arrays and host cache lists
+    assert lib.entmtp_kv_compact_batched_device(2, p, 4, p, None, ptrs, ptrs, 1, 0, 8, 100, 128,
+                                                None) == api.EINVAL
+    assert lib.entmtp_kv_compact_batched_device(2, p, 4, p, p, ptrs, nulls, 1, 0, 8, 100, 128,
+                                                None) == api.EINVAL
+    assert lib.entmtp_kv_compact_batched_device(2, p, 4, p, p, ptrs, ptrs, 1, 0, 8, 100, 12,
+                                                None) == api.EINVAL
+    assert lib.entmtp_kv_compact_batched_device(2, p, 0, p, p, ptrs, ptrs, 1, 0, 8, 100, 128,
+                                                None) == api.EINVAL
+    # the workspace bound: zero for invalid arguments, per sequence for a batch
+    ws = api.tree_attn_batched_device_workspace
+    assert ws(host_bank, 0, 32, 8, 128, 4096) == 0
+    assert ws(host_bank, api.B_MAX + 1, 32, 8, 128, 4096) == 0
+    assert ws(host_bank, 2, 30, 8, 128, 4096) == 0
+    assert ws(host_bank, 2, 32, 8, 64, 4096) == 0
+    assert ws(host_bank, 2, 32, 8, 128, 0) == 0
+    one = ws(host_bank, 1, 32, 8, 128, 4096)
+    assert one > 0
+    assert one * 4 - 2 * 256 <= ws(host_bank, 4, 32, 8, 128, 4096) <= 4 * one
+    assert ws(host_bank, 1, 32, 8, 128, 8192) >= one
+
+
 def test_kernel_calls_reject_bad_arguments_without_launching():
     lib = api.lib
     host_bank = api.Bank([[-1, 0]], device=None)
