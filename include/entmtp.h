@@ -470,7 +470,7 @@ int32_t entmtp_kv_compact_batched(int32_t B, const int32_t* path, int32_t path_c
  * Batched form with the prefix lengths in DEVICE memory: prefix_len[B] is a
  * device int32 array (k_caches / v_caches stay HOST arrays of device
  * pointers); otherwise as entmtp_kv_compact_batched.  A sequence whose
- * prefix_len[b] is negative is left unchanged.
+ * prefix_len[b] lies outside [0, cap) is left unchanged.
  * Errors (host-checked): EINVAL, EHIP.
  */
 int32_t entmtp_kv_compact_batched_device(int32_t B, const int32_t* path, int32_t path_capacity,

@@ -116,7 +116,8 @@ __global__ __launch_bounds__(kAcceptThreads) void accept_batched_device_kernel(A
   const int tr = p.topo[b], r0 = p.row_off[b], r1 = p.row_off[b + 1];
   const bool named = tr >= 0 && tr < p.n_trees;
   const int T = p.trees[named ? tr : 0].T;
-  const bool ok = named && r0 >= 0 && r0 + T <= r1 && r0 + T <= p.rows_cap &&
+  const long long end = static_cast<long long>(r0) + T;   // (64-bit: the entries are unchecked)
+  const bool ok = named && r0 >= 0 && end <= r1 && end <= p.rows_cap &&
                   p.trees[named ? tr : 0].D + 1 <= p.path_cap;
   int* path = p.path + static_cast<size_t>(b) * p.path_cap;
   if (!ok) {

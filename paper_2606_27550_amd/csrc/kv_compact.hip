@@ -39,7 +39,9 @@ __global__ __launch_bounds__(kCompactThreads) void kv_compact_kernel(CompactArgs
   const int b = blockIdx.x / per_seq, rest = blockIdx.x % per_seq;
   const int layer = rest / p.Hkv, g = rest % p.Hkv;
   const int d = p.d, cap = p.cap, L = p.dev ? p.dev->L : (p.L_dev ? p.L_dev[b] : p.L[b]);
-  if (L < 0) return;   // (a device-held prefix length the host could not check)
+  // a device-held prefix length the host could not check: outside [0, cap)
+  // no row can move (and L + j stays far from overflow below cap)
+  if (L < 0 || L >= cap) return;
   const int* path = p.path + static_cast<size_t>(b) * p.path_cap;
   const size_t base = static_cast<size_t>(layer) * p.layer_stride + static_cast<size_t>(g) * cap * d;
   int a = p.by_value ? p.a_v : p.accept_len[b];

@@ -230,8 +230,9 @@ __device__ __forceinline__ SeqPlan resolve_batch(const BatchArgs& p, int b) {
   const bool named = lane < p.B && tr >= 0 && tr < p.n_trees;
   int T = 0;
   if (named) T = p.trees[tr].T;   // only lanes holding a bank index read the table
+  const long long end = static_cast<long long>(r0) + T;   // (64-bit: the entries are unchecked)
   const bool ok = named && L >= 0 && static_cast<long long>(L) + T <= p.cap && r0 >= 0 &&
-                  r0 + T <= r1 && r0 + T <= p.rows_cap;
+                  end <= r1 && end <= p.rows_cap;
   if (!ok) T = 0;
   const int nblocks = T ? (L + T + KB - 1) / KB : 0;
   int nt = T ? tree_tiles(p.G, T) : 1;

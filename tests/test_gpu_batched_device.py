@@ -74,7 +74,7 @@ def device_attn(api, bank, inp, topo, lens, Hq, Hkv, cap, row_off, rows_cap, fil
     vt = np.zeros((rows_cap, Hkv, D_HEAD), np.uint16)
     for b in range(B):
         T = inp[b].q.shape[0]
-        r0 = row_off[b]
+        r0 = int(row_off[b])
         if 0 <= r0 and r0 + T <= rows_cap:
             q[r0:r0 + T], kt[r0:r0 + T], vt[r0:r0 + T] = inp[b].q, inp[b].k_tree, inp[b].v_tree
     kcs = [dev_bf16(x.k_cache) for x in inp]
@@ -118,20 +118,21 @@ def test_attn_device_arrays_rows_anywhere_and_invalid_entries(api, trees):
     Hq, Hkv = 8, 2
     n = len(trees)
     cap = 1024
-    topo = [2, n, 3, 1, 4]
+    topo = [2, n, 3, 1, 4, 4]
     Ts = [len(trees[t]) if t < n else 8 for t in topo]
-    lens = [300, 50, cap - Ts[2] + 1, 900, 120]          # sequence 2: one slot short
+    lens = [300, 50, cap - Ts[2] + 1, 900, 120, 10]      # sequence 2: one slot short
     bank = api.Bank(trees)
     inp = inputs(trees, [min(t, n - 1) for t in topo], [min(L, cap - 128) for L in lens], Hq, Hkv,
                  cap, 302)
-    row_off = np.zeros(6, np.int32)
+    row_off = np.zeros(7, np.int32)
     row_off[0] = 5
     row_off[1] = row_off[0] + Ts[0] + 3                  # a gap of three rows
     row_off[2] = row_off[1] + 9
     row_off[3] = 200
     row_off[4] = row_off[3] + Ts[3] - 1                  # sequence 3: one row short
-    row_off[5] = row_off[4] + Ts[4] + 2
-    rows_cap = int(row_off[5]) + 4
+    rows_cap = int(row_off[4]) + Ts[4] + 6
+    row_off[5] = 2**31 - 100                             # sequence 5: rows past 2^31
+    row_off[6] = 2**31 - 1
     assert row_off[2] + Ts[2] <= row_off[3]
     d_out, d_k, d_v = device_attn(api, bank, inp, topo, lens, Hq, Hkv, cap, row_off, rows_cap)
     fill_bits = host_bits(torch.full((1,), 7.0, dtype=torch.bfloat16, device="cuda"))[0]
@@ -147,7 +148,7 @@ def test_attn_device_arrays_rows_anywhere_and_invalid_entries(api, trees):
         np.testing.assert_array_equal(d_v[b][:, :L + T], rv[:, :L + T])
         done[r0:r0 + T] = True
     assert (d_out[~done] == fill_bits).all()
-    for b in (1, 2, 3):
+    for b in (1, 2, 3, 5):
         np.testing.assert_array_equal(d_k[b], inp[b].k_cache)
         np.testing.assert_array_equal(d_v[b], inp[b].v_cache)
 
@@ -206,9 +207,10 @@ def test_accept_device_arrays_invalid_entries(api, trees):
     does."""
     bank = api.Bank(trees)
     T0, T1 = bank.T[2], bank.T[1]
-    topo = np.array([2, len(trees), 1, 4, 0], np.int32)
+    topo = np.array([2, len(trees), 1, 4, 0, 4], np.int32)
     rows_cap = T0 + T1 + 200
-    row_off = np.array([0, T0, T0 + 1, T0 + T1, rows_cap - 4, rows_cap + 4], np.int32)
+    # sequence 5's rows start 100 below 2^31 (their end does not fit in int32)
+    row_off = np.array([0, T0, T0 + 1, T0 + T1, rows_cap - 4, 2**31 - 100, 2**31 - 1], np.int32)
     tok_v, am_v, p1_v = accept_inputs(trees, bank, [2], 31)
     tok = np.zeros(rows_cap, np.int32)
     am = np.zeros(rows_cap, np.int32)
@@ -257,14 +259,15 @@ def test_compact_device_arrays_equal_host_arrays(api, trees):
     v1 = [dev_bf16(c[1]) for c in caches]
     api.kv_compact_batched(dev_i32(paths), dev_i32(acc), lens, k1, v1)
     lens_d = list(lens)
-    lens_d[3] = -1                     # a negative prefix length: that sequence is left alone
+    lens_d[3] = -1                     # prefix lengths outside [0, cap): left alone
+    lens_d[1] = 2**31 - 2
     k2 = [dev_bf16(c[0]) for c in caches]
     v2 = [dev_bf16(c[1]) for c in caches]
     api.kv_compact_batched_device(dev_i32(paths), dev_i32(acc), dev_i32(np.asarray(lens_d, np.int32)),
                                   k2, v2)
     torch.cuda.synchronize()
     for b in range(B):
-        if b == 3:
+        if b in (1, 3):
             np.testing.assert_array_equal(host_bits(k2[b]), caches[b][0])
             np.testing.assert_array_equal(host_bits(v2[b]), caches[b][1])
         else:
