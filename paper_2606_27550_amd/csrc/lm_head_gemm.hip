@@ -209,6 +209,24 @@ __device__ __forceinline__ void gemm_tile(
                    : "v"(frag[buf][mi]), "v"(frag[buf][Sh::MI + ni])
                    : "memory");
   };
+  // An empty assembly statement that takes and returns every accumulator.
+  // mfma_drain() orders memory accesses only: without this the compiler may
+  // schedule arithmetic on the accumulators (the statistics epilogue) ahead of
+  // the drain, into the last products' latency, or sink their zeroing past it
+  // towards the first products.  Pinned right after the zeroing and right
+  // after the final drain, they cross neither (the assembly statements keep
+  // their order).
+  auto pin_acc = [&]() {
+#pragma unroll
+    for (int mi = 0; mi < Sh::MI; ++mi)
+#pragma unroll
+      for (int ni = 0; ni < Sh::NI; ++ni) {
+        if constexpr (Sh::ACC_AGPR)
+          asm volatile("" : "+a"(acc[mi][ni]));
+        else
+          asm volatile("" : "+v"(acc[mi][ni]));
+      }
+  };
   // the fragments in the order the products need them: X blocks (every
   // product of the first W block uses one), then W blocks
   auto frag_at = [&](int n) { return n < Sh::NI ? Sh::MI + n : n - Sh::NI; };
@@ -234,6 +252,7 @@ __device__ __forceinline__ void gemm_tile(
   stage_barrier();
 #pragma unroll
   for (int n = 0; n < Sh::NF; ++n) read_one(frag[0][frag_at(n)], ring, 0, frag_at(n));
+  pin_acc();
   mfma_drain();   // the accumulators' zeroing precedes their first product
 
   // Step c, K = c mod 6 (slot and load set depend on K only).  A k-step's
@@ -302,6 +321,7 @@ __device__ __forceinline__ void gemm_tile(
   if constexpr (kTail > 3) step(I3{}, 6 * kRounds + 3);
   if constexpr (kTail > 4) step(I4{}, 6 * kRounds + 4);
   mfma_drain();
+  pin_acc();
 
   const int vbase = r0 + wm * Sh::WM + 4 * lg;   // first of the lane's rows in block mi = 0
   if (logits) {
