@@ -227,9 +227,12 @@ __device__ __forceinline__ SeqPlan resolve_batch(const BatchArgs& p, int b) {
     r0 = p.row_off_dev[lane];
     r1 = p.row_off_dev[lane + 1];
   }
+  // every bank tree's size, lane k holding tree k's (requested with the
+  // entries above, so one memory round trip covers both)
+  const int tree_T = lane < p.n_trees ? p.trees[lane].T : 0;
   const bool named = lane < p.B && tr >= 0 && tr < p.n_trees;
-  int T = 0;
-  if (named) T = p.trees[tr].T;   // only lanes holding a bank index read the table
+  const int T_named = __shfl(tree_T, named ? tr : 0, 64);
+  int T = named ? T_named : 0;
   const long long end = static_cast<long long>(r0) + T;   // (64-bit: the entries are unchecked)
   const bool ok = named && L >= 0 && static_cast<long long>(L) + T <= p.cap && r0 >= 0 &&
                   end <= r1 && end <= p.rows_cap;
