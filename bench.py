@@ -444,8 +444,9 @@ def histogram(vals):
 def main():
     args = parse()
     if args.gpus != 1 or int(os.environ.get("WORLD_SIZE", "1")) != 1:
-        print("bench.py runs on one GPU only: the tree-verification path of this build is "
-              "single-GPU (see DESIGN.md for how it would shard)", file=sys.stderr)
+        print("bench.py runs on one GPU only: the tree-verification path is single-GPU "
+              "(sharding across GPUs -- KV heads and vocabulary slices -- is designed, not built)",
+              file=sys.stderr)
         sys.exit(2)
 
     import torch
