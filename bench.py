@@ -93,6 +93,13 @@ def parse():
     ap.add_argument("--gpu-scheduler", action="store_true", help="same as --scheduler gpu")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="only run plain 256 MiB device copies (reference for HBM byte counters)")
+    ap.add_argument("--lm-rows", default="",
+                    help="only time the LM head with statistics partials over this many rows "
+                         "(comma-separated counts; the batched verification pass's many-row "
+                         "case), one JSON line per count")
+    ap.add_argument("--lm-vocab", type=int, default=128256)
+    ap.add_argument("--lm-hidden", type=int, default=4096)
+    ap.add_argument("--lm-calls", type=int, default=30)
     return ap.parse_args()
 
 
@@ -147,6 +154,41 @@ class TimingEvent:
 
 def log(*a):
     print("[bench]", *a, file=sys.stderr, flush=True)
+
+
+def lm_rows(args, api, torch):
+    """The LM head with statistics partials (entmtp_verify_logits_partials,
+    no logits) over T rows, for each requested T: `--lm-calls` back-to-back
+    calls between two events after five untimed ones; seeded N(0, 1) hidden
+    rows, W ~ N(0, 0.02^2), bf16."""
+    V, hid = args.lm_vocab, args.lm_hidden
+    dev = torch.device("cuda:0")
+    g = torch.Generator(device=dev).manual_seed(11)
+    W = (torch.randn((V, hid), generator=g, device=dev) * 0.02).to(torch.bfloat16)
+    for T in (int(x) for x in args.lm_rows.split(",") if x):
+        X = torch.randn((T, hid), generator=g, device=dev).to(torch.bfloat16)
+        ws = torch.empty(api.stats_partials_bytes(T, hid, V), dtype=torch.uint8, device=dev)
+        for _ in range(5):
+            api.verify_logits_partials(X, W, None, 1.0, ws)
+        torch.cuda.synchronize()
+        e0, e1 = TimingEvent(), TimingEvent()
+        hip = TimingEvent._hip
+        stream = ctypes.c_void_p(torch.cuda.current_stream().cuda_stream)
+        hip.hipEventRecord.argtypes = [ctypes.c_void_p, ctypes.c_void_p]
+        hip.hipEventRecord(e0.ptr, stream)
+        for _ in range(args.lm_calls):
+            api.verify_logits_partials(X, W, None, 1.0, ws)
+        hip.hipEventRecord(e1.ptr, stream)
+        torch.cuda.synchronize()
+        us = e0.elapsed_time(e1) * 1e3 / args.lm_calls
+        flops = 2.0 * T * V * hid
+        print(json.dumps({"lm_head_rows": T, "vocab": V, "hidden": hid, "calls": args.lm_calls,
+                          "us_per_call": round(us, 2),
+                          "TFLOPs": round(flops / us / 1e6, 1),
+                          "mfma_frac_bf16": round(flops / us / 1e6 / MFMA_PEAK_BF16_TFLOPS, 4),
+                          "W_GBps": round(V * hid * 2 / us / 1e3, 1),
+                          "timing": "HIP events around back-to-back calls on one stream"}),
+              flush=True)
 
 
 class SingleSeq:
@@ -456,6 +498,9 @@ def main():
         sys.exit("bench.py needs a GPU")
     if args.calibrate_copy:
         calibrate_copy()
+        return
+    if args.lm_rows:
+        lm_rows(args, api, torch)
         return
     torch.cuda.set_device(torch.device("cuda:0"))
     lib = api.lib
