@@ -57,6 +57,10 @@ constexpr float kLazyLog2 = 8.f;     // the running max is raised only past this
 constexpr int VT_LD = 36;            // bf16 per V^T row in LDS (32 keys + pad)
 constexpr int kMaxSplits = 32;
 constexpr int kMinBlocksPerSplit = 4;   // one block per wave at least
+// A batch's blocks-per-split target: its key-block streams (one per KV head,
+// query group and 32-key block: what a workgroup reads) over this many
+// workgroups per CU.
+constexpr int kBatchWgPerCu = 3;
 constexpr int kMaxSeqs = ENTMTP_B_MAX;
 
 __host__ __device__ inline int rows_padded(int G, int T) {
@@ -239,12 +243,13 @@ __device__ __forceinline__ SeqPlan resolve_batch(const BatchArgs& p, int b) {
   if (!ok) T = 0;
   const int nblocks = T ? (L + T + KB - 1) / KB : 0;
   int nt = T ? tree_tiles(p.G, T) : 1;
-  long long work = T ? static_cast<long long>(p.Hkv) * (rows_padded(p.G, T) / kQTile) * nblocks : 0;
 #pragma unroll
-  for (int off = 32; off >= 1; off >>= 1) {
-    nt = max(nt, __shfl_xor(nt, off, 64));
-    work += __shfl_xor(work, off, 64);
-  }
+  for (int off = 32; off >= 1; off >>= 1) nt = max(nt, __shfl_xor(nt, off, 64));
+  long long work =
+      T ? static_cast<long long>(p.Hkv) * query_groups(rows_padded(p.G, T) / kQTile, nt) * nblocks
+        : 0;
+#pragma unroll
+  for (int off = 32; off >= 1; off >>= 1) work += __shfl_xor(work, off, 64);
   const int Tb = __shfl(T, b, 64);
   if (Tb == 0) {
     q.T = 0;
@@ -272,8 +277,7 @@ __device__ __forceinline__ SeqPlan resolve_batch(const BatchArgs& p, int b) {
   if (p.B == 1) {
     ns = split_single(nb, p.Hkv * q.nqg, p.cus * wg_per_cu(nt));
   } else {
-    work = (work + nt - 1) / nt;
-    const long long per_wg = (work + 4LL * p.cus - 1) / (4LL * p.cus);
+    const long long per_wg = (work + kBatchWgPerCu * p.cus - 1) / (kBatchWgPerCu * p.cus);
     const int target_bps = static_cast<int>(per_wg > kMinBlocksPerSplit ? per_wg : kMinBlocksPerSplit);
     ns = (nb + target_bps - 1) / target_bps;
     const int bound = split_bound(nb);
@@ -1246,7 +1250,7 @@ struct CallShape {
 
 // Plans the sequences of one call: per-sequence split counts (a lone
 // sequence fills the CUs by itself; a batch shares one blocks-per-split
-// target sized to about four workgroups per CU), grid ranges and the packed
+// target sized to about kBatchWgPerCu workgroups per CU), grid ranges and the packed
 // workspace layout (output partials, then (max, sum) partials).
 CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const int32_t* L,
                     entmtp_bf16* const* kc, entmtp_bf16* const* vc, int cap, int Hq, int Hkv,
@@ -1265,16 +1269,17 @@ CallShape plan_call(const entmtp_bank* bank, int B, const int32_t* topo, const i
   const int cus = device_cus();
   a.cus = cus;
   a.nt = 1;   // the largest tile count any sequence needs
-  long long work = 0;
+  for (int b = 0; b < B; ++b) {
+    const int nt = tree_tiles(a.G, bank->desc[topo[b]].T);
+    a.nt = nt > a.nt ? nt : a.nt;
+  }
+  long long work = 0;   // key-block streams
   for (int b = 0; b < B; ++b) {
     const int T = bank->desc[topo[b]].T;
-    const int nqt = rows_padded(a.G, T) / kQTile;
-    const int nt = tree_tiles(a.G, T);
-    a.nt = nt > a.nt ? nt : a.nt;
-    work += static_cast<long long>(Hkv) * nqt * ((L[b] + T + KB - 1) / KB);
+    const int nqg = query_groups(rows_padded(a.G, T) / kQTile, a.nt);
+    work += static_cast<long long>(Hkv) * nqg * ((L[b] + T + KB - 1) / KB);
   }
-  work = (work + a.nt - 1) / a.nt;
-  const long long per_wg = (work + 4LL * cus - 1) / (4LL * cus);
+  const long long per_wg = (work + kBatchWgPerCu * cus - 1) / (kBatchWgPerCu * cus);
   const int target_bps = static_cast<int>(per_wg > kMinBlocksPerSplit ? per_wg : kMinBlocksPerSplit);
 
   CallShape sh;
