@@ -490,6 +490,15 @@ int32_t entmtp_kv_compact_batched_device(int32_t B, const int32_t* path, int32_t
 int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, float tau_on,
                            float tau_off);
 
+/* The same ladder for a batch of sequences, each with its own rung (§4
+ * "Policy", applied per sequence): rung[B] (host, in/out) moves one step on
+ * s[B] (host), the per-sequence top-1 probability the acceptance reports.
+ * Every rung is checked before any is changed; on an error rung[] is left as
+ * it was.  Errors: EINVAL (B < 0, null array, n_rungs < 1, tau_off > tau_on,
+ * a rung outside [0, n_rungs)). */
+int32_t entmtp_ladder_next_batched(int32_t B, int32_t* rung, const float* s, int32_t n_rungs,
+                                   float tau_on, float tau_off);
+
 /*
  * Speculative-sampling verification (§2.1: keep a draft token t with
  * probability min(1, p(t) / p_hat(t)), else draw a replacement from

@@ -89,6 +89,7 @@ _SIGNATURES = {
     "entmtp_kv_compact": (_c_i32, [_c_p, _c_i32, _c_p, _c_i32, _c_p, _c_p, _c_i32, _c_i64, _c_i32,
                                    _c_i32, _c_i32, _c_p]),
     "entmtp_ladder_next": (_c_i32, [_c_i32, _c_i32, _c_f32, _c_f32, _c_f32]),
+    "entmtp_ladder_next_batched": (_c_i32, [_c_i32, _c_p, _c_p, _c_i32, _c_f32, _c_f32]),
     "entmtp_step_workspace": (_c_sz, [_c_p, ctypes.POINTER(StepConfig)]),
     "entmtp_step_create": (_c_i32, [_c_p, ctypes.POINTER(StepConfig), ctypes.POINTER(_c_p)]),
     "entmtp_step_destroy": (None, [_c_p]),
@@ -722,6 +723,17 @@ def kv_compact(path, accept_len, prefix_len: int, k_cache, v_cache, stream=None)
 
 def ladder_next(rung: int, n_rungs: int, s: float, tau_on: float, tau_off: float) -> int:
     return _check(lib.entmtp_ladder_next(rung, n_rungs, s, tau_on, tau_off))
+
+
+def ladder_next_batched(rung: np.ndarray, s: np.ndarray, n_rungs: int, tau_on: float,
+                        tau_off: float) -> None:
+    """rung: int32 host array [B], moved in place on float32 s [B]."""
+    _need(isinstance(rung, np.ndarray) and rung.dtype == np.int32 and rung.flags.c_contiguous,
+          "rung must be a contiguous int32 numpy array")
+    _need(isinstance(s, np.ndarray) and s.dtype == np.float32 and s.flags.c_contiguous
+          and s.shape == rung.shape, "s must be a contiguous float32 numpy array shaped like rung")
+    _check(lib.entmtp_ladder_next_batched(rung.size, _np_p(rung), _np_p(s), n_rungs, tau_on,
+                                          tau_off))
 
 
 def version() -> str:

@@ -222,6 +222,21 @@ extern "C" int32_t entmtp_ladder_next(int32_t rung, int32_t n_rungs, float s, fl
   return ladder_step(rung, n_rungs, s, tau_on, tau_off);
 }
 
+extern "C" int32_t entmtp_ladder_next_batched(int32_t B, int32_t* rung, const float* s,
+                                              int32_t n_rungs, float tau_on, float tau_off) {
+  clear_error();
+  ENTMTP_CHECK_ARG(B >= 0, ENTMTP_EINVAL, "B = %d < 0", B);
+  ENTMTP_CHECK_ARG(B == 0 || (rung && s), ENTMTP_EINVAL, "null rung or s array");
+  ENTMTP_CHECK_ARG(n_rungs >= 1, ENTMTP_EINVAL, "n_rungs = %d < 1", n_rungs);
+  ENTMTP_CHECK_ARG(tau_off <= tau_on, ENTMTP_EINVAL, "tau_off %g > tau_on %g",
+                   static_cast<double>(tau_off), static_cast<double>(tau_on));
+  for (int32_t b = 0; b < B; ++b)
+    ENTMTP_CHECK_ARG(rung[b] >= 0 && rung[b] < n_rungs, ENTMTP_EINVAL,
+                     "rung[%d] = %d outside [0, %d)", b, rung[b], n_rungs);
+  for (int32_t b = 0; b < B; ++b) rung[b] = ladder_step(rung[b], n_rungs, s[b], tau_on, tau_off);
+  return ENTMTP_OK;
+}
+
 // NextChildren(T, D) of Algorithm 1 and the joint tree T u F built from it:
 // a node's next-ranked child hangs under it, so each node of depth below D
 // contributes exactly one candidate, appended in node order.

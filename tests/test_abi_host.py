@@ -256,6 +256,39 @@ def test_ladder_matches_oracle():
         api.ladder_next(0, 5, 0.5, 0.6, 0.8)
 
 
+def test_ladder_batched_matches_oracle():
+    """One ladder per sequence, moved by one call: the hand-traced fixture in
+    every lane, then 16 independent sequences over 2000 steps against the
+    oracle, with s drawn on and next to both thresholds."""
+    g = golden("ladder_trace.json")
+    rung = np.zeros(4, np.int32)
+    for s, want in zip(g["s"], g["rungs"]):
+        api.ladder_next_batched(rung, np.full(4, s, np.float32), g["n_rungs"], g["tau_on"],
+                                g["tau_off"])
+        assert rung.tolist() == [want] * 4
+    rng = np.random.default_rng(3)
+    on, off = float(np.float32(0.8)), float(np.float32(0.6))
+    edges = np.array([0.8, 0.6, np.nextafter(np.float32(0.8), np.float32(1)),
+                      np.nextafter(np.float32(0.6), np.float32(0))], np.float32)
+    rung = rng.integers(0, 5, 16).astype(np.int32)
+    want = [int(r) for r in rung]
+    for _ in range(2000):
+        s = rng.random(16).astype(np.float32)
+        pick = rng.random(16) < 0.2
+        s[pick] = edges[rng.integers(0, 4, int(pick.sum()))]
+        api.ladder_next_batched(rung, s, 5, 0.8, 0.6)
+        want = [orc.ladder_next(w, 5, float(x), on, off) for w, x in zip(want, s)]
+        assert rung.tolist() == want
+    # an invalid rung anywhere leaves every rung unchanged
+    bad = np.array([1, 2, 5, 0], np.int32)
+    with pytest.raises(api.EntmtpError):
+        api.ladder_next_batched(bad, np.ones(4, np.float32), 5, 0.8, 0.6)
+    assert bad.tolist() == [1, 2, 5, 0]
+    with pytest.raises(api.EntmtpError):
+        api.ladder_next_batched(np.zeros(2, np.int32), np.ones(2, np.float32), 5, 0.6, 0.8)
+    api.ladder_next_batched(np.zeros(0, np.int32), np.zeros(0, np.float32), 5, 0.8, 0.6)
+
+
 def test_frontier_tree_matches_oracle():
     """entmtp_frontier_tree (the joint tree T u F, through the C ABI) against
     the oracle's NextChildren."""
