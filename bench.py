@@ -703,8 +703,8 @@ def run_batched(args, api, synth, torch, lib):
     32:8, vocabulary 128256.  A step, in dependency order on one stream:
     batched tree attention, the LM head with statistics over the
     concatenated rows, batched greedy acceptance and compaction; then the
-    host reads every sequence's (accept length, s) and moves each sequence's
-    ladder.  The hidden rows of a step are gathered from a staged pool per
+    host reads every sequence's (accept length, s) in one copy and moves
+    every sequence's ladder in one call.  The hidden rows of a step are gathered from a staged pool per
     sequence (the model would hand them over contiguous); the draft tokens
     of every (step, sequence, tree) are drawn before the timed region and a
     step's are written from pinned memory; the attention is issued first, as
